@@ -1,0 +1,492 @@
+"""Pins for the CPU oracle: checks against what the paper and mathematics fix.
+
+Every test here runs on the CPU.  None of them re-types the oracle's own loop:
+each compares it with a different formulation (the square display, a masked
+dense product through numpy's BLAS, a brute-force enumeration of the basis
+products, the semidirect formula, closed-form counts, invariants such as
+associativity and the adjoint identity, finite differences, libm's erf,
+torch's bfloat16 cast) or with hand-evaluated golden values.
+"""
+
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import Alg
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _read_golden(name):
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, *vals = line.split()
+            out[key] = np.array([float(v) for v in vals])
+    return out
+
+
+def rng(*seed):
+    return np.random.default_rng(list(seed))
+
+
+def square_typed(q, bs, A, B, law="star"):
+    """A *_q B through the typed projection: row block i of A has type i."""
+    alg = Alg.equal(q, q * bs, q * bs, law)
+    t = np.repeat(np.arange(q), bs).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, A, B)
+    return Y
+
+
+def masked_dense_fwd(alg, t, X, W):
+    """Independent formulation: Y[I_i] = X[I_i] (W . Mask_i),
+    Mask_i[kk, n] = [group(kk) in {i, group(n)}] (Sec. 4, eqs. typed-diag/-off)."""
+    gk = np.repeat(np.arange(alg.q), alg.s)
+    gn = np.repeat(np.arange(alg.q), alg.r)
+    Y = np.zeros((X.shape[0], alg.N))
+    for i in range(alg.q):
+        rows = np.nonzero(t == i)[0]
+        if alg.law == "dense":
+            mask = np.ones((alg.K, alg.N))
+        else:
+            mask = ((gk[:, None] == i) | (gk[:, None] == gn[None, :])).astype(float)
+        Y[rows] = X[rows] @ (W * mask)
+    return Y
+
+
+# ---- P1: the q = 2 display ---------------------------------------------------
+
+def test_q2_display_golden_scalars():
+    g = _read_golden("q2_display_scalar.txt")
+    X = g["X"].reshape(2, 2)
+    W = g["W"].reshape(2, 2)
+    t = np.array([0, 1], dtype=np.int32)
+    Y, _, _, _ = oracle.proj_fwd(Alg(2, (1, 1), (1, 1), "star"), t, X, W)
+    np.testing.assert_array_equal(Y.ravel(), g["STAR"])
+    Yd, _, _, _ = oracle.proj_fwd(Alg(2, (1, 1), (1, 1), "dense"), t, X, W)
+    np.testing.assert_array_equal(Yd.ravel(), g["DENSE"])
+
+
+@pytest.mark.parametrize("bs", [1, 3, 8])
+def test_q2_display_blocks(bs):
+    """Sec. 1 eq. six-product with matrix blocks: type-1 rows give
+    [A Wa, A Wu + U Wd], type-2 rows give [V Wa + D Wv, D Wd]."""
+    g = rng(1, bs)
+    A, U, V, D = (g.standard_normal((bs, bs)) for _ in range(4))
+    Wa, Wu, Wv, Wd = (g.standard_normal((bs, bs)) for _ in range(4))
+    X = np.block([[A, U], [V, D]])
+    W = np.block([[Wa, Wu], [Wv, Wd]])
+    expect = np.block([[A @ Wa, A @ Wu + U @ Wd], [V @ Wa + D @ Wv, D @ Wd]])
+    got = square_typed(2, bs, X, W)
+    np.testing.assert_allclose(got, expect, rtol=0, atol=1e-12)
+    # the two removed products really are absent: perturbing U.Wv's factor
+    # pair only through that product changes nothing
+    W2 = np.block([[Wa, Wu], [Wv + 1.0, Wd]])
+    got2 = square_typed(2, bs, X, W2)
+    np.testing.assert_allclose(got2[:bs], got[:bs], rtol=0, atol=0)
+
+
+def test_q2_interleaved_rows():
+    """Rows of the two types interleaved (t = b mod 2) as in a sequence."""
+    g = rng(2)
+    M, s = 10, (3, 5)
+    alg = Alg(2, s, (4, 2))
+    X = g.standard_normal((M, alg.K))
+    W = g.standard_normal((alg.K, alg.N))
+    t = (np.arange(M) % 2).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, W)
+    x1, x2 = X[:, :3], X[:, 3:]
+    Wa, Wu, Wv, Wd = W[:3, :4], W[:3, 4:], W[3:, :4], W[3:, 4:]
+    for b in range(M):
+        if t[b] == 0:
+            exp = np.concatenate([x1[b] @ Wa, x1[b] @ Wu + x2[b] @ Wd])
+        else:
+            exp = np.concatenate([x1[b] @ Wa + x2[b] @ Wv, x2[b] @ Wd])
+        np.testing.assert_allclose(Y[b], exp, atol=1e-12)
+
+
+# ---- P2, P3: reductions to ordinary products --------------------------------
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+def test_q1_is_gemm(law):
+    g = rng(3)
+    X, W = g.standard_normal((7, 6)), g.standard_normal((6, 5))
+    Y, _, _, _ = oracle.proj_fwd(Alg(1, (6,), (5,), law), np.zeros(7, np.int32), X, W)
+    np.testing.assert_allclose(Y, X @ W, atol=1e-12)
+
+
+@pytest.mark.parametrize("q,s,r", [(2, (4, 4), (3, 3)), (3, (2, 5, 1), (4, 1, 3)), (4, (2,) * 4, (3,) * 4)])
+def test_dense_law_is_gemm(q, s, r):
+    g = rng(4, q)
+    alg = Alg(q, s, r, "dense")
+    X, W = g.standard_normal((9, alg.K)), g.standard_normal((alg.K, alg.N))
+    t = g.integers(0, q, 9).astype(np.int32)
+    Y, _, _, ppt = oracle.proj_fwd(alg, t, X, W)
+    np.testing.assert_allclose(Y, X @ W, atol=1e-12)
+    assert list(ppt) == [q * q] * q
+
+
+# ---- P4: masked dense --------------------------------------------------------
+
+@pytest.mark.parametrize("q,s,r", [(2, (3, 5), (4, 2)), (3, (2, 5, 1), (4, 1, 3)),
+                                   (5, (1, 2, 3, 2, 1), (2, 2, 1, 3, 4)), (4, (4,) * 4, (4,) * 4)])
+def test_masked_dense_forward(q, s, r):
+    g = rng(5, q)
+    alg = Alg(q, s, r)
+    M = 23
+    X, W = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, W)
+    np.testing.assert_allclose(Y, masked_dense_fwd(alg, t, X, W), atol=1e-12)
+
+
+def test_masked_dense_backward():
+    """dX[I_i] = dY[I_i] (W . Mask_i)^T ; dW = sum_i (X[I_i]^T dY[I_i]) . Mask_i."""
+    q, s, r = 3, (2, 4, 3), (3, 2, 5)
+    alg = Alg(q, s, r)
+    g = rng(6)
+    M = 17
+    X, W, dY = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N)), g.standard_normal((M, alg.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    gk = np.repeat(np.arange(q), s)
+    gn = np.repeat(np.arange(q), r)
+    dX_exp = np.zeros((M, alg.K))
+    dW_exp = np.zeros((alg.K, alg.N))
+    for i in range(q):
+        rows = np.nonzero(t == i)[0]
+        mask = ((gk[:, None] == i) | (gk[:, None] == gn[None, :])).astype(float)
+        dX_exp[rows] = dY[rows] @ (W * mask).T
+        dW_exp += (X[rows].T @ dY[rows]) * mask
+    np.testing.assert_allclose(oracle.proj_bwd_data(alg, t, dY, W), dX_exp, atol=1e-12)
+    dW, db = oracle.proj_bwd_weight(alg, t, X, dY)
+    np.testing.assert_allclose(dW, dW_exp, atol=1e-12)
+    np.testing.assert_allclose(db, dY.sum(0), atol=1e-12)
+
+
+# ---- P5: brute-force structure constants of Q_q (x) M_b ----------------------
+
+def _basis_product_table(q):
+    """Nonzero basis products of Q_q (eq. graph-basis-products):
+    e_i e_i = e_i, e_i a_ij = a_ij, a_ij e_j = a_ij.  Slots are (row, col)
+    pairs: (i,i) is the vertex e_i, (i,j) the edge a_ij.  Returns a dict
+    (slot_x, slot_w) -> slot of the product."""
+    table = {}
+    for i in range(q):
+        table[((i, i), (i, i))] = (i, i)
+        for j in range(q):
+            if j != i:
+                table[((i, i), (i, j))] = (i, j)
+                table[((i, j), (j, j))] = (i, j)
+    return table
+
+
+@pytest.mark.parametrize("q,bs", [(1, 2), (2, 1), (2, 2), (3, 2), (4, 1), (4, 3)])
+def test_bruteforce_structure_constants(q, bs):
+    """Expand A and B over the basis slot (x) E_uv of Q_q (x) M_b and sum every
+    nonzero basis product, then compare with the oracle's typed projection and
+    its square-rule routine."""
+    table = _basis_product_table(q)
+    assert len(table) == 2 * q * q - q  # eq. q-rank
+    g = rng(7, q, bs)
+    n = q * bs
+    A, B = g.standard_normal((n, n)), g.standard_normal((n, n))
+    C = np.zeros((n, n))
+    for (sx, sw), sc in table.items():
+        for u in range(bs):
+            for v in range(bs):
+                a = A[sx[0] * bs + u, sx[1] * bs + v]
+                for z in range(bs):  # E_uv E_vz = E_uz
+                    C[sc[0] * bs + u, sc[1] * bs + z] += a * B[sw[0] * bs + v, sw[1] * bs + z]
+    np.testing.assert_allclose(square_typed(q, bs, A, B), C, atol=1e-12)
+    np.testing.assert_allclose(oracle.square_star(q, bs, A, B), C, atol=1e-12)
+    assert sum(oracle.products_per_type("star", q, i) for i in range(q)) == len(table)
+
+
+# ---- golden: the Q_3 square rule ------------------------------------------------
+
+def test_q3_square_rule_golden():
+    g = _read_golden("q3_square_rule.txt")
+    A, B = g["A"].reshape(3, 3), g["B"].reshape(3, 3)
+    np.testing.assert_array_equal(square_typed(3, 1, A, B).ravel(), g["STAR"])
+    np.testing.assert_array_equal(oracle.square_star(3, 1, A, B).ravel(), g["STAR"])
+
+
+# ---- P6, P8: associativity, unit, semidirect form ----------------------------
+
+@pytest.mark.parametrize("q", [2, 3, 4, 5])
+def test_associativity_and_unit(q):
+    bs = 3
+    g = rng(8, q)
+    n = q * bs
+    A, B, C = (g.standard_normal((n, n)) for _ in range(3))
+    lhs = square_typed(q, bs, square_typed(q, bs, A, B), C)
+    rhs = square_typed(q, bs, A, square_typed(q, bs, B, C))
+    np.testing.assert_allclose(lhs, rhs, atol=1e-11)
+    E = np.eye(n)
+    np.testing.assert_allclose(square_typed(q, bs, E, B), B, atol=0)
+    np.testing.assert_allclose(square_typed(q, bs, A, E), A, atol=0)
+    # the ordinary product is associative too, but the two laws differ
+    assert not np.allclose(square_typed(q, bs, A, B), A @ B)
+
+
+def _semidirect(q, bs, A, B):
+    """App. "Direct Associativity Check": (d,n)*(d',n') = (dd', dn' + nd')
+    with (dn')_ij = d_i n'_ij and (nd')_ij = n_ij d'_j, over matrix blocks."""
+    blk = lambda P, i, j: P[i * bs:(i + 1) * bs, j * bs:(j + 1) * bs]
+    out = np.zeros_like(A)
+    for i in range(q):
+        blk(out, i, i)[:] = blk(A, i, i) @ blk(B, i, i)
+    for i in range(q):
+        for j in range(q):
+            if i != j:
+                blk(out, i, j)[:] = blk(A, i, i) @ blk(B, i, j) + blk(A, i, j) @ blk(B, j, j)
+    return out
+
+
+@pytest.mark.parametrize("q", [2, 3, 5])
+def test_semidirect_form(q):
+    bs = 2
+    g = rng(9, q)
+    A, B = g.standard_normal((q * bs, q * bs)), g.standard_normal((q * bs, q * bs))
+    np.testing.assert_allclose(square_typed(q, bs, A, B), _semidirect(q, bs, A, B), atol=1e-12)
+
+
+# ---- P7: composition of typed projections ------------------------------------
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+def test_composition(q):
+    """eq. association-intro / general-associativity, rectangular groups:
+    Phi_{W2}(Phi_{W1}(X)) = Phi_{W1 * W2}(X), where W1 * W2 is the algebra
+    product of the two banks (row group i of W1 is a type-i row)."""
+    g = rng(10, q)
+    s = tuple(int(v) for v in g.integers(1, 4, q))
+    r1 = tuple(int(v) for v in g.integers(1, 4, q))
+    r2 = tuple(int(v) for v in g.integers(1, 4, q))
+    a1, a2, a12 = Alg(q, s, r1), Alg(q, r1, r2), Alg(q, s, r2)
+    M = 13
+    X = g.standard_normal((M, a1.K))
+    W1, W2 = g.standard_normal((a1.K, a1.N)), g.standard_normal((a2.K, a2.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    t_w1 = np.repeat(np.arange(q), s).astype(np.int32)
+    W12, _, _, _ = oracle.proj_fwd(a2, t_w1, W1, W2)  # rows of W1 in group i have type i
+    Y1, _, _, _ = oracle.proj_fwd(a1, t, X, W1)
+    lhs, _, _, _ = oracle.proj_fwd(a2, t, Y1, W2)
+    rhs, _, _, _ = oracle.proj_fwd(a12, t, X, W12)
+    np.testing.assert_allclose(lhs, rhs, atol=1e-11)
+
+
+# ---- P9, P10: identity bank, row locality ------------------------------------
+
+@pytest.mark.parametrize("q", [1, 2, 3, 4])
+def test_identity_bank(q):
+    g = rng(11, q)
+    s = tuple(int(v) for v in g.integers(1, 5, q))
+    alg = Alg(q, s, s)
+    X = g.standard_normal((11, alg.K))
+    t = g.integers(0, q, 11).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, np.eye(alg.K))
+    np.testing.assert_array_equal(Y, X)
+
+
+def test_row_locality():
+    """Prop. "Causality": the projection acts on each row independently."""
+    alg = Alg(3, (2, 3, 4), (3, 3, 2))
+    g = rng(12)
+    M = 9
+    X, W = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N))
+    t = (np.arange(M) % 3).astype(np.int32)
+    bias = g.standard_normal(alg.N)
+    Y0, _, _, _ = oracle.proj_fwd(alg, t, X, W, bias, "gelu")
+    for b in range(M):
+        X2 = X.copy()
+        X2[b] += g.standard_normal(alg.K)
+        Y2, _, _, _ = oracle.proj_fwd(alg, t, X2, W, bias, "gelu")
+        changed = np.nonzero(np.any(Y2 != Y0, axis=1))[0]
+        assert list(changed) == [b]
+        # and the result of a row does not depend on its neighbours' presence
+        Yb, _, _, _ = oracle.proj_fwd(alg, t[b:b + 1], X[b:b + 1], W, bias, "gelu")
+        np.testing.assert_array_equal(Yb[0], Y0[b])
+
+
+# ---- P11: backward -------------------------------------------------------------
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+def test_adjoint_identity(law):
+    """<Phi(X,W), G> = <X, dX> = <W, dW>, exact by bilinearity (App. VJPs)."""
+    alg = Alg(4, (2, 3, 1, 2), (3, 1, 2, 2), law)
+    g = rng(13)
+    M = 15
+    X, W, G = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N)), g.standard_normal((M, alg.N))
+    t = g.integers(0, 4, M).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, W)
+    dX = oracle.proj_bwd_data(alg, t, G, W)
+    dW, _ = oracle.proj_bwd_weight(alg, t, X, G)
+    a, b, c = np.sum(Y * G), np.sum(X * dX), np.sum(W * dW)
+    assert abs(a - b) < 1e-10 * max(1, abs(a)) and abs(a - c) < 1e-10 * max(1, abs(a))
+    # the adjoint pairs fail for a wrong gradient: the dense gradient under the star law
+    if law == "star":
+        dXd = oracle.proj_bwd_data(Alg(alg.q, alg.s, alg.r, "dense"), t, G, W)
+        assert abs(np.sum(X * dXd) - a) > 1e-3
+
+
+def test_finite_differences_through_activation():
+    """Central differences of L = <G, Phi_W2(act(Phi_W1(X) + b1)) + b2> against
+    the chained VJPs (act' applied to the pre-activation)."""
+    up, down = Alg(2, (2, 3), (3, 2)), Alg(2, (3, 2), (2, 2))
+    g = rng(14)
+    M = 5
+    X = g.standard_normal((M, up.K))
+    W1, W2 = g.standard_normal((up.K, up.N)) * 0.7, g.standard_normal((down.K, down.N)) * 0.7
+    b1, b2 = g.standard_normal(up.N), g.standard_normal(down.N)
+    G = g.standard_normal((M, down.N))
+    t = (np.arange(M) % 2).astype(np.int32)
+
+    def loss(X_, W1_, W2_, b1_, b2_):
+        _, _, Y = oracle.ffn_fwd(up, down, t, X_, W1_, b1_, W2_, b2_, "gelu", mirror_bf16=False)
+        return float(np.sum(G * Y))
+
+    Z, H, _ = oracle.ffn_fwd(up, down, t, X, W1, b1, W2, b2, "gelu", mirror_bf16=False)
+    gr = oracle.ffn_bwd(up, down, t, X, Z, H, W1, W2, G, "gelu", mirror_bf16=False)
+    h = 1e-5
+    for name, arr, grad in [("X", X, gr["dX"]), ("W1", W1, gr["dW_up"]), ("W2", W2, gr["dW_down"]),
+                            ("b1", b1, gr["db_up"]), ("b2", b2, gr["db_down"])]:
+        flat = arr.reshape(-1)
+        for idx in range(flat.size):
+            old = flat[idx]
+            flat[idx] = old + h
+            lp = loss(X, W1, W2, b1, b2)
+            flat[idx] = old - h
+            lm = loss(X, W1, W2, b1, b2)
+            flat[idx] = old
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - grad.reshape(-1)[idx]) < 1e-6 * max(1.0, abs(fd)), (name, idx)
+
+
+def test_bwd_weight_entries_match_full():
+    alg = Alg(3, (4, 2, 3), (2, 5, 3))
+    g = rng(15)
+    M = 19
+    X, dY = g.standard_normal((M, alg.K)), g.standard_normal((M, alg.N))
+    t = g.integers(0, 3, M).astype(np.int32)
+    t[t == 1] = 0  # an absent type: its off-diagonal row of blocks is zero
+    dW, _ = oracle.proj_bwd_weight(alg, t, X, dY)
+    kk, nn = np.meshgrid(np.arange(alg.K), np.arange(alg.N), indexing="ij")
+    ent = oracle.bwd_weight_entries(alg, t, X, dY, kk.ravel(), nn.ravel())
+    np.testing.assert_allclose(ent.reshape(alg.K, alg.N), dW, atol=1e-12)
+    # type 1 absent: W_1j (j != 1) gets no gradient
+    np.testing.assert_array_equal(dW[4:6, :2], 0)
+    np.testing.assert_array_equal(dW[4:6, 7:], 0)
+    assert np.all(dW[4:6, 2:7] != 0)
+
+
+# ---- P12: counts ---------------------------------------------------------------
+
+@pytest.mark.parametrize("q", [1, 2, 3, 4, 8, 16])
+def test_product_counts(q):
+    for i in range(q):
+        assert oracle.products_per_type("star", q, i) == 2 * q - 1
+        assert oracle.products_per_type("dense", q, i) == q * q
+    # rho_q = (2q-1)/q^2 for equal groups (eq. rho)
+    alg = Alg.equal(q, 8 * q, 4 * q)
+    for i in range(q):
+        assert oracle.row_macs(alg, i) * q * q == (2 * q - 1) * alg.K * alg.N
+
+
+def test_unequal_row_cost_and_batch_cost():
+    """eq. unequal-row-cost C_i = D_diag + s_i (N - r_i) and
+    eq. rectangular-batch-cost, against the MACs the oracle visits."""
+    s, r = (2, 5, 3, 1), (4, 1, 2, 6)
+    alg = Alg(4, s, r)
+    D_diag = sum(a * b for a, b in zip(s, r))
+    N = sum(r)
+    for i in range(4):
+        assert oracle.row_macs(alg, i) == D_diag + s[i] * (N - r[i])
+    g = rng(16)
+    M = 31
+    t = g.integers(0, 4, M).astype(np.int32)
+    X, W = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N))
+    _, _, macs, _ = oracle.proj_fwd(alg, t, X, W)
+    Mi = np.bincount(t, minlength=4)
+    assert macs == M * D_diag + sum(int(Mi[i]) * s[i] * (N - r[i]) for i in range(4))
+
+
+# ---- P13: activations ------------------------------------------------------------
+
+def test_gelu_against_libm():
+    zs = np.linspace(-8, 8, 161)
+    for z in zs:
+        exact = 0.5 * z * (1 + math.erf(z / math.sqrt(2)))
+        assert abs(oracle.act("gelu", z)[()] - exact) <= 1e-15 * max(1, abs(exact))
+        tanh_form = 0.5 * z * (1 + math.tanh(math.sqrt(2 / math.pi) * (z + 0.044715 * z ** 3)))
+        assert abs(oracle.act("gelu_tanh", z)[()] - tanh_form) <= 1e-15 * max(1, abs(tanh_form))
+    assert oracle.act("none", 1.25)[()] == 1.25
+
+
+@pytest.mark.parametrize("kind", ["gelu", "gelu_tanh", "none"])
+def test_activation_gradient_fd(kind):
+    h = 1e-6
+    for z in np.linspace(-6, 6, 61):
+        fd = (oracle.act(kind, z + h)[()] - oracle.act(kind, z - h)[()]) / (2 * h)
+        assert abs(fd - oracle.act_grad(kind, z)[()]) < 1e-8
+
+
+def test_bias_and_activation_applied():
+    alg = Alg(2, (3, 3), (3, 3))
+    g = rng(17)
+    X = g.standard_normal((6, 6))
+    bias = g.standard_normal(6)
+    t = (np.arange(6) % 2).astype(np.int32)
+    Y, Z, _, _ = oracle.proj_fwd(alg, t, X, np.eye(6), bias, "gelu", want_z=True)
+    np.testing.assert_allclose(Z, X + bias, atol=1e-15)
+    erf = np.vectorize(math.erf)
+    np.testing.assert_allclose(Y, 0.5 * Z * (1 + erf(Z / math.sqrt(2))), atol=1e-15)
+
+
+# ---- P14: bfloat16 rounding -----------------------------------------------------------
+
+def test_round_bf16_against_torch():
+    torch = pytest.importorskip("torch")
+    import synth
+    g = rng(18)
+    x = np.concatenate([
+        g.standard_normal(20000).astype(np.float32),
+        (g.standard_normal(2000) * 1e-30).astype(np.float32),
+        (g.standard_normal(2000) * 1e30).astype(np.float32),
+        # exact ties: 8 significant bits plus a trailing half
+        np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 2 ** -130 * 3, 0.0, -0.0], np.float32),
+    ])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x.astype(np.float64)), ref)
+    np.testing.assert_array_equal(synth.bf16_bits_to_f64(synth.f32_to_bf16_bits(x)), ref)
+
+
+# ---- P15: decode stack of one layer ------------------------------------------------------
+
+def test_decode_one_layer_is_ffn_plus_residual():
+    up, down = Alg(2, (4, 4), (8, 8)), Alg(2, (8, 8), (4, 4))
+    g = rng(19)
+    M = 3
+    X = oracle.round_bf16(g.standard_normal((M, 8)))
+    Wu, Wd = g.standard_normal((8, 16)) * 0.1, g.standard_normal((16, 8)) * 0.1
+    bu, bd = g.standard_normal(16) * 0.1, g.standard_normal(8) * 0.1
+    t = np.array([1, 0, 1], np.int32)
+    h = oracle.decode_stack(up, down, t, X, [Wu], [bu], [Wd], [bd])
+    _, _, f = oracle.ffn_fwd(up, down, t, X, Wu, bu, Wd, bd)
+    np.testing.assert_allclose(h, X + f, atol=0)
+    # the stack applies its layers in order
+    h2 = oracle.decode_stack(up, down, t, X, [Wu, Wu * 0.5], [bu, bu], [Wd, Wd], [bd, bd])
+    a = oracle.round_bf16(h)
+    _, _, f2 = oracle.ffn_fwd(up, down, t, a, Wu * 0.5, bu, Wd, bd)
+    np.testing.assert_allclose(h2, h + f2, atol=0)
+
+
+def test_out_of_range_type_rejected():
+    alg = Alg(2, (2, 2), (2, 2))
+    with pytest.raises(ValueError):
+        oracle.proj_fwd(alg, np.array([0, 2], np.int32), np.zeros((2, 4)), np.zeros((4, 4)))
