@@ -1,0 +1,228 @@
+/*
+ * star_proj.h -- C ABI of the MI355X (gfx950) row-typed associative-algebra
+ * projection library (libstarq.so).
+ *
+ * The operation (Sec. 4, "Transformer Projections", eqs. typed-diag and
+ * typed-off; Sec. 5.1, Alg. 1).  X is M x K, W is K x N, both row-major.  The
+ * K input features form q contiguous groups of widths s[0..q-1] and the N
+ * output features q contiguous groups of widths r[0..q-1]; W_kj is the block
+ * of rows of input group k and columns of output group j.  Row b carries a
+ * type t_b in [0, q).  A type-i row computes, for every output group j,
+ *
+ *     y_j = sum over k in B(i,j) of x_k W_kj
+ *
+ * with B(i,j) = {i, j} as a set for the complete-graph algebra Q_q
+ * (STAR_LAW_STAR: y_i = x_i W_ii and y_j = x_i W_ij + x_j W_jj for j != i),
+ * or B(i,j) = {0..q-1} for the ordinary product XW (STAR_LAW_DENSE, the
+ * same-code dense control).  All q x q blocks of W are parameters; blocks a
+ * row's support skips are never read for that row.  The paper's 1-based
+ * cyclic schedule tau(p) = 1 + ((p-1) mod q) is t = p mod q for 0-based
+ * positions; the library takes the type vector explicitly and bakes in no
+ * schedule.
+ *
+ * Conventions shared by every entry point
+ *  - Pointers named "device" are HIP device pointers on the current device;
+ *    "host" pointers are read during the call only.  The caller owns and
+ *    allocates every buffer, including the workspace; the library keeps no
+ *    pointer after a call returns.
+ *  - Calls are asynchronous on `stream` (0 = the null stream).  Argument
+ *    errors are found on the host before anything is launched: the call then
+ *    returns a non-zero status and writes nothing.  A failed launch returns
+ *    STAR_ERR_HIP.  Nothing is printed and no exception crosses the ABI.
+ *  - Group widths must be positive multiples of 8 and q at most STAR_MAX_Q.
+ *    Operand, output and workspace pointers must be 16-byte aligned.
+ *  - Row types must lie in [0, q).  This is not checked by the compute calls
+ *    (star_validate_types checks it); a row with an out-of-range type is left
+ *    out of every product and its output row is not written.
+ *  - M = 0 is a no-op returning STAR_OK.  A type with no rows is legal; the
+ *    weight-gradient blocks only that type reaches are written as zeros.
+ *  - Operand dtypes: all-F32 or all-BF16 (BF16 operands accumulate in FP32).
+ *    Outputs may be F32 or BF16.  Weight and bias gradients are always F32.
+ *    Biases are F32.
+ *  - Determinism: every output element has one owner and is summed in a fixed
+ *    order, so repeated calls on the same inputs give bitwise equal results.
+ */
+#ifndef STAR_PROJ_H
+#define STAR_PROJ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define STAR_MAX_Q 64
+
+typedef enum {
+    STAR_OK = 0,
+    STAR_ERR_ARG = 1,        /* null pointer, bad enum, q out of range */
+    STAR_ERR_SHAPE = 2,      /* widths inconsistent, sizes too large */
+    STAR_ERR_DTYPE = 3,      /* unsupported dtype combination */
+    STAR_ERR_ALIGN = 4,      /* width not a multiple of 8, pointer not 16-byte aligned */
+    STAR_ERR_WORKSPACE = 5,  /* workspace missing or smaller than star_workspace_bytes() */
+    STAR_ERR_UNSUPPORTED = 6,
+    STAR_ERR_HIP = 7         /* a HIP runtime call or launch failed */
+} star_status;
+
+typedef enum { STAR_F32 = 0, STAR_BF16 = 1 } star_dtype;
+
+/* Pointwise activation applied after the bias.  GELU is the erf form
+ * 0.5 z (1 + erf(z / sqrt 2)); GELU_TANH the tanh approximation.  The paper
+ * keeps activations at their usual definitions (Sec. 4, "Projection
+ * Shapes"). */
+typedef enum { STAR_ACT_NONE = 0, STAR_ACT_GELU = 1, STAR_ACT_GELU_TANH = 2 } star_act;
+
+/* STAR_LAW_STAR: B(i,j) = {i,j} (Sec. 5.1).  STAR_LAW_DENSE: all q^2 block
+ * products, i.e. the ordinary product XW (eq. dense-two), run through the
+ * same kernels as the control. */
+typedef enum { STAR_LAW_STAR = 0, STAR_LAW_DENSE = 1 } star_law;
+
+/* An algebra layout.  s and r are host arrays of q widths (input groups,
+ * output groups). */
+typedef struct {
+    int32_t q;
+    const int64_t *s;
+    const int64_t *r;
+    star_law law;
+} star_algebra;
+
+typedef enum {
+    STAR_OP_FWD = 0,
+    STAR_OP_BWD_DATA = 1,
+    STAR_OP_BWD_WEIGHT = 2,
+    STAR_OP_FFN_FWD = 3,
+    STAR_OP_DECODE = 4
+} star_op;
+
+/*
+ * Forward projection with fused bias and activation (Alg. 1; eqs. typed-diag,
+ * typed-off).
+ *   row_type  device int32[M]
+ *   X         device [M, K] row-major, dtype xt
+ *   W         device [K, N] row-major (the canonical bank, never repacked),
+ *             dtype wt == xt
+ *   bias      device float[N] or NULL; added to every output column for
+ *             every row type
+ *   Z_out     device [M, N] of dtype yt, or NULL: the pre-activation
+ *             Z = X *_q W + bias, kept for the backward pass
+ *   Y         device [M, N] of dtype yt: act(Z)
+ *   ws        device workspace of at least
+ *             star_workspace_bytes(STAR_OP_FWD, alg, NULL, M) bytes
+ */
+star_status star_proj_fwd(const star_algebra *alg, int64_t M, const int32_t *row_type,
+                          const void *X, star_dtype xt, const void *W, star_dtype wt,
+                          const float *bias, star_act act, void *Z_out, void *Y,
+                          star_dtype yt, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Activation gradient (App. "Vector--Jacobian Products", eqs. vjp-xi and
+ * vjp-xj): for a type-i row with output gradient dY,
+ *   dX_i = sum_j dY_j W_ij^T   and   dX_k = dY_k W_kk^T (k != i)
+ * (law DENSE: dX = dY W^T).  If Z_prev is given, the result is multiplied
+ * elementwise by act_prev'(Z_prev): the gradient through the activation that
+ * produced this projection's input, fused into the epilogue.
+ *   dY      device [M, N], dtype dyt
+ *   W       device [K, N], dtype wt == dyt
+ *   Z_prev  device [M, K] of dtype dyt, or NULL
+ *   dX      device [M, K] of dtype dxt, overwritten
+ *   ws      at least star_workspace_bytes(STAR_OP_BWD_DATA, alg, NULL, M) bytes
+ */
+star_status star_proj_bwd_data(const star_algebra *alg, int64_t M, const int32_t *row_type,
+                               const void *dY, star_dtype dyt, const void *W, star_dtype wt,
+                               const void *Z_prev, star_act act_prev, void *dX,
+                               star_dtype dxt, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Weight and bias gradients (eqs. vjp-wii, vjp-wij, vjp-wjj):
+ *   dW_jj = sum over all rows of x_j^T dY_j
+ *   dW_ij = sum over rows of type i of x_i^T dY_j   (j != i)
+ *   dbias = sum over all rows of dY
+ * (law DENSE: dW = X^T dY).  dW and dbias are overwritten with the full-batch
+ * sums; a block that no row reaches is written as zeros.
+ *   X      device [M, K], dtype xt
+ *   dY     device [M, N], dtype dyt == xt
+ *   dW     device float[K, N]
+ *   dbias  device float[N] or NULL
+ *   ws     at least star_workspace_bytes(STAR_OP_BWD_WEIGHT, alg, NULL, M) bytes
+ */
+star_status star_proj_bwd_weight(const star_algebra *alg, int64_t M, const int32_t *row_type,
+                                 const void *X, star_dtype xt, const void *dY, star_dtype dyt,
+                                 float *dW, float *dbias, void *ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/*
+ * Two-map FFN forward with the same row types on both projections
+ * (Sec. 4, "Projection Shapes"; Sec. 5.2):
+ *   Z_up = X *_q W_up + b_up;  H = act(Z_up);  Y = H *_q W_down + b_down.
+ * up is D -> F, down is F -> D (down's input widths equal up's output
+ * widths).  Operands and H have dtype dt; Z_up (optional, for the backward
+ * pass) has dtype dt; Y has dtype yt.
+ *   X device [M, D]; W_up device [D, F]; W_down device [F, D];
+ *   b_up device float[F] or NULL; b_down device float[D] or NULL;
+ *   Z_up device [M, F] or NULL; H device [M, F]; Y device [M, D].
+ *   ws at least star_workspace_bytes(STAR_OP_FFN_FWD, up, down, M) bytes.
+ */
+star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64_t M,
+                         const int32_t *row_type, const void *X, const void *W_up,
+                         const float *b_up, const void *W_down, const float *b_down,
+                         star_act act, void *Z_up, void *H, void *Y, star_dtype dt,
+                         star_dtype yt, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One decode step of an FFN stack (Sec. 5.3, "One-Token Inference": the FFN
+ * applies Alg. 1 with the new position's row type).  M rows (one new token
+ * per sequence, M <= 64) run through n_layers layers of
+ *   h <- h + (act(a *_q W_up[l] + b_up[l]) *_q W_down[l] + b_down[l]),
+ * where a is h rounded to bfloat16 and h starts as X and is carried in FP32
+ * (without `residual` the FFN output replaces h).  The hidden activation is
+ * stored in bfloat16.  This is a skinny, weight-bandwidth-bound product: every
+ * weight block that some row's support reaches is read once per step.
+ *   row_type  device int32[M]
+ *   X         device bf16 [M, D]
+ *   W_up, W_down, b_up, b_down: host arrays of n_layers device pointers
+ *             (bf16 [D, F], bf16 [F, D], float[F] or NULL, float[D] or NULL)
+ *   Y         device [M, D] of dtype yt: the final h
+ *   ws        at least star_workspace_bytes(STAR_OP_DECODE, up, down, M) bytes
+ */
+star_status star_decode(const star_algebra *up, const star_algebra *down, int32_t n_layers,
+                        int64_t M, const int32_t *row_type, const void *X,
+                        const void *const *W_up, const float *const *b_up,
+                        const void *const *W_down, const float *const *b_down,
+                        star_act act, int32_t residual, void *Y, star_dtype yt,
+                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes an entry point needs (alg2 is the down algebra for
+ * STAR_OP_FFN_FWD and STAR_OP_DECODE, else ignored).  Returns 0 for invalid
+ * arguments. */
+size_t star_workspace_bytes(int32_t op, const star_algebra *alg, const star_algebra *alg2,
+                            int64_t M);
+
+/* Block products a type-i row evaluates, written to host per_type[q]:
+ * 2q-1 for STAR_LAW_STAR (eq. q-rank: 2q^2 - q over all types), q^2 for
+ * STAR_LAW_DENSE. */
+star_status star_count_products(const star_algebra *alg, int64_t *per_type);
+
+/* Multiply-accumulates of one forward pass over rows with the given
+ * per-type counts (eq. rectangular-batch-cost):
+ * sum_i rows_per_type[i] * (D_diag + s_i (N - r_i)) for the star law. */
+star_status star_count_macs(const star_algebra *alg, const int64_t *rows_per_type,
+                            int64_t *macs);
+
+/* Counts the rows whose type lies outside [0, q) and stores the count in
+ * host *n_bad.  Synchronises `stream`.  ws: at least 16 bytes of device
+ * memory. */
+star_status star_validate_types(int64_t M, const int32_t *row_type, int32_t q,
+                                int64_t *n_bad, void *ws, size_t ws_bytes,
+                                hipStream_t stream);
+
+/* Static description of a status code. */
+const char *star_status_string(star_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STAR_PROJ_H */

@@ -1,0 +1,271 @@
+"""ctypes binding of libstarq's C ABI (``include/star_proj.h``).
+
+Argument marshalling only: torch tensors supply device pointers, the current
+HIP stream, and (when the caller passes none) output and workspace buffers.
+Every step of the computation runs in the library's HIP kernels.  Importing
+this module fails loudly if ``libstarq.so`` has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libstarq.so")
+
+STAR_OK = 0
+STATUS_NAMES = {0: "STAR_OK", 1: "STAR_ERR_ARG", 2: "STAR_ERR_SHAPE", 3: "STAR_ERR_DTYPE",
+                4: "STAR_ERR_ALIGN", 5: "STAR_ERR_WORKSPACE", 6: "STAR_ERR_UNSUPPORTED",
+                7: "STAR_ERR_HIP"}
+DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2}
+LAWS = {"star": 0, "dense": 1}
+OPS = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2, "ffn_fwd": 3, "decode": 4}
+MAX_Q = 64
+
+
+class StarError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} "
+                         f"({star_status_string(status)})")
+
+
+class _CAlgebra(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_int32), ("s", ctypes.POINTER(ctypes.c_int64)),
+                ("r", ctypes.POINTER(ctypes.c_int64)), ("law", ctypes.c_int)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_32814_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    A = ctypes.POINTER(_CAlgebra)
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    E = ctypes.c_int
+    lib.star_proj_fwd.argtypes = [A, i64, P, P, E, P, E, P, E, P, P, E, P, sz, P]
+    lib.star_proj_bwd_data.argtypes = [A, i64, P, P, E, P, E, P, E, P, E, P, sz, P]
+    lib.star_proj_bwd_weight.argtypes = [A, i64, P, P, E, P, E, P, P, P, sz, P]
+    lib.star_ffn_fwd.argtypes = [A, A, i64, P, P, P, P, P, P, E, P, P, P, E, E, P, sz, P]
+    lib.star_decode.argtypes = [A, A, i32, i64, P, P, ctypes.POINTER(P), ctypes.POINTER(P),
+                                ctypes.POINTER(P), ctypes.POINTER(P), E, i32, P, E, P, sz, P]
+    lib.star_workspace_bytes.argtypes = [i32, A, A, i64]
+    lib.star_workspace_bytes.restype = sz
+    lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
+    lib.star_count_macs.argtypes = [A, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    lib.star_validate_types.argtypes = [i64, P, i32, ctypes.POINTER(i64), P, sz, P]
+    lib.star_status_string.argtypes = [E]
+    lib.star_status_string.restype = ctypes.c_char_p
+    for name in ("star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
+                 "star_decode", "star_count_products", "star_count_macs", "star_validate_types"):
+        getattr(lib, name).restype = E
+    return lib
+
+
+LIB = _load()
+
+
+class Algebra:
+    """q groups of input widths ``s`` and output widths ``r`` under a law."""
+
+    def __init__(self, q: int, s: Sequence[int], r: Sequence[int], law: str = "star"):
+        self.q, self.law = int(q), law
+        self.s, self.r = tuple(int(v) for v in s), tuple(int(v) for v in r)
+        if len(self.s) != self.q or len(self.r) != self.q:
+            raise ValueError("s and r need q entries each")
+        self._s = (ctypes.c_int64 * self.q)(*self.s)
+        self._r = (ctypes.c_int64 * self.q)(*self.r)
+        self._c = _CAlgebra(self.q, ctypes.cast(self._s, ctypes.POINTER(ctypes.c_int64)),
+                            ctypes.cast(self._r, ctypes.POINTER(ctypes.c_int64)), LAWS[law])
+
+    @classmethod
+    def equal(cls, q: int, K: int, N: int, law: str = "star") -> "Algebra":
+        if K % q or N % q:
+            raise ValueError("equal groups need q | K and q | N")
+        return cls(q, [K // q] * q, [N // q] * q, law)
+
+    @property
+    def K(self) -> int:
+        return sum(self.s)
+
+    @property
+    def N(self) -> int:
+        return sum(self.r)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self._c)
+
+    def with_law(self, law: str) -> "Algebra":
+        return Algebra(self.q, self.s, self.r, law)
+
+    def __repr__(self):
+        return f"Algebra(q={self.q}, s={self.s}, r={self.r}, law={self.law!r})"
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check(status: int, where: str):
+    if status != STAR_OK:
+        raise StarError(status, where)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype not in DTYPES:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return DTYPES[t.dtype]
+
+
+def _ws(op: str, alg: Algebra, alg2, M: int, device, ws):
+    need = star_workspace_bytes(op, alg, alg2, M)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
+
+
+def star_status_string(status: int) -> str:
+    return LIB.star_status_string(int(status)).decode()
+
+
+def star_workspace_bytes(op: str, alg: Algebra, alg2: Algebra | None, M: int) -> int:
+    return int(LIB.star_workspace_bytes(OPS[op], alg.ref, alg2.ref if alg2 else None, int(M)))
+
+
+def star_count_products(alg: Algebra) -> list[int]:
+    out = (ctypes.c_int64 * alg.q)()
+    _check(LIB.star_count_products(alg.ref, out), "star_count_products")
+    return list(out)
+
+
+def star_count_macs(alg: Algebra, rows_per_type: Sequence[int]) -> int:
+    rows = (ctypes.c_int64 * alg.q)(*[int(v) for v in rows_per_type])
+    macs = ctypes.c_int64()
+    _check(LIB.star_count_macs(alg.ref, rows, ctypes.byref(macs)), "star_count_macs")
+    return int(macs.value)
+
+
+def star_validate_types(row_type: torch.Tensor, q: int, ws=None) -> int:
+    n_bad = ctypes.c_int64()
+    ws = ws if ws is not None else torch.empty(16, dtype=torch.uint8, device=row_type.device)
+    _check(LIB.star_validate_types(row_type.numel(), _ptr(row_type), int(q), ctypes.byref(n_bad),
+                                   _ptr(ws), ws.numel(), _stream(row_type.device)),
+           "star_validate_types")
+    return int(n_bad.value)
+
+
+def star_proj_fwd(alg: Algebra, row_type: torch.Tensor, X: torch.Tensor, W: torch.Tensor,
+                  bias: torch.Tensor | None = None, act: str = "none", Z_out=None, Y=None,
+                  out_dtype=None, ws=None):
+    """Y = act(X *_q W + bias).  ``Z_out=True`` allocates and returns the
+    pre-activation too.  Returns Y, or (Y, Z) when Z_out is requested."""
+    M = X.shape[0]
+    dev = X.device
+    out_dtype = out_dtype or X.dtype
+    if Y is None:
+        Y = torch.empty((M, alg.N), dtype=out_dtype, device=dev)
+    want_z = Z_out is not None and Z_out is not False
+    if Z_out is True:
+        Z_out = torch.empty((M, alg.N), dtype=Y.dtype, device=dev)
+    ws, nbytes = _ws("fwd", alg, None, M, dev, ws)
+    _check(LIB.star_proj_fwd(alg.ref, M, _ptr(row_type), _ptr(X), _dt(X), _ptr(W), _dt(W),
+                             _ptr(bias), ACTS[act], _ptr(Z_out) if want_z else None, _ptr(Y),
+                             _dt(Y), _ptr(ws), nbytes, _stream(dev)), "star_proj_fwd")
+    return (Y, Z_out) if want_z else Y
+
+
+def star_proj_bwd_data(alg: Algebra, row_type: torch.Tensor, dY: torch.Tensor, W: torch.Tensor,
+                       Z_prev: torch.Tensor | None = None, act_prev: str = "none", dX=None,
+                       out_dtype=None, ws=None):
+    """dX = (dY *_q^T W) [. act_prev'(Z_prev)]."""
+    M = dY.shape[0]
+    dev = dY.device
+    if dX is None:
+        dX = torch.empty((M, alg.K), dtype=out_dtype or dY.dtype, device=dev)
+    ws, nbytes = _ws("bwd_data", alg, None, M, dev, ws)
+    _check(LIB.star_proj_bwd_data(alg.ref, M, _ptr(row_type), _ptr(dY), _dt(dY), _ptr(W), _dt(W),
+                                  _ptr(Z_prev), ACTS[act_prev], _ptr(dX), _dt(dX), _ptr(ws),
+                                  nbytes, _stream(dev)), "star_proj_bwd_data")
+    return dX
+
+
+def star_proj_bwd_weight(alg: Algebra, row_type: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
+                         dW=None, dbias=None, want_dbias: bool = True, ws=None):
+    """(dW, dbias) in fp32; dbias is None unless requested."""
+    M = X.shape[0]
+    dev = X.device
+    if dW is None:
+        dW = torch.empty((alg.K, alg.N), dtype=torch.float32, device=dev)
+    if dbias is None and want_dbias:
+        dbias = torch.empty(alg.N, dtype=torch.float32, device=dev)
+    ws, nbytes = _ws("bwd_weight", alg, None, M, dev, ws)
+    _check(LIB.star_proj_bwd_weight(alg.ref, M, _ptr(row_type), _ptr(X), _dt(X), _ptr(dY),
+                                    _dt(dY), _ptr(dW), _ptr(dbias), _ptr(ws), nbytes,
+                                    _stream(dev)), "star_proj_bwd_weight")
+    return dW, dbias
+
+
+def star_ffn_fwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                 W_up: torch.Tensor, b_up, W_down: torch.Tensor, b_down, act: str = "gelu",
+                 save_z: bool = True, H=None, Y=None, Z_up=None, out_dtype=None, ws=None):
+    """Returns (Z_up or None, H, Y)."""
+    M = X.shape[0]
+    dev = X.device
+    if H is None:
+        H = torch.empty((M, up.N), dtype=X.dtype, device=dev)
+    if Y is None:
+        Y = torch.empty((M, down.N), dtype=out_dtype or X.dtype, device=dev)
+    if save_z and Z_up is None:
+        Z_up = torch.empty((M, up.N), dtype=X.dtype, device=dev)
+    ws, nbytes = _ws("ffn_fwd", up, down, M, dev, ws)
+    _check(LIB.star_ffn_fwd(up.ref, down.ref, M, _ptr(row_type), _ptr(X), _ptr(W_up), _ptr(b_up),
+                            _ptr(W_down), _ptr(b_down), ACTS[act], _ptr(Z_up) if save_z else None,
+                            _ptr(H), _ptr(Y), _dt(X), _dt(Y), _ptr(ws), nbytes, _stream(dev)),
+           "star_ffn_fwd")
+    return (Z_up if save_z else None), H, Y
+
+
+def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                W_ups: Sequence[torch.Tensor], b_ups, W_downs: Sequence[torch.Tensor], b_downs,
+                act: str = "gelu", residual: bool = True, Y=None, out_dtype=None, ws=None):
+    """One decode step through ``len(W_ups)`` FFN layers; returns Y."""
+    M = X.shape[0]
+    dev = X.device
+    L = len(W_ups)
+    if Y is None:
+        Y = torch.empty((M, up.K), dtype=out_dtype or X.dtype, device=dev)
+    P = ctypes.c_void_p
+    wu = (P * L)(*[t.data_ptr() for t in W_ups])
+    wd = (P * L)(*[t.data_ptr() for t in W_downs])
+    bu = (P * L)(*[t.data_ptr() if t is not None else None for t in b_ups]) if b_ups is not None else None
+    bd = (P * L)(*[t.data_ptr() if t is not None else None for t in b_downs]) if b_downs is not None else None
+    ws, nbytes = _ws("decode", up, down, M, dev, ws)
+    _check(LIB.star_decode(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), wu, bu, wd, bd,
+                           ACTS[act], int(bool(residual)), _ptr(Y), _dt(Y), _ptr(ws), nbytes,
+                           _stream(dev)), "star_decode")
+    return Y
+
+
+def star_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                 Z_up: torch.Tensor, H: torch.Tensor, W_up: torch.Tensor, W_down: torch.Tensor,
+                 dY: torch.Tensor, act: str = "gelu", ws=None):
+    """Backward of ``star_ffn_fwd`` as four library calls on one stream:
+    dZ = (dY *^T W_down) . act'(Z_up)  (fused epilogue);  dW_down, db_down from
+    (H, dY);  dW_up, db_up from (X, dZ);  dX = dZ *^T W_up.
+    Returns a dict of dX, dZ, dW_up, db_up, dW_down, db_down."""
+    dZ = star_proj_bwd_data(down, row_type, dY, W_down, Z_prev=Z_up, act_prev=act,
+                            out_dtype=X.dtype, ws=ws)
+    dW_down, db_down = star_proj_bwd_weight(down, row_type, H, dY, ws=ws)
+    dW_up, db_up = star_proj_bwd_weight(up, row_type, X, dZ, ws=ws)
+    dX = star_proj_bwd_data(up, row_type, dZ, W_up, ws=ws)
+    return dict(dX=dX, dZ=dZ, dW_up=dW_up, db_up=db_up, dW_down=dW_down, db_down=db_down)

@@ -1,0 +1,537 @@
+// C ABI of libstarq: argument validation, workspace layout, tile planning
+// and kernel launches.  Every argument error is detected here, before any
+// launch.  The only process-wide state is a read-only cache of each device's
+// compute-unit count.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/star_proj.h"
+#include "kernels.hpp"
+
+namespace {
+
+using namespace starq;
+
+static_assert(STAR_MAX_Q == kMaxQGroups, "one q limit for the ABI and the kernels");
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxDim = (int64_t{1} << 30);
+
+size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+struct Alg {
+  int q = 0;
+  int law = 0;
+  int64_t S[kMaxQGroups + 1];  // input group starts
+  int64_t R[kMaxQGroups + 1];  // output group starts
+  int64_t K() const { return S[q]; }
+  int64_t N() const { return R[q]; }
+  int64_t s(int g) const { return S[g + 1] - S[g]; }
+  int64_t r(int g) const { return R[g + 1] - R[g]; }
+};
+
+star_status parse_alg(const star_algebra* a, Alg& out) {
+  if (!a || !a->s || !a->r) return STAR_ERR_ARG;
+  if (a->q < 1 || a->q > kMaxQGroups) return STAR_ERR_ARG;
+  if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE) return STAR_ERR_ARG;
+  out.q = a->q;
+  out.law = a->law;
+  out.S[0] = out.R[0] = 0;
+  for (int g = 0; g < a->q; ++g) {
+    if (a->s[g] <= 0 || a->r[g] <= 0) return STAR_ERR_SHAPE;
+    if (a->s[g] % 8 || a->r[g] % 8) return STAR_ERR_ALIGN;
+    out.S[g + 1] = out.S[g] + a->s[g];
+    out.R[g + 1] = out.R[g] + a->r[g];
+    if (out.S[g + 1] > kMaxDim || out.R[g + 1] > kMaxDim) return STAR_ERR_SHAPE;
+  }
+  return STAR_OK;
+}
+
+bool valid_dtype(star_dtype d) { return d == STAR_F32 || d == STAR_BF16; }
+bool valid_act(star_act a) {
+  return a == STAR_ACT_NONE || a == STAR_ACT_GELU || a == STAR_ACT_GELU_TANH;
+}
+
+int cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64) {
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  if (dev < 64) cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+// ---- workspace layouts -----------------------------------------------------
+
+struct PlanWs {
+  size_t perm = 0, offsets = 0, end = 0;
+};
+PlanWs plan_layout(int64_t M, int q, size_t base = 0) {
+  PlanWs w;
+  w.perm = base;
+  w.offsets = align_up(w.perm + sizeof(int32_t) * static_cast<size_t>(std::max<int64_t>(M, 1)));
+  w.end = align_up(w.offsets + sizeof(int32_t) * (q + 1));
+  return w;
+}
+
+int tiles_of(int64_t w, int tile) { return static_cast<int>((w + tile - 1) / tile); }
+
+int bwd_weight_nsplit(const Alg& a, int64_t M) {
+  int64_t mt = 0, nt = 0;
+  for (int g = 0; g < a.q; ++g) {
+    mt += tiles_of(a.s(g), kTileM);
+    nt += tiles_of(a.r(g), kTileN);
+  }
+  const int64_t base = mt * nt;
+  int64_t ns = (512 + base - 1) / base;
+  ns = std::min<int64_t>(ns, 8);
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, M / 1024));
+  return static_cast<int>(std::max<int64_t>(ns, 1));
+}
+
+struct BwdWs {
+  PlanWs plan;
+  int nsplit = 1;
+  size_t partial = 0, dbias_part = 0, end = 0;
+};
+BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
+  BwdWs w;
+  w.plan = plan_layout(M, a.q);
+  w.nsplit = bwd_weight_nsplit(a, M);
+  size_t cur = w.plan.end;
+  if (w.nsplit > 1) {
+    w.partial = cur;
+    cur = align_up(cur + sizeof(float) * static_cast<size_t>(w.nsplit) * a.K() * a.N());
+    w.dbias_part = cur;
+    cur = align_up(cur + sizeof(float) * static_cast<size_t>(w.nsplit) * a.N());
+  }
+  w.end = cur;
+  return w;
+}
+
+struct DecodeWs {
+  size_t h = 0, xb = 0, H = 0, partial = 0, counters = 0, end = 0;
+  int nt_up = 0, nt_down = 0, nk_up = 0, nk_down = 0;
+};
+DecodeWs decode_layout(const Alg& up, const Alg& down, int64_t M) {
+  DecodeWs w;
+  for (int g = 0; g < up.q; ++g) {
+    w.nt_up += tiles_of(up.r(g), kDecodeTileN);
+    w.nk_up += tiles_of(up.s(g), kDecodeChunkK);
+  }
+  for (int g = 0; g < down.q; ++g) {
+    w.nt_down += tiles_of(down.r(g), kDecodeTileN);
+    w.nk_down += tiles_of(down.s(g), kDecodeChunkK);
+  }
+  const int64_t D = up.K(), F = up.N();
+  size_t cur = 0;
+  w.h = cur;
+  cur = align_up(cur + sizeof(float) * M * D);
+  w.xb = cur;
+  cur = align_up(cur + sizeof(uint16_t) * M * D);
+  w.H = cur;
+  cur = align_up(cur + sizeof(uint16_t) * M * F);
+  w.partial = cur;
+  const int64_t part = std::max<int64_t>(static_cast<int64_t>(w.nk_up) * F,
+                                         static_cast<int64_t>(w.nk_down) * D);
+  cur = align_up(cur + sizeof(float) * kDecodeMaxRows * part);
+  w.counters = cur;
+  cur = align_up(cur + sizeof(int32_t) * (w.nt_up + w.nt_down));
+  w.end = cur;
+  return w;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// ---- launch helpers ----------------------------------------------------------
+
+void fill_common(GemmParams& p, const Alg& a, int64_t M, int elem, const int32_t* perm,
+                 const int32_t* offsets) {
+  std::memset(&p, 0, sizeof(p));
+  p.q = a.q;
+  p.law = a.law;
+  p.M = static_cast<int32_t>(M);
+  p.K = static_cast<int32_t>(a.K());
+  p.N = static_cast<int32_t>(a.N());
+  p.elem = elem;
+  p.perm = perm;
+  p.offsets = offsets;
+  for (int g = 0; g <= a.q; ++g) {
+    p.S[g] = static_cast<int32_t>(a.S[g]);
+    p.R[g] = static_cast<int32_t>(a.R[g]);
+  }
+  p.nsplit = 1;
+}
+
+// column-tile prefix over groups of widths given by starts G
+void fill_tiles(int32_t* pfx, const int64_t* G, int q, int tile) {
+  pfx[0] = 0;
+  for (int g = 0; g < q; ++g) pfx[g + 1] = pfx[g] + tiles_of(G[g + 1] - G[g], tile);
+}
+
+int persistent_grid(int64_t upper_tiles) {
+  const int64_t cap = 2 * static_cast<int64_t>(cu_count());
+  int64_t g = std::min<int64_t>(std::max<int64_t>(upper_tiles, 1), cap);
+  g = (g + 7) / 8 * 8;
+  return static_cast<int>(g);
+}
+
+star_status hip_status(hipError_t e) { return e == hipSuccess ? STAR_OK : STAR_ERR_HIP; }
+
+star_status run_plan(const int32_t* row_type, int64_t M, int q, void* ws, const PlanWs& pw,
+                     hipStream_t stream) {
+  return hip_status(launch_type_plan(row_type, M, q, at<int32_t>(ws, pw.perm),
+                                     at<int32_t>(ws, pw.offsets), stream));
+}
+
+star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t* offsets,
+                    const void* X, const void* W, int elem, const float* bias, star_act act,
+                    void* Z, void* Y, star_dtype yt, hipStream_t stream) {
+  GemmParams p;
+  fill_common(p, a, M, elem, perm, offsets);
+  fill_tiles(p.NTp, a.R, a.q, kTileN);
+  p.A = X;
+  p.B = W;
+  p.bias = bias;
+  p.act = act;
+  p.Z = Z;
+  p.Y = Y;
+  p.ydtype = yt;
+  const int64_t upper = (M / kTileM + a.q + 1) * static_cast<int64_t>(p.NTp[a.q]);
+  return hip_status(launch_gemm(kModeFwd, p, persistent_grid(upper), stream));
+}
+
+star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a) {
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (M > 0 && !row_type) return STAR_ERR_ARG;
+  if (row_type && !aligned4(row_type)) return STAR_ERR_ALIGN;
+  return STAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* star_status_string(star_status s) {
+  switch (s) {
+    case STAR_OK: return "ok";
+    case STAR_ERR_ARG: return "invalid argument";
+    case STAR_ERR_SHAPE: return "invalid shape";
+    case STAR_ERR_DTYPE: return "unsupported dtype combination";
+    case STAR_ERR_ALIGN: return "misaligned pointer or width";
+    case STAR_ERR_WORKSPACE: return "workspace missing or too small";
+    case STAR_ERR_UNSUPPORTED: return "unsupported configuration";
+    case STAR_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_algebra* alg2,
+                            int64_t M) {
+  Alg a;
+  if (parse_alg(alg, a) != STAR_OK || M < 0) return 0;
+  switch (op) {
+    case STAR_OP_FWD:
+    case STAR_OP_BWD_DATA:
+    case STAR_OP_FFN_FWD:
+      return plan_layout(M, a.q).end;
+    case STAR_OP_BWD_WEIGHT:
+      return bwd_weight_layout(a, M).end;
+    case STAR_OP_DECODE: {
+      Alg d;
+      if (parse_alg(alg2, d) != STAR_OK) return 0;
+      return decode_layout(a, d, std::min<int64_t>(M, kDecodeMaxRows)).end;
+    }
+    default:
+      return 0;
+  }
+}
+
+star_status star_count_products(const star_algebra* alg, int64_t* per_type) {
+  Alg a;
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (!per_type) return STAR_ERR_ARG;
+  for (int i = 0; i < a.q; ++i) {
+    int64_t n = 0;
+    for (int j = 0; j < a.q; ++j)
+      for (int k = 0; k < a.q; ++k) n += (a.law == STAR_LAW_DENSE || k == i || k == j) ? 1 : 0;
+    per_type[i] = n;
+  }
+  return STAR_OK;
+}
+
+star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_type, int64_t* macs) {
+  Alg a;
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (!rows_per_type || !macs) return STAR_ERR_ARG;
+  int64_t total = 0;
+  for (int i = 0; i < a.q; ++i) {
+    int64_t row = 0;
+    for (int j = 0; j < a.q; ++j)
+      for (int k = 0; k < a.q; ++k)
+        if (a.law == STAR_LAW_DENSE || k == i || k == j) row += a.s(k) * a.r(j);
+    total += rows_per_type[i] * row;
+  }
+  *macs = total;
+  return STAR_OK;
+}
+
+star_status star_proj_fwd(const star_algebra* alg, int64_t M, const int32_t* row_type,
+                          const void* X, star_dtype xt, const void* W, star_dtype wt,
+                          const float* bias, star_act act, void* Z_out, void* Y, star_dtype yt,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  Alg a;
+  star_status st = check_common(alg, M, row_type, a);
+  if (st != STAR_OK) return st;
+  if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(yt) || xt != wt) return STAR_ERR_DTYPE;
+  if (!valid_act(act)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!X || !W || !Y) return STAR_ERR_ARG;
+  if (!aligned16(X) || !aligned16(W) || !aligned16(Y) || (Z_out && !aligned16(Z_out)) ||
+      (bias && !aligned4(bias)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, a.q);
+  if (!ws || ws_bytes < pw.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  st = run_plan(row_type, M, a.q, ws, pw, stream);
+  if (st != STAR_OK) return st;
+  return run_fwd(a, M, at<int32_t>(ws, pw.perm), at<int32_t>(ws, pw.offsets), X, W,
+                 xt == STAR_BF16 ? 1 : 0, bias, act, Z_out, Y, yt, stream);
+}
+
+star_status star_proj_bwd_data(const star_algebra* alg, int64_t M, const int32_t* row_type,
+                               const void* dY, star_dtype dyt, const void* W, star_dtype wt,
+                               const void* Z_prev, star_act act_prev, void* dX, star_dtype dxt,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+  Alg a;
+  star_status st = check_common(alg, M, row_type, a);
+  if (st != STAR_OK) return st;
+  if (!valid_dtype(dyt) || !valid_dtype(wt) || !valid_dtype(dxt) || dyt != wt)
+    return STAR_ERR_DTYPE;
+  if (!valid_act(act_prev)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!dY || !W || !dX) return STAR_ERR_ARG;
+  if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (Z_prev && !aligned16(Z_prev)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, a.q);
+  if (!ws || ws_bytes < pw.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  st = run_plan(row_type, M, a.q, ws, pw, stream);
+  if (st != STAR_OK) return st;
+  GemmParams p;
+  fill_common(p, a, M, dyt == STAR_BF16 ? 1 : 0, at<int32_t>(ws, pw.perm),
+              at<int32_t>(ws, pw.offsets));
+  fill_tiles(p.NTp, a.S, a.q, kTileN);
+  p.A = dY;
+  p.B = W;
+  p.Zprev = Z_prev;
+  p.act = Z_prev ? act_prev : STAR_ACT_NONE;
+  p.Y = dX;
+  p.ydtype = dxt;
+  const int64_t upper = (M / kTileM + a.q + 1) * static_cast<int64_t>(p.NTp[a.q]);
+  return hip_status(launch_gemm(kModeBwdData, p, persistent_grid(upper), stream));
+}
+
+star_status star_proj_bwd_weight(const star_algebra* alg, int64_t M, const int32_t* row_type,
+                                 const void* X, star_dtype xt, const void* dY, star_dtype dyt,
+                                 float* dW, float* dbias, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  Alg a;
+  star_status st = check_common(alg, M, row_type, a);
+  if (st != STAR_OK) return st;
+  if (!valid_dtype(xt) || !valid_dtype(dyt) || xt != dyt) return STAR_ERR_DTYPE;
+  if (!dW) return STAR_ERR_ARG;
+  if (M > 0 && (!X || !dY)) return STAR_ERR_ARG;
+  if ((X && !aligned16(X)) || (dY && !aligned16(dY)) || !aligned16(dW) ||
+      (dbias && !aligned4(dbias)))
+    return STAR_ERR_ALIGN;
+  const BwdWs bw = bwd_weight_layout(a, M);
+  if (!ws || ws_bytes < bw.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  // M = 0 still defines the output: an empty sum
+  if (M == 0) {
+    hipError_t e = launch_fill_zero(dW, a.K() * a.N(), stream);
+    if (e == hipSuccess && dbias) e = launch_fill_zero(dbias, a.N(), stream);
+    return hip_status(e);
+  }
+  st = run_plan(row_type, M, a.q, ws, bw.plan, stream);
+  if (st != STAR_OK) return st;
+  GemmParams p;
+  fill_common(p, a, M, xt == STAR_BF16 ? 1 : 0, at<int32_t>(ws, bw.plan.perm),
+              at<int32_t>(ws, bw.plan.offsets));
+  fill_tiles(p.NTp, a.R, a.q, kTileN);
+  fill_tiles(p.MTp, a.S, a.q, kTileM);
+  p.A = X;
+  p.B = dY;
+  p.dW = dW;
+  p.dbias = dbias;
+  p.nsplit = bw.nsplit;
+  if (bw.nsplit > 1) {
+    p.partial = at<float>(ws, bw.partial);
+    p.dbias_part = at<float>(ws, bw.dbias_part);
+  }
+  const int64_t upper = static_cast<int64_t>(p.MTp[a.q]) * p.NTp[a.q] * p.nsplit;
+  st = hip_status(launch_gemm(kModeBwdWeight, p, persistent_grid(upper), stream));
+  if (st != STAR_OK || bw.nsplit == 1) return st;
+  return hip_status(launch_split_reduce(p, stream));
+}
+
+star_status star_ffn_fwd(const star_algebra* up, const star_algebra* down, int64_t M,
+                         const int32_t* row_type, const void* X, const void* W_up,
+                         const float* b_up, const void* W_down, const float* b_down,
+                         star_act act, void* Z_up, void* H, void* Y, star_dtype dt,
+                         star_dtype yt, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Alg u, d;
+  star_status st = check_common(up, M, row_type, u);
+  if (st != STAR_OK) return st;
+  st = parse_alg(down, d);
+  if (st != STAR_OK) return st;
+  if (d.q != u.q) return STAR_ERR_SHAPE;
+  for (int g = 0; g < u.q; ++g)
+    if (d.s(g) != u.r(g)) return STAR_ERR_SHAPE;
+  if (!valid_dtype(dt) || !valid_dtype(yt)) return STAR_ERR_DTYPE;
+  if (!valid_act(act)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!X || !W_up || !W_down || !H || !Y) return STAR_ERR_ARG;
+  if (!aligned16(X) || !aligned16(W_up) || !aligned16(W_down) || !aligned16(H) ||
+      !aligned16(Y) || (Z_up && !aligned16(Z_up)) || (b_up && !aligned4(b_up)) ||
+      (b_down && !aligned4(b_down)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, u.q);
+  if (!ws || ws_bytes < pw.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  st = run_plan(row_type, M, u.q, ws, pw, stream);
+  if (st != STAR_OK) return st;
+  const int elem = dt == STAR_BF16 ? 1 : 0;
+  const int32_t* perm = at<int32_t>(ws, pw.perm);
+  const int32_t* offs = at<int32_t>(ws, pw.offsets);
+  st = run_fwd(u, M, perm, offs, X, W_up, elem, b_up, act, Z_up, H, dt, stream);
+  if (st != STAR_OK) return st;
+  return run_fwd(d, M, perm, offs, H, W_down, elem, b_down, STAR_ACT_NONE, nullptr, Y, yt, stream);
+}
+
+star_status star_decode(const star_algebra* up, const star_algebra* down, int32_t n_layers,
+                        int64_t M, const int32_t* row_type, const void* X,
+                        const void* const* W_up, const float* const* b_up,
+                        const void* const* W_down, const float* const* b_down, star_act act,
+                        int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  Alg u, d;
+  star_status st = check_common(up, M, row_type, u);
+  if (st != STAR_OK) return st;
+  st = parse_alg(down, d);
+  if (st != STAR_OK) return st;
+  if (d.K() != u.N() || d.N() != u.K()) return STAR_ERR_SHAPE;
+  if (M > kDecodeMaxRows) return STAR_ERR_UNSUPPORTED;
+  if (n_layers < 1) return STAR_ERR_ARG;
+  if (!valid_dtype(yt)) return STAR_ERR_DTYPE;
+  if (!valid_act(act)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!X || !W_up || !W_down || !Y) return STAR_ERR_ARG;
+  if (!aligned16(X) || !aligned16(Y)) return STAR_ERR_ALIGN;
+  for (int l = 0; l < n_layers; ++l) {
+    if (!W_up[l] || !W_down[l]) return STAR_ERR_ARG;
+    if (!aligned16(W_up[l]) || !aligned16(W_down[l])) return STAR_ERR_ALIGN;
+    if ((b_up && b_up[l] && !aligned4(b_up[l])) || (b_down && b_down[l] && !aligned4(b_down[l])))
+      return STAR_ERR_ALIGN;
+  }
+  const DecodeWs dw = decode_layout(u, d, M);
+  if (!ws || ws_bytes < dw.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+
+  float* h = at<float>(ws, dw.h);
+  uint16_t* xb = at<uint16_t>(ws, dw.xb);
+  uint16_t* Hb = at<uint16_t>(ws, dw.H);
+  float* part = at<float>(ws, dw.partial);
+  int32_t* cnt = at<int32_t>(ws, dw.counters);
+  st = hip_status(launch_decode_init(static_cast<const uint16_t*>(X), M * u.K(), h, xb, cnt,
+                                     dw.nt_up + dw.nt_down, stream));
+  if (st != STAR_OK) return st;
+
+  auto fill = [&](DecodePhase& p, const Alg& a) {
+    std::memset(&p, 0, sizeof(p));
+    p.q = a.q;
+    p.law = a.law;
+    p.M = static_cast<int32_t>(M);
+    p.K = static_cast<int32_t>(a.K());
+    p.N = static_cast<int32_t>(a.N());
+    for (int g = 0; g <= a.q; ++g) {
+      p.S[g] = static_cast<int32_t>(a.S[g]);
+      p.R[g] = static_cast<int32_t>(a.R[g]);
+    }
+    fill_tiles(p.NTp, a.R, a.q, kDecodeTileN);
+    fill_tiles(p.KCp, a.S, a.q, kDecodeChunkK);
+    p.types = row_type;
+    p.partial = part;
+    p.act = act;
+    p.residual = residual;
+  };
+  DecodePhase pu, pd;
+  fill(pu, u);
+  fill(pd, d);
+  pu.mode = 0;
+  pu.A = xb;
+  pu.out_bf16 = Hb;
+  pu.counters = cnt;
+  pd.mode = 1;
+  pd.A = Hb;
+  pd.h = h;
+  pd.counters = cnt + dw.nt_up;
+  pd.ydtype = yt;
+  for (int l = 0; l < n_layers; ++l) {
+    pu.W = static_cast<const uint16_t*>(W_up[l]);
+    pu.bias = b_up ? b_up[l] : nullptr;
+    st = hip_status(launch_decode_phase(pu, stream));
+    if (st != STAR_OK) return st;
+    pd.W = static_cast<const uint16_t*>(W_down[l]);
+    pd.bias = b_down ? b_down[l] : nullptr;
+    const bool last = (l == n_layers - 1);
+    pd.out_bf16 = last ? nullptr : xb;
+    pd.Y = last ? Y : nullptr;
+    st = hip_status(launch_decode_phase(pd, stream));
+    if (st != STAR_OK) return st;
+  }
+  return STAR_OK;
+}
+
+star_status star_validate_types(int64_t M, const int32_t* row_type, int32_t q, int64_t* n_bad,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!n_bad || q < 1) return STAR_ERR_ARG;
+  if (M < 0) return STAR_ERR_SHAPE;
+  *n_bad = 0;
+  if (M == 0) return STAR_OK;
+  if (!row_type) return STAR_ERR_ARG;
+  if (!ws || ws_bytes < 16) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  auto* cnt = static_cast<unsigned long long*>(ws);
+  hipError_t e = hipMemsetAsync(cnt, 0, sizeof(unsigned long long), stream);
+  if (e == hipSuccess) e = launch_count_bad_types(row_type, M, q, cnt, stream);
+  unsigned long long host = 0;
+  if (e == hipSuccess) e = hipMemcpyAsync(&host, cnt, sizeof(host), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return STAR_ERR_HIP;
+  *n_bad = static_cast<int64_t>(host);
+  return STAR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+// Internal host-side interface between the C ABI and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace starq {
+
+constexpr int kMaxQGroups = 64;
+
+enum GemmMode : int { kModeFwd = 0, kModeBwdData = 1, kModeBwdWeight = 2 };
+
+// Arguments of one grouped typed GEMM launch (all three modes).
+//
+//   FWD        C[rows of type i, output group j] = sum_seg X[rows, seg] W[seg, j]
+//   BWD_DATA   C[rows of type i, input group g]  = sum_seg dY[rows, seg] W[g, seg]^T
+//   BWD_WEIGHT C[input group g, output group j]  = sum_rows X[rows, g]^T dY[rows, j]
+//
+// Group starts S (input side of W, K), R (output side of W, N) and the
+// column-tile prefix NTp over the column groups of C are host-computed.
+struct GemmParams {
+  int32_t q;
+  int32_t law;  // 0 star, 1 dense
+  int32_t M;
+  int32_t K;
+  int32_t N;
+  int32_t elem;  // 0 f32, 1 bf16 (operands)
+  const int32_t* perm;
+  const int32_t* offsets;
+  int32_t S[kMaxQGroups + 1];
+  int32_t R[kMaxQGroups + 1];
+  int32_t NTp[kMaxQGroups + 1];  // column tiles of C per column group, prefix
+  int32_t MTp[kMaxQGroups + 1];  // BWD_WEIGHT: row tiles of C per input group, prefix
+  const void* A;
+  const void* B;
+  // FWD epilogue
+  const float* bias;
+  int32_t act;
+  void* Z;
+  void* Y;  // FWD: Y; BWD_DATA: dX
+  int32_t ydtype;
+  // BWD_DATA epilogue
+  const void* Zprev;
+  // BWD_WEIGHT outputs
+  float* dW;
+  float* dbias;
+  float* partial;     // [nsplit][K][N] when nsplit > 1
+  float* dbias_part;  // [nsplit][N] when nsplit > 1
+  int32_t nsplit;
+};
+
+hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* perm,
+                            int32_t* offsets, hipStream_t stream);
+hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
+                                  unsigned long long* n_bad, hipStream_t stream);
+
+// Grid size (workgroups) of the persistent GEMM for a given mode.
+hipError_t launch_gemm(int mode, const GemmParams& p, int grid, hipStream_t stream);
+hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
+// Zero-fills n floats with a kernel (safe to record in a HIP graph).
+hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream);
+
+// Tile sizes of the GEMM (rows and columns of C per workgroup).
+constexpr int kTileM = 128;
+constexpr int kTileN = 128;
+constexpr int kGemmThreads = 256;
+
+// ---- decode ----------------------------------------------------------------
+
+constexpr int kDecodeMaxRows = 64;
+constexpr int kDecodeTileN = 64;
+constexpr int kDecodeChunkK = 128;
+
+struct DecodePhase {
+  int32_t q;
+  int32_t law;
+  int32_t M;
+  int32_t K;  // input width of this projection
+  int32_t N;  // output width
+  int32_t S[kMaxQGroups + 1];
+  int32_t R[kMaxQGroups + 1];
+  int32_t NTp[kMaxQGroups + 1];  // column tiles per output group, prefix
+  int32_t KCp[kMaxQGroups + 1];  // K chunks per input group, prefix
+  const int32_t* types;
+  const uint16_t* A;   // bf16 [M][K]
+  const uint16_t* W;   // bf16 [K][N]
+  const float* bias;   // [N] or null
+  float* partial;      // [n_kchunks][kDecodeMaxRows][N]
+  int32_t* counters;   // [n_col_tiles]
+  int32_t mode;        // 0: up (H = act(z) -> out_bf16); 1: down (h += z)
+  int32_t act;
+  int32_t residual;
+  uint16_t* out_bf16;  // up: H [M][N]; down: bf16(h) for the next layer (or null)
+  float* h;            // down: running state [M][N] (fp32)
+  void* Y;             // down, last layer: final output
+  int32_t ydtype;
+};
+
+hipError_t launch_decode_init(const uint16_t* X, int64_t n, float* h, uint16_t* xb,
+                              int32_t* counters, int n_counters, hipStream_t stream);
+hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
+
+}  // namespace starq

@@ -1,0 +1,131 @@
+// Type plan: the per-type row index sets I_i of Alg. 1 as one stable
+// permutation of the rows grouped by type, plus per-type offsets.
+//
+// One workgroup of 1024 threads (16 wavefronts).  The rows are cut into 16
+// contiguous chunks, one per wavefront; a wavefront walks its chunk in
+// windows of 64 rows.  Lanes holding the same type find each other with
+// ballots over the type bits (a match-any), so each window costs O(log q)
+// ballots and no atomics.  Pass 1 counts rows per (wavefront, type); the
+// counts are scanned into exclusive bases; pass 2 re-walks the chunks and
+// writes each row at base + rank-within-window, which keeps the order of
+// rows of one type (stable).  Rows with a type outside [0, q) go to a
+// trailing bucket after all valid rows, so perm stays a permutation and no
+// tile ever reads them.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace starq {
+
+namespace {
+
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanWaves = kPlanThreads / 64;
+
+__device__ __forceinline__ uint64_t match_type(int t, bool valid, int nbits) {
+  uint64_t m = __ballot(valid);
+  if (!valid) m = ~m;
+  for (int bit = 0; bit < nbits; ++bit) {
+    const bool set = (t >> bit) & 1;
+    const uint64_t b = __ballot(set);
+    m &= set ? b : ~b;
+  }
+  return m;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* __restrict__ types,
+                                                                 int32_t M, int q, int nbits,
+                                                                 int32_t* __restrict__ perm,
+                                                                 int32_t* __restrict__ offsets) {
+  // counts[w][t], t = q is the out-of-range bucket
+  __shared__ int32_t counts[kPlanWaves][kMaxQ + 1];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < kPlanWaves * (kMaxQ + 1); i += kPlanThreads)
+    (&counts[0][0])[i] = 0;
+  __syncthreads();
+
+  const int32_t chunk = ((M + kPlanWaves - 1) / kPlanWaves + 63) & ~63;
+  const int32_t lo = wave * chunk;
+  const int32_t hi = min(M, lo + chunk);
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+  // pass 1: counts
+  for (int32_t base = lo; base < hi; base += 64) {
+    const int32_t row = base + lane;
+    const bool in = row < hi;
+    int t = in ? types[row] : 0;
+    const bool valid_type = t >= 0 && t < q;
+    if (!valid_type) t = q;
+    const uint64_t active = __ballot(in);
+    const uint64_t m = match_type(t, t < q, nbits) & active;
+    if (in && (m & lt_mask) == 0) counts[wave][t] += __popcll(m);
+  }
+  __syncthreads();
+
+  // exclusive scan: offsets over types, then bases per (wave, type)
+  if (threadIdx.x == 0) {
+    int32_t run = 0;
+    for (int t = 0; t <= q; ++t) {
+      if (t < q) offsets[t] = run;
+      if (t == q) offsets[q] = run;  // end of valid rows
+      for (int w = 0; w < kPlanWaves; ++w) {
+        const int32_t c = counts[w][t];
+        counts[w][t] = run;
+        run += c;
+      }
+    }
+  }
+  __syncthreads();
+
+  // pass 2: stable scatter
+  for (int32_t base = lo; base < hi; base += 64) {
+    const int32_t row = base + lane;
+    const bool in = row < hi;
+    int t = in ? types[row] : 0;
+    if (!(t >= 0 && t < q)) t = q;
+    const uint64_t active = __ballot(in);
+    const uint64_t m = match_type(t, t < q, nbits) & active;
+    if (in) {
+      const int32_t pos = counts[wave][t] + __popcll(m & lt_mask);
+      perm[pos] = row;
+    }
+    // all lanes have read counts[wave][*] before the leaders advance them
+    __builtin_amdgcn_wave_barrier();
+    if (in && (m & lt_mask) == 0) counts[wave][t] += __popcll(m);
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+__global__ void count_bad_types_kernel(const int32_t* __restrict__ types, int64_t M, int q,
+                                       unsigned long long* __restrict__ n_bad) {
+  unsigned long long local = 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < M;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int t = types[i];
+    local += (t < 0 || t >= q) ? 1ull : 0ull;
+  }
+  for (int off = 32; off > 0; off >>= 1) local += __shfl_down(local, off);
+  if ((threadIdx.x & 63) == 0 && local) atomicAdd(n_bad, local);
+}
+
+}  // namespace
+
+hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* perm,
+                            int32_t* offsets, hipStream_t stream) {
+  int nbits = 0;
+  while ((1 << nbits) < q + 1) ++nbits;
+  hipLaunchKernelGGL(type_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, types,
+                     static_cast<int32_t>(M), q, nbits, perm, offsets);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
+                                  unsigned long long* n_bad, hipStream_t stream) {
+  const int64_t blocks64 = (M + 255) / 256;
+  const int blocks = static_cast<int>(blocks64 < 1024 ? (blocks64 > 0 ? blocks64 : 1) : 1024);
+  hipLaunchKernelGGL(count_bad_types_kernel, dim3(blocks), dim3(256), 0, stream, types, M, q,
+                     n_bad);
+  return hipGetLastError();
+}
+
+}  // namespace starq

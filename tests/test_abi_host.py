@@ -1,0 +1,118 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry point
+the header declares, and rejects bad arguments before launching anything.
+No test here launches a kernel, so all run without a GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "star_proj.h")
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2609_32814_amd as P
+    return P
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(star_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(P):
+    names = declared_functions()
+    assert {"star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
+            "star_decode"} <= set(names)
+    lib = ctypes.CDLL(P.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_names_match_abi(P):
+    for n in declared_functions():
+        assert hasattr(P, n), n
+
+
+def test_count_products(P):
+    for q in (1, 2, 3, 8, 16, 64):
+        a = P.Algebra.equal(q, 8 * q, 8 * q)
+        assert P.star_count_products(a) == [2 * q - 1] * q
+        assert P.star_count_products(a.with_law("dense")) == [q * q] * q
+
+
+def test_count_macs_closed_form(P):
+    """eq. rectangular-batch-cost: M D_diag + sum_i M_i s_i (N - r_i)."""
+    s, r = [8, 40, 16], [24, 8, 56]
+    a = P.Algebra(3, s, r)
+    rows = [5, 0, 11]
+    D = sum(x * y for x, y in zip(s, r))
+    N = sum(r)
+    expect = sum(rows) * D + sum(m * si * (N - ri) for m, si, ri in zip(rows, s, r))
+    assert P.star_count_macs(a, rows) == expect
+    assert P.star_count_macs(a.with_law("dense"), rows) == sum(rows) * sum(s) * N
+
+
+def test_workspace_sizes(P):
+    a = P.Algebra.equal(2, 768, 3072)
+    d = P.Algebra.equal(2, 3072, 768)
+    fwd = P.star_workspace_bytes("fwd", a, None, 8192)
+    assert fwd >= 4 * 8192 + 4 * 3
+    bw = P.star_workspace_bytes("bwd_weight", a, None, 16384)
+    assert bw >= fwd
+    dec = P.star_workspace_bytes("decode", a, d, 64)
+    assert dec >= 64 * 768 * 4 + 64 * 768 * 2 + 64 * 3072 * 2
+    assert P.star_workspace_bytes("fwd", P.Algebra(2, [7, 9], [8, 8]), None, 10) == 0
+
+
+def _raw_fwd(P, alg_c, M, xt=1, wt=1, yt=1, X=16, W=16, Y=16, ws=16, ws_bytes=1 << 20,
+             rt=16, act=0):
+    # fake, aligned, never-dereferenced pointers: these calls must fail validation
+    V = ctypes.c_void_p
+    return P.binding.LIB.star_proj_fwd(alg_c, M, V(rt) if rt else None, V(X) if X else None, xt,
+                                       V(W) if W else None, wt, None, act, None,
+                                       V(Y) if Y else None, yt, V(ws) if ws else None, ws_bytes,
+                                       None)
+
+
+def test_argument_errors_before_launch(P):
+    import paper_2609_32814_amd.binding as B
+    good = P.Algebra.equal(2, 64, 64)
+    assert _raw_fwd(P, None, 4) == 1                                   # null algebra
+    assert _raw_fwd(P, P.Algebra(2, [12, 52], [32, 32]).ref, 4) == 4   # width not multiple of 8
+    assert _raw_fwd(P, good.ref, 4, xt=0, wt=1) == 3                   # mixed operand dtypes
+    assert _raw_fwd(P, good.ref, 4, yt=5) == 3                         # bad dtype
+    assert _raw_fwd(P, good.ref, 4, act=9) == 1                        # bad activation
+    assert _raw_fwd(P, good.ref, 4, X=0) == 1                          # null operand
+    assert _raw_fwd(P, good.ref, 4, X=18) == 4                         # misaligned operand
+    assert _raw_fwd(P, good.ref, 4, ws_bytes=8) == 5                   # workspace too small
+    assert _raw_fwd(P, good.ref, 4, ws=0) == 5                         # no workspace
+    assert _raw_fwd(P, good.ref, -1) == 2                              # negative M
+    assert _raw_fwd(P, good.ref, 0, X=0, W=0, Y=0, ws=0, rt=0) == 0    # M = 0: no-op
+    big = B.Algebra(65, [8] * 65, [8] * 65)
+    assert _raw_fwd(P, big.ref, 4) == 1                                # q above STAR_MAX_Q
+    assert P.star_status_string(5).startswith("workspace")
+
+
+def test_decode_rejects_too_many_rows(P):
+    V = ctypes.c_void_p
+    up, dn = P.Algebra.equal(2, 64, 128), P.Algebra.equal(2, 128, 64)
+    arr = (V * 1)(V(16))
+    st = P.binding.LIB.star_decode(up.ref, dn.ref, 1, 65, V(16), V(16), arr, None, arr, None, 1,
+                                   1, V(16), 1, V(16), 1 << 30, None)
+    assert st == 6
+    st = P.binding.LIB.star_decode(up.ref, P.Algebra.equal(2, 128, 32).ref, 1, 4, V(16), V(16),
+                                   arr, None, arr, None, 1, 1, V(16), 1, V(16), 1 << 30, None)
+    assert st == 2
+
+
+def test_ffn_rejects_mismatched_widths(P):
+    V = ctypes.c_void_p
+    up, dn = P.Algebra(2, [32, 32], [64, 64]), P.Algebra(2, [56, 72], [32, 32])
+    st = P.binding.LIB.star_ffn_fwd(up.ref, dn.ref, 4, V(16), V(16), V(16), None, V(16), None, 1,
+                                    None, V(16), V(16), 1, 1, V(16), 1 << 20, None)
+    assert st == 2

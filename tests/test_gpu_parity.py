@@ -1,0 +1,378 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 CPU oracle.
+
+Every case draws its inputs from ``synth`` with a fixed seed, runs the same
+values through both sides and compares element by element with the relative
+Frobenius bar of the operand precision (``helpers.TOL_*``).  Small cases span
+several 128 x 128 tiles with ragged tails; the full-size cases use the shapes
+and launch configuration the benchmark times and compare sampled rows (the
+projection is row-local) or sampled weight-gradient entries.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import TOL_BF16, TOL_F32, f32_dev, rel_fro, to_dev, to_host, types_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    assert torch.cuda.is_available(), "GPU parity tests need a GPU"
+    import paper_2609_32814_amd as P
+    return P
+
+
+def algs(P, q, s, r, law="star"):
+    return P.Algebra(q, s, r, law), oracle.Alg(q, tuple(s), tuple(r), law)
+
+
+def bar(dtype):
+    return TOL_F32 if dtype == "f32" else TOL_BF16
+
+
+# ---- forward -------------------------------------------------------------------
+
+def test_cfg1_fp32_q2(P):
+    """64 x 128 rows of two 64-wide groups, W 128 x 128, N(0,1), t = b mod 2."""
+    ga, oa = algs(P, 2, [64, 64], [64, 64])
+    X = synth.gaussian(1, 0, (64, 128), 1.0, "f32")
+    W = synth.gaussian(1, 1, (128, 128), 1.0, "f32")
+    t = synth.cyclic_types(64, 2)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W))
+    ref, _, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact)
+    assert rel_fro(to_host(Y), ref) <= TOL_F32
+    # against the masked dense product too (independent formulation)
+    gk = np.repeat([0, 1], 64)
+    for i in (0, 1):
+        rows = t == i
+        mask = (gk[:, None] == i) | (gk[:, None] == gk[None, :])
+        np.testing.assert_allclose(to_host(Y)[rows], X.exact[rows] @ (W.exact * mask),
+                                   rtol=0, atol=1e-4)
+
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("dtype,out", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
+@pytest.mark.parametrize("q,s,r,M,types", [
+    (2, [64, 64], [64, 64], 64, "cyclic"),
+    (2, [136, 120], [200, 56], 333, "cyclic"),
+    (3, [64, 24, 104], [96, 160, 40], 517, "random"),
+    (5, [16, 32, 8, 48, 24], [40, 8, 72, 16, 32], 700, "random"),
+    (4, [32] * 4, [48] * 4, 300, "missing"),       # one type class is empty
+    (8, [16] * 8, [32] * 8, 258, "offset"),
+    (1, [72], [136], 130, "cyclic"),
+])
+def test_fwd_parity(P, law, dtype, out, q, s, r, M, types):
+    import torch
+    ga, oa = algs(P, q, s, r, law)
+    seed = 100 + q
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, dtype)
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, dtype)
+    bias = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
+    rng = np.random.default_rng([seed, 3])
+    if types == "cyclic":
+        t = synth.cyclic_types(M, q)
+    elif types == "offset":
+        t = synth.cyclic_types(M, q, offset=3)
+    else:
+        t = rng.integers(0, q, M).astype(np.int32)
+        if types == "missing":
+            t[t == 1] = 2
+    odt = torch.float32 if out == "f32" else torch.bfloat16
+    Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
+                           Z_out=True, out_dtype=odt)
+    refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, bias.exact, "gelu", want_z=True)
+    tol = TOL_F32 if (dtype == "f32" and out == "f32") else TOL_BF16
+    assert rel_fro(to_host(Z), refZ) <= tol
+    assert rel_fro(to_host(Y), refY) <= tol
+
+
+def test_fwd_one_row_of_each_type(P):
+    ga, oa = algs(P, 4, [24, 40, 16, 48], [32, 8, 56, 24])
+    for ty in range(4):
+        t = np.array([ty], np.int32)
+        X = synth.gaussian(7, ty, (1, oa.K), 1.0, "f32")
+        W = synth.gaussian(7, 10, (oa.K, oa.N), 1.0, "f32")
+        Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W))
+        ref, _, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact)
+        assert rel_fro(to_host(Y), ref) <= TOL_F32
+
+
+def test_fwd_max_q(P):
+    q = 64
+    ga, oa = algs(P, q, [8] * q, [16] * q)
+    M = 1000
+    X = synth.gaussian(8, 0, (M, oa.K), 1.0, "bf16")
+    W = synth.gaussian(8, 1, (oa.K, oa.N), 0.05, "bf16")
+    t = synth.cyclic_types(M, q)
+    import torch
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), out_dtype=torch.float32)
+    ref, _, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact)
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
+def test_fwd_m0_is_noop(P):
+    import torch
+    ga, _ = algs(P, 2, [64, 64], [64, 64])
+    Y = torch.full((0, 128), 7.0, device="cuda")
+    X = torch.empty((0, 128), device="cuda")
+    W = torch.zeros((128, 128), device="cuda")
+    P.star_proj_fwd(ga, torch.empty(0, dtype=torch.int32, device="cuda"), X, W, Y=Y)
+    torch.cuda.synchronize()
+
+
+def test_out_of_range_types_left_out(P):
+    import torch
+    ga, oa = algs(P, 3, [32, 32, 64], [64, 32, 32])
+    M = 200
+    X = synth.gaussian(9, 0, (M, oa.K), 1.0, "f32")
+    W = synth.gaussian(9, 1, (oa.K, oa.N), 1.0, "f32")
+    t = synth.cyclic_types(M, 3)
+    bad = np.array([5, 77, 150])
+    t_bad = t.copy()
+    t_bad[bad] = [3, -1, 9]
+    td = types_dev(t_bad)
+    assert P.star_validate_types(td, 3) == 3
+    assert P.star_validate_types(types_dev(t), 3) == 0
+    Y = torch.full((M, oa.N), 12345.0, device="cuda")
+    P.star_proj_fwd(ga, td, to_dev(X), to_dev(W), Y=Y)
+    got = to_host(Y)
+    assert np.all(got[bad] == 12345.0)
+    good = np.setdiff1d(np.arange(M), bad)
+    ref, _, _, _ = oracle.proj_fwd(oa, t[good], X.exact[good], W.exact)
+    assert rel_fro(got[good], ref) <= TOL_F32
+
+
+# ---- backward -------------------------------------------------------------------
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("q,s,r,M", [
+    (2, [64, 64], [96, 160], 333),
+    (3, [40, 64, 24], [48, 16, 136], 450),
+    (4, [32] * 4, [64] * 4, 257),
+])
+@pytest.mark.parametrize("fused", [False, True])
+def test_bwd_data_parity(P, law, dtype, q, s, r, M, fused):
+    ga, oa = algs(P, q, s, r, law)
+    seed = 200 + q
+    dY = synth.gaussian(seed, 0, (M, oa.N), 1.0, dtype)
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, dtype)
+    Zp = synth.gaussian(seed, 2, (M, oa.K), 1.0, dtype) if fused else None
+    t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+    import torch
+    dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W),
+                              Z_prev=to_dev(Zp) if fused else None,
+                              act_prev="gelu" if fused else "none", out_dtype=torch.float32)
+    ref = oracle.proj_bwd_data(oa, t, dY.exact, W.exact, Zprev=Zp.exact if fused else None,
+                               act_prev="gelu" if fused else "none")
+    assert rel_fro(to_host(dX), ref) <= bar(dtype)
+
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("q,s,r,M", [
+    (2, [64, 64], [96, 160], 333),      # one split
+    (3, [40, 64, 24], [48, 16, 136], 4100),  # several splits, ragged
+    (4, [32] * 4, [64] * 4, 2049),
+    (2, [128, 128], [128, 128], 0),     # empty batch: zero gradients
+])
+def test_bwd_weight_parity(P, law, dtype, q, s, r, M):
+    ga, oa = algs(P, q, s, r, law)
+    seed = 300 + q
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, dtype)
+    dY = synth.gaussian(seed, 1, (M, oa.N), 1.0, dtype)
+    t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+    dW, db = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    rW, rb = oracle.proj_bwd_weight(oa, t, X.exact, dY.exact)
+    if M == 0:
+        assert np.all(to_host(dW) == 0) and np.all(to_host(db) == 0)
+        return
+    assert rel_fro(to_host(dW), rW) <= bar(dtype)
+    assert rel_fro(to_host(db), rb) <= bar(dtype)
+    # bitwise reproducible
+    dW2, db2 = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    assert np.array_equal(to_host(dW2), to_host(dW)) and np.array_equal(to_host(db2), to_host(db))
+
+
+def test_bwd_weight_absent_type_gives_zero_blocks(P):
+    ga, oa = algs(P, 3, [32, 48, 40], [56, 24, 64])
+    M = 600
+    X = synth.gaussian(11, 0, (M, oa.K), 1.0, "bf16")
+    dY = synth.gaussian(11, 1, (M, oa.N), 1.0, "bf16")
+    t = synth.cyclic_types(M, 3)
+    t[t == 1] = 0
+    dW, _ = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    g = to_host(dW)
+    # row block of group 1 (rows 32..80), off-diagonal columns: exactly zero
+    assert np.all(g[32:80, :56] == 0) and np.all(g[32:80, 80:] == 0)
+    rW, _ = oracle.proj_bwd_weight(oa, t, X.exact, dY.exact)
+    assert rel_fro(g, rW) <= TOL_BF16
+
+
+# ---- FFN forward + backward ----------------------------------------------------------
+
+@pytest.mark.parametrize("q,D,F,M", [(2, 256, 1024, 1000), (4, 128, 512, 777)])
+def test_ffn_train_step_parity(P, q, D, F, M):
+    import torch
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q)
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q)
+    seed = 400 + q
+    X = synth.gaussian(seed, 0, (M, D), 1.0, "bf16")
+    Wu = synth.gaussian(seed, 1, (D, F), 0.02, "bf16")
+    Wd = synth.gaussian(seed, 2, (F, D), 0.02, "bf16")
+    bu = synth.gaussian(seed, 3, (F,), 0.02, "f32")
+    bd = synth.gaussian(seed, 4, (D,), 0.02, "f32")
+    dY = synth.gaussian(seed, 5, (M, D), 1.0, "bf16")
+    t = synth.sequence_types(M, q, 256)
+    td = types_dev(t)
+    Z, H, Y = P.star_ffn_fwd(up_g, dn_g, td, to_dev(X), to_dev(Wu), f32_dev(bu.exact), to_dev(Wd),
+                             f32_dev(bd.exact), "gelu", out_dtype=torch.float32)
+    rZ, rH, rY = oracle.ffn_fwd(up_o, dn_o, t, X.exact, Wu.exact, bu.exact, Wd.exact, bd.exact)
+    assert rel_fro(to_host(Z), rZ) <= TOL_BF16
+    assert rel_fro(to_host(H), rH) <= TOL_BF16
+    assert rel_fro(to_host(Y), rY) <= TOL_BF16
+    g = P.star_ffn_bwd(up_g, dn_g, td, to_dev(X), Z, H, to_dev(Wu), to_dev(Wd), to_dev(dY), "gelu")
+    # the oracle's backward consumes its own forward's stored tensors
+    ref = oracle.ffn_bwd(up_o, dn_o, t, X.exact, rZ, rH, Wu.exact, Wd.exact, dY.exact)
+    for k in ("dZ", "dX", "dW_up", "db_up", "dW_down", "db_down"):
+        assert rel_fro(to_host(g[k]), ref[k]) <= TOL_BF16, k
+
+
+# ---- decode -------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M", [1, 8, 32, 64])
+@pytest.mark.parametrize("D,F,L", [(256, 1024, 3), (768, 3072, 12)])
+def test_decode_parity(P, M, D, F, L):
+    import torch
+    up_g, up_o = algs(P, 2, [D // 2] * 2, [F // 2] * 2)
+    dn_g, dn_o = algs(P, 2, [F // 2] * 2, [D // 2] * 2)
+    seed = 500 + L
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.02, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.02, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 70 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 100 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = (synth.decode_positions(seed, M) % 2).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                      [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                      [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+    # the same step again gives bitwise the same result (counters reset)
+    Y2 = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                       [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                       [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
+    assert torch.equal(Y, Y2)
+
+
+def test_decode_one_type_only_skips_blocks(P):
+    """M = 1 of type 0: only the diagonal blocks and row block 0 are read;
+    the result still matches the oracle (skipped chunks contribute nothing)."""
+    import torch
+    D, F = 256, 512
+    up_g, up_o = algs(P, 2, [D // 2] * 2, [F // 2] * 2)
+    dn_g, dn_o = algs(P, 2, [F // 2] * 2, [D // 2] * 2)
+    Wu = synth.gaussian(600, 1, (D, F), 0.05, "bf16")
+    Wd = synth.gaussian(600, 2, (F, D), 0.05, "bf16")
+    X = synth.gaussian(600, 3, (1, D), 1.0, "bf16")
+    for ty in (0, 1):
+        t = np.array([ty], np.int32)
+        Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(Wu)], None, [to_dev(Wd)],
+                          None, "gelu", False, out_dtype=torch.float32)
+        ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [Wu.exact], [np.zeros(F)], [Wd.exact],
+                                  [np.zeros(D)], residual=False)
+        assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
+# ---- full-size workloads (sampled) ---------------------------------------------------
+
+def _sample_rows(M, n, seed):
+    rng = np.random.default_rng([seed, 999])
+    rows = np.unique(np.concatenate([[0, 1, M - 2, M - 1], rng.choice(M, n, replace=False)]))
+    return rows
+
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+def test_cfg2_full_size_sampled(P, law):
+    """M = 8192 (8 x 1024), 768 -> 3072 in blocks 384 x 1536, bias + GELU,
+    bf16 in / fp32 accumulate / bf16 out, t = position-in-sequence mod 2."""
+    M, K, N = 8192, 768, 3072
+    ga, oa = algs(P, 2, [384, 384], [1536, 1536], law)
+    X = synth.gaussian(2, 0, (M, K), 1.0, "bf16")
+    W = synth.gaussian(2, 1, (K, N), 0.02, "bf16")
+    b = synth.gaussian(2, 2, (N,), 0.02, "f32")
+    t = synth.sequence_types(M, 2, 1024)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(b.exact), "gelu")
+    rows = _sample_rows(M, 300, 2)
+    ref, _, _, _ = oracle.proj_fwd(oa, t[rows], X.exact[rows], W.exact, b.exact, "gelu")
+    assert rel_fro(to_host(Y[rows]), ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("q", [2, 4, 8, 16])
+def test_cfg4_qsweep_full_size_sampled(P, q):
+    """Square star_q projection, block 256, d = 256 q, M = 16384, t = b mod q."""
+    import torch
+    M, d = 16384, 256 * q
+    ga, oa = algs(P, q, [256] * q, [256] * q)
+    X = synth.gaussian(4, q, (M, d), 1.0, "bf16")
+    W = synth.gaussian(4, 100 + q, (d, d), (1.0 / d) ** 0.5, "bf16")
+    t = synth.cyclic_types(M, q)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W))
+    rows = _sample_rows(M, 256, 4 + q)
+    ref, _, macs, ppt = oracle.proj_fwd(oa, t[rows], X.exact[rows], W.exact)
+    assert rel_fro(to_host(Y[rows]), ref) <= TOL_BF16
+    # retained block products: 2q - 1 per type, vs q^2 for the dense law
+    assert P.star_count_products(ga) == [2 * q - 1] * q == list(ppt)
+    assert P.star_count_products(ga.with_law("dense")) == [q * q] * q
+    assert P.star_count_macs(ga, np.bincount(t, minlength=q)) * q * q == (2 * q - 1) * M * d * d
+    del Y
+    torch.cuda.empty_cache()
+
+
+def test_cfg3_full_size_sampled(P):
+    """Training shapes: M = 16384 (16 x 1024), up 768 -> 3072 GELU, down 3072 -> 768.
+    Forward and activation gradients on sampled rows (row-local); weight
+    gradients on sampled entries of the full-batch sum."""
+    import torch
+    M, D, F = 16384, 768, 3072
+    up_g, up_o = algs(P, 2, [384, 384], [1536, 1536])
+    dn_g, dn_o = algs(P, 2, [1536, 1536], [384, 384])
+    X = synth.gaussian(3, 0, (M, D), 1.0, "bf16")
+    Wu = synth.gaussian(3, 1, (D, F), 0.02, "bf16")
+    Wd = synth.gaussian(3, 2, (F, D), 0.02, "bf16")
+    bu = synth.gaussian(3, 3, (F,), 0.02, "f32")
+    bd = synth.gaussian(3, 4, (D,), 0.02, "f32")
+    dY = synth.gaussian(3, 5, (M, D), 1.0, "bf16")
+    t = synth.sequence_types(M, 2, 1024)
+    td = types_dev(t)
+    Xd, Wud, Wdd, dYd = to_dev(X), to_dev(Wu), to_dev(Wd), to_dev(dY)
+    Z, H, Y = P.star_ffn_fwd(up_g, dn_g, td, Xd, Wud, f32_dev(bu.exact), Wdd, f32_dev(bd.exact),
+                             "gelu")
+    g = P.star_ffn_bwd(up_g, dn_g, td, Xd, Z, H, Wud, Wdd, dYd, "gelu")
+    rows = _sample_rows(M, 200, 3)
+    rZ, rH, rY = oracle.ffn_fwd(up_o, dn_o, t[rows], X.exact[rows], Wu.exact, bu.exact, Wd.exact,
+                                bd.exact)
+    assert rel_fro(to_host(Y[rows]), rY) <= TOL_BF16
+    rg = oracle.ffn_bwd(up_o, dn_o, t[rows], X.exact[rows], rZ, rH, Wu.exact, Wd.exact,
+                        dY.exact[rows])
+    assert rel_fro(to_host(g["dZ"][rows]), rg["dZ"]) <= TOL_BF16
+    assert rel_fro(to_host(g["dX"][rows]), rg["dX"]) <= TOL_BF16
+    # weight gradients at full size on sampled entries, from the GPU's own
+    # stored H and dZ would make the oracle depend on the HIP path, so check
+    # the weight-gradient kernel at the same shapes on synthetic operands
+    rng = np.random.default_rng([3, 77])
+    for alg_g, alg_o, A_id, B_id, K_, N_ in ((up_g, up_o, 10, 11, D, F), (dn_g, dn_o, 12, 13, F, D)):
+        A = synth.gaussian(3, A_id, (M, K_), 1.0, "bf16")
+        B = synth.gaussian(3, B_id, (M, N_), 1.0, "bf16")
+        dW, db = P.star_proj_bwd_weight(alg_g, td, to_dev(A), to_dev(B))
+        kk = rng.integers(0, K_, 2048)
+        nn = rng.integers(0, N_, 2048)
+        ref = oracle.bwd_weight_entries(alg_o, t, A.exact, B.exact, kk, nn)
+        assert rel_fro(to_host(dW)[kk, nn], ref) <= TOL_BF16
+        assert rel_fro(to_host(db), B.exact.sum(0)) <= TOL_BF16
+    torch.cuda.empty_cache()
