@@ -30,7 +30,7 @@
  *    returns a non-zero status and writes nothing.  A failed launch returns
  *    STAR_ERR_HIP.  Nothing is printed and no exception crosses the ABI.
  *  - Group widths must be positive multiples of 8 and q at most STAR_MAX_Q.
- *    Operand, output and workspace pointers must be 16-byte aligned.
+ *    Operand, output, bias and workspace pointers must be 16-byte aligned.
  *  - Row types must lie in [0, q).  This is not checked by the compute calls
  *    (star_validate_types checks it); a row with an out-of-range type is left
  *    out of every product and its output row is not written.
@@ -193,6 +193,43 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
                         const void *const *W_down, const float *const *b_down,
                         star_act act, int32_t residual, void *Y, star_dtype yt,
                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Type plan: the per-type row sets I_i of Alg. 1 (line "I_i <- {b : tau(p_b)
+ * = i}") as one stable permutation of the rows grouped by type plus q+1
+ * offsets.  Every compute call needs it; the plain entry points build it in
+ * their workspace on each call, the *_planned entry points take one built
+ * here, so calls that share row types (the six products of an FFN training
+ * step, repeated replays) build it once.
+ *   plan  device buffer of at least star_plan_bytes(q, M) bytes, 16-byte
+ *         aligned; it holds int32 perm[M] followed (at a 256-byte boundary)
+ *         by int32 offsets[q+1].  Rows with a type outside [0, q) are placed
+ *         after offsets[q] and left out of every product.
+ */
+size_t star_plan_bytes(int32_t q, int64_t M);
+star_status star_type_plan(int32_t q, int64_t M, const int32_t *row_type, void *plan,
+                           size_t plan_bytes, hipStream_t stream);
+
+/* star_proj_fwd with a plan built by star_type_plan for the same rows (no
+ * workspace needed). */
+star_status star_proj_fwd_planned(const star_algebra *alg, int64_t M, const void *plan,
+                                  const void *X, star_dtype xt, const void *W, star_dtype wt,
+                                  const float *bias, star_act act, void *Z_out, void *Y,
+                                  star_dtype yt, hipStream_t stream);
+
+/* star_proj_bwd_data with a prebuilt plan (no workspace needed). */
+star_status star_proj_bwd_data_planned(const star_algebra *alg, int64_t M, const void *plan,
+                                       const void *dY, star_dtype dyt, const void *W,
+                                       star_dtype wt, const void *Z_prev, star_act act_prev,
+                                       void *dX, star_dtype dxt, hipStream_t stream);
+
+/* star_proj_bwd_weight with a prebuilt plan.  ws holds the split partial
+ * sums: at least star_workspace_bytes(STAR_OP_BWD_WEIGHT, alg, NULL, M)
+ * bytes (may be NULL when that size equals star_plan_bytes(q, M)). */
+star_status star_proj_bwd_weight_planned(const star_algebra *alg, int64_t M, const void *plan,
+                                         const void *X, star_dtype xt, const void *dY,
+                                         star_dtype dyt, float *dW, float *dbias, void *ws,
+                                         size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes an entry point needs (alg2 is the down algebra for
  * STAR_OP_FFN_FWD and STAR_OP_DECODE, else ignored).  Returns 0 for invalid

@@ -82,6 +82,8 @@ def _load():
         lib.oracle_row_macs.argtypes = [i32, i32, i64p, i64p, i32]
         lib.oracle_square_star.restype = None
         lib.oracle_square_star.argtypes = [i32, i64, f64p, f64p, f64p]
+        lib.oracle_num_threads.restype = i32
+        lib.oracle_num_threads.argtypes = []
         lib.oracle_in_support.restype = i32
         lib.oracle_in_support.argtypes = [i32, i32, i32, i32]
         _lib = lib
@@ -119,6 +121,11 @@ class Alg:
 
     def _arrays(self):
         return (np.asarray(self.s, dtype=np.int64), np.asarray(self.r, dtype=np.int64))
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's loops run on."""
+    return int(_load().oracle_num_threads())
 
 
 def in_support(law: str, i: int, j: int, k: int) -> bool:

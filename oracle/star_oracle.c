@@ -376,3 +376,16 @@ int oracle_bwd_weight_entries(int q, const int64_t *s, const int64_t *r, int law
     }
     return 0;
 }
+
+/* Number of OpenMP threads the parallel loops above use. */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -59,10 +59,18 @@ def _load() -> ctypes.CDLL:
     lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
     lib.star_count_macs.argtypes = [A, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.star_validate_types.argtypes = [i64, P, i32, ctypes.POINTER(i64), P, sz, P]
+    lib.star_plan_bytes.argtypes = [i32, i64]
+    lib.star_plan_bytes.restype = sz
+    lib.star_type_plan.argtypes = [i32, i64, P, P, sz, P]
+    lib.star_proj_fwd_planned.argtypes = [A, i64, P, P, E, P, E, P, E, P, P, E, P]
+    lib.star_proj_bwd_data_planned.argtypes = [A, i64, P, P, E, P, E, P, E, P, E, P]
+    lib.star_proj_bwd_weight_planned.argtypes = [A, i64, P, P, E, P, E, P, P, P, sz, P]
     lib.star_status_string.argtypes = [E]
     lib.star_status_string.restype = ctypes.c_char_p
     for name in ("star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
-                 "star_decode", "star_count_products", "star_count_macs", "star_validate_types"):
+                 "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
+                 "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
+                 "star_proj_bwd_weight_planned"):
         getattr(lib, name).restype = E
     return lib
 
@@ -164,6 +172,66 @@ def star_validate_types(row_type: torch.Tensor, q: int, ws=None) -> int:
     return int(n_bad.value)
 
 
+def star_plan_bytes(q: int, M: int) -> int:
+    return int(LIB.star_plan_bytes(int(q), int(M)))
+
+
+def star_type_plan(q: int, row_type: torch.Tensor, plan=None):
+    """Builds the type plan of ``row_type`` (device uint8 buffer)."""
+    M = row_type.numel()
+    dev = row_type.device
+    if plan is None:
+        plan = torch.empty(max(star_plan_bytes(q, M), 16), dtype=torch.uint8, device=dev)
+    _check(LIB.star_type_plan(int(q), M, _ptr(row_type), _ptr(plan), plan.numel(), _stream(dev)),
+           "star_type_plan")
+    return plan
+
+
+def star_proj_fwd_planned(alg: Algebra, plan: torch.Tensor, X: torch.Tensor, W: torch.Tensor,
+                          bias: torch.Tensor | None = None, act: str = "none", Z_out=None,
+                          Y=None, out_dtype=None):
+    M = X.shape[0]
+    dev = X.device
+    if Y is None:
+        Y = torch.empty((M, alg.N), dtype=out_dtype or X.dtype, device=dev)
+    want_z = Z_out is not None and Z_out is not False
+    if Z_out is True:
+        Z_out = torch.empty((M, alg.N), dtype=Y.dtype, device=dev)
+    _check(LIB.star_proj_fwd_planned(alg.ref, M, _ptr(plan), _ptr(X), _dt(X), _ptr(W), _dt(W),
+                                     _ptr(bias), ACTS[act], _ptr(Z_out) if want_z else None,
+                                     _ptr(Y), _dt(Y), _stream(dev)), "star_proj_fwd_planned")
+    return (Y, Z_out) if want_z else Y
+
+
+def star_proj_bwd_data_planned(alg: Algebra, plan: torch.Tensor, dY: torch.Tensor,
+                               W: torch.Tensor, Z_prev=None, act_prev: str = "none", dX=None,
+                               out_dtype=None):
+    M = dY.shape[0]
+    dev = dY.device
+    if dX is None:
+        dX = torch.empty((M, alg.K), dtype=out_dtype or dY.dtype, device=dev)
+    _check(LIB.star_proj_bwd_data_planned(alg.ref, M, _ptr(plan), _ptr(dY), _dt(dY), _ptr(W),
+                                          _dt(W), _ptr(Z_prev), ACTS[act_prev], _ptr(dX),
+                                          _dt(dX), _stream(dev)), "star_proj_bwd_data_planned")
+    return dX
+
+
+def star_proj_bwd_weight_planned(alg: Algebra, plan: torch.Tensor, X: torch.Tensor,
+                                 dY: torch.Tensor, dW=None, dbias=None, want_dbias: bool = True,
+                                 ws=None):
+    M = X.shape[0]
+    dev = X.device
+    if dW is None:
+        dW = torch.empty((alg.K, alg.N), dtype=torch.float32, device=dev)
+    if dbias is None and want_dbias:
+        dbias = torch.empty(alg.N, dtype=torch.float32, device=dev)
+    ws, nbytes = _ws("bwd_weight", alg, None, M, dev, ws)
+    _check(LIB.star_proj_bwd_weight_planned(alg.ref, M, _ptr(plan), _ptr(X), _dt(X), _ptr(dY),
+                                            _dt(dY), _ptr(dW), _ptr(dbias), _ptr(ws), nbytes,
+                                            _stream(dev)), "star_proj_bwd_weight_planned")
+    return dW, dbias
+
+
 def star_proj_fwd(alg: Algebra, row_type: torch.Tensor, X: torch.Tensor, W: torch.Tensor,
                   bias: torch.Tensor | None = None, act: str = "none", Z_out=None, Y=None,
                   out_dtype=None, ws=None):
@@ -258,14 +326,16 @@ def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Ten
 
 def star_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
                  Z_up: torch.Tensor, H: torch.Tensor, W_up: torch.Tensor, W_down: torch.Tensor,
-                 dY: torch.Tensor, act: str = "gelu", ws=None):
-    """Backward of ``star_ffn_fwd`` as four library calls on one stream:
-    dZ = (dY *^T W_down) . act'(Z_up)  (fused epilogue);  dW_down, db_down from
-    (H, dY);  dW_up, db_up from (X, dZ);  dX = dZ *^T W_up.
+                 dY: torch.Tensor, act: str = "gelu", plan=None, ws=None):
+    """Backward of ``star_ffn_fwd``: one type plan, then four library calls
+    on one stream: dZ = (dY *^T W_down) . act'(Z_up) (fused epilogue);
+    dW_down, db_down from (H, dY); dW_up, db_up from (X, dZ); dX = dZ *^T W_up.
     Returns a dict of dX, dZ, dW_up, db_up, dW_down, db_down."""
-    dZ = star_proj_bwd_data(down, row_type, dY, W_down, Z_prev=Z_up, act_prev=act,
-                            out_dtype=X.dtype, ws=ws)
-    dW_down, db_down = star_proj_bwd_weight(down, row_type, H, dY, ws=ws)
-    dW_up, db_up = star_proj_bwd_weight(up, row_type, X, dZ, ws=ws)
-    dX = star_proj_bwd_data(up, row_type, dZ, W_up, ws=ws)
+    if plan is None:
+        plan = star_type_plan(up.q, row_type)
+    dZ = star_proj_bwd_data_planned(down, plan, dY, W_down, Z_prev=Z_up, act_prev=act,
+                                    out_dtype=X.dtype)
+    dW_down, db_down = star_proj_bwd_weight_planned(down, plan, H, dY, ws=ws)
+    dW_up, db_up = star_proj_bwd_weight_planned(up, plan, X, dZ, ws=ws)
+    dX = star_proj_bwd_data_planned(up, plan, dZ, W_up)
     return dict(dX=dX, dZ=dZ, dW_up=dW_up, db_up=db_up, dW_down=dW_down, db_down=db_down)

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 
 #include "../../include/star_proj.h"
@@ -89,14 +90,19 @@ PlanWs plan_layout(int64_t M, int q, size_t base = 0) {
 
 int tiles_of(int64_t w, int tile) { return static_cast<int>((w + tile - 1) / tile); }
 
+// Column-tile width of the weight-gradient GEMM: 128 columns (the
+// contraction is over rows, the output K x N is small).
+constexpr int kBwdWeightNW = 2;
+
 int bwd_weight_nsplit(const Alg& a, int64_t M) {
   int64_t mt = 0, nt = 0;
   for (int g = 0; g < a.q; ++g) {
     mt += tiles_of(a.s(g), kTileM);
-    nt += tiles_of(a.r(g), kTileN);
+    nt += tiles_of(a.r(g), 64 * kBwdWeightNW);
   }
   const int64_t base = mt * nt;
-  int64_t ns = (512 + base - 1) / base;
+  // about one tile per CU of a 256-CU device, rows per split >= 1024
+  int64_t ns = (256 + base - 1) / base;
   ns = std::min<int64_t>(ns, 8);
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, M / 1024));
   return static_cast<int>(std::max<int64_t>(ns, 1));
@@ -185,11 +191,27 @@ void fill_tiles(int32_t* pfx, const int64_t* G, int q, int tile) {
   for (int g = 0; g < q; ++g) pfx[g + 1] = pfx[g] + tiles_of(G[g + 1] - G[g], tile);
 }
 
+// One workgroup per CU at most (each uses 96-128 KB of LDS); a multiple of
+// 8 so that every XCD gets the same number of workgroups.
 int persistent_grid(int64_t upper_tiles) {
-  const int64_t cap = 2 * static_cast<int64_t>(cu_count());
+  const int64_t cap = static_cast<int64_t>(cu_count());
   int64_t g = std::min<int64_t>(std::max<int64_t>(upper_tiles, 1), cap);
   g = (g + 7) / 8 * 8;
   return static_cast<int>(g);
+}
+
+// Column-tile width of the forward and activation-gradient GEMMs: 128
+// columns (nw = 2).  The 256-column variant (nw = 4) holds 256 accumulators
+// per lane and spills; STARQ_GEMM_NW=4 selects it for experiments.
+int choose_nw(const int64_t* G, int q, int64_t rows_upper) {
+  if (const char* env = std::getenv("STARQ_GEMM_NW")) {
+    const int v = std::atoi(env);
+    if (v == 2 || v == 4) return v;
+  }
+  (void)G;
+  (void)q;
+  (void)rows_upper;
+  return 2;
 }
 
 star_status hip_status(hipError_t e) { return e == hipSuccess ? STAR_OK : STAR_ERR_HIP; }
@@ -205,7 +227,6 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
                     void* Z, void* Y, star_dtype yt, hipStream_t stream) {
   GemmParams p;
   fill_common(p, a, M, elem, perm, offsets);
-  fill_tiles(p.NTp, a.R, a.q, kTileN);
   p.A = X;
   p.B = W;
   p.bias = bias;
@@ -213,8 +234,11 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
   p.Z = Z;
   p.Y = Y;
   p.ydtype = yt;
-  const int64_t upper = (M / kTileM + a.q + 1) * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_gemm(kModeFwd, p, persistent_grid(upper), stream));
+  const int64_t rows_upper = M / kTileM + a.q;
+  const int nw = choose_nw(a.R, a.q, rows_upper);
+  fill_tiles(p.NTp, a.R, a.q, 64 * nw);
+  const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
+  return hip_status(launch_gemm(kModeFwd, p, nw, persistent_grid(upper), stream));
 }
 
 star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a) {
@@ -296,6 +320,47 @@ star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_typ
   return STAR_OK;
 }
 
+size_t star_plan_bytes(int32_t q, int64_t M) {
+  if (q < 1 || q > kMaxQGroups || M < 0 || M > kMaxDim) return 0;
+  return plan_layout(M, q).end;
+}
+
+star_status star_type_plan(int32_t q, int64_t M, const int32_t* row_type, void* plan,
+                           size_t plan_bytes, hipStream_t stream) {
+  if (q < 1 || q > kMaxQGroups) return STAR_ERR_ARG;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (M == 0) return STAR_OK;
+  if (!row_type || !plan) return STAR_ERR_ARG;
+  if (!aligned4(row_type) || !aligned16(plan)) return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, q);
+  if (plan_bytes < pw.end) return STAR_ERR_WORKSPACE;
+  return run_plan(row_type, M, q, plan, pw, stream);
+}
+
+// The *_planned entry points take a plan built by star_type_plan; the
+// plain entry points build it into the head of their workspace first.
+
+star_status star_proj_fwd_planned(const star_algebra* alg, int64_t M, const void* plan,
+                                  const void* X, star_dtype xt, const void* W, star_dtype wt,
+                                  const float* bias, star_act act, void* Z_out, void* Y,
+                                  star_dtype yt, hipStream_t stream) {
+  Alg a;
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(yt) || xt != wt) return STAR_ERR_DTYPE;
+  if (!valid_act(act)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!plan || !X || !W || !Y) return STAR_ERR_ARG;
+  if (!aligned16(plan) || !aligned16(X) || !aligned16(W) || !aligned16(Y) ||
+      (Z_out && !aligned16(Z_out)) || (bias && !aligned16(bias)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, a.q);
+  void* pl = const_cast<void*>(plan);
+  return run_fwd(a, M, at<int32_t>(pl, pw.perm), at<int32_t>(pl, pw.offsets), X, W,
+                 xt == STAR_BF16 ? 1 : 0, bias, act, Z_out, Y, yt, stream);
+}
+
 star_status star_proj_fwd(const star_algebra* alg, int64_t M, const int32_t* row_type,
                           const void* X, star_dtype xt, const void* W, star_dtype wt,
                           const float* bias, star_act act, void* Z_out, void* Y, star_dtype yt,
@@ -308,15 +373,48 @@ star_status star_proj_fwd(const star_algebra* alg, int64_t M, const int32_t* row
   if (M == 0) return STAR_OK;
   if (!X || !W || !Y) return STAR_ERR_ARG;
   if (!aligned16(X) || !aligned16(W) || !aligned16(Y) || (Z_out && !aligned16(Z_out)) ||
-      (bias && !aligned4(bias)))
+      (bias && !aligned16(bias)))
     return STAR_ERR_ALIGN;
   const PlanWs pw = plan_layout(M, a.q);
   if (!ws || ws_bytes < pw.end) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
   st = run_plan(row_type, M, a.q, ws, pw, stream);
   if (st != STAR_OK) return st;
-  return run_fwd(a, M, at<int32_t>(ws, pw.perm), at<int32_t>(ws, pw.offsets), X, W,
-                 xt == STAR_BF16 ? 1 : 0, bias, act, Z_out, Y, yt, stream);
+  return star_proj_fwd_planned(alg, M, ws, X, xt, W, wt, bias, act, Z_out, Y, yt, stream);
+}
+
+star_status star_proj_bwd_data_planned(const star_algebra* alg, int64_t M, const void* plan,
+                                       const void* dY, star_dtype dyt, const void* W,
+                                       star_dtype wt, const void* Z_prev, star_act act_prev,
+                                       void* dX, star_dtype dxt, hipStream_t stream) {
+  Alg a;
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (!valid_dtype(dyt) || !valid_dtype(wt) || !valid_dtype(dxt) || dyt != wt)
+    return STAR_ERR_DTYPE;
+  if (!valid_act(act_prev)) return STAR_ERR_ARG;
+  if (M == 0) return STAR_OK;
+  if (!plan || !dY || !W || !dX) return STAR_ERR_ARG;
+  if (!aligned16(plan) || !aligned16(dY) || !aligned16(W) || !aligned16(dX) ||
+      (Z_prev && !aligned16(Z_prev)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, a.q);
+  void* pl = const_cast<void*>(plan);
+  GemmParams p;
+  fill_common(p, a, M, dyt == STAR_BF16 ? 1 : 0, at<int32_t>(pl, pw.perm),
+              at<int32_t>(pl, pw.offsets));
+  p.A = dY;
+  p.B = W;
+  p.Zprev = Z_prev;
+  p.act = Z_prev ? act_prev : STAR_ACT_NONE;
+  p.Y = dX;
+  p.ydtype = dxt;
+  const int64_t rows_upper = M / kTileM + a.q;
+  const int nw = choose_nw(a.S, a.q, rows_upper);
+  fill_tiles(p.NTp, a.S, a.q, 64 * nw);
+  const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
+  return hip_status(launch_gemm(kModeBwdData, p, nw, persistent_grid(upper), stream));
 }
 
 star_status star_proj_bwd_data(const star_algebra* alg, int64_t M, const int32_t* row_type,
@@ -338,18 +436,53 @@ star_status star_proj_bwd_data(const star_algebra* alg, int64_t M, const int32_t
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
   st = run_plan(row_type, M, a.q, ws, pw, stream);
   if (st != STAR_OK) return st;
+  return star_proj_bwd_data_planned(alg, M, ws, dY, dyt, W, wt, Z_prev, act_prev, dX, dxt,
+                                    stream);
+}
+
+star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, const void* plan,
+                                         const void* X, star_dtype xt, const void* dY,
+                                         star_dtype dyt, float* dW, float* dbias, void* ws,
+                                         size_t ws_bytes, hipStream_t stream) {
+  Alg a;
+  star_status st = parse_alg(alg, a);
+  if (st != STAR_OK) return st;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (!valid_dtype(xt) || !valid_dtype(dyt) || xt != dyt) return STAR_ERR_DTYPE;
+  if (!dW) return STAR_ERR_ARG;
+  if (M > 0 && (!X || !dY || !plan)) return STAR_ERR_ARG;
+  if ((X && !aligned16(X)) || (dY && !aligned16(dY)) || !aligned16(dW) ||
+      (dbias && !aligned4(dbias)) || (plan && !aligned16(plan)))
+    return STAR_ERR_ALIGN;
+  const BwdWs bw = bwd_weight_layout(a, M);
+  if (bw.nsplit > 1 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
+  if (ws && !aligned16(ws)) return STAR_ERR_ALIGN;
+  // M = 0 still defines the output: an empty sum
+  if (M == 0) {
+    hipError_t e = launch_fill_zero(dW, a.K() * a.N(), stream);
+    if (e == hipSuccess && dbias) e = launch_fill_zero(dbias, a.N(), stream);
+    return hip_status(e);
+  }
+  const PlanWs pw = plan_layout(M, a.q);
+  void* pl = const_cast<void*>(plan);
   GemmParams p;
-  fill_common(p, a, M, dyt == STAR_BF16 ? 1 : 0, at<int32_t>(ws, pw.perm),
-              at<int32_t>(ws, pw.offsets));
-  fill_tiles(p.NTp, a.S, a.q, kTileN);
-  p.A = dY;
-  p.B = W;
-  p.Zprev = Z_prev;
-  p.act = Z_prev ? act_prev : STAR_ACT_NONE;
-  p.Y = dX;
-  p.ydtype = dxt;
-  const int64_t upper = (M / kTileM + a.q + 1) * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_gemm(kModeBwdData, p, persistent_grid(upper), stream));
+  fill_common(p, a, M, xt == STAR_BF16 ? 1 : 0, at<int32_t>(pl, pw.perm),
+              at<int32_t>(pl, pw.offsets));
+  fill_tiles(p.NTp, a.R, a.q, 64 * kBwdWeightNW);
+  fill_tiles(p.MTp, a.S, a.q, kTileM);
+  p.A = X;
+  p.B = dY;
+  p.dW = dW;
+  p.dbias = dbias;
+  p.nsplit = bw.nsplit;
+  if (bw.nsplit > 1) {
+    p.partial = at<float>(ws, bw.partial);
+    p.dbias_part = at<float>(ws, bw.dbias_part);
+  }
+  const int64_t upper = static_cast<int64_t>(p.MTp[a.q]) * p.NTp[a.q] * p.nsplit;
+  st = hip_status(launch_gemm(kModeBwdWeight, p, kBwdWeightNW, persistent_grid(upper), stream));
+  if (st != STAR_OK || bw.nsplit == 1) return st;
+  return hip_status(launch_split_reduce(p, stream));
 }
 
 star_status star_proj_bwd_weight(const star_algebra* alg, int64_t M, const int32_t* row_type,
@@ -368,32 +501,12 @@ star_status star_proj_bwd_weight(const star_algebra* alg, int64_t M, const int32
   const BwdWs bw = bwd_weight_layout(a, M);
   if (!ws || ws_bytes < bw.end) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
-  // M = 0 still defines the output: an empty sum
-  if (M == 0) {
-    hipError_t e = launch_fill_zero(dW, a.K() * a.N(), stream);
-    if (e == hipSuccess && dbias) e = launch_fill_zero(dbias, a.N(), stream);
-    return hip_status(e);
+  if (M > 0) {
+    st = run_plan(row_type, M, a.q, ws, bw.plan, stream);
+    if (st != STAR_OK) return st;
   }
-  st = run_plan(row_type, M, a.q, ws, bw.plan, stream);
-  if (st != STAR_OK) return st;
-  GemmParams p;
-  fill_common(p, a, M, xt == STAR_BF16 ? 1 : 0, at<int32_t>(ws, bw.plan.perm),
-              at<int32_t>(ws, bw.plan.offsets));
-  fill_tiles(p.NTp, a.R, a.q, kTileN);
-  fill_tiles(p.MTp, a.S, a.q, kTileM);
-  p.A = X;
-  p.B = dY;
-  p.dW = dW;
-  p.dbias = dbias;
-  p.nsplit = bw.nsplit;
-  if (bw.nsplit > 1) {
-    p.partial = at<float>(ws, bw.partial);
-    p.dbias_part = at<float>(ws, bw.dbias_part);
-  }
-  const int64_t upper = static_cast<int64_t>(p.MTp[a.q]) * p.NTp[a.q] * p.nsplit;
-  st = hip_status(launch_gemm(kModeBwdWeight, p, persistent_grid(upper), stream));
-  if (st != STAR_OK || bw.nsplit == 1) return st;
-  return hip_status(launch_split_reduce(p, stream));
+  return star_proj_bwd_weight_planned(alg, M, ws, X, xt, dY, dyt, dW, dbias, ws, ws_bytes,
+                                      stream);
 }
 
 star_status star_ffn_fwd(const star_algebra* up, const star_algebra* down, int64_t M,
@@ -414,8 +527,8 @@ star_status star_ffn_fwd(const star_algebra* up, const star_algebra* down, int64
   if (M == 0) return STAR_OK;
   if (!X || !W_up || !W_down || !H || !Y) return STAR_ERR_ARG;
   if (!aligned16(X) || !aligned16(W_up) || !aligned16(W_down) || !aligned16(H) ||
-      !aligned16(Y) || (Z_up && !aligned16(Z_up)) || (b_up && !aligned4(b_up)) ||
-      (b_down && !aligned4(b_down)))
+      !aligned16(Y) || (Z_up && !aligned16(Z_up)) || (b_up && !aligned16(b_up)) ||
+      (b_down && !aligned16(b_down)))
     return STAR_ERR_ALIGN;
   const PlanWs pw = plan_layout(M, u.q);
   if (!ws || ws_bytes < pw.end) return STAR_ERR_WORKSPACE;

@@ -2,10 +2,11 @@
 // activation gradient and its weight gradient (Alg. 1 and the VJPs of the
 // appendix) in one persistent kernel template.
 //
-// Work decomposition.  C is tiled in 128 x 128 tiles, one per workgroup
-// iteration (256 threads = 4 wavefronts in a 2 x 2 arrangement, 64 x 64 of
-// C per wavefront as 2 x 2 blocks of v_mfma_f32_32x32x16_bf16, or of
-// v_mfma_f32_32x32x2f32 for fp32 operands).
+// Work decomposition.  C is cut into tiles of 256 rows x BN columns
+// (BN = 64 * WN with WN = 2 or 4).  A workgroup of 4 wavefronts (one per
+// SIMD) computes a tile; the wavefronts form a 2 x 2 grid and each owns
+// 128 x (32 * WN) of C as 4 x WN blocks of v_mfma_f32_32x32x16_bf16 (or of
+// v_mfma_f32_32x32x2f32 for fp32 operands), accumulated in AGPRs.
 //
 //  * FWD: a tile is (row type i, row tile of I_i, output group j, column
 //    tile).  Its K range is the concatenation of the input groups in
@@ -25,21 +26,34 @@
 //    second kernel sums in a fixed order.  The bias gradient is summed from
 //    the dY tiles that the diagonal tiles already stage.
 //
-// Scheduling.  The kernel is persistent: a grid of about two workgroups per
-// CU walks the tile list.  Tiles with the longer contraction run first
+// Scheduling.  The kernel is persistent: one workgroup per CU walks its
+// share of the tile list.  Tiles with the longer contraction come first
 // (pass 0), the shorter ones after (pass 1).  Within a pass the list is cut
 // into 8 contiguous chunks, one per XCD (workgroups are dispatched
-// round-robin over the 8 XCDs), and consecutive tiles of a chunk share their
-// weight panel, so concurrently running tiles of one XCD hit the same L2.
+// round-robin over the 8 XCDs), and consecutive tiles of a chunk share
+// their weight panel, so the tiles running together on one XCD hit the same
+// L2.  A workgroup runs its tiles as one flat sequence of K steps: while the
+// last step of a tile computes, the first step of the next tile (whose row
+// indices were fetched a whole tile earlier) is already being loaded.
 //
-// Operand staging.  Each K step moves 128 bytes of K per row into LDS
-// (64 bf16 or 32 fp32), double-buffered with one barrier per step.  Operands
-// whose rows are K-contiguous are copied 16 bytes per lane; operands that are
-// contiguous along the output dimension (W in the forward product, X and dY
-// in the weight gradient) are transposed in registers on their way into LDS
-// (each lane loads 4 bf16 rows x 8 columns, or 2 fp32 rows x 4 columns, and
-// writes 8-byte K-contiguous pieces), so every MFMA operand is read from LDS
-// as one 16-byte vector per lane.
+// LDS layout.  Each K step stages 8 "kpacks" (16 bytes of K: 8 bf16 or 4
+// fp32) per tile row, double-buffered.  A tile is stored kpack-major:
+// unit (kp, row) holds the 16 bytes of K of that row, at
+// (kp * rows + swz(row, kp)) * 16, where swz XORs the low three bits of the
+// row with bits 3..5 of the row and the kpack index.  With it the three
+// access patterns are free of bank conflicts: the MFMA operand read (32
+// consecutive rows, one kpack), the direct store of K-contiguous rows
+// (8 kpacks of one row from 8 lanes) and the transposed store.  Operands
+// that are contiguous along the tile rows (W in the forward product, X and
+// dY in the weight gradient) are transposed in registers on the way: each
+// thread loads 4 source rows x 16 bytes and writes one 4-element piece per
+// tile row.  Fragments for the next 16-wide K slice are read from LDS while
+// the MFMAs of the current slice run.
+//
+// Epilogue.  The MFMA is issued with the operands swapped (it computes
+// C^T blocks), so each lane ends with 4 consecutive columns of one row of
+// C and writes them as one 8- or 16-byte store.  GELU uses the erf
+// approximation 7.1.26 of Abramowitz & Stegun (absolute error <= 1.5e-7).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -47,31 +61,39 @@ namespace starq {
 
 namespace {
 
-constexpr int BM = kTileM;
-constexpr int BN = kTileN;
-constexpr int kThreads = kGemmThreads;
-constexpr int kRowBytes = 144;  // 128 bytes of K + 16 bytes of padding
-constexpr int kTileBytes = BM * kRowBytes;
-static_assert(BM == BN, "A and B LDS tiles share one layout");
-constexpr int kSmemBytes = 4 * kTileBytes;  // A and B, double-buffered
+constexpr int BM = kTileM;  // 256
+constexpr int THREADS = 256;
 
-enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3 };
-
-template <typename T> struct Traits;
-template <> struct Traits<float> {
-  static constexpr int VEC = 4;  // elements per 16-byte vector
-  static constexpr int BK = 32;  // K per step (128 bytes)
-  static constexpr int TK = 2;   // K rows per transposed 8-byte LDS write
+template <typename T> struct Tr;
+template <> struct Tr<float> {
+  static constexpr int VEC = 4;  // elements per 16-byte kpack
+  static constexpr int BK = 32;  // K per step: 8 kpacks
 };
-template <> struct Traits<uint16_t> {
+template <> struct Tr<uint16_t> {
   static constexpr int VEC = 8;
   static constexpr int BK = 64;
-  static constexpr int TK = 4;
 };
+
+template <int WN> struct Geo {
+  static constexpr int BN = 64 * WN;
+  static constexpr int A_BYTES = 8 * BM * 16;
+  static constexpr int B_BYTES = 8 * BN * 16;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int SMEM = 2 * STAGE;
+};
+
+__device__ __forceinline__ int swz(int row, int kp) { return row ^ (((row >> 3) ^ kp) & 7); }
+
+template <int ROWS>
+__device__ __forceinline__ int unit_off(int kp, int row) {
+  return (kp * ROWS + swz(row, kp)) * 16;
+}
 
 __device__ __forceinline__ uint32_t word_of(const uint4& r, int w) {
   return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
 }
+
+enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3 };
 
 __device__ __forceinline__ int sel_for(int mode, int law, int pass) {
   if (law == 1) return pass == 0 ? kSelAll : kSelNone;
@@ -96,165 +118,369 @@ __device__ __forceinline__ int col_tile_global(const GemmParams& p, int sel, int
   return c;
 }
 
+// D += A B with the operands of the C^T block: a = B-tile fragment (rows of
+// D are columns of C), b = A-tile fragment (columns of D are rows of C).
 __device__ __forceinline__ void mma(f32x16_t& acc, const uint4& a, const uint4& b, uint16_t) {
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                 __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
 }
-
 __device__ __forceinline__ void mma(f32x16_t& acc, const uint4& a, const uint4& b, float) {
-  // lane half h supplies K elements 4h..4h+3 of this 8-wide slice, one per
-  // instruction; A and B use the same assignment, so the products pair up.
+  // lane half h supplies K element 4 kp + j of instruction j; both operands
+  // use the same assignment, so the products pair up.
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
 }
 
-// ---- operand staging -------------------------------------------------------
+// ---- GELU -------------------------------------------------------------------
 
-// K-contiguous rows: LDS row r <- src[rowid[r]][k0 .. k0+BK), zero outside
-// [.., kend) or for rowid < 0.  Thread t covers rows t/8 + 32u, 16-byte
-// chunk t%8.
-template <typename T>
-__device__ __forceinline__ void load_k(uint4 (&reg)[4], const T* __restrict__ src, int64_t ld,
-                                       const int32_t (&rowid)[4], int32_t k0, int32_t kend) {
-  constexpr int VEC = Traits<T>::VEC;
-  const int32_t kk = k0 + (threadIdx.x & 7) * VEC;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    if (rowid[u] >= 0 && kk < kend)
-      reg[u] = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(rowid[u]) * ld + kk);
-    else
-      reg[u] = make_uint4(0, 0, 0, 0);
+constexpr float kLog2e = 1.4426950408889634f;
+
+// erf from Abramowitz & Stegun 7.1.26: erf(x) = 1 - (a1 t + ... + a5 t^5)
+// exp(-x^2), t = 1 / (1 + p x), x >= 0; |error| <= 1.5e-7.  The reciprocal
+// and exponential are the hardware approximations (about 1 ulp).
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  float poly = 1.061405429f;
+  poly = poly * t - 1.453152027f;
+  poly = poly * t + 1.421413741f;
+  poly = poly * t - 0.284496736f;
+  poly = poly * t + 0.254829592f;
+  poly *= t;
+  const float y = 1.0f - poly * __builtin_amdgcn_exp2f(-(ax * ax) * kLog2e);
+  return copysignf(y, x);
+}
+
+__device__ __forceinline__ float act_apply(int act, float z) {
+  if (act == kActGelu) return 0.5f * z * (1.0f + erf_as7126(z * 0.70710678118654752f));
+  if (act == kActGeluTanh) {
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    return 0.5f * z * (1.0f + tanhf(u));
+  }
+  return z;
+}
+
+__device__ __forceinline__ float act_deriv(int act, float z) {
+  if (act == kActGelu)
+    return 0.5f * (1.0f + erf_as7126(z * 0.70710678118654752f)) +
+           z * 0.39894228040143268f * __builtin_amdgcn_exp2f(-0.5f * z * z * kLog2e);
+  if (act == kActGeluTanh) {
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    const float t = tanhf(u);
+    const float du = 0.79788456080286536f * (1.0f + 0.134145f * z * z);
+    return 0.5f * (1.0f + t) + 0.5f * z * (1.0f - t * t) * du;
+  }
+  return 1.0f;
+}
+
+// 4 consecutive values of a row of an fp32 or bf16 matrix
+__device__ __forceinline__ void store4(void* base, int dtype, int64_t idx, const float (&v)[4]) {
+  if (dtype == 0) {
+    *reinterpret_cast<float4*>(static_cast<float*>(base) + idx) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    uint2 w;
+    w.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    w.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(base) + idx) = w;
   }
 }
 
-__device__ __forceinline__ void store_k(char* lds, const uint4 (&reg)[4]) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-    *reinterpret_cast<uint4*>(lds + ((threadIdx.x >> 3) + 32 * u) * kRowBytes +
-                              (threadIdx.x & 7) * 16) = reg[u];
+__device__ __forceinline__ void load4(const void* base, int dtype, int64_t idx, float (&v)[4]) {
+  if (dtype == 0) {
+    const float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + idx);
+    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+  } else {
+    const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(base) + idx);
+    v[0] = bf16_to_f32(w.x & 0xffffu); v[1] = bf16_to_f32(w.x >> 16);
+    v[2] = bf16_to_f32(w.y & 0xffffu); v[3] = bf16_to_f32(w.y >> 16);
+  }
 }
 
-// Output-contiguous source: LDS row c (a column of the source) <- source
-// rows k0 .. k0+BK at column c0 + c.  Source row of K index k is
-// srow(k) (or < 0 to zero it).
-template <typename T> struct TGeom {
-  static constexpr int VEC = Traits<T>::VEC;
-  static constexpr int TK = Traits<T>::TK;
-  static constexpr int CB = BN / VEC;              // column chunks
-  static constexpr int KB = Traits<T>::BK / TK;    // K pieces
-  static constexpr int BPT = CB * KB / kThreads;   // blocks per thread
-  static_assert(BPT * TK == 4, "four 16-byte staging registers per operand");
+// One 16-byte load that reads zeros when `ok` is false.  The address is
+// clamped to the (always valid) first element instead of branching.
+template <typename T>
+__device__ __forceinline__ uint4 load16(const T* __restrict__ src, int64_t off, bool ok) {
+  const uint4 v = *reinterpret_cast<const uint4*>(src + (ok ? off : 0));
+  return ok ? v : make_uint4(0, 0, 0, 0);
+}
+
+// ---- operand staging -----------------------------------------------------
+
+// K-contiguous source rows.  Unit u = tid + THREADS * i covers kpack u % 8
+// of tile row u / 8 (8 lanes read one 128-byte row segment).
+template <typename T, int ROWS>
+struct DirectLoader {
+  static constexpr int VEC = Tr<T>::VEC;
+  static constexpr int UPT = ROWS * 8 / THREADS;
+  static_assert(UPT * THREADS == ROWS * 8, "whole units per thread");
+  uint4 reg[UPT];
+
+  __device__ __forceinline__ static int row_of(int i) { return (threadIdx.x + THREADS * i) >> 3; }
+  __device__ __forceinline__ static int kp_of() { return threadIdx.x & 7; }
+
+  __device__ __forceinline__ void load(const T* __restrict__ src, int64_t ld, const int32_t* rowid,
+                                       int32_t k0, int32_t kend) {
+    const int32_t kk = k0 + kp_of() * VEC;
+#pragma unroll
+    for (int i = 0; i < UPT; ++i)
+      reg[i] = load16(src, static_cast<int64_t>(rowid[i]) * ld + kk, rowid[i] >= 0 && kk < kend);
+  }
+  __device__ __forceinline__ void store(char* lds) const {
+#pragma unroll
+    for (int i = 0; i < UPT; ++i)
+      *reinterpret_cast<uint4*>(lds + unit_off<ROWS>(kp_of(), row_of(i))) = reg[i];
+  }
 };
 
-template <typename T, typename RowFn>
-__device__ __forceinline__ void load_t(uint4 (&reg)[4], const T* __restrict__ src, int64_t ld,
-                                       int32_t k0, int32_t c0, int32_t cend, RowFn srow) {
-  using G = TGeom<T>;
-#pragma unroll
-  for (int blk = 0; blk < G::BPT; ++blk) {
-    const int b = threadIdx.x + kThreads * blk;
-    const int cb = b % G::CB;
-    const int kb = b / G::CB;
-    const int32_t col = c0 + cb * G::VEC;
-#pragma unroll
-    for (int e = 0; e < G::TK; ++e) {
-      const int32_t row = srow(k0 + kb * G::TK + e);
-      if (row >= 0 && col < cend)
-        reg[blk * G::TK + e] =
-            *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row) * ld + col);
-      else
-        reg[blk * G::TK + e] = make_uint4(0, 0, 0, 0);
-    }
-  }
-}
+// Source contiguous along the tile rows (a source row is one K index).
+// Block b = tid + THREADS * i covers source rows 4 q .. 4 q + 3 (q = b / CB)
+// and tile rows VEC c .. VEC c + VEC - 1 (c = b % CB).
+template <typename T, int ROWS>
+struct TransLoader {
+  static constexpr int VEC = Tr<T>::VEC;
+  static constexpr int CB = ROWS / VEC;
+  static constexpr int NQ = Tr<T>::BK / 4;
+  static constexpr int BPT = CB * NQ / THREADS;
+  static_assert(BPT * THREADS == CB * NQ, "whole blocks per thread");
+  static_assert(THREADS % CB == 0, "a thread keeps its column chunk across blocks");
+  uint4 reg[BPT][4];
 
-// Transposed write of the staged blocks; optionally adds every staged value
-// into per-column sums (colsum[v] for column chunk cb, element v).
-template <typename T, bool kSum>
-__device__ __forceinline__ void store_t(char* lds, const uint4 (&reg)[4], float* colsum) {
-  using G = TGeom<T>;
+  __device__ __forceinline__ static int cb_of() { return threadIdx.x % CB; }
+  __device__ __forceinline__ static int q_of(int i) { return (threadIdx.x + THREADS * i) / CB; }
+
+  template <typename RowFn>
+  __device__ __forceinline__ void load(const T* __restrict__ src, int64_t ld, int32_t k0, int32_t c0,
+                                       int32_t cend, RowFn srow) {
+    const int32_t col = c0 + cb_of() * VEC;
 #pragma unroll
-  for (int blk = 0; blk < G::BPT; ++blk) {
-    const int b = threadIdx.x + kThreads * blk;
-    const int cb = b % G::CB;
-    const int kb = b / G::CB;
+    for (int i = 0; i < BPT; ++i) {
 #pragma unroll
-    for (int v = 0; v < G::VEC; ++v) {
-      uint2 piece;
-      if constexpr (sizeof(T) == 2) {
-        const int w = v >> 1;
-        const int sh = (v & 1) * 16;
-        const uint32_t e0 = (word_of(reg[blk * 4 + 0], w) >> sh) & 0xffffu;
-        const uint32_t e1 = (word_of(reg[blk * 4 + 1], w) >> sh) & 0xffffu;
-        const uint32_t e2 = (word_of(reg[blk * 4 + 2], w) >> sh) & 0xffffu;
-        const uint32_t e3 = (word_of(reg[blk * 4 + 3], w) >> sh) & 0xffffu;
-        piece.x = e0 | (e1 << 16);
-        piece.y = e2 | (e3 << 16);
-        if constexpr (kSum)
-          colsum[v] += (bf16_to_f32(e0) + bf16_to_f32(e1)) + (bf16_to_f32(e2) + bf16_to_f32(e3));
-      } else {
-        piece.x = word_of(reg[blk * 2 + 0], v);
-        piece.y = word_of(reg[blk * 2 + 1], v);
-        if constexpr (kSum) colsum[v] += __uint_as_float(piece.x) + __uint_as_float(piece.y);
+      for (int e = 0; e < 4; ++e) {
+        const int32_t row = srow(k0 + 4 * q_of(i) + e);
+        reg[i][e] = load16(src, static_cast<int64_t>(row) * ld + col, row >= 0 && col < cend);
       }
-      *reinterpret_cast<uint2*>(lds + (cb * G::VEC + v) * kRowBytes + kb * G::TK * sizeof(T)) =
-          piece;
     }
   }
-}
 
-template <typename T>
-__device__ __forceinline__ void compute_step(const char* As, const char* Bs, f32x16_t (&acc)[2][2]) {
+  // optionally adds the staged values into per-column sums colsum[v]
+  template <bool kSum>
+  __device__ __forceinline__ void store(char* lds, float* colsum) const {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int kbase = 4 * q_of(i);
+      const int kp = kbase / VEC;
+      const int boff = (kbase % VEC) * static_cast<int>(sizeof(T));
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) {
+        const int row = cb_of() * VEC + v;
+        char* dst = lds + unit_off<ROWS>(kp, row) + boff;
+        if constexpr (sizeof(T) == 2) {
+          const int w = v >> 1, sh = (v & 1) * 16;
+          const uint32_t e0 = (word_of(reg[i][0], w) >> sh) & 0xffffu;
+          const uint32_t e1 = (word_of(reg[i][1], w) >> sh) & 0xffffu;
+          const uint32_t e2 = (word_of(reg[i][2], w) >> sh) & 0xffffu;
+          const uint32_t e3 = (word_of(reg[i][3], w) >> sh) & 0xffffu;
+          *reinterpret_cast<uint2*>(dst) = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+          if constexpr (kSum)
+            colsum[v] += (bf16_to_f32(e0) + bf16_to_f32(e1)) + (bf16_to_f32(e2) + bf16_to_f32(e3));
+        } else {
+          const uint4 piece = make_uint4(word_of(reg[i][0], v), word_of(reg[i][1], v),
+                                         word_of(reg[i][2], v), word_of(reg[i][3], v));
+          *reinterpret_cast<uint4*>(dst) = piece;
+          if constexpr (kSum)
+            colsum[v] += (__uint_as_float(piece.x) + __uint_as_float(piece.y)) +
+                         (__uint_as_float(piece.z) + __uint_as_float(piece.w));
+        }
+      }
+    }
+  }
+};
+
+template <int MODE, typename T, int WN> struct OperandLoaders;
+template <typename T, int WN> struct OperandLoaders<kModeFwd, T, WN> {
+  using A = DirectLoader<T, BM>;
+  using B = TransLoader<T, Geo<WN>::BN>;
+};
+template <typename T, int WN> struct OperandLoaders<kModeBwdData, T, WN> {
+  using A = DirectLoader<T, BM>;
+  using B = DirectLoader<T, Geo<WN>::BN>;
+};
+template <typename T, int WN> struct OperandLoaders<kModeBwdWeight, T, WN> {
+  using A = TransLoader<T, BM>;
+  using B = TransLoader<T, Geo<WN>::BN>;
+};
+
+// Eight K steps of 16 (bf16) or 8 (fp32) per LDS stage: 4 slices, each one
+// kpack per lane half.  Fragments of slice rs + 1 are read while the MFMAs
+// of slice rs issue.
+template <typename T, int WN>
+__device__ __forceinline__ void compute_step(const char* As, const char* Bs, f32x16_t (&acc)[4][WN]) {
+  constexpr int BN = Geo<WN>::BN;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 31, lh = lane >> 5;
-  const char* a_base = As + (wm * 64 + lr) * kRowBytes + lh * 16;
-  const char* b_base = Bs + (wn * 64 + lr) * kRowBytes + lh * 16;
+  uint4 fa[2][4], fb[2][WN];
+  auto read = [&](int rs, int set) {
+    const int kp = 2 * rs + lh;
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+      fa[set][mi] = *reinterpret_cast<const uint4*>(As + unit_off<BM>(kp, wm * 128 + mi * 32 + lr));
+#pragma unroll
+    for (int ni = 0; ni < WN; ++ni)
+      fb[set][ni] = *reinterpret_cast<const uint4*>(Bs + unit_off<BN>(kp, wn * (32 * WN) + ni * 32 + lr));
+  };
+  read(0, 0);
 #pragma unroll
   for (int rs = 0; rs < 4; ++rs) {
-    const uint4 a0 = *reinterpret_cast<const uint4*>(a_base + rs * 32);
-    const uint4 a1 = *reinterpret_cast<const uint4*>(a_base + 32 * kRowBytes + rs * 32);
-    const uint4 b0 = *reinterpret_cast<const uint4*>(b_base + rs * 32);
-    const uint4 b1 = *reinterpret_cast<const uint4*>(b_base + 32 * kRowBytes + rs * 32);
-    mma(acc[0][0], a0, b0, T());
-    mma(acc[0][1], a0, b1, T());
-    mma(acc[1][0], a1, b0, T());
-    mma(acc[1][1], a1, b1, T());
+    if (rs + 1 < 4) read(rs + 1, (rs + 1) & 1);
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], T());
+  }
+  // Pin the pipeline order for the scheduler: the reads of slice 0 and 1,
+  // then each slice's MFMAs followed by the reads of the slice after next.
+  constexpr int kReads = 4 + WN;
+  constexpr int kMfma = 4 * WN * (sizeof(T) == 2 ? 1 : 4);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * kReads, 0);
+#pragma unroll
+  for (int rs = 0; rs < 4; ++rs) {
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+    if (rs + 2 < 4) __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
   }
 }
 
-// Local row / column of C held by accumulator element e of block (mi, ni).
-__device__ __forceinline__ int acc_row(int mi, int e) {
+// ---- tile iteration ----------------------------------------------------------
+
+struct Tile {
+  int32_t cls, cg, mt, split;
+  int32_t cstart, cend;                          // columns of C
+  int32_t rstart, rend;                          // BWD_WEIGHT: rows of C
+  int32_t seg0_lo, seg0_hi, seg1_lo, seg1_hi;    // K ranges
+  int32_t n0, nsteps;                            // K steps in segment 0, in total
+  int32_t pos0, nrows;                           // FWD/BWD_DATA: rows in perm
+  int32_t do_dbias;
+};
+
+template <int MODE, int LAW, int BN, int BK>
+__device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls, int32_t u,
+                                          int32_t units) {
+  Tile t;
+  const int32_t ru = u % units;
+  const int ct = col_tile_global(p, sel, cls, u / units);
+  int cg = 0;
+  while (ct >= p.NTp[cg + 1]) ++cg;
+  const int nt = ct - p.NTp[cg];
+  t.cls = cls;
+  t.cg = cg;
+  t.seg1_lo = t.seg1_hi = 0;
+  t.rstart = t.rend = 0;
+  t.split = 0;
+  t.do_dbias = 0;
+  t.pos0 = t.nrows = 0;
+  if constexpr (MODE == kModeFwd) {
+    t.mt = ru;
+    t.cstart = p.R[cg] + nt * BN;
+    t.cend = p.R[cg + 1];
+    if (LAW == 1) {
+      t.seg0_lo = 0; t.seg0_hi = p.K;
+    } else {
+      t.seg0_lo = p.S[cg]; t.seg0_hi = p.S[cg + 1];
+      if (cg != cls) { t.seg1_lo = p.S[cls]; t.seg1_hi = p.S[cls + 1]; }
+    }
+  } else if constexpr (MODE == kModeBwdData) {
+    t.mt = ru;
+    t.cstart = p.S[cg] + nt * BN;
+    t.cend = p.S[cg + 1];
+    if (LAW == 1 || cg == cls) {
+      t.seg0_lo = 0; t.seg0_hi = p.N;
+    } else {
+      t.seg0_lo = p.R[cg]; t.seg0_hi = p.R[cg + 1];
+    }
+  } else {
+    t.mt = ru / p.nsplit;
+    t.split = ru % p.nsplit;
+    t.cstart = p.R[cg] + nt * BN;
+    t.cend = p.R[cg + 1];
+    t.rstart = p.S[cls] + t.mt * BM;
+    t.rend = p.S[cls + 1];
+    int32_t lo, hi;
+    if (LAW == 0 && cg != cls) {
+      lo = p.offsets[cls]; hi = p.offsets[cls + 1];
+    } else {
+      lo = 0; hi = p.offsets[p.q];
+    }
+    const int32_t cs = (hi - lo + p.nsplit - 1) / p.nsplit;
+    t.seg0_lo = min(hi, lo + t.split * cs);
+    t.seg0_hi = min(hi, t.seg0_lo + cs);
+    t.do_dbias = (p.dbias != nullptr) && (cg == cls) && (t.mt == 0);
+  }
+  if constexpr (MODE != kModeBwdWeight) {
+    t.pos0 = p.offsets[cls] + t.mt * BM;
+    t.nrows = min(BM, p.offsets[cls + 1] - t.pos0);
+  }
+  t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
+  t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;
+  // every field is uniform over the workgroup: keep it in scalar registers
+  int32_t* f = reinterpret_cast<int32_t*>(&t);
+#pragma unroll
+  for (int k = 0; k < static_cast<int>(sizeof(Tile) / sizeof(int32_t)); ++k)
+    f[k] = __builtin_amdgcn_readfirstlane(f[k]);
+  return t;
+}
+
+// Gathered row indices a thread needs for one FWD/BWD_DATA tile: the rows
+// of its direct A loads and the rows its epilogue writes.
+template <int UPT>
+struct Rows {
+  int32_t a[UPT];
+  int32_t e[4];
+};
+
+template <int UPT>
+__device__ __forceinline__ void fetch_rows(const GemmParams& p, const Tile& t, Rows<UPT>& r) {
   const int lane = threadIdx.x & 63;
   const int wm = (threadIdx.x >> 6) >> 1;
-  return wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-}
-__device__ __forceinline__ int acc_col(int ni) {
-  const int lane = threadIdx.x & 63;
-  const int wn = (threadIdx.x >> 6) & 1;
-  return wn * 64 + ni * 32 + (lane & 31);
+#pragma unroll
+  for (int i = 0; i < UPT; ++i) {
+    const int row = (threadIdx.x + THREADS * i) >> 3;
+    r.a[i] = row < t.nrows ? p.perm[t.pos0 + row] : -1;
+  }
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi) {
+    const int row = wm * 128 + mi * 32 + (lane & 31);
+    r.e[mi] = row < t.nrows ? p.perm[t.pos0 + row] : -1;
+  }
 }
 
-template <typename T, int MODE>
-__global__ __launch_bounds__(kThreads, 2) void star_gemm_kernel(const GemmParams p) {
-  constexpr int BK = Traits<T>::BK;
-  __shared__ __attribute__((aligned(16))) char smem[kSmemBytes];
-  __shared__ int32_t rows_s[BM];
+template <typename T, int MODE, int LAW, int WN>
+__global__ __launch_bounds__(THREADS, 1) void star_gemm_kernel(const GemmParams p) {
+  using G = Geo<WN>;
+  using LA = typename OperandLoaders<MODE, T, WN>::A;
+  using LB = typename OperandLoaders<MODE, T, WN>::B;
+  constexpr int BK = Tr<T>::BK;
+  constexpr int BN = G::BN;
+  constexpr int VEC = Tr<T>::VEC;
+  constexpr int UPT = DirectLoader<T, BM>::UPT;  // row ids of the gathered A rows
+  constexpr int BUPT = DirectLoader<T, BN>::UPT;   // BWD_DATA: rows of W per thread
+  extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int32_t units_s[kMaxQGroups];
-  __shared__ int32_t pfx_s[kMaxQGroups + 1];
+  __shared__ int32_t pfx_s[2][kMaxQGroups + 1];
 
-  auto As = [&](int buf) { return smem + buf * kTileBytes; };
-  auto Bs = [&](int buf) { return smem + (2 + buf) * kTileBytes; };
+  auto As = [&](int buf) { return smem + buf * G::STAGE; };
+  auto Bs = [&](int buf) { return smem + buf * G::STAGE + G::A_BYTES; };
   const T* __restrict__ Ag = static_cast<const T*>(p.A);
   const T* __restrict__ Bg = static_cast<const T*>(p.B);
   const int q = p.q;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lr = lane & 31, lh = lane >> 5;
 
-  // row units per class: row tiles of I_i (FWD, BWD_DATA) or row tiles of
-  // input group g times the split count (BWD_WEIGHT)
-  for (int i = threadIdx.x; i < q; i += kThreads) {
+  for (int i = threadIdx.x; i < q; i += THREADS) {
     if constexpr (MODE == kModeBwdWeight) {
       units_s[i] = (p.MTp[i + 1] - p.MTp[i]) * p.nsplit;
     } else {
@@ -262,242 +488,256 @@ __global__ __launch_bounds__(kThreads, 2) void star_gemm_kernel(const GemmParams
       units_s[i] = (mi + BM - 1) / BM;
     }
   }
-
-  const int xcd = blockIdx.x & 7;
-  const int slot0 = blockIdx.x >> 3;
-  const int slot_stride = gridDim.x >> 3;
-
-  for (int pass = 0; pass < 2; ++pass) {
-    const int sel = sel_for(MODE, p.law, pass);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int32_t run = 0;
-      for (int i = 0; i < q; ++i) {
-        pfx_s[i] = run;
-        run += units_s[i] * ncols_sel(p, sel, i);
-      }
-      pfx_s[q] = run;
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    const int sel = sel_for(MODE, LAW, threadIdx.x);
+    int32_t run = 0;
+    for (int i = 0; i < q; ++i) {
+      pfx_s[threadIdx.x][i] = run;
+      run += units_s[i] * ncols_sel(p, sel, i);
     }
-    __syncthreads();
-    const int32_t total = pfx_s[q];
-    const int32_t chunk = (total + 7) >> 3;
+    pfx_s[threadIdx.x][q] = run;
+  }
+  __syncthreads();
 
-    for (int32_t slot = slot0; slot < chunk; slot += slot_stride) {
-      const int32_t logical = xcd * chunk + slot;
-      if (logical >= total) break;
+  // ---- this workgroup's tile sequence ----
+  const int xcd = blockIdx.x & 7;
+  const int slot_stride = gridDim.x >> 3;
+  int it_pass = 0;
+  int32_t it_slot = blockIdx.x >> 3;
+
+  // zero tile of a weight-gradient split with an empty row range
+  auto write_zero_tile = [&](const Tile& t) {
+    float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(t.split) * p.K * p.N : p.dW;
+    for (int idx = threadIdx.x; idx < BM * BN / 4; idx += THREADS) {
+      const int32_t r = t.rstart + idx / (BN / 4);
+      const int32_t c = t.cstart + (idx % (BN / 4)) * 4;
+      if (r < t.rend && c < t.cend)
+        *reinterpret_cast<float4*>(out + static_cast<int64_t>(r) * p.N + c) = make_float4(0, 0, 0, 0);
+    }
+    if (t.do_dbias) {
+      for (int c = threadIdx.x; c < BN; c += THREADS) {
+        const int32_t gc = t.cstart + c;
+        if (gc < t.cend) {
+          if (p.nsplit > 1) p.dbias_part[static_cast<int64_t>(t.split) * p.N + gc] = 0.f;
+          else p.dbias[gc] = 0.f;
+        }
+      }
+    }
+  };
+
+  auto advance = [&](Tile& t) -> bool {
+    while (it_pass < 2) {
+      const int32_t total = pfx_s[it_pass][q];
+      const int32_t chunk = (total + 7) >> 3;
+      const int32_t logical = xcd * chunk + it_slot;
+      if (it_slot >= chunk || logical >= total) {
+        ++it_pass;
+        it_slot = blockIdx.x >> 3;
+        continue;
+      }
+      it_slot += slot_stride;
       int cls = 0;
-      while (logical >= pfx_s[cls + 1]) ++cls;
-      const int32_t u = logical - pfx_s[cls];
-      const int32_t ru = u % units_s[cls];
-      const int ct = col_tile_global(p, sel, cls, u / units_s[cls]);
-      int cg = 0;
-      while (ct >= p.NTp[cg + 1]) ++cg;
-      const int nt = ct - p.NTp[cg];
-
-      // ---- tile geometry -------------------------------------------------
-      int32_t cstart, cend;          // columns of C (global index space)
-      int32_t seg0_lo = 0, seg0_hi = 0, seg1_lo = 0, seg1_hi = 0;  // K ranges
-      int32_t rstart = 0, rend = 0;  // BWD_WEIGHT: rows of C (kk)
-      int32_t split = 0, mt;
-      bool do_dbias = false;
-      if constexpr (MODE == kModeFwd) {
-        mt = ru;
-        cstart = p.R[cg] + nt * BN;
-        cend = p.R[cg + 1];
-        if (p.law == 1) {
-          seg0_lo = 0; seg0_hi = p.K;
-        } else {
-          seg0_lo = p.S[cg]; seg0_hi = p.S[cg + 1];
-          if (cg != cls) { seg1_lo = p.S[cls]; seg1_hi = p.S[cls + 1]; }
-        }
-      } else if constexpr (MODE == kModeBwdData) {
-        mt = ru;
-        cstart = p.S[cg] + nt * BN;
-        cend = p.S[cg + 1];
-        if (p.law == 1 || cg == cls) {
-          seg0_lo = 0; seg0_hi = p.N;
-        } else {
-          seg0_lo = p.R[cg]; seg0_hi = p.R[cg + 1];
-        }
-      } else {
-        mt = ru / p.nsplit;
-        split = ru % p.nsplit;
-        cstart = p.R[cg] + nt * BN;
-        cend = p.R[cg + 1];
-        rstart = p.S[cls] + mt * BM;
-        rend = p.S[cls + 1];
-        int32_t lo, hi;
-        if (p.law == 0 && cg != cls) {
-          lo = p.offsets[cls]; hi = p.offsets[cls + 1];
-        } else {
-          lo = 0; hi = p.offsets[q];
-        }
-        const int32_t len = hi - lo;
-        const int32_t cs = (len + p.nsplit - 1) / p.nsplit;
-        seg0_lo = min(hi, lo + split * cs);
-        seg0_hi = min(hi, seg0_lo + cs);
-        do_dbias = (p.dbias != nullptr) && (cg == cls) && (mt == 0);
+      while (logical >= pfx_s[it_pass][cls + 1]) ++cls;
+      const int sel = sel_for(MODE, LAW, it_pass);
+      t = make_tile<MODE, LAW, BN, BK>(p, sel, cls, logical - pfx_s[it_pass][cls], units_s[cls]);
+      if (t.nsteps == 0) {  // only weight-gradient splits can be empty
+        write_zero_tile(t);
+        continue;
       }
-      const int32_t n0 = (seg0_hi - seg0_lo + BK - 1) / BK;
-      const int32_t n1 = (seg1_hi - seg1_lo + BK - 1) / BK;
-      const int32_t nsteps = n0 + n1;
+      return true;
+    }
+    return false;
+  };
 
-      __syncthreads();  // previous tile is done with rows_s and LDS
-      if constexpr (MODE != kModeBwdWeight) {
-        const int32_t pos0 = p.offsets[cls] + mt * BM;
-        const int32_t nrows = min(BM, p.offsets[cls + 1] - pos0);
-        if (threadIdx.x < BM) rows_s[threadIdx.x] = threadIdx.x < nrows ? p.perm[pos0 + threadIdx.x] : -1;
+  Tile cur, nxt;
+  if (!advance(cur)) return;
+  bool has_nxt = advance(nxt);
+  Rows<UPT> rc, rn;
+  if constexpr (MODE != kModeBwdWeight) {
+    fetch_rows(p, cur, rc);
+    if (has_nxt) fetch_rows(p, nxt, rn);
+  }
+  int32_t brow[BUPT];
+  float colsum[VEC], colsum_n[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) colsum[v] = colsum_n[v] = 0.f;
+
+  LA la;
+  LB lb;
+  // stage s of tile t into the loader registers
+  auto load_stage = [&](const Tile& t, const Rows<UPT>& r, int32_t s) {
+    int32_t k0, kend;
+    if (s < t.n0) { k0 = t.seg0_lo + s * BK; kend = t.seg0_hi; }
+    else { k0 = t.seg1_lo + (s - t.n0) * BK; kend = t.seg1_hi; }
+    if constexpr (MODE == kModeFwd) {
+      la.load(Ag, p.K, r.a, k0, kend);
+      lb.load(Bg, p.N, k0, t.cstart, t.cend, [&](int32_t k) { return k < kend ? k : -1; });
+    } else if constexpr (MODE == kModeBwdData) {
+#pragma unroll
+      for (int i = 0; i < BUPT; ++i) {
+        const int32_t kk = t.cstart + DirectLoader<T, BN>::row_of(i);
+        brow[i] = kk < t.cend ? kk : -1;
       }
-      __syncthreads();
+      la.load(Ag, p.N, r.a, k0, kend);
+      lb.load(Bg, p.N, brow, k0, kend);
+    } else {
+      const int32_t* __restrict__ perm = p.perm;
+      auto srow = [&](int32_t k) { return k < kend ? perm[k] : -1; };
+      la.load(Ag, p.K, k0, t.rstart, t.rend, srow);
+      lb.load(Bg, p.N, k0, t.cstart, t.cend, srow);
+    }
+  };
+  auto store_stage = [&](int buf, bool dbias, float* cs) {
+    if constexpr (MODE == kModeFwd) {
+      la.store(As(buf));
+      lb.template store<false>(Bs(buf), cs);
+    } else if constexpr (MODE == kModeBwdData) {
+      la.store(As(buf));
+      lb.store(Bs(buf));
+    } else {
+      la.template store<false>(As(buf), cs);
+      if (dbias) lb.template store<true>(Bs(buf), cs);
+      else lb.template store<false>(Bs(buf), cs);
+    }
+  };
 
-      int32_t arow[4];
-      int32_t brow[4];
-      if constexpr (MODE != kModeBwdWeight) {
+  load_stage(cur, rc, 0);
+  store_stage(0, cur.do_dbias, colsum);  // colsum starts at zero
+  __syncthreads();
+
+  int buf = 0;
+  while (true) {
+    f32x16_t acc[4][WN];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) arow[u] = rows_s[(threadIdx.x >> 3) + 32 * u];
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
+
+    for (int32_t s = 0; s < cur.nsteps; ++s) {
+      // the next stage: step s + 1 of this tile, or step 0 of the next one
+      const bool more = s + 1 < cur.nsteps;
+      const bool next_stage = more || has_nxt;
+      const Tile lt = more ? cur : nxt;
+      if (next_stage) {
+        Rows<UPT> lrow;
+#pragma unroll
+        for (int i = 0; i < UPT; ++i) lrow.a[i] = more ? rc.a[i] : rn.a[i];
+        load_stage(lt, lrow, more ? s + 1 : 0);
       }
-      if constexpr (MODE == kModeBwdData) {
+      compute_step<T, WN>(As(buf), Bs(buf), acc);
+      if (next_stage) {
+        float cs[VEC];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int32_t kk = cstart + (threadIdx.x >> 3) + 32 * u;
-          brow[u] = kk < cend ? kk : -1;
-        }
-      }
-
-      float colsum[8];
+        for (int v = 0; v < VEC; ++v) cs[v] = 0.f;
+        store_stage(buf ^ 1, lt.do_dbias, cs);
+        if constexpr (MODE == kModeBwdWeight) {
 #pragma unroll
-      for (int v = 0; v < 8; ++v) colsum[v] = 0.f;
-
-      auto step_range = [&](int32_t s, int32_t& k0, int32_t& kend) {
-        if (s < n0) { k0 = seg0_lo + s * BK; kend = seg0_hi; }
-        else { k0 = seg1_lo + (s - n0) * BK; kend = seg1_hi; }
-      };
-
-      uint4 ra[4], rb[4];
-      auto load_stage = [&](int32_t s) {
-        int32_t k0, kend;
-        step_range(s, k0, kend);
-        if constexpr (MODE == kModeFwd) {
-          load_k<T>(ra, Ag, p.K, arow, k0, kend);
-          load_t<T>(rb, Bg, p.N, k0, cstart, cend,
-                    [&](int32_t k) { return k < kend ? k : -1; });
-        } else if constexpr (MODE == kModeBwdData) {
-          load_k<T>(ra, Ag, p.N, arow, k0, kend);
-          load_k<T>(rb, Bg, p.N, brow, k0, kend);
-        } else {
-          const int32_t* __restrict__ perm = p.perm;
-          auto srow = [&](int32_t k) { return k < kend ? perm[k] : -1; };
-          load_t<T>(ra, Ag, p.K, k0, rstart, rend, srow);
-          load_t<T>(rb, Bg, p.N, k0, cstart, cend, srow);
-        }
-      };
-      auto store_stage = [&](int buf) {
-        if constexpr (MODE == kModeFwd) {
-          store_k(As(buf), ra);
-          store_t<T, false>(Bs(buf), rb, colsum);
-        } else if constexpr (MODE == kModeBwdData) {
-          store_k(As(buf), ra);
-          store_k(Bs(buf), rb);
-        } else {
-          store_t<T, false>(As(buf), ra, colsum);
-          if (do_dbias) store_t<T, true>(Bs(buf), rb, colsum);
-          else store_t<T, false>(Bs(buf), rb, colsum);
-        }
-      };
-
-      f32x16_t acc[2][2];
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
-
-      if (nsteps > 0) {
-        load_stage(0);
-        store_stage(0);
-        __syncthreads();
-        for (int32_t s = 0; s < nsteps; ++s) {
-          if (s + 1 < nsteps) load_stage(s + 1);
-          compute_step<T>(As(s & 1), Bs(s & 1), acc);
-          if (s + 1 < nsteps) store_stage((s + 1) & 1);
-          __syncthreads();
-        }
-      }
-
-      // ---- epilogue --------------------------------------------------------
-      if constexpr (MODE == kModeFwd) {
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int32_t gcol = cstart + acc_col(ni);
-          if (gcol >= cend) continue;
-          const float bv = p.bias ? p.bias[gcol] : 0.f;
-#pragma unroll
-          for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int32_t grow = rows_s[acc_row(mi, e)];
-              if (grow < 0) continue;
-              const float z = acc[mi][ni][e] + bv;
-              const int64_t idx = static_cast<int64_t>(grow) * p.N + gcol;
-              if (p.Z) store_out(p.Z, p.ydtype, idx, z);
-              store_out(p.Y, p.ydtype, idx, act_fwd(p.act, z));
-            }
-        }
-      } else if constexpr (MODE == kModeBwdData) {
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int32_t gcol = cstart + acc_col(ni);
-          if (gcol >= cend) continue;
-#pragma unroll
-          for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int32_t grow = rows_s[acc_row(mi, e)];
-              if (grow < 0) continue;
-              const int64_t idx = static_cast<int64_t>(grow) * p.K + gcol;
-              float v = acc[mi][ni][e];
-              if (p.Zprev) v *= act_grad(p.act, load_in(p.Zprev, p.elem == 0 ? 0 : 1, idx));
-              store_out(p.Y, p.ydtype, idx, v);
-            }
-        }
-      } else {
-        float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(split) * p.K * p.N : p.dW;
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int32_t gcol = cstart + acc_col(ni);
-          if (gcol >= cend) continue;
-#pragma unroll
-          for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int32_t grow = rstart + acc_row(mi, e);
-              if (grow >= rend) continue;
-              out[static_cast<int64_t>(grow) * p.N + gcol] = acc[mi][ni][e];
-            }
-        }
-        if (do_dbias) {
-          // column sums of the staged dY: thread t holds column chunk
-          // t % CB; reduce over the threads sharing it through LDS.
-          using G = TGeom<T>;
-          constexpr int kSlots = kThreads / G::CB;
-          float* red = reinterpret_cast<float*>(smem);
-          const int cb = threadIdx.x % G::CB;
-          const int slotr = threadIdx.x / G::CB;
-#pragma unroll
-          for (int v = 0; v < G::VEC; ++v) red[slotr * BN + cb * G::VEC + v] = colsum[v];
-          __syncthreads();
-          if (threadIdx.x < BN) {
-            float sum = 0.f;
-            for (int sl = 0; sl < kSlots; ++sl) sum += red[sl * BN + threadIdx.x];
-            const int32_t gcol = cstart + threadIdx.x;
-            if (gcol < cend) {
-              if (p.nsplit > 1) p.dbias_part[static_cast<int64_t>(split) * p.N + gcol] = sum;
-              else p.dbias[gcol] = sum;
-            }
+          for (int v = 0; v < VEC; ++v) {
+            colsum[v] += more ? cs[v] : 0.f;
+            colsum_n[v] += more ? 0.f : cs[v];
           }
         }
       }
+      __syncthreads();
+      buf ^= 1;
+    }
+    // `buf` now holds the next tile's first stage; `buf ^ 1` is free until
+    // the next store into it
+
+    // ---- epilogue of `cur` ----
+    // lane holds C[row m][columns n .. n+3] with m = wm*128 + mi*32 + lr and
+    // n = wn*32*WN + ni*32 + 8a + 4lh, values acc[mi][ni][4a .. 4a+3]
+    if constexpr (MODE == kModeFwd || MODE == kModeBwdData) {
+      const int64_t ldc = (MODE == kModeFwd) ? p.N : p.K;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) {
+        const int32_t grow = rc.e[mi];
+        if (grow < 0) continue;
+#pragma unroll
+        for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const int32_t gcol = cur.cstart + wn * (32 * WN) + ni * 32 + 8 * a + 4 * lh;
+            if (gcol >= cur.cend) continue;
+            const int64_t idx = static_cast<int64_t>(grow) * ldc + gcol;
+            float v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = acc[mi][ni][4 * a + j];
+            if constexpr (MODE == kModeFwd) {
+              if (p.bias) {
+                const float4 bv = *reinterpret_cast<const float4*>(p.bias + gcol);
+                v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+              }
+              if (p.Z) store4(p.Z, p.ydtype, idx, v);
+              if (p.act != kActNone) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v[j] = act_apply(p.act, v[j]);
+              }
+            } else {
+              if (p.Zprev) {
+                float z[4];
+                load4(p.Zprev, p.elem == 0 ? 0 : 1, idx, z);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v[j] *= act_deriv(p.act, z[j]);
+              }
+            }
+            store4(p.Y, p.ydtype, idx, v);
+          }
+      }
+    } else {
+      float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(cur.split) * p.K * p.N : p.dW;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) {
+        const int32_t grow = cur.rstart + wm * 128 + mi * 32 + lr;
+        if (grow >= cur.rend) continue;
+#pragma unroll
+        for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const int32_t gcol = cur.cstart + wn * (32 * WN) + ni * 32 + 8 * a + 4 * lh;
+            if (gcol >= cur.cend) continue;
+            *reinterpret_cast<float4*>(out + static_cast<int64_t>(grow) * p.N + gcol) =
+                make_float4(acc[mi][ni][4 * a], acc[mi][ni][4 * a + 1], acc[mi][ni][4 * a + 2],
+                            acc[mi][ni][4 * a + 3]);
+          }
+      }
+      if (cur.do_dbias) {
+        // column sums of the staged dY: a thread keeps one column chunk;
+        // reduce over the threads sharing it through LDS (free stage buffer)
+        constexpr int kSlots = THREADS / LB::CB;
+        float* red = reinterpret_cast<float*>(As(buf ^ 1));
+        const int cb = LB::cb_of();
+        const int slotr = threadIdx.x / LB::CB;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) red[slotr * BN + cb * VEC + v] = colsum[v];
+        __syncthreads();
+        for (int c = threadIdx.x; c < BN; c += THREADS) {
+          float sum = 0.f;
+          for (int sl = 0; sl < kSlots; ++sl) sum += red[sl * BN + c];
+          const int32_t gcol = cur.cstart + c;
+          if (gcol < cur.cend) {
+            if (p.nsplit > 1) p.dbias_part[static_cast<int64_t>(cur.split) * p.N + gcol] = sum;
+            else p.dbias[gcol] = sum;
+          }
+        }
+        __syncthreads();
+      }
+    }
+
+    if (!has_nxt) break;
+    cur = nxt;
+    rc = rn;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+      colsum[v] = colsum_n[v];
+      colsum_n[v] = 0.f;
+    }
+    has_nxt = advance(nxt);
+    if constexpr (MODE != kModeBwdWeight) {
+      if (has_nxt) fetch_rows(p, nxt, rn);
     }
   }
 }
@@ -529,23 +769,40 @@ __global__ void fill_zero_kernel(float* __restrict__ dst, int64_t n) {
     dst[i] = 0.f;
 }
 
-template <typename T, int MODE>
+template <typename T, int MODE, int WN>
 hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((star_gemm_kernel<T, MODE>), dim3(grid), dim3(kThreads), 0, stream, p);
+  using G = Geo<WN>;
+  auto kern = (p.law == 1) ? star_gemm_kernel<T, MODE, 1, WN> : star_gemm_kernel<T, MODE, 0, WN>;
+  // allow more than the default dynamic LDS once per kernel (idempotent)
+  static const hipError_t attr = [] {
+    hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 0, WN>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
+    if (a != hipSuccess) return a;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
+  }();
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(THREADS), G::SMEM, stream, p);
   return hipGetLastError();
+}
+
+template <int MODE, int WN>
+hipError_t launch_mode(const GemmParams& p, int grid, hipStream_t stream) {
+  if (p.elem == 1) return launch_typed<uint16_t, MODE, WN>(p, grid, stream);
+  return launch_typed<float, MODE, WN>(p, grid, stream);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int mode, const GemmParams& p, int grid, hipStream_t stream) {
-  if (p.elem == 1) {
-    if (mode == kModeFwd) return launch_typed<uint16_t, kModeFwd>(p, grid, stream);
-    if (mode == kModeBwdData) return launch_typed<uint16_t, kModeBwdData>(p, grid, stream);
-    return launch_typed<uint16_t, kModeBwdWeight>(p, grid, stream);
+hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream) {
+  if (nw == 4) {
+    if (mode == kModeFwd) return launch_mode<kModeFwd, 4>(p, grid, stream);
+    if (mode == kModeBwdData) return launch_mode<kModeBwdData, 4>(p, grid, stream);
+    return launch_mode<kModeBwdWeight, 4>(p, grid, stream);
   }
-  if (mode == kModeFwd) return launch_typed<float, kModeFwd>(p, grid, stream);
-  if (mode == kModeBwdData) return launch_typed<float, kModeBwdData>(p, grid, stream);
-  return launch_typed<float, kModeBwdWeight>(p, grid, stream);
+  if (mode == kModeFwd) return launch_mode<kModeFwd, 2>(p, grid, stream);
+  if (mode == kModeBwdData) return launch_mode<kModeBwdData, 2>(p, grid, stream);
+  return launch_mode<kModeBwdWeight, 2>(p, grid, stream);
 }
 
 hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream) {

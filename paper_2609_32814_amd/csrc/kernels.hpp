@@ -54,16 +54,15 @@ hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* per
 hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
                                   unsigned long long* n_bad, hipStream_t stream);
 
-// Grid size (workgroups) of the persistent GEMM for a given mode.
-hipError_t launch_gemm(int mode, const GemmParams& p, int grid, hipStream_t stream);
+// Persistent grouped GEMM: tiles of kTileM rows x (64 * nw) columns
+// (nw = 2 or 4), `grid` workgroups of 128 * nw threads.
+hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream);
 hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
 // Zero-fills n floats with a kernel (safe to record in a HIP graph).
 hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream);
 
-// Tile sizes of the GEMM (rows and columns of C per workgroup).
-constexpr int kTileM = 128;
-constexpr int kTileN = 128;
-constexpr int kGemmThreads = 256;
+// Rows of C per GEMM tile.
+constexpr int kTileM = 256;
 
 // ---- decode ----------------------------------------------------------------
 

@@ -376,3 +376,21 @@ def test_cfg3_full_size_sampled(P):
         assert rel_fro(to_host(dW)[kk, nn], ref) <= TOL_BF16
         assert rel_fro(to_host(db), B.exact.sum(0)) <= TOL_BF16
     torch.cuda.empty_cache()
+
+
+def test_planned_entry_points_match(P):
+    """A plan built once and reused gives the same bits as the plain calls."""
+    import torch
+    ga, oa = algs(P, 3, [64, 32, 32], [96, 64, 32])
+    M = 700
+    X = to_dev(synth.gaussian(12, 0, (M, oa.K), 1.0, "bf16"))
+    W = to_dev(synth.gaussian(12, 1, (oa.K, oa.N), 0.05, "bf16"))
+    dY = to_dev(synth.gaussian(12, 2, (M, oa.N), 1.0, "bf16"))
+    t = types_dev(np.random.default_rng([12, 3]).integers(0, 3, M).astype(np.int32))
+    plan = P.star_type_plan(3, t)
+    assert torch.equal(P.star_proj_fwd(ga, t, X, W, act="gelu"),
+                       P.star_proj_fwd_planned(ga, plan, X, W, act="gelu"))
+    assert torch.equal(P.star_proj_bwd_data(ga, t, dY, W), P.star_proj_bwd_data_planned(ga, plan, dY, W))
+    a, b = P.star_proj_bwd_weight(ga, t, X, dY)
+    c, d = P.star_proj_bwd_weight_planned(ga, plan, X, dY)
+    assert torch.equal(a, c) and torch.equal(b, d)
