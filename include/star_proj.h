@@ -179,7 +179,9 @@ star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64
  * where a is h rounded to bfloat16 and h starts as X and is carried in FP32
  * (without `residual` the FFN output replaces h).  The hidden activation is
  * stored in bfloat16.  This is a skinny, weight-bandwidth-bound product: every
- * weight block that some row's support reaches is read once per step.
+ * weight block that some row's support reaches is read once per step, and a
+ * block no row's support reaches is not read.  D and F must be at most 4096
+ * (STAR_ERR_UNSUPPORTED otherwise); M at most 64.
  *   row_type  device int32[M]
  *   X         device bf16 [M, D]
  *   W_up, W_down, b_up, b_down: host arrays of n_layers device pointers

@@ -129,19 +129,10 @@ BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
 }
 
 struct DecodeWs {
-  size_t h = 0, xb = 0, H = 0, partial = 0, counters = 0, end = 0;
-  int nt_up = 0, nt_down = 0, nk_up = 0, nk_down = 0;
+  size_t h = 0, xb = 0, H = 0, end = 0;
 };
-DecodeWs decode_layout(const Alg& up, const Alg& down, int64_t M) {
+DecodeWs decode_layout(const Alg& up, int64_t M) {
   DecodeWs w;
-  for (int g = 0; g < up.q; ++g) {
-    w.nt_up += tiles_of(up.r(g), kDecodeTileN);
-    w.nk_up += tiles_of(up.s(g), kDecodeChunkK);
-  }
-  for (int g = 0; g < down.q; ++g) {
-    w.nt_down += tiles_of(down.r(g), kDecodeTileN);
-    w.nk_down += tiles_of(down.s(g), kDecodeChunkK);
-  }
   const int64_t D = up.K(), F = up.N();
   size_t cur = 0;
   w.h = cur;
@@ -150,12 +141,6 @@ DecodeWs decode_layout(const Alg& up, const Alg& down, int64_t M) {
   cur = align_up(cur + sizeof(uint16_t) * M * D);
   w.H = cur;
   cur = align_up(cur + sizeof(uint16_t) * M * F);
-  w.partial = cur;
-  const int64_t part = std::max<int64_t>(static_cast<int64_t>(w.nk_up) * F,
-                                         static_cast<int64_t>(w.nk_down) * D);
-  cur = align_up(cur + sizeof(float) * kDecodeMaxRows * part);
-  w.counters = cur;
-  cur = align_up(cur + sizeof(int32_t) * (w.nt_up + w.nt_down));
   w.end = cur;
   return w;
 }
@@ -282,7 +267,7 @@ size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_alge
     case STAR_OP_DECODE: {
       Alg d;
       if (parse_alg(alg2, d) != STAR_OK) return 0;
-      return decode_layout(a, d, std::min<int64_t>(M, kDecodeMaxRows)).end;
+      return decode_layout(a, std::min<int64_t>(M, kDecodeMaxRows)).end;
     }
     default:
       return 0;
@@ -555,7 +540,7 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
   st = parse_alg(down, d);
   if (st != STAR_OK) return st;
   if (d.K() != u.N() || d.N() != u.K()) return STAR_ERR_SHAPE;
-  if (M > kDecodeMaxRows) return STAR_ERR_UNSUPPORTED;
+  if (M > kDecodeMaxRows || u.K() > kDecodeMaxK || u.N() > kDecodeMaxK) return STAR_ERR_UNSUPPORTED;
   if (n_layers < 1) return STAR_ERR_ARG;
   if (!valid_dtype(yt)) return STAR_ERR_DTYPE;
   if (!valid_act(act)) return STAR_ERR_ARG;
@@ -565,22 +550,16 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
   for (int l = 0; l < n_layers; ++l) {
     if (!W_up[l] || !W_down[l]) return STAR_ERR_ARG;
     if (!aligned16(W_up[l]) || !aligned16(W_down[l])) return STAR_ERR_ALIGN;
-    if ((b_up && b_up[l] && !aligned4(b_up[l])) || (b_down && b_down[l] && !aligned4(b_down[l])))
+    if ((b_up && b_up[l] && !aligned16(b_up[l])) || (b_down && b_down[l] && !aligned16(b_down[l])))
       return STAR_ERR_ALIGN;
   }
-  const DecodeWs dw = decode_layout(u, d, M);
+  const DecodeWs dw = decode_layout(u, M);
   if (!ws || ws_bytes < dw.end) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
 
   float* h = at<float>(ws, dw.h);
   uint16_t* xb = at<uint16_t>(ws, dw.xb);
   uint16_t* Hb = at<uint16_t>(ws, dw.H);
-  float* part = at<float>(ws, dw.partial);
-  int32_t* cnt = at<int32_t>(ws, dw.counters);
-  st = hip_status(launch_decode_init(static_cast<const uint16_t*>(X), M * u.K(), h, xb, cnt,
-                                     dw.nt_up + dw.nt_down, stream));
-  if (st != STAR_OK) return st;
-
   auto fill = [&](DecodePhase& p, const Alg& a) {
     std::memset(&p, 0, sizeof(p));
     p.q = a.q;
@@ -593,9 +572,7 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
       p.R[g] = static_cast<int32_t>(a.R[g]);
     }
     fill_tiles(p.NTp, a.R, a.q, kDecodeTileN);
-    fill_tiles(p.KCp, a.S, a.q, kDecodeChunkK);
     p.types = row_type;
-    p.partial = part;
     p.act = act;
     p.residual = residual;
   };
@@ -603,22 +580,23 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
   fill(pu, u);
   fill(pd, d);
   pu.mode = 0;
-  pu.A = xb;
   pu.out_bf16 = Hb;
-  pu.counters = cnt;
   pd.mode = 1;
   pd.A = Hb;
-  pd.h = h;
-  pd.counters = cnt + dw.nt_up;
   pd.ydtype = yt;
   for (int l = 0; l < n_layers; ++l) {
+    const bool first = (l == 0), last = (l == n_layers - 1);
+    pu.A = first ? static_cast<const uint16_t*>(X) : xb;
     pu.W = static_cast<const uint16_t*>(W_up[l]);
     pu.bias = b_up ? b_up[l] : nullptr;
     st = hip_status(launch_decode_phase(pu, stream));
     if (st != STAR_OK) return st;
     pd.W = static_cast<const uint16_t*>(W_down[l]);
     pd.bias = b_down ? b_down[l] : nullptr;
-    const bool last = (l == n_layers - 1);
+    // h_prev: X itself for the first layer, the fp32 state afterwards
+    pd.h_init = first ? static_cast<const uint16_t*>(X) : nullptr;
+    pd.h_in = first ? nullptr : h;
+    pd.h_out = last ? nullptr : h;
     pd.out_bf16 = last ? nullptr : xb;
     pd.Y = last ? Y : nullptr;
     st = hip_status(launch_decode_phase(pd, stream));

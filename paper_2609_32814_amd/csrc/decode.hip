@@ -1,25 +1,30 @@
 // Decode-step projection for few rows (one new token per sequence, M <= 64).
 //
 // Single-token FFN decode is a matrix-vector problem bound by weight
-// bandwidth (Sec. 4.2 notes decode needs its own implementation; Sec. 5.3).
-// The batched kernel's per-type gathering would read a shared diagonal block
-// once per row type present; here every weight block that some row's
-// support reaches is streamed exactly once per step instead, and rows whose
-// support skips the block multiply zeros.
+// bandwidth (Sec. 4.2 notes that decode needs its own implementation;
+// Sec. 5.3).  The batched kernel's per-type gathering would read a shared
+// diagonal block once per row type present; here every weight block that
+// some row's support reaches is streamed exactly once per step, and rows
+// whose support skips the block multiply zeros.
 //
-// Grid: (column tiles of 64 outputs within an output group j) x (K chunks of
-// 128 inputs within an input group g).  A workgroup
-//  1. decides which of the M rows need block (g, j): k = g in B(t_b, j);
-//     if none does, the chunk is skipped and its weights are never read;
-//  2. stages its rows' inputs (masked per row) and the 128 x 64 weight tile
-//     (transposed in registers) in LDS;
-//  3. multiplies with v_mfma_f32_32x32x16_bf16 (64 x 64 x 128 per tile);
-//  4. writes an fp32 partial, then counts itself done on the column tile's
-//     counter.  The last workgroup to finish a column tile sums the partials
-//     of its non-skipped chunks in chunk order (deterministic), adds the
-//     bias, and applies the phase's epilogue: H = bf16(act(z)) for the up
-//     projection; h += z (or h = z), a = bf16(h) for the down projection.
-// There is no waiting on other workgroups, so no workgroup can stall.
+// A workgroup owns 16 output columns (inside one output group j) over the
+// whole K range, so no partial sums cross workgroups and no workgroup ever
+// waits on another (a kernel boundary separates dependent phases).  K is cut
+// into 32-row slices; a slice is needed when some row's support reaches one
+// of its input groups (k in B(t_b, j)).  Each of the 4 wavefronts streams
+// every fourth needed slice straight from global memory into LDS with one
+// 16-byte-per-lane direct load (32 rows x 32 bytes = 1 KB per slice), all
+// issued before any is consumed, so the whole weight tile is in flight at
+// once.  The wavefront then reads each slice back with the LDS transpose
+// read (two reads give every lane 8 consecutive K values of one column),
+// loads the rows' 8-element input pieces (zero where the support skips
+// them), and multiplies with v_mfma_f32_16x16x32_bf16.  The four
+// wavefronts' partial sums are added in LDS in a fixed order, then the bias,
+// activation or residual are applied and the outputs written.
+//
+// Column tiles are mapped to workgroups so that the four tiles sharing a
+// 128-byte line of a weight row run on the same XCD (workgroups are
+// dispatched round-robin over the 8 XCDs) and share one L2 fetch.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -28,178 +33,215 @@ namespace starq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int TN = kDecodeTileN;    // 64 output columns
-constexpr int TKc = kDecodeChunkK;  // 128 inputs
-constexpr int MR = kDecodeMaxRows;  // 64 rows
-constexpr int kRowBytes = TKc * 2 + 16;  // 272
+constexpr int TN = kDecodeTileN;      // 16 output columns
+constexpr int SLICE = kDecodeSliceK;  // 32 K rows
+constexpr int MR = kDecodeMaxRows;    // 64 rows
+constexpr int kRedBytes = 4 * 4 * 64 * 16;  // 4 waves x 4 row blocks x 64 lanes x float4
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+#define STARQ_LDS __attribute__((address_space(3)))
 
 __device__ __forceinline__ bool in_support(int law, int i, int j, int k) {
   return law == 1 || k == i || k == j;
 }
 
-__device__ __forceinline__ uint32_t word_of(const uint4& r, int w) {
-  return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
+__device__ __forceinline__ int group_of(const int32_t* starts, int q, int32_t x) {
+  int g = 0;
+  while (g + 1 < q && x >= starts[g + 1]) ++g;
+  return g;
 }
 
 __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhase p) {
-  __shared__ __attribute__((aligned(16))) char As[MR * kRowBytes];
-  __shared__ __attribute__((aligned(16))) char Bs[TN * kRowBytes];
-  __shared__ int32_t need_s[MR];
-  __shared__ int32_t any_g[kMaxQGroups];
-  __shared__ int32_t last_s;
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ unsigned long long rowmask_s[kMaxQGroups];
+  __shared__ int16_t slices_s[kDecodeMaxK / SLICE];
+  __shared__ int32_t nslices_s;
+  __shared__ int32_t wave_cnt_s[2];
 
   const int tid = threadIdx.x;
-  const int ct = blockIdx.x;
-  const int kc = blockIdx.y;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+
+  // column tile of this workgroup (XCD-aware: 4 consecutive tiles per XCD)
+  const int b = blockIdx.x;
+  const int xcd = b & 7, s = b >> 3;
+  const int ct = 4 * (8 * (s >> 2) + xcd) + (s & 3);
+  const int nt_total = p.NTp[p.q];
+  if (ct >= nt_total) return;
   int j = 0;
   while (ct >= p.NTp[j + 1]) ++j;
-  int g = 0;
-  while (kc >= p.KCp[g + 1]) ++g;
   const int32_t n0 = p.R[j] + (ct - p.NTp[j]) * TN;
   const int32_t nend = p.R[j + 1];
-  const int32_t k0 = p.S[g] + (kc - p.KCp[g]) * TKc;
-  const int32_t kend = p.S[g + 1];
 
-  if (tid < MR) need_s[tid] = (tid < p.M) && in_support(p.law, p.types[tid], j, g);
-  const int any = __syncthreads_or(tid < MR ? need_s[tid] : 0);
-
-  if (any) {
-    // stage the rows' inputs: row r = tid/16 + 16u, 16-byte chunk tid%16
-    uint4 ra[4];
-    const int kq = (tid & 15) * 8;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = (tid >> 4) + 16 * u;
-      if (need_s[r] && k0 + kq < kend)
-        ra[u] = *reinterpret_cast<const uint4*>(p.A + static_cast<int64_t>(r) * p.K + k0 + kq);
-      else
-        ra[u] = make_uint4(0, 0, 0, 0);
+  // which rows need block (g, j), per input group g: wave 0 holds one row
+  // per lane and takes one ballot per group
+  if (wave == 0) {
+    const int t = lane < p.M ? p.types[lane] : -1;
+    for (int g = 0; g < p.q; ++g) {
+      const unsigned long long m = __ballot(lane < p.M && in_support(p.law, t, j, g));
+      if (lane == 0) rowmask_s[g] = m;
     }
-    // stage the weight tile: rows k0 + 4 kb + e, columns n0 + 8 cb .. +8
-    uint4 rw[4];
-    const int cb = tid & 7;
-    const int kb = tid >> 3;
-    const int32_t col = n0 + cb * 8;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int32_t k = k0 + kb * 4 + e;
-      if (k < kend && col < nend)
-        rw[e] = *reinterpret_cast<const uint4*>(p.W + static_cast<int64_t>(k) * p.N + col);
-      else
-        rw[e] = make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      *reinterpret_cast<uint4*>(As + ((tid >> 4) + 16 * u) * kRowBytes + (tid & 15) * 16) = ra[u];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const int w = v >> 1, sh = (v & 1) * 16;
-      uint2 piece;
-      piece.x = ((word_of(rw[0], w) >> sh) & 0xffffu) | (((word_of(rw[1], w) >> sh) & 0xffffu) << 16);
-      piece.y = ((word_of(rw[2], w) >> sh) & 0xffffu) | (((word_of(rw[3], w) >> sh) & 0xffffu) << 16);
-      *reinterpret_cast<uint2*>(Bs + (cb * 8 + v) * kRowBytes + kb * 8) = piece;
-    }
-    __syncthreads();
-
-    const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int lr = lane & 31, lh = lane >> 5;
-    f32x16_t acc;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-    if (wm * 32 < p.M) {
-      const char* a_base = As + (wm * 32 + lr) * kRowBytes + lh * 16;
-      const char* b_base = Bs + (wn * 32 + lr) * kRowBytes + lh * 16;
-#pragma unroll
-      for (int s = 0; s < TKc / 16; ++s) {
-        const uint4 a = *reinterpret_cast<const uint4*>(a_base + s * 32);
-        const uint4 b = *reinterpret_cast<const uint4*>(b_base + s * 32);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                      __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+  }
+  __syncthreads();
+  // needed slices, in K order: one slice per thread, compacted with ballots
+  {
+    const int nsl = (p.K + SLICE - 1) / SLICE;  // <= 128, the first two waves
+    bool need = false;
+    if (tid < nsl) {
+      for (int piece = 0; piece < SLICE / 8; ++piece) {
+        const int32_t k = tid * SLICE + piece * 8;
+        if (k < p.K && rowmask_s[group_of(p.S, p.q, k)]) need = true;
       }
-      const int32_t n = n0 + wn * 32 + lr;
-      if (n < nend) {
-        float* part = p.partial + static_cast<int64_t>(kc) * MR * p.N;
+    }
+    const unsigned long long bal = __ballot(need);
+    if (wave < 2 && lane == 0) wave_cnt_s[wave] = __popcll(bal);
+    __syncthreads();
+    if (need) {
+      const int before = (wave == 1 ? wave_cnt_s[0] : 0) +
+                         __popcll(bal & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+      slices_s[before] = static_cast<int16_t>(tid);
+    }
+    if (tid == 0) nslices_s = wave_cnt_s[0] + wave_cnt_s[1];
+  }
+  __syncthreads();
+  const int nslices = nslices_s;
+
+  // stream this wave's slices into LDS: lane l carries row l/2, 16 bytes
+  // (8 columns) at half l%2.  Rows past K repeat row K-1 and columns past
+  // the group repeat its first column (finite values; their products are
+  // either multiplied by zero inputs or never stored).
+  for (int i = wave; i < nslices; i += 4) {
+    int32_t row = slices_s[i] * SLICE + (lane >> 1);
+    row = row < p.K ? row : p.K - 1;
+    int32_t col = n0 + 8 * (lane & 1);
+    col = col < nend ? col : n0;
+    const uint16_t* g = p.W + static_cast<int64_t>(row) * p.N + col;
+    __builtin_amdgcn_global_load_lds(g, (STARQ_LDS void*)(lds + i * 1024), 16, 0, 0);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  __asm__ volatile("" ::: "memory");
+
+  // compute: lane group G = lane/16 holds K rows 8G..8G+7 of a slice for
+  // column n0 + lane%16 (transpose reads), and the input pieces of rows
+  // 16 mb + lane%16
+  const int G = lane >> 4;
+  const int pl = lane & 15;
+  const int mblocks = (p.M + 15) >> 4;
+  f32x4_t acc[4];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = wm * 32 + 8 * (e >> 2) + 4 * lh + (e & 3);
-          if (r < p.M) part[static_cast<int64_t>(r) * p.N + n] = acc[e];
+  for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // input pieces of slice `i` (zero where the row's support skips it),
+  // prefetched two slices ahead
+  auto load_x = [&](int i, uint4 (&xv)[4]) {
+    const int32_t kk = slices_s[i] * SLICE + 8 * G;
+    const unsigned long long gm = kk < p.K ? rowmask_s[group_of(p.S, p.q, kk)] : 0ull;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const int m = 16 * mb + pl;
+      const bool ok = mb < mblocks && m < p.M && ((gm >> m) & 1ull);
+      const uint4 xa = *reinterpret_cast<const uint4*>(p.A + (ok ? static_cast<int64_t>(m) * p.K + kk : 0));
+      xv[mb] = ok ? xa : make_uint4(0, 0, 0, 0);
+    }
+  };
+  uint4 x0[4], x1[4], x2[4];
+  if (wave < nslices) load_x(wave, x0);
+  if (wave + 4 < nslices) load_x(wave + 4, x1);
+  for (int i = wave; i < nslices; i += 4) {
+    if (i + 8 < nslices) load_x(i + 8, x2);
+    const char* base = lds + i * 1024 + (8 * G + (pl >> 2)) * 32 + (pl & 3) * 8;
+    const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base));
+    const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base + 128));
+    uint4 wf;
+    wf.x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
+    wf.y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
+    wf.z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
+    wf.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      if (mb < mblocks) {
+        // D[n][m] += W^T x^T: lane ends with 4 consecutive columns of row m
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf),
+                                                          __builtin_bit_cast(bf16x8_t, x0[mb]),
+                                                          acc[mb], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      x0[mb] = x1[mb];
+      x1[mb] = x2[mb];
+    }
+  }
+
+  // add the four waves' partial sums in a fixed order
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + (kDecodeMaxK / SLICE) * 1024);
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) red[(wave * 4 + mb) * 64 + lane] = acc[mb];
+  __syncthreads();
+  {
+    const int mb = tid >> 6;
+    const int l = tid & 63;
+    const int m = 16 * mb + (l & 15);
+    const int32_t n = n0 + 4 * (l >> 4);
+    if (mb < mblocks && m < p.M && n < nend) {
+      f32x4_t z = red[(0 * 4 + mb) * 64 + l];
+      z += red[(1 * 4 + mb) * 64 + l];
+      z += red[(2 * 4 + mb) * 64 + l];
+      z += red[(3 * 4 + mb) * 64 + l];
+      if (p.bias) {
+        const float4 bv = *reinterpret_cast<const float4*>(p.bias + n);
+        z[0] += bv.x; z[1] += bv.y; z[2] += bv.z; z[3] += bv.w;
+      }
+      const int64_t o = static_cast<int64_t>(m) * p.N + n;
+      if (p.mode == 0) {
+        uint2 w;
+        w.x = f32_to_bf16(act_fwd(p.act, z[0])) | (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, z[1]))) << 16);
+        w.y = f32_to_bf16(act_fwd(p.act, z[2])) | (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, z[3]))) << 16);
+        *reinterpret_cast<uint2*>(p.out_bf16 + o) = w;
+      } else {
+        float hv[4];
+        if (p.residual) {
+          if (p.h_init) {
+            const uint2 hi = *reinterpret_cast<const uint2*>(p.h_init + o);
+            hv[0] = bf16_to_f32(hi.x & 0xffffu); hv[1] = bf16_to_f32(hi.x >> 16);
+            hv[2] = bf16_to_f32(hi.y & 0xffffu); hv[3] = bf16_to_f32(hi.y >> 16);
+          } else {
+            const float4 hp = *reinterpret_cast<const float4*>(p.h_in + o);
+            hv[0] = hp.x; hv[1] = hp.y; hv[2] = hp.z; hv[3] = hp.w;
+          }
+        } else {
+          hv[0] = hv[1] = hv[2] = hv[3] = 0.f;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hv[e] += z[e];
+        if (p.h_out) *reinterpret_cast<float4*>(p.h_out + o) = make_float4(hv[0], hv[1], hv[2], hv[3]);
+        if (p.out_bf16) {
+          uint2 w;
+          w.x = f32_to_bf16(hv[0]) | (static_cast<uint32_t>(f32_to_bf16(hv[1])) << 16);
+          w.y = f32_to_bf16(hv[2]) | (static_cast<uint32_t>(f32_to_bf16(hv[3])) << 16);
+          *reinterpret_cast<uint2*>(p.out_bf16 + o) = w;
+        }
+        if (p.Y) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) store_out(p.Y, p.ydtype, o + e, hv[e]);
         }
       }
     }
   }
-
-  // publish this chunk, then let the last workgroup of the column tile reduce
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int nk = gridDim.y;
-    const int old = atomicAdd(&p.counters[ct], 1);
-    last_s = (old == nk - 1);
-  }
-  __syncthreads();
-  if (!last_s) return;
-  __threadfence();
-  if (tid == 0) p.counters[ct] = 0;  // ready for the next launch
-  if (tid < p.q) {
-    int a = 0;
-    for (int b = 0; b < p.M; ++b) a |= in_support(p.law, p.types[b], j, tid);
-    any_g[tid] = a;
-  }
-  __syncthreads();
-
-  const int nk = gridDim.y;
-  for (int idx = tid; idx < p.M * TN; idx += kThreads) {
-    const int r = idx / TN;
-    const int32_t n = n0 + idx % TN;
-    if (n >= nend) continue;
-    float z = 0.f;
-    int gg = 0;
-    for (int c = 0; c < nk; ++c) {
-      while (c >= p.KCp[gg + 1]) ++gg;
-      if (!any_g[gg]) continue;
-      // a chunk that ran but had no row needing it for this row still wrote
-      // zeros for that row
-      z += __builtin_nontemporal_load(p.partial + (static_cast<int64_t>(c) * MR + r) * p.N + n);
-    }
-    if (p.bias) z += p.bias[n];
-    const int64_t o = static_cast<int64_t>(r) * p.N + n;
-    if (p.mode == 0) {
-      p.out_bf16[o] = f32_to_bf16(act_fwd(p.act, z));
-    } else {
-      const float hv = p.residual ? p.h[o] + z : z;
-      p.h[o] = hv;
-      if (p.out_bf16) p.out_bf16[o] = f32_to_bf16(hv);
-      if (p.Y) store_out(p.Y, p.ydtype, o, hv);
-    }
-  }
-}
-
-__global__ void decode_init_kernel(const uint16_t* __restrict__ X, int64_t n, float* __restrict__ h,
-                                   uint16_t* __restrict__ xb, int32_t* __restrict__ counters,
-                                   int n_counters) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const uint16_t v = X[i];
-    h[i] = bf16_to_f32(v);
-    xb[i] = v;
-  }
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_counters; i += gridDim.x * blockDim.x)
-    counters[i] = 0;
 }
 
 }  // namespace
 
-hipError_t launch_decode_init(const uint16_t* X, int64_t n, float* h, uint16_t* xb,
-                              int32_t* counters, int n_counters, hipStream_t stream) {
-  hipLaunchKernelGGL(decode_init_kernel, dim3(64), dim3(256), 0, stream, X, n, h, xb, counters,
-                     n_counters);
-  return hipGetLastError();
-}
+size_t decode_phase_smem() { return (kDecodeMaxK / SLICE) * 1024 + kRedBytes; }
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream) {
-  dim3 grid(p.NTp[p.q], p.KCp[p.q]);
-  hipLaunchKernelGGL(decode_phase_kernel, grid, dim3(kThreads), 0, stream, p);
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(decode_phase_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+      static_cast<int>(decode_phase_smem()));
+  if (attr != hipSuccess) return attr;
+  const int nt = p.NTp[p.q];
+  const int grid = (nt + 31) / 32 * 32;
+  hipLaunchKernelGGL(decode_phase_kernel, dim3(grid), dim3(kThreads), decode_phase_smem(), stream, p);
   return hipGetLastError();
 }
 

@@ -1,0 +1,236 @@
+// Pieces shared by the grouped GEMM kernels: tile enumeration, MFMA
+// wrappers, the GELU epilogue and 4-wide output stores.
+#pragma once
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace starq {
+namespace gemm {
+
+constexpr int BM = kTileM;  // 256
+constexpr int THREADS = 256;
+
+template <typename T> struct Tr;
+template <> struct Tr<float> {
+  static constexpr int VEC = 4;  // elements per 16-byte kpack
+  static constexpr int BK = 32;  // K per step: 8 kpacks
+};
+template <> struct Tr<uint16_t> {
+  static constexpr int VEC = 8;
+  static constexpr int BK = 64;
+};
+
+template <int WN> struct Geo {
+  static constexpr int BN = 64 * WN;
+  static constexpr int A_BYTES = 8 * BM * 16;
+  static constexpr int B_BYTES = 8 * BN * 16;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int SMEM = 2 * STAGE;
+};
+
+__device__ __forceinline__ int swz(int row, int kp) { return row ^ (((row >> 3) ^ kp) & 7); }
+
+template <int ROWS>
+__device__ __forceinline__ int unit_off(int kp, int row) {
+  return (kp * ROWS + swz(row, kp)) * 16;
+}
+
+__device__ __forceinline__ uint32_t word_of(const uint4& r, int w) {
+  return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
+}
+
+enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3 };
+
+__device__ __forceinline__ int sel_for(int mode, int law, int pass) {
+  if (law == 1) return pass == 0 ? kSelAll : kSelNone;
+  if (mode == kModeFwd) return pass == 0 ? kSelExcept : kSelOnly;
+  return pass == 0 ? kSelOnly : kSelExcept;  // BWD_DATA and BWD_WEIGHT
+}
+
+__device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
+  const int nti = p.NTp[i + 1] - p.NTp[i];
+  const int nt = p.NTp[p.q];
+  switch (sel) {
+    case kSelOnly: return nti;
+    case kSelExcept: return nt - nti;
+    case kSelAll: return nt;
+    default: return 0;
+  }
+}
+
+__device__ __forceinline__ int col_tile_global(const GemmParams& p, int sel, int i, int c) {
+  if (sel == kSelOnly) return p.NTp[i] + c;
+  if (sel == kSelExcept) return c < p.NTp[i] ? c : c + (p.NTp[i + 1] - p.NTp[i]);
+  return c;
+}
+
+// D += A B with the operands of the C^T block: a = B-tile fragment (rows of
+// D are columns of C), b = A-tile fragment (columns of D are rows of C).
+__device__ __forceinline__ void mma(f32x16_t& acc, const uint4& a, const uint4& b, uint16_t) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x16_t& acc, const uint4& a, const uint4& b, float) {
+  // lane half h supplies K element 4 kp + j of instruction j; both operands
+  // use the same assignment, so the products pair up.
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+// ---- GELU -------------------------------------------------------------------
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// erf from Abramowitz & Stegun 7.1.26: erf(x) = 1 - (a1 t + ... + a5 t^5)
+// exp(-x^2), t = 1 / (1 + p x), x >= 0; |error| <= 1.5e-7.  The reciprocal
+// and exponential are the hardware approximations (about 1 ulp).
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  float poly = 1.061405429f;
+  poly = poly * t - 1.453152027f;
+  poly = poly * t + 1.421413741f;
+  poly = poly * t - 0.284496736f;
+  poly = poly * t + 0.254829592f;
+  poly *= t;
+  const float y = 1.0f - poly * __builtin_amdgcn_exp2f(-(ax * ax) * kLog2e);
+  return copysignf(y, x);
+}
+
+__device__ __forceinline__ float act_apply(int act, float z) {
+  if (act == kActGelu) return 0.5f * z * (1.0f + erf_as7126(z * 0.70710678118654752f));
+  if (act == kActGeluTanh) {
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    return 0.5f * z * (1.0f + tanhf(u));
+  }
+  return z;
+}
+
+__device__ __forceinline__ float act_deriv(int act, float z) {
+  if (act == kActGelu)
+    return 0.5f * (1.0f + erf_as7126(z * 0.70710678118654752f)) +
+           z * 0.39894228040143268f * __builtin_amdgcn_exp2f(-0.5f * z * z * kLog2e);
+  if (act == kActGeluTanh) {
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    const float t = tanhf(u);
+    const float du = 0.79788456080286536f * (1.0f + 0.134145f * z * z);
+    return 0.5f * (1.0f + t) + 0.5f * z * (1.0f - t * t) * du;
+  }
+  return 1.0f;
+}
+
+// 4 consecutive values of a row of an fp32 or bf16 matrix
+__device__ __forceinline__ void store4(void* base, int dtype, int64_t idx, const float (&v)[4]) {
+  if (dtype == 0) {
+    *reinterpret_cast<float4*>(static_cast<float*>(base) + idx) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    uint2 w;
+    w.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+    w.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(base) + idx) = w;
+  }
+}
+
+__device__ __forceinline__ void load4(const void* base, int dtype, int64_t idx, float (&v)[4]) {
+  if (dtype == 0) {
+    const float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + idx);
+    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+  } else {
+    const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(base) + idx);
+    v[0] = bf16_to_f32(w.x & 0xffffu); v[1] = bf16_to_f32(w.x >> 16);
+    v[2] = bf16_to_f32(w.y & 0xffffu); v[3] = bf16_to_f32(w.y >> 16);
+  }
+}
+
+// One 16-byte load that reads zeros when `ok` is false.  The address is
+// clamped to the (always valid) first element instead of branching.
+template <typename T>
+__device__ __forceinline__ uint4 load16(const T* __restrict__ src, int64_t off, bool ok) {
+  const uint4 v = *reinterpret_cast<const uint4*>(src + (ok ? off : 0));
+  return ok ? v : make_uint4(0, 0, 0, 0);
+}
+
+// ---- tile iteration ----------------------------------------------------------
+
+struct Tile {
+  int32_t cls, cg, mt, split;
+  int32_t cstart, cend;                          // columns of C
+  int32_t rstart, rend;                          // BWD_WEIGHT: rows of C
+  int32_t seg0_lo, seg0_hi, seg1_lo, seg1_hi;    // K ranges
+  int32_t n0, nsteps;                            // K steps in segment 0, in total
+  int32_t pos0, nrows;                           // FWD/BWD_DATA: rows in perm
+  int32_t do_dbias;
+};
+
+template <int MODE, int LAW, int BN, int BK>
+__device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls, int32_t u,
+                                          int32_t units) {
+  Tile t;
+  const int32_t ru = u % units;
+  const int ct = col_tile_global(p, sel, cls, u / units);
+  int cg = 0;
+  while (ct >= p.NTp[cg + 1]) ++cg;
+  const int nt = ct - p.NTp[cg];
+  t.cls = cls;
+  t.cg = cg;
+  t.seg1_lo = t.seg1_hi = 0;
+  t.rstart = t.rend = 0;
+  t.split = 0;
+  t.do_dbias = 0;
+  t.pos0 = t.nrows = 0;
+  if constexpr (MODE == kModeFwd) {
+    t.mt = ru;
+    t.cstart = p.R[cg] + nt * BN;
+    t.cend = p.R[cg + 1];
+    if (LAW == 1) {
+      t.seg0_lo = 0; t.seg0_hi = p.K;
+    } else {
+      t.seg0_lo = p.S[cg]; t.seg0_hi = p.S[cg + 1];
+      if (cg != cls) { t.seg1_lo = p.S[cls]; t.seg1_hi = p.S[cls + 1]; }
+    }
+  } else if constexpr (MODE == kModeBwdData) {
+    t.mt = ru;
+    t.cstart = p.S[cg] + nt * BN;
+    t.cend = p.S[cg + 1];
+    if (LAW == 1 || cg == cls) {
+      t.seg0_lo = 0; t.seg0_hi = p.N;
+    } else {
+      t.seg0_lo = p.R[cg]; t.seg0_hi = p.R[cg + 1];
+    }
+  } else {
+    t.mt = ru / p.nsplit;
+    t.split = ru % p.nsplit;
+    t.cstart = p.R[cg] + nt * BN;
+    t.cend = p.R[cg + 1];
+    t.rstart = p.S[cls] + t.mt * BM;
+    t.rend = p.S[cls + 1];
+    int32_t lo, hi;
+    if (LAW == 0 && cg != cls) {
+      lo = p.offsets[cls]; hi = p.offsets[cls + 1];
+    } else {
+      lo = 0; hi = p.offsets[p.q];
+    }
+    const int32_t cs = (hi - lo + p.nsplit - 1) / p.nsplit;
+    t.seg0_lo = min(hi, lo + t.split * cs);
+    t.seg0_hi = min(hi, t.seg0_lo + cs);
+    t.do_dbias = (p.dbias != nullptr) && (cg == cls) && (t.mt == 0);
+  }
+  if constexpr (MODE != kModeBwdWeight) {
+    t.pos0 = p.offsets[cls] + t.mt * BM;
+    t.nrows = min(BM, p.offsets[cls + 1] - t.pos0);
+  }
+  t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
+  t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;
+  // every field is uniform over the workgroup: keep it in scalar registers
+  int32_t* f = reinterpret_cast<int32_t*>(&t);
+#pragma unroll
+  for (int k = 0; k < static_cast<int>(sizeof(Tile) / sizeof(int32_t)); ++k)
+    f[k] = __builtin_amdgcn_readfirstlane(f[k]);
+  return t;
+}
+
+}  // namespace gemm
+}  // namespace starq

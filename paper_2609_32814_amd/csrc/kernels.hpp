@@ -66,10 +66,13 @@ constexpr int kTileM = 256;
 
 // ---- decode ----------------------------------------------------------------
 
-constexpr int kDecodeMaxRows = 64;
-constexpr int kDecodeTileN = 64;
-constexpr int kDecodeChunkK = 128;
+constexpr int kDecodeMaxRows = 64;  // rows per step (one new token per sequence)
+constexpr int kDecodeTileN = 16;    // output columns per workgroup
+constexpr int kDecodeSliceK = 32;   // K rows per streamed slice
+constexpr int kDecodeMaxK = 4096;   // input width of either projection
 
+// One projection of one decode step: out = epilogue(A *_q W + bias) over M
+// rows, a workgroup per 16 output columns.
 struct DecodePhase {
   int32_t q;
   int32_t law;
@@ -79,24 +82,21 @@ struct DecodePhase {
   int32_t S[kMaxQGroups + 1];
   int32_t R[kMaxQGroups + 1];
   int32_t NTp[kMaxQGroups + 1];  // column tiles per output group, prefix
-  int32_t KCp[kMaxQGroups + 1];  // K chunks per input group, prefix
   const int32_t* types;
   const uint16_t* A;   // bf16 [M][K]
   const uint16_t* W;   // bf16 [K][N]
   const float* bias;   // [N] or null
-  float* partial;      // [n_kchunks][kDecodeMaxRows][N]
-  int32_t* counters;   // [n_col_tiles]
-  int32_t mode;        // 0: up (H = act(z) -> out_bf16); 1: down (h += z)
+  int32_t mode;        // 0: up (out_bf16 = act(z)); 1: down (h = h_prev + z)
   int32_t act;
   int32_t residual;
-  uint16_t* out_bf16;  // up: H [M][N]; down: bf16(h) for the next layer (or null)
-  float* h;            // down: running state [M][N] (fp32)
-  void* Y;             // down, last layer: final output
+  uint16_t* out_bf16;     // up: H [M][N]; down: bf16(h) for the next layer, or null
+  const float* h_in;      // down, later layers: running state h_prev [M][N] (fp32)
+  const uint16_t* h_init; // down, first layer: h_prev read from this bf16 [M][N]
+  float* h_out;           // down: new running state [M][N] (fp32), or null
+  void* Y;                // down, last layer: final output, or null
   int32_t ydtype;
 };
 
-hipError_t launch_decode_init(const uint16_t* X, int64_t n, float* h, uint16_t* xb,
-                              int32_t* counters, int n_counters, hipStream_t stream);
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
 
 }  // namespace starq

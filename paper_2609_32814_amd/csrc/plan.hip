@@ -1,8 +1,11 @@
 // Type plan: the per-type row index sets I_i of Alg. 1 as one stable
 // permutation of the rows grouped by type, plus per-type offsets.
 //
-// One workgroup of 1024 threads (16 wavefronts).  The rows are cut into 16
-// contiguous chunks, one per wavefront; a wavefront walks its chunk in
+// One workgroup of 1024 threads (16 wavefronts).  All threads first copy the
+// type vector into LDS as bytes with independent coalesced loads (one round
+// trip to memory instead of one per window), for up to 64 Ki rows; longer
+// vectors are read from memory in the passes below.  The rows are cut into
+// 16 contiguous chunks, one per wavefront; a wavefront walks its chunk in
 // windows of 64 rows.  Lanes holding the same type find each other with
 // ballots over the type bits (a match-any), so each window costs O(log q)
 // ballots and no atomics.  Pass 1 counts rows per (wavefront, type); the
@@ -20,6 +23,7 @@ namespace {
 
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kPlanLdsRows = 65536;
 
 __device__ __forceinline__ uint64_t match_type(int t, bool valid, int nbits) {
   uint64_t m = __ballot(valid);
@@ -38,11 +42,34 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
                                                                  int32_t* __restrict__ offsets) {
   // counts[w][t], t = q is the out-of-range bucket
   __shared__ int32_t counts[kPlanWaves][kMaxQ + 1];
+  __shared__ uint8_t tl[kPlanLdsRows];  // type (or q if out of range) per row
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   for (int i = threadIdx.x; i < kPlanWaves * (kMaxQ + 1); i += kPlanThreads)
     (&counts[0][0])[i] = 0;
+  const bool in_lds = M <= kPlanLdsRows;
+  if (in_lds) {
+    constexpr int kBatch = 8;
+    for (int32_t base = 0; base < M; base += kPlanThreads * kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int32_t row = base + u * kPlanThreads + threadIdx.x;
+        v[u] = row < M ? types[row] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int32_t row = base + u * kPlanThreads + threadIdx.x;
+        if (row < M) tl[row] = static_cast<uint8_t>((v[u] >= 0 && v[u] < q) ? v[u] : q);
+      }
+    }
+  }
   __syncthreads();
+  auto type_of = [&](int32_t row) -> int {
+    if (in_lds) return tl[row];
+    const int t = types[row];
+    return (t >= 0 && t < q) ? t : q;
+  };
 
   const int32_t chunk = ((M + kPlanWaves - 1) / kPlanWaves + 63) & ~63;
   const int32_t lo = wave * chunk;
@@ -53,9 +80,7 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
   for (int32_t base = lo; base < hi; base += 64) {
     const int32_t row = base + lane;
     const bool in = row < hi;
-    int t = in ? types[row] : 0;
-    const bool valid_type = t >= 0 && t < q;
-    if (!valid_type) t = q;
+    const int t = in ? type_of(row) : 0;
     const uint64_t active = __ballot(in);
     const uint64_t m = match_type(t, t < q, nbits) & active;
     if (in && (m & lt_mask) == 0) counts[wave][t] += __popcll(m);
@@ -66,8 +91,7 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
   if (threadIdx.x == 0) {
     int32_t run = 0;
     for (int t = 0; t <= q; ++t) {
-      if (t < q) offsets[t] = run;
-      if (t == q) offsets[q] = run;  // end of valid rows
+      offsets[t] = run;  // offsets[q]: end of the valid rows
       for (int w = 0; w < kPlanWaves; ++w) {
         const int32_t c = counts[w][t];
         counts[w][t] = run;
@@ -81,8 +105,7 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
   for (int32_t base = lo; base < hi; base += 64) {
     const int32_t row = base + lane;
     const bool in = row < hi;
-    int t = in ? types[row] : 0;
-    if (!(t >= 0 && t < q)) t = q;
+    const int t = in ? type_of(row) : 0;
     const uint64_t active = __ballot(in);
     const uint64_t m = match_type(t, t < q, nbits) & active;
     if (in) {
