@@ -201,6 +201,43 @@ int choose_nw(const int64_t* G, int q, int64_t rows_upper) {
 
 star_status hip_status(hipError_t e) { return e == hipSuccess ? STAR_OK : STAR_ERR_HIP; }
 
+// bf16 operands with 128-column tiles take the kernel fed by direct
+// global-to-LDS copies; STARQ_GEMM_SYNC=1 keeps the register-staged one.
+bool use_async_gemm() {
+  static const bool sync = [] {
+    const char* env = std::getenv("STARQ_GEMM_SYNC");
+    return env && std::atoi(env) == 1;
+  }();
+  return !sync;
+}
+
+// The pipelined kernel needs every tile to span at least two K steps of 64:
+// in the forward every contraction group (s_j under the star law, K under
+// the dense law) and in the activation gradient every output group r_j and N
+// must exceed 64 columns.
+bool async_shape_ok(int mode, const GemmParams& p) {
+  constexpr int32_t kMinK = 65;
+  if (mode == kModeFwd) {
+    if (p.law == 1) return p.K >= kMinK;
+    for (int g = 0; g < p.q; ++g)
+      if (p.S[g + 1] - p.S[g] < kMinK) return false;
+    return true;
+  }
+  if (p.N < kMinK) return false;
+  if (p.law == 1) return true;
+  for (int g = 0; g < p.q; ++g)
+    if (p.R[g + 1] - p.R[g] < kMinK) return false;
+  return true;
+}
+
+// `upper` bounds the number of tiles.
+hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
+                            hipStream_t stream) {
+  if (p.elem == 1 && nw == 2 && use_async_gemm() && async_shape_ok(mode, p))
+    return launch_gemm_async(mode, p, upper, cu_count(), stream);
+  return launch_gemm(mode, p, nw, persistent_grid(upper), stream);
+}
+
 star_status run_plan(const int32_t* row_type, int64_t M, int q, void* ws, const PlanWs& pw,
                      hipStream_t stream) {
   return hip_status(launch_type_plan(row_type, M, q, at<int32_t>(ws, pw.perm),
@@ -223,7 +260,7 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
   const int nw = choose_nw(a.R, a.q, rows_upper);
   fill_tiles(p.NTp, a.R, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_gemm(kModeFwd, p, nw, persistent_grid(upper), stream));
+  return hip_status(launch_proj_gemm(kModeFwd, p, nw, upper, stream));
 }
 
 star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a) {
@@ -399,7 +436,7 @@ star_status star_proj_bwd_data_planned(const star_algebra* alg, int64_t M, const
   const int nw = choose_nw(a.S, a.q, rows_upper);
   fill_tiles(p.NTp, a.S, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_gemm(kModeBwdData, p, nw, persistent_grid(upper), stream));
+  return hip_status(launch_proj_gemm(kModeBwdData, p, nw, upper, stream));
 }
 
 star_status star_proj_bwd_data(const star_algebra* alg, int64_t M, const int32_t* row_type,

@@ -317,7 +317,8 @@ __global__ __launch_bounds__(THREADS, 1) void star_gemm_kernel(const GemmParams 
       int cls = 0;
       while (logical >= pfx_s[it_pass][cls + 1]) ++cls;
       const int sel = sel_for(MODE, LAW, it_pass);
-      t = make_tile<MODE, LAW, BN, BK>(p, sel, cls, logical - pfx_s[it_pass][cls], units_s[cls]);
+      t = make_tile<MODE, LAW, BN, BK>(p, sel, cls, logical - pfx_s[it_pass][cls], units_s[cls],
+                                       p.offsets);
       if (t.nsteps == 0) {  // only weight-gradient splits can be empty
         write_zero_tile(t);
         continue;

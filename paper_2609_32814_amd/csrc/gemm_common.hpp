@@ -100,11 +100,17 @@ __device__ __forceinline__ float erf_as7126(float x) {
   return copysignf(y, x);
 }
 
+// tanh(u) = 1 - 2 / (1 + exp(2u)); the absolute error stays near 1e-7 over
+// the whole range (saturating to +-1), which is what the tanh-form GELU needs.
+__device__ __forceinline__ float tanh_fast(float u) {
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(2.0f * kLog2e * u));
+}
+
 __device__ __forceinline__ float act_apply(int act, float z) {
   if (act == kActGelu) return 0.5f * z * (1.0f + erf_as7126(z * 0.70710678118654752f));
   if (act == kActGeluTanh) {
     const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
-    return 0.5f * z * (1.0f + tanhf(u));
+    return 0.5f * z * (1.0f + tanh_fast(u));
   }
   return z;
 }
@@ -115,7 +121,7 @@ __device__ __forceinline__ float act_deriv(int act, float z) {
            z * 0.39894228040143268f * __builtin_amdgcn_exp2f(-0.5f * z * z * kLog2e);
   if (act == kActGeluTanh) {
     const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
-    const float t = tanhf(u);
+    const float t = tanh_fast(u);
     const float du = 0.79788456080286536f * (1.0f + 0.134145f * z * z);
     return 0.5f * (1.0f + t) + 0.5f * z * (1.0f - t * t) * du;
   }
@@ -165,12 +171,26 @@ struct Tile {
   int32_t do_dbias;
 };
 
+// `offs` holds the q + 1 type offsets of the plan (global memory or an LDS
+// copy).
 template <int MODE, int LAW, int BN, int BK>
 __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls, int32_t u,
-                                          int32_t units) {
+                                          int32_t units, const int32_t* offs) {
   Tile t;
-  const int32_t ru = u % units;
-  const int ct = col_tile_global(p, sel, cls, u / units);
+  // Forward and activation gradient: column tiles vary fastest, so that the
+  // tiles of one XCD chunk cover a few row tiles across all their column
+  // tiles (their rows stay in that XCD's L2 while the weights stream).
+  // Weight gradient: row-tile x split units vary fastest.
+  int32_t ru, cidx;
+  if constexpr (MODE == kModeBwdWeight) {
+    ru = u % units;
+    cidx = u / units;
+  } else {
+    const int32_t nc = ncols_sel(p, sel, cls);
+    ru = u / nc;
+    cidx = u % nc;
+  }
+  const int ct = col_tile_global(p, sel, cls, cidx);
   int cg = 0;
   while (ct >= p.NTp[cg + 1]) ++cg;
   const int nt = ct - p.NTp[cg];
@@ -209,9 +229,9 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.rend = p.S[cls + 1];
     int32_t lo, hi;
     if (LAW == 0 && cg != cls) {
-      lo = p.offsets[cls]; hi = p.offsets[cls + 1];
+      lo = offs[cls]; hi = offs[cls + 1];
     } else {
-      lo = 0; hi = p.offsets[p.q];
+      lo = 0; hi = offs[p.q];
     }
     const int32_t cs = (hi - lo + p.nsplit - 1) / p.nsplit;
     t.seg0_lo = min(hi, lo + t.split * cs);
@@ -219,8 +239,8 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.do_dbias = (p.dbias != nullptr) && (cg == cls) && (t.mt == 0);
   }
   if constexpr (MODE != kModeBwdWeight) {
-    t.pos0 = p.offsets[cls] + t.mt * BM;
-    t.nrows = min(BM, p.offsets[cls + 1] - t.pos0);
+    t.pos0 = offs[cls] + t.mt * BM;
+    t.nrows = min(BM, offs[cls + 1] - t.pos0);
   }
   t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
   t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;

@@ -146,6 +146,93 @@ def test_out_of_range_types_left_out(P):
     assert rel_fro(got[good], ref) <= TOL_F32
 
 
+# ---- bf16 shapes with every K group wider than 64 (the pipelined kernel) --------
+
+PIPE_SHAPES = [
+    # several row tiles per type with a ragged last one; K groups with tails
+    # of 8..56 past a multiple of 64; output groups that end inside a tile
+    (2, [200, 136], [328, 200], 1500, "cyclic"),
+    (3, [72, 264, 96], [136, 72, 392], 2000, "random"),
+    # long contractions (17 and 9 K steps) and a one-type class of 1 row
+    (2, [1040, 520], [264, 136], 771, "one_row"),
+    (1, [776], [392], 1100, "cyclic"),
+]
+
+
+def _types(kind, M, q, seed):
+    rng = np.random.default_rng([seed, 3])
+    if kind == "cyclic":
+        return synth.cyclic_types(M, q)
+    t = rng.integers(0, q, M).astype(np.int32)
+    if kind == "one_row":
+        t[:] = 0
+        t[M // 2] = 1
+    return t
+
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+@pytest.mark.parametrize("q,s,r,M,types", PIPE_SHAPES)
+def test_fwd_pipelined_shapes(P, law, out, q, s, r, M, types):
+    import torch
+    ga, oa = algs(P, q, s, r, law)
+    seed = 400 + q + M
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, "bf16")
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.03, "bf16")
+    bias = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
+    t = _types(types, M, q, seed)
+    odt = torch.float32 if out == "f32" else torch.bfloat16
+    Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
+                           Z_out=True, out_dtype=odt)
+    refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, bias.exact, "gelu", want_z=True)
+    assert rel_fro(to_host(Z), refZ) <= TOL_BF16
+    assert rel_fro(to_host(Y), refY) <= TOL_BF16
+    # every row individually (a dropped or duplicated tile shows up here)
+    diff = np.linalg.norm(to_host(Z) - refZ, axis=1) / np.maximum(np.linalg.norm(refZ, axis=1), 1e-30)
+    assert diff.max() <= 4 * TOL_BF16
+
+
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("q,s,r,M,types", PIPE_SHAPES)
+def test_bwd_data_pipelined_shapes(P, law, fused, q, s, r, M, types):
+    import torch
+    ga, oa = algs(P, q, s, r, law)
+    seed = 500 + q + M
+    dY = synth.gaussian(seed, 0, (M, oa.N), 1.0, "bf16")
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.03, "bf16")
+    Zp = synth.gaussian(seed, 2, (M, oa.K), 1.0, "bf16") if fused else None
+    t = _types(types, M, q, seed)
+    dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W),
+                              Z_prev=to_dev(Zp) if fused else None,
+                              act_prev="gelu" if fused else "none", out_dtype=torch.float32)
+    ref = oracle.proj_bwd_data(oa, t, dY.exact, W.exact, Zprev=Zp.exact if fused else None,
+                               act_prev="gelu" if fused else "none")
+    got = to_host(dX)
+    assert rel_fro(got, ref) <= TOL_BF16
+    diff = np.linalg.norm(got - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-30)
+    assert diff.max() <= 4 * TOL_BF16
+
+
+def test_pipelined_out_of_range_types_left_out(P):
+    import torch
+    ga, oa = algs(P, 2, [136, 200], [264, 72])
+    M = 900
+    X = synth.gaussian(13, 0, (M, oa.K), 1.0, "bf16")
+    W = synth.gaussian(13, 1, (oa.K, oa.N), 0.03, "bf16")
+    t = synth.cyclic_types(M, 2)
+    bad = np.array([0, 255, 256, 899])
+    t_bad = t.copy()
+    t_bad[bad] = [2, -5, 7, 1000]
+    Y = torch.full((M, oa.N), 12345.0, device="cuda")
+    P.star_proj_fwd(ga, types_dev(t_bad), to_dev(X), to_dev(W), Y=Y)
+    got = to_host(Y)
+    assert np.all(got[bad] == 12345.0)
+    good = np.setdiff1d(np.arange(M), bad)
+    ref, _, _, _ = oracle.proj_fwd(oa, t[good], X.exact[good], W.exact)
+    assert rel_fro(got[good], ref) <= TOL_BF16
+
+
 # ---- backward -------------------------------------------------------------------
 
 @pytest.mark.parametrize("law", ["star", "dense"])
