@@ -14,8 +14,8 @@ Also reported in the same line: the same-code dense control (ordinary XW
 through the same kernels), warm and cache-flushed kernel times, the decode
 stack (12 layers, M in {1, 8, 32, 64}) in HBM GB/s and FFN tokens/s, the
 roofline of the dominant kernel measured with HIP events, and the CPU oracle
-timed on this host.  ``--all`` adds the training step and the fixed-block q
-sweep (as extra JSON lines on stderr).
+timed on this host, plus the FFN training step (M = 16384, forward and
+backward) and the fixed-block q sweep (q = 2..16) unless ``--no-extra``.
 """
 
 from __future__ import annotations
@@ -36,7 +36,17 @@ PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 FLUSH_BYTES = 512 << 20    # twice the 256 MB Infinity Cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "star_gemm_fwd_cfg2_traffic.json")
-GEMM_SRC = os.path.join(ROOT, "paper_2609_32814_amd", "csrc", "gemm.hip")
+GEMM_SRCS = [os.path.join(ROOT, "paper_2609_32814_amd", "csrc", f)
+             for f in ("gemm_async.hip", "gemm_common.hpp")]
+GEMM_KERNEL = "star_gemm_async_kernel<fwd, star, gelu>"
+
+
+def gemm_src_hash():
+    h = hashlib.sha256()
+    for f in GEMM_SRCS:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def log(*a):
@@ -51,7 +61,11 @@ def parse():
     ap.add_argument("--trials", type=int, default=12, help="cache-flushed trials per kernel")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--all", action="store_true", help="also the training step and q sweep")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the training step and the q sweep")
+    ap.add_argument("--all", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 256 MiB device copy (for HBM counter calibration)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     return ap.parse_args()
 
@@ -78,12 +92,16 @@ def main():
     import numpy as np
     import torch
 
-    import paper_2609_32814_amd as P
-    import synth
-
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.calibrate_copy:
+        calibrate_copy(torch, dev)
+        return
+
+    import paper_2609_32814_amd as P
+    import synth
+
     T = Timer(torch)
     flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
 
@@ -169,13 +187,12 @@ def main():
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
-        src_hash = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
-        if tr.get("gemm_src_sha256") == src_hash:
+        if tr.get("gemm_src_sha256") == gemm_src_hash():
             traffic = tr.get("hbm_bytes_per_launch")
 
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic, "kernel": "star_gemm_kernel<bf16, fwd, star>",
+                "traffic": traffic, "kernel": GEMM_KERNEL,
                 "kernel_mean_us": round(kern * 1e3, 2)}
     dense_ctrl = {
         "kernel_mean_us": round(d_kern_mean * 1e3, 2),
@@ -217,9 +234,9 @@ def main():
     if not args.no_decode:
         result["decode"] = bench_decode(P, synth, torch, np, dev, T, flush, args)
 
-    if args.all:
-        bench_training(P, synth, torch, np, dev, T, args)
-        bench_qsweep(P, synth, torch, np, dev, T, flush, args)
+    if not args.no_extra:
+        result["training"] = bench_training(P, synth, torch, np, dev, T, args)
+        result["qsweep"] = bench_qsweep(P, synth, torch, np, dev, T, flush, args)
 
     # ---- CPU oracle baseline -------------------------------------------------
     if not args.no_cpu:
@@ -241,6 +258,19 @@ def main():
         log(f"  cpu oracle: {cpu_val*1e3:.2f} GFLOP/s on {oracle.num_threads()} threads")
 
     print(json.dumps(result), flush=True)
+
+
+def calibrate_copy(torch, dev):
+    """A plain device-to-device copy of 256 MiB, five times: the reference
+    kernel whose FETCH_SIZE / WRITE_SIZE counters give the scale factor for
+    the GEMM's counters."""
+    n = 256 << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 5 x {n} bytes read and written")
 
 
 def decode_weight_bytes(q, D, F, types, L, law="star"):
@@ -368,6 +398,7 @@ def bench_training(P, synth, torch, np, dev, T, args):
     res["speedup"] = round(res["dense"]["step_ms"] / res["star"]["step_ms"], 3)
     res["mfma_peak_frac"] = round(res["star"]["tflops"] / PEAK_BF16_TFLOPS, 4)
     log("training:", json.dumps(res))
+    return res
 
 
 def bench_qsweep(P, synth, torch, np, dev, T, flush, args):
@@ -408,6 +439,7 @@ def bench_qsweep(P, synth, torch, np, dev, T, flush, args):
         del X, W, Y
         torch.cuda.empty_cache()
     log("qsweep:", json.dumps(out))
+    return out
 
 
 if __name__ == "__main__":
