@@ -211,30 +211,21 @@ bool use_async_gemm() {
   return !sync;
 }
 
-// The pipelined kernel needs every tile to span at least two K steps of 64:
-// in the forward every contraction group (s_j under the star law, K under
-// the dense law) and in the activation gradient every output group r_j and N
-// must exceed 64 columns.
-bool async_shape_ok(int mode, const GemmParams& p) {
-  constexpr int32_t kMinK = 65;
-  if (mode == kModeFwd) {
-    if (p.law == 1) return p.K >= kMinK;
-    for (int g = 0; g < p.q; ++g)
-      if (p.S[g + 1] - p.S[g] < kMinK) return false;
-    return true;
-  }
-  if (p.N < kMinK) return false;
-  if (p.law == 1) return true;
-  for (int g = 0; g < p.q; ++g)
-    if (p.R[g + 1] - p.R[g] < kMinK) return false;
-  return true;
-}
-
-// `upper` bounds the number of tiles.
+// bf16 operands take the kernel fed by direct global-to-LDS copies (its
+// column tiles are wider, so the tile counts are redone for it);
+// STARQ_GEMM_SYNC=1 keeps the register-staged one.  `upper` bounds the
+// number of tiles of the register-staged kernel.
 hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
                             hipStream_t stream) {
-  if (p.elem == 1 && nw == 2 && use_async_gemm() && async_shape_ok(mode, p))
-    return launch_gemm_async(mode, p, upper, cu_count(), stream);
+  if (p.elem == 1 && use_async_gemm()) {
+    GemmParams pa = p;
+    const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
+    const int tn = gemm_async_tile_n();
+    pa.NTp[0] = 0;
+    for (int g = 0; g < p.q; ++g) pa.NTp[g + 1] = pa.NTp[g] + (G[g + 1] - G[g] + tn - 1) / tn;
+    const int64_t rows_upper = static_cast<int64_t>(p.M) / kTileM + p.q;
+    return launch_gemm_async(mode, pa, rows_upper * pa.NTp[p.q], cu_count(), stream);
+  }
   return launch_gemm(mode, p, nw, persistent_grid(upper), stream);
 }
 

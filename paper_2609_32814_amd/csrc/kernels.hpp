@@ -57,10 +57,11 @@ hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
 // Persistent grouped GEMM: tiles of kTileM rows x (64 * nw) columns
 // (nw = 2 or 4), `grid` workgroups of 128 * nw threads.
 hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream);
-// bf16 forward / activation-gradient GEMM with tiles of kTileM x 128 fed by
-// direct global-to-LDS copies through a three-stage ring; `upper_tiles`
-// bounds the tile count and `cus` is the device's CU count (the kernel
-// picks its persistent grid from both).
+// bf16 forward / activation-gradient GEMM fed by direct global-to-LDS
+// copies: tiles of kTileM x gemm_async_tile_n() (p.NTp must count column
+// tiles of that width); `upper_tiles` bounds the tile count and `cus` is the
+// device's CU count (the kernel picks its persistent grid from both).
+int gemm_async_tile_n();
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream);
 hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
