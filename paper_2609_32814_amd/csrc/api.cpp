@@ -145,6 +145,46 @@ DecodeWs decode_layout(const Alg& up, int64_t M) {
   return w;
 }
 
+// The single-launch decode stack: 16-column tiles of F (up) and of D (down),
+// the down contraction over F cut into ns chunks so both phases have about
+// as many items; usable when every item's inputs and two weight slots fit
+// in LDS, the grid fits on the device at one workgroup per CU and the layer
+// pointers fit in the kernel arguments.
+struct StackPlan {
+  bool ok = false;
+  int ns = 1, kc = 0, nt_up = 0, nt_dn = 0, grid = 0;
+  size_t H = 0, hb = 0, h = 0, part = 0, cnt = 0, end = 0;
+};
+StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers) {
+  StackPlan sp;
+  const int64_t D = u.K(), F = u.N();
+  for (int g = 0; g < u.q; ++g) sp.nt_up += static_cast<int>(tiles_of(u.r(g), kDecodeTileN));
+  for (int g = 0; g < d.q; ++g) sp.nt_dn += static_cast<int>(tiles_of(d.r(g), kDecodeTileN));
+  sp.ns = static_cast<int>(std::max<int64_t>(1, (sp.nt_up + sp.nt_dn - 1) / sp.nt_dn));
+  sp.kc = static_cast<int>((F + sp.ns - 1) / sp.ns);
+  sp.kc = (sp.kc + 127) / 128 * 128;
+  sp.ns = static_cast<int>((F + sp.kc - 1) / sp.kc);
+  sp.grid = std::max(sp.nt_up, sp.nt_dn * sp.ns);
+  size_t cur = 0;
+  sp.H = cur;
+  cur = align_up(cur + sizeof(uint16_t) * M * F);
+  sp.hb = cur;
+  cur = align_up(cur + 2 * sizeof(uint16_t) * M * D);
+  sp.h = cur;
+  cur = align_up(cur + sizeof(float) * M * D);
+  sp.part = cur;
+  cur = align_up(cur + sizeof(float) * sp.ns * M * D);
+  sp.cnt = cur;
+  cur = align_up(cur + sizeof(int32_t) * (3 + sp.nt_dn));
+  sp.end = cur;
+  bool same_groups = u.q == d.q && u.law == d.law;
+  for (int g = 0; same_groups && g <= u.q; ++g) same_groups = d.S[g] == u.R[g] && d.R[g] == u.S[g];
+  sp.ok = M >= 1 && M <= kDecodeMaxRows && n_layers <= kStackMaxLayers && same_groups &&
+          decode_stack_smem(static_cast<int>(M), static_cast<int>(std::max<int64_t>(D, sp.kc))) > 0 &&
+          sp.grid <= cu_count();
+  return sp;
+}
+
 template <typename T>
 T* at(void* ws, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
@@ -215,6 +255,15 @@ bool use_async_gemm() {
 // column tiles are wider, so the tile counts are redone for it);
 // STARQ_GEMM_SYNC=1 keeps the register-staged one.  `upper` bounds the
 // number of tiles of the register-staged kernel.
+// STARQ_DECODE_PHASES=1 runs the decode stack as one kernel per projection.
+bool use_decode_stack() {
+  static const bool phases = [] {
+    const char* env = std::getenv("STARQ_DECODE_PHASES");
+    return env && std::atoi(env) == 1;
+  }();
+  return !phases;
+}
+
 hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
                             hipStream_t stream) {
   if (p.elem == 1 && use_async_gemm()) {
@@ -295,7 +344,8 @@ size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_alge
     case STAR_OP_DECODE: {
       Alg d;
       if (parse_alg(alg2, d) != STAR_OK) return 0;
-      return decode_layout(a, std::min<int64_t>(M, kDecodeMaxRows)).end;
+      const int64_t m = std::min<int64_t>(M, kDecodeMaxRows);
+      return std::max(decode_layout(a, m).end, stack_plan(a, d, std::max<int64_t>(m, 1), 1).end);
     }
     default:
       return 0;
@@ -582,8 +632,50 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
       return STAR_ERR_ALIGN;
   }
   const DecodeWs dw = decode_layout(u, M);
-  if (!ws || ws_bytes < dw.end) return STAR_ERR_WORKSPACE;
+  const StackPlan sp = stack_plan(u, d, M, n_layers);
+  if (!ws || ws_bytes < std::max(dw.end, sp.end)) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
+
+  if (sp.ok && use_decode_stack()) {
+    DecodeStack k;
+    std::memset(&k, 0, sizeof(k));
+    k.q = u.q;
+    k.law = u.law;
+    k.M = static_cast<int32_t>(M);
+    k.D = static_cast<int32_t>(u.K());
+    k.F = static_cast<int32_t>(u.N());
+    k.L = n_layers;
+    k.act = act;
+    k.residual = residual;
+    k.ydtype = yt;
+    k.ns = sp.ns;
+    k.kc = sp.kc;
+    k.nt_up = sp.nt_up;
+    k.nt_dn = sp.nt_dn;
+    for (int g = 0; g <= u.q; ++g) {
+      k.SD[g] = static_cast<int32_t>(u.S[g]);
+      k.SF[g] = static_cast<int32_t>(u.R[g]);
+    }
+    fill_tiles(k.NTu, u.R, u.q, kDecodeTileN);
+    fill_tiles(k.NTd, d.R, d.q, kDecodeTileN);
+    k.types = row_type;
+    k.X = static_cast<const uint16_t*>(X);
+    for (int l = 0; l < n_layers; ++l) {
+      k.Wu[l] = static_cast<const uint16_t*>(W_up[l]);
+      k.Wd[l] = static_cast<const uint16_t*>(W_down[l]);
+      k.bu[l] = b_up ? b_up[l] : nullptr;
+      k.bd[l] = b_down ? b_down[l] : nullptr;
+    }
+    k.Y = Y;
+    k.H = at<uint16_t>(ws, sp.H);
+    k.hb = at<uint16_t>(ws, sp.hb);
+    k.h = at<float>(ws, sp.h);
+    k.part = at<float>(ws, sp.part);
+    k.cnt = at<int32_t>(ws, sp.cnt);
+    st = hip_status(launch_fill_zero(reinterpret_cast<float*>(k.cnt), 3 + sp.nt_dn, stream));
+    if (st != STAR_OK) return st;
+    return hip_status(launch_decode_stack(k, sp.grid, stream));
+  }
 
   float* h = at<float>(ws, dw.h);
   uint16_t* xb = at<uint16_t>(ws, dw.xb);

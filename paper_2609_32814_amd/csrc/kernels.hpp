@@ -104,6 +104,35 @@ struct DecodePhase {
   int32_t ydtype;
 };
 
+// The whole decode stack in one persistent launch (see decode_stack.hip).
+constexpr int kStackMaxLayers = 32;
+struct DecodeStack {
+  int32_t q, law, M, D, F, L, act, residual, ydtype;
+  int32_t ns, kc;         // down projection: K split into ns chunks of kc
+  int32_t nt_up, nt_dn;   // 16-column tiles of F and of D
+  int32_t SD[kMaxQGroups + 1];   // D groups: up input, down output
+  int32_t SF[kMaxQGroups + 1];   // F groups: up output, down input
+  int32_t NTu[kMaxQGroups + 1];  // column-tile prefix over the F groups
+  int32_t NTd[kMaxQGroups + 1];  // column-tile prefix over the D groups
+  const int32_t* types;
+  const uint16_t* X;
+  const uint16_t* Wu[kStackMaxLayers];
+  const uint16_t* Wd[kStackMaxLayers];
+  const float* bu[kStackMaxLayers];
+  const float* bd[kStackMaxLayers];
+  void* Y;
+  uint16_t* H;    // [M][F] bf16, the current layer's hidden activation
+  uint16_t* hb;   // [2][M][D] bf16, the next up projection's input (layer parity)
+  float* h;       // [M][D] fp32 residual state
+  float* part;    // [ns][M][D] fp32 down-projection partial sums
+  int32_t* cnt;   // [3 + nt_dn]: up arrivals, down arrivals, error flag, per-tile arrivals
+};
+// Dynamic LDS bytes the stack kernel needs, or 0 when the shape does not fit.
+size_t decode_stack_smem(int M, int kmax);
+// Launches the stack kernel cooperatively on grid = max(nt_up, nt_dn * ns)
+// workgroups (all resident at once); p.cnt must be zero.
+hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);
+
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
 
 }  // namespace starq

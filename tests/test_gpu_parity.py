@@ -376,6 +376,54 @@ def test_decode_one_type_only_skips_blocks(P):
         assert rel_fro(to_host(Y), ref) <= TOL_BF16
 
 
+@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("M", [5, 40])
+def test_decode_unequal_groups_q3(P, law, M):
+    """q = 3 with unequal widths (D = 128 + 64 + 192, F = 256 + 128 + 384),
+    random types: output tiles end inside 16-column tiles and K slices
+    straddle group boundaries."""
+    import torch
+    sD, sF = [128, 64, 192], [256, 128, 384]
+    up_g, up_o = algs(P, 3, sD, sF, law)
+    dn_g, dn_o = algs(P, 3, sF, sD, law)
+    D, F, L = sum(sD), sum(sF), 2
+    seed = 700 + M
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.03, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.03, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 70 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 100 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = np.random.default_rng([seed, 5]).integers(0, 3, M).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                      [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                      [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.bfloat16)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    # bf16 output against the oracle's result rounded the same way
+    assert rel_fro(to_host(Y), oracle.round_bf16(ref)) <= TOL_BF16
+
+
+@pytest.mark.parametrize("M", [8, 64])
+def test_decode_wide_model(P, M):
+    """D = 1024, F = 2048: at M = 64 the inputs no longer fit next to two
+    weight slots in LDS and the stack runs one kernel per projection; at
+    M = 8 it runs as one launch.  Both must match the oracle."""
+    import torch
+    D, F, L = 1024, 2048, 2
+    up_g, up_o = algs(P, 2, [D // 2] * 2, [F // 2] * 2)
+    dn_g, dn_o = algs(P, 2, [F // 2] * 2, [D // 2] * 2)
+    seed = 800 + M
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.02, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.02, "bf16") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = (synth.decode_positions(seed, M) % 2).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu], None,
+                      [to_dev(w) for w in Wd], None, "gelu", True, out_dtype=torch.float32)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [np.zeros(F)] * L,
+                              [w.exact for w in Wd], [np.zeros(D)] * L)
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
 # ---- full-size workloads (sampled) ---------------------------------------------------
 
 def _sample_rows(M, n, seed):
