@@ -108,10 +108,34 @@ int bwd_weight_nsplit(const Alg& a, int64_t M) {
   return static_cast<int>(std::max<int64_t>(ns, 1));
 }
 
+// Weight gradient with bf16 operands (pipelined kernel, 256 x 256 tiles):
+// the same rule on its own tile count.
+int bwd_weight_nsplit_async(const Alg& a, int64_t M) {
+  const int tn = gemm_async_tile_n();
+  int64_t mt = 0, nt = 0;
+  for (int g = 0; g < a.q; ++g) {
+    mt += tiles_of(a.s(g), kTileM);
+    nt += tiles_of(a.r(g), tn);
+  }
+  const int64_t base = mt * nt;
+  int64_t ns = (256 + base - 1) / base;
+  ns = std::min<int64_t>(ns, 8);
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, M / 1024));
+  return static_cast<int>(std::max<int64_t>(ns, 1));
+}
+
+constexpr int kColSumChunks = 64;  // row chunks of the bias-gradient column sums
+
+// Workspace of the weight gradient: the plan, then either the fp32 path's
+// split partials or the bf16 path's type-sorted copies of X and dY, split
+// partials and bias-gradient chunk sums (the two paths share the space).
 struct BwdWs {
   PlanWs plan;
   int nsplit = 1;
-  size_t partial = 0, dbias_part = 0, end = 0;
+  size_t partial = 0, dbias_part = 0;
+  int nsplit_a = 1;
+  size_t xs = 0, dys = 0, partial_a = 0, colsum = 0;
+  size_t end = 0;
 };
 BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
   BwdWs w;
@@ -124,7 +148,20 @@ BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
     w.dbias_part = cur;
     cur = align_up(cur + sizeof(float) * static_cast<size_t>(w.nsplit) * a.N());
   }
-  w.end = cur;
+  const size_t end32 = cur;
+  w.nsplit_a = bwd_weight_nsplit_async(a, M);
+  cur = w.plan.end;
+  w.xs = cur;
+  cur = align_up(cur + sizeof(uint16_t) * static_cast<size_t>(M) * a.K());
+  w.dys = cur;
+  cur = align_up(cur + sizeof(uint16_t) * static_cast<size_t>(M) * a.N());
+  if (w.nsplit_a > 1) {
+    w.partial_a = cur;
+    cur = align_up(cur + sizeof(float) * static_cast<size_t>(w.nsplit_a) * a.K() * a.N());
+  }
+  w.colsum = cur;
+  cur = align_up(cur + sizeof(float) * static_cast<size_t>(kColSumChunks) * a.N());
+  w.end = std::max(end32, cur);
   return w;
 }
 
@@ -518,7 +555,8 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
       (dbias && !aligned4(dbias)) || (plan && !aligned16(plan)))
     return STAR_ERR_ALIGN;
   const BwdWs bw = bwd_weight_layout(a, M);
-  if (bw.nsplit > 1 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
+  const bool pipelined = xt == STAR_BF16 && use_async_gemm();
+  if ((pipelined || bw.nsplit > 1) && M > 0 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
   if (ws && !aligned16(ws)) return STAR_ERR_ALIGN;
   // M = 0 still defines the output: an empty sum
   if (M == 0) {
@@ -531,6 +569,36 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   GemmParams p;
   fill_common(p, a, M, xt == STAR_BF16 ? 1 : 0, at<int32_t>(pl, pw.perm),
               at<int32_t>(pl, pw.offsets));
+  if (pipelined) {
+    // sort X and dY rows by type once; every tile then contracts over a
+    // contiguous row range of the copies
+    uint16_t* xs = at<uint16_t>(ws, bw.xs);
+    uint16_t* dys = at<uint16_t>(ws, bw.dys);
+    st = hip_status(launch_gather_rows(static_cast<const uint16_t*>(X), p.K, p.perm, p.offsets,
+                                       a.q, p.M, xs, stream));
+    if (st == STAR_OK)
+      st = hip_status(launch_gather_rows(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets,
+                                         a.q, p.M, dys, stream));
+    if (st != STAR_OK) return st;
+    fill_tiles(p.NTp, a.R, a.q, gemm_async_tile_n());
+    fill_tiles(p.MTp, a.S, a.q, kTileM);
+    p.A = xs;
+    p.B = dys;
+    p.dW = dW;
+    p.nsplit = bw.nsplit_a;
+    if (bw.nsplit_a > 1) p.partial = at<float>(ws, bw.partial_a);
+    const int64_t upper = static_cast<int64_t>(p.MTp[a.q]) * p.NTp[a.q] * p.nsplit;
+    st = hip_status(launch_gemm_async(kModeBwdWeight, p, upper, cu_count(), stream));
+    if (st == STAR_OK && bw.nsplit_a > 1)
+      st = hip_status(launch_sum_partials(p.partial, p.nsplit, static_cast<int64_t>(p.K) * p.N, dW, stream));
+    if (st != STAR_OK || !dbias) return st;
+    // dbias = column sums of dY over the rows of valid type, in fixed chunks
+    const int32_t chunk = static_cast<int32_t>((M + kColSumChunks - 1) / kColSumChunks);
+    float* cs = at<float>(ws, bw.colsum);
+    st = hip_status(launch_column_sum(dys, p.N, p.offsets, a.q, chunk, kColSumChunks, cs, stream));
+    if (st != STAR_OK) return st;
+    return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
+  }
   fill_tiles(p.NTp, a.R, a.q, 64 * kBwdWeightNW);
   fill_tiles(p.MTp, a.S, a.q, kTileM);
   p.A = X;

@@ -589,6 +589,13 @@ hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream) {
   return hipGetLastError();
 }
 
+hipError_t launch_sum_partials(const float* part, int n_parts, int64_t n, float* out,
+                               hipStream_t stream) {
+  const int blocks = static_cast<int>(std::min<int64_t>(2048, (n / 4 + 255) / 256 + 1));
+  hipLaunchKernelGGL(split_reduce_kernel, dim3(blocks), dim3(256), 0, stream, part, n_parts, n, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream) {
   const int64_t nKN = static_cast<int64_t>(p.K) * p.N;
   int blocks = static_cast<int>(std::min<int64_t>(2048, (nKN / 4 + 255) / 256 + 1));

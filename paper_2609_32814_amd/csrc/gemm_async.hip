@@ -137,7 +137,12 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
 
   for (int i = threadIdx.x; i <= q; i += kThreads) offs_s[i] = p.offsets[i];
   __syncthreads();
-  for (int i = threadIdx.x; i < q; i += kThreads) units_s[i] = (offs_s[i + 1] - offs_s[i] + BM - 1) / BM;
+  for (int i = threadIdx.x; i < q; i += kThreads) {
+    if constexpr (MODE == kModeBwdWeight)
+      units_s[i] = (p.MTp[i + 1] - p.MTp[i]) * p.nsplit;  // row tiles of K group i x splits
+    else
+      units_s[i] = (offs_s[i + 1] - offs_s[i] + BM - 1) / BM;  // row tiles of type class i
+  }
   __syncthreads();
   if (threadIdx.x < 2) {
     const int sel = sel_for(MODE, LAW, threadIdx.x);
@@ -177,9 +182,26 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     return false;
   };
 
+  // weight gradient: a split whose row range is empty contributes zeros
+  auto zero_tile = [&](const Tile& t) {
+    float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(t.split) * p.K * p.N : p.dW;
+    for (int idx = threadIdx.x; idx < BM * BN / 4; idx += kThreads) {
+      const int32_t r = t.rstart + idx / (BN / 4);
+      const int32_t c = t.cstart + (idx % (BN / 4)) * 4;
+      if (r < t.rend && c < t.cend)
+        *reinterpret_cast<float4*>(out + static_cast<int64_t>(r) * p.N + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+
   Iter cit{0, static_cast<int32_t>(blockIdx.x >> 3)};
   Tile ct;
   if (!advance(cit, ct)) return;
+  if constexpr (MODE == kModeBwdWeight) {
+    while (ct.nsteps == 0) {
+      zero_tile(ct);
+      if (!advance(cit, ct)) return;
+    }
+  }
 
   // ---- load side: tile lt (sequence number lseq, step ls), next tile ln ----
   Iter lit = cit;
@@ -194,6 +216,20 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     rl[j] = row < lt.nrows ? p.perm[lt.pos0 + row] : -1;
   }
   bool has_ln = advance(lit, ln);
+  // the load side passes over tiles without K steps (weight-gradient splits
+  // with empty row ranges); the compute side writes their zeros
+  auto skip_empty = [&]() {
+    if constexpr (MODE == kModeBwdWeight) {
+      while (lvalid && lt.nsteps == 0) {
+        if (has_ln) {
+          lt = ln;
+          has_ln = advance(lit, ln);
+        } else {
+          lvalid = false;
+        }
+      }
+    }
+  };
 
   // A stage is copied in three parts so that the copies can be spread over
   // the MFMAs of the step being computed: stage_begin picks the stage's K
@@ -227,6 +263,22 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   auto stage_copy = [&](int j) {
     if (!lvalid) return;
     const int ii = wave + kWaves * j;
+    if constexpr (MODE == kModeBwdWeight) {
+      // A = X rows (type-sorted copy) over the tile's K columns, B = dY rows
+      // over its N columns; 2 positions of 256 columns per copy, both
+      // N-contiguous like W in the forward product
+      const int kr = 2 * ii + (lane >> 5);
+      const int c = (lane & 31) ^ (4 * (kr & 3));
+      const int32_t pos = sk0 + kr;
+      const int32_t ka = lt.rstart + 8 * c;
+      const int32_t nb = lt.cstart + 8 * c;
+      const bool pin = pos < skend;
+      const void* ga = (pin && ka < lt.rend) ? static_cast<const void*>(Ag + static_cast<int64_t>(pos) * p.K + ka) : zero;
+      const void* gb = (pin && nb < lt.cend) ? static_cast<const void*>(Bg + static_cast<int64_t>(pos) * p.N + nb) : zero;
+      dma16(ga, lds_addr(sA + ii * 1024));
+      dma16(gb, lds_addr(sB + ii * 1024));
+      return;
+    }
     {
       // A: gathered K-contiguous rows, 8 rows per copy
       const int64_t lda = (MODE == kModeFwd) ? p.K : p.N;
@@ -279,6 +331,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         ++lseq;
         ls = 0;
         has_ln = advance(lit, ln);
+        skip_empty();
       } else {
         lvalid = false;
       }
@@ -287,7 +340,30 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   static_assert(DMA_A == 4 && DMA_B == 4, "one A and one B copy per K slice of a step");
 
   // fragments of one 16-wide K slice
+  // 8 consecutive K values of one column from an N-contiguous tile, by two
+  // transposing reads (K rows k and k + 4 of each 4 x 16 block)
+  auto tr_frag = [&](const char* T, int k, int col) -> uint4 {
+    const char* a0 = T + kcol_off(k, col >> 3) + ((col >> 2) & 1) * 8;
+    const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0));
+    const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0 + 4 * 512));
+    uint4 f;
+    f.x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
+    f.y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
+    f.z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
+    f.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
+    return f;
+  };
   auto read_frags = [&](const char* As, const char* Bs, int rs, uint4 (&fa)[4], uint4 (&fb)[2]) {
+    if constexpr (MODE == kModeBwdWeight) {
+      const int gq = lane >> 4, pp = lane & 15;
+      const int k = 16 * rs + 8 * (gq >> 1) + (pp >> 2);
+      const int cq = 16 * (gq & 1) + 4 * (pp & 3);
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) fa[mi] = tr_frag(As, k, wm * 128 + mi * 32 + cq);
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) fb[ni] = tr_frag(Bs, k, wn * 64 + ni * 32 + cq);
+      return;
+    }
     const int kp = 2 * rs + lh;
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
@@ -326,11 +402,12 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
 
   // prologue: the first tile's rows for its epilogue, then stage 0
-  if (wave < 4) {
+  if (MODE != kModeBwdWeight && wave < 4) {
     const int r = 64 * wave + lane;
     dma4(r < ct.nrows ? static_cast<const void*>(p.perm + ct.pos0 + r) : zero,
          lds_addr(&rows_s[0][64 * wave]));
   }
+  skip_empty();
   stage_begin(0);
 #pragma unroll
   for (int j = 0; j < DMA_A; ++j) stage_copy(j);
@@ -362,6 +439,23 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     if (++cs < ct.nsteps) continue;
 
     // ---- epilogue of tile ct ----
+    if constexpr (MODE == kModeBwdWeight) {
+      // dW rows k (C rows) x 4 consecutive columns n per lane group
+      float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(ct.split) * p.K * p.N : p.dW;
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) {
+        const int32_t k = ct.rstart + wm * 128 + mi * 32 + lr;
+        float* yr = out + static_cast<int64_t>(k) * p.N + ct.cstart + wn * 64 + 4 * lh;
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+            if (k < ct.rend && ct.cstart + wn * 64 + ni * 32 + 8 * a + 4 * lh < ct.cend)
+              *reinterpret_cast<float4*>(yr + ni * 32 + 8 * a) =
+                  make_float4(acc[mi][ni][4 * a], acc[mi][ni][4 * a + 1], acc[mi][ni][4 * a + 2],
+                              acc[mi][ni][4 * a + 3]);
+      }
+    } else
     // The arithmetic runs over all 128 accumulators of the lane without
     // control flow (so independent values interleave); only the memory
     // accesses are predicated on the row and column being inside the tile.
@@ -459,6 +553,17 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       store_tile(p.Y);
     }
     if (!advance(cit, ct)) break;
+    if constexpr (MODE == kModeBwdWeight) {
+      bool more = true;
+      while (ct.nsteps == 0) {
+        zero_tile(ct);
+        if (!advance(cit, ct)) {
+          more = false;
+          break;
+        }
+      }
+      if (!more) break;
+    }
     ++cseq;
     cs = 0;
 #pragma unroll
@@ -508,7 +613,65 @@ int gemm_async_tile_n() { return BN; }
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream) {
   if (mode == kModeFwd) return launch_async<kModeFwd>(p, upper_tiles, cus, stream);
+  if (mode == kModeBwdWeight)
+    return p.law == 1 ? launch_one<kModeBwdWeight, 1, kActNone>(p, upper_tiles, cus, stream)
+                      : launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream);
   return launch_async<kModeBwdData>(p, upper_tiles, cus, stream);
+}
+
+namespace {
+
+// dst row r = src row perm[r] for the rows of valid type (r < offsets[q]),
+// 16 bytes per thread
+__global__ void gather_rows_kernel(const uint16_t* __restrict__ src, int32_t width,
+                                   const int32_t* __restrict__ perm,
+                                   const int32_t* __restrict__ offsets, int q, int32_t M,
+                                   uint16_t* __restrict__ dst) {
+  const int32_t rows = offsets[q];
+  const int32_t per_row = width / 8;
+  const int64_t total = static_cast<int64_t>(M) * per_row;
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int32_t r = static_cast<int32_t>(i / per_row);
+    if (r >= rows) continue;
+    const int32_t c = static_cast<int32_t>(i - static_cast<int64_t>(r) * per_row) * 8;
+    *reinterpret_cast<uint4*>(dst + static_cast<int64_t>(r) * width + c) =
+        *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(perm[r]) * width + c);
+  }
+}
+
+// part[c][n] = sum of rows [c * chunk, (c + 1) * chunk) of the first
+// offsets[q] rows of the bf16 matrix src [rows][N], summed in row order
+__global__ void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
+                                  const int32_t* __restrict__ offsets, int q, int32_t chunk,
+                                  float* __restrict__ part) {
+  const int32_t rows = offsets[q];
+  const int32_t c = blockIdx.y;
+  const int32_t n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  const int32_t r0 = c * chunk, r1 = min(rows, r0 + chunk);
+  float sum = 0.f;
+  for (int32_t r = r0; r < r1; ++r) sum += bf16_to_f32(src[static_cast<int64_t>(r) * N + n]);
+  part[static_cast<int64_t>(c) * N + n] = sum;
+}
+
+}  // namespace
+
+hipError_t launch_gather_rows(const uint16_t* src, int32_t width, const int32_t* perm,
+                              const int32_t* offsets, int q, int32_t M, uint16_t* dst,
+                              hipStream_t stream) {
+  const int64_t total = static_cast<int64_t>(M) * (width / 8);
+  const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(4096, (total + 255) / 256)));
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(256), 0, stream, src, width, perm,
+                     offsets, q, M, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* offsets, int q,
+                             int32_t chunk, int nchunks, float* part, hipStream_t stream) {
+  hipLaunchKernelGGL(column_sum_kernel, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
+                     N, offsets, q, chunk, part);
+  return hipGetLastError();
 }
 
 }  // namespace starq
