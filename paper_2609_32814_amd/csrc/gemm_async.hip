@@ -156,30 +156,35 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   __syncthreads();
 
   // ---- tile iterators (the compute side and the load side walk one list) ----
+  // XCD x (workgroups w with w % 8 == x) owns a contiguous chunk of each
+  // pass's tiles; its workgroups deal out the two chunks as one list, pass 0
+  // (the longer, two-segment contractions) first, so that a workgroup that
+  // got two long tiles gets no short one and the steps per workgroup even
+  // out.
   const int xcd = blockIdx.x & 7;
   const int slot_stride = gridDim.x >> 3;
+  int32_t pbase[2], pcount[2];
+#pragma unroll
+  for (int ps = 0; ps < 2; ++ps) {
+    const int32_t total = pfx_s[ps][q];
+    const int32_t chunk = (total + 7) >> 3;
+    pbase[ps] = xcd * chunk;
+    pcount[ps] = max(0, min(total - xcd * chunk, chunk));
+  }
   struct Iter {
-    int pass;
-    int32_t slot;
+    int32_t v;  // position in this XCD's list
   };
   auto advance = [&](Iter& it, Tile& t) -> bool {
-    while (it.pass < 2) {
-      const int32_t total = pfx_s[it.pass][q];
-      const int32_t chunk = (total + 7) >> 3;
-      const int32_t logical = xcd * chunk + it.slot;
-      if (it.slot >= chunk || logical >= total) {
-        ++it.pass;
-        it.slot = blockIdx.x >> 3;
-        continue;
-      }
-      it.slot += slot_stride;
-      int cls = 0;
-      while (logical >= pfx_s[it.pass][cls + 1]) ++cls;
-      t = make_tile<MODE, LAW, BN, BK>(p, sel_for(MODE, LAW, it.pass), cls,
-                                       logical - pfx_s[it.pass][cls], units_s[cls], offs_s);
-      return true;
-    }
-    return false;
+    const int32_t v = it.v;
+    if (v >= pcount[0] + pcount[1]) return false;
+    it.v += slot_stride;
+    const int ps = v < pcount[0] ? 0 : 1;
+    const int32_t logical = pbase[ps] + (ps == 0 ? v : v - pcount[0]);
+    int cls = 0;
+    while (logical >= pfx_s[ps][cls + 1]) ++cls;
+    t = make_tile<MODE, LAW, BN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pfx_s[ps][cls],
+                                     units_s[cls], offs_s);
+    return true;
   };
 
   // weight gradient: a split whose row range is empty contributes zeros
@@ -193,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     }
   };
 
-  Iter cit{0, static_cast<int32_t>(blockIdx.x >> 3)};
+  Iter cit{static_cast<int32_t>(blockIdx.x >> 3)};
   Tile ct;
   if (!advance(cit, ct)) return;
   if constexpr (MODE == kModeBwdWeight) {
@@ -641,18 +646,39 @@ __global__ void gather_rows_kernel(const uint16_t* __restrict__ src, int32_t wid
 }
 
 // part[c][n] = sum of rows [c * chunk, (c + 1) * chunk) of the first
-// offsets[q] rows of the bf16 matrix src [rows][N], summed in row order
-__global__ void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
-                                  const int32_t* __restrict__ offsets, int q, int32_t chunk,
-                                  float* __restrict__ part) {
+// offsets[q] rows of the bf16 matrix src [rows][N].  A block covers 256
+// columns: thread (g, r) adds 8 columns (one 16-byte load per row) over rows
+// r, r + 8, ... of the chunk in order, then the 8 row lanes are added in
+// order through LDS, so the result does not depend on scheduling.
+__global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
+                                                         const int32_t* __restrict__ offsets, int q,
+                                                         int32_t chunk, float* __restrict__ part) {
+  __shared__ float red[8][256 + 4];
   const int32_t rows = offsets[q];
   const int32_t c = blockIdx.y;
-  const int32_t n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
+  const int g = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int32_t n0 = blockIdx.x * 256 + 8 * g;
   const int32_t r0 = c * chunk, r1 = min(rows, r0 + chunk);
-  float sum = 0.f;
-  for (int32_t r = r0; r < r1; ++r) sum += bf16_to_f32(src[static_cast<int64_t>(r) * N + n]);
-  part[static_cast<int64_t>(c) * N + n] = sum;
+  float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (n0 < N) {
+    for (int32_t r = r0 + rl; r < r1; r += 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r) * N + n0);
+      sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
+      sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
+      sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
+      sum[6] += bf16_to_f32(v.w & 0xffffu); sum[7] += bf16_to_f32(v.w >> 16);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rl][8 * g + e] = sum[e];
+  __syncthreads();
+  const int32_t n = blockIdx.x * 256 + threadIdx.x;
+  if (n < N) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += red[k][threadIdx.x];
+    part[static_cast<int64_t>(c) * N + n] = t;
+  }
 }
 
 }  // namespace
