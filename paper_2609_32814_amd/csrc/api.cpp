@@ -212,12 +212,13 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers) {
   sp.part = cur;
   cur = align_up(cur + sizeof(float) * sp.ns * M * D);
   sp.cnt = cur;
-  cur = align_up(cur + sizeof(int32_t) * (3 + sp.nt_dn));
+  cur = align_up(cur + sizeof(int32_t) * decode_stack_counters(sp.nt_dn));
   sp.end = cur;
   bool same_groups = u.q == d.q && u.law == d.law;
   for (int g = 0; same_groups && g <= u.q; ++g) same_groups = d.S[g] == u.R[g] && d.R[g] == u.S[g];
   sp.ok = M >= 1 && M <= kDecodeMaxRows && n_layers <= kStackMaxLayers && same_groups &&
-          decode_stack_smem(static_cast<int>(M), static_cast<int>(std::max<int64_t>(D, sp.kc))) > 0 &&
+          decode_stack_smem(static_cast<int>(M), static_cast<int>(std::max<int64_t>(D, sp.kc)), static_cast<int>(D),
+                            sp.ns) > 0 &&
           sp.grid <= cu_count();
   return sp;
 }
@@ -740,7 +741,7 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
     k.h = at<float>(ws, sp.h);
     k.part = at<float>(ws, sp.part);
     k.cnt = at<int32_t>(ws, sp.cnt);
-    st = hip_status(launch_fill_zero(reinterpret_cast<float*>(k.cnt), 3 + sp.nt_dn, stream));
+    st = hip_status(launch_fill_zero(reinterpret_cast<float*>(k.cnt), decode_stack_counters(sp.nt_dn), stream));
     if (st != STAR_OK) return st;
     return hip_status(launch_decode_stack(k, sp.grid, stream));
   }

@@ -18,13 +18,26 @@
 //
 // Cross-workgroup data (H, the next layer's input, the residual, the
 // partial sums) is written with agent-coherent stores and read with
-// agent-coherent loads (copies into LDS with sc0 sc1), so no cache
+// agent-coherent loads (copies into LDS with sc1), so no cache
 // write-back or invalidate is needed; arrival counters are agent-scope
 // atomics that only grow (a layer's target is a multiple of the item
-// count).  The down chunks of one tile are summed by whichever of its
-// workgroups arrives last, in chunk order, so results do not depend on
-// timing.  Every wait is bounded: after about half a second of spinning the
-// kernel raises the error flag and carries on, so it always terminates.
+// count).  An all-workgroup arrival is spread over kSubCounters counters,
+// each on its own 256-byte line, and a waiter sums them with one vector
+// load: many workgroups adding to one address serialise at the memory
+// side, which on this part costs more than the extra lanes of the poll.
+// The slice plan of an item depends only on the row types, so it is made
+// once per launch; each layer only issues the copies.
+//
+// Summing the down chunks, in chunk order either way, so results do not
+// depend on timing: for a few rows (RES kernels) every workgroup keeps the
+// running state h in LDS and, once all chunks of a layer have arrived,
+// sums them itself into its copy of h and into the next up input (two
+// hand-offs per layer); for more rows the chunks of one tile are summed by
+// whichever of its workgroups arrives last, which writes h and the next
+// input for everyone (three hand-offs).  The last layer always sums by last
+// arrival, to write Y.  Every wait is bounded: after about half a second of
+// spinning the kernel raises the error flag and carries on, so it always
+// terminates.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -122,6 +135,11 @@ __device__ __forceinline__ Item down_item(const DecodeStack& p) {
   return it;
 }
 
+// MB: 16-row blocks of the step (M <= 16 MB).  RES: the running state h is
+// kept in every workgroup's LDS (small M only) and the next layer's up
+// items sum the down chunks themselves, so a layer needs two hand-offs
+// instead of three; the last layer still sums by last arrival to write Y.
+template <int MB, bool RES>
 __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStack p) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // per weight slot (0: up item, 1: down item): rows needing each K group,
@@ -138,26 +156,30 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int M = p.M;
-  const int mblocks = (M + 15) >> 4;
   const int kmax = (max(p.D, p.kc) + 127) & ~127;
+  constexpr int NOFF = kMaxSlices / 4;  // slices per wave and slot
   // staging writes whole 1 KB copies, so round the x buffer up to 1 KB
   const int xbytes = max((M * kmax * 2 + 1023) & ~1023, kRedBytes);
   char* xbuf = lds;
   char* slot_base[2] = {lds + xbytes, lds + xbytes + (kmax / SLICE) * 1024};
-  int32_t* cnt_up = p.cnt;
-  int32_t* cnt_dn = p.cnt + 1;
-  int32_t* err = p.cnt + 2;
-  int32_t* tile_cnt = p.cnt + 3;
+  // RES: the running state [M][D] fp32, then the staging of the down
+  // chunks, res_rows rows at a time (chunk c at stg + c * cstride bytes)
+  float* hres = reinterpret_cast<float*>(lds + xbytes + 2 * (kmax / SLICE) * 1024);
+  char* stg = reinterpret_cast<char*>(hres) + ((M * p.D * 4 + 1023) & ~1023);
+  const int cstride = (p.res_rows * p.D * 4 + 1023) & ~1023;
+  int32_t* err = p.cnt;
+  int32_t* cnt_up = p.cnt + kCounterStride;
+  int32_t* cnt_dn = cnt_up + kCounterStride * kSubCounters;
+  int32_t* tile_cnt = cnt_dn + kCounterStride * kSubCounters;  // one line per down tile
   const void* zero = g_stack_zero;
 
   const Item iu = up_item(p);
   const Item idn = down_item(p);
 
   // Which rows need input group g for output group j (one ballot per
-  // group by wave 0), then the needed slices of [k_lo, k_hi) in K order,
-  // then the copies of those slices of W into the slot.
-  auto plan_and_copy = [&](int slot, const Item& it, const int32_t* KS, const uint16_t* W,
-                           int32_t ldw) {
+  // group by wave 0), then the needed slices of [k_lo, k_hi) in K order and
+  // the rows each 8-wide piece of them serves.
+  auto plan = [&](int slot, const Item& it, const int32_t* KS) {
     if (wave == 0) {
       const int t = lane < M ? p.types[lane] : -1;
       for (int g = 0; g < p.q; ++g) {
@@ -188,26 +210,54 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       const int32_t k = it.k_lo + slices_s[slot][tid >> 2] * SLICE + 8 * (tid & 3);
       pmask_s[slot][tid >> 2][tid & 3] = k < it.k_hi ? rowmask_s[slot][group_of(KS, p.q, k)] : 0ull;
     }
-    // (read by compute after the barrier that precedes it)
-    char* sb = slot_base[slot];
-    for (int i = wave; i < ns_; i += 4) {
-      int32_t row = it.k_lo + slices_s[slot][i] * SLICE + (lane >> 1);
-      row = row < it.k_hi ? row : it.k_hi - 1;  // finite filler, its inputs are zero
-      int32_t col = it.n0 + 8 * (lane & 1);
-      col = col < it.nend ? col : it.n0;
-      dma16(W + static_cast<int64_t>(row) * ldw + col, lds_addr(sb + i * 1024));
-    }
+    __syncthreads();
   };
 
-  // Bounded wait until *c >= target (thread 0 spins, the others wait at the
-  // barrier).
-  auto wait_for = [&](int32_t* c, int32_t target) {
-    if (tid == 0) {
+  // Element offsets into W of this lane's 16 bytes of slice wave + 4 t of a
+  // slot, computed once: the per-layer copies then issue without waiting on
+  // LDS.  Slices past the plan get offset -1.
+  auto copy_offsets = [&](int slot, const Item& it, int32_t ldw, int32_t (&off)[NOFF]) {
+    const int ns_ = nslices_s[slot];
+#pragma unroll
+    for (int t = 0; t < NOFF; ++t) {
+      const int i = wave + 4 * t;
+      off[t] = -1;
+      if (i < ns_) {
+        int32_t row = it.k_lo + slices_s[slot][i] * SLICE + (lane >> 1);
+        row = row < it.k_hi ? row : it.k_hi - 1;  // finite filler, its inputs are zero
+        int32_t col = it.n0 + 8 * (lane & 1);
+        col = col < it.nend ? col : it.n0;
+        off[t] = row * ldw + col;
+      }
+    }
+  };
+  auto copy = [&](int slot, const uint16_t* W, const int32_t (&off)[NOFF]) {
+    char* sb = slot_base[slot];
+#pragma unroll
+    for (int t = 0; t < NOFF; ++t)
+      if (off[t] >= 0) dma16(W + off[t], lds_addr(sb + (wave + 4 * t) * 1024));
+  };
+
+  // Arrival on this workgroup's sub-counter of a set, and a bounded wait
+  // until the set's sum reaches target (wave 0 polls, the others wait at
+  // the barrier).
+  auto arrive = [&](int32_t* set) {
+    __hip_atomic_fetch_add(set + kCounterStride * (blockIdx.x % kSubCounters), 1, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto wait_for = [&](int32_t* set, int32_t target) {
+    if (wave == 0) {
       int spins = 0;
-      while (static_cast<int32_t>(ld_agent(reinterpret_cast<uint32_t*>(c))) < target) {
+      while (true) {
+        int32_t v = lane < kSubCounters
+                        ? static_cast<int32_t>(ld_agent(reinterpret_cast<uint32_t*>(set + kCounterStride * lane)))
+                        : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+        if (v >= target) break;
         __builtin_amdgcn_s_sleep(1);
         if (++spins > kSpinLimit) {
-          st_agent(reinterpret_cast<uint32_t*>(err), 1u);
+          if (lane == 0) st_agent(reinterpret_cast<uint32_t*>(err), 1u);
           break;
         }
       }
@@ -235,90 +285,163 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
     }
   };
 
+  // RES, layer l >= 1: h_l = sum of the down chunks of layer l - 1 (chunk
+  // order) + bias (+ h_{l-1}), kept in hres and written as the swizzled bf16
+  // up input (K = D, padded to a multiple of 128 with zeros).  The chunks
+  // come in by agent-coherent copies into the staging area, res_rows rows
+  // at a time; each thread then takes pairs of columns.
+  auto stage_resident = [&](int l) {
+    const int kx = (p.D + 127) & ~127;
+    const int half = kx / 2;
+    const float* b = p.bd[l - 1];
+    for (int m0 = 0; m0 < M; m0 += p.res_rows) {
+      const int rows = min(p.res_rows, M - m0);
+      const int bytes = rows * p.D * 4;
+      const int nblk = (bytes + 1023) >> 10;
+      for (int c = 0; c < p.ns; ++c) {
+        const char* src = reinterpret_cast<const char*>(p.part + (static_cast<int64_t>(c) * M + m0) * p.D);
+        for (int blk = wave; blk < nblk; blk += 4) {
+          const int o = blk * 1024 + lane * 16;
+          const void* g = o < bytes ? static_cast<const void*>(src + o) : zero;
+          dma16_sys(g, lds_addr(stg + c * cstride + blk * 1024));
+        }
+      }
+      wait_vm_all();
+      __syncthreads();
+      for (int e = tid; e < rows * half; e += kThreads) {
+        const int mm = e / half;
+        const int m = m0 + mm;
+        const int k = 2 * (e - mm * half);
+        uint32_t packed = 0;
+        if (k < p.D) {
+          float v0 = 0.f, v1 = 0.f;
+          for (int c = 0; c < p.ns; ++c) {
+            const float2 w = *reinterpret_cast<const float2*>(stg + c * cstride + (mm * p.D + k) * 4);
+            v0 += w.x;
+            v1 += w.y;
+          }
+          if (b) {
+            v0 += b[k];
+            v1 += b[k + 1];
+          }
+          float* hr = hres + m * p.D + k;
+          if (p.residual) {
+            v0 += hr[0];
+            v1 += hr[1];
+          }
+          hr[0] = v0;
+          hr[1] = v1;
+          packed = f32_to_bf16(v0) | (static_cast<uint32_t>(f32_to_bf16(v1)) << 16);
+        }
+        const int c = (k >> 3) ^ (m & 15);
+        *reinterpret_cast<uint32_t*>(xbuf + (m * kx + 8 * c + (k & 7)) * 2) = packed;
+      }
+      __syncthreads();  // the staging area is free for the next rows
+    }
+  };
+
   // acc over the item's slices; lane group G = lane / 16 holds K rows
-  // 8G..8G+7 of a slice for column n0 + lane % 16, and rows 16 mb + lane % 16
-  auto compute = [&](int slot, const Item& it, f32x4_t (&acc)[4]) {
+  // 8G..8G+7 of a slice for column n0 + lane % 16, and rows 16 mb + lane % 16.
+  // A wave's slices are wave, wave + 4, ...; RB of them have their LDS reads
+  // in flight together.
+  constexpr int RB = MB == 1 ? 8 : (MB == 2 ? 4 : 2);
+  auto compute = [&](int slot, const Item& it, f32x4_t (&acc)[MB]) {
     const int G = lane >> 4;
     const int pl = lane & 15;
     const int kx = (it.k_hi - it.k_lo + 127) & ~127;
     const int ns_ = nslices_s[slot];
     const char* sb = slot_base[slot];
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    // operands of slice i: the weight fragment and the masked input pieces
-    auto load = [&](int i, uint4& wf, uint4 (&xv)[4]) {
-      const char* base = sb + i * 1024 + (8 * G + (pl >> 2)) * 32 + (pl & 3) * 8;
-      const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base));
-      const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base + 128));
-      wf.x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
-      wf.y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
-      wf.z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
-      wf.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
-      const int32_t krel = slices_s[slot][i] * SLICE + 8 * G;
-      const unsigned long long gm = pmask_s[slot][i][G];
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int t0 = 0; wave + 4 * t0 < ns_; t0 += RB) {
+      uint4 wf[RB], xv[RB][MB];
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        if (mb < mblocks) {
-          const int m = 16 * mb + pl;
-          const int mr = min(m, M - 1);  // rows past M read row M - 1, then zero
-          const int c = (krel >> 3) ^ (mr & 15);
-          xv[mb] = *reinterpret_cast<const uint4*>(xbuf + (mr * kx + 8 * c) * 2);
-          if (!(m < M && ((gm >> m) & 1ull))) xv[mb] = make_uint4(0, 0, 0, 0);
+      for (int r = 0; r < RB; ++r) {
+        const int i = wave + 4 * (t0 + r);
+        if (i < ns_) {
+          const char* base = sb + i * 1024 + (8 * G + (pl >> 2)) * 32 + (pl & 3) * 8;
+          const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base));
+          const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base + 128));
+          wf[r].x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
+          wf[r].y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
+          wf[r].z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
+          wf[r].w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
+          const int32_t krel = slices_s[slot][i] * SLICE + 8 * G;
+          const unsigned long long gm = pmask_s[slot][i][G];
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const int m = 16 * mb + pl;
+            const int mr = min(m, M - 1);  // rows past M read row M - 1, then zero
+            const int c = (krel >> 3) ^ (mr & 15);
+            xv[r][mb] = *reinterpret_cast<const uint4*>(xbuf + (mr * kx + 8 * c) * 2);
+            if (!(m < M && ((gm >> m) & 1ull))) xv[r][mb] = make_uint4(0, 0, 0, 0);
+          }
         }
       }
-    };
-    auto mfma = [&](const uint4& wf, const uint4 (&xv)[4]) {
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        if (mb < mblocks)
-          // D[n][m] += W^T x^T: the lane ends with 4 consecutive columns of row m
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf),
-                                                            __builtin_bit_cast(bf16x8_t, xv[mb]),
-                                                            acc[mb], 0, 0, 0);
-    };
-    // two slices per round: both slices' LDS reads are in flight together
-    for (int i0 = wave; i0 < ns_; i0 += 8) {
-      uint4 wf0, wf1, xv0[4], xv1[4];
-      load(i0, wf0, xv0);
-      const bool two = i0 + 4 < ns_;
-      if (two) load(i0 + 4, wf1, xv1);
-      mfma(wf0, xv0);
-      if (two) mfma(wf1, xv1);
+      for (int r = 0; r < RB; ++r) {
+        if (wave + 4 * (t0 + r) < ns_) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+            // D[n][m] += W^T x^T: the lane ends with 4 consecutive columns of row m
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf[r]),
+                                                              __builtin_bit_cast(bf16x8_t, xv[r][mb]),
+                                                              acc[mb], 0, 0, 0);
+        }
+      }
     }
   };
 
   // Fixed-order sum of the four waves' partials (through LDS, reusing the
   // x buffer); thread tid then owns rows 16 mb + l % 16, columns
-  // n0 + 4 (l / 16) .. + 3 with mb = tid / 64, l = tid % 64.
-  auto reduce = [&](f32x4_t (&acc)[4], f32x4_t& z) {
+  // n0 + 4 (l / 16) .. + 3 with mb = tid / 64, l = tid % 64 (mb < MB).
+  auto reduce = [&](f32x4_t (&acc)[MB], f32x4_t& z) {
     __syncthreads();  // every wave is done with the x buffer
     f32x4_t* red = reinterpret_cast<f32x4_t*>(xbuf);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) red[(wave * 4 + mb) * 64 + lane] = acc[mb];
+    for (int mb = 0; mb < MB; ++mb) red[(wave * 4 + mb) * 64 + lane] = acc[mb];
     __syncthreads();
     const int mb = tid >> 6;
-    z = red[(0 * 4 + mb) * 64 + lane];
-    z += red[(1 * 4 + mb) * 64 + lane];
-    z += red[(2 * 4 + mb) * 64 + lane];
-    z += red[(3 * 4 + mb) * 64 + lane];
+    z = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (mb < MB) {
+      z = red[(0 * 4 + mb) * 64 + lane];
+      z += red[(1 * 4 + mb) * 64 + lane];
+      z += red[(2 * 4 + mb) * 64 + lane];
+      z += red[(3 * 4 + mb) * 64 + lane];
+    }
   };
 
   const int my_m = 16 * (tid >> 6) + (lane & 15);
   const int my_dn = 4 * (lane >> 4);
 
-  // prologue: weights of layer 0's items
-  if (iu.valid) plan_and_copy(0, iu, p.SD, p.Wu[0], p.F);
-  if (idn.valid) plan_and_copy(1, idn, p.SF, p.Wd[0], p.D);
+  // prologue: slice plans and copy offsets, then the weights of layer 0
+  int32_t off_u[NOFF], off_d[NOFF];
+  if (iu.valid) plan(0, iu, p.SD);
+  if (idn.valid) plan(1, idn, p.SF);
+  if (iu.valid) copy_offsets(0, iu, p.F, off_u);
+  if (idn.valid) copy_offsets(1, idn, p.D, off_d);
+  if (iu.valid) copy(0, p.Wu[0], off_u);
+  if (idn.valid) copy(1, p.Wd[0], off_d);
+  if (RES) {
+    for (int e = tid; e < M * p.D; e += kThreads) hres[e] = bf16_to_f32(p.X[e]);
+  }
 
+  const int dn_per_layer = RES ? p.nt_dn * p.ns : p.nt_dn;
   for (int l = 0; l < p.L; ++l) {
+    const bool last = l + 1 == p.L;
     // ---------------- up projection: H = act(x W_up + b_up) ----------------
-    if (l > 0) wait_for(cnt_dn, p.nt_dn * l);
+    if (l > 0) {
+      wait_for(cnt_dn, dn_per_layer * l);
+      if (RES) stage_resident(l);
+    }
     if (iu.valid) {
-      const uint16_t* xin = (l == 0) ? p.X : p.hb + static_cast<int64_t>(l & 1) * M * p.D;
-      stage_x(iu, xin, p.D);
-      wait_vm_all();
-      __syncthreads();
-      f32x4_t acc[4], z;
+      if (!RES || l == 0) {
+        const uint16_t* xin = (l == 0) ? p.X : p.hb + static_cast<int64_t>(l & 1) * M * p.D;
+        stage_x(iu, xin, p.D);
+        wait_vm_all();
+        __syncthreads();
+      }
+      f32x4_t acc[MB], z;
       compute(0, iu, acc);
       reduce(acc, z);
       const int32_t n = iu.n0 + my_dn;
@@ -337,10 +460,10 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       }
       wait_vm_all();  // the stores have reached the coherent level
       __syncthreads();
-      if (tid == 0) __hip_atomic_fetch_add(cnt_up, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (tid == 0) arrive(cnt_up);
       // slot 0 is free (every wave passed the barriers above): the next
       // layer's up weights stream in while this workgroup waits
-      if (l + 1 < p.L) plan_and_copy(0, iu, p.SD, p.Wu[l + 1], p.F);
+      if (!last) copy(0, p.Wu[l + 1], off_u);
     }
 
     // ---------------- down projection: h += H W_down + b_down ----------------
@@ -350,7 +473,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       stage_x(idn, p.H, p.F);
       wait_vm_all();
       __syncthreads();
-      f32x4_t acc[4], z;
+      f32x4_t acc[MB], z;
       compute(1, idn, acc);
       reduce(acc, z);
       const int32_t n = idn.n0 + my_dn;
@@ -362,55 +485,65 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       }
       wait_vm_all();
       __syncthreads();
-      if (tid == 0) {
-        const int old = __hip_atomic_fetch_add(tile_cnt + ct, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        flag_s = (old == p.ns * (l + 1) - 1);
-      }
-      __syncthreads();
-      if (flag_s) {
-        // last chunk of this tile to arrive: sum the chunks in order
-        if (mine) {
-          float v[4] = {0.f, 0.f, 0.f, 0.f};
-          for (int c = 0; c < p.ns; ++c) {
-            const uint32_t* src = reinterpret_cast<const uint32_t*>(
-                p.part + (static_cast<int64_t>(c) * M + my_m) * p.D + n);
+      if (RES && !last) {
+        // the next layer's up items sum the chunks
+        if (tid == 0) arrive(cnt_dn);
+      } else {
+        if (tid == 0) {
+          const int old =
+              __hip_atomic_fetch_add(tile_cnt + kCounterStride * ct, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          // RES: the tile counters count the last layer only
+          flag_s = (old == (RES ? p.ns - 1 : p.ns * (l + 1) - 1));
+        }
+        __syncthreads();
+        if (flag_s) {
+          // last chunk of this tile to arrive: sum the chunks in order
+          if (mine) {
+            float v[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int c = 0; c < p.ns; ++c) {
+              const uint32_t* src = reinterpret_cast<const uint32_t*>(
+                  p.part + (static_cast<int64_t>(c) * M + my_m) * p.D + n);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(ld_agent(src + e));
-          }
-          const float* b = p.bd[l];
-          if (b) {
-            const float4 bv = *reinterpret_cast<const float4*>(b + n);
-            v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
-          }
-          const int64_t o = static_cast<int64_t>(my_m) * p.D + n;
-          if (p.residual) {
-            if (l == 0) {
-              const uint2 xi = *reinterpret_cast<const uint2*>(p.X + o);
-              v[0] += bf16_to_f32(xi.x & 0xffffu); v[1] += bf16_to_f32(xi.x >> 16);
-              v[2] += bf16_to_f32(xi.y & 0xffffu); v[3] += bf16_to_f32(xi.y >> 16);
+              for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(ld_agent(src + e));
+            }
+            const float* b = p.bd[l];
+            if (b) {
+              const float4 bv = *reinterpret_cast<const float4*>(b + n);
+              v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+            }
+            const int64_t o = static_cast<int64_t>(my_m) * p.D + n;
+            if (p.residual) {
+              if (RES) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] += hres[o + e];
+              } else if (l == 0) {
+                const uint2 xi = *reinterpret_cast<const uint2*>(p.X + o);
+                v[0] += bf16_to_f32(xi.x & 0xffffu); v[1] += bf16_to_f32(xi.x >> 16);
+                v[2] += bf16_to_f32(xi.y & 0xffffu); v[3] += bf16_to_f32(xi.y >> 16);
+              } else {
+                const uint32_t* hs = reinterpret_cast<const uint32_t*>(p.h + o);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(ld_agent(hs + e));
+              }
+            }
+            if (!last) {
+              uint32_t* hd = reinterpret_cast<uint32_t*>(p.h + o);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) st_agent(hd + e, __float_as_uint(v[e]));
+              uint32_t* xd = reinterpret_cast<uint32_t*>(p.hb + static_cast<int64_t>((l + 1) & 1) * M * p.D + o);
+              st_agent(xd, f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16));
+              st_agent(xd + 1, f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16));
             } else {
-              const uint32_t* hs = reinterpret_cast<const uint32_t*>(p.h + o);
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(ld_agent(hs + e));
+              for (int e = 0; e < 4; ++e) store_out(p.Y, p.ydtype, o + e, v[e]);
             }
           }
-          if (l + 1 < p.L) {
-            uint32_t* hd = reinterpret_cast<uint32_t*>(p.h + o);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) st_agent(hd + e, __float_as_uint(v[e]));
-            uint32_t* xd = reinterpret_cast<uint32_t*>(p.hb + static_cast<int64_t>((l + 1) & 1) * M * p.D + o);
-            st_agent(xd, f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16));
-            st_agent(xd + 1, f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16));
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) store_out(p.Y, p.ydtype, o + e, v[e]);
-          }
+          wait_vm_all();
+          __syncthreads();
+          if (tid == 0 && !last) arrive(cnt_dn);
         }
-        wait_vm_all();
-        __syncthreads();
-        if (tid == 0) __hip_atomic_fetch_add(cnt_dn, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      if (l + 1 < p.L) plan_and_copy(1, idn, p.SF, p.Wd[l + 1], p.D);
+      if (!last) copy(1, p.Wd[l + 1], off_d);
     }
   }
   wait_vm_all();
@@ -418,25 +551,60 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
 
 }  // namespace
 
-size_t decode_stack_smem(int M, int kmax) {
-  if (M < 1 || M > kDecodeMaxRows || kmax < SLICE || kmax > kMaxSlices * SLICE) return 0;
+// Rows per step up to which the running state stays in LDS (RES kernels).
+constexpr int kResidentMaxRows = 2;
+constexpr size_t kStackLdsCap = 150 * 1024;
+
+static size_t stack_lds_base(int M, int kmax) {
   kmax = (kmax + 127) & ~127;
   const size_t xbytes = std::max<size_t>((static_cast<size_t>(M) * kmax * 2 + 1023) & ~size_t(1023), kRedBytes);
-  const size_t total = xbytes + 2 * static_cast<size_t>(kmax / SLICE) * 1024;
-  return total <= 150 * 1024 ? total : 0;
+  return xbytes + 2 * static_cast<size_t>(kmax / SLICE) * 1024;
+}
+static size_t stack_lds_res(int M, int kmax, int D, int ns, int rows) {
+  const size_t state = (static_cast<size_t>(M) * D * 4 + 1023) & ~size_t(1023);
+  const size_t cstride = (static_cast<size_t>(rows) * D * 4 + 1023) & ~size_t(1023);
+  return stack_lds_base(M, kmax) + state + static_cast<size_t>(ns) * cstride;
+}
+// Rows of down chunks staged per round in a RES kernel (0: not resident).
+static int stack_res_rows(int M, int kmax, int D, int ns) {
+  if (M > kResidentMaxRows) return 0;
+  int rows = 0;
+  for (int r = 1; r <= M; ++r)
+    if (stack_lds_res(M, kmax, D, ns, r) <= kStackLdsCap) rows = r;
+  return rows;
+}
+
+size_t decode_stack_smem(int M, int kmax, int D, int ns) {
+  if (M < 1 || M > kDecodeMaxRows || kmax < SLICE || kmax > kMaxSlices * SLICE) return 0;
+  const int rows = stack_res_rows(M, kmax, D, ns);
+  const size_t total = rows > 0 ? stack_lds_res(M, kmax, D, ns, rows) : stack_lds_base(M, kmax);
+  return total <= kStackLdsCap ? total : 0;
+}
+
+template <int MB, bool RES>
+static hipError_t launch_stack(const DecodeStack& p, int grid, size_t smem, hipStream_t stream) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      kStackLdsCap);
+  if (attr != hipSuccess) return attr;
+  DecodeStack arg = p;
+  arg.res_rows = RES ? stack_res_rows(p.M, std::max(p.D, p.kc), p.D, p.ns) : 0;
+  void* args[] = {&arg};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), dim3(grid),
+                                    dim3(kThreads), args, static_cast<unsigned>(smem), stream);
 }
 
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream) {
-  const size_t smem = decode_stack_smem(p.M, std::max(p.D, p.kc));
+  const int kmax = std::max(p.D, p.kc);
+  const size_t smem = decode_stack_smem(p.M, kmax, p.D, p.ns);
   if (smem == 0) return hipErrorInvalidValue;
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(decode_stack_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-      150 * 1024);
-  if (attr != hipSuccess) return attr;
-  DecodeStack arg = p;
-  void* args[] = {&arg};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(decode_stack_kernel), dim3(grid),
-                                    dim3(kThreads), args, static_cast<unsigned>(smem), stream);
+  if (stack_res_rows(p.M, kmax, p.D, p.ns) > 0) return launch_stack<1, true>(p, grid, smem, stream);
+  switch ((p.M + 15) / 16) {
+    case 1: return launch_stack<1, false>(p, grid, smem, stream);
+    case 2: return launch_stack<2, false>(p, grid, smem, stream);
+    case 3: return launch_stack<3, false>(p, grid, smem, stream);
+    default: return launch_stack<4, false>(p, grid, smem, stream);
+  }
 }
 
 }  // namespace starq

@@ -120,6 +120,7 @@ constexpr int kStackMaxLayers = 32;
 struct DecodeStack {
   int32_t q, law, M, D, F, L, act, residual, ydtype;
   int32_t ns, kc;         // down projection: K split into ns chunks of kc
+  int32_t res_rows;       // set by the launcher: rows of down chunks staged per round
   int32_t nt_up, nt_dn;   // 16-column tiles of F and of D
   int32_t SD[kMaxQGroups + 1];   // D groups: up input, down output
   int32_t SF[kMaxQGroups + 1];   // F groups: up output, down input
@@ -136,10 +137,17 @@ struct DecodeStack {
   uint16_t* hb;   // [2][M][D] bf16, the next up projection's input (layer parity)
   float* h;       // [M][D] fp32 residual state
   float* part;    // [ns][M][D] fp32 down-projection partial sums
-  int32_t* cnt;   // [3 + nt_dn]: up arrivals, down arrivals, error flag, per-tile arrivals
+  int32_t* cnt;   // decode_stack_counters(nt_dn) int32: error flag, up and down arrival
+                  // sub-counters, per-tile down arrivals, each on its own 256-byte line
 };
+// Arrival counters: each sits alone on a 256-byte line (kCounterStride ints).
+constexpr int kCounterStride = 64;
+constexpr int kSubCounters = 32;
+inline int64_t decode_stack_counters(int nt_dn) {
+  return static_cast<int64_t>(kCounterStride) * (1 + 2 * kSubCounters + nt_dn);
+}
 // Dynamic LDS bytes the stack kernel needs, or 0 when the shape does not fit.
-size_t decode_stack_smem(int M, int kmax);
+size_t decode_stack_smem(int M, int kmax, int D, int ns);
 // Launches the stack kernel cooperatively on grid = max(nt_up, nt_dn * ns)
 // workgroups (all resident at once); p.cnt must be zero.
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);

@@ -331,8 +331,8 @@ def test_ffn_train_step_parity(P, q, D, F, M):
 
 # ---- decode -------------------------------------------------------------------------
 
-@pytest.mark.parametrize("M", [1, 8, 32, 64])
-@pytest.mark.parametrize("D,F,L", [(256, 1024, 3), (768, 3072, 12)])
+@pytest.mark.parametrize("M", [1, 8, 12, 20, 32, 64])
+@pytest.mark.parametrize("D,F,L", [(256, 1024, 1), (256, 1024, 3), (768, 3072, 12)])
 def test_decode_parity(P, M, D, F, L):
     import torch
     up_g, up_o = algs(P, 2, [D // 2] * 2, [F // 2] * 2)
