@@ -418,12 +418,33 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   for (int j = 0; j < DMA_A; ++j) stage_copy(j);
   stage_end();
 
+  // first columns of the lane's groups of 4 consecutive outputs
+  auto lcol = [&](int ni, int a) { return wn * 64 + ni * 32 + 8 * a + 4 * lh; };
+
   int32_t cseq = 0, cs = 0;
   int slot = 0;
   while (true) {
     wait_vm_all();    // this wave's copies for stage `slot` have landed
     block_barrier();  // and everyone's; the other slot (computed last step) is free
     stage_begin(slot ^ 1);
+    if (cs == 0) {
+      // a tile starts: the accumulators start from the bias (forward; its
+      // copy came with this step's operands) or from zero
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
+          if constexpr (MODE == kModeFwd) bv = *reinterpret_cast<const float4*>(&bias_s[cseq & (kRowBufs - 1)][lcol(ni, a)]);
+#pragma unroll
+          for (int mi = 0; mi < 4; ++mi) {
+            acc[mi][ni][4 * a + 0] = bv.x;
+            acc[mi][ni][4 * a + 1] = bv.y;
+            acc[mi][ni][4 * a + 2] = bv.z;
+            acc[mi][ni][4 * a + 3] = bv.w;
+          }
+        }
+    }
     {
       const char* As = smem + slot * STAGE_BYTES;
       const char* Bs = As + A_BYTES;
@@ -475,7 +496,6 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         rv[mi] = row < ct.nrows;
         rbase[mi] = static_cast<int64_t>(rv[mi] ? rows_s[buf][row] : 0) * ldc + ct.cstart;
       }
-      auto lcol = [&](int ni, int a) { return wn * 64 + ni * 32 + 8 * a + 4 * lh; };
 #pragma unroll
       for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
@@ -512,19 +532,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         }
       };
       if constexpr (MODE == kModeFwd) {
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            const float4 bv = *reinterpret_cast<const float4*>(&bias_s[buf][lcol(ni, a)]);
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi) {
-              acc[mi][ni][4 * a + 0] += bv.x;
-              acc[mi][ni][4 * a + 1] += bv.y;
-              acc[mi][ni][4 * a + 2] += bv.z;
-              acc[mi][ni][4 * a + 3] += bv.w;
-            }
-          }
+        // (the bias is already in: the accumulators started from it)
         if (p.Z) store_tile(p.Z);
         if constexpr (ACT != kActNone) {
 #pragma unroll
@@ -571,12 +579,6 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     }
     ++cseq;
     cs = 0;
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
   }
   // every copy into LDS lands before the workgroup ends
   wait_vm_all();

@@ -108,27 +108,27 @@ __device__ __forceinline__ float tanh_fast(float u) {
 
 // Exact-form GELU, z Phi(z) = z (1 + erf(z / sqrt 2)) / 2, with erf from
 // Abramowitz & Stegun 7.1.28: erf(x) = 1 - (1 + a1 x + ... + a6 x^6)^-16 for
-// x >= 0, |error| <= 3e-7.  The 1 / sqrt 2 is folded into the coefficients
-// (b_k = a_k 2^(-k/2)); with r = p(|z|)^-16, GELU is z - z r / 2 for z >= 0
-// and z r / 2 below.  One reciprocal and no exponential: cheaper than
-// 7.1.26 in the epilogue.  Absolute error at most 1e-6 in fp32 (checked
-// against the exact function on [-12, 12]); p^16 overflows to infinity for
-// large |z| and r becomes 0, the right limit.
+// x >= 0, |error| <= 3e-7.  With r = p(|z| / sqrt 2)^-16 the identity
+// z Phi(z) = max(z, 0) - |z| r / 2 holds for either sign of z; the 1 / sqrt 2
+// goes into the coefficients (a_k 2^(-k/2)) and the 1 / 2 too, by scaling
+// the whole polynomial by 2^(1/16).  So: six FMAs, four squarings, one
+// reciprocal, a max and an FMA, and no exponential.  Absolute error at most
+// 1e-6 in fp32 (checked against the exact function on [-12, 12]); p^16
+// overflows to infinity for large |z|, where r = 0 is the right limit.
 __device__ __forceinline__ float gelu_erf(float z) {
   const float az = fabsf(z);
-  float p = 5.3829750000e-06f;
-  p = p * az + 4.8890635643e-05f;
-  p = p * az + 3.8003575000e-05f;
-  p = p * az + 3.2776263241e-03f;
-  p = p * az + 2.1141006150e-02f;
-  p = p * az + 4.9867346967e-02f;
-  p = p * az + 1.0f;
+  float p = 5.6212996640e-06f;
+  p = p * az + 5.1055209008e-05f;
+  p = p * az + 3.9686137011e-05f;
+  p = p * az + 3.4227392389e-03f;
+  p = p * az + 2.2076998457e-02f;
+  p = p * az + 5.2075163037e-02f;
+  p = p * az + 1.0442737824e+00f;
   p *= p;
   p *= p;
   p *= p;
   p *= p;
-  const float h = 0.5f * z * __builtin_amdgcn_rcpf(p);
-  return z >= 0.0f ? z - h : h;
+  return fmaf(-az, __builtin_amdgcn_rcpf(p), fmaxf(z, 0.0f));
 }
 
 __device__ __forceinline__ float act_apply(int act, float z) {
