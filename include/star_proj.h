@@ -197,9 +197,9 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
                         void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Type plan: the per-type row sets I_i of Alg. 1 (line "I_i <- {b : tau(p_b)
- * = i}") as one stable permutation of the rows grouped by type plus q+1
- * offsets.  Every compute call needs it; the plain entry points build it in
+ * Type plan: the per-type row sets I_i of Algorithm alg:projection (the rows
+ * whose position has type i) as one stable permutation of the rows grouped
+ * by type plus q+1 offsets.  Every compute call needs it; the plain entry points build it in
  * their workspace on each call, the *_planned entry points take one built
  * here, so calls that share row types (the six products of an FFN training
  * step, repeated replays) build it once.

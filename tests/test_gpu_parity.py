@@ -529,3 +529,61 @@ def test_planned_entry_points_match(P):
     a, b = P.star_proj_bwd_weight(ga, t, X, dY)
     c, d = P.star_proj_bwd_weight_planned(ga, plan, X, dY)
     assert torch.equal(a, c) and torch.equal(b, d)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("q,M,bad", [(2, 8192, False), (1, 300, False), (3, 1000, True),
+                                     (64, 5000, True), (7, 70001, True), (16, 64, False)])
+def test_type_plan_is_stable_partition(P, q, M, bad):
+    """The plan is the stable partition of the rows by type (a stable sort of
+    the type keys, out-of-range types as a last key) and the per-type
+    starts; checked element by element against numpy's stable sort."""
+    import torch
+    rng = np.random.default_rng([11, q, M])
+    t = rng.integers(0, q, size=M).astype(np.int32)
+    if bad:
+        idx = rng.choice(M, size=max(1, M // 17), replace=False)
+        t[idx] = rng.choice(np.array([-3, q, q + 5, 1 << 20], dtype=np.int32), size=idx.size)
+    plan = P.star_type_plan(q, types_dev(t)).cpu().numpy()
+    perm = plan[:4 * M].view(np.int32)
+    off0 = (4 * M + 255) // 256 * 256
+    offsets = plan[off0:off0 + 4 * (q + 1)].view(np.int32)
+    key = np.where((t >= 0) & (t < q), t, q)
+    np.testing.assert_array_equal(perm, np.argsort(key, kind="stable"))
+    np.testing.assert_array_equal(offsets, [(key < i).sum() for i in range(q + 1)])
+
+
+@pytest.mark.gpu
+def test_graph_replay_matches_eager(P):
+    """The type plan and the fused forward GEMM captured in one HIP graph give
+    the eager result on every replay, with other eager work and
+    synchronisations between the replays (the plan's scan and the GEMM's
+    tile walk must not keep state across launches)."""
+    import torch
+    q, s, r, M = 2, 384, 1536, 2048
+    ga = P.Algebra.equal(q, 2 * s, 2 * r)
+    X = to_dev(synth.gaussian(9, 0, (M, 2 * s), 1.0, "bf16"))
+    W = to_dev(synth.gaussian(9, 1, (2 * s, 2 * r), 0.02, "bf16"))
+    b = f32_dev(synth.gaussian(9, 2, (2 * r,), 0.02, "f32").raw)
+    t = types_dev(synth.sequence_types(M, q, 512))
+    plan = torch.empty(P.star_plan_bytes(q, M), dtype=torch.uint8, device="cuda")
+    Y = torch.empty((M, 2 * r), dtype=torch.bfloat16, device="cuda")
+    P.star_type_plan(q, t, plan)
+    ref = P.star_proj_fwd_planned(ga, plan, X, W, b, "gelu").clone()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        P.star_type_plan(q, t, plan)
+        P.star_proj_fwd_planned(ga, plan, X, W, b, "gelu", Y=Y)
+    other = P.Algebra.equal(4, 256, 512)
+    for rep in range(4):
+        Y.zero_()
+        plan.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y, ref), f"replay {rep}"
+        # eager work in between, on the same buffers' neighbours
+        Xo = torch.randn(300, 256, device="cuda").to(torch.bfloat16)
+        Wo = torch.randn(256, 512, device="cuda").to(torch.bfloat16)
+        P.star_proj_fwd(other, types_dev(np.arange(300) % 4), Xo, Wo)
+        torch.cuda.synchronize()
