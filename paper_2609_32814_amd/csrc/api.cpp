@@ -127,14 +127,14 @@ int bwd_weight_nsplit_async(const Alg& a, int64_t M) {
 constexpr int kColSumChunks = 64;  // row chunks of the bias-gradient column sums
 
 // Workspace of the weight gradient: the plan, then either the fp32 path's
-// split partials or the bf16 path's type-sorted copies of X and dY, split
-// partials and bias-gradient chunk sums (the two paths share the space).
+// split partials or the bf16 path's split partials and bias-gradient chunk
+// sums (the two paths share the space).
 struct BwdWs {
   PlanWs plan;
   int nsplit = 1;
   size_t partial = 0, dbias_part = 0;
   int nsplit_a = 1;
-  size_t xs = 0, dys = 0, partial_a = 0, colsum = 0;
+  size_t partial_a = 0, colsum = 0;
   size_t end = 0;
 };
 BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
@@ -151,10 +151,6 @@ BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
   const size_t end32 = cur;
   w.nsplit_a = bwd_weight_nsplit_async(a, M);
   cur = w.plan.end;
-  w.xs = cur;
-  cur = align_up(cur + sizeof(uint16_t) * static_cast<size_t>(M) * a.K());
-  w.dys = cur;
-  cur = align_up(cur + sizeof(uint16_t) * static_cast<size_t>(M) * a.N());
   if (w.nsplit_a > 1) {
     w.partial_a = cur;
     cur = align_up(cur + sizeof(float) * static_cast<size_t>(w.nsplit_a) * a.K() * a.N());
@@ -571,20 +567,12 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   fill_common(p, a, M, xt == STAR_BF16 ? 1 : 0, at<int32_t>(pl, pw.perm),
               at<int32_t>(pl, pw.offsets));
   if (pipelined) {
-    // sort X and dY rows by type once; every tile then contracts over a
-    // contiguous row range of the copies
-    uint16_t* xs = at<uint16_t>(ws, bw.xs);
-    uint16_t* dys = at<uint16_t>(ws, bw.dys);
-    st = hip_status(launch_gather_rows(static_cast<const uint16_t*>(X), p.K, p.perm, p.offsets,
-                                       a.q, p.M, xs, stream));
-    if (st == STAR_OK)
-      st = hip_status(launch_gather_rows(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets,
-                                         a.q, p.M, dys, stream));
-    if (st != STAR_OK) return st;
+    // every tile contracts over a range of type-sorted positions; the
+    // kernel reads the rows of X and dY at those positions through perm
     fill_tiles(p.NTp, a.R, a.q, gemm_async_tile_n());
     fill_tiles(p.MTp, a.S, a.q, kTileM);
-    p.A = xs;
-    p.B = dys;
+    p.A = X;
+    p.B = dY;
     p.dW = dW;
     p.nsplit = bw.nsplit_a;
     if (bw.nsplit_a > 1) p.partial = at<float>(ws, bw.partial_a);
@@ -596,7 +584,8 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
     // dbias = column sums of dY over the rows of valid type, in fixed chunks
     const int32_t chunk = static_cast<int32_t>((M + kColSumChunks - 1) / kColSumChunks);
     float* cs = at<float>(ws, bw.colsum);
-    st = hip_status(launch_column_sum(dys, p.N, p.offsets, a.q, chunk, kColSumChunks, cs, stream));
+    st = hip_status(launch_column_sum(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets, a.q, chunk,
+                                      kColSumChunks, cs, stream));
     if (st != STAR_OK) return st;
     return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
   }

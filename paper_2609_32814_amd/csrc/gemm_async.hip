@@ -125,6 +125,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   __shared__ int32_t pfx_s[2][kMaxQGroups + 1];
   __shared__ __attribute__((aligned(16))) int32_t rows_s[kRowBufs][BM];
   __shared__ __attribute__((aligned(16))) float bias_s[kRowBufs][BN];
+  // weight gradient: rows (perm entries) of the positions a stage contracts
+  // over, two stages' worth
+  __shared__ __attribute__((aligned(16))) int32_t prow_s[2][BK];
 
   const uint16_t* __restrict__ Ag = static_cast<const uint16_t*>(p.A);
   const uint16_t* __restrict__ Bg = static_cast<const uint16_t*>(p.B);
@@ -214,6 +217,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   int32_t lseq = 0, ls = 0;
   bool lvalid = true;
   bool rows_from_lds = false;  // rl must be refilled from rows_s
+  // weight gradient: stage counter of the load side, and whether the rows
+  // of each perm slot were copied ahead for the stage that will use it
+  int32_t lstg = 0;
+  uint32_t pok = 0;  // bit i: perm slot i holds the rows of the stage that will read it
   int32_t rl[DMA_A];  // gathered row of A copy j: tile row 8 (wave + 8 j) + lane / 8
 #pragma unroll
   for (int j = 0; j < DMA_A; ++j) {
@@ -264,24 +271,61 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       sk0 = lt.seg1_lo + (ls - lt.n0) * BK;
       skend = lt.seg1_hi;
     }
+    if constexpr (MODE == kModeBwdWeight) {
+      if (!((pok >> (lstg & 1)) & 1u)) {
+        // the rows of this stage were not copied ahead (first stage, or the
+        // tile after an empty one): fetch them now (nothing else is in
+        // flight at a step's start)
+        if (wave == 0) {
+          const int32_t pos = sk0 + lane;
+          dma4(pos < skend ? static_cast<const void*>(p.perm + pos) : zero, lds_addr(&prow_s[lstg & 1][0]));
+        }
+        wait_vm_all();
+        block_barrier();
+      }
+    }
   };
   auto stage_copy = [&](int j) {
     if (!lvalid) return;
     const int ii = wave + kWaves * j;
     if constexpr (MODE == kModeBwdWeight) {
-      // A = X rows (type-sorted copy) over the tile's K columns, B = dY rows
-      // over its N columns; 2 positions of 256 columns per copy, both
-      // N-contiguous like W in the forward product
+      // A = X rows over the tile's K columns, B = dY rows over its N
+      // columns, at the tile's positions in the type-sorted order (rows from
+      // perm, copied ahead into prow_s); 2 positions of 256 columns per
+      // copy, both N-contiguous like W in the forward product
       const int kr = 2 * ii + (lane >> 5);
       const int c = (lane & 31) ^ (4 * (kr & 3));
       const int32_t pos = sk0 + kr;
       const int32_t ka = lt.rstart + 8 * c;
       const int32_t nb = lt.cstart + 8 * c;
       const bool pin = pos < skend;
-      const void* ga = (pin && ka < lt.rend) ? static_cast<const void*>(Ag + static_cast<int64_t>(pos) * p.K + ka) : zero;
-      const void* gb = (pin && nb < lt.cend) ? static_cast<const void*>(Bg + static_cast<int64_t>(pos) * p.N + nb) : zero;
+      const int64_t row = pin ? prow_s[lstg & 1][kr] : 0;
+      const void* ga = (pin && ka < lt.rend) ? static_cast<const void*>(Ag + row * p.K + ka) : zero;
+      const void* gb = (pin && nb < lt.cend) ? static_cast<const void*>(Bg + row * p.N + nb) : zero;
       dma16(ga, lds_addr(sA + ii * 1024));
       dma16(gb, lds_addr(sB + ii * 1024));
+      if (j == 0) {
+        // rows of the next stage, into the other perm slot (free: its last
+        // reader was the previous step's copies)
+        int32_t nlo = 0, nhi = 0;
+        bool next = false;
+        if (ls + 1 < lt.nsteps) {
+          nlo = lt.seg0_lo + (ls + 1) * BK;
+          nhi = lt.seg0_hi;
+          next = true;
+        } else if (has_ln && ln.nsteps > 0) {
+          nlo = ln.seg0_lo;
+          nhi = ln.seg0_hi;
+          next = true;
+        }
+        const uint32_t bit = 1u << ((lstg + 1) & 1);
+        pok = next ? (pok | bit) : (pok & ~bit);
+        if (next && wave == 0) {
+          const int32_t npos = nlo + lane;
+          dma4(npos < nhi ? static_cast<const void*>(p.perm + npos) : zero,
+               lds_addr(&prow_s[(lstg + 1) & 1][0]));
+        }
+      }
       return;
     }
     {
@@ -329,6 +373,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   };
   auto stage_end = [&]() {
     if (!lvalid) return;
+    ++lstg;
     if (++ls == lt.nsteps) {
       if (has_ln) {
         rows_from_lds = true;
@@ -628,31 +673,14 @@ hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles,
 
 namespace {
 
-// dst row r = src row perm[r] for the rows of valid type (r < offsets[q]),
-// 16 bytes per thread
-__global__ void gather_rows_kernel(const uint16_t* __restrict__ src, int32_t width,
-                                   const int32_t* __restrict__ perm,
-                                   const int32_t* __restrict__ offsets, int q, int32_t M,
-                                   uint16_t* __restrict__ dst) {
-  const int32_t rows = offsets[q];
-  const int32_t per_row = width / 8;
-  const int64_t total = static_cast<int64_t>(M) * per_row;
-  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < total;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    const int32_t r = static_cast<int32_t>(i / per_row);
-    if (r >= rows) continue;
-    const int32_t c = static_cast<int32_t>(i - static_cast<int64_t>(r) * per_row) * 8;
-    *reinterpret_cast<uint4*>(dst + static_cast<int64_t>(r) * width + c) =
-        *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(perm[r]) * width + c);
-  }
-}
-
-// part[c][n] = sum of rows [c * chunk, (c + 1) * chunk) of the first
-// offsets[q] rows of the bf16 matrix src [rows][N].  A block covers 256
-// columns: thread (g, r) adds 8 columns (one 16-byte load per row) over rows
+// part[c][n] = sum over the type-sorted positions [c * chunk, (c + 1) *
+// chunk) of the first offsets[q] (the rows of valid type) of the bf16
+// matrix src [M][N], row perm[position].  A block covers 256 columns:
+// thread (g, r) adds 8 columns (one 16-byte load per row) over positions
 // r, r + 8, ... of the chunk in order, then the 8 row lanes are added in
 // order through LDS, so the result does not depend on scheduling.
 __global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
+                                                         const int32_t* __restrict__ perm,
                                                          const int32_t* __restrict__ offsets, int q,
                                                          int32_t chunk, float* __restrict__ part) {
   __shared__ float red[8][256 + 4];
@@ -664,7 +692,7 @@ __global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restr
   float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (n0 < N) {
     for (int32_t r = r0 + rl; r < r1; r += 8) {
-      const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r) * N + n0);
+      const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(perm[r]) * N + n0);
       sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
       sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
       sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
@@ -685,20 +713,10 @@ __global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restr
 
 }  // namespace
 
-hipError_t launch_gather_rows(const uint16_t* src, int32_t width, const int32_t* perm,
-                              const int32_t* offsets, int q, int32_t M, uint16_t* dst,
-                              hipStream_t stream) {
-  const int64_t total = static_cast<int64_t>(M) * (width / 8);
-  const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(4096, (total + 255) / 256)));
-  hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(256), 0, stream, src, width, perm,
-                     offsets, q, M, dst);
-  return hipGetLastError();
-}
-
-hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* offsets, int q,
-                             int32_t chunk, int nchunks, float* part, hipStream_t stream) {
+hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm, const int32_t* offsets,
+                             int q, int32_t chunk, int nchunks, float* part, hipStream_t stream) {
   hipLaunchKernelGGL(column_sum_kernel, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
-                     N, offsets, q, chunk, part);
+                     N, perm, offsets, q, chunk, part);
   return hipGetLastError();
 }
 
