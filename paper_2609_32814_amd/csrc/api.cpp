@@ -584,8 +584,8 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
     // dbias = column sums of dY over the rows of valid type, in fixed chunks
     const int32_t chunk = static_cast<int32_t>((M + kColSumChunks - 1) / kColSumChunks);
     float* cs = at<float>(ws, bw.colsum);
-    st = hip_status(launch_column_sum(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets, a.q, chunk,
-                                      kColSumChunks, cs, stream));
+    st = hip_status(launch_column_sum(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets, a.q, p.M,
+                                      chunk, kColSumChunks, cs, stream));
     if (st != STAR_OK) return st;
     return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
   }

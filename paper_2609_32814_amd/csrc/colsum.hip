@@ -1,0 +1,62 @@
+// Bias gradient of the weight-gradient path: column sums of dY over the
+// rows of valid type, in fixed row chunks (the chunks are then summed in
+// order), so dbias does not depend on timing.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace starq {
+
+namespace {
+
+// part[c][n] = sum over rows [c * chunk, (c + 1) * chunk) of the rows of
+// valid type of the bf16 matrix src [M][N].  When every row has a valid type
+// (offsets[q] == M) the rows are taken in their own order (contiguous
+// reads); otherwise in type-sorted order, row perm[position] for positions
+// below offsets[q].  A block covers 256 columns: thread (g, r) adds 8
+// columns (one 16-byte load per row) over rows r, r + 8, ... of the chunk in
+// order, then the 8 row lanes are added in order through LDS, so the result
+// does not depend on scheduling.
+__global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
+                                                         const int32_t* __restrict__ perm,
+                                                         const int32_t* __restrict__ offsets, int q,
+                                                         int32_t M, int32_t chunk, float* __restrict__ part) {
+  __shared__ float red[8][256 + 4];
+  const int32_t rows = offsets[q];
+  const bool natural = rows == M;
+  const int32_t c = blockIdx.y;
+  const int g = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int32_t n0 = blockIdx.x * 256 + 8 * g;
+  const int32_t r0 = c * chunk, r1 = min(rows, r0 + chunk);
+  float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (n0 < N) {
+    for (int32_t r = r0 + rl; r < r1; r += 8) {
+      const int32_t row = natural ? r : perm[r];
+      const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row) * N + n0);
+      sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
+      sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
+      sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
+      sum[6] += bf16_to_f32(v.w & 0xffffu); sum[7] += bf16_to_f32(v.w >> 16);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rl][8 * g + e] = sum[e];
+  __syncthreads();
+  const int32_t n = blockIdx.x * 256 + threadIdx.x;
+  if (n < N) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += red[k][threadIdx.x];
+    part[static_cast<int64_t>(c) * N + n] = t;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm, const int32_t* offsets,
+                             int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream) {
+  hipLaunchKernelGGL(column_sum_kernel, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
+                     N, perm, offsets, q, M, chunk, part);
+  return hipGetLastError();
+}
+
+}  // namespace starq

@@ -62,11 +62,11 @@ hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStrea
 // tiles of that width); `upper_tiles` bounds the tile count and `cus` is the
 // device's CU count (the kernel picks its persistent grid from both).
 int gemm_async_tile_n();
-// part[c][n] = sum over the type-sorted positions [c chunk, (c + 1) chunk)
-// below offsets[q] of the bf16 matrix src [M][N] (row perm[position]), in
-// position order.
+// part[c][n] = sum over rows [c chunk, (c + 1) chunk) of the rows of valid
+// type of the bf16 matrix src [M][N]: in row order when every row is valid,
+// else in type-sorted order (row perm[position], positions below offsets[q]).
 hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm, const int32_t* offsets,
-                             int q, int32_t chunk, int nchunks, float* part, hipStream_t stream);
+                             int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream);
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream);
 hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
