@@ -42,10 +42,16 @@ GEMM_KERNEL = "star_gemm_async_kernel<fwd, star, gelu>"
 
 
 def gemm_src_hash():
+    """SHA-256 of the GEMM sources with // comments and blank lines removed,
+    so that the stored traffic counters stay valid across comment edits and
+    go stale on any change to the code itself."""
     h = hashlib.sha256()
     for f in GEMM_SRCS:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            for line in fh:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()
 
 

@@ -1,24 +1,30 @@
 // Grouped, row-typed GEMM for bf16 operands with an asynchronous LDS
-// pipeline: the forward projection and its activation gradient.
+// pipeline: the forward projection, its activation gradient and its weight
+// gradient.
 //
 // Tiles of C are 256 rows (of one type class) x 256 columns (of one output
 // group), computed by one workgroup of 8 wavefronts (2 x 4, 128 x 64 each,
 // swapped-operand v_mfma_f32_32x32x16_bf16 so a lane ends with 4 consecutive
 // output columns).  Two passes of tiles (two-segment contractions first),
-// XCD-contiguous chunks and the epilogue follow the register-staged kernel.
+// dealt out per XCD as one list; the epilogue follows the register-staged
+// kernel.  Weight gradient: C = X^T dY over the type-sorted positions of the
+// rows whose support pairs the tile's groups, rows read in place through
+// perm (the rows of each stage's 64 positions are copied into LDS one stage
+// ahead), split along the positions into deterministic partials.
 //
 // Operands go from global memory straight into LDS with
 // global_load_lds_dwordx4 (16 bytes per lane, 1 KB per wavefront
 // instruction): no staging registers.  A K step is 64 wide, so every row of
 // the A tile is one whole 128-byte line per step (measured on gfx950: copies
 // of 64-byte row segments move half the bytes per clock that whole lines do).
-// Two 64 KB stages: the copy of step s + 1 is issued right after the barrier
-// that opens step s and overlaps its 64 MFMAs per wave.  The load side walks
+// Two 64 KB stages: the copy of step s + 1 is issued in four slices
+// interleaved with the MFMAs of step s (after the barrier that opens it).  The load side walks
 // the tile sequence one step ahead of the compute side, across tile
 // boundaries.  Everything else a tile needs from memory arrives by the same
-// kind of copies: the gathered row indices of the next tile and the bias of
-// the current one (a plain load whose value is used would make the compiler
-// wait for every copy in flight, which it does not see).  Lanes whose
+// kind of copies: the gathered row indices of the next tile, the bias of
+// the current one (it seeds the accumulators) and, for the weight gradient,
+// the rows of the next stage (a plain load whose value is used would make
+// the compiler wait for every copy in flight, which it does not see).  Lanes whose
 // element lies outside an operand (rows past a type's count, K or columns
 // past a group's end) copy from a page of zeros.
 //
@@ -28,7 +34,8 @@
 //    c ^ ((r >> 1) & 7).  Eight lanes of a copy fill one row (the global side
 //    reads the row's 128 contiguous bytes, permuted across lanes); a 32-row
 //    MFMA operand read hits 16 distinct bank slots per 16 rows.
-//  * N-contiguous rows (W in the forward product): 64 K rows of 256 columns
+//  * N-contiguous rows (W in the forward product; X and dY rows in the
+//    weight gradient, where K runs over positions): 64 K rows of 256 columns
 //    (512 bytes), chunk c of K row k stored at chunk c ^ 4 (k & 3).  The
 //    operand read uses ds_read_b64_tr_b16: in each 16-lane group, lanes
 //    4r + q point at columns 4q..4q+3 of K row r and lane i receives column i
