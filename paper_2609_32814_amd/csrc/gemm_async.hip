@@ -290,6 +290,13 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         wait_vm_all();
         block_barrier();
       }
+      // this wave's rows for the stage's copies, read once (rl[j]: the row at
+      // position sk0 + 2 (wave + 8 j) + lane / 32, or -1 past the range)
+#pragma unroll
+      for (int j = 0; j < DMA_A; ++j) {
+        const int kr = 2 * (wave + kWaves * j) + (lane >> 5);
+        rl[j] = sk0 + kr < skend ? prow_s[lstg & 1][kr] : -1;
+      }
     }
   };
   auto stage_copy = [&](int j) {
@@ -302,11 +309,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       // copy, both N-contiguous like W in the forward product
       const int kr = 2 * ii + (lane >> 5);
       const int c = (lane & 31) ^ (4 * (kr & 3));
-      const int32_t pos = sk0 + kr;
       const int32_t ka = lt.rstart + 8 * c;
       const int32_t nb = lt.cstart + 8 * c;
-      const bool pin = pos < skend;
-      const int64_t row = pin ? prow_s[lstg & 1][kr] : 0;
+      const bool pin = rl[j] >= 0;
+      const int64_t row = rl[j];
       const void* ga = (pin && ka < lt.rend) ? static_cast<const void*>(Ag + row * p.K + ka) : zero;
       const void* gb = (pin && nb < lt.cend) ? static_cast<const void*>(Bg + row * p.N + nb) : zero;
       dma16(ga, lds_addr(sA + ii * 1024));
