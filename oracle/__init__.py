@@ -13,7 +13,11 @@ between two products (rounding to nearest even).
 Conventions (Sec. 4 of the paper): X is M x K, W is K x N (input groups are
 row blocks of W, output groups column blocks), groups are contiguous in index
 order, row types are 0-based.  Law ``"star"`` is the complete-graph algebra
-Q_q with B(i,j) = {i,j}; law ``"dense"`` is the ordinary product.
+Q_q with B(i,j) = {i,j}; law ``"dense"`` is the ordinary product; law
+``"tensor2"`` is the tensor power Q_2^{(x)L} (q = 2^L, appendix "The
+Tensor-Square Candidate"): a type-a row reaches input group b for output group
+d when every bit of b equals that bit of a or of d (L = 2: the pilot's
+36-product law).
 """
 
 from __future__ import annotations
@@ -29,7 +33,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "star_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-LAWS = {"star": 0, "dense": 1}
+LAWS = {"star": 0, "dense": 1, "tensor2": 2}
 ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2}
 
 
@@ -82,6 +86,8 @@ def _load():
         lib.oracle_row_macs.argtypes = [i32, i32, i64p, i64p, i32]
         lib.oracle_square_star.restype = None
         lib.oracle_square_star.argtypes = [i32, i64, f64p, f64p, f64p]
+        lib.oracle_square_law.restype = None
+        lib.oracle_square_law.argtypes = [i32, i32, i64, f64p, f64p, f64p]
         lib.oracle_num_threads.restype = i32
         lib.oracle_num_threads.argtypes = []
         lib.oracle_in_support.restype = i32
@@ -261,6 +267,18 @@ def square_star(q: int, bs: int, A, B) -> np.ndarray:
     C = np.empty((n, n), dtype=np.float64)
     _load().oracle_square_star(q, bs, _p(A, ctypes.c_double), _p(B, ctypes.c_double),
                                _p(C, ctypes.c_double))
+    return C
+
+
+def square_law(law: str, q: int, bs: int, A, B) -> np.ndarray:
+    """Row-column rule with the law's support: (A*B)_ij = sum over k in
+    B(i,j) of A_ik B_kj, for q x q block arrays of b x b blocks."""
+    A, B = _f64(A), _f64(B)
+    n = q * bs
+    assert A.shape == (n, n) and B.shape == (n, n)
+    C = np.empty((n, n), dtype=np.float64)
+    _load().oracle_square_law(LAWS[law], q, bs, _p(A, ctypes.c_double), _p(B, ctypes.c_double),
+                              _p(C, ctypes.c_double))
     return C
 
 

@@ -29,6 +29,12 @@
  *          typed-off).
  *   law 1 (ordinary product, the dense control): B(i,j) = {0..q-1}
  *          (eq. dense-two for q = 2).
+ *   law 2 (tensor power Q_2^{(x)L} of the two-group law, q = 2^L; appendix
+ *          "The Tensor-Square Candidate", eq. recursive-unequal-cost): types
+ *          and group indices are bit strings of length L (index
+ *          g = sum_k g_k 2^k), and a type-a row reaches input group b for
+ *          output group d when every bit of b equals the same bit of a or of
+ *          d.  L = 1 is Q_2; L = 2 is the pilot's 36-product law.
  *
  * Activations: 0 none, 1 GELU with the exact erf form
  * 0.5 z (1 + erf(z / sqrt 2)), 2 GELU with the tanh form.  The paper keeps
@@ -42,6 +48,7 @@
 
 #define ORACLE_LAW_STAR 0
 #define ORACLE_LAW_DENSE 1
+#define ORACLE_LAW_TENSOR2 2
 
 #define ORACLE_ACT_NONE 0
 #define ORACLE_ACT_GELU 1
@@ -52,6 +59,14 @@
 int oracle_in_support(int law, int i, int j, int k)
 {
     if (law == ORACLE_LAW_DENSE) return 1;
+    if (law == ORACLE_LAW_TENSOR2) {
+        /* beta_k in {alpha_k, delta_k} for every bit k */
+        for (int bit = 0; bit < 30; ++bit) {
+            const int b = (k >> bit) & 1, a = (i >> bit) & 1, d = (j >> bit) & 1;
+            if (b != a && b != d) return 0;
+        }
+        return 1;
+    }
     return k == i || k == j;
 }
 
@@ -325,6 +340,8 @@ int oracle_proj_bwd_weight(int q, const int64_t *s, const int64_t *r, int law,
  * Written directly from the square rule, independently of the typed
  * projection above.
  */
+void oracle_square_law(int law, int q, int64_t bs, const double *A, const double *B, double *C);
+
 void oracle_square_star(int q, int64_t bs, const double *A, const double *B, double *C)
 {
     const int64_t n = q * bs;
@@ -388,4 +405,29 @@ int oracle_num_threads(void)
 #else
     return 1;
 #endif
+}
+
+/*
+ * C = A * B for square block arrays under any law: (A*B)_ij is the sum over
+ * k in B(i,j) of A_ik B_kj (the row-column rule with the law's support).
+ * For law 0 this is oracle_square_star; the tests check law 2 against the
+ * tensor product of two copies of the q = 2 rule.
+ */
+void oracle_square_law(int law, int q, int64_t bs, const double *A, const double *B, double *C)
+{
+    const int64_t n = q * bs;
+    memset(C, 0, sizeof(double) * (size_t)(n * n));
+    #define BLK(P, i, j, u, v) (P)[((i) * bs + (u)) * n + (j) * bs + (v)]
+    for (int i = 0; i < q; ++i)
+        for (int j = 0; j < q; ++j)
+            for (int k = 0; k < q; ++k) {
+                if (!oracle_in_support(law, i, j, k)) continue;
+                for (int64_t u = 0; u < bs; ++u)
+                    for (int64_t v = 0; v < bs; ++v) {
+                        double acc = 0.0;
+                        for (int64_t w = 0; w < bs; ++w) acc += BLK(A, i, k, u, w) * BLK(B, k, j, w, v);
+                        BLK(C, i, j, u, v) += acc;
+                    }
+            }
+    #undef BLK
 }

@@ -259,8 +259,8 @@ def test_semidirect_form(q):
 
 # ---- P7: composition of typed projections ------------------------------------
 
-@pytest.mark.parametrize("q", [2, 3, 4])
-def test_composition(q):
+@pytest.mark.parametrize("q,law", [(2, "star"), (3, "star"), (4, "star"), (4, "tensor2")])
+def test_composition(q, law):
     """eq. association-intro / general-associativity, rectangular groups:
     Phi_{W2}(Phi_{W1}(X)) = Phi_{W1 * W2}(X), where W1 * W2 is the algebra
     product of the two banks (row group i of W1 is a type-i row)."""
@@ -268,7 +268,7 @@ def test_composition(q):
     s = tuple(int(v) for v in g.integers(1, 4, q))
     r1 = tuple(int(v) for v in g.integers(1, 4, q))
     r2 = tuple(int(v) for v in g.integers(1, 4, q))
-    a1, a2, a12 = Alg(q, s, r1), Alg(q, r1, r2), Alg(q, s, r2)
+    a1, a2, a12 = Alg(q, s, r1, law), Alg(q, r1, r2, law), Alg(q, s, r2, law)
     M = 13
     X = g.standard_normal((M, a1.K))
     W1, W2 = g.standard_normal((a1.K, a1.N)), g.standard_normal((a2.K, a2.N))
@@ -316,7 +316,7 @@ def test_row_locality():
 
 # ---- P11: backward -------------------------------------------------------------
 
-@pytest.mark.parametrize("law", ["star", "dense"])
+@pytest.mark.parametrize("law", ["star", "dense", "tensor2"])
 def test_adjoint_identity(law):
     """<Phi(X,W), G> = <X, dX> = <W, dW>, exact by bilinearity (App. VJPs)."""
     alg = Alg(4, (2, 3, 1, 2), (3, 1, 2, 2), law)
@@ -490,3 +490,79 @@ def test_out_of_range_type_rejected():
     alg = Alg(2, (2, 2), (2, 2))
     with pytest.raises(ValueError):
         oracle.proj_fwd(alg, np.array([0, 2], np.int32), np.zeros((2, 4)), np.zeros((4, 4)))
+
+
+# ---- the tensor-power law Q_2^(x)L (appendix "The Tensor-Square Candidate") ------
+
+def _tensor_square_table():
+    """Nonzero basis products of Q_2 (x) Q_2 built from two copies of the Q_2
+    table: (x1 (x) x2)(w1 (x) w2) = (x1 w1) (x) (x2 w2).  A slot of the tensor
+    square is a pair of group indices made of one bit per factor
+    (g = g1 + 2 g2)."""
+    t2 = _basis_product_table(2)
+    comb = lambda a, b: (a[0] + 2 * b[0], a[1] + 2 * b[1])
+    table = {}
+    for (x1, w1), c1 in t2.items():
+        for (x2, w2), c2 in t2.items():
+            table[(comb(x1, x2), comb(w1, w2))] = comb(c1, c2)
+    return table
+
+
+@pytest.mark.parametrize("bs", [1, 2, 3])
+def test_tensor_square_structure_constants(bs):
+    """The tensor square of the two-group law, multiplied out from its Kronecker
+    structure constants, is the oracle's law "tensor2" at q = 4, both as a
+    square-rule product and through the typed projection; it has the 36
+    block products the paper counts (4 x 1 + 8 x 2 + 4 x 4)."""
+    table = _tensor_square_table()
+    assert len(table) == 36
+    q = 4
+    g = rng(31, bs)
+    n = q * bs
+    A, B = g.standard_normal((n, n)), g.standard_normal((n, n))
+    C = np.zeros((n, n))
+    for (sx, sw), sc in table.items():
+        for u in range(bs):
+            for v in range(bs):
+                a = A[sx[0] * bs + u, sx[1] * bs + v]
+                for z in range(bs):
+                    C[sc[0] * bs + u, sc[1] * bs + z] += a * B[sw[0] * bs + v, sw[1] * bs + z]
+    np.testing.assert_allclose(oracle.square_law("tensor2", q, bs, A, B), C, atol=1e-12)
+    np.testing.assert_allclose(square_typed(q, bs, A, B, law="tensor2"), C, atol=1e-12)
+    assert sum(oracle.products_per_type("tensor2", q, i) for i in range(q)) == 36
+    # a different law from the direct four-group one (28 products)
+    assert sum(oracle.products_per_type("star", q, i) for i in range(q)) == 28
+    assert not np.allclose(square_typed(q, bs, A, B, law="star"), C)
+
+
+def test_tensor_power_one_is_the_two_group_law():
+    g = rng(32)
+    A, B = g.standard_normal((6, 6)), g.standard_normal((6, 6))
+    np.testing.assert_allclose(square_typed(2, 3, A, B, law="tensor2"), square_typed(2, 3, A, B), atol=0)
+
+
+@pytest.mark.parametrize("q", [4, 8])
+def test_tensor_power_associativity_and_unit(q):
+    """The tensor product of associative unital algebras is associative with
+    the product of the units."""
+    bs = 2
+    g = rng(33, q)
+    n = q * bs
+    A, B, C = (g.standard_normal((n, n)) for _ in range(3))
+    sq = lambda X, Y: square_typed(q, bs, X, Y, law="tensor2")
+    np.testing.assert_allclose(sq(sq(A, B), C), sq(A, sq(B, C)), atol=1e-11)
+    E = np.eye(n)
+    np.testing.assert_allclose(sq(E, B), B, atol=0)
+    np.testing.assert_allclose(sq(A, E), A, atol=0)
+
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+def test_tensor_power_counts(L):
+    """6^L block products in all (the recursive algorithm's count), and for
+    equal widths with every type present the MACs of a type average (3/4)^L of
+    the dense projection (eq. recursive-uniform-cost)."""
+    q = 2 ** L
+    assert sum(oracle.products_per_type("tensor2", q, i) for i in range(q)) == 6 ** L
+    alg = Alg.equal(q, 4 * q, 8 * q, "tensor2")
+    total = sum(oracle.row_macs(alg, i) for i in range(q))
+    assert total * 4 ** L == 3 ** L * q * alg.K * alg.N
