@@ -77,8 +77,14 @@ typedef enum { STAR_ACT_NONE = 0, STAR_ACT_GELU = 1, STAR_ACT_GELU_TANH = 2 } st
 
 /* STAR_LAW_STAR: B(i,j) = {i,j} (Sec. 5.1).  STAR_LAW_DENSE: all q^2 block
  * products, i.e. the ordinary product XW (eq. dense-two), run through the
- * same kernels as the control. */
-typedef enum { STAR_LAW_STAR = 0, STAR_LAW_DENSE = 1 } star_law;
+ * same kernels as the control.  STAR_LAW_TENSOR2: the tensor power
+ * Q_2^{(x)L} of the two-group law (appendix "The Tensor-Square Candidate",
+ * eq. recursive-unequal-cost) with q = 2^L groups: a type-i row reaches input
+ * group k for output group j when every bit of k equals that bit of i or of
+ * j (2^h(i,j) products per output group, 6^L in all).  q must be 1, 2 or 4
+ * (STAR_ERR_UNSUPPORTED otherwise); q = 2 is STAR_LAW_STAR, q = 4 the
+ * 36-product law of the paper's pretraining pilot. */
+typedef enum { STAR_LAW_STAR = 0, STAR_LAW_DENSE = 1, STAR_LAW_TENSOR2 = 2 } star_law;
 
 /* An algebra layout.  s and r are host arrays of q widths (input groups,
  * output groups). */

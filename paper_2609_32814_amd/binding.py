@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "STAR_OK", 1: "STAR_ERR_ARG", 2: "STAR_ERR_SHAPE", 3: "STAR_E
                 7: "STAR_ERR_HIP"}
 DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2}
-LAWS = {"star": 0, "dense": 1}
+LAWS = {"star": 0, "dense": 1, "tensor2": 2}
 OPS = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2, "ffn_fwd": 3, "decode": 4}
 MAX_Q = 64
 

@@ -38,10 +38,19 @@ struct Alg {
   int64_t r(int g) const { return R[g + 1] - R[g]; }
 };
 
+// k in B(i, j) for the law (host side of the kernels' rule)
+bool host_in_support(int law, int i, int j, int k) {
+  if (law == STAR_LAW_TENSOR2) return ((k ^ i) & (k ^ j)) == 0;
+  return law == STAR_LAW_DENSE || k == i || k == j;
+}
+
 star_status parse_alg(const star_algebra* a, Alg& out) {
   if (!a || !a->s || !a->r) return STAR_ERR_ARG;
   if (a->q < 1 || a->q > kMaxQGroups) return STAR_ERR_ARG;
-  if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE) return STAR_ERR_ARG;
+  if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE && a->law != STAR_LAW_TENSOR2) return STAR_ERR_ARG;
+  // the tensor power needs q = 2^L; the kernels take every contraction as
+  // at most two contiguous group ranges, which holds for L <= 2
+  if (a->law == STAR_LAW_TENSOR2 && a->q != 1 && a->q != 2 && a->q != 4) return STAR_ERR_UNSUPPORTED;
   out.q = a->q;
   out.law = a->law;
   out.S[0] = out.R[0] = 0;
@@ -394,7 +403,7 @@ star_status star_count_products(const star_algebra* alg, int64_t* per_type) {
   for (int i = 0; i < a.q; ++i) {
     int64_t n = 0;
     for (int j = 0; j < a.q; ++j)
-      for (int k = 0; k < a.q; ++k) n += (a.law == STAR_LAW_DENSE || k == i || k == j) ? 1 : 0;
+      for (int k = 0; k < a.q; ++k) n += host_in_support(a.law, i, j, k) ? 1 : 0;
     per_type[i] = n;
   }
   return STAR_OK;
@@ -410,7 +419,7 @@ star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_typ
     int64_t row = 0;
     for (int j = 0; j < a.q; ++j)
       for (int k = 0; k < a.q; ++k)
-        if (a.law == STAR_LAW_DENSE || k == i || k == j) row += a.s(k) * a.r(j);
+        if (host_in_support(a.law, i, j, k)) row += a.s(k) * a.r(j);
     total += rows_per_type[i] * row;
   }
   *macs = total;

@@ -41,7 +41,10 @@ constexpr int kRedBytes = 4 * 4 * 64 * 16;  // 4 waves x 4 row blocks x 64 lanes
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define STARQ_LDS __attribute__((address_space(3)))
 
+// k in B(i, j): law 0 {i, j}; law 1 every group; law 2 (tensor power of
+// the two-group law) every bit of k equal to that bit of i or of j
 __device__ __forceinline__ bool in_support(int law, int i, int j, int k) {
+  if (law == 2) return ((k ^ i) & (k ^ j)) == 0;
   return law == 1 || k == i || k == j;
 }
 

@@ -87,7 +87,10 @@ __device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// k in B(i, j): law 0 {i, j}; law 1 every group; law 2 (tensor power of
+// the two-group law) every bit of k equal to that bit of i or of j
 __device__ __forceinline__ bool in_support(int law, int i, int j, int k) {
+  if (law == 2) return ((k ^ i) & (k ^ j)) == 0;
   return law == 1 || k == i || k == j;
 }
 __device__ __forceinline__ int group_of(const int32_t* starts, int q, int32_t x) {

@@ -551,13 +551,17 @@ __global__ void fill_zero_kernel(float* __restrict__ dst, int64_t n) {
 template <typename T, int MODE, int WN>
 hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
   using G = Geo<WN>;
-  auto kern = (p.law == 1) ? star_gemm_kernel<T, MODE, 1, WN> : star_gemm_kernel<T, MODE, 0, WN>;
+  auto kern = p.law == 1 ? star_gemm_kernel<T, MODE, 1, WN>
+                         : (p.law == 2 ? star_gemm_kernel<T, MODE, 2, WN> : star_gemm_kernel<T, MODE, 0, WN>);
   // allow more than the default dynamic LDS once per kernel (idempotent)
   static const hipError_t attr = [] {
     hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 0, WN>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
+    if (a == hipSuccess)
+      a = hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
     if (a != hipSuccess) return a;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>),
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 2, WN>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
   }();
   if (attr != hipSuccess) return attr;

@@ -322,13 +322,21 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         // reader was the previous step's copies)
         int32_t nlo = 0, nhi = 0;
         bool next = false;
+        // positions of step st of tile t (segment 0, then segment 1)
+        auto stage_range = [](const Tile& t, int32_t st, int32_t& lo, int32_t& hi) {
+          if (st < t.n0) {
+            lo = t.seg0_lo + st * BK;
+            hi = t.seg0_hi;
+          } else {
+            lo = t.seg1_lo + (st - t.n0) * BK;
+            hi = t.seg1_hi;
+          }
+        };
         if (ls + 1 < lt.nsteps) {
-          nlo = lt.seg0_lo + (ls + 1) * BK;
-          nhi = lt.seg0_hi;
+          stage_range(lt, ls + 1, nlo, nhi);
           next = true;
         } else if (has_ln && ln.nsteps > 0) {
-          nlo = ln.seg0_lo;
-          nhi = ln.seg0_hi;
+          stage_range(ln, 0, nlo, nhi);
           next = true;
         }
         const uint32_t bit = 1u << ((lstg + 1) & 1);
@@ -667,6 +675,7 @@ hipError_t launch_act(const GemmParams& p, int64_t upper, int cus, hipStream_t s
 
 template <int MODE>
 hipError_t launch_async(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
+  if (p.law == 2) return launch_act<MODE, 2>(p, upper, cus, stream);
   return p.law == 1 ? launch_act<MODE, 1>(p, upper, cus, stream)
                     : launch_act<MODE, 0>(p, upper, cus, stream);
 }
@@ -680,7 +689,8 @@ hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles,
   if (mode == kModeFwd) return launch_async<kModeFwd>(p, upper_tiles, cus, stream);
   if (mode == kModeBwdWeight)
     return p.law == 1 ? launch_one<kModeBwdWeight, 1, kActNone>(p, upper_tiles, cus, stream)
-                      : launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream);
+                      : (p.law == 2 ? launch_one<kModeBwdWeight, 2, kActNone>(p, upper_tiles, cus, stream)
+                                    : launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream));
   return launch_async<kModeBwdData>(p, upper_tiles, cus, stream);
 }
 

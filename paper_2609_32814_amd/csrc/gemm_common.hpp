@@ -40,17 +40,68 @@ __device__ __forceinline__ uint32_t word_of(const uint4& r, int w) {
   return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
 }
 
-enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3 };
+enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3, kSelTensor = 4 };
 
+// Law 2, the tensor power of the two-group law (q = 2^L): input group k is
+// in B(i, j) when every bit of k equals that bit of i or of j.
+__device__ __forceinline__ bool tensor_in_support(int i, int j, int k) { return ((k ^ i) & (k ^ j)) == 0; }
+
+// Law 2: bit x set when x is in the contraction of a tile of class i (a row
+// type; for the weight gradient an input group) and C-column group j:
+//  forward: input groups x in B(i, j);
+//  activation gradient (C columns are input group j): output groups x with
+//  j in B(i, x);
+//  weight gradient (C rows input group i, columns output group j): row
+//  types x with i in B(x, j).
+__device__ __forceinline__ uint32_t tensor_mask(int mode, int q, int i, int j) {
+  uint32_t m = 0;
+  for (int x = 0; x < q; ++x) {
+    const bool in = mode == kModeFwd ? tensor_in_support(i, j, x)
+                                     : (mode == kModeBwdData ? tensor_in_support(i, x, j) : tensor_in_support(x, j, i));
+    if (in) m |= 1u << x;
+  }
+  return m;
+}
+// maximal runs of consecutive set bits (each run is one contiguous range)
+__device__ __forceinline__ int mask_runs(uint32_t m) { return __popc(m & ~(m << 1)); }
+// the first two runs: [lo0, hi0) and [lo1, hi1) (empty when absent)
+__device__ __forceinline__ void mask_ranges(uint32_t m, int& lo0, int& hi0, int& lo1, int& hi1) {
+  lo0 = hi0 = lo1 = hi1 = 0;
+  if (!m) return;
+  lo0 = __builtin_ctz(m);
+  hi0 = lo0 + __builtin_ctz(~(m >> lo0));
+  const uint32_t rest = hi0 >= 32 ? 0u : (m & ~((1u << hi0) - 1u));
+  if (!rest) return;
+  lo1 = __builtin_ctz(rest);
+  hi1 = lo1 + __builtin_ctz(~(rest >> lo1));
+}
+
+// A pass selects, per class, the C-column groups of its tiles: the star
+// law puts the tiles with two K segments first, the dense law has one pass;
+// law 2 sorts by the number of runs of the contraction mask (two, then
+// one), with the mode folded into the selector.
 __device__ __forceinline__ int sel_for(int mode, int law, int pass) {
   if (law == 1) return pass == 0 ? kSelAll : kSelNone;
+  if (law == 2) return kSelTensor + 2 * mode + pass;
   if (mode == kModeFwd) return pass == 0 ? kSelExcept : kSelOnly;
   return pass == 0 ? kSelOnly : kSelExcept;  // BWD_DATA and BWD_WEIGHT
+}
+// law 2: is column group j of class i in the selector's pass?
+__device__ __forceinline__ bool tensor_in_pass(const GemmParams& p, int sel, int i, int j) {
+  const int mode = (sel - kSelTensor) >> 1, pass = (sel - kSelTensor) & 1;
+  const int runs = mask_runs(tensor_mask(mode, p.q, i, j));
+  return runs == (pass == 0 ? 2 : 1);
 }
 
 __device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
   const int nti = p.NTp[i + 1] - p.NTp[i];
   const int nt = p.NTp[p.q];
+  if (sel >= kSelTensor) {
+    int n = 0;
+    for (int j = 0; j < p.q; ++j)
+      if (tensor_in_pass(p, sel, i, j)) n += p.NTp[j + 1] - p.NTp[j];
+    return n;
+  }
   switch (sel) {
     case kSelOnly: return nti;
     case kSelExcept: return nt - nti;
@@ -62,6 +113,16 @@ __device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
 __device__ __forceinline__ int col_tile_global(const GemmParams& p, int sel, int i, int c) {
   if (sel == kSelOnly) return p.NTp[i] + c;
   if (sel == kSelExcept) return c < p.NTp[i] ? c : c + (p.NTp[i + 1] - p.NTp[i]);
+  if (sel >= kSelTensor) {
+    // the c-th column tile over the pass's groups, in group order
+    for (int j = 0; j < p.q; ++j) {
+      if (!tensor_in_pass(p, sel, i, j)) continue;
+      const int ntj = p.NTp[j + 1] - p.NTp[j];
+      if (c < ntj) return p.NTp[j] + c;
+      c -= ntj;
+    }
+    return p.NTp[p.q];  // not reached: c < ncols_sel
+  }
   return c;
 }
 
@@ -217,7 +278,7 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
   }
   const int ct = col_tile_global(p, sel, cls, cidx);
   int cg = 0;
-  while (ct >= p.NTp[cg + 1]) ++cg;
+  while (cg + 1 < p.q && ct >= p.NTp[cg + 1]) ++cg;
   const int nt = ct - p.NTp[cg];
   t.cls = cls;
   t.cg = cg;
@@ -232,6 +293,11 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.cend = p.R[cg + 1];
     if (LAW == 1) {
       t.seg0_lo = 0; t.seg0_hi = p.K;
+    } else if (LAW == 2) {
+      int a0, a1, b0, b1;
+      mask_ranges(tensor_mask(kModeFwd, p.q, cls, cg), a0, a1, b0, b1);
+      t.seg0_lo = p.S[a0]; t.seg0_hi = p.S[a1];
+      t.seg1_lo = p.S[b0]; t.seg1_hi = p.S[b1];
     } else {
       t.seg0_lo = p.S[cg]; t.seg0_hi = p.S[cg + 1];
       if (cg != cls) { t.seg1_lo = p.S[cls]; t.seg1_hi = p.S[cls + 1]; }
@@ -240,7 +306,12 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.mt = ru;
     t.cstart = p.S[cg] + nt * BN;
     t.cend = p.S[cg + 1];
-    if (LAW == 1 || cg == cls) {
+    if (LAW == 2) {
+      int a0, a1, b0, b1;
+      mask_ranges(tensor_mask(kModeBwdData, p.q, cls, cg), a0, a1, b0, b1);
+      t.seg0_lo = p.R[a0]; t.seg0_hi = p.R[a1];
+      t.seg1_lo = p.R[b0]; t.seg1_hi = p.R[b1];
+    } else if (LAW == 1 || cg == cls) {
       t.seg0_lo = 0; t.seg0_hi = p.N;
     } else {
       t.seg0_lo = p.R[cg]; t.seg0_hi = p.R[cg + 1];
@@ -252,15 +323,26 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.cend = p.R[cg + 1];
     t.rstart = p.S[cls] + t.mt * BM;
     t.rend = p.S[cls + 1];
-    int32_t lo, hi;
-    if (LAW == 0 && cg != cls) {
-      lo = offs[cls]; hi = offs[cls + 1];
+    // the type-sorted positions this tile contracts over: one or two
+    // ranges, cut into nsplit chunks of their concatenation
+    int32_t a0, a1, b0 = 0, b1 = 0;
+    if (LAW == 2) {
+      int ta0, ta1, tb0, tb1;
+      mask_ranges(tensor_mask(kModeBwdWeight, p.q, cls, cg), ta0, ta1, tb0, tb1);
+      a0 = offs[ta0]; a1 = offs[ta1];
+      b0 = offs[tb0]; b1 = offs[tb1];
+    } else if (LAW == 0 && cg != cls) {
+      a0 = offs[cls]; a1 = offs[cls + 1];
     } else {
-      lo = 0; hi = offs[p.q];
+      a0 = 0; a1 = offs[p.q];
     }
-    const int32_t cs = (hi - lo + p.nsplit - 1) / p.nsplit;
-    t.seg0_lo = min(hi, lo + t.split * cs);
-    t.seg0_hi = min(hi, t.seg0_lo + cs);
+    const int32_t len0 = a1 - a0, len = len0 + (b1 - b0);
+    const int32_t cs = (len + p.nsplit - 1) / p.nsplit;
+    const int32_t c0 = min(len, t.split * cs), c1 = min(len, c0 + cs);
+    t.seg0_lo = a0 + min(c0, len0);
+    t.seg0_hi = a0 + min(c1, len0);
+    t.seg1_lo = b0 + max(c0 - len0, 0);
+    t.seg1_hi = b0 + max(c1 - len0, 0);
     t.do_dbias = (p.dbias != nullptr) && (cg == cls) && (t.mt == 0);
   }
   if constexpr (MODE != kModeBwdWeight) {

@@ -116,3 +116,18 @@ def test_ffn_rejects_mismatched_widths(P):
     st = P.binding.LIB.star_ffn_fwd(up.ref, dn.ref, 4, V(16), V(16), V(16), None, V(16), None, 1,
                                     None, V(16), V(16), 1, 1, V(16), 1 << 20, None)
     assert st == 2
+
+
+def test_tensor_power_law_counts_and_limits(P):
+    """Law TENSOR2: 9 block products per type at q = 4 (36 in all, the
+    paper's count), the two-group law at q = 2, MACs against the oracle's
+    support, and q outside {1, 2, 4} refused before any launch."""
+    import oracle
+    a = P.Algebra.equal(4, 768, 3072, "tensor2")
+    assert P.star_count_products(a) == [9] * 4
+    assert P.star_count_products(P.Algebra.equal(2, 64, 64, "tensor2")) == [3, 3]
+    rows = [5, 0, 7, 3]
+    oa = oracle.Alg.equal(4, 768, 3072, "tensor2")
+    assert P.star_count_macs(a, rows) == sum(n * oracle.row_macs(oa, i) for i, n in enumerate(rows))
+    with pytest.raises(RuntimeError):
+        P.star_count_products(P.Algebra.equal(8, 64, 64, "tensor2"))

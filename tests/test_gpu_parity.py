@@ -587,3 +587,131 @@ def test_graph_replay_matches_eager(P):
         Wo = torch.randn(256, 512, device="cuda").to(torch.bfloat16)
         P.star_proj_fwd(other, types_dev(np.arange(300) % 4), Xo, Wo)
         torch.cuda.synchronize()
+
+
+# ---- the tensor-power law Q_2^(x)2 (q = 4; the paper's pilot law) ------------------
+
+def _interval_types(M, q=4, period=768):
+    """The pilot's interval schedule: type = floor((p mod period) / (period / q))."""
+    return ((np.arange(M) % period) // (period // q)).astype(np.int32)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype,out", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
+@pytest.mark.parametrize("q,s,r,M,types", [
+    (4, [192] * 4, [768] * 4, 2048, "interval"),       # the FFN up shape, pipelined kernel
+    (4, [768] * 4, [192] * 4, 1100, "random"),         # the FFN down shape
+    (4, [72, 40, 96, 64], [136, 200, 56, 96], 777, "random"),
+    (4, [32] * 4, [48] * 4, 300, "missing"),           # one type class empty
+    (2, [136, 120], [200, 56], 333, "cyclic"),          # L = 1: the two-group law
+])
+def test_tensor2_fwd_parity(P, dtype, out, q, s, r, M, types):
+    import torch
+    ga, oa = algs(P, q, s, r, "tensor2")
+    seed = 600 + q + M
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, dtype)
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, dtype)
+    bias = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
+    if types == "interval":
+        t = _interval_types(M, q)
+    elif types == "cyclic":
+        t = synth.cyclic_types(M, q)
+    else:
+        t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+        if types == "missing":
+            t[t == 1] = 2
+    odt = torch.float32 if out == "f32" else torch.bfloat16
+    Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
+                           Z_out=True, out_dtype=odt)
+    refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, bias.exact, "gelu", want_z=True)
+    tol = TOL_F32 if (dtype == "f32" and out == "f32") else TOL_BF16
+    assert rel_fro(to_host(Z), refZ) <= tol
+    assert rel_fro(to_host(Y), refY) <= tol
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("q,s,r,M", [(4, [192] * 4, [768] * 4, 1500), (4, [40, 96, 64, 72], [56, 128, 80, 200], 611)])
+def test_tensor2_bwd_data_parity(P, dtype, fused, q, s, r, M):
+    import torch
+    ga, oa = algs(P, q, s, r, "tensor2")
+    seed = 700 + M
+    dY = synth.gaussian(seed, 0, (M, oa.N), 1.0, dtype)
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, dtype)
+    Zp = synth.gaussian(seed, 2, (M, oa.K), 1.0, dtype) if fused else None
+    t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+    dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W),
+                              Z_prev=to_dev(Zp) if fused else None,
+                              act_prev="gelu" if fused else "none", out_dtype=torch.float32)
+    ref = oracle.proj_bwd_data(oa, t, dY.exact, W.exact, Zprev=Zp.exact if fused else None,
+                               act_prev="gelu" if fused else "none")
+    assert rel_fro(to_host(dX), ref) <= bar(dtype)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("q,s,r,M", [(4, [192] * 4, [768] * 4, 4100), (4, [40, 64, 24, 72], [48, 16, 136, 64], 2049)])
+def test_tensor2_bwd_weight_parity(P, dtype, q, s, r, M):
+    """Off-diagonal blocks contract over two or four type classes (two ranges
+    of type-sorted positions for some blocks), cut into deterministic splits."""
+    ga, oa = algs(P, q, s, r, "tensor2")
+    seed = 800 + M
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, dtype)
+    dY = synth.gaussian(seed, 1, (M, oa.N), 1.0, dtype)
+    t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+    dW, db = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    rW, rb = oracle.proj_bwd_weight(oa, t, X.exact, dY.exact)
+    assert rel_fro(to_host(dW), rW) <= bar(dtype)
+    assert rel_fro(to_host(db), rb) <= bar(dtype)
+    dW2, db2 = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    assert np.array_equal(to_host(dW2), to_host(dW)) and np.array_equal(to_host(db2), to_host(db))
+
+
+@pytest.mark.gpu
+def test_tensor2_ffn_train_step_parity(P):
+    import torch
+    q, D, F, M = 4, 256, 1024, 1000
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q, "tensor2")
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q, "tensor2")
+    seed = 900
+    X = synth.gaussian(seed, 0, (M, D), 1.0, "bf16")
+    Wu = synth.gaussian(seed, 1, (D, F), 0.02, "bf16")
+    Wd = synth.gaussian(seed, 2, (F, D), 0.02, "bf16")
+    bu = synth.gaussian(seed, 3, (F,), 0.02, "f32")
+    bd = synth.gaussian(seed, 4, (D,), 0.02, "f32")
+    dY = synth.gaussian(seed, 5, (M, D), 1.0, "bf16")
+    t = _interval_types(M, q, 256)
+    td = types_dev(t)
+    Z, H, Y = P.star_ffn_fwd(up_g, dn_g, td, to_dev(X), to_dev(Wu), f32_dev(bu.exact), to_dev(Wd),
+                             f32_dev(bd.exact), "gelu", out_dtype=torch.float32)
+    rZ, rH, rY = oracle.ffn_fwd(up_o, dn_o, t, X.exact, Wu.exact, bu.exact, Wd.exact, bd.exact)
+    assert rel_fro(to_host(Z), rZ) <= TOL_BF16
+    assert rel_fro(to_host(H), rH) <= TOL_BF16
+    assert rel_fro(to_host(Y), rY) <= TOL_BF16
+    g = P.star_ffn_bwd(up_g, dn_g, td, to_dev(X), Z, H, to_dev(Wu), to_dev(Wd), to_dev(dY), "gelu")
+    ref = oracle.ffn_bwd(up_o, dn_o, t, X.exact, rZ, rH, Wu.exact, Wd.exact, dY.exact)
+    for k in ("dZ", "dX", "dW_up", "db_up", "dW_down", "db_down"):
+        assert rel_fro(to_host(g[k]), ref[k]) <= TOL_BF16, k
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("M", [1, 8, 40])
+def test_tensor2_decode_parity(P, M):
+    import torch
+    q, D, F, L = 4, 256, 1024, 3
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q, "tensor2")
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q, "tensor2")
+    seed = 950 + M
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.02, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.02, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 70 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 100 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = ((synth.decode_positions(seed, M) % 768) // 192).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                      [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                      [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
