@@ -273,6 +273,7 @@ def main():
     if not args.no_extra:
         result["training"] = bench_training(P, synth, torch, np, dev, T, args)
         result["qsweep"] = bench_qsweep(P, synth, torch, np, dev, T, flush, args)
+        result["tensor2"] = bench_tensor2(P, synth, torch, np, dev, T, args)
 
     # ---- CPU oracle baseline -------------------------------------------------
     if not args.no_cpu:
@@ -450,6 +451,46 @@ def bench_training(P, synth, torch, np, dev, T, args):
     res["speedup"] = round(res["dense"]["step_ms"] / res["star"]["step_ms"], 3)
     res["mfma_peak_frac"] = round(res["star"]["tflops"] / PEAK_BF16_TFLOPS, 4)
     log("training:", json.dumps(res))
+    return res
+
+
+def bench_tensor2(P, synth, torch, np, dev, T, args):
+    """The pilot's law, the tensor square of the two-group law (q = 4, 36
+    block products), on the FFN up-projection shape: M = 8192, 768 -> 3072
+    in groups of 192 / 768, bias + GELU, interval row types
+    floor((p mod 768) / 192); the same-code dense control beside it."""
+    M, K, N, q = 8192, 768, 3072, 4
+    alg = P.Algebra.equal(q, K, N, "tensor2")
+    X = to_dev_bf16(synth.gaussian(6, 0, (M, K), 1.0, "bf16"), torch, dev)
+    W = to_dev_bf16(synth.gaussian(6, 1, (K, N), 0.02, "bf16"), torch, dev)
+    b = torch.from_numpy(synth.gaussian(6, 2, (N,), 0.02, "f32").raw).to(dev)
+    t = ((np.arange(M) % 768) // 192).astype(np.int32)
+    td = torch.from_numpy(t).to(dev)
+    plan = P.star_type_plan(q, td)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    rows = np.bincount(t, minlength=q)
+    res = {"workload": "Q_2 (x) Q_2 FFN up-projection + bias + GELU, M=8192, 768->3072 in groups "
+                       "192/768, bf16, row type = floor((p mod 768) / 192)"}
+    for law in ("tensor2", "dense"):
+        a = alg.with_law(law)
+        for _ in range(args.warmup):
+            P.star_proj_fwd_planned(a, plan, X, W, b, "gelu", Y=Y)
+        torch.cuda.synchronize()
+        n = max(20, args.steps)
+        ks = [(T.ev(), T.ev()) for _ in range(n)]
+        for s0, s1 in ks:
+            s0.record()
+            P.star_proj_fwd_planned(a, plan, X, W, b, "gelu", Y=Y)
+            s1.record()
+        torch.cuda.synchronize()
+        ms = statistics.mean(s0.elapsed_time(s1) for s0, s1 in ks)
+        fl = 2 * P.star_count_macs(a, rows)
+        res[law] = {"kernel_us": round(ms * 1e3, 1), "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
+                    "gflop": round(fl / 1e9, 3)}
+    res["speedup"] = round(res["dense"]["kernel_us"] / res["tensor2"]["kernel_us"], 3)
+    res["ideal"] = round(16 / 9, 3)
+    res["products_per_type"] = P.star_count_products(alg)[0]
+    log("tensor2:", json.dumps(res))
     return res
 
 
