@@ -78,19 +78,21 @@ __device__ __forceinline__ void mask_ranges(uint32_t m, int& lo0, int& hi0, int&
 
 // A pass selects, per class, the C-column groups of its tiles: the star
 // law puts the tiles with two K segments first, the dense law has one pass;
-// law 2 sorts by the number of runs of the contraction mask (two, then
-// one), with the mode folded into the selector.
+// law 2 puts the tiles that contract over more than half of the groups
+// first, with the mode folded into the selector.
 __device__ __forceinline__ int sel_for(int mode, int law, int pass) {
   if (law == 1) return pass == 0 ? kSelAll : kSelNone;
   if (law == 2) return kSelTensor + 2 * mode + pass;
   if (mode == kModeFwd) return pass == 0 ? kSelExcept : kSelOnly;
   return pass == 0 ? kSelOnly : kSelExcept;  // BWD_DATA and BWD_WEIGHT
 }
-// law 2: is column group j of class i in the selector's pass?
+// law 2: is column group j of class i in the selector's pass?  Pass 0
+// holds the tiles whose contraction spans more than half of the groups (the
+// longest), pass 1 the rest, so that long tiles start first.
 __device__ __forceinline__ bool tensor_in_pass(const GemmParams& p, int sel, int i, int j) {
   const int mode = (sel - kSelTensor) >> 1, pass = (sel - kSelTensor) & 1;
-  const int runs = mask_runs(tensor_mask(mode, p.q, i, j));
-  return runs == (pass == 0 ? 2 : 1);
+  const bool wide = 2 * __popc(tensor_mask(mode, p.q, i, j)) > p.q;
+  return pass == 0 ? wide : !wide;
 }
 
 __device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
