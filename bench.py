@@ -490,6 +490,38 @@ def bench_tensor2(P, synth, torch, np, dev, T, args):
     res["speedup"] = round(res["dense"]["kernel_us"] / res["tensor2"]["kernel_us"], 3)
     res["ideal"] = round(16 / 9, 3)
     res["products_per_type"] = P.star_count_products(alg)[0]
+    del X, W, Y, plan
+    torch.cuda.empty_cache()
+
+    # the same law through the 12-layer decode stack (d_model 768, d_ff 3072)
+    D, F, L = 768, 3072, 12
+    up, dn = P.Algebra.equal(q, D, F, "tensor2"), P.Algebra.equal(q, F, D, "tensor2")
+    Wu = [to_dev_bf16(synth.gaussian(6, 10 + l, (D, F), 0.02, "bf16"), torch, dev) for l in range(L)]
+    Wd = [to_dev_bf16(synth.gaussian(6, 40 + l, (F, D), 0.02, "bf16"), torch, dev) for l in range(L)]
+    bu = [torch.from_numpy(synth.gaussian(6, 70 + l, (F,), 0.02, "f32").raw).to(dev) for l in range(L)]
+    bdn = [torch.from_numpy(synth.gaussian(6, 100 + l, (D,), 0.02, "f32").raw).to(dev) for l in range(L)]
+    dec = {}
+    for Md in (1, 64):
+        Xd = to_dev_bf16(synth.gaussian(6, 200 + Md, (Md, D), 1.0, "bf16"), torch, dev)
+        tdd = torch.from_numpy(((synth.decode_positions(6, Md) % 768) // 192).astype(np.int32)).to(dev)
+        Yd = torch.empty((Md, D), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(P.star_workspace_bytes("decode", up, dn, Md), dtype=torch.uint8, device=dev)
+        one = {}
+        for law in ("tensor2", "dense"):
+            u, d = up.with_law(law), dn.with_law(law)
+            for _ in range(args.warmup):
+                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws)
+            torch.cuda.synchronize()
+            n = max(20, args.steps)
+            e0, e1 = T.ev(), T.ev()
+            e0.record()
+            for _ in range(n):
+                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            one[law] = {"step_us_warm": round(e0.elapsed_time(e1) / n * 1e3, 1)}
+        dec[f"M{Md}"] = one
+    res["decode"] = dec
     log("tensor2:", json.dumps(res))
     return res
 
