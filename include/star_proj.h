@@ -105,7 +105,8 @@ typedef enum {
 
 /*
  * Forward projection with fused bias and activation (Alg. 1; eqs. typed-diag,
- * typed-off).
+ * typed-off): a type-i row's output group j is the sum of x_k W_kj over the
+ * input groups k in the law's B(i, j).
  *   row_type  device int32[M]
  *   X         device [M, K] row-major, dtype xt
  *   W         device [K, N] row-major (the canonical bank, never repacked),
@@ -127,7 +128,8 @@ star_status star_proj_fwd(const star_algebra *alg, int64_t M, const int32_t *row
  * Activation gradient (App. "Vector--Jacobian Products", eqs. vjp-xi and
  * vjp-xj): for a type-i row with output gradient dY,
  *   dX_i = sum_j dY_j W_ij^T   and   dX_k = dY_k W_kk^T (k != i)
- * (law DENSE: dX = dY W^T).  If Z_prev is given, the result is multiplied
+ * (law DENSE: dX = dY W^T; in general dX_k = sum of dY_j W_kj^T over the
+ * output groups j whose B(i, j) holds k).  If Z_prev is given, the result is multiplied
  * elementwise by act_prev'(Z_prev): the gradient through the activation that
  * produced this projection's input, fused into the epilogue.
  *   dY      device [M, N], dtype dyt
@@ -146,7 +148,8 @@ star_status star_proj_bwd_data(const star_algebra *alg, int64_t M, const int32_t
  *   dW_jj = sum over all rows of x_j^T dY_j
  *   dW_ij = sum over rows of type i of x_i^T dY_j   (j != i)
  *   dbias = sum over all rows of dY
- * (law DENSE: dW = X^T dY).  dW and dbias are overwritten with the full-batch
+ * (law DENSE: dW = X^T dY; in general dW_kj sums x_k^T dY_j over the rows whose
+ * type i has k in B(i, j)).  dW and dbias are overwritten with the full-batch
  * sums; a block that no row reaches is written as zeros.
  *   X      device [M, K], dtype xt
  *   dY     device [M, N], dtype dyt == xt
