@@ -34,7 +34,7 @@ _SRC = os.path.join(_HERE, "star_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 LAWS = {"star": 0, "dense": 1, "tensor2": 2}
-ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2}
+ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2, "silu": 3}
 
 
 def build(force: bool = False) -> str:
@@ -318,6 +318,48 @@ def ffn_bwd(up: Alg, down: Alg, t, X, Z, H, W_up, W_down, dY, act: str = "gelu",
     dW_down, db_down = proj_bwd_weight(down, t, H, dY)
     dW_up, db_up = proj_bwd_weight(up, t, X, dZ)
     return dict(dX=dX, dZ=dZ, dW_up=dW_up, db_up=db_up, dW_down=dW_down, db_down=db_down)
+
+
+def swiglu_ffn_fwd(up: Alg, down: Alg, t, X, W_gate, b_gate, W_up, b_up, W_down, b_down,
+                   mirror_bf16: bool = True):
+    """Gated FFN (SwiGLU) with the same row types on all three projections:
+    Z_g = X * W_gate + b_gate;  Z_u = X * W_up + b_up;
+    H = silu(Z_g) . Z_u;  Y = H * W_down + b_down.
+    Gate and up are two projections of the same layout ``up``.  With
+    ``mirror_bf16`` Z_g, Z_u and H are rounded to bfloat16, as the GPU path
+    stores them.  Returns (Z_g, Z_u, H, Y)."""
+    Zg, _, _, _ = proj_fwd(up, t, X, W_gate, b_gate, "none")
+    Zu, _, _, _ = proj_fwd(up, t, X, W_up, b_up, "none")
+    if mirror_bf16:
+        Zg, Zu = round_bf16(Zg), round_bf16(Zu)
+    H = act("silu", Zg) * Zu
+    if mirror_bf16:
+        H = round_bf16(H)
+    Y, _, _, _ = proj_fwd(down, t, H, W_down, b_down, "none")
+    return Zg, Zu, H, Y
+
+
+def swiglu_ffn_bwd(up: Alg, down: Alg, t, X, Zg, Zu, H, W_gate, W_up, W_down, dY,
+                   mirror_bf16: bool = True):
+    """Backward of ``swiglu_ffn_fwd``:
+    dH = dY *^T W_down;  dZ_g = dH . Z_u . silu'(Z_g);  dZ_u = dH . silu(Z_g);
+    dX = dZ_g *^T W_gate + dZ_u *^T W_up;  dW_gate, db_gate from (X, dZ_g);
+    dW_up, db_up from (X, dZ_u);  dW_down, db_down from (H, dY).
+    With ``mirror_bf16`` the stored dH, dZ_g and dZ_u are rounded to
+    bfloat16.  Returns a dict of the gradients and dZ_g, dZ_u."""
+    dH = proj_bwd_data(down, t, dY, W_down)
+    if mirror_bf16:
+        dH = round_bf16(dH)
+    dZg = dH * Zu * act_grad("silu", Zg)
+    dZu = dH * act("silu", Zg)
+    if mirror_bf16:
+        dZg, dZu = round_bf16(dZg), round_bf16(dZu)
+    dX = proj_bwd_data(up, t, dZg, W_gate) + proj_bwd_data(up, t, dZu, W_up)
+    dW_gate, db_gate = proj_bwd_weight(up, t, X, dZg)
+    dW_up, db_up = proj_bwd_weight(up, t, X, dZu)
+    dW_down, db_down = proj_bwd_weight(down, t, H, dY)
+    return dict(dX=dX, dZ_gate=dZg, dZ_up=dZu, dW_gate=dW_gate, db_gate=db_gate, dW_up=dW_up,
+                db_up=db_up, dW_down=dW_down, db_down=db_down)
 
 
 def decode_stack(up: Alg, down: Alg, t, X, W_ups, b_ups, W_downs, b_downs,

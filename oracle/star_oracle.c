@@ -37,7 +37,8 @@
  *          d.  L = 1 is Q_2; L = 2 is the pilot's 36-product law.
  *
  * Activations: 0 none, 1 GELU with the exact erf form
- * 0.5 z (1 + erf(z / sqrt 2)), 2 GELU with the tanh form.  The paper keeps
+ * 0.5 z (1 + erf(z / sqrt 2)), 2 GELU with the tanh form, 3 SiLU
+ * z / (1 + exp(-z)) (the gate of a SwiGLU FFN).  The paper keeps
  * biases and pointwise activations at their usual definitions (Sec. 4,
  * "Projection Shapes"); which activation to use is not fixed by the paper.
  */
@@ -53,6 +54,7 @@
 #define ORACLE_ACT_NONE 0
 #define ORACLE_ACT_GELU 1
 #define ORACLE_ACT_GELU_TANH 2
+#define ORACLE_ACT_SILU 3
 
 /* k in B(i,j)?  Sec. 5.1: B(i,j) = {i,j} as a set for Q_q; all k for the
  * ordinary product. */
@@ -91,6 +93,8 @@ double oracle_act(int act, double z)
         double u = kSqrt2OverPi * (z + 0.044715 * z * z * z);
         return 0.5 * z * (1.0 + tanh(u));
     }
+    case ORACLE_ACT_SILU:
+        return z / (1.0 + exp(-z));
     default:
         return z;
     }
@@ -108,6 +112,11 @@ double oracle_act_grad(int act, double z)
         double t = tanh(u);
         double du = kSqrt2OverPi * (1.0 + 3.0 * 0.044715 * z * z);
         return 0.5 * (1.0 + t) + 0.5 * z * (1.0 - t * t) * du;
+    }
+    case ORACLE_ACT_SILU: {
+        /* s + z s (1 - s) with s the logistic sigmoid */
+        double sg = 1.0 / (1.0 + exp(-z));
+        return sg + z * sg * (1.0 - sg);
     }
     default:
         return 1.0;

@@ -428,7 +428,14 @@ def test_gelu_against_libm():
     assert oracle.act("none", 1.25)[()] == 1.25
 
 
-@pytest.mark.parametrize("kind", ["gelu", "gelu_tanh", "none"])
+def test_silu_against_scipy():
+    """SiLU z sigma(z), with scipy's logistic function as the reference."""
+    from scipy.special import expit
+    zs = np.linspace(-30, 30, 241)
+    np.testing.assert_allclose(oracle.act("silu", zs), zs * expit(zs), rtol=1e-14, atol=1e-300)
+
+
+@pytest.mark.parametrize("kind", ["gelu", "gelu_tanh", "silu", "none"])
 def test_activation_gradient_fd(kind):
     h = 1e-6
     for z in np.linspace(-6, 6, 61):
@@ -566,3 +573,39 @@ def test_tensor_power_counts(L):
     alg = Alg.equal(q, 4 * q, 8 * q, "tensor2")
     total = sum(oracle.row_macs(alg, i) for i in range(q))
     assert total * 4 ** L == 3 ** L * q * alg.K * alg.N
+
+
+# ---- gated FFN (SwiGLU) compositions ---------------------------------------------
+
+def test_swiglu_ffn_is_its_formula_and_gradients_match_fd():
+    """The gated FFN through the typed projections equals the same FFN built
+    from masked dense products; its backward matches central differences of a
+    scalar loss (fp64, no bf16 mirroring)."""
+    from scipy.special import expit
+    up, down = Alg(2, (3, 5), (4, 6)), Alg(2, (4, 6), (3, 5))
+    g = rng(41)
+    M = 9
+    X = g.standard_normal((M, up.K))
+    Wg, Wu = g.standard_normal((up.K, up.N)), g.standard_normal((up.K, up.N))
+    Wd = g.standard_normal((down.K, down.N))
+    bg, bu, bd = g.standard_normal(up.N), g.standard_normal(up.N), g.standard_normal(down.N)
+    t = g.integers(0, 2, M).astype(np.int32)
+    Zg, Zu, H, Y = oracle.swiglu_ffn_fwd(up, down, t, X, Wg, bg, Wu, bu, Wd, bd, mirror_bf16=False)
+    zg = masked_dense_fwd(up, t, X, Wg) + bg
+    zu = masked_dense_fwd(up, t, X, Wu) + bu
+    h = zg * expit(zg) * zu
+    np.testing.assert_allclose(H, h, atol=1e-12)
+    np.testing.assert_allclose(Y, masked_dense_fwd(down, t, h, Wd) + bd, atol=1e-11)
+    G = g.standard_normal(Y.shape)
+    grads = oracle.swiglu_ffn_bwd(up, down, t, X, Zg, Zu, H, Wg, Wu, Wd, G, mirror_bf16=False)
+    loss = lambda **kw: np.sum(oracle.swiglu_ffn_fwd(up, down, t, kw.get("X", X), kw.get("Wg", Wg), bg,
+                                                     kw.get("Wu", Wu), bu, kw.get("Wd", Wd), bd,
+                                                     mirror_bf16=False)[3] * G)
+    eps = 1e-6
+    for name, arr, key in (("X", X, "dX"), ("Wg", Wg, "dW_gate"), ("Wu", Wu, "dW_up"), ("Wd", Wd, "dW_down")):
+        for (a_, b_) in [(0, 0), (2, 3), (arr.shape[0] - 1, arr.shape[1] - 1)]:
+            P_, Mn = arr.copy(), arr.copy()
+            P_[a_, b_] += eps
+            Mn[a_, b_] -= eps
+            fd = (loss(**{name: P_}) - loss(**{name: Mn})) / (2 * eps)
+            assert abs(fd - grads[key][a_, b_]) < 1e-6 * max(1, abs(fd)), (name, a_, b_)
