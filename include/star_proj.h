@@ -266,6 +266,27 @@ star_status star_validate_types(int64_t M, const int32_t *row_type, int32_t q,
                                 int64_t *n_bad, void *ws, size_t ws_bytes,
                                 hipStream_t stream);
 
+/*
+ * Gated FFN (SwiGLU) pieces.  The paper's gated FFN has two D x F maps (gate
+ * and up) and one F x D map, each a row-typed projection with the same row
+ * types (Sec. 4, "Projection Shapes"; Sec. "Small Pretraining Study", the pilot's
+ * bias-free SwiGLU FFN); the gate and the product keep their usual
+ * definitions.  The three projections run through star_proj_*; these calls
+ * are the elementwise steps between them.  n elements (a multiple of 8) of
+ * dtype dt, every buffer device memory, 16-byte aligned, not overlapping;
+ * silu(z) = z / (1 + exp(-z)).
+ *   star_swiglu_fwd:  H = silu(Z_gate) . Z_up
+ *   star_swiglu_bwd:  dZ_gate = dH . Z_up . silu'(Z_gate);  dZ_up = dH . silu(Z_gate)
+ *   star_add:         out = a + b (the two activation gradients of a gated
+ *                     FFN's input); out may alias a or b.
+ */
+star_status star_swiglu_fwd(int64_t n, const void *Z_gate, const void *Z_up, star_dtype dt, void *H,
+                            hipStream_t stream);
+star_status star_swiglu_bwd(int64_t n, const void *dH, const void *Z_gate, const void *Z_up,
+                            star_dtype dt, void *dZ_gate, void *dZ_up, hipStream_t stream);
+star_status star_add(int64_t n, const void *a, const void *b, star_dtype dt, void *out,
+                     hipStream_t stream);
+
 /* Static description of a status code. */
 const char *star_status_string(star_status s);
 

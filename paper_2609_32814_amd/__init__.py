@@ -13,7 +13,8 @@ _EXPORTS = (
     "star_plan_bytes", "star_proj_bwd_data", "star_proj_bwd_data_planned",
     "star_proj_bwd_weight", "star_proj_bwd_weight_planned", "star_proj_fwd",
     "star_proj_fwd_planned", "star_status_string", "star_type_plan", "star_validate_types",
-    "star_workspace_bytes",
+    "star_workspace_bytes", "star_swiglu_fwd", "star_swiglu_bwd", "star_add", "star_swiglu_ffn_fwd",
+    "star_swiglu_ffn_bwd",
 )
 
 __all__ = list(_EXPORTS)

@@ -65,12 +65,15 @@ def _load() -> ctypes.CDLL:
     lib.star_proj_fwd_planned.argtypes = [A, i64, P, P, E, P, E, P, E, P, P, E, P]
     lib.star_proj_bwd_data_planned.argtypes = [A, i64, P, P, E, P, E, P, E, P, E, P]
     lib.star_proj_bwd_weight_planned.argtypes = [A, i64, P, P, E, P, E, P, P, P, sz, P]
+    lib.star_swiglu_fwd.argtypes = [i64, P, P, E, P, P]
+    lib.star_swiglu_bwd.argtypes = [i64, P, P, P, E, P, P, P]
+    lib.star_add.argtypes = [i64, P, P, E, P, P]
     lib.star_status_string.argtypes = [E]
     lib.star_status_string.restype = ctypes.c_char_p
     for name in ("star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
                  "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
-                 "star_proj_bwd_weight_planned"):
+                 "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add"):
         getattr(lib, name).restype = E
     return lib
 
@@ -339,3 +342,67 @@ def star_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Te
     dW_up, db_up = star_proj_bwd_weight_planned(up, plan, X, dZ, ws=ws)
     dX = star_proj_bwd_data_planned(up, plan, dZ, W_up)
     return dict(dX=dX, dZ=dZ, dW_up=dW_up, db_up=db_up, dW_down=dW_down, db_down=db_down)
+
+
+# ---- gated FFN (SwiGLU) --------------------------------------------------------------
+
+
+def star_swiglu_fwd(Z_gate: torch.Tensor, Z_up: torch.Tensor, H=None) -> torch.Tensor:
+    """H = silu(Z_gate) . Z_up (elementwise, on the GPU)."""
+    if H is None:
+        H = torch.empty_like(Z_gate)
+    _check(LIB.star_swiglu_fwd(Z_gate.numel(), _ptr(Z_gate), _ptr(Z_up), _dt(Z_gate), _ptr(H),
+                               _stream(Z_gate.device)), "star_swiglu_fwd")
+    return H
+
+
+def star_swiglu_bwd(dH: torch.Tensor, Z_gate: torch.Tensor, Z_up: torch.Tensor):
+    """(dZ_gate, dZ_up) = (dH . Z_up . silu'(Z_gate), dH . silu(Z_gate))."""
+    dZg, dZu = torch.empty_like(dH), torch.empty_like(dH)
+    _check(LIB.star_swiglu_bwd(dH.numel(), _ptr(dH), _ptr(Z_gate), _ptr(Z_up), _dt(dH), _ptr(dZg),
+                               _ptr(dZu), _stream(dH.device)), "star_swiglu_bwd")
+    return dZg, dZu
+
+
+def star_add(a: torch.Tensor, b: torch.Tensor, out=None) -> torch.Tensor:
+    """out = a + b (elementwise, on the GPU; out may be a or b)."""
+    if out is None:
+        out = torch.empty_like(a)
+    _check(LIB.star_add(a.numel(), _ptr(a), _ptr(b), _dt(a), _ptr(out), _stream(a.device)), "star_add")
+    return out
+
+
+def star_swiglu_ffn_fwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                        W_gate: torch.Tensor, b_gate, W_up: torch.Tensor, b_up, W_down: torch.Tensor,
+                        b_down, plan=None, out_dtype=None):
+    """Gated FFN with one type plan for its three projections:
+    Z_g = X *_q W_gate + b_gate, Z_u = X *_q W_up + b_up, H = silu(Z_g) . Z_u,
+    Y = H *_q W_down + b_down.  Returns (Z_g, Z_u, H, Y)."""
+    if plan is None:
+        plan = star_type_plan(up.q, row_type)
+    Zg = star_proj_fwd_planned(up, plan, X, W_gate, b_gate, "none")
+    Zu = star_proj_fwd_planned(up, plan, X, W_up, b_up, "none")
+    H = star_swiglu_fwd(Zg, Zu)
+    Y = star_proj_fwd_planned(down, plan, H, W_down, b_down, "none", out_dtype=out_dtype)
+    return Zg, Zu, H, Y
+
+
+def star_swiglu_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                        Z_gate: torch.Tensor, Z_up: torch.Tensor, H: torch.Tensor, W_gate: torch.Tensor,
+                        W_up: torch.Tensor, W_down: torch.Tensor, dY: torch.Tensor, plan=None, ws=None):
+    """Backward of ``star_swiglu_ffn_fwd``: dH = dY *^T W_down; the gate's
+    elementwise backward; dX = dZ_g *^T W_gate + dZ_u *^T W_up; the three
+    weight and bias gradients.  Returns a dict of dX, dZ_gate, dZ_up,
+    dW_gate, db_gate, dW_up, db_up, dW_down, db_down."""
+    if plan is None:
+        plan = star_type_plan(up.q, row_type)
+    dH = star_proj_bwd_data_planned(down, plan, dY, W_down, out_dtype=X.dtype)
+    dZg, dZu = star_swiglu_bwd(dH, Z_gate, Z_up)
+    dW_down, db_down = star_proj_bwd_weight_planned(down, plan, H, dY, ws=ws)
+    dW_gate, db_gate = star_proj_bwd_weight_planned(up, plan, X, dZg, ws=ws)
+    dW_up, db_up = star_proj_bwd_weight_planned(up, plan, X, dZu, ws=ws)
+    # the two input gradients in fp32, summed once
+    dX = star_proj_bwd_data_planned(up, plan, dZg, W_gate, out_dtype=torch.float32)
+    dX = star_add(dX, star_proj_bwd_data_planned(up, plan, dZu, W_up, out_dtype=torch.float32), out=dX)
+    return dict(dX=dX, dZ_gate=dZg, dZ_up=dZu, dW_gate=dW_gate, db_gate=db_gate, dW_up=dW_up,
+                db_up=db_up, dW_down=dW_down, db_down=db_down)

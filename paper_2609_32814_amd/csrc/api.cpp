@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 
 #include "../../include/star_proj.h"
 #include "kernels.hpp"
@@ -810,6 +811,40 @@ star_status star_validate_types(int64_t M, const int32_t* row_type, int32_t q, i
   if (e != hipSuccess) return STAR_ERR_HIP;
   *n_bad = static_cast<int64_t>(host);
   return STAR_OK;
+}
+
+namespace {
+star_status check_elementwise(int64_t n, star_dtype dt, std::initializer_list<const void*> ptrs) {
+  if (!valid_dtype(dt)) return STAR_ERR_DTYPE;
+  if (n < 0 || n > kMaxDim * kMaxDim) return STAR_ERR_SHAPE;
+  if (n % 8) return STAR_ERR_ALIGN;
+  if (n == 0) return STAR_OK;
+  for (const void* q : ptrs) {
+    if (!q) return STAR_ERR_ARG;
+    if (!aligned16(q)) return STAR_ERR_ALIGN;
+  }
+  return STAR_OK;
+}
+}  // namespace
+
+star_status star_swiglu_fwd(int64_t n, const void* Z_gate, const void* Z_up, star_dtype dt, void* H,
+                            hipStream_t stream) {
+  star_status st = check_elementwise(n, dt, {Z_gate, Z_up, H});
+  if (st != STAR_OK || n == 0) return st;
+  return hip_status(launch_swiglu_fwd(n, dt == STAR_BF16 ? 1 : 0, Z_gate, Z_up, H, stream));
+}
+
+star_status star_swiglu_bwd(int64_t n, const void* dH, const void* Z_gate, const void* Z_up, star_dtype dt,
+                            void* dZ_gate, void* dZ_up, hipStream_t stream) {
+  star_status st = check_elementwise(n, dt, {dH, Z_gate, Z_up, dZ_gate, dZ_up});
+  if (st != STAR_OK || n == 0) return st;
+  return hip_status(launch_swiglu_bwd(n, dt == STAR_BF16 ? 1 : 0, dH, Z_gate, Z_up, dZ_gate, dZ_up, stream));
+}
+
+star_status star_add(int64_t n, const void* a, const void* b, star_dtype dt, void* out, hipStream_t stream) {
+  star_status st = check_elementwise(n, dt, {a, b, out});
+  if (st != STAR_OK || n == 0) return st;
+  return hip_status(launch_add(n, dt == STAR_BF16 ? 1 : 0, a, b, out, stream));
 }
 
 }  // extern "C"

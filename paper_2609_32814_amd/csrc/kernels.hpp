@@ -69,6 +69,12 @@ hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm
                              int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream);
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream);
+// Gated FFN elementwise parts (swiglu.hip); n a multiple of 8, elem 1 bf16
+// or 0 fp32, 16-byte aligned buffers.
+hipError_t launch_swiglu_fwd(int64_t n, int elem, const void* zg, const void* zu, void* h, hipStream_t stream);
+hipError_t launch_swiglu_bwd(int64_t n, int elem, const void* dh, const void* zg, const void* zu, void* dzg,
+                             void* dzu, hipStream_t stream);
+hipError_t launch_add(int64_t n, int elem, const void* a, const void* b, void* out, hipStream_t stream);
 hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
 // out[i] = sum over c < n_parts of part[c * n + i], in c order.
 hipError_t launch_sum_partials(const float* part, int n_parts, int64_t n, float* out,

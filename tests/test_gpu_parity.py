@@ -715,3 +715,74 @@ def test_tensor2_decode_parity(P, M):
     ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
                               [w.exact for w in Wd], [b.exact for b in bd])
     assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
+def test_tensor2_full_size_sampled(P):
+    """The bench's tensor-square workload at full size (M = 8192, 768 -> 3072 in
+    groups 192 / 768, bias + GELU, interval types), through the planned entry
+    point as the bench launches it; sampled rows against the oracle."""
+    M, K, N, q = 8192, 768, 3072, 4
+    ga, oa = algs(P, q, [192] * 4, [768] * 4, "tensor2")
+    X = synth.gaussian(6, 0, (M, K), 1.0, "bf16")
+    W = synth.gaussian(6, 1, (K, N), 0.02, "bf16")
+    b = synth.gaussian(6, 2, (N,), 0.02, "f32")
+    t = _interval_types(M, q)
+    plan = P.star_type_plan(q, types_dev(t))
+    Y = P.star_proj_fwd_planned(ga, plan, to_dev(X), to_dev(W), f32_dev(b.exact), "gelu")
+    rows = _sample_rows(M, 300, 6)
+    ref, _, _, _ = oracle.proj_fwd(oa, t[rows], X.exact[rows], W.exact, b.exact, "gelu")
+    assert rel_fro(to_host(Y[rows]), ref) <= TOL_BF16
+
+
+# ---- gated FFN (SwiGLU) -------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_swiglu_elementwise(P, dtype):
+    import torch
+    n = 4096 * 3
+    Zg = synth.gaussian(61, 0, (n,), 2.0, dtype)
+    Zu = synth.gaussian(61, 1, (n,), 1.0, dtype)
+    dH = synth.gaussian(61, 2, (n,), 1.0, dtype)
+    H = P.star_swiglu_fwd(to_dev(Zg), to_dev(Zu))
+    ref = oracle.act("silu", Zg.exact) * Zu.exact
+    assert rel_fro(to_host(H), ref) <= bar(dtype)
+    dZg, dZu = P.star_swiglu_bwd(to_dev(dH), to_dev(Zg), to_dev(Zu))
+    assert rel_fro(to_host(dZg), dH.exact * Zu.exact * oracle.act_grad("silu", Zg.exact)) <= bar(dtype)
+    assert rel_fro(to_host(dZu), dH.exact * oracle.act("silu", Zg.exact)) <= bar(dtype)
+    a = to_dev(Zg)
+    out = P.star_add(a, to_dev(Zu), out=a)  # in place
+    assert rel_fro(to_host(out), Zg.exact + Zu.exact) <= bar(dtype)
+
+
+@pytest.mark.parametrize("q,law,bias", [(2, "star", True), (4, "tensor2", False), (2, "dense", True)])
+def test_swiglu_ffn_train_step_parity(P, q, law, bias):
+    """Gated FFN forward and backward (three projections with one plan, the
+    elementwise gate, the summed input gradient) against the oracle."""
+    import torch
+    D, F, M = 256, 512, 1000
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q, law)
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q, law)
+    seed = 970 + q
+    X = synth.gaussian(seed, 0, (M, D), 1.0, "bf16")
+    Wg = synth.gaussian(seed, 1, (D, F), 0.05, "bf16")
+    Wu = synth.gaussian(seed, 2, (D, F), 0.05, "bf16")
+    Wd = synth.gaussian(seed, 3, (F, D), 0.05, "bf16")
+    bg = synth.gaussian(seed, 4, (F,), 0.02, "f32") if bias else None
+    bu = synth.gaussian(seed, 5, (F,), 0.02, "f32") if bias else None
+    bd = synth.gaussian(seed, 6, (D,), 0.02, "f32") if bias else None
+    dY = synth.gaussian(seed, 7, (M, D), 1.0, "bf16")
+    t = _interval_types(M, q, 256) if law == "tensor2" else synth.sequence_types(M, q, 256)
+    td = types_dev(t)
+    dev_b = lambda b: f32_dev(b.exact) if b is not None else None
+    ex_b = lambda b: b.exact if b is not None else None
+    Zg, Zu, H, Y = P.star_swiglu_ffn_fwd(up_g, dn_g, td, to_dev(X), to_dev(Wg), dev_b(bg), to_dev(Wu),
+                                         dev_b(bu), to_dev(Wd), dev_b(bd), out_dtype=torch.float32)
+    rZg, rZu, rH, rY = oracle.swiglu_ffn_fwd(up_o, dn_o, t, X.exact, Wg.exact, ex_b(bg), Wu.exact,
+                                             ex_b(bu), Wd.exact, ex_b(bd))
+    for got, ref, k in ((Zg, rZg, "Zg"), (Zu, rZu, "Zu"), (H, rH, "H"), (Y, rY, "Y")):
+        assert rel_fro(to_host(got), ref) <= TOL_BF16, k
+    g = P.star_swiglu_ffn_bwd(up_g, dn_g, td, to_dev(X), Zg, Zu, H, to_dev(Wg), to_dev(Wu), to_dev(Wd),
+                              to_dev(dY))
+    ref = oracle.swiglu_ffn_bwd(up_o, dn_o, t, X.exact, rZg, rZu, rH, Wg.exact, Wu.exact, Wd.exact, dY.exact)
+    for k in ("dZ_gate", "dZ_up", "dX", "dW_gate", "db_gate", "dW_up", "db_up", "dW_down", "db_down"):
+        assert rel_fro(to_host(g[k]), ref[k]) <= TOL_BF16, k
