@@ -274,6 +274,7 @@ def main():
         result["training"] = bench_training(P, synth, torch, np, dev, T, args)
         result["qsweep"] = bench_qsweep(P, synth, torch, np, dev, T, flush, args)
         result["tensor2"] = bench_tensor2(P, synth, torch, np, dev, T, args)
+        result["pilot_ffn"] = bench_pilot_ffn(P, synth, torch, np, dev, T, args)
 
     # ---- CPU oracle baseline -------------------------------------------------
     if not args.no_cpu:
@@ -523,6 +524,51 @@ def bench_tensor2(P, synth, torch, np, dev, T, args):
         dec[f"M{Md}"] = one
     res["decode"] = dec
     log("tensor2:", json.dumps(res))
+    return res
+
+
+def bench_pilot_ffn(P, synth, torch, np, dev, T, args):
+    """The pretraining pilot's FFN: bias-free SwiGLU, D = 768, F = 1536, under
+    the tensor-square law Q_2 (x) Q_2 with interval row types, one training
+    step (three projections forward, their activation and weight gradients)
+    at M = 16384 tokens, beside the same-code dense control."""
+    M, D, F, q = 16384, 768, 1536, 4
+    up, dn = P.Algebra.equal(q, D, F, "tensor2"), P.Algebra.equal(q, F, D, "tensor2")
+    X = to_dev_bf16(synth.gaussian(8, 0, (M, D), 1.0, "bf16"), torch, dev)
+    Wg = to_dev_bf16(synth.gaussian(8, 1, (D, F), 0.02, "bf16"), torch, dev)
+    Wu = to_dev_bf16(synth.gaussian(8, 2, (D, F), 0.02, "bf16"), torch, dev)
+    Wd = to_dev_bf16(synth.gaussian(8, 3, (F, D), 0.02, "bf16"), torch, dev)
+    dY = to_dev_bf16(synth.gaussian(8, 4, (M, D), 1.0, "bf16"), torch, dev)
+    t = ((np.arange(M) % 768) // 192).astype(np.int32)
+    td = torch.from_numpy(t).to(dev)
+    rows = np.bincount(t, minlength=q)
+    res = {"workload": "bias-free SwiGLU FFN 768 -> 2 x 1536 -> 768, Q_2 (x) Q_2, M=16384, bf16, "
+                       "row type = floor((p mod 768) / 192); forward + backward"}
+    for law in ("tensor2", "dense"):
+        u, d = up.with_law(law), dn.with_law(law)
+        plan = P.star_type_plan(q, td)
+
+        def step():
+            P.star_type_plan(q, td, plan)
+            Zg, Zu, H, _ = P.star_swiglu_ffn_fwd(u, d, td, X, Wg, None, Wu, None, Wd, None, plan=plan)
+            P.star_swiglu_ffn_bwd(u, d, td, X, Zg, Zu, H, Wg, Wu, Wd, dY, plan=plan)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        n = max(10, args.steps // 2)
+        e0, e1 = T.ev(), T.ev()
+        e0.record()
+        for _ in range(n):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        fl = 3 * 2 * (2 * P.star_count_macs(u, rows) + P.star_count_macs(d, rows))
+        res[law] = {"step_ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 2),
+                    "gflop": round(fl / 1e9, 2)}
+    res["speedup"] = round(res["dense"]["step_ms"] / res["tensor2"]["step_ms"], 3)
+    log("pilot_ffn:", json.dumps(res))
     return res
 
 
