@@ -168,9 +168,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   // ---- tile iterators (the compute side and the load side walk one list) ----
   // XCD x (workgroups w with w % 8 == x) owns a contiguous chunk of each
   // pass's tiles; its workgroups deal out the two chunks as one list, pass 0
-  // (the longer, two-segment contractions) first, so that a workgroup that
-  // got two long tiles gets no short one and the steps per workgroup even
-  // out.
+  // (the longer contractions) first.
   const int xcd = blockIdx.x & 7;
   const int slot_stride = gridDim.x >> 3;
   int32_t pbase[2], pcount[2];
@@ -181,13 +179,18 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     pbase[ps] = xcd * chunk;
     pcount[ps] = max(0, min(total - xcd * chunk, chunk));
   }
+  // The XCD's workgroups take its list in snake order: in round r the
+  // workgroup in place s (of S) takes item r S + s for even r and
+  // r S + S - 1 - s for odd r, so a workgroup that got one of the first
+  // (longest) items gets one of the last (shortest) ones if any.
   struct Iter {
-    int32_t v;  // position in this XCD's list
+    int32_t r;  // this workgroup's round
   };
+  const int xslot = blockIdx.x >> 3;
   auto advance = [&](Iter& it, Tile& t) -> bool {
-    const int32_t v = it.v;
+    const int32_t v = it.r * slot_stride + ((it.r & 1) ? slot_stride - 1 - xslot : xslot);
     if (v >= pcount[0] + pcount[1]) return false;
-    it.v += slot_stride;
+    ++it.r;
     const int ps = v < pcount[0] ? 0 : 1;
     const int32_t logical = pbase[ps] + (ps == 0 ? v : v - pcount[0]);
     int cls = 0;
@@ -208,7 +211,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     }
   };
 
-  Iter cit{static_cast<int32_t>(blockIdx.x >> 3)};
+  Iter cit{0};
   Tile ct;
   if (!advance(cit, ct)) return;
   if constexpr (MODE == kModeBwdWeight) {
