@@ -35,7 +35,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int TN = kDecodeTileN;      // 16 output columns
 constexpr int SLICE = kDecodeSliceK;  // 32 K rows
-constexpr int MR = kDecodeMaxRows;    // 64 rows
 constexpr int kRedBytes = 4 * 4 * 64 * 16;  // 4 waves x 4 row blocks x 64 lanes x float4
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));

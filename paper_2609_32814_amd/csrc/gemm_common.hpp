@@ -91,7 +91,7 @@ __device__ __forceinline__ int sel_for(int mode, int law, int pass) {
 // longest), pass 1 the rest, so that long tiles start first.
 __device__ __forceinline__ bool tensor_in_pass(const GemmParams& p, int sel, int i, int j) {
   const int mode = (sel - kSelTensor) >> 1, pass = (sel - kSelTensor) & 1;
-  const bool wide = 2 * __popc(tensor_mask(mode, p.q, i, j)) > p.q;
+  const bool wide = 2 * static_cast<int>(__popc(tensor_mask(mode, p.q, i, j))) > p.q;
   return pass == 0 ? wide : !wide;
 }
 
