@@ -206,6 +206,26 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
                         void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * star_decode for a gated FFN stack (SwiGLU; Sec. 4, "Projection Shapes", and
+ * the pilot's bias-free SwiGLU FFN of Sec. "Small Pretraining Study"):
+ *   h <- h + ((silu(a *_q W_gate[l] + b_gate[l]) . (a *_q W_up[l] + b_up[l]))
+ *             *_q W_down[l] + b_down[l]),
+ * with a, h and H as in star_decode; W_gate has W_up's layout and the same
+ * row types.  Runs as the persistent stack only: STAR_ERR_UNSUPPORTED when
+ * its three weight slots do not fit in LDS (for D = 768: M above 52).
+ *   W_gate, b_gate  host arrays of n_layers device pointers (bf16 [D, F],
+ *                   float[F] or NULL); b_gate may be NULL
+ *   ws              at least star_workspace_bytes(STAR_OP_DECODE, up, down, M) bytes
+ */
+star_status star_decode_gated(const star_algebra *up, const star_algebra *down, int32_t n_layers,
+                              int64_t M, const int32_t *row_type, const void *X,
+                              const void *const *W_gate, const float *const *b_gate,
+                              const void *const *W_up, const float *const *b_up,
+                              const void *const *W_down, const float *const *b_down,
+                              int32_t residual, void *Y, star_dtype yt, void *ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/*
  * Type plan: the per-type row sets I_i of Algorithm alg:projection (the rows
  * whose position has type i) as one stable permutation of the rows grouped
  * by type plus q+1 offsets.  Every compute call needs it; the plain entry points build it in

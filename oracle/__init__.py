@@ -377,3 +377,23 @@ def decode_stack(up: Alg, down: Alg, t, X, W_ups, b_ups, W_downs, b_downs,
         _, _, f = ffn_fwd(up, down, t, a, Wu, bu, Wd, bd, act, mirror_bf16)
         h = h + f if residual else f
     return h
+
+
+def decode_stack_gated(up: Alg, down: Alg, t, X, W_gates, b_gates, W_ups, b_ups, W_downs, b_downs,
+                       residual: bool = True, mirror_bf16: bool = True):
+    """Gated-FFN (SwiGLU) stack for one decode step:
+    h <- h + (silu(a W_gate + b_gate) . (a W_up + b_up)) W_down + b_down with
+    a the bfloat16 rounding of h; the hidden H is stored in bfloat16, h is
+    carried at full precision (the pre-activations stay in fp32, as the GPU
+    stack keeps them in registers).  Returns the final h."""
+    h = _f64(X)
+    for Wg, bg, Wu, bu, Wd, bd in zip(W_gates, b_gates, W_ups, b_ups, W_downs, b_downs):
+        a = round_bf16(h) if mirror_bf16 else h
+        Zg, _, _, _ = proj_fwd(up, t, a, Wg, bg, "none")
+        Zu, _, _, _ = proj_fwd(up, t, a, Wu, bu, "none")
+        H = act("silu", Zg) * Zu
+        if mirror_bf16:
+            H = round_bf16(H)
+        f, _, _, _ = proj_fwd(down, t, H, Wd, bd, "none")
+        h = h + f if residual else f
+    return h

@@ -54,6 +54,9 @@ def _load() -> ctypes.CDLL:
     lib.star_ffn_fwd.argtypes = [A, A, i64, P, P, P, P, P, P, E, P, P, P, E, E, P, sz, P]
     lib.star_decode.argtypes = [A, A, i32, i64, P, P, ctypes.POINTER(P), ctypes.POINTER(P),
                                 ctypes.POINTER(P), ctypes.POINTER(P), E, i32, P, E, P, sz, P]
+    lib.star_decode_gated.argtypes = [A, A, i32, i64, P, P, ctypes.POINTER(P), ctypes.POINTER(P),
+                                      ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
+                                      ctypes.POINTER(P), i32, P, E, P, sz, P]
     lib.star_workspace_bytes.argtypes = [i32, A, A, i64]
     lib.star_workspace_bytes.restype = sz
     lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
@@ -73,7 +76,8 @@ def _load() -> ctypes.CDLL:
     for name in ("star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
                  "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
-                 "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add"):
+                 "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add",
+                 "star_decode_gated"):
         getattr(lib, name).restype = E
     return lib
 
@@ -324,6 +328,26 @@ def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Ten
     _check(LIB.star_decode(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), wu, bu, wd, bd,
                            ACTS[act], int(bool(residual)), _ptr(Y), _dt(Y), _ptr(ws), nbytes,
                            _stream(dev)), "star_decode")
+    return Y
+
+
+def star_decode_gated(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                      W_gates: Sequence[torch.Tensor], b_gates, W_ups: Sequence[torch.Tensor], b_ups,
+                      W_downs: Sequence[torch.Tensor], b_downs, residual: bool = True, Y=None,
+                      out_dtype=None, ws=None):
+    """One decode step through ``len(W_ups)`` gated-FFN (SwiGLU) layers; returns Y."""
+    M = X.shape[0]
+    dev = X.device
+    L = len(W_ups)
+    if Y is None:
+        Y = torch.empty((M, up.K), dtype=out_dtype or X.dtype, device=dev)
+    P = ctypes.c_void_p
+    arr = lambda ts: (P * L)(*[t.data_ptr() for t in ts])
+    opt = lambda ts: (P * L)(*[t.data_ptr() if t is not None else None for t in ts]) if ts is not None else None
+    ws, nbytes = _ws("decode", up, down, M, dev, ws)
+    _check(LIB.star_decode_gated(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), arr(W_gates), opt(b_gates),
+                                 arr(W_ups), opt(b_ups), arr(W_downs), opt(b_downs), int(bool(residual)),
+                                 _ptr(Y), _dt(Y), _ptr(ws), nbytes, _stream(dev)), "star_decode_gated")
     return Y
 
 

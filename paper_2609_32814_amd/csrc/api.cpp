@@ -198,7 +198,7 @@ struct StackPlan {
   int ns = 1, kc = 0, nt_up = 0, nt_dn = 0, grid = 0;
   size_t H = 0, hb = 0, h = 0, part = 0, cnt = 0, end = 0;
 };
-StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers) {
+StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool gated = false) {
   StackPlan sp;
   const int64_t D = u.K(), F = u.N();
   for (int g = 0; g < u.q; ++g) sp.nt_up += static_cast<int>(tiles_of(u.r(g), kDecodeTileN));
@@ -224,7 +224,7 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers) {
   for (int g = 0; same_groups && g <= u.q; ++g) same_groups = d.S[g] == u.R[g] && d.R[g] == u.S[g];
   sp.ok = M >= 1 && M <= kDecodeMaxRows && n_layers <= kStackMaxLayers && same_groups &&
           decode_stack_smem(static_cast<int>(M), static_cast<int>(std::max<int64_t>(D, sp.kc)), static_cast<int>(D),
-                            sp.ns) > 0 &&
+                            sp.ns, gated) > 0 &&
           sp.grid <= cu_count();
   return sp;
 }
@@ -674,12 +674,18 @@ star_status star_ffn_fwd(const star_algebra* up, const star_algebra* down, int64
   return run_fwd(d, M, perm, offs, H, W_down, elem, b_down, STAR_ACT_NONE, nullptr, Y, yt, stream);
 }
 
-star_status star_decode(const star_algebra* up, const star_algebra* down, int32_t n_layers,
-                        int64_t M, const int32_t* row_type, const void* X,
-                        const void* const* W_up, const float* const* b_up,
+}  // extern "C"
+
+namespace {
+// The decode step behind star_decode and star_decode_gated (W_gate non-null:
+// gated FFN, persistent stack only).
+star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_t n_layers, int64_t M,
+                        const int32_t* row_type, const void* X, const void* const* W_gate,
+                        const float* const* b_gate, const void* const* W_up, const float* const* b_up,
                         const void* const* W_down, const float* const* b_down, star_act act,
                         int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
+  const bool gated = W_gate != nullptr;
   Alg u, d;
   star_status st = check_common(up, M, row_type, u);
   if (st != STAR_OK) return st;
@@ -694,17 +700,20 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
   if (!X || !W_up || !W_down || !Y) return STAR_ERR_ARG;
   if (!aligned16(X) || !aligned16(Y)) return STAR_ERR_ALIGN;
   for (int l = 0; l < n_layers; ++l) {
-    if (!W_up[l] || !W_down[l]) return STAR_ERR_ARG;
-    if (!aligned16(W_up[l]) || !aligned16(W_down[l])) return STAR_ERR_ALIGN;
-    if ((b_up && b_up[l] && !aligned16(b_up[l])) || (b_down && b_down[l] && !aligned16(b_down[l])))
+    if (!W_up[l] || !W_down[l] || (gated && !W_gate[l])) return STAR_ERR_ARG;
+    if (!aligned16(W_up[l]) || !aligned16(W_down[l]) || (gated && !aligned16(W_gate[l]))) return STAR_ERR_ALIGN;
+    if ((b_up && b_up[l] && !aligned16(b_up[l])) || (b_down && b_down[l] && !aligned16(b_down[l])) ||
+        (gated && b_gate && b_gate[l] && !aligned16(b_gate[l])))
       return STAR_ERR_ALIGN;
   }
   const DecodeWs dw = decode_layout(u, M);
-  const StackPlan sp = stack_plan(u, d, M, n_layers);
+  const StackPlan sp = stack_plan(u, d, M, n_layers, gated);
   if (!ws || ws_bytes < std::max(dw.end, sp.end)) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  // the gated FFN runs only in the persistent stack
+  if (gated && !sp.ok) return STAR_ERR_UNSUPPORTED;
 
-  if (sp.ok && use_decode_stack()) {
+  if (sp.ok && (gated || use_decode_stack())) {
     DecodeStack k;
     std::memset(&k, 0, sizeof(k));
     k.q = u.q;
@@ -733,7 +742,12 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
       k.Wd[l] = static_cast<const uint16_t*>(W_down[l]);
       k.bu[l] = b_up ? b_up[l] : nullptr;
       k.bd[l] = b_down ? b_down[l] : nullptr;
+      if (gated) {
+        k.Wg[l] = static_cast<const uint16_t*>(W_gate[l]);
+        k.bg[l] = b_gate ? b_gate[l] : nullptr;
+      }
     }
+    k.gated = gated ? 1 : 0;
     k.Y = Y;
     k.H = at<uint16_t>(ws, sp.H);
     k.hb = at<uint16_t>(ws, sp.hb);
@@ -791,6 +805,32 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
     if (st != STAR_OK) return st;
   }
   return STAR_OK;
+}
+}  // namespace
+
+extern "C" {
+
+star_status star_decode(const star_algebra* up, const star_algebra* down, int32_t n_layers,
+                        int64_t M, const int32_t* row_type, const void* X,
+                        const void* const* W_up, const float* const* b_up,
+                        const void* const* W_down, const float* const* b_down, star_act act,
+                        int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  return decode_impl(up, down, n_layers, M, row_type, X, nullptr, nullptr, W_up, b_up, W_down, b_down,
+                     act, residual, Y, yt, ws, ws_bytes, stream);
+}
+
+star_status star_decode_gated(const star_algebra* up, const star_algebra* down, int32_t n_layers,
+                              int64_t M, const int32_t* row_type, const void* X,
+                              const void* const* W_gate, const float* const* b_gate,
+                              const void* const* W_up, const float* const* b_up,
+                              const void* const* W_down, const float* const* b_down,
+                              int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (M > 0 && !W_gate) return STAR_ERR_ARG;
+  static const void* const no_layers[1] = {nullptr};
+  return decode_impl(up, down, n_layers, M, row_type, X, W_gate ? W_gate : no_layers, b_gate, W_up, b_up,
+                     W_down, b_down, STAR_ACT_NONE, residual, Y, yt, ws, ws_bytes, stream);
 }
 
 star_status star_validate_types(int64_t M, const int32_t* row_type, int32_t q, int64_t* n_bad,

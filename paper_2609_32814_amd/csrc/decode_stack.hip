@@ -164,10 +164,14 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   // staging writes whole 1 KB copies, so round the x buffer up to 1 KB
   const int xbytes = max((M * kmax * 2 + 1023) & ~1023, kRedBytes);
   char* xbuf = lds;
-  char* slot_base[2] = {lds + xbytes, lds + xbytes + (kmax / SLICE) * 1024};
+  // slots: 0 up weights, 1 down weights, 2 (gated FFN) gate weights; the
+  // gate item is the up item, so slot 2 shares slot 0's slice plan
+  const int nslots = p.gated ? 3 : 2;
+  char* slot_base[3] = {lds + xbytes, lds + xbytes + (kmax / SLICE) * 1024,
+                        lds + xbytes + 2 * (kmax / SLICE) * 1024};
   // RES: the running state [M][D] fp32, then the staging of the down
   // chunks, res_rows rows at a time (chunk c at stg + c * cstride bytes)
-  float* hres = reinterpret_cast<float*>(lds + xbytes + 2 * (kmax / SLICE) * 1024);
+  float* hres = reinterpret_cast<float*>(lds + xbytes + nslots * (kmax / SLICE) * 1024);
   char* stg = reinterpret_cast<char*>(hres) + ((M * p.D * 4 + 1023) & ~1023);
   const int cstride = (p.res_rows * p.D * 4 + 1023) & ~1023;
   int32_t* err = p.cnt;
@@ -348,12 +352,13 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   // A wave's slices are wave, wave + 4, ...; RB of them have their LDS reads
   // in flight together.
   constexpr int RB = MB == 1 ? 8 : (MB == 2 ? 4 : 2);
-  auto compute = [&](int slot, const Item& it, f32x4_t (&acc)[MB]) {
+  // (slot: the slice plan; data_slot: where the weights are)
+  auto compute = [&](int slot, int data_slot, const Item& it, f32x4_t (&acc)[MB]) {
     const int G = lane >> 4;
     const int pl = lane & 15;
     const int kx = (it.k_hi - it.k_lo + 127) & ~127;
     const int ns_ = nslices_s[slot];
-    const char* sb = slot_base[slot];
+    const char* sb = slot_base[data_slot];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int t0 = 0; wave + 4 * t0 < ns_; t0 += RB) {
@@ -424,6 +429,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   if (iu.valid) copy_offsets(0, iu, p.F, off_u);
   if (idn.valid) copy_offsets(1, idn, p.D, off_d);
   if (iu.valid) copy(0, p.Wu[0], off_u);
+  if (iu.valid && p.gated) copy(2, p.Wg[0], off_u);
   if (idn.valid) copy(1, p.Wd[0], off_d);
   if (RES) {
     for (int e = tid; e < M * p.D; e += kThreads) hres[e] = bf16_to_f32(p.X[e]);
@@ -444,8 +450,11 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
         wait_vm_all();
         __syncthreads();
       }
-      f32x4_t acc[MB], z;
-      compute(0, iu, acc);
+      // both products first: the cross-wave sums reuse the x buffer
+      f32x4_t acc[MB], accg[MB], z, zg = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if (p.gated) compute(0, 2, iu, accg);
+      compute(0, 0, iu, acc);
+      if (p.gated) reduce(accg, zg);
       reduce(acc, z);
       const int32_t n = iu.n0 + my_dn;
       if (my_m < M && n < iu.nend) {
@@ -455,11 +464,23 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
           const float4 bv = *reinterpret_cast<const float4*>(b + n);
           v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
         }
+        if (p.gated) {
+          // gated FFN: H = silu(x W_gate + b_gate) . (x W_up + b_up)
+          float g[4] = {zg[0], zg[1], zg[2], zg[3]};
+          const float* bgl = p.bg[l];
+          if (bgl) {
+            const float4 bv = *reinterpret_cast<const float4*>(bgl + n);
+            g[0] += bv.x; g[1] += bv.y; g[2] += bv.z; g[3] += bv.w;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] *= g[e] / (1.0f + __expf(-g[e]));
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = act_fwd(p.act, v[e]);
+        }
         uint32_t* dst = reinterpret_cast<uint32_t*>(p.H + static_cast<int64_t>(my_m) * p.F + n);
-        st_agent(dst, f32_to_bf16(act_fwd(p.act, v[0])) |
-                          (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, v[1]))) << 16));
-        st_agent(dst + 1, f32_to_bf16(act_fwd(p.act, v[2])) |
-                              (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, v[3]))) << 16));
+        st_agent(dst, f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16));
+        st_agent(dst + 1, f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16));
       }
       wait_vm_all();  // the stores have reached the coherent level
       __syncthreads();
@@ -467,6 +488,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       // slot 0 is free (every wave passed the barriers above): the next
       // layer's up weights stream in while this workgroup waits
       if (!last) copy(0, p.Wu[l + 1], off_u);
+      if (!last && p.gated) copy(2, p.Wg[l + 1], off_u);
     }
 
     // ---------------- down projection: h += H W_down + b_down ----------------
@@ -477,7 +499,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       wait_vm_all();
       __syncthreads();
       f32x4_t acc[MB], z;
-      compute(1, idn, acc);
+      compute(1, 1, idn, acc);
       reduce(acc, z);
       const int32_t n = idn.n0 + my_dn;
       const bool mine = my_m < M && n < idn.nend;
@@ -558,29 +580,30 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
 constexpr int kResidentMaxRows = 2;
 constexpr size_t kStackLdsCap = 150 * 1024;
 
-static size_t stack_lds_base(int M, int kmax) {
+// slots: up and down weights, plus the gate weights of a gated FFN
+static size_t stack_lds_base(int M, int kmax, bool gated) {
   kmax = (kmax + 127) & ~127;
   const size_t xbytes = std::max<size_t>((static_cast<size_t>(M) * kmax * 2 + 1023) & ~size_t(1023), kRedBytes);
-  return xbytes + 2 * static_cast<size_t>(kmax / SLICE) * 1024;
+  return xbytes + (gated ? 3 : 2) * static_cast<size_t>(kmax / SLICE) * 1024;
 }
-static size_t stack_lds_res(int M, int kmax, int D, int ns, int rows) {
+static size_t stack_lds_res(int M, int kmax, int D, int ns, int rows, bool gated) {
   const size_t state = (static_cast<size_t>(M) * D * 4 + 1023) & ~size_t(1023);
   const size_t cstride = (static_cast<size_t>(rows) * D * 4 + 1023) & ~size_t(1023);
-  return stack_lds_base(M, kmax) + state + static_cast<size_t>(ns) * cstride;
+  return stack_lds_base(M, kmax, gated) + state + static_cast<size_t>(ns) * cstride;
 }
 // Rows of down chunks staged per round in a RES kernel (0: not resident).
-static int stack_res_rows(int M, int kmax, int D, int ns) {
+static int stack_res_rows(int M, int kmax, int D, int ns, bool gated) {
   if (M > kResidentMaxRows) return 0;
   int rows = 0;
   for (int r = 1; r <= M; ++r)
-    if (stack_lds_res(M, kmax, D, ns, r) <= kStackLdsCap) rows = r;
+    if (stack_lds_res(M, kmax, D, ns, r, gated) <= kStackLdsCap) rows = r;
   return rows;
 }
 
-size_t decode_stack_smem(int M, int kmax, int D, int ns) {
+size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated) {
   if (M < 1 || M > kDecodeMaxRows || kmax < SLICE || kmax > kMaxSlices * SLICE) return 0;
-  const int rows = stack_res_rows(M, kmax, D, ns);
-  const size_t total = rows > 0 ? stack_lds_res(M, kmax, D, ns, rows) : stack_lds_base(M, kmax);
+  const int rows = stack_res_rows(M, kmax, D, ns, gated);
+  const size_t total = rows > 0 ? stack_lds_res(M, kmax, D, ns, rows, gated) : stack_lds_base(M, kmax, gated);
   return total <= kStackLdsCap ? total : 0;
 }
 
@@ -591,7 +614,7 @@ static hipError_t launch_stack(const DecodeStack& p, int grid, size_t smem, hipS
       kStackLdsCap);
   if (attr != hipSuccess) return attr;
   DecodeStack arg = p;
-  arg.res_rows = RES ? stack_res_rows(p.M, std::max(p.D, p.kc), p.D, p.ns) : 0;
+  arg.res_rows = RES ? stack_res_rows(p.M, std::max(p.D, p.kc), p.D, p.ns, p.gated != 0) : 0;
   void* args[] = {&arg};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), dim3(grid),
                                     dim3(kThreads), args, static_cast<unsigned>(smem), stream);
@@ -599,9 +622,9 @@ static hipError_t launch_stack(const DecodeStack& p, int grid, size_t smem, hipS
 
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream) {
   const int kmax = std::max(p.D, p.kc);
-  const size_t smem = decode_stack_smem(p.M, kmax, p.D, p.ns);
+  const size_t smem = decode_stack_smem(p.M, kmax, p.D, p.ns, p.gated != 0);
   if (smem == 0) return hipErrorInvalidValue;
-  if (stack_res_rows(p.M, kmax, p.D, p.ns) > 0) return launch_stack<1, true>(p, grid, smem, stream);
+  if (stack_res_rows(p.M, kmax, p.D, p.ns, p.gated != 0) > 0) return launch_stack<1, true>(p, grid, smem, stream);
   switch ((p.M + 15) / 16) {
     case 1: return launch_stack<1, false>(p, grid, smem, stream);
     case 2: return launch_stack<2, false>(p, grid, smem, stream);

@@ -135,6 +135,9 @@ struct DecodeStack {
   const uint16_t* Wd[kStackMaxLayers];
   const float* bu[kStackMaxLayers];
   const float* bd[kStackMaxLayers];
+  int32_t gated;                      // gated FFN: H = silu(x W_gate + b_gate) . (x W_up + b_up)
+  const uint16_t* Wg[kStackMaxLayers];
+  const float* bg[kStackMaxLayers];
   void* Y;
   uint16_t* H;    // [M][F] bf16, the current layer's hidden activation
   uint16_t* hb;   // [2][M][D] bf16, the next up projection's input (layer parity)
@@ -150,7 +153,7 @@ inline int64_t decode_stack_counters(int nt_dn) {
   return static_cast<int64_t>(kCounterStride) * (1 + 2 * kSubCounters + nt_dn);
 }
 // Dynamic LDS bytes the stack kernel needs, or 0 when the shape does not fit.
-size_t decode_stack_smem(int M, int kmax, int D, int ns);
+size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated);
 // Launches the stack kernel cooperatively on grid = max(nt_up, nt_dn * ns)
 // workgroups (all resident at once); p.cnt must be zero.
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);

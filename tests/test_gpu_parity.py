@@ -786,3 +786,49 @@ def test_swiglu_ffn_train_step_parity(P, q, law, bias):
     ref = oracle.swiglu_ffn_bwd(up_o, dn_o, t, X.exact, rZg, rZu, rH, Wg.exact, Wu.exact, Wd.exact, dY.exact)
     for k in ("dZ_gate", "dZ_up", "dX", "dW_gate", "db_gate", "dW_up", "db_up", "dW_down", "db_down"):
         assert rel_fro(to_host(g[k]), ref[k]) <= TOL_BF16, k
+
+
+@pytest.mark.parametrize("law,q,D,F,L,M", [
+    ("star", 2, 256, 1024, 3, 1), ("star", 2, 256, 1024, 3, 8), ("star", 2, 256, 1024, 3, 40),
+    ("tensor2", 4, 256, 1024, 3, 1), ("tensor2", 4, 256, 1024, 3, 33), ("dense", 2, 256, 1024, 2, 8),
+    ("tensor2", 4, 768, 1536, 12, 1), ("tensor2", 4, 768, 1536, 12, 48),   # the pilot's FFN
+])
+def test_decode_gated_parity(P, law, q, D, F, L, M):
+    import torch
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q, law)
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q, law)
+    seed = 990 + M + L
+    W = {k: [synth.gaussian(seed, off + l, shp, 0.02, "bf16") for l in range(L)]
+         for k, off, shp in (("g", 10, (D, F)), ("u", 40, (D, F)), ("d", 70, (F, D)))}
+    b = {k: [synth.gaussian(seed, off + l, (n,), 0.02, "f32") for l in range(L)]
+         for k, off, n in (("g", 100, F), ("u", 130, F), ("d", 160, D))}
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    pos = synth.decode_positions(seed, M)
+    t = (((pos % 768) // 192) if law == "tensor2" else (pos % q)).astype(np.int32)
+    dev = lambda k: [to_dev(w) for w in W[k]]
+    devb = lambda k: [f32_dev(x.exact) for x in b[k]]
+    Y = P.star_decode_gated(up_g, dn_g, types_dev(t), to_dev(X), dev("g"), devb("g"), dev("u"), devb("u"),
+                            dev("d"), devb("d"), True, out_dtype=torch.float32)
+    ex = lambda k: [w.exact for w in W[k]]
+    exb = lambda k: [x.exact for x in b[k]]
+    ref = oracle.decode_stack_gated(up_o, dn_o, t, X.exact, ex("g"), exb("g"), ex("u"), exb("u"), ex("d"),
+                                    exb("d"))
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+    Y2 = P.star_decode_gated(up_g, dn_g, types_dev(t), to_dev(X), dev("g"), devb("g"), dev("u"), devb("u"),
+                             dev("d"), devb("d"), True, out_dtype=torch.float32)
+    assert torch.equal(Y, Y2)
+
+
+def test_decode_gated_refuses_what_does_not_fit(P):
+    """Three weight slots do not fit LDS at D = 768 beyond 52 rows: refused
+    before any launch, and the plain stack still takes the same shape."""
+    import torch
+    q, D, F, M = 4, 768, 1536, 64
+    up_g, _ = algs(P, q, [D // q] * q, [F // q] * q, "tensor2")
+    dn_g, _ = algs(P, q, [F // q] * q, [D // q] * q, "tensor2")
+    w = lambda shp: torch.zeros(shp, dtype=torch.bfloat16, device="cuda")
+    X = w((M, D))
+    t = types_dev(np.zeros(M, np.int32))
+    with pytest.raises(RuntimeError, match="unsupported|not supported"):
+        P.star_decode_gated(up_g, dn_g, t, X, [w((D, F))], None, [w((D, F))], None, [w((F, D))], None)
+    P.star_decode(up_g, dn_g, t, X, [w((D, F))], None, [w((F, D))], None, "gelu")

@@ -609,3 +609,25 @@ def test_swiglu_ffn_is_its_formula_and_gradients_match_fd():
             Mn[a_, b_] -= eps
             fd = (loss(**{name: P_}) - loss(**{name: Mn})) / (2 * eps)
             assert abs(fd - grads[key][a_, b_]) < 1e-6 * max(1, abs(fd)), (name, a_, b_)
+
+
+def test_gated_decode_stack_is_layers_of_the_gated_ffn():
+    """Without bf16 mirroring, one layer of the gated decode stack is the
+    residual plus the gated FFN's output, and L layers compose."""
+    up, down = Alg(2, (4, 4), (6, 6)), Alg(2, (6, 6), (4, 4))
+    g = rng(43)
+    M, L = 3, 2
+    X = g.standard_normal((M, 8))
+    t = np.array([0, 1, 1], np.int32)
+    Ws = [[g.standard_normal((8, 12)) for _ in range(L)], [g.standard_normal((8, 12)) for _ in range(L)],
+          [g.standard_normal((12, 8)) for _ in range(L)]]
+    bs = [[g.standard_normal(12) for _ in range(L)], [g.standard_normal(12) for _ in range(L)],
+          [g.standard_normal(8) for _ in range(L)]]
+    h = X.copy()
+    for l in range(L):
+        _, _, _, Y = oracle.swiglu_ffn_fwd(up, down, t, h, Ws[0][l], bs[0][l], Ws[1][l], bs[1][l],
+                                           Ws[2][l], bs[2][l], mirror_bf16=False)
+        h = h + Y
+    got = oracle.decode_stack_gated(up, down, t, X, Ws[0], bs[0], Ws[1], bs[1], Ws[2], bs[2],
+                                    mirror_bf16=False)
+    np.testing.assert_allclose(got, h, atol=1e-12)
