@@ -543,7 +543,8 @@ def bench_pilot_ffn(P, synth, torch, np, dev, T, args):
     td = torch.from_numpy(t).to(dev)
     rows = np.bincount(t, minlength=q)
     res = {"workload": "bias-free SwiGLU FFN 768 -> 2 x 1536 -> 768, Q_2 (x) Q_2, M=16384, bf16, "
-                       "row type = floor((p mod 768) / 192); forward + backward"}
+                       "row type = floor((p mod 768) / 192); forward + backward; and its 12-layer "
+                       "decode stack at M in {1, 48}"}
     for law in ("tensor2", "dense"):
         u, d = up.with_law(law), dn.with_law(law)
         plan = P.star_type_plan(q, td)
@@ -568,6 +569,37 @@ def bench_pilot_ffn(P, synth, torch, np, dev, T, args):
         res[law] = {"step_ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 2),
                     "gflop": round(fl / 1e9, 2)}
     res["speedup"] = round(res["dense"]["step_ms"] / res["tensor2"]["step_ms"], 3)
+    del X, Wg, Wu, Wd, dY
+    torch.cuda.empty_cache()
+
+    # the pilot's 12-layer gated decode stack (weights 12 x 3 x 768 x 1536 bf16 = 84.9 MB)
+    L = 12
+    Wgs = [to_dev_bf16(synth.gaussian(8, 10 + l, (D, F), 0.02, "bf16"), torch, dev) for l in range(L)]
+    Wus = [to_dev_bf16(synth.gaussian(8, 40 + l, (D, F), 0.02, "bf16"), torch, dev) for l in range(L)]
+    Wds = [to_dev_bf16(synth.gaussian(8, 70 + l, (F, D), 0.02, "bf16"), torch, dev) for l in range(L)]
+    dec = {}
+    for Md in (1, 48):
+        Xd = to_dev_bf16(synth.gaussian(8, 200 + Md, (Md, D), 1.0, "bf16"), torch, dev)
+        tdd = torch.from_numpy(((synth.decode_positions(8, Md) % 768) // 192).astype(np.int32)).to(dev)
+        Yd = torch.empty((Md, D), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(P.star_workspace_bytes("decode", up, dn, Md), dtype=torch.uint8, device=dev)
+        one = {}
+        for law in ("tensor2", "dense"):
+            u, d = up.with_law(law), dn.with_law(law)
+            for _ in range(args.warmup):
+                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws)
+            torch.cuda.synchronize()
+            n = max(20, args.steps)
+            e0, e1 = T.ev(), T.ev()
+            e0.record()
+            for _ in range(n):
+                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / n * 1e3
+            one[law] = {"step_us_warm": round(us, 1), "tokens_per_s": round(Md / (us * 1e-6), 1)}
+        dec[f"M{Md}"] = one
+    res["decode"] = dec
     log("pilot_ffn:", json.dumps(res))
     return res
 
