@@ -832,3 +832,25 @@ def test_decode_gated_refuses_what_does_not_fit(P):
     with pytest.raises(RuntimeError, match="unsupported|not supported"):
         P.star_decode_gated(up_g, dn_g, t, X, [w((D, F))], None, [w((D, F))], None, [w((F, D))], None)
     P.star_decode(up_g, dn_g, t, X, [w((D, F))], None, [w((F, D))], None, "gelu")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_max_q_narrow_groups(P, dtype):
+    """q = 64 (the largest the ABI takes) with 8-wide groups: every tile spans
+    many groups' worth of classes; forward, activation and weight gradients."""
+    import torch
+    q, w, M = 64, 8, 1000
+    ga, oa = algs(P, q, [w] * q, [w] * q)
+    X = synth.gaussian(77, 0, (M, q * w), 1.0, dtype)
+    W = synth.gaussian(77, 1, (q * w, q * w), 0.1, dtype)
+    dY = synth.gaussian(77, 2, (M, q * w), 1.0, dtype)
+    t = np.random.default_rng([77, 3]).integers(0, q, M).astype(np.int32)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), out_dtype=torch.float32)
+    ref, _, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact)
+    assert rel_fro(to_host(Y), ref) <= bar(dtype)
+    dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W), out_dtype=torch.float32)
+    assert rel_fro(to_host(dX), oracle.proj_bwd_data(oa, t, dY.exact, W.exact)) <= bar(dtype)
+    dW, db = P.star_proj_bwd_weight(ga, types_dev(t), to_dev(X), to_dev(dY))
+    rW, rb = oracle.proj_bwd_weight(oa, t, X.exact, dY.exact)
+    assert rel_fro(to_host(dW), rW) <= bar(dtype)
+    assert rel_fro(to_host(db), rb) <= bar(dtype)
