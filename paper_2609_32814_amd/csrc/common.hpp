@@ -1,6 +1,8 @@
 // Device-side helpers shared by the gfx950 kernels of libstarq.
 #pragma once
 
+#include <atomic>
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -79,6 +81,20 @@ __device__ __forceinline__ void store_out(void* base, int dtype, int64_t idx, fl
 __device__ __forceinline__ float load_in(const void* base, int dtype, int64_t idx) {
   if (dtype == 0) return static_cast<const float*>(base)[idx];
   return bf16_to_f32(static_cast<const uint16_t*>(base)[idx]);
+}
+
+
+// Raises a kernel's dynamic-LDS limit to `bytes` once per device: the
+// attribute belongs to the function on the current device, so `done`
+// (one per kernel) records the devices already set.
+inline hipError_t ensure_lds_limit(const void* fn, std::atomic<unsigned long long>& done, int bytes) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+  const unsigned long long bit = dev < 64 ? (1ull << dev) : 0ull;
+  if (bit && (done.load(std::memory_order_relaxed) & bit)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_relaxed);
+  return e;
 }
 
 }  // namespace starq

@@ -237,9 +237,9 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
 size_t decode_phase_smem() { return (kDecodeMaxK / SLICE) * 1024 + kRedBytes; }
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(decode_phase_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-      static_cast<int>(decode_phase_smem()));
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(decode_phase_kernel), lds_set,
+                                           static_cast<int>(decode_phase_smem()));
   if (attr != hipSuccess) return attr;
   const int nt = p.NTp[p.q];
   const int grid = (nt + 31) / 32 * 32;

@@ -609,9 +609,9 @@ size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated) {
 
 template <int MB, bool RES>
 static hipError_t launch_stack(const DecodeStack& p, int grid, size_t smem, hipStream_t stream) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), hipFuncAttributeMaxDynamicSharedMemorySize,
-      kStackLdsCap);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr =
+      ensure_lds_limit(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), lds_set, kStackLdsCap);
   if (attr != hipSuccess) return attr;
   DecodeStack arg = p;
   arg.res_rows = RES ? stack_res_rows(p.M, std::max(p.D, p.kc), p.D, p.ns, p.gated != 0) : 0;

@@ -553,17 +553,14 @@ hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
   using G = Geo<WN>;
   auto kern = p.law == 1 ? star_gemm_kernel<T, MODE, 1, WN>
                          : (p.law == 2 ? star_gemm_kernel<T, MODE, 2, WN> : star_gemm_kernel<T, MODE, 0, WN>);
-  // allow more than the default dynamic LDS once per kernel (idempotent)
-  static const hipError_t attr = [] {
-    hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 0, WN>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
-    if (a == hipSuccess)
-      a = hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
-    if (a != hipSuccess) return a;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 2, WN>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
-  }();
+  // allow more than the default dynamic LDS (once per kernel and device)
+  static std::atomic<unsigned long long> lds_set[3] = {{0}, {0}, {0}};
+  hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 0, WN>), lds_set[0],
+                                     G::SMEM);
+  if (attr == hipSuccess)
+    attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>), lds_set[1], G::SMEM);
+  if (attr == hipSuccess)
+    attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 2, WN>), lds_set[2], G::SMEM);
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(THREADS), G::SMEM, stream, p);
   return hipGetLastError();

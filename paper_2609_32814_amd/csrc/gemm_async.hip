@@ -656,8 +656,8 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
 template <int MODE, int LAW, int ACT>
 hipError_t launch_one(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
   auto kern = star_gemm_async_kernel<MODE, LAW, ACT>;
-  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(kern), lds_set, SMEM);
   if (attr != hipSuccess) return attr;
   // persistent grid: one workgroup per CU, a multiple of 8 so that every
   // XCD gets the same number
