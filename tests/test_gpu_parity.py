@@ -854,3 +854,33 @@ def test_max_q_narrow_groups(P, dtype):
     rW, rb = oracle.proj_bwd_weight(oa, t, X.exact, dY.exact)
     assert rel_fro(to_host(dW), rW) <= bar(dtype)
     assert rel_fro(to_host(db), rb) <= bar(dtype)
+
+
+@pytest.mark.parametrize("case", ["many_layers", "other_groups"])
+def test_decode_per_projection_path(P, case):
+    """Shapes the persistent stack does not take run one launch per projection:
+    more layers than the stack holds (33), or a down projection whose output
+    groups differ from the up projection's input groups."""
+    import torch
+    if case == "many_layers":
+        q, L, M = 2, 33, 5
+        up_g, up_o = algs(P, q, [64, 64], [128, 128])
+        dn_g, dn_o = algs(P, q, [128, 128], [64, 64])
+    else:
+        q, L, M = 2, 3, 9
+        up_g, up_o = algs(P, q, [64, 64], [128, 128])
+        dn_g, dn_o = algs(P, q, [128, 128], [40, 88])
+    D, F = up_o.K, up_o.N
+    seed = 1100 + L
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.05, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 100 + l, (F, D), 0.05, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 200 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 300 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = (synth.decode_positions(seed, M) % q).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                      [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                      [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
