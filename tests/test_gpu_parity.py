@@ -884,3 +884,41 @@ def test_decode_per_projection_path(P, case):
     ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
                               [w.exact for w in Wd], [b.exact for b in bd])
     assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tanh_gelu_paths(P, dtype):
+    """The tanh form of GELU in the forward epilogue, in the activation
+    gradient's fused derivative and in the decode stack."""
+    import torch
+    q = 2
+    ga, oa = algs(P, q, [192, 192], [384, 384])
+    M = 700
+    seed = 1200
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, dtype)
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, dtype)
+    b = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
+    t = np.random.default_rng([seed, 3]).integers(0, q, M).astype(np.int32)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(b.exact), "gelu_tanh",
+                        out_dtype=torch.float32)
+    ref, _, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, b.exact, "gelu_tanh")
+    assert rel_fro(to_host(Y), ref) <= bar(dtype)
+    dY = synth.gaussian(seed, 4, (M, oa.N), 1.0, dtype)
+    Zp = synth.gaussian(seed, 5, (M, oa.K), 1.0, dtype)
+    dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W), Z_prev=to_dev(Zp),
+                              act_prev="gelu_tanh", out_dtype=torch.float32)
+    refd = oracle.proj_bwd_data(oa, t, dY.exact, W.exact, Zprev=Zp.exact, act_prev="gelu_tanh")
+    assert rel_fro(to_host(dX), refd) <= bar(dtype)
+    if dtype == "bf16":
+        up_g, up_o = algs(P, q, [64, 64], [256, 256])
+        dn_g, dn_o = algs(P, q, [256, 256], [64, 64])
+        L, Md = 2, 3
+        Wu = [synth.gaussian(seed, 10 + l, (128, 512), 0.05, "bf16") for l in range(L)]
+        Wd = [synth.gaussian(seed, 20 + l, (512, 128), 0.05, "bf16") for l in range(L)]
+        Xd = synth.gaussian(seed, 30, (Md, 128), 1.0, "bf16")
+        td = np.array([0, 1, 1], np.int32)
+        Yd = P.star_decode(up_g, dn_g, types_dev(td), to_dev(Xd), [to_dev(w) for w in Wu], None,
+                           [to_dev(w) for w in Wd], None, "gelu_tanh", True, out_dtype=torch.float32)
+        refdd = oracle.decode_stack(up_o, dn_o, td, Xd.exact, [w.exact for w in Wu], [None] * L,
+                                    [w.exact for w in Wd], [None] * L, act="gelu_tanh")
+        assert rel_fro(to_host(Yd), refdd) <= TOL_BF16
