@@ -8,10 +8,10 @@
 // 16 contiguous chunks, one per wavefront; a wavefront walks its chunk in
 // windows of 64 rows.  Lanes holding the same type find each other with
 // ballots over the type bits (a match-any), so each window costs O(log q)
-// ballots and no atomics.  Pass 1 counts rows per (wavefront, type); the
-// counts are scanned into exclusive bases; pass 2 re-walks the chunks and
-// writes each row at base + rank-within-window, which keeps the order of
-// rows of one type (stable).  Rows with a type outside [0, q) go to a
+// ballots and no atomics.  Pass 1 counts rows per (wavefront, type); one
+// wavefront scans the counts into exclusive bases with lane shuffles; pass 2
+// re-walks the chunks and writes each row at base + rank-within-window,
+// which keeps the order of rows of one type (stable).  Rows with a type outside [0, q) go to a
 // trailing bucket after all valid rows, so perm stays a permutation and no
 // tile ever reads them.
 #include "common.hpp"
@@ -87,16 +87,28 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
   }
   __syncthreads();
 
-  // exclusive scan: offsets over types, then bases per (wave, type)
-  if (threadIdx.x == 0) {
-    int32_t run = 0;
-    for (int t = 0; t <= q; ++t) {
-      offsets[t] = run;  // offsets[q]: end of the valid rows
-      for (int w = 0; w < kPlanWaves; ++w) {
-        const int32_t c = counts[w][t];
-        counts[w][t] = run;
-        run += c;
+  // exclusive scan of the counts in (type, wavefront) order, by wavefront 0
+  // with lane shuffles, 64 entries a round: the bases per (wavefront, type),
+  // and per type the offset (offsets[q]: end of the valid rows)
+  if (wave == 0) {
+    const int n = (q + 1) * kPlanWaves;
+    int32_t carry = 0;
+    for (int base = 0; base < n; base += 64) {
+      const int e = base + lane;
+      const int t = e / kPlanWaves, w = e % kPlanWaves;
+      const int32_t c = e < n ? counts[w][t] : 0;
+      int32_t incl = c;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int32_t u = __shfl_up(incl, d);
+        if (lane >= d) incl += u;
       }
+      if (e < n) {
+        const int32_t excl = carry + incl - c;
+        counts[w][t] = excl;
+        if (w == 0) offsets[t] = excl;
+      }
+      carry += __shfl(incl, 63);
     }
   }
   __syncthreads();
