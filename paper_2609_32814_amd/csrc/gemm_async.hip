@@ -103,6 +103,12 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// whether rows wm * 128 .. wm * 128 + 127 of a tile with `nrows` rows hold
+// any row (uniform over the wave)
+__device__ __forceinline__ bool wave_rows_live(int wm, int32_t nrows) {
+  return __builtin_amdgcn_readfirstlane(wm * (BM / 2) < nrows ? 1 : 0) != 0;
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
       static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p)));
@@ -127,9 +133,12 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 template <int MODE, int LAW, int ACT>
 __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const GemmParams p) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  __shared__ int32_t units_s[kMaxQGroups];
+  // row tiles per class: [0] BM rows, [1] BM / 2 rows (weight gradient:
+  // row tiles x splits, both)
+  __shared__ int32_t units_s[2][kMaxQGroups];
   __shared__ int32_t offs_s[kMaxQGroups + 1];
-  __shared__ int32_t pfx_s[2][kMaxQGroups + 1];
+  // tile prefix sums per class: pass 0, pass 1, pass 1 in half-height tiles
+  __shared__ int32_t pfx_s[3][kMaxQGroups + 1];
   __shared__ __attribute__((aligned(16))) int32_t rows_s[kRowBufs][BM];
   __shared__ __attribute__((aligned(16))) float bias_s[kRowBufs][BN];
   // weight gradient: rows (perm entries) of the positions a stage contracts
@@ -148,22 +157,41 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   for (int i = threadIdx.x; i <= q; i += kThreads) offs_s[i] = p.offsets[i];
   __syncthreads();
   for (int i = threadIdx.x; i < q; i += kThreads) {
-    if constexpr (MODE == kModeBwdWeight)
-      units_s[i] = (p.MTp[i + 1] - p.MTp[i]) * p.nsplit;  // row tiles of K group i x splits
-    else
-      units_s[i] = (offs_s[i + 1] - offs_s[i] + BM - 1) / BM;  // row tiles of type class i
+    if constexpr (MODE == kModeBwdWeight) {
+      units_s[0][i] = units_s[1][i] = (p.MTp[i + 1] - p.MTp[i]) * p.nsplit;  // row tiles of K group i x splits
+    } else {
+      // row tiles of type class i
+      units_s[0][i] = (offs_s[i + 1] - offs_s[i] + BM - 1) / BM;
+      units_s[1][i] = (offs_s[i + 1] - offs_s[i] + BM / 2 - 1) / (BM / 2);
+    }
   }
   __syncthreads();
-  if (threadIdx.x < 2) {
-    const int sel = sel_for(MODE, LAW, threadIdx.x);
+  if (threadIdx.x < 3) {
+    const int ps = threadIdx.x == 0 ? 0 : 1;
+    const int sel = sel_for(MODE, LAW, ps);
     int32_t run = 0;
     for (int i = 0; i < q; ++i) {
       pfx_s[threadIdx.x][i] = run;
-      run += units_s[i] * ncols_sel(p, sel, i);
+      run += units_s[threadIdx.x == 2 ? 1 : 0][i] * ncols_sel(p, sel, i);
     }
     pfx_s[threadIdx.x][q] = run;
   }
   __syncthreads();
+  // Half-height tiles for pass 1 (star law) when whole tiles would deal out
+  // unevenly: pass 0 fills at most one round of the grid, the two passes do
+  // not fit in one, and so many pass-1 tiles remain that some workgroups get
+  // a pass-0 and a pass-1 tile while the mean load is at least half a pass-1
+  // tile below that (counted with equal groups, where a pass-0 tile has twice
+  // the K steps of a pass-1 tile).  Half-height pass-1 tiles are dealt to the
+  // workgroups without a pass-0 tile first; in such a tile the waves of the
+  // empty half skip their MFMAs and epilogue.
+  const int32_t n0 = pfx_s[0][q], n1 = pfx_s[1][q], ng = static_cast<int32_t>(gridDim.x);
+  const int32_t whole_max = n1 > 2 * (ng - n0) ? 3 : 2;  // in pass-1 tiles
+  const bool half1 =
+      MODE != kModeBwdWeight && LAW == 0 &&
+      __builtin_amdgcn_readfirstlane(n1 > 0 && n0 <= ng && n0 + n1 > ng &&
+                                     2 * (whole_max * ng - 2 * n0 - n1) >= ng) != 0;
+  const int p1 = half1 ? 2 : 1;  // the prefix sums pass 1 uses
 
   // ---- tile iterators (the compute side and the load side walk one list) ----
   // XCD x (workgroups w with w % 8 == x) owns a contiguous chunk of each
@@ -174,7 +202,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   int32_t pbase[2], pcount[2];
 #pragma unroll
   for (int ps = 0; ps < 2; ++ps) {
-    const int32_t total = pfx_s[ps][q];
+    const int32_t total = pfx_s[ps == 0 ? 0 : p1][q];
     const int32_t chunk = (total + 7) >> 3;
     pbase[ps] = xcd * chunk;
     pcount[ps] = max(0, min(total - xcd * chunk, chunk));
@@ -187,16 +215,22 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     int32_t r;  // this workgroup's round
   };
   const int xslot = blockIdx.x >> 3;
+  // With half-height pass-1 tiles, every round after the first runs in
+  // reverse place order, so the half tiles go first to the workgroups that
+  // had no pass-0 tile (the high places of round 0).
   auto advance = [&](Iter& it, Tile& t) -> bool {
-    const int32_t v = it.r * slot_stride + ((it.r & 1) ? slot_stride - 1 - xslot : xslot);
+    const bool rev = half1 ? it.r > 0 : (it.r & 1) != 0;
+    const int32_t v = it.r * slot_stride + (rev ? slot_stride - 1 - xslot : xslot);
     if (v >= pcount[0] + pcount[1]) return false;
     ++it.r;
     const int ps = v < pcount[0] ? 0 : 1;
     const int32_t logical = pbase[ps] + (ps == 0 ? v : v - pcount[0]);
+    const int32_t* pf = pfx_s[ps == 0 ? 0 : p1];
     int cls = 0;
-    while (logical >= pfx_s[ps][cls + 1]) ++cls;
-    t = make_tile<MODE, LAW, BN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pfx_s[ps][cls],
-                                     units_s[cls], offs_s);
+    while (logical >= pf[cls + 1]) ++cls;
+    const bool hh = ps == 1 && half1;
+    t = make_tile<MODE, LAW, BN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pf[cls],
+                                     units_s[hh ? 1 : 0][cls], offs_s, hh ? BM / 2 : BM);
     return true;
   };
 
@@ -517,16 +551,21 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     {
       const char* As = smem + slot * STAGE_BYTES;
       const char* Bs = As + A_BYTES;
+      // a wave whose 128 rows are all past the tile's rows (half-height
+      // tiles) skips the MFMAs
+      const bool wact = MODE == kModeBwdWeight || wave_rows_live(wm, ct.nrows);
       uint4 fa[2][4], fb[2][2];
       read_frags(As, Bs, 0, fa[0], fb[0]);
 #pragma unroll
       for (int rs = 0; rs < 4; ++rs) {
         if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
         stage_copy(rs);  // the next stage's copies ride along with the MFMAs
+        if (wact) {
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+          for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-          for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
+            for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
+        }
       }
     }
     stage_end();
@@ -550,7 +589,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
                   make_float4(acc[mi][ni][4 * a], acc[mi][ni][4 * a + 1], acc[mi][ni][4 * a + 2],
                               acc[mi][ni][4 * a + 3]);
       }
-    } else
+    } else if (wave_rows_live(wm, ct.nrows))
     // The arithmetic runs over all 128 accumulators of the lane without
     // control flow (so independent values interleave); only the memory
     // accesses are predicated on the row and column being inside the tile.

@@ -260,10 +260,11 @@ struct Tile {
 };
 
 // `offs` holds the q + 1 type offsets of the plan (global memory or an LDS
-// copy).
+// copy).  Forward and activation gradient: row tiles are `bm` rows (BM, or
+// BM / 2 for the half-height tiles that balance a short last round).
 template <int MODE, int LAW, int BN, int BK>
 __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls, int32_t u,
-                                          int32_t units, const int32_t* offs) {
+                                          int32_t units, const int32_t* offs, int bm = BM) {
   Tile t;
   // Forward and activation gradient: column tiles vary fastest, so that the
   // tiles of one XCD chunk cover a few row tiles across all their column
@@ -348,8 +349,8 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.do_dbias = (p.dbias != nullptr) && (cg == cls) && (t.mt == 0);
   }
   if constexpr (MODE != kModeBwdWeight) {
-    t.pos0 = offs[cls] + t.mt * BM;
-    t.nrows = min(BM, offs[cls + 1] - t.pos0);
+    t.pos0 = offs[cls] + t.mt * bm;
+    t.nrows = min(bm, offs[cls + 1] - t.pos0);
   }
   t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
   t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;

@@ -259,6 +259,46 @@ def test_bwd_data_parity(P, law, dtype, q, s, r, M, fused):
     assert rel_fro(to_host(dX), ref) <= bar(dtype)
 
 
+@pytest.mark.parametrize("law", ["star", "tensor2"])
+@pytest.mark.parametrize("mode", ["fwd", "bwd_data"])
+def test_half_height_last_round(P, law, mode):
+    """Shapes whose first pass of tiles fits in one round of the persistent
+    grid (256 workgroups) while whole tiles would deal out unevenly: with the
+    star law the second pass then runs in half-height tiles (128 of 256 rows;
+    the waves of the empty half skip their MFMAs and epilogue) dealt to the
+    workgroups without a first-pass tile first.  Every output against the
+    oracle; the type counts are not multiples of 128, so the last half tile
+    of each class is ragged.  (fwd: 2 x 13 row tiles x 8 column tiles per
+    pass; activation gradient: 2 x 24 row tiles x 4 column tiles per pass.
+    The tensor-square law runs the same shapes in whole tiles.)"""
+    import torch
+    q = 2 if law == "star" else 4
+    if mode == "fwd":
+        s, r, M = [256 // q] * q, [4096 // q] * q, 6181
+    else:
+        s, r, M = [2048 // q] * q, [256 // q] * q, 12037
+    ga, oa = algs(P, q, s, r, law)
+    seed = 400 + q
+    t = synth.cyclic_types(M, q)
+    if mode == "fwd":
+        X = synth.gaussian(seed, 0, (M, oa.K), 1.0, "bf16")
+        W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, "bf16")
+        bias = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
+        Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
+                               Z_out=True)
+        refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, bias.exact, "gelu", want_z=True)
+        assert rel_fro(to_host(Z), refZ) <= TOL_BF16
+        assert rel_fro(to_host(Y), refY) <= TOL_BF16
+    else:
+        dY = synth.gaussian(seed, 0, (M, oa.N), 1.0, "bf16")
+        W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, "bf16")
+        Zp = synth.gaussian(seed, 2, (M, oa.K), 1.0, "bf16")
+        dX = P.star_proj_bwd_data(ga, types_dev(t), to_dev(dY), to_dev(W), Z_prev=to_dev(Zp),
+                                  act_prev="gelu", out_dtype=torch.float32)
+        ref = oracle.proj_bwd_data(oa, t, dY.exact, W.exact, Zprev=Zp.exact, act_prev="gelu")
+        assert rel_fro(to_host(dX), ref) <= TOL_BF16
+
+
 @pytest.mark.parametrize("law", ["star", "dense"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("q,s,r,M", [
