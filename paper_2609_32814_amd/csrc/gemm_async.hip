@@ -6,8 +6,9 @@
 // group), computed by one workgroup of 8 wavefronts (2 x 4, 128 x 64 each,
 // swapped-operand v_mfma_f32_32x32x16_bf16 so a lane ends with 4 consecutive
 // output columns).  Two passes of tiles (two-segment contractions first),
-// dealt out per XCD as one list; the epilogue follows the register-staged
-// kernel.  Weight gradient: C = X^T dY over the type-sorted positions of the
+// dealt out per XCD as one list (the second pass in tiles of 128 rows when
+// whole tiles would leave the load uneven); the epilogue follows the
+// register-staged kernel.  Weight gradient: C = X^T dY over the type-sorted positions of the
 // rows whose support pairs the tile's groups, rows read in place through
 // perm (the rows of each stage's 64 positions are copied into LDS one stage
 // ahead), split along the positions into deterministic partials.
