@@ -196,7 +196,8 @@ DecodeWs decode_layout(const Alg& up, int64_t M) {
 struct StackPlan {
   bool ok = false;
   int ns = 1, kc = 0, nt_up = 0, nt_dn = 0, grid = 0;
-  size_t H = 0, hb = 0, h = 0, part = 0, cnt = 0, end = 0;
+  size_t H = 0, hb = 0, h = 0, part = 0, tH = 0, tpart = 0, cnt = 0, end = 0;
+  bool resident = false;
 };
 StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool gated = false) {
   StackPlan sp;
@@ -217,6 +218,18 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool g
   cur = align_up(cur + sizeof(float) * M * D);
   sp.part = cur;
   cur = align_up(cur + sizeof(float) * sp.ns * M * D);
+  // tagged hand-off words right before the counters: one fill clears both
+  const int kmax = static_cast<int>(std::max<int64_t>(D, sp.kc));
+  sp.resident = M >= 1 && M <= kDecodeMaxRows &&
+                decode_stack_resident(static_cast<int>(M), kmax, static_cast<int>(D), sp.ns, gated, sp.nt_up,
+                                      sp.nt_dn);
+  sp.tH = cur;
+  sp.tpart = cur;
+  if (sp.resident) {
+    cur = align_up(cur + sizeof(uint64_t) * M * (F / 2));
+    sp.tpart = cur;
+    cur = align_up(cur + sizeof(uint64_t) * 2 * sp.ns * M * D);
+  }
   sp.cnt = cur;
   cur = align_up(cur + sizeof(int32_t) * decode_stack_counters(sp.nt_dn));
   sp.end = cur;
@@ -754,7 +767,10 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
     k.h = at<float>(ws, sp.h);
     k.part = at<float>(ws, sp.part);
     k.cnt = at<int32_t>(ws, sp.cnt);
-    st = hip_status(launch_fill_zero(reinterpret_cast<float*>(k.cnt), decode_stack_counters(sp.nt_dn), stream));
+    k.tH = sp.resident ? at<uint64_t>(ws, sp.tH) : nullptr;
+    k.tpart = sp.resident ? at<uint64_t>(ws, sp.tpart) : nullptr;
+    st = hip_status(launch_fill_zero(at<float>(ws, sp.tH),
+                                     static_cast<int64_t>((sp.end - sp.tH) / sizeof(float)), stream));
     if (st != STAR_OK) return st;
     return hip_status(launch_decode_stack(k, sp.grid, stream));
   }

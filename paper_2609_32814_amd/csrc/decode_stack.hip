@@ -17,7 +17,7 @@
 // layer-to-layer dependencies instead of starting at each kernel boundary.
 //
 // Cross-workgroup data (H, the next layer's input, the residual, the
-// partial sums) is written with agent-coherent stores and read with
+// partial sums) is otherwise written with agent-coherent stores and read with
 // agent-coherent loads (copies into LDS with sc1), so no cache
 // write-back or invalidate is needed; arrival counters are agent-scope
 // atomics that only grow (a layer's target is a multiple of the item
@@ -30,14 +30,21 @@
 //
 // Summing the down chunks, in chunk order either way, so results do not
 // depend on timing: for a few rows (RES kernels) every workgroup keeps the
-// running state h in LDS and, once all chunks of a layer have arrived,
-// sums them itself into its copy of h and into the next up input (two
-// hand-offs per layer); for more rows the chunks of one tile are summed by
-// whichever of its workgroups arrives last, which writes h and the next
-// input for everyone (three hand-offs).  The last layer always sums by last
-// arrival, to write Y.  Every wait is bounded: after about half a second of
-// spinning the kernel raises the error flag and carries on, so it always
-// terminates.
+// running state h in LDS and, in the next layer, sums the chunks itself
+// into its copy of h and into the next up input; for more rows the chunks
+// of one tile are summed by whichever of its workgroups arrives last, which
+// writes h and the next input for everyone (three hand-offs per layer).
+//
+// RES kernels hand H and the down chunks over as tagged 64-bit words (the
+// data and the writing layer plus one, stored and loaded whole): a reader
+// polls the words it needs until they carry the layer it waits for, so
+// the wait and the data read are one load, and a writer neither waits for
+// its stores to land nor bumps a counter.  The down chunks alternate
+// between two buffers by layer parity; every workgroup owns a down item
+// and reads all chunks of a layer before it writes its own of the next, so
+// no chunk is overwritten before every workgroup has read it.  Every wait
+// is bounded: after about half a second of spinning the kernel raises the
+// error flag and carries on, so it always terminates.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -85,6 +92,30 @@ __device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
 }
 __device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Tagged hand-off words: the data in the low half, the writing layer plus
+// one in the high half, stored and loaded whole (single-copy atomic), so a
+// reader that sees the tag it waits for has the data with it.
+__device__ __forceinline__ void st_tagged(uint64_t* p, uint32_t v, uint32_t tag) {
+  __hip_atomic_store(p, (static_cast<uint64_t>(tag) << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_tagged(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// The data of word w (loaded from src), reloading until it carries tag;
+// after about half a second it raises the error flag and gives up.
+__device__ __forceinline__ uint32_t settle(const uint64_t* src, uint64_t w, uint32_t tag, int32_t* err) {
+  int spins = 0;
+  while (static_cast<uint32_t>(w >> 32) != tag) {
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > kSpinLimit) {
+      st_agent(reinterpret_cast<uint32_t*>(err), 1u);
+      break;
+    }
+    w = ld_tagged(src);
+  }
+  return static_cast<uint32_t>(w);
 }
 
 // k in B(i, j): law 0 {i, j}; law 1 every group; law 2 (tensor power of
@@ -295,56 +326,96 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   // RES, layer l >= 1: h_l = sum of the down chunks of layer l - 1 (chunk
   // order) + bias (+ h_{l-1}), kept in hres and written as the swizzled bf16
   // up input (K = D, padded to a multiple of 128 with zeros).  The chunks
-  // come in by agent-coherent copies into the staging area, res_rows rows
-  // at a time; each thread then takes pairs of columns.
+  // are tagged words (tag l, buffer (l - 1) & 1), polled in place: the wait
+  // for the other workgroups and the read of their data are one load.  Each
+  // thread takes four consecutive columns of one row.
   auto stage_resident = [&](int l) {
+    __syncthreads();  // every wave is done with the x buffer
     const int kx = (p.D + 127) & ~127;
-    const int half = kx / 2;
+    const int quads = kx / 4;
     const float* b = p.bd[l - 1];
-    for (int m0 = 0; m0 < M; m0 += p.res_rows) {
-      const int rows = min(p.res_rows, M - m0);
-      const int bytes = rows * p.D * 4;
-      const int nblk = (bytes + 1023) >> 10;
-      for (int c = 0; c < p.ns; ++c) {
-        const char* src = reinterpret_cast<const char*>(p.part + (static_cast<int64_t>(c) * M + m0) * p.D);
-        for (int blk = wave; blk < nblk; blk += 4) {
-          const int o = blk * 1024 + lane * 16;
-          const void* g = o < bytes ? static_cast<const void*>(src + o) : zero;
-          dma16_sys(g, lds_addr(stg + c * cstride + blk * 1024));
+    const uint32_t tag = static_cast<uint32_t>(l);
+    const uint64_t* tp = p.tpart + static_cast<int64_t>((l - 1) & 1) * p.ns * M * p.D;
+    for (int e = tid; e < M * quads; e += kThreads) {
+      const int m = e / quads;
+      const int k = 4 * (e - m * quads);
+      uint2 packed = make_uint2(0u, 0u);
+      if (k < p.D) {
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int c0 = 0; c0 < p.ns; c0 += 4) {
+          uint64_t w[4][4];
+          const uint64_t* src[4];
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const int c = min(c0 + cc, p.ns - 1);
+            src[cc] = tp + (static_cast<int64_t>(c) * M + m) * p.D + k;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) w[cc][x] = ld_tagged(src[cc] + x);
+          }
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            if (c0 + cc < p.ns) {
+#pragma unroll
+              for (int x = 0; x < 4; ++x) v[x] += __uint_as_float(settle(src[cc] + x, w[cc][x], tag, err));
+            }
+          }
         }
-      }
-      wait_vm_all();
-      __syncthreads();
-      for (int e = tid; e < rows * half; e += kThreads) {
-        const int mm = e / half;
-        const int m = m0 + mm;
-        const int k = 2 * (e - mm * half);
-        uint32_t packed = 0;
-        if (k < p.D) {
-          float v0 = 0.f, v1 = 0.f;
-          for (int c = 0; c < p.ns; ++c) {
-            const float2 w = *reinterpret_cast<const float2*>(stg + c * cstride + (mm * p.D + k) * 4);
-            v0 += w.x;
-            v1 += w.y;
-          }
-          if (b) {
-            v0 += b[k];
-            v1 += b[k + 1];
-          }
-          float* hr = hres + m * p.D + k;
-          if (p.residual) {
-            v0 += hr[0];
-            v1 += hr[1];
-          }
-          hr[0] = v0;
-          hr[1] = v1;
-          packed = f32_to_bf16(v0) | (static_cast<uint32_t>(f32_to_bf16(v1)) << 16);
+        if (b) {
+          const float4 bv = *reinterpret_cast<const float4*>(b + k);
+          v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
         }
-        const int c = (k >> 3) ^ (m & 15);
-        *reinterpret_cast<uint32_t*>(xbuf + (m * kx + 8 * c + (k & 7)) * 2) = packed;
+        float* hr = hres + m * p.D + k;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          if (p.residual) v[x] += hr[x];
+          hr[x] = v[x];
+        }
+        packed.x = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+        packed.y = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
       }
-      __syncthreads();  // the staging area is free for the next rows
+      const int c = (k >> 3) ^ (m & 15);
+      *reinterpret_cast<uint2*>(xbuf + (m * kx + 8 * c + (k & 7)) * 2) = packed;
     }
+    wait_vm_all();  // the weight copies issued before
+    __syncthreads();
+  };
+
+  // RES: the down item's slice of H (tagged bf16 pairs of layer l, tag
+  // l + 1) polled in place into the swizzled x buffer; inputs past k_hi are
+  // zero.
+  auto stage_h = [&](const Item& it, uint32_t tag) {
+    __syncthreads();  // every wave is done with the x buffer
+    const int kx = (it.k_hi - it.k_lo + 127) & ~127;
+    const int pairs = kx / 2;
+    const int total = M * pairs;
+    const int64_t ldh = p.F / 2;
+    for (int e0 = tid; e0 < total; e0 += 4 * kThreads) {
+      uint64_t w[4];
+      const uint64_t* src[4];
+      bool ok[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int e = e0 + r * kThreads;
+        const int m = min(e / pairs, M - 1);
+        const int k = it.k_lo + 2 * (e - (e / pairs) * pairs);
+        ok[r] = e < total && k < it.k_hi;
+        src[r] = p.tH + m * ldh + (ok[r] ? k / 2 : 0);
+        w[r] = ok[r] ? ld_tagged(src[r]) : 0ull;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int e = e0 + r * kThreads;
+        if (e < total) {
+          const int m = e / pairs;
+          const int kr = 2 * (e - m * pairs);
+          const uint32_t v = ok[r] ? settle(src[r], w[r], tag, err) : 0u;
+          const int c = (kr >> 3) ^ (m & 15);
+          *reinterpret_cast<uint32_t*>(xbuf + (m * kx + 8 * c + (kr & 7)) * 2) = v;
+        }
+      }
+    }
+    wait_vm_all();  // the weight copies issued before
+    __syncthreads();
   };
 
   // acc over the item's slices; lane group G = lane / 16 holds K rows
@@ -435,13 +506,14 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
     for (int e = tid; e < M * p.D; e += kThreads) hres[e] = bf16_to_f32(p.X[e]);
   }
 
-  const int dn_per_layer = RES ? p.nt_dn * p.ns : p.nt_dn;
   for (int l = 0; l < p.L; ++l) {
     const bool last = l + 1 == p.L;
     // ---------------- up projection: H = act(x W_up + b_up) ----------------
     if (l > 0) {
-      wait_for(cnt_dn, dn_per_layer * l);
-      if (RES) stage_resident(l);
+      if (RES)
+        stage_resident(l);
+      else
+        wait_for(cnt_dn, p.nt_dn * l);
     }
     if (iu.valid) {
       if (!RES || l == 0) {
@@ -478,13 +550,25 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = act_fwd(p.act, v[e]);
         }
-        uint32_t* dst = reinterpret_cast<uint32_t*>(p.H + static_cast<int64_t>(my_m) * p.F + n);
-        st_agent(dst, f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16));
-        st_agent(dst + 1, f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16));
+        const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+        const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+        if (RES) {
+          uint64_t* dst = p.tH + static_cast<int64_t>(my_m) * (p.F / 2) + n / 2;
+          st_tagged(dst, lo, static_cast<uint32_t>(l + 1));
+          st_tagged(dst + 1, hi, static_cast<uint32_t>(l + 1));
+        } else {
+          uint32_t* dst = reinterpret_cast<uint32_t*>(p.H + static_cast<int64_t>(my_m) * p.F + n);
+          st_agent(dst, lo);
+          st_agent(dst + 1, hi);
+        }
       }
-      wait_vm_all();  // the stores have reached the coherent level
-      __syncthreads();
-      if (tid == 0) arrive(cnt_up);
+      if (!RES) {
+        wait_vm_all();  // the stores have reached the coherent level
+        __syncthreads();
+        if (tid == 0) arrive(cnt_up);
+      } else {
+        __syncthreads();
+      }
       // slot 0 is free (every wave passed the barriers above): the next
       // layer's up weights stream in while this workgroup waits
       if (!last) copy(0, p.Wu[l + 1], off_u);
@@ -492,8 +576,49 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
     }
 
     // ---------------- down projection: h += H W_down + b_down ----------------
-    wait_for(cnt_up, p.nt_up * (l + 1));
-    if (idn.valid) {
+    if (!RES) wait_for(cnt_up, p.nt_up * (l + 1));
+    if (idn.valid && RES) {
+      const int s = blockIdx.x % p.ns;
+      stage_h(idn, static_cast<uint32_t>(l + 1));
+      f32x4_t acc[MB], z;
+      compute(1, 1, idn, acc);
+      reduce(acc, z);
+      const int32_t n = idn.n0 + my_dn;
+      const bool mine = my_m < M && n < idn.nend;
+      uint64_t* tp = p.tpart + static_cast<int64_t>(l & 1) * p.ns * M * p.D;
+      if (mine) {
+        uint64_t* dst = tp + (static_cast<int64_t>(s) * M + my_m) * p.D + n;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) st_tagged(dst + e, __float_as_uint(z[e]), static_cast<uint32_t>(l + 1));
+      }
+      if (last && s == 0 && mine) {
+        // the tile's first chunk sums all of them in chunk order once each
+        // carries this layer's tag
+        const uint32_t tag = static_cast<uint32_t>(l + 1);
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < p.ns; ++c) {
+          const uint64_t* src = tp + (static_cast<int64_t>(c) * M + my_m) * p.D + n;
+          uint64_t w[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = ld_tagged(src + e);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(settle(src + e, w[e], tag, err));
+        }
+        const float* b = p.bd[l];
+        if (b) {
+          const float4 bv = *reinterpret_cast<const float4*>(b + n);
+          v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+        }
+        const int64_t o = static_cast<int64_t>(my_m) * p.D + n;
+        if (p.residual) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += hres[o + e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) store_out(p.Y, p.ydtype, o + e, v[e]);
+      }
+      if (!last) copy(1, p.Wd[l + 1], off_d);
+    } else if (idn.valid) {
       const int ct = blockIdx.x / p.ns, s = blockIdx.x % p.ns;
       stage_x(idn, p.H, p.F);
       wait_vm_all();
@@ -510,15 +635,11 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       }
       wait_vm_all();
       __syncthreads();
-      if (RES && !last) {
-        // the next layer's up items sum the chunks
-        if (tid == 0) arrive(cnt_dn);
-      } else {
+      {
         if (tid == 0) {
           const int old =
               __hip_atomic_fetch_add(tile_cnt + kCounterStride * ct, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          // RES: the tile counters count the last layer only
-          flag_s = (old == (RES ? p.ns - 1 : p.ns * (l + 1) - 1));
+          flag_s = (old == p.ns * (l + 1) - 1);
         }
         __syncthreads();
         if (flag_s) {
@@ -538,10 +659,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
             }
             const int64_t o = static_cast<int64_t>(my_m) * p.D + n;
             if (p.residual) {
-              if (RES) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] += hres[o + e];
-              } else if (l == 0) {
+              if (l == 0) {
                 const uint2 xi = *reinterpret_cast<const uint2*>(p.X + o);
                 v[0] += bf16_to_f32(xi.x & 0xffffu); v[1] += bf16_to_f32(xi.x >> 16);
                 v[2] += bf16_to_f32(xi.y & 0xffffu); v[3] += bf16_to_f32(xi.y >> 16);
@@ -600,6 +718,15 @@ static int stack_res_rows(int M, int kmax, int D, int ns, bool gated) {
   return rows;
 }
 
+// Resident hand-offs keep a down partial buffer per layer parity; a writer
+// of layer l + 2 reuses the buffer of layer l once its tile's up items are
+// done, which every workgroup's read of layer l precedes only if every
+// workgroup owns a down item (each reads all partials before it writes its
+// own).
+bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up, int nt_dn) {
+  return nt_dn * ns >= nt_up && stack_res_rows(M, kmax, D, ns, gated) > 0;
+}
+
 size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated) {
   if (M < 1 || M > kDecodeMaxRows || kmax < SLICE || kmax > kMaxSlices * SLICE) return 0;
   const int rows = stack_res_rows(M, kmax, D, ns, gated);
@@ -624,7 +751,10 @@ hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t strea
   const int kmax = std::max(p.D, p.kc);
   const size_t smem = decode_stack_smem(p.M, kmax, p.D, p.ns, p.gated != 0);
   if (smem == 0) return hipErrorInvalidValue;
-  if (stack_res_rows(p.M, kmax, p.D, p.ns, p.gated != 0) > 0) return launch_stack<1, true>(p, grid, smem, stream);
+  if (decode_stack_resident(p.M, kmax, p.D, p.ns, p.gated != 0, p.nt_up, p.nt_dn)) {
+    if (!p.tH || !p.tpart) return hipErrorInvalidValue;
+    return launch_stack<1, true>(p, grid, smem, stream);
+  }
   switch ((p.M + 15) / 16) {
     case 1: return launch_stack<1, false>(p, grid, smem, stream);
     case 2: return launch_stack<2, false>(p, grid, smem, stream);

@@ -145,6 +145,10 @@ struct DecodeStack {
   float* part;    // [ns][M][D] fp32 down-projection partial sums
   int32_t* cnt;   // decode_stack_counters(nt_dn) int32: error flag, up and down arrival
                   // sub-counters, per-tile down arrivals, each on its own 256-byte line
+  // resident kernels only (zero at launch): 64-bit words (tag << 32 | data),
+  // the tag being the layer that wrote the word plus one
+  uint64_t* tH;     // [M][F / 2] bf16 pairs of H
+  uint64_t* tpart;  // [2][ns][M][D] fp32 down partial sums, by layer parity
 };
 // Arrival counters: each sits alone on a 256-byte line (kCounterStride ints).
 constexpr int kCounterStride = 64;
@@ -154,6 +158,9 @@ inline int64_t decode_stack_counters(int nt_dn) {
 }
 // Dynamic LDS bytes the stack kernel needs, or 0 when the shape does not fit.
 size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated);
+// Whether the stack keeps the running state in every workgroup's LDS and hands
+// data over as tagged words (then tH and tpart must be set and zero).
+bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up, int nt_dn);
 // Launches the stack kernel cooperatively on grid = max(nt_up, nt_dn * ns)
 // workgroups (all resident at once); p.cnt must be zero.
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);
