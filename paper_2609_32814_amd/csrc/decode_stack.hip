@@ -200,11 +200,8 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   const int nslots = p.gated ? 3 : 2;
   char* slot_base[3] = {lds + xbytes, lds + xbytes + (kmax / SLICE) * 1024,
                         lds + xbytes + 2 * (kmax / SLICE) * 1024};
-  // RES: the running state [M][D] fp32, then the staging of the down
-  // chunks, res_rows rows at a time (chunk c at stg + c * cstride bytes)
+  // RES: the running state [M][D] fp32
   float* hres = reinterpret_cast<float*>(lds + xbytes + nslots * (kmax / SLICE) * 1024);
-  char* stg = reinterpret_cast<char*>(hres) + ((M * p.D * 4 + 1023) & ~1023);
-  const int cstride = (p.res_rows * p.D * 4 + 1023) & ~1023;
   int32_t* err = p.cnt;
   int32_t* cnt_up = p.cnt + kCounterStride;
   int32_t* cnt_dn = cnt_up + kCounterStride * kSubCounters;
@@ -696,6 +693,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
 
 // Rows per step up to which the running state stays in LDS (RES kernels).
 constexpr int kResidentMaxRows = 2;
+static_assert(kResidentMaxRows <= 16, "resident kernels cover one 16-row block");
 constexpr size_t kStackLdsCap = 150 * 1024;
 
 // slots: up and down weights, plus the gate weights of a gated FFN
@@ -704,33 +702,23 @@ static size_t stack_lds_base(int M, int kmax, bool gated) {
   const size_t xbytes = std::max<size_t>((static_cast<size_t>(M) * kmax * 2 + 1023) & ~size_t(1023), kRedBytes);
   return xbytes + (gated ? 3 : 2) * static_cast<size_t>(kmax / SLICE) * 1024;
 }
-static size_t stack_lds_res(int M, int kmax, int D, int ns, int rows, bool gated) {
+static size_t stack_lds_res(int M, int kmax, int D, bool gated) {
   const size_t state = (static_cast<size_t>(M) * D * 4 + 1023) & ~size_t(1023);
-  const size_t cstride = (static_cast<size_t>(rows) * D * 4 + 1023) & ~size_t(1023);
-  return stack_lds_base(M, kmax, gated) + state + static_cast<size_t>(ns) * cstride;
+  return stack_lds_base(M, kmax, gated) + state;
 }
-// Rows of down chunks staged per round in a RES kernel (0: not resident).
-static int stack_res_rows(int M, int kmax, int D, int ns, bool gated) {
-  if (M > kResidentMaxRows) return 0;
-  int rows = 0;
-  for (int r = 1; r <= M; ++r)
-    if (stack_lds_res(M, kmax, D, ns, r, gated) <= kStackLdsCap) rows = r;
-  return rows;
-}
-
 // Resident hand-offs keep a down partial buffer per layer parity; a writer
 // of layer l + 2 reuses the buffer of layer l once its tile's up items are
 // done, which every workgroup's read of layer l precedes only if every
 // workgroup owns a down item (each reads all partials before it writes its
 // own).
 bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up, int nt_dn) {
-  return nt_dn * ns >= nt_up && stack_res_rows(M, kmax, D, ns, gated) > 0;
+  return M <= kResidentMaxRows && nt_dn * ns >= nt_up && stack_lds_res(M, kmax, D, gated) <= kStackLdsCap;
 }
 
 size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated) {
   if (M < 1 || M > kDecodeMaxRows || kmax < SLICE || kmax > kMaxSlices * SLICE) return 0;
-  const int rows = stack_res_rows(M, kmax, D, ns, gated);
-  const size_t total = rows > 0 ? stack_lds_res(M, kmax, D, ns, rows, gated) : stack_lds_base(M, kmax, gated);
+  const size_t res = stack_lds_res(M, kmax, D, gated);
+  const size_t total = M <= kResidentMaxRows && res <= kStackLdsCap ? res : stack_lds_base(M, kmax, gated);
   return total <= kStackLdsCap ? total : 0;
 }
 
@@ -741,10 +729,15 @@ static hipError_t launch_stack(const DecodeStack& p, int grid, size_t smem, hipS
       ensure_lds_limit(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), lds_set, kStackLdsCap);
   if (attr != hipSuccess) return attr;
   DecodeStack arg = p;
-  arg.res_rows = RES ? stack_res_rows(p.M, std::max(p.D, p.kc), p.D, p.ns, p.gated != 0) : 0;
   void* args[] = {&arg};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), dim3(grid),
-                                    dim3(kThreads), args, static_cast<unsigned>(smem), stream);
+  // An ordinary launch: the grid is at most one workgroup per CU and a
+  // workgroup fits on any CU, so on a device that is not held by other work
+  // every workgroup is resident at once.  (A cooperative launch, which
+  // guarantees that, added about 18 us to every step.)  Should other work hold
+  // CUs longer than a wait's bound, the waits time out and the kernel raises
+  // its error flag instead of hanging.
+  return hipLaunchKernel(reinterpret_cast<const void*>(decode_stack_kernel<MB, RES>), dim3(grid), dim3(kThreads),
+                         args, static_cast<unsigned>(smem), stream);
 }
 
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream) {

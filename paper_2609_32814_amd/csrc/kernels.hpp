@@ -123,7 +123,6 @@ constexpr int kStackMaxLayers = 32;
 struct DecodeStack {
   int32_t q, law, M, D, F, L, act, residual, ydtype;
   int32_t ns, kc;         // down projection: K split into ns chunks of kc
-  int32_t res_rows;       // set by the launcher: rows of down chunks staged per round
   int32_t nt_up, nt_dn;   // 16-column tiles of F and of D
   int32_t SD[kMaxQGroups + 1];   // D groups: up input, down output
   int32_t SF[kMaxQGroups + 1];   // F groups: up output, down input
@@ -161,8 +160,9 @@ size_t decode_stack_smem(int M, int kmax, int D, int ns, bool gated);
 // Whether the stack keeps the running state in every workgroup's LDS and hands
 // data over as tagged words (then tH and tpart must be set and zero).
 bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up, int nt_dn);
-// Launches the stack kernel cooperatively on grid = max(nt_up, nt_dn * ns)
-// workgroups (all resident at once); p.cnt must be zero.
+// Launches the stack kernel on grid = max(nt_up, nt_dn * ns) <= CU count
+// workgroups, which must all be resident at once (an ordinary launch on a
+// device not held by other work); p.cnt must be zero.
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
