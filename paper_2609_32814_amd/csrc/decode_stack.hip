@@ -103,19 +103,29 @@ __device__ __forceinline__ void st_tagged(uint64_t* p, uint32_t v, uint32_t tag)
 __device__ __forceinline__ uint64_t ld_tagged(const uint64_t* p) {
   return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// The data of word w (loaded from src), reloading until it carries tag;
-// after about half a second it raises the error flag and gives up.
-__device__ __forceinline__ uint32_t settle(const uint64_t* src, uint64_t w, uint32_t tag, int32_t* err) {
+// Settles n words at once: reloads every word that does not yet carry tag,
+// all together, until none is left, so the wait ends one round trip after
+// the last word lands however many of them came late.  Slots with
+// src[i] == nullptr are ignored.  After about half a second it raises the error flag
+// and gives up.
+template <int N>
+__device__ __forceinline__ void settle_all(const uint64_t* const (&src)[N], uint64_t (&w)[N], uint32_t tag,
+                                           int32_t* err) {
   int spins = 0;
-  while (static_cast<uint32_t>(w >> 32) != tag) {
+  while (true) {
+    bool done = true;
+#pragma unroll
+    for (int i = 0; i < N; ++i) done &= src[i] == nullptr || static_cast<uint32_t>(w[i] >> 32) == tag;
+    if (done) break;
     __builtin_amdgcn_s_sleep(1);
     if (++spins > kSpinLimit) {
       st_agent(reinterpret_cast<uint32_t*>(err), 1u);
       break;
     }
-    w = ld_tagged(src);
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (src[i] != nullptr && static_cast<uint32_t>(w[i] >> 32) != tag) w[i] = ld_tagged(src[i]);
   }
-  return static_cast<uint32_t>(w);
 }
 
 // k in B(i, j): law 0 {i, j}; law 1 every group; law 2 (tensor power of
@@ -340,20 +350,23 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       if (k < p.D) {
         float v[4] = {0.f, 0.f, 0.f, 0.f};
         for (int c0 = 0; c0 < p.ns; c0 += 4) {
-          uint64_t w[4][4];
-          const uint64_t* src[4];
+          uint64_t w[16];
+          const uint64_t* src[16];
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            const int c = min(c0 + cc, p.ns - 1);
-            src[cc] = tp + (static_cast<int64_t>(c) * M + m) * p.D + k;
+            const uint64_t* base = tp + (static_cast<int64_t>(c0 + cc) * M + m) * p.D + k;
 #pragma unroll
-            for (int x = 0; x < 4; ++x) w[cc][x] = ld_tagged(src[cc] + x);
+            for (int x = 0; x < 4; ++x) {
+              src[4 * cc + x] = c0 + cc < p.ns ? base + x : nullptr;
+              w[4 * cc + x] = c0 + cc < p.ns ? ld_tagged(base + x) : 0ull;
+            }
           }
+          settle_all(src, w, tag, err);
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
             if (c0 + cc < p.ns) {
 #pragma unroll
-              for (int x = 0; x < 4; ++x) v[x] += __uint_as_float(settle(src[cc] + x, w[cc][x], tag, err));
+              for (int x = 0; x < 4; ++x) v[x] += __uint_as_float(static_cast<uint32_t>(w[4 * cc + x]));
             }
           }
         }
@@ -396,16 +409,17 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
         const int m = min(e / pairs, M - 1);
         const int k = it.k_lo + 2 * (e - (e / pairs) * pairs);
         ok[r] = e < total && k < it.k_hi;
-        src[r] = p.tH + m * ldh + (ok[r] ? k / 2 : 0);
+        src[r] = ok[r] ? p.tH + m * ldh + k / 2 : nullptr;
         w[r] = ok[r] ? ld_tagged(src[r]) : 0ull;
       }
+      settle_all(src, w, tag, err);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int e = e0 + r * kThreads;
         if (e < total) {
           const int m = e / pairs;
           const int kr = 2 * (e - m * pairs);
-          const uint32_t v = ok[r] ? settle(src[r], w[r], tag, err) : 0u;
+          const uint32_t v = ok[r] ? static_cast<uint32_t>(w[r]) : 0u;
           const int c = (kr >> 3) ^ (m & 15);
           *reinterpret_cast<uint32_t*>(xbuf + (m * kx + 8 * c + (kr & 7)) * 2) = v;
         }
@@ -593,13 +607,26 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
         // carries this layer's tag
         const uint32_t tag = static_cast<uint32_t>(l + 1);
         float v[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < p.ns; ++c) {
-          const uint64_t* src = tp + (static_cast<int64_t>(c) * M + my_m) * p.D + n;
-          uint64_t w[4];
+        for (int c0 = 0; c0 < p.ns; c0 += 4) {
+          uint64_t w[16];
+          const uint64_t* src[16];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w[e] = ld_tagged(src + e);
+          for (int cc = 0; cc < 4; ++cc) {
+            const uint64_t* base = tp + (static_cast<int64_t>(c0 + cc) * M + my_m) * p.D + n;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(settle(src + e, w[e], tag, err));
+            for (int e = 0; e < 4; ++e) {
+              src[4 * cc + e] = c0 + cc < p.ns ? base + e : nullptr;
+              w[4 * cc + e] = c0 + cc < p.ns ? ld_tagged(base + e) : 0ull;
+            }
+          }
+          settle_all(src, w, tag, err);
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            if (c0 + cc < p.ns) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(static_cast<uint32_t>(w[4 * cc + e]));
+            }
+          }
         }
         const float* b = p.bd[l];
         if (b) {
