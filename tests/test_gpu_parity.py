@@ -371,7 +371,7 @@ def test_ffn_train_step_parity(P, q, D, F, M):
 
 # ---- decode -------------------------------------------------------------------------
 
-@pytest.mark.parametrize("M", [1, 8, 12, 20, 32, 64])
+@pytest.mark.parametrize("M", [1, 2, 8, 12, 20, 32, 64])
 @pytest.mark.parametrize("D,F,L", [(256, 1024, 1), (256, 1024, 3), (768, 3072, 12)])
 def test_decode_parity(P, M, D, F, L):
     import torch
@@ -395,6 +395,39 @@ def test_decode_parity(P, M, D, F, L):
                        [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
                        [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
     assert torch.equal(Y, Y2)
+
+
+@pytest.mark.parametrize("M", [1, 2])
+def test_decode_few_rows_more_up_tiles_than_down_items(P, M):
+    """D = 24 + 24, F = 200 + 200: 26 up tiles of 16 columns but only 4 down
+    tiles x 4 chunks of 128, so some workgroups own no down item and the
+    stack must not keep the running state resident (its double-buffered
+    partials rely on every workgroup reading them before writing its own);
+    it runs the counter hand-offs instead, and must match the oracle over
+    several layers and give the same bits twice."""
+    import torch
+    sD, sF = [24, 24], [200, 200]
+    up_g, up_o = algs(P, 2, sD, sF)
+    dn_g, dn_o = algs(P, 2, sF, sD)
+    D, F, L = sum(sD), sum(sF), 4
+    seed = 900 + M
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.05, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.05, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 70 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 100 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = (np.arange(M) % 2).astype(np.int32)
+
+    def run():
+        return P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                             [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                             [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32)
+
+    Y = run()
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+    assert torch.equal(Y, run())
 
 
 def test_decode_one_type_only_skips_blocks(P):
