@@ -180,9 +180,10 @@ __device__ __forceinline__ Item down_item(const DecodeStack& p) {
 }
 
 // MB: 16-row blocks of the step (M <= 16 MB).  RES: the running state h is
-// kept in every workgroup's LDS (small M only) and the next layer's up
-// items sum the down chunks themselves, so a layer needs two hand-offs
-// instead of three; the last layer still sums by last arrival to write Y.
+// kept in every workgroup's LDS (small M only), H and the down chunks travel
+// as tagged words, and the next layer's up items sum the chunks themselves,
+// so a layer needs two hand-offs instead of three; in the last layer each
+// down tile's first chunk sums the tile's chunks to write Y.
 template <int MB, bool RES>
 __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStack p) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
