@@ -197,6 +197,11 @@ star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64
  *             (bf16 [D, F], bf16 [F, D], float[F] or NULL, float[D] or NULL)
  *   Y         device [M, D] of dtype yt: the final h
  *   ws        at least star_workspace_bytes(STAR_OP_DECODE, up, down, M) bytes
+ * Where the stack fits, it runs as one persistent launch of at most one
+ * workgroup per CU whose workgroups wait on each other, so they must all be
+ * resident at once: the device must not be held by long-running work on other
+ * streams meanwhile.  If it is, a wait reaches its bound (about half a second)
+ * and the step finishes with an unspecified Y instead of hanging.
  */
 star_status star_decode(const star_algebra *up, const star_algebra *down, int32_t n_layers,
                         int64_t M, const int32_t *row_type, const void *X,
