@@ -355,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
           const uint64_t* src[16];
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            const uint64_t* base = tp + (static_cast<int64_t>(c0 + cc) * M + m) * p.D + k;
+            const uint64_t* base = tp + (static_cast<int64_t>(min(c0 + cc, p.ns - 1)) * M + m) * p.D + k;
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
               src[4 * cc + x] = c0 + cc < p.ns ? base + x : nullptr;
@@ -613,7 +613,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
           const uint64_t* src[16];
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            const uint64_t* base = tp + (static_cast<int64_t>(c0 + cc) * M + my_m) * p.D + n;
+            const uint64_t* base = tp + (static_cast<int64_t>(min(c0 + cc, p.ns - 1)) * M + my_m) * p.D + n;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               src[4 * cc + e] = c0 + cc < p.ns ? base + e : nullptr;
