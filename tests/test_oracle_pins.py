@@ -4,7 +4,8 @@ Every test here runs on the CPU.  None of them re-types the oracle's own loop:
 each compares it with a different formulation (the square display, a masked
 dense product through numpy's BLAS, a brute-force enumeration of the basis
 products, the semidirect formula, closed-form counts, invariants such as
-associativity and the adjoint identity, finite differences, libm's erf,
+associativity and the adjoint identity, finite differences, tabulated and
+series values of the normal distribution function, scipy's ndtr,
 torch's bfloat16 cast) or with hand-evaluated golden values.
 """
 
@@ -418,14 +419,114 @@ def test_unequal_row_cost_and_batch_cost():
 
 # ---- P13: activations ------------------------------------------------------------
 
-def test_gelu_against_libm():
-    zs = np.linspace(-8, 8, 161)
-    for z in zs:
-        exact = 0.5 * z * (1 + math.erf(z / math.sqrt(2)))
-        assert abs(oracle.act("gelu", z)[()] - exact) <= 1e-15 * max(1, abs(exact))
-        tanh_form = 0.5 * z * (1 + math.tanh(math.sqrt(2 / math.pi) * (z + 0.044715 * z ** 3)))
-        assert abs(oracle.act("gelu_tanh", z)[()] - tanh_form) <= 1e-15 * max(1, abs(tanh_form))
-    assert oracle.act("none", 1.25)[()] == 1.25
+def _phi_table():
+    """Tabulated values of the standard normal distribution function."""
+    out = []
+    with open(os.path.join(GOLDEN, "normal_cdf.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                x, p = line.split()
+                out.append((float(x), float(p)))
+    return out
+
+
+def _dec_phi(x, prec=60):
+    """Phi(x) = (1 + erf(x / sqrt 2)) / 2 in decimal arithmetic, erf by its
+    Maclaurin series 2/sqrt(pi) sum_n (-1)^n x^(2n+1) / (n! (2n+1)) (no libm;
+    pi by the Gauss-Legendre iteration)."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = prec
+    a, b, t, p = Decimal(1), Decimal(1) / Decimal(2).sqrt(), Decimal(1) / 4, Decimal(1)
+    for _ in range(8):
+        an = (a + b) / 2
+        b = (a * b).sqrt()
+        t -= p * (a - an) ** 2
+        a, p = an, 2 * p
+    pi = (a + b) ** 2 / (4 * t)
+    u = Decimal(repr(float(x))) / Decimal(2).sqrt()
+    term, total, n = u, u, 0
+    while True:
+        n += 1
+        term = -term * u * u / n
+        add = term / (2 * n + 1)
+        total += add
+        if abs(add) < Decimal(10) ** (-prec + 5):
+            break
+    erf = 2 / pi.sqrt() * total
+    return (1 + erf) / 2, pi
+
+
+def test_gelu_erf_form_against_tabulated_phi():
+    """GELU(z) = z Phi(z) and GELU'(z) = Phi(z) + z phi(z) at tabulated points
+    of Phi (both signs: Phi(-x) = 1 - Phi(x)); phi(z) = exp(-z^2/2)/sqrt(2 pi)."""
+    for x, P in _phi_table():
+        for z, Pz in ((x, P), (-x, 1.0 - P)):
+            assert abs(oracle.act("gelu", z)[()] - z * Pz) <= 2e-15 * max(1.0, abs(z))
+            dens = math.exp(-0.5 * z * z) / math.sqrt(2 * math.pi)
+            assert abs(oracle.act_grad("gelu", z)[()] - (Pz + z * dens)) <= 2e-15 * max(1.0, abs(z))
+    assert oracle.act("gelu", 0.0)[()] == 0.0
+    assert oracle.act_grad("gelu", 0.0)[()] == 0.5
+
+
+def test_gelu_erf_form_against_ndtr():
+    """The same functions against scipy's normal distribution function (the
+    Cephes ndtr, not libm's erf) on a dense grid and the tails.  Absolute
+    bound: in the far negative tail 1 + erf(z / sqrt 2) cancels to a few ulps
+    of 1, so the oracle is accurate to ~1e-16 absolute there, not relative."""
+    from scipy.special import ndtr
+    zs = np.concatenate([np.linspace(-12, 12, 4801), [-40.0, -20.0, 20.0, 40.0, 1e-8, -1e-8]])
+    np.testing.assert_allclose(oracle.act("gelu", zs), zs * ndtr(zs), rtol=1e-13, atol=1e-14)
+    dens = np.exp(-0.5 * zs * zs) / np.sqrt(2 * np.pi)
+    np.testing.assert_allclose(oracle.act_grad("gelu", zs), ndtr(zs) + zs * dens, rtol=1e-12, atol=1e-15)
+
+
+def test_gelu_erf_form_against_decimal_series():
+    """And against Phi evaluated in 60-digit decimal arithmetic from erf's
+    power series, on points of [-6, 6]."""
+    for z in np.linspace(-6, 6, 49):
+        phi, _ = _dec_phi(z)
+        assert abs(oracle.act("gelu", z)[()] - z * float(phi)) <= 1e-15 * max(1.0, abs(z))
+
+
+def _dec_gelu_tanh(z, prec=50):
+    """Tanh-form GELU 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))) and its
+    derivative in decimal arithmetic: tanh(u) = (e^(2u) - 1) / (e^(2u) + 1) with
+    the decimal module's exp, and d/dz = 0.5 (1 + t) + 0.5 z (1 - t^2) u'(z),
+    u'(z) = sqrt(2/pi) (1 + 3 * 0.044715 z^2)."""
+    from decimal import Decimal, getcontext
+    _, pi = _dec_phi(0.0, prec)
+    getcontext().prec = prec
+    zd = Decimal(repr(float(z)))
+    c = (2 / pi).sqrt()
+    k = Decimal("0.044715")
+    u = c * (zd + k * zd ** 3)
+    e = (2 * u).exp()
+    t = (e - 1) / (e + 1)
+    val = zd * (1 + t) / 2
+    du = c * (1 + 3 * k * zd * zd)
+    der = (1 + t) / 2 + zd * (1 - t * t) * du / 2
+    return float(val), float(der)
+
+
+def test_gelu_tanh_form_against_decimal():
+    for z in np.concatenate([np.linspace(-8, 8, 65), [0.5, -0.5, 1.0, 2.0]]):
+        val, der = _dec_gelu_tanh(z)
+        assert abs(oracle.act("gelu_tanh", z)[()] - val) <= 2e-15 * max(1.0, abs(val))
+        assert abs(oracle.act_grad("gelu_tanh", z)[()] - der) <= 1e-14
+    # worked value: z = 1, u = sqrt(2/pi) * 1.044715 = 0.83356..., tanh(u) =
+    # 0.68238..., GELU_tanh(1) = 0.5 (1 + tanh u) = 0.84119...
+    assert abs(oracle.act("gelu_tanh", 1.0)[()] - 0.8411919906082768) < 1e-15
+
+
+def test_gelu_tanh_form_gap_to_erf_form():
+    """The tanh form differs from the exact form by at most 4.8e-4 (the
+    largest gap, 4.73e-4, sits near |z| = 2.70), and is not the same function."""
+    zs = np.linspace(-12, 12, 24001)
+    gap = np.abs(oracle.act("gelu_tanh", zs) - oracle.act("gelu", zs))
+    assert gap.max() <= 4.8e-4
+    assert gap.max() >= 4.6e-4
+    assert abs(abs(zs[gap.argmax()]) - 2.70) < 0.02
 
 
 def test_silu_against_scipy():
@@ -444,6 +545,9 @@ def test_activation_gradient_fd(kind):
 
 
 def test_bias_and_activation_applied():
+    """Z = X W + bias through an identity bank, then Y = Z Phi(Z) with Phi
+    from scipy's ndtr."""
+    from scipy.special import ndtr
     alg = Alg(2, (3, 3), (3, 3))
     g = rng(17)
     X = g.standard_normal((6, 6))
@@ -451,8 +555,7 @@ def test_bias_and_activation_applied():
     t = (np.arange(6) % 2).astype(np.int32)
     Y, Z, _, _ = oracle.proj_fwd(alg, t, X, np.eye(6), bias, "gelu", want_z=True)
     np.testing.assert_allclose(Z, X + bias, atol=1e-15)
-    erf = np.vectorize(math.erf)
-    np.testing.assert_allclose(Y, 0.5 * Z * (1 + erf(Z / math.sqrt(2))), atol=1e-15)
+    np.testing.assert_allclose(Y, Z * ndtr(Z), atol=1e-15)
 
 
 # ---- P14: bfloat16 rounding -----------------------------------------------------------
