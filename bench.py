@@ -345,7 +345,7 @@ def bench_decode(P, synth, torch, np, dev, T, flush, args):
             u, d = up.with_law(law), dn.with_law(law)
 
             def step():
-                P.star_decode(u, d, td, X, Wu, bu, Wd, bdn, "gelu", True, Y=Y, ws=ws)
+                P.star_decode(u, d, td, X, Wu, bu, Wd, bdn, "gelu", True, Y=Y, ws=ws, check=False)
 
             for _ in range(args.warmup):
                 step()
@@ -511,13 +511,13 @@ def bench_tensor2(P, synth, torch, np, dev, T, args):
         for law in ("tensor2", "dense"):
             u, d = up.with_law(law), dn.with_law(law)
             for _ in range(args.warmup):
-                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws)
+                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws, check=False)
             torch.cuda.synchronize()
             n = max(20, args.steps)
             e0, e1 = T.ev(), T.ev()
             e0.record()
             for _ in range(n):
-                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws)
+                P.star_decode(u, d, tdd, Xd, Wu, bu, Wd, bdn, "gelu", True, Y=Yd, ws=ws, check=False)
             e1.record()
             torch.cuda.synchronize()
             one[law] = {"step_us_warm": round(e0.elapsed_time(e1) / n * 1e3, 1)}
@@ -587,13 +587,13 @@ def bench_pilot_ffn(P, synth, torch, np, dev, T, args):
         for law in ("tensor2", "dense"):
             u, d = up.with_law(law), dn.with_law(law)
             for _ in range(args.warmup):
-                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws)
+                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws, check=False)
             torch.cuda.synchronize()
             n = max(20, args.steps)
             e0, e1 = T.ev(), T.ev()
             e0.record()
             for _ in range(n):
-                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws)
+                P.star_decode_gated(u, d, tdd, Xd, Wgs, None, Wus, None, Wds, None, True, Y=Yd, ws=ws, check=False)
             e1.record()
             torch.cuda.synchronize()
             us = e0.elapsed_time(e1) / n * 1e3

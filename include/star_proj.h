@@ -32,8 +32,10 @@
  *  - Group widths must be positive multiples of 8 and q at most STAR_MAX_Q.
  *    Operand, output, bias and workspace pointers must be 16-byte aligned.
  *  - Row types must lie in [0, q).  This is not checked by the compute calls
- *    (star_validate_types checks it); a row with an out-of-range type is left
- *    out of every product and its output row is not written.
+ *    (star_validate_types checks it).  In the projection and FFN calls a row
+ *    with an out-of-range type is left out of every product and its output
+ *    row is not written; in the decode calls such a row has an empty support
+ *    (see star_decode).  No other row is affected either way.
  *  - M = 0 is a no-op returning STAR_OK.  A type with no rows is legal; the
  *    weight-gradient blocks only that type reaches are written as zeros.
  *  - Operand dtypes: all-F32 or all-BF16 (BF16 operands accumulate in FP32).
@@ -72,7 +74,10 @@ typedef enum { STAR_F32 = 0, STAR_BF16 = 1 } star_dtype;
 /* Pointwise activation applied after the bias.  GELU is the erf form
  * 0.5 z (1 + erf(z / sqrt 2)); GELU_TANH the tanh approximation.  The paper
  * keeps activations at their usual definitions (Sec. 4, "Projection
- * Shapes"). */
+ * Shapes").  Every kernel evaluates them in fp32 with the same explicit
+ * approximations: values within 1e-6 + 2^-22 |value| of the exact function
+ * (the erf form through Abramowitz & Stegun 7.1.28), derivatives within 1e-6
+ * (erf form, A&S 7.1.26) or 5e-6 (tanh form). */
 typedef enum { STAR_ACT_NONE = 0, STAR_ACT_GELU = 1, STAR_ACT_GELU_TANH = 2 } star_act;
 
 /* STAR_LAW_STAR: B(i,j) = {i,j} (Sec. 5.1).  STAR_LAW_DENSE: all q^2 block
@@ -190,9 +195,13 @@ star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64
  * stored in bfloat16.  This is a skinny, weight-bandwidth-bound product: every
  * weight block that some row's support reaches is read once per step, and a
  * block no row's support reaches is not read.  D and F must be at most 4096
- * (STAR_ERR_UNSUPPORTED otherwise); M at most 64.
+ * (STAR_ERR_UNSUPPORTED otherwise); M at most 64.  A row whose type lies
+ * outside [0, q) reaches no weight block: each layer adds act(b_up) *_q
+ * nothing + b_down = b_down, so its Y row is X + the sum of the b_down[l]
+ * (without `residual`: b_down of the last layer, or zeros without biases).
  *   row_type  device int32[M]
- *   X         device bf16 [M, D]
+ *   X         device [M, D] of dtype xt, which must be STAR_BF16 (the
+ *             weights are bf16 too); STAR_ERR_DTYPE otherwise
  *   W_up, W_down, b_up, b_down: host arrays of n_layers device pointers
  *             (bf16 [D, F], bf16 [F, D], float[F] or NULL, float[D] or NULL)
  *   Y         device [M, D] of dtype yt: the final h
@@ -200,15 +209,28 @@ star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64
  * Where the stack fits, it runs as one persistent launch of at most one
  * workgroup per CU whose workgroups wait on each other, so they must all be
  * resident at once: the device must not be held by long-running work on other
- * streams meanwhile.  If it is, a wait reaches its bound (about half a second)
- * and the step finishes with an unspecified Y instead of hanging.
+ * streams meanwhile.  If it is, a wait reaches its bound (about half a second),
+ * the kernel raises the workspace's error flag, every later wait of the step
+ * gives up at once, and the step finishes with an unspecified Y instead of
+ * hanging.  star_decode_status reports the flag; every call clears it first.
  */
 star_status star_decode(const star_algebra *up, const star_algebra *down, int32_t n_layers,
-                        int64_t M, const int32_t *row_type, const void *X,
+                        int64_t M, const int32_t *row_type, const void *X, star_dtype xt,
                         const void *const *W_up, const float *const *b_up,
                         const void *const *W_down, const float *const *b_down,
                         star_act act, int32_t residual, void *Y, star_dtype yt,
                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Whether the last star_decode or star_decode_gated call that used workspace
+ * `ws` lost its step to a wait bound (see star_decode): waits for the work
+ * queued on `stream` (synchronises it), then writes 1 (Y of that call is
+ * unspecified) or 0 (no wait ran out) to host *timed_out.
+ *   ws  the device workspace passed to that call (the flag is its first
+ *       int32); ws_bytes its size, at least 4
+ */
+star_status star_decode_status(const void *ws, size_t ws_bytes, int32_t *timed_out,
+                               hipStream_t stream);
 
 /*
  * star_decode for a gated FFN stack (SwiGLU; Sec. 4, "Projection Shapes", and
@@ -223,7 +245,7 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
  *   ws              at least star_workspace_bytes(STAR_OP_DECODE, up, down, M) bytes
  */
 star_status star_decode_gated(const star_algebra *up, const star_algebra *down, int32_t n_layers,
-                              int64_t M, const int32_t *row_type, const void *X,
+                              int64_t M, const int32_t *row_type, const void *X, star_dtype xt,
                               const void *const *W_gate, const float *const *b_gate,
                               const void *const *W_up, const float *const *b_up,
                               const void *const *W_down, const float *const *b_down,

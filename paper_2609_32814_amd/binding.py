@@ -52,11 +52,12 @@ def _load() -> ctypes.CDLL:
     lib.star_proj_bwd_data.argtypes = [A, i64, P, P, E, P, E, P, E, P, E, P, sz, P]
     lib.star_proj_bwd_weight.argtypes = [A, i64, P, P, E, P, E, P, P, P, sz, P]
     lib.star_ffn_fwd.argtypes = [A, A, i64, P, P, P, P, P, P, E, P, P, P, E, E, P, sz, P]
-    lib.star_decode.argtypes = [A, A, i32, i64, P, P, ctypes.POINTER(P), ctypes.POINTER(P),
+    lib.star_decode.argtypes = [A, A, i32, i64, P, P, E, ctypes.POINTER(P), ctypes.POINTER(P),
                                 ctypes.POINTER(P), ctypes.POINTER(P), E, i32, P, E, P, sz, P]
-    lib.star_decode_gated.argtypes = [A, A, i32, i64, P, P, ctypes.POINTER(P), ctypes.POINTER(P),
+    lib.star_decode_gated.argtypes = [A, A, i32, i64, P, P, E, ctypes.POINTER(P), ctypes.POINTER(P),
                                       ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
                                       ctypes.POINTER(P), i32, P, E, P, sz, P]
+    lib.star_decode_status.argtypes = [P, sz, ctypes.POINTER(i32), P]
     lib.star_workspace_bytes.argtypes = [i32, A, A, i64]
     lib.star_workspace_bytes.restype = sz
     lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
@@ -77,7 +78,7 @@ def _load() -> ctypes.CDLL:
                  "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
                  "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add",
-                 "star_decode_gated"):
+                 "star_decode_gated", "star_decode_status"):
         getattr(lib, name).restype = E
     return lib
 
@@ -146,7 +147,55 @@ def _ws(op: str, alg: Algebra, alg2, M: int, device, ws):
     need = star_workspace_bytes(op, alg, alg2, M)
     if ws is None:
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=device)
+    if not ws.is_contiguous() or ws.device != device:
+        raise ValueError("ws must be a contiguous buffer on the operands' device")
     return ws, ws.numel() * ws.element_size()
+
+
+def _need(t, name: str, shape, dtypes=None, device=None):
+    """Checks a tensor argument before its pointer crosses the ABI: a device
+    tensor of the expected shape and dtype, dense in row-major order (the
+    library reads every buffer as a plain row-major array)."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if tuple(t.shape) != tuple(int(v) for v in shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {tuple(dtypes)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major, no strides)")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    return t
+
+
+def _gpu(device):
+    """Every tensor of a call sits on `device`; it must be a GPU."""
+    if torch.device(device).type != "cuda":
+        raise ValueError("the library takes GPU tensors only")
+
+
+def _opt(t, name: str, shape, dtypes=None, device=None):
+    return None if t is None else _need(t, name, shape, dtypes, device)
+
+
+_FLOATS = (torch.float32, torch.bfloat16)
+_F32 = (torch.float32,)
+_BF16 = (torch.bfloat16,)
+_I32 = (torch.int32,)
+
+
+def _rows(X, name: str, K: int):
+    if not isinstance(X, torch.Tensor) or X.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D tensor")
+    _need(X, name, (X.shape[0], K), _FLOATS)
+    return X.shape[0], X.device
+
+
+def _types(row_type, M: int, device):
+    return _need(row_type, "row_type", (M,), _I32, device)
 
 
 def star_status_string(status: int) -> str:
@@ -172,7 +221,9 @@ def star_count_macs(alg: Algebra, rows_per_type: Sequence[int]) -> int:
 
 def star_validate_types(row_type: torch.Tensor, q: int, ws=None) -> int:
     n_bad = ctypes.c_int64()
+    _types(row_type, row_type.numel(), row_type.device)
     ws = ws if ws is not None else torch.empty(16, dtype=torch.uint8, device=row_type.device)
+    _gpu(row_type.device)
     _check(LIB.star_validate_types(row_type.numel(), _ptr(row_type), int(q), ctypes.byref(n_bad),
                                    _ptr(ws), ws.numel(), _stream(row_type.device)),
            "star_validate_types")
@@ -187,8 +238,11 @@ def star_type_plan(q: int, row_type: torch.Tensor, plan=None):
     """Builds the type plan of ``row_type`` (device uint8 buffer)."""
     M = row_type.numel()
     dev = row_type.device
+    _types(row_type, M, dev)
     if plan is None:
         plan = torch.empty(max(star_plan_bytes(q, M), 16), dtype=torch.uint8, device=dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
+    _gpu(dev)
     _check(LIB.star_type_plan(int(q), M, _ptr(row_type), _ptr(plan), plan.numel(), _stream(dev)),
            "star_type_plan")
     return plan
@@ -197,13 +251,19 @@ def star_type_plan(q: int, row_type: torch.Tensor, plan=None):
 def star_proj_fwd_planned(alg: Algebra, plan: torch.Tensor, X: torch.Tensor, W: torch.Tensor,
                           bias: torch.Tensor | None = None, act: str = "none", Z_out=None,
                           Y=None, out_dtype=None):
-    M = X.shape[0]
-    dev = X.device
+    M, dev = _rows(X, "X", alg.K)
+    _need(W, "W", (alg.K, alg.N), (X.dtype,), dev)
+    _opt(bias, "bias", (alg.N,), _F32, dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
     if Y is None:
         Y = torch.empty((M, alg.N), dtype=out_dtype or X.dtype, device=dev)
+    _need(Y, "Y", (M, alg.N), _FLOATS, dev)
     want_z = Z_out is not None and Z_out is not False
     if Z_out is True:
         Z_out = torch.empty((M, alg.N), dtype=Y.dtype, device=dev)
+    if want_z:
+        _need(Z_out, "Z_out", (M, alg.N), (Y.dtype,), dev)
+    _gpu(dev)
     _check(LIB.star_proj_fwd_planned(alg.ref, M, _ptr(plan), _ptr(X), _dt(X), _ptr(W), _dt(W),
                                      _ptr(bias), ACTS[act], _ptr(Z_out) if want_z else None,
                                      _ptr(Y), _dt(Y), _stream(dev)), "star_proj_fwd_planned")
@@ -213,10 +273,14 @@ def star_proj_fwd_planned(alg: Algebra, plan: torch.Tensor, X: torch.Tensor, W: 
 def star_proj_bwd_data_planned(alg: Algebra, plan: torch.Tensor, dY: torch.Tensor,
                                W: torch.Tensor, Z_prev=None, act_prev: str = "none", dX=None,
                                out_dtype=None):
-    M = dY.shape[0]
-    dev = dY.device
+    M, dev = _rows(dY, "dY", alg.N)
+    _need(W, "W", (alg.K, alg.N), (dY.dtype,), dev)
+    _opt(Z_prev, "Z_prev", (M, alg.K), (dY.dtype,), dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
     if dX is None:
         dX = torch.empty((M, alg.K), dtype=out_dtype or dY.dtype, device=dev)
+    _need(dX, "dX", (M, alg.K), _FLOATS, dev)
+    _gpu(dev)
     _check(LIB.star_proj_bwd_data_planned(alg.ref, M, _ptr(plan), _ptr(dY), _dt(dY), _ptr(W),
                                           _dt(W), _ptr(Z_prev), ACTS[act_prev], _ptr(dX),
                                           _dt(dX), _stream(dev)), "star_proj_bwd_data_planned")
@@ -226,12 +290,16 @@ def star_proj_bwd_data_planned(alg: Algebra, plan: torch.Tensor, dY: torch.Tenso
 def star_proj_bwd_weight_planned(alg: Algebra, plan: torch.Tensor, X: torch.Tensor,
                                  dY: torch.Tensor, dW=None, dbias=None, want_dbias: bool = True,
                                  ws=None):
-    M = X.shape[0]
-    dev = X.device
+    M, dev = _rows(X, "X", alg.K)
+    _need(dY, "dY", (M, alg.N), (X.dtype,), dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
     if dW is None:
         dW = torch.empty((alg.K, alg.N), dtype=torch.float32, device=dev)
     if dbias is None and want_dbias:
         dbias = torch.empty(alg.N, dtype=torch.float32, device=dev)
+    _need(dW, "dW", (alg.K, alg.N), _F32, dev)
+    _opt(dbias, "dbias", (alg.N,), _F32, dev)
+    _gpu(dev)
     ws, nbytes = _ws("bwd_weight", alg, None, M, dev, ws)
     _check(LIB.star_proj_bwd_weight_planned(alg.ref, M, _ptr(plan), _ptr(X), _dt(X), _ptr(dY),
                                             _dt(dY), _ptr(dW), _ptr(dbias), _ptr(ws), nbytes,
@@ -244,14 +312,20 @@ def star_proj_fwd(alg: Algebra, row_type: torch.Tensor, X: torch.Tensor, W: torc
                   out_dtype=None, ws=None):
     """Y = act(X *_q W + bias).  ``Z_out=True`` allocates and returns the
     pre-activation too.  Returns Y, or (Y, Z) when Z_out is requested."""
-    M = X.shape[0]
-    dev = X.device
+    M, dev = _rows(X, "X", alg.K)
+    _types(row_type, M, dev)
+    _need(W, "W", (alg.K, alg.N), (X.dtype,), dev)
+    _opt(bias, "bias", (alg.N,), _F32, dev)
     out_dtype = out_dtype or X.dtype
     if Y is None:
         Y = torch.empty((M, alg.N), dtype=out_dtype, device=dev)
+    _need(Y, "Y", (M, alg.N), _FLOATS, dev)
     want_z = Z_out is not None and Z_out is not False
     if Z_out is True:
         Z_out = torch.empty((M, alg.N), dtype=Y.dtype, device=dev)
+    if want_z:
+        _need(Z_out, "Z_out", (M, alg.N), (Y.dtype,), dev)
+    _gpu(dev)
     ws, nbytes = _ws("fwd", alg, None, M, dev, ws)
     _check(LIB.star_proj_fwd(alg.ref, M, _ptr(row_type), _ptr(X), _dt(X), _ptr(W), _dt(W),
                              _ptr(bias), ACTS[act], _ptr(Z_out) if want_z else None, _ptr(Y),
@@ -263,10 +337,14 @@ def star_proj_bwd_data(alg: Algebra, row_type: torch.Tensor, dY: torch.Tensor, W
                        Z_prev: torch.Tensor | None = None, act_prev: str = "none", dX=None,
                        out_dtype=None, ws=None):
     """dX = (dY *_q^T W) [. act_prev'(Z_prev)]."""
-    M = dY.shape[0]
-    dev = dY.device
+    M, dev = _rows(dY, "dY", alg.N)
+    _types(row_type, M, dev)
+    _need(W, "W", (alg.K, alg.N), (dY.dtype,), dev)
+    _opt(Z_prev, "Z_prev", (M, alg.K), (dY.dtype,), dev)
     if dX is None:
         dX = torch.empty((M, alg.K), dtype=out_dtype or dY.dtype, device=dev)
+    _need(dX, "dX", (M, alg.K), _FLOATS, dev)
+    _gpu(dev)
     ws, nbytes = _ws("bwd_data", alg, None, M, dev, ws)
     _check(LIB.star_proj_bwd_data(alg.ref, M, _ptr(row_type), _ptr(dY), _dt(dY), _ptr(W), _dt(W),
                                   _ptr(Z_prev), ACTS[act_prev], _ptr(dX), _dt(dX), _ptr(ws),
@@ -277,12 +355,16 @@ def star_proj_bwd_data(alg: Algebra, row_type: torch.Tensor, dY: torch.Tensor, W
 def star_proj_bwd_weight(alg: Algebra, row_type: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
                          dW=None, dbias=None, want_dbias: bool = True, ws=None):
     """(dW, dbias) in fp32; dbias is None unless requested."""
-    M = X.shape[0]
-    dev = X.device
+    M, dev = _rows(X, "X", alg.K)
+    _types(row_type, M, dev)
+    _need(dY, "dY", (M, alg.N), (X.dtype,), dev)
     if dW is None:
         dW = torch.empty((alg.K, alg.N), dtype=torch.float32, device=dev)
     if dbias is None and want_dbias:
         dbias = torch.empty(alg.N, dtype=torch.float32, device=dev)
+    _need(dW, "dW", (alg.K, alg.N), _F32, dev)
+    _opt(dbias, "dbias", (alg.N,), _F32, dev)
+    _gpu(dev)
     ws, nbytes = _ws("bwd_weight", alg, None, M, dev, ws)
     _check(LIB.star_proj_bwd_weight(alg.ref, M, _ptr(row_type), _ptr(X), _dt(X), _ptr(dY),
                                     _dt(dY), _ptr(dW), _ptr(dbias), _ptr(ws), nbytes,
@@ -294,14 +376,25 @@ def star_ffn_fwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Te
                  W_up: torch.Tensor, b_up, W_down: torch.Tensor, b_down, act: str = "gelu",
                  save_z: bool = True, H=None, Y=None, Z_up=None, out_dtype=None, ws=None):
     """Returns (Z_up or None, H, Y)."""
-    M = X.shape[0]
-    dev = X.device
+    M, dev = _rows(X, "X", up.K)
+    _types(row_type, M, dev)
+    if down.K != up.N or down.N != up.K:
+        raise ValueError("down must map the up projection's output back to its input width")
+    _need(W_up, "W_up", (up.K, up.N), (X.dtype,), dev)
+    _need(W_down, "W_down", (down.K, down.N), (X.dtype,), dev)
+    _opt(b_up, "b_up", (up.N,), _F32, dev)
+    _opt(b_down, "b_down", (down.N,), _F32, dev)
     if H is None:
         H = torch.empty((M, up.N), dtype=X.dtype, device=dev)
     if Y is None:
         Y = torch.empty((M, down.N), dtype=out_dtype or X.dtype, device=dev)
     if save_z and Z_up is None:
         Z_up = torch.empty((M, up.N), dtype=X.dtype, device=dev)
+    _need(H, "H", (M, up.N), (X.dtype,), dev)
+    _need(Y, "Y", (M, down.N), _FLOATS, dev)
+    if save_z:
+        _need(Z_up, "Z_up", (M, up.N), (X.dtype,), dev)
+    _gpu(dev)
     ws, nbytes = _ws("ffn_fwd", up, down, M, dev, ws)
     _check(LIB.star_ffn_fwd(up.ref, down.ref, M, _ptr(row_type), _ptr(X), _ptr(W_up), _ptr(b_up),
                             _ptr(W_down), _ptr(b_down), ACTS[act], _ptr(Z_up) if save_z else None,
@@ -310,44 +403,96 @@ def star_ffn_fwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Te
     return (Z_up if save_z else None), H, Y
 
 
-def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
-                W_ups: Sequence[torch.Tensor], b_ups, W_downs: Sequence[torch.Tensor], b_downs,
-                act: str = "gelu", residual: bool = True, Y=None, out_dtype=None, ws=None):
-    """One decode step through ``len(W_ups)`` FFN layers; returns Y."""
-    M = X.shape[0]
-    dev = X.device
-    L = len(W_ups)
+def _decode_args(up: Algebra, down: Algebra, row_type, X, L: int, Y, out_dtype, weights, biases):
+    if not isinstance(X, torch.Tensor) or X.dtype != torch.bfloat16:
+        raise TypeError("decode takes a bfloat16 X")
+    M, dev = _rows(X, "X", up.K)
+    _types(row_type, M, dev)
+    if down.K != up.N or down.N != up.K:
+        raise ValueError("down must map the up projection's output back to its input width")
+    for name, ts, shape in weights:
+        if len(ts) != L:
+            raise ValueError(f"{name} needs one tensor per layer ({L})")
+        for t in ts:
+            _need(t, name, shape, _BF16, dev)
+    for name, ts, shape in biases:
+        if ts is None:
+            continue
+        if len(ts) != L:
+            raise ValueError(f"{name} needs one entry per layer ({L})")
+        for t in ts:
+            _opt(t, name, shape, _F32, dev)
     if Y is None:
         Y = torch.empty((M, up.K), dtype=out_dtype or X.dtype, device=dev)
+    _need(Y, "Y", (M, up.K), _FLOATS, dev)
+    return M, dev, Y
+
+
+def star_decode_status(ws: torch.Tensor) -> bool:
+    """True when the last decode call on workspace ``ws`` lost its step to a
+    wait bound (its Y is then unspecified).  Synchronises the stream."""
+    flag = ctypes.c_int32()
+    _need(ws, "ws", tuple(ws.shape))
+    _gpu(ws.device)
+    _check(LIB.star_decode_status(_ptr(ws), ws.numel() * ws.element_size(), ctypes.byref(flag),
+                                  _stream(ws.device)), "star_decode_status")
+    return bool(flag.value)
+
+
+def _decode_checked(ws, check: bool, where: str):
+    if check and star_decode_status(ws):
+        raise RuntimeError(f"{where}: a wait of the decode stack ran out (the device was not free "
+                           "for all of its workgroups); the step's output is unspecified")
+
+
+def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                W_ups: Sequence[torch.Tensor], b_ups, W_downs: Sequence[torch.Tensor], b_downs,
+                act: str = "gelu", residual: bool = True, Y=None, out_dtype=None, ws=None,
+                check: bool = True):
+    """One decode step through ``len(W_ups)`` FFN layers; returns Y.  With
+    ``check`` (the default) the call synchronises and raises if the step was
+    lost to a wait bound; pass ``check=False`` (and a ``ws`` to read with
+    ``star_decode_status`` later) inside timed loops and graph captures."""
+    L = len(W_ups)
+    M, dev, Y = _decode_args(up, down, row_type, X, L, Y, out_dtype,
+                             [("W_up", W_ups, (up.K, up.N)), ("W_down", W_downs, (down.K, down.N))],
+                             [("b_up", b_ups, (up.N,)), ("b_down", b_downs, (down.N,))])
     P = ctypes.c_void_p
     wu = (P * L)(*[t.data_ptr() for t in W_ups])
     wd = (P * L)(*[t.data_ptr() for t in W_downs])
     bu = (P * L)(*[t.data_ptr() if t is not None else None for t in b_ups]) if b_ups is not None else None
     bd = (P * L)(*[t.data_ptr() if t is not None else None for t in b_downs]) if b_downs is not None else None
+    _gpu(dev)
     ws, nbytes = _ws("decode", up, down, M, dev, ws)
-    _check(LIB.star_decode(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), wu, bu, wd, bd,
+    _check(LIB.star_decode(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), _dt(X), wu, bu, wd, bd,
                            ACTS[act], int(bool(residual)), _ptr(Y), _dt(Y), _ptr(ws), nbytes,
                            _stream(dev)), "star_decode")
+    _decode_checked(ws, check, "star_decode")
     return Y
 
 
 def star_decode_gated(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
                       W_gates: Sequence[torch.Tensor], b_gates, W_ups: Sequence[torch.Tensor], b_ups,
                       W_downs: Sequence[torch.Tensor], b_downs, residual: bool = True, Y=None,
-                      out_dtype=None, ws=None):
-    """One decode step through ``len(W_ups)`` gated-FFN (SwiGLU) layers; returns Y."""
-    M = X.shape[0]
-    dev = X.device
+                      out_dtype=None, ws=None, check: bool = True):
+    """One decode step through ``len(W_ups)`` gated-FFN (SwiGLU) layers;
+    returns Y (``check`` as in star_decode)."""
     L = len(W_ups)
-    if Y is None:
-        Y = torch.empty((M, up.K), dtype=out_dtype or X.dtype, device=dev)
+    M, dev, Y = _decode_args(up, down, row_type, X, L, Y, out_dtype,
+                             [("W_gate", W_gates, (up.K, up.N)), ("W_up", W_ups, (up.K, up.N)),
+                              ("W_down", W_downs, (down.K, down.N))],
+                             [("b_gate", b_gates, (up.N,)), ("b_up", b_ups, (up.N,)),
+                              ("b_down", b_downs, (down.N,))])
     P = ctypes.c_void_p
     arr = lambda ts: (P * L)(*[t.data_ptr() for t in ts])
     opt = lambda ts: (P * L)(*[t.data_ptr() if t is not None else None for t in ts]) if ts is not None else None
+    _gpu(dev)
     ws, nbytes = _ws("decode", up, down, M, dev, ws)
-    _check(LIB.star_decode_gated(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), arr(W_gates), opt(b_gates),
-                                 arr(W_ups), opt(b_ups), arr(W_downs), opt(b_downs), int(bool(residual)),
-                                 _ptr(Y), _dt(Y), _ptr(ws), nbytes, _stream(dev)), "star_decode_gated")
+    _check(LIB.star_decode_gated(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), _dt(X), arr(W_gates),
+                                 opt(b_gates), arr(W_ups), opt(b_ups), arr(W_downs), opt(b_downs),
+                                 int(bool(residual)), _ptr(Y), _dt(Y), _ptr(ws), nbytes, _stream(dev)),
+           "star_decode_gated")
+    _decode_checked(ws, check, "star_decode_gated")
     return Y
 
 
@@ -373,8 +518,12 @@ def star_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Te
 
 def star_swiglu_fwd(Z_gate: torch.Tensor, Z_up: torch.Tensor, H=None) -> torch.Tensor:
     """H = silu(Z_gate) . Z_up (elementwise, on the GPU)."""
+    _need(Z_gate, "Z_gate", tuple(Z_gate.shape), _FLOATS)
+    _need(Z_up, "Z_up", tuple(Z_gate.shape), (Z_gate.dtype,), Z_gate.device)
     if H is None:
         H = torch.empty_like(Z_gate)
+    _need(H, "H", tuple(Z_gate.shape), (Z_gate.dtype,), Z_gate.device)
+    _gpu(Z_gate.device)
     _check(LIB.star_swiglu_fwd(Z_gate.numel(), _ptr(Z_gate), _ptr(Z_up), _dt(Z_gate), _ptr(H),
                                _stream(Z_gate.device)), "star_swiglu_fwd")
     return H
@@ -382,7 +531,11 @@ def star_swiglu_fwd(Z_gate: torch.Tensor, Z_up: torch.Tensor, H=None) -> torch.T
 
 def star_swiglu_bwd(dH: torch.Tensor, Z_gate: torch.Tensor, Z_up: torch.Tensor):
     """(dZ_gate, dZ_up) = (dH . Z_up . silu'(Z_gate), dH . silu(Z_gate))."""
+    _need(dH, "dH", tuple(dH.shape), _FLOATS)
+    _need(Z_gate, "Z_gate", tuple(dH.shape), (dH.dtype,), dH.device)
+    _need(Z_up, "Z_up", tuple(dH.shape), (dH.dtype,), dH.device)
     dZg, dZu = torch.empty_like(dH), torch.empty_like(dH)
+    _gpu(dH.device)
     _check(LIB.star_swiglu_bwd(dH.numel(), _ptr(dH), _ptr(Z_gate), _ptr(Z_up), _dt(dH), _ptr(dZg),
                                _ptr(dZu), _stream(dH.device)), "star_swiglu_bwd")
     return dZg, dZu
@@ -390,8 +543,12 @@ def star_swiglu_bwd(dH: torch.Tensor, Z_gate: torch.Tensor, Z_up: torch.Tensor):
 
 def star_add(a: torch.Tensor, b: torch.Tensor, out=None) -> torch.Tensor:
     """out = a + b (elementwise, on the GPU; out may be a or b)."""
+    _need(a, "a", tuple(a.shape), _FLOATS)
+    _need(b, "b", tuple(a.shape), (a.dtype,), a.device)
     if out is None:
         out = torch.empty_like(a)
+    _need(out, "out", tuple(a.shape), (a.dtype,), a.device)
+    _gpu(a.device)
     _check(LIB.star_add(a.numel(), _ptr(a), _ptr(b), _dt(a), _ptr(out), _stream(a.device)), "star_add")
     return out
 

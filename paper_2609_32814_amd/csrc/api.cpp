@@ -171,13 +171,19 @@ BwdWs bwd_weight_layout(const Alg& a, int64_t M) {
   return w;
 }
 
+// Every decode workspace starts with the status line: the decode stack's
+// error flag (int32 at offset 0, raised when one of its bounded waits ran
+// out) on a 256-byte line of its own, zeroed by every star_decode call and
+// read by star_decode_status.
+constexpr size_t kDecodeStatusBytes = kCounterStride * sizeof(int32_t);
+
 struct DecodeWs {
   size_t h = 0, xb = 0, H = 0, end = 0;
 };
 DecodeWs decode_layout(const Alg& up, int64_t M) {
   DecodeWs w;
   const int64_t D = up.K(), F = up.N();
-  size_t cur = 0;
+  size_t cur = kDecodeStatusBytes;
   w.h = cur;
   cur = align_up(cur + sizeof(float) * M * D);
   w.xb = cur;
@@ -192,11 +198,13 @@ DecodeWs decode_layout(const Alg& up, int64_t M) {
 // the down contraction over F cut into ns chunks so both phases have about
 // as many items; usable when every item's inputs and two weight slots fit
 // in LDS, the grid fits on the device at one workgroup per CU and the layer
-// pointers fit in the kernel arguments.
+// pointers fit in the kernel arguments.  Layout: the counters (the first of
+// them the status line) and the tagged hand-off words first, so that one
+// fill clears them all, then H, the bf16 inputs, h and the down partials.
 struct StackPlan {
   bool ok = false;
   int ns = 1, kc = 0, nt_up = 0, nt_dn = 0, grid = 0;
-  size_t H = 0, hb = 0, h = 0, part = 0, tH = 0, tpart = 0, cnt = 0, end = 0;
+  size_t H = 0, hb = 0, h = 0, part = 0, tH = 0, tpart = 0, cnt = 0, zero_end = 0, end = 0;
   bool resident = false;
 };
 StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool gated = false) {
@@ -209,7 +217,21 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool g
   sp.kc = (sp.kc + 127) / 128 * 128;
   sp.ns = static_cast<int>((F + sp.kc - 1) / sp.kc);
   sp.grid = std::max(sp.nt_up, sp.nt_dn * sp.ns);
+  const int kmax = static_cast<int>(std::max<int64_t>(D, sp.kc));
+  sp.resident = M >= 1 && M <= kDecodeMaxRows &&
+                decode_stack_resident(static_cast<int>(M), kmax, static_cast<int>(D), sp.ns, gated, sp.nt_up,
+                                      sp.nt_dn);
   size_t cur = 0;
+  sp.cnt = cur;
+  cur = align_up(cur + sizeof(int32_t) * decode_stack_counters(sp.nt_dn));
+  sp.tH = cur;
+  sp.tpart = cur;
+  if (sp.resident) {
+    cur = align_up(cur + sizeof(uint64_t) * M * (F / 2));
+    sp.tpart = cur;
+    cur = align_up(cur + sizeof(uint64_t) * 2 * sp.ns * M * D);
+  }
+  sp.zero_end = cur;
   sp.H = cur;
   cur = align_up(cur + sizeof(uint16_t) * M * F);
   sp.hb = cur;
@@ -218,26 +240,11 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool g
   cur = align_up(cur + sizeof(float) * M * D);
   sp.part = cur;
   cur = align_up(cur + sizeof(float) * sp.ns * M * D);
-  // tagged hand-off words right before the counters: one fill clears both
-  const int kmax = static_cast<int>(std::max<int64_t>(D, sp.kc));
-  sp.resident = M >= 1 && M <= kDecodeMaxRows &&
-                decode_stack_resident(static_cast<int>(M), kmax, static_cast<int>(D), sp.ns, gated, sp.nt_up,
-                                      sp.nt_dn);
-  sp.tH = cur;
-  sp.tpart = cur;
-  if (sp.resident) {
-    cur = align_up(cur + sizeof(uint64_t) * M * (F / 2));
-    sp.tpart = cur;
-    cur = align_up(cur + sizeof(uint64_t) * 2 * sp.ns * M * D);
-  }
-  sp.cnt = cur;
-  cur = align_up(cur + sizeof(int32_t) * decode_stack_counters(sp.nt_dn));
   sp.end = cur;
   bool same_groups = u.q == d.q && u.law == d.law;
   for (int g = 0; same_groups && g <= u.q; ++g) same_groups = d.S[g] == u.R[g] && d.R[g] == u.S[g];
   sp.ok = M >= 1 && M <= kDecodeMaxRows && n_layers <= kStackMaxLayers && same_groups &&
-          decode_stack_smem(static_cast<int>(M), static_cast<int>(std::max<int64_t>(D, sp.kc)), static_cast<int>(D),
-                            sp.ns, gated) > 0 &&
+          decode_stack_smem(static_cast<int>(M), kmax, static_cast<int>(D), sp.ns, gated) > 0 &&
           sp.grid <= cu_count();
   return sp;
 }
@@ -282,48 +289,19 @@ int persistent_grid(int64_t upper_tiles) {
   return static_cast<int>(g);
 }
 
-// Column-tile width of the forward and activation-gradient GEMMs: 128
-// columns (nw = 2).  The 256-column variant (nw = 4) holds 256 accumulators
-// per lane and spills; STARQ_GEMM_NW=4 selects it for experiments.
-int choose_nw(const int64_t* G, int q, int64_t rows_upper) {
-  if (const char* env = std::getenv("STARQ_GEMM_NW")) {
-    const int v = std::atoi(env);
-    if (v == 2 || v == 4) return v;
-  }
-  (void)G;
-  (void)q;
-  (void)rows_upper;
-  return 2;
-}
+// Column-tile width of the fp32 kernel's forward and activation-gradient
+// tiles: 128 columns.
+constexpr int kFp32NW = 2;
 
 star_status hip_status(hipError_t e) { return e == hipSuccess ? STAR_OK : STAR_ERR_HIP; }
 
-// bf16 operands with 128-column tiles take the kernel fed by direct
-// global-to-LDS copies; STARQ_GEMM_SYNC=1 keeps the register-staged one.
-bool use_async_gemm() {
-  static const bool sync = [] {
-    const char* env = std::getenv("STARQ_GEMM_SYNC");
-    return env && std::atoi(env) == 1;
-  }();
-  return !sync;
-}
-
 // bf16 operands take the kernel fed by direct global-to-LDS copies (its
-// column tiles are wider, so the tile counts are redone for it);
-// STARQ_GEMM_SYNC=1 keeps the register-staged one.  `upper` bounds the
-// number of tiles of the register-staged kernel.
-// STARQ_DECODE_PHASES=1 runs the decode stack as one kernel per projection.
-bool use_decode_stack() {
-  static const bool phases = [] {
-    const char* env = std::getenv("STARQ_DECODE_PHASES");
-    return env && std::atoi(env) == 1;
-  }();
-  return !phases;
-}
-
+// column tiles are wider, so the tile counts are redone for it); fp32
+// operands the register-staged one.  `upper` bounds the number of tiles of
+// the register-staged kernel.
 hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
                             hipStream_t stream) {
-  if (p.elem == 1 && use_async_gemm()) {
+  if (p.elem == 1) {
     GemmParams pa = p;
     const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
     const int tn = gemm_async_tile_n();
@@ -354,7 +332,7 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
   p.Y = Y;
   p.ydtype = yt;
   const int64_t rows_upper = M / kTileM + a.q;
-  const int nw = choose_nw(a.R, a.q, rows_upper);
+  const int nw = kFp32NW;
   fill_tiles(p.NTp, a.R, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
   return hip_status(launch_proj_gemm(kModeFwd, p, nw, upper, stream));
@@ -531,7 +509,7 @@ star_status star_proj_bwd_data_planned(const star_algebra* alg, int64_t M, const
   p.Y = dX;
   p.ydtype = dxt;
   const int64_t rows_upper = M / kTileM + a.q;
-  const int nw = choose_nw(a.S, a.q, rows_upper);
+  const int nw = kFp32NW;
   fill_tiles(p.NTp, a.S, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
   return hip_status(launch_proj_gemm(kModeBwdData, p, nw, upper, stream));
@@ -575,7 +553,7 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
       (dbias && !aligned4(dbias)) || (plan && !aligned16(plan)))
     return STAR_ERR_ALIGN;
   const BwdWs bw = bwd_weight_layout(a, M);
-  const bool pipelined = xt == STAR_BF16 && use_async_gemm();
+  const bool pipelined = xt == STAR_BF16;
   if ((pipelined || bw.nsplit > 1) && M > 0 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
   if (ws && !aligned16(ws)) return STAR_ERR_ALIGN;
   // M = 0 still defines the output: an empty sum
@@ -693,7 +671,7 @@ namespace {
 // The decode step behind star_decode and star_decode_gated (W_gate non-null:
 // gated FFN, persistent stack only).
 star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_t n_layers, int64_t M,
-                        const int32_t* row_type, const void* X, const void* const* W_gate,
+                        const int32_t* row_type, const void* X, star_dtype xt, const void* const* W_gate,
                         const float* const* b_gate, const void* const* W_up, const float* const* b_up,
                         const void* const* W_down, const float* const* b_down, star_act act,
                         int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
@@ -707,7 +685,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
   if (d.K() != u.N() || d.N() != u.K()) return STAR_ERR_SHAPE;
   if (M > kDecodeMaxRows || u.K() > kDecodeMaxK || u.N() > kDecodeMaxK) return STAR_ERR_UNSUPPORTED;
   if (n_layers < 1) return STAR_ERR_ARG;
-  if (!valid_dtype(yt)) return STAR_ERR_DTYPE;
+  if (!valid_dtype(yt) || xt != STAR_BF16) return STAR_ERR_DTYPE;
   if (!valid_act(act)) return STAR_ERR_ARG;
   if (M == 0) return STAR_OK;
   if (!X || !W_up || !W_down || !Y) return STAR_ERR_ARG;
@@ -726,7 +704,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
   // the gated FFN runs only in the persistent stack
   if (gated && !sp.ok) return STAR_ERR_UNSUPPORTED;
 
-  if (sp.ok && (gated || use_decode_stack())) {
+  if (sp.ok) {
     DecodeStack k;
     std::memset(&k, 0, sizeof(k));
     k.q = u.q;
@@ -769,12 +747,15 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
     k.cnt = at<int32_t>(ws, sp.cnt);
     k.tH = sp.resident ? at<uint64_t>(ws, sp.tH) : nullptr;
     k.tpart = sp.resident ? at<uint64_t>(ws, sp.tpart) : nullptr;
-    st = hip_status(launch_fill_zero(at<float>(ws, sp.tH),
-                                     static_cast<int64_t>((sp.end - sp.tH) / sizeof(float)), stream));
+    st = hip_status(launch_fill_zero(at<float>(ws, sp.cnt),
+                                     static_cast<int64_t>((sp.zero_end - sp.cnt) / sizeof(float)), stream));
     if (st != STAR_OK) return st;
     return hip_status(launch_decode_stack(k, sp.grid, stream));
   }
 
+  // the status line reads zero: the per-projection kernels do not wait
+  st = hip_status(launch_fill_zero(at<float>(ws, 0), kDecodeStatusBytes / sizeof(float), stream));
+  if (st != STAR_OK) return st;
   float* h = at<float>(ws, dw.h);
   uint16_t* xb = at<uint16_t>(ws, dw.xb);
   uint16_t* Hb = at<uint16_t>(ws, dw.H);
@@ -827,17 +808,29 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
 extern "C" {
 
 star_status star_decode(const star_algebra* up, const star_algebra* down, int32_t n_layers,
-                        int64_t M, const int32_t* row_type, const void* X,
+                        int64_t M, const int32_t* row_type, const void* X, star_dtype xt,
                         const void* const* W_up, const float* const* b_up,
                         const void* const* W_down, const float* const* b_down, star_act act,
                         int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
                         hipStream_t stream) {
-  return decode_impl(up, down, n_layers, M, row_type, X, nullptr, nullptr, W_up, b_up, W_down, b_down,
+  return decode_impl(up, down, n_layers, M, row_type, X, xt, nullptr, nullptr, W_up, b_up, W_down, b_down,
                      act, residual, Y, yt, ws, ws_bytes, stream);
 }
 
+star_status star_decode_status(const void* ws, size_t ws_bytes, int32_t* timed_out, hipStream_t stream) {
+  if (!ws || !timed_out) return STAR_ERR_ARG;
+  if (ws_bytes < sizeof(int32_t)) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  int32_t host = 0;
+  hipError_t e = hipMemcpyAsync(&host, ws, sizeof(host), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return STAR_ERR_HIP;
+  *timed_out = host != 0 ? 1 : 0;
+  return STAR_OK;
+}
+
 star_status star_decode_gated(const star_algebra* up, const star_algebra* down, int32_t n_layers,
-                              int64_t M, const int32_t* row_type, const void* X,
+                              int64_t M, const int32_t* row_type, const void* X, star_dtype xt,
                               const void* const* W_gate, const float* const* b_gate,
                               const void* const* W_up, const float* const* b_up,
                               const void* const* W_down, const float* const* b_down,
@@ -845,7 +838,7 @@ star_status star_decode_gated(const star_algebra* up, const star_algebra* down, 
                               hipStream_t stream) {
   if (M > 0 && !W_gate) return STAR_ERR_ARG;
   static const void* const no_layers[1] = {nullptr};
-  return decode_impl(up, down, n_layers, M, row_type, X, W_gate ? W_gate : no_layers, b_gate, W_up, b_up,
+  return decode_impl(up, down, n_layers, M, row_type, X, xt, W_gate ? W_gate : no_layers, b_gate, W_up, b_up,
                      W_down, b_down, STAR_ACT_NONE, residual, Y, yt, ws, ws_bytes, stream);
 }
 

@@ -32,27 +32,83 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // ---- activations -----------------------------------------------------------
-// Exact GELU uses the ROCm device library's erff; the tanh form its tanhf.
+// One GELU for every kernel (GEMM epilogues and the decode kernels), with
+// explicit approximations whose error bounds are stated and tested.
 
 enum Act : int { kActNone = 0, kActGelu = 1, kActGeluTanh = 2 };
 
-__device__ __forceinline__ float act_fwd(int act, float z) {
-  if (act == kActGelu) return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+constexpr float kLog2e = 1.4426950408889634f;
+
+// erf from Abramowitz & Stegun 7.1.26: erf(x) = 1 - (a1 t + ... + a5 t^5)
+// exp(-x^2), t = 1 / (1 + p x), x >= 0; |error| <= 1.5e-7.  The reciprocal
+// and exponential are the hardware approximations (about 1 ulp).
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  float poly = 1.061405429f;
+  poly = poly * t - 1.453152027f;
+  poly = poly * t + 1.421413741f;
+  poly = poly * t - 0.284496736f;
+  poly = poly * t + 0.254829592f;
+  poly *= t;
+  const float y = 1.0f - poly * __builtin_amdgcn_exp2f(-(ax * ax) * kLog2e);
+  return copysignf(y, x);
+}
+
+// tanh(u) = 1 - 2 / (1 + exp(2u)); the absolute error stays near 1e-7 over
+// the whole range (saturating to +-1), which is what the tanh-form GELU needs.
+__device__ __forceinline__ float tanh_fast(float u) {
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(2.0f * kLog2e * u));
+}
+
+// Exact-form GELU, z Phi(z) = z (1 + erf(z / sqrt 2)) / 2, with erf from
+// Abramowitz & Stegun 7.1.28: erf(x) = 1 - (1 + a1 x + ... + a6 x^6)^-16 for
+// x >= 0, |error| <= 3e-7.  With r = p(|z| / sqrt 2)^-16 the identity
+// z Phi(z) = max(z, 0) - |z| r / 2 holds for either sign of z; the 1 / sqrt 2
+// goes into the coefficients (a_k 2^(-k/2)) and the 1 / 2 too, by scaling
+// the whole polynomial by 2^(1/16).  So: six FMAs, four squarings, one
+// reciprocal, a max and an FMA, and no exponential.  Error in fp32 at most
+// 1e-6 + 2^-22 |GELU(z)| for every z (the test of the device activations
+// checks this element by element over [-12, 12] and the tails); p^16
+// overflows to infinity for large |z|, where r = 0 is the right limit.
+__device__ __forceinline__ float gelu_erf(float z) {
+  const float az = fabsf(z);
+  float p = 5.6212996640e-06f;
+  p = p * az + 5.1055209008e-05f;
+  p = p * az + 3.9686137011e-05f;
+  p = p * az + 3.4227392389e-03f;
+  p = p * az + 2.2076998457e-02f;
+  p = p * az + 5.2075163037e-02f;
+  p = p * az + 1.0442737824e+00f;
+  p *= p;
+  p *= p;
+  p *= p;
+  p *= p;
+  return fmaf(-az, __builtin_amdgcn_rcpf(p), fmaxf(z, 0.0f));
+}
+
+// Tanh form 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))): error at most
+// 1e-6 + 2^-22 |value|.
+__device__ __forceinline__ float act_apply(int act, float z) {
+  if (act == kActGelu) return gelu_erf(z);
   if (act == kActGeluTanh) {
-    float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
-    return 0.5f * z * (1.0f + tanhf(u));
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    return 0.5f * z * (1.0f + tanh_fast(u));
   }
   return z;
 }
 
-__device__ __forceinline__ float act_grad(int act, float z) {
+// d act / dz.  Erf form Phi(z) + z phi(z) (Phi through A&S 7.1.26): error
+// at most 1e-6.  Tanh form: error at most 5e-6 (the 1 - t^2 factor loses
+// digits where tanh saturates).
+__device__ __forceinline__ float act_deriv(int act, float z) {
   if (act == kActGelu)
-    return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) +
-           z * 0.39894228040143268f * __expf(-0.5f * z * z);
+    return 0.5f * (1.0f + erf_as7126(z * 0.70710678118654752f)) +
+           z * 0.39894228040143268f * __builtin_amdgcn_exp2f(-0.5f * z * z * kLog2e);
   if (act == kActGeluTanh) {
-    float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
-    float t = tanhf(u);
-    float du = 0.79788456080286536f * (1.0f + 0.134145f * z * z);
+    const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
+    const float t = tanh_fast(u);
+    const float du = 0.79788456080286536f * (1.0f + 0.134145f * z * z);
     return 0.5f * (1.0f + t) + 0.5f * z * (1.0f - t * t) * du;
   }
   return 1.0f;

@@ -78,9 +78,11 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   // which rows need block (g, j), per input group g: wave 0 holds one row
   // per lane and takes one ballot per group
   if (wave == 0) {
+    // a row whose type lies outside [0, q) has an empty support
     const int t = lane < p.M ? p.types[lane] : -1;
+    const bool valid = t >= 0 && t < p.q;
     for (int g = 0; g < p.q; ++g) {
-      const unsigned long long m = __ballot(lane < p.M && in_support(p.law, t, j, g));
+      const unsigned long long m = __ballot(valid && in_support(p.law, t, j, g));
       if (lane == 0) rowmask_s[g] = m;
     }
   }
@@ -197,8 +199,8 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
       const int64_t o = static_cast<int64_t>(m) * p.N + n;
       if (p.mode == 0) {
         uint2 w;
-        w.x = f32_to_bf16(act_fwd(p.act, z[0])) | (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, z[1]))) << 16);
-        w.y = f32_to_bf16(act_fwd(p.act, z[2])) | (static_cast<uint32_t>(f32_to_bf16(act_fwd(p.act, z[3]))) << 16);
+        w.x = f32_to_bf16(act_apply(p.act, z[0])) | (static_cast<uint32_t>(f32_to_bf16(act_apply(p.act, z[1]))) << 16);
+        w.y = f32_to_bf16(act_apply(p.act, z[2])) | (static_cast<uint32_t>(f32_to_bf16(act_apply(p.act, z[3]))) << 16);
         *reinterpret_cast<uint2*>(p.out_bf16 + o) = w;
       } else {
         float hv[4];

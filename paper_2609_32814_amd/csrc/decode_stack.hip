@@ -44,7 +44,10 @@
 // and reads all chunks of a layer before it writes its own of the next, so
 // no chunk is overwritten before every workgroup has read it.  Every wait
 // is bounded: after about half a second of spinning the kernel raises the
-// error flag and carries on, so it always terminates.
+// error flag (the first word of the workspace, which star_decode_status
+// reads) and carries on, so it always terminates; a wait that finds the
+// flag raised gives up at once, so a lost step ends after one bound, not
+// one per wait.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -58,6 +61,7 @@ constexpr int SLICE = 32;       // K rows per weight slice (1 KB)
 constexpr int kMaxSlices = 32;  // per item (K chunk <= 1024)
 constexpr int kRedBytes = 4 * 4 * 64 * 16;
 constexpr int kSpinLimit = 1 << 18;  // about 0.5 s per wait
+constexpr int kFlagPoll = 255;       // a waiter reads the error flag every 256 spins
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define STARQ_LDS __attribute__((address_space(3)))
@@ -122,6 +126,8 @@ __device__ __forceinline__ void settle_all(const uint64_t* const (&src)[N], uint
       st_agent(reinterpret_cast<uint32_t*>(err), 1u);
       break;
     }
+    // once some wait has timed out the step is lost: stop waiting at once
+    if ((spins & kFlagPoll) == 0 && ld_agent(reinterpret_cast<const uint32_t*>(err)) != 0u) break;
 #pragma unroll
     for (int i = 0; i < N; ++i)
       if (src[i] != nullptr && static_cast<uint32_t>(w[i] >> 32) != tag) w[i] = ld_tagged(src[i]);
@@ -227,9 +233,11 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   // the rows each 8-wide piece of them serves.
   auto plan = [&](int slot, const Item& it, const int32_t* KS) {
     if (wave == 0) {
+      // a row whose type lies outside [0, q) has an empty support
       const int t = lane < M ? p.types[lane] : -1;
+      const bool valid = t >= 0 && t < p.q;
       for (int g = 0; g < p.q; ++g) {
-        const unsigned long long m = __ballot(lane < M && in_support(p.law, t, it.j, g));
+        const unsigned long long m = __ballot(valid && in_support(p.law, t, it.j, g));
         if (lane == 0) rowmask_s[slot][g] = m;
       }
     }
@@ -306,6 +314,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
           if (lane == 0) st_agent(reinterpret_cast<uint32_t*>(err), 1u);
           break;
         }
+        if ((spins & kFlagPoll) == 0 && ld_agent(reinterpret_cast<const uint32_t*>(err)) != 0u) break;
       }
     }
     __syncthreads();
@@ -560,7 +569,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
           for (int e = 0; e < 4; ++e) v[e] *= g[e] / (1.0f + __expf(-g[e]));
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = act_fwd(p.act, v[e]);
+          for (int e = 0; e < 4; ++e) v[e] = act_apply(p.act, v[e]);
         }
         const uint32_t lo = f32_to_bf16(v[0]) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
         const uint32_t hi = f32_to_bf16(v[2]) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);

@@ -1,9 +1,10 @@
-// Grouped, row-typed GEMM on gfx950 MFMA: the forward projection, its
-// activation gradient and its weight gradient (Alg. 1 and the VJPs of the
-// appendix) in one persistent kernel template.
+// Grouped, row-typed GEMM on gfx950 MFMA for fp32 operands: the forward
+// projection, its activation gradient and its weight gradient (Alg. 1 and
+// the VJPs of the appendix) in one persistent kernel template.  bf16
+// operands run in the pipelined kernel of gemm_async.hip.
 //
 // Work decomposition.  C is cut into tiles of 256 rows x BN columns
-// (BN = 64 * WN with WN = 2 or 4).  A workgroup of 4 wavefronts (one per
+// (BN = 64 * WN, WN = 2).  A workgroup of 4 wavefronts (one per
 // SIMD) computes a tile; the wavefronts form a 2 x 2 grid and each owns
 // 128 x (32 * WN) of C as 4 x WN blocks of v_mfma_f32_32x32x16_bf16 (or of
 // v_mfma_f32_32x32x2f32 for fp32 operands), accumulated in AGPRs.
@@ -52,9 +53,8 @@
 //
 // Epilogue.  The MFMA is issued with the operands swapped (it computes
 // C^T blocks), so each lane ends with 4 consecutive columns of one row of
-// C and writes them as one 8- or 16-byte store.  GELU uses the erf
-// approximation 7.1.28 of Abramowitz & Stegun (one reciprocal, absolute
-// error of the GELU value <= 1e-6 in fp32); its derivative uses 7.1.26.
+// C and writes them as one 8- or 16-byte store.  The activation and its
+// derivative are the shared ones of common.hpp.
 #include "gemm_common.hpp"
 
 namespace starq {
@@ -566,20 +566,17 @@ hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// fp32 operands only: bf16 operands run in the pipelined kernel.
 template <int MODE, int WN>
 hipError_t launch_mode(const GemmParams& p, int grid, hipStream_t stream) {
-  if (p.elem == 1) return launch_typed<uint16_t, MODE, WN>(p, grid, stream);
+  if (p.elem != 0) return hipErrorInvalidValue;
   return launch_typed<float, MODE, WN>(p, grid, stream);
 }
 
 }  // namespace
 
 hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream) {
-  if (nw == 4) {
-    if (mode == kModeFwd) return launch_mode<kModeFwd, 4>(p, grid, stream);
-    if (mode == kModeBwdData) return launch_mode<kModeBwdData, 4>(p, grid, stream);
-    return launch_mode<kModeBwdWeight, 4>(p, grid, stream);
-  }
+  if (nw != 2) return hipErrorInvalidValue;
   if (mode == kModeFwd) return launch_mode<kModeFwd, 2>(p, grid, stream);
   if (mode == kModeBwdData) return launch_mode<kModeBwdData, 2>(p, grid, stream);
   return launch_mode<kModeBwdWeight, 2>(p, grid, stream);

@@ -54,8 +54,8 @@ hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* per
 hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
                                   unsigned long long* n_bad, hipStream_t stream);
 
-// Persistent grouped GEMM: tiles of kTileM rows x (64 * nw) columns
-// (nw = 2 or 4), `grid` workgroups of 128 * nw threads.
+// Persistent grouped GEMM for fp32 operands: tiles of kTileM rows x 128
+// columns (nw must be 2), `grid` workgroups of 256 threads.
 hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream);
 // bf16 forward / activation-gradient GEMM fed by direct global-to-LDS
 // copies: tiles of kTileM x gemm_async_tile_n() (p.NTp must count column

@@ -102,12 +102,56 @@ def test_decode_rejects_too_many_rows(P):
     V = ctypes.c_void_p
     up, dn = P.Algebra.equal(2, 64, 128), P.Algebra.equal(2, 128, 64)
     arr = (V * 1)(V(16))
-    st = P.binding.LIB.star_decode(up.ref, dn.ref, 1, 65, V(16), V(16), arr, None, arr, None, 1,
+    st = P.binding.LIB.star_decode(up.ref, dn.ref, 1, 65, V(16), V(16), 1, arr, None, arr, None, 1,
                                    1, V(16), 1, V(16), 1 << 30, None)
     assert st == 6
-    st = P.binding.LIB.star_decode(up.ref, P.Algebra.equal(2, 128, 32).ref, 1, 4, V(16), V(16),
+    st = P.binding.LIB.star_decode(up.ref, P.Algebra.equal(2, 128, 32).ref, 1, 4, V(16), V(16), 1,
                                    arr, None, arr, None, 1, 1, V(16), 1, V(16), 1 << 30, None)
     assert st == 2
+    # X must be bfloat16
+    st = P.binding.LIB.star_decode(up.ref, dn.ref, 1, 4, V(16), V(16), 0, arr, None, arr, None, 1,
+                                   1, V(16), 1, V(16), 1 << 30, None)
+    assert st == 3
+
+
+def test_decode_status_argument_errors(P):
+    """The status call checks its arguments on the host (no device access)."""
+    V = ctypes.c_void_p
+    flag = ctypes.c_int32(7)
+    assert P.binding.LIB.star_decode_status(None, 16, ctypes.byref(flag), None) == 1
+    assert P.binding.LIB.star_decode_status(V(16), 16, None, None) == 1
+    assert P.binding.LIB.star_decode_status(V(16), 2, ctypes.byref(flag), None) == 5
+    assert P.binding.LIB.star_decode_status(V(8), 16, ctypes.byref(flag), None) == 4
+    assert flag.value == 7
+
+
+def test_binding_refuses_bad_tensors(P):
+    """The binding checks shapes, dtypes, contiguity and devices before any
+    pointer crosses the ABI (CPU tensors are refused too, so this runs here)."""
+    import torch
+    alg = P.Algebra.equal(2, 64, 128)
+    X = torch.zeros(8, 64)
+    W = torch.zeros(64, 128)
+    t = torch.zeros(8, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        P.star_proj_fwd(alg, t, X, W)
+    with pytest.raises(ValueError, match="shape"):
+        P.star_proj_fwd(alg, t, torch.zeros(8, 65), W)
+    with pytest.raises(ValueError, match="shape"):
+        P.star_proj_fwd(alg, t, X, torch.zeros(64, 127))
+    with pytest.raises(TypeError, match="dtype"):
+        P.star_proj_fwd(alg, t, X, W.to(torch.bfloat16))
+    with pytest.raises(TypeError, match="dtype"):
+        P.star_proj_fwd(alg, t.to(torch.int64), X, W)
+    with pytest.raises(ValueError, match="shape"):
+        P.star_proj_fwd(alg, t[:7], X, W)
+    with pytest.raises(ValueError, match="contiguous"):
+        P.star_proj_fwd(alg, t, torch.zeros(64, 8).t(), W)
+    with pytest.raises(ValueError, match="shape"):
+        P.star_proj_bwd_weight(alg, t, X, torch.zeros(8, 64))
+    up, dn = P.Algebra.equal(2, 64, 128), P.Algebra.equal(2, 128, 64)
+    with pytest.raises(TypeError, match="bfloat16"):
+        P.star_decode(up, dn, t, X, [W.to(torch.bfloat16)], None, [W.t().contiguous().to(torch.bfloat16)], None)
 
 
 def test_ffn_rejects_mismatched_widths(P):

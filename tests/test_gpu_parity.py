@@ -449,6 +449,47 @@ def test_decode_one_type_only_skips_blocks(P):
         assert rel_fro(to_host(Y), ref) <= TOL_BF16
 
 
+@pytest.mark.parametrize("path", ["stack_resident", "stack", "per_projection"])
+def test_decode_out_of_range_types(P, path):
+    """A row whose type lies outside [0, q) has an empty support in decode:
+    every layer adds only b_down, so its Y row is X + the sum of the b_down[l]
+    (fp32, in layer order); the other rows match the oracle run on them alone,
+    and the step's status flag is clear.  The three decode kernels: the
+    resident stack (M <= 2), the counter stack, the per-projection kernel
+    (33 layers: more than the stack holds)."""
+    import torch
+    q = 2
+    if path == "stack_resident":
+        D, F, L, t = 256, 512, 3, np.array([1, 7], np.int32)
+    elif path == "stack":
+        D, F, L, t = 256, 512, 3, np.array([0, 1, 5, -1, 1, 0, 2, 0, 1], np.int32)
+    else:
+        D, F, L, t = 128, 256, 33, np.array([0, 1, 5, -1, 1], np.int32)
+    M = t.size
+    up_g, up_o = algs(P, q, [D // 2] * 2, [F // 2] * 2)
+    dn_g, dn_o = algs(P, q, [F // 2] * 2, [D // 2] * 2)
+    seed = 1400 + M
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.05, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 100 + l, (F, D), 0.05, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 200 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 300 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    ws = torch.empty(P.star_workspace_bytes("decode", up_g, dn_g, M), dtype=torch.uint8, device="cuda")
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu],
+                      [f32_dev(b.exact) for b in bu], [to_dev(w) for w in Wd],
+                      [f32_dev(b.exact) for b in bd], "gelu", True, out_dtype=torch.float32, ws=ws)
+    assert not P.star_decode_status(ws)
+    got = to_host(Y)
+    ok = (t >= 0) & (t < q)
+    ref = oracle.decode_stack(up_o, dn_o, t[ok], X.exact[ok], [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(got[ok], ref) <= TOL_BF16
+    h = X.exact[~ok].astype(np.float32)
+    for b in bd:
+        h = (h + b.exact.astype(np.float32)).astype(np.float32)
+    np.testing.assert_allclose(got[~ok], h.astype(np.float64), rtol=1e-6, atol=1e-6)
+
+
 @pytest.mark.parametrize("law", ["star", "dense"])
 @pytest.mark.parametrize("M", [5, 40])
 def test_decode_unequal_groups_q3(P, law, M):
