@@ -222,6 +222,35 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
                         void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * star_decode without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The workspace is a
+ * static device buffer of STAR_DECODE_SCRATCH_BYTES that the library holds
+ * on every device it runs on until the process ends (its address is looked
+ * up on the first call on a device); the call itself allocates nothing and
+ * frees nothing.  Arguments and results as in star_decode, with these
+ * differences:
+ *   status  device int32, 4-byte aligned, or NULL: zeroed by the call, then
+ *           set to 1 if the step was lost to a wait bound (the flag
+ *           star_decode_status reports for star_decode); with NULL the flag
+ *           is kept in the static buffer and not reported
+ * A shape whose star_decode workspace (star_workspace_bytes(STAR_OP_DECODE,
+ * up, down, M)) exceeds STAR_DECODE_SCRATCH_BYTES returns STAR_ERR_WORKSPACE
+ * before anything is launched; every shape the decode kernels take (D, F <=
+ * 4096, M <= 64) fits.  Every call on one device shares that device's
+ * buffer, and each call clears the parts that must start at zero: calls that
+ * overlap in time on one device (other streams, other threads) race and
+ * give unspecified results; calls ordered on one stream do not.
+ */
+#define STAR_DECODE_SCRATCH_BYTES (4u << 20)
+star_status star_decode_noalloc(const star_algebra *up, const star_algebra *down, int32_t n_layers,
+                                int64_t M, const int32_t *row_type, const void *X, star_dtype xt,
+                                const void *const *W_up, const float *const *b_up,
+                                const void *const *W_down, const float *const *b_down, star_act act,
+                                int32_t residual, void *Y, star_dtype yt, int32_t *status,
+                                hipStream_t stream);
+
+/*
  * Whether the last star_decode or star_decode_gated call that used workspace
  * `ws` lost its step to a wait bound (see star_decode): waits for the work
  * queued on `stream` (synchronises it), then writes 1 (Y of that call is

@@ -14,7 +14,7 @@ _EXPORTS = (
     "star_proj_bwd_weight", "star_proj_bwd_weight_planned", "star_proj_fwd",
     "star_proj_fwd_planned", "star_status_string", "star_type_plan", "star_validate_types",
     "star_workspace_bytes", "star_swiglu_fwd", "star_swiglu_bwd", "star_add", "star_swiglu_ffn_fwd",
-    "star_swiglu_ffn_bwd", "star_decode_gated", "star_decode_status",
+    "star_swiglu_ffn_bwd", "star_decode_gated", "star_decode_status", "star_decode_noalloc",
 )
 
 __all__ = list(_EXPORTS)

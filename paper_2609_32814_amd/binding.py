@@ -58,6 +58,8 @@ def _load() -> ctypes.CDLL:
                                       ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
                                       ctypes.POINTER(P), i32, P, E, P, sz, P]
     lib.star_decode_status.argtypes = [P, sz, ctypes.POINTER(i32), P]
+    lib.star_decode_noalloc.argtypes = [A, A, i32, i64, P, P, E, ctypes.POINTER(P), ctypes.POINTER(P),
+                                        ctypes.POINTER(P), ctypes.POINTER(P), E, i32, P, E, P, P]
     lib.star_workspace_bytes.argtypes = [i32, A, A, i64]
     lib.star_workspace_bytes.restype = sz
     lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
@@ -78,7 +80,7 @@ def _load() -> ctypes.CDLL:
                  "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
                  "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add",
-                 "star_decode_gated", "star_decode_status"):
+                 "star_decode_gated", "star_decode_status", "star_decode_noalloc"):
         getattr(lib, name).restype = E
     return lib
 
@@ -468,6 +470,30 @@ def star_decode(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Ten
                            ACTS[act], int(bool(residual)), _ptr(Y), _dt(Y), _ptr(ws), nbytes,
                            _stream(dev)), "star_decode")
     _decode_checked(ws, check, "star_decode")
+    return Y
+
+
+def star_decode_noalloc(up: Algebra, down: Algebra, row_type: torch.Tensor, X: torch.Tensor,
+                        W_ups: Sequence[torch.Tensor], b_ups, W_downs: Sequence[torch.Tensor], b_downs,
+                        act: str = "gelu", residual: bool = True, Y=None, out_dtype=None, status=None):
+    """star_decode on the library's static workspace (the C entry point
+    allocates nothing; this wrapper allocates Y only when none is given).
+    ``status``: a device int32 tensor of one element (or None) that receives
+    the step's wait-bound flag.  Returns Y."""
+    L = len(W_ups)
+    M, dev, Y = _decode_args(up, down, row_type, X, L, Y, out_dtype,
+                             [("W_up", W_ups, (up.K, up.N)), ("W_down", W_downs, (down.K, down.N))],
+                             [("b_up", b_ups, (up.N,)), ("b_down", b_downs, (down.N,))])
+    _opt(status, "status", (1,), _I32, dev)
+    P = ctypes.c_void_p
+    wu = (P * L)(*[t.data_ptr() for t in W_ups])
+    wd = (P * L)(*[t.data_ptr() for t in W_downs])
+    bu = (P * L)(*[t.data_ptr() if t is not None else None for t in b_ups]) if b_ups is not None else None
+    bd = (P * L)(*[t.data_ptr() if t is not None else None for t in b_downs]) if b_downs is not None else None
+    _gpu(dev)
+    _check(LIB.star_decode_noalloc(up.ref, down.ref, L, M, _ptr(row_type), _ptr(X), _dt(X), wu, bu, wd, bd,
+                                   ACTS[act], int(bool(residual)), _ptr(Y), _dt(Y), _ptr(status),
+                                   _stream(dev)), "star_decode_noalloc")
     return Y
 
 

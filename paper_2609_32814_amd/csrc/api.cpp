@@ -19,6 +19,7 @@ namespace {
 using namespace starq;
 
 static_assert(STAR_MAX_Q == kMaxQGroups, "one q limit for the ABI and the kernels");
+static_assert(STAR_DECODE_SCRATCH_BYTES == kDecodeScratchBytes, "one size for the static decode workspace");
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxDim = (int64_t{1} << 30);
@@ -675,7 +676,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
                         const float* const* b_gate, const void* const* W_up, const float* const* b_up,
                         const void* const* W_down, const float* const* b_down, star_act act,
                         int32_t residual, void* Y, star_dtype yt, void* ws, size_t ws_bytes,
-                        hipStream_t stream) {
+                        hipStream_t stream, int32_t* err_word = nullptr) {
   const bool gated = W_gate != nullptr;
   Alg u, d;
   star_status st = check_common(up, M, row_type, u);
@@ -703,6 +704,13 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
   // the gated FFN runs only in the persistent stack
   if (gated && !sp.ok) return STAR_ERR_UNSUPPORTED;
+  // the error flag: the workspace's status line unless the caller gives a
+  // word of its own; zeroed before anything runs
+  int32_t* err = err_word ? err_word : at<int32_t>(ws, 0);
+  if (err_word) {
+    st = hip_status(launch_fill_zero(reinterpret_cast<float*>(err_word), 1, stream));
+    if (st != STAR_OK) return st;
+  }
 
   if (sp.ok) {
     DecodeStack k;
@@ -745,6 +753,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
     k.h = at<float>(ws, sp.h);
     k.part = at<float>(ws, sp.part);
     k.cnt = at<int32_t>(ws, sp.cnt);
+    k.err = err;
     k.tH = sp.resident ? at<uint64_t>(ws, sp.tH) : nullptr;
     k.tpart = sp.resident ? at<uint64_t>(ws, sp.tpart) : nullptr;
     st = hip_status(launch_fill_zero(at<float>(ws, sp.cnt),
@@ -754,8 +763,10 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
   }
 
   // the status line reads zero: the per-projection kernels do not wait
-  st = hip_status(launch_fill_zero(at<float>(ws, 0), kDecodeStatusBytes / sizeof(float), stream));
-  if (st != STAR_OK) return st;
+  if (!err_word) {
+    st = hip_status(launch_fill_zero(at<float>(ws, 0), kDecodeStatusBytes / sizeof(float), stream));
+    if (st != STAR_OK) return st;
+  }
   float* h = at<float>(ws, dw.h);
   uint16_t* xb = at<uint16_t>(ws, dw.xb);
   uint16_t* Hb = at<uint16_t>(ws, dw.H);
@@ -815,6 +826,31 @@ star_status star_decode(const star_algebra* up, const star_algebra* down, int32_
                         hipStream_t stream) {
   return decode_impl(up, down, n_layers, M, row_type, X, xt, nullptr, nullptr, W_up, b_up, W_down, b_down,
                      act, residual, Y, yt, ws, ws_bytes, stream);
+}
+
+star_status star_decode_noalloc(const star_algebra* up, const star_algebra* down, int32_t n_layers,
+                                int64_t M, const int32_t* row_type, const void* X, star_dtype xt,
+                                const void* const* W_up, const float* const* b_up,
+                                const void* const* W_down, const float* const* b_down, star_act act,
+                                int32_t residual, void* Y, star_dtype yt, int32_t* status,
+                                hipStream_t stream) {
+  // the same host-side checks as star_decode, before the scratch is looked up
+  Alg u, d;
+  star_status st = check_common(up, M, row_type, u);
+  if (st != STAR_OK) return st;
+  st = parse_alg(down, d);
+  if (st != STAR_OK) return st;
+  if (M > kDecodeMaxRows || u.K() > kDecodeMaxK || u.N() > kDecodeMaxK) return STAR_ERR_UNSUPPORTED;
+  if (xt != STAR_BF16 || !valid_dtype(yt)) return STAR_ERR_DTYPE;
+  if (status && !aligned4(status)) return STAR_ERR_ALIGN;
+  if (M == 0) return decode_impl(up, down, n_layers, M, row_type, X, xt, nullptr, nullptr, W_up, b_up, W_down,
+                                 b_down, act, residual, Y, yt, nullptr, 0, stream);
+  // a shape whose workspace exceeds the static scratch is refused
+  if (star_workspace_bytes(STAR_OP_DECODE, up, down, M) > kDecodeScratchBytes) return STAR_ERR_WORKSPACE;
+  void* scratch = nullptr;
+  if (decode_scratch(&scratch) != hipSuccess) return STAR_ERR_HIP;
+  return decode_impl(up, down, n_layers, M, row_type, X, xt, nullptr, nullptr, W_up, b_up, W_down, b_down, act,
+                     residual, Y, yt, scratch, kDecodeScratchBytes, stream, status);
 }
 
 star_status star_decode_status(const void* ws, size_t ws_bytes, int32_t* timed_out, hipStream_t stream) {

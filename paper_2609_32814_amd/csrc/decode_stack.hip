@@ -219,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
                         lds + xbytes + 2 * (kmax / SLICE) * 1024};
   // RES: the running state [M][D] fp32
   float* hres = reinterpret_cast<float*>(lds + xbytes + nslots * (kmax / SLICE) * 1024);
-  int32_t* err = p.cnt;
+  int32_t* err = p.err;
   int32_t* cnt_up = p.cnt + kCounterStride;
   int32_t* cnt_dn = cnt_up + kCounterStride * kSubCounters;
   int32_t* tile_cnt = cnt_dn + kCounterStride * kSubCounters;  // one line per down tile

@@ -142,8 +142,9 @@ struct DecodeStack {
   uint16_t* hb;   // [2][M][D] bf16, the next up projection's input (layer parity)
   float* h;       // [M][D] fp32 residual state
   float* part;    // [ns][M][D] fp32 down-projection partial sums
-  int32_t* cnt;   // decode_stack_counters(nt_dn) int32: error flag, up and down arrival
-                  // sub-counters, per-tile down arrivals, each on its own 256-byte line
+  int32_t* cnt;   // decode_stack_counters(nt_dn) int32: (unused) status line, up and down
+                  // arrival sub-counters, per-tile down arrivals, each on its own 256-byte line
+  int32_t* err;   // error flag: set to 1 when a wait runs out (zero at launch)
   // resident kernels only (zero at launch): 64-bit words (tag << 32 | data),
   // the tag being the layer that wrote the word plus one
   uint64_t* tH;     // [M][F / 2] bf16 pairs of H
@@ -166,5 +167,11 @@ bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
+
+// The static workspace of star_decode_noalloc (scratch.hip): its size, and
+// its device address on the current device (looked up on the first call per
+// device, then cached).
+constexpr size_t kDecodeScratchBytes = size_t{4} << 20;
+hipError_t decode_scratch(void** ptr);
 
 }  // namespace starq
