@@ -17,7 +17,11 @@ Q_q with B(i,j) = {i,j}; law ``"dense"`` is the ordinary product; law
 ``"tensor2"`` is the tensor power Q_2^{(x)L} (q = 2^L, appendix "The
 Tensor-Square Candidate"): a type-a row reaches input group b for output group
 d when every bit of b equals that bit of a or of d (L = 2: the pilot's
-36-product law).
+36-product law); law ``"graph"`` is the graph algebra Q_G of a directed graph
+on the q groups (Sec. "Graph Products with Exact Cost"), given as ``edges``, a
+q x q 0/1 matrix (edges[i][j] = 1 for the edge i -> j, diagonal ignored): a
+type-i row's slots are its vertex slot i and the edge slots (i, j) of its
+out-edges, B(i,i) = {i}, B(i,j) = {i, j} for an edge and empty for a non-edge.
 """
 
 from __future__ import annotations
@@ -33,7 +37,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "star_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-LAWS = {"star": 0, "dense": 1, "tensor2": 2}
+LAWS = {"star": 0, "dense": 1, "tensor2": 2, "graph": 3}
 ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2, "silu": 3}
 
 
@@ -60,17 +64,18 @@ def _load():
         i32p = ctypes.POINTER(ctypes.c_int32)
         f64p = ctypes.POINTER(ctypes.c_double)
         i64, i32, f64 = ctypes.c_int64, ctypes.c_int, ctypes.c_double
+        u8p = ctypes.POINTER(ctypes.c_uint8)
         lib.oracle_proj_fwd.restype = i64
-        lib.oracle_proj_fwd.argtypes = [i32, i64p, i64p, i32, i64, i32p, f64p, f64p,
+        lib.oracle_proj_fwd.argtypes = [i32, i64p, i64p, i32, u8p, i64, i32p, f64p, f64p,
                                         f64p, i32, f64p, f64p, i64p]
         lib.oracle_proj_bwd_data.restype = i32
-        lib.oracle_proj_bwd_data.argtypes = [i32, i64p, i64p, i32, i64, i32p, f64p,
+        lib.oracle_proj_bwd_data.argtypes = [i32, i64p, i64p, i32, u8p, i64, i32p, f64p,
                                              f64p, f64p, i32, f64p]
         lib.oracle_proj_bwd_weight.restype = i32
-        lib.oracle_proj_bwd_weight.argtypes = [i32, i64p, i64p, i32, i64, i32p, f64p,
+        lib.oracle_proj_bwd_weight.argtypes = [i32, i64p, i64p, i32, u8p, i64, i32p, f64p,
                                                f64p, f64p, f64p]
         lib.oracle_bwd_weight_entries.restype = i32
-        lib.oracle_bwd_weight_entries.argtypes = [i32, i64p, i64p, i32, i64, i32p,
+        lib.oracle_bwd_weight_entries.argtypes = [i32, i64p, i64p, i32, u8p, i64, i32p,
                                                   f64p, f64p, i64, i64p, i64p, f64p]
         lib.oracle_round_bf16.restype = f64
         lib.oracle_round_bf16.argtypes = [f64]
@@ -81,17 +86,17 @@ def _load():
         lib.oracle_act_grad.restype = f64
         lib.oracle_act_grad.argtypes = [i32, f64]
         lib.oracle_products_per_type.restype = i64
-        lib.oracle_products_per_type.argtypes = [i32, i32, i32]
+        lib.oracle_products_per_type.argtypes = [i32, u8p, i32, i32]
         lib.oracle_row_macs.restype = i64
-        lib.oracle_row_macs.argtypes = [i32, i32, i64p, i64p, i32]
+        lib.oracle_row_macs.argtypes = [i32, u8p, i32, i64p, i64p, i32]
         lib.oracle_square_star.restype = None
         lib.oracle_square_star.argtypes = [i32, i64, f64p, f64p, f64p]
         lib.oracle_square_law.restype = None
-        lib.oracle_square_law.argtypes = [i32, i32, i64, f64p, f64p, f64p]
+        lib.oracle_square_law.argtypes = [i32, u8p, i32, i64, f64p, f64p, f64p]
         lib.oracle_num_threads.restype = i32
         lib.oracle_num_threads.argtypes = []
         lib.oracle_in_support.restype = i32
-        lib.oracle_in_support.argtypes = [i32, i32, i32, i32]
+        lib.oracle_in_support.argtypes = [i32, u8p, i32, i32, i32, i32]
         _lib = lib
     return _lib
 
@@ -112,10 +117,11 @@ class Alg:
     s: tuple
     r: tuple
     law: str = "star"
+    edges: tuple = None  # law "graph": q x q 0/1 rows, edges[i][j] for i -> j
 
     @staticmethod
-    def equal(q: int, K: int, N: int, law: str = "star") -> "Alg":
-        return Alg(q, (K // q,) * q, (N // q,) * q, law)
+    def equal(q: int, K: int, N: int, law: str = "star", edges=None) -> "Alg":
+        return Alg(q, (K // q,) * q, (N // q,) * q, law, _edge_tuple(edges))
 
     @property
     def K(self) -> int:
@@ -129,22 +135,45 @@ class Alg:
         return (np.asarray(self.s, dtype=np.int64), np.asarray(self.r, dtype=np.int64))
 
 
+def _edge_tuple(edges):
+    if edges is None:
+        return None
+    return tuple(tuple(int(bool(v)) for v in row) for row in edges)
+
+
+def _edges(law: str, q: int, edges):
+    """The q x q edge bytes for law "graph" (None for the other laws)."""
+    if law != "graph":
+        return None
+    if edges is None:
+        raise ValueError('law "graph" needs edges')
+    e = np.ascontiguousarray(np.asarray(edges, dtype=np.uint8).reshape(q, q))
+    return e
+
+
+def _alg_edges(alg: Alg):
+    return _edges(alg.law, alg.q, alg.edges)
+
+
 def num_threads() -> int:
     """OpenMP threads the oracle's loops run on."""
     return int(_load().oracle_num_threads())
 
 
-def in_support(law: str, i: int, j: int, k: int) -> bool:
-    return bool(_load().oracle_in_support(LAWS[law], i, j, k))
+def in_support(law: str, i: int, j: int, k: int, q: int = 64, edges=None) -> bool:
+    e = _edges(law, q, edges)
+    return bool(_load().oracle_in_support(LAWS[law], _p(e, ctypes.c_uint8), q, i, j, k))
 
 
-def products_per_type(law: str, q: int, i: int) -> int:
-    return int(_load().oracle_products_per_type(LAWS[law], q, i))
+def products_per_type(law: str, q: int, i: int, edges=None) -> int:
+    e = _edges(law, q, edges)
+    return int(_load().oracle_products_per_type(LAWS[law], _p(e, ctypes.c_uint8), q, i))
 
 
 def row_macs(alg: Alg, i: int) -> int:
     s, r = alg._arrays()
-    return int(_load().oracle_row_macs(LAWS[alg.law], alg.q, _p(s, ctypes.c_int64),
+    e = _alg_edges(alg)
+    return int(_load().oracle_row_macs(LAWS[alg.law], _p(e, ctypes.c_uint8), alg.q, _p(s, ctypes.c_int64),
                                        _p(r, ctypes.c_int64), i))
 
 
@@ -191,7 +220,8 @@ def proj_fwd(alg: Alg, t, X, W, bias=None, act: str = "none", want_z: bool = Fal
     b = _f64(bias) if bias is not None else None
     ppt = np.zeros(alg.q, dtype=np.int64)
     macs = _load().oracle_proj_fwd(alg.q, _p(s, ctypes.c_int64), _p(r, ctypes.c_int64),
-                                   LAWS[alg.law], M, _p(t, ctypes.c_int32),
+                                   LAWS[alg.law], _p(_alg_edges(alg), ctypes.c_uint8), M,
+                                   _p(t, ctypes.c_int32),
                                    _p(X, ctypes.c_double), _p(W, ctypes.c_double),
                                    _p(b, ctypes.c_double), ACTS[act],
                                    _p(Z, ctypes.c_double), _p(Y, ctypes.c_double),
@@ -213,7 +243,8 @@ def proj_bwd_data(alg: Alg, t, dY, W, Zprev=None, act_prev: str = "none"):
     if zp is not None:
         assert zp.shape == (M, alg.K)
     rc = _load().oracle_proj_bwd_data(alg.q, _p(s, ctypes.c_int64), _p(r, ctypes.c_int64),
-                                      LAWS[alg.law], M, _p(t, ctypes.c_int32),
+                                      LAWS[alg.law], _p(_alg_edges(alg), ctypes.c_uint8), M,
+                                   _p(t, ctypes.c_int32),
                                       _p(dY, ctypes.c_double), _p(W, ctypes.c_double),
                                       _p(zp, ctypes.c_double), ACTS[act_prev],
                                       _p(dX, ctypes.c_double))
@@ -232,7 +263,8 @@ def proj_bwd_weight(alg: Alg, t, X, dY):
     dW = np.empty((alg.K, alg.N), dtype=np.float64)
     db = np.empty(alg.N, dtype=np.float64)
     rc = _load().oracle_proj_bwd_weight(alg.q, _p(s, ctypes.c_int64), _p(r, ctypes.c_int64),
-                                        LAWS[alg.law], M, _p(t, ctypes.c_int32),
+                                        LAWS[alg.law], _p(_alg_edges(alg), ctypes.c_uint8), M,
+                                   _p(t, ctypes.c_int32),
                                         _p(X, ctypes.c_double), _p(dY, ctypes.c_double),
                                         _p(dW, ctypes.c_double), _p(db, ctypes.c_double))
     if rc:
@@ -250,7 +282,8 @@ def bwd_weight_entries(alg: Alg, t, X, dY, kk, nn):
     s, r = alg._arrays()
     out = np.empty(kk.size, dtype=np.float64)
     rc = _load().oracle_bwd_weight_entries(alg.q, _p(s, ctypes.c_int64), _p(r, ctypes.c_int64),
-                                           LAWS[alg.law], M, _p(t, ctypes.c_int32),
+                                           LAWS[alg.law], _p(_alg_edges(alg), ctypes.c_uint8), M,
+                                   _p(t, ctypes.c_int32),
                                            _p(X, ctypes.c_double), _p(dY, ctypes.c_double),
                                            kk.size, _p(kk, ctypes.c_int64), _p(nn, ctypes.c_int64),
                                            _p(out, ctypes.c_double))
@@ -270,15 +303,16 @@ def square_star(q: int, bs: int, A, B) -> np.ndarray:
     return C
 
 
-def square_law(law: str, q: int, bs: int, A, B) -> np.ndarray:
+def square_law(law: str, q: int, bs: int, A, B, edges=None) -> np.ndarray:
     """Row-column rule with the law's support: (A*B)_ij = sum over k in
     B(i,j) of A_ik B_kj, for q x q block arrays of b x b blocks."""
     A, B = _f64(A), _f64(B)
     n = q * bs
     assert A.shape == (n, n) and B.shape == (n, n)
     C = np.empty((n, n), dtype=np.float64)
-    _load().oracle_square_law(LAWS[law], q, bs, _p(A, ctypes.c_double), _p(B, ctypes.c_double),
-                              _p(C, ctypes.c_double))
+    e = _edges(law, q, edges)
+    _load().oracle_square_law(LAWS[law], _p(e, ctypes.c_uint8), q, bs, _p(A, ctypes.c_double),
+                              _p(B, ctypes.c_double), _p(C, ctypes.c_double))
     return C
 
 

@@ -35,6 +35,19 @@
  *          g = sum_k g_k 2^k), and a type-a row reaches input group b for
  *          output group d when every bit of b equals the same bit of a or of
  *          d.  L = 1 is Q_2; L = 2 is the pilot's 36-product law.
+ *   law 3 (graph algebra Q_G of a directed graph G on the q groups without
+ *          self-loops; Sec. "Graph Products with Exact Cost", eqs.
+ *          graph-basis-products, graph-product-vertex, graph-product-edge):
+ *          the slots of a type-i row are its vertex slot i and the edge slots
+ *          (i, j) of the edges leaving i.  So B(i,i) = {i}; B(i,j) = {i, j}
+ *          for an edge i -> j; and B(i,j) is empty for a non-edge j != i: that
+ *          output group is not a slot of the row, its product is zero (the
+ *          bias and activation still apply, as everywhere).  edges[i q + j]
+ *          != 0 marks the edge i -> j (the diagonal is ignored).  The
+ *          complete graph is law 0.
+ *
+ * Every routine that takes a law also takes `edges` (q x q bytes, read for
+ * law 3 only; NULL otherwise).
  *
  * Activations: 0 none, 1 GELU with the exact erf form
  * 0.5 z (1 + erf(z / sqrt 2)), 2 GELU with the tanh form, 3 SiLU
@@ -50,6 +63,7 @@
 #define ORACLE_LAW_STAR 0
 #define ORACLE_LAW_DENSE 1
 #define ORACLE_LAW_TENSOR2 2
+#define ORACLE_LAW_GRAPH 3
 
 #define ORACLE_ACT_NONE 0
 #define ORACLE_ACT_GELU 1
@@ -58,9 +72,14 @@
 
 /* k in B(i,j)?  Sec. 5.1: B(i,j) = {i,j} as a set for Q_q; all k for the
  * ordinary product. */
-int oracle_in_support(int law, int i, int j, int k)
+int oracle_in_support(int law, const unsigned char *edges, int q, int i, int j, int k)
 {
     if (law == ORACLE_LAW_DENSE) return 1;
+    if (law == ORACLE_LAW_GRAPH) {
+        if (j == i) return k == i;
+        if (!edges || !edges[i * q + j]) return 0; /* output group j is no slot of a type-i row */
+        return k == i || k == j;                   /* x_i W_ij + x_j W_jj */
+    }
     if (law == ORACLE_LAW_TENSOR2) {
         /* beta_k in {alpha_k, delta_k} for every bit k */
         for (int bit = 0; bit < 30; ++bit) {
@@ -155,23 +174,23 @@ void oracle_round_bf16_array(int64_t n, const double *x, double *y)
 /* Number of block products a type-i row visits in Alg. 1: the pairs (j,k)
  * with k in B(i,j).  2q-1 for Q_q (eq. q-rank counts 2q^2 - q over all q
  * types), q^2 for the ordinary product. */
-int64_t oracle_products_per_type(int law, int q, int i)
+int64_t oracle_products_per_type(int law, const unsigned char *edges, int q, int i)
 {
     int64_t n = 0;
     for (int j = 0; j < q; ++j)
         for (int k = 0; k < q; ++k)
-            n += oracle_in_support(law, i, j, k);
+            n += oracle_in_support(law, edges, q, i, j, k);
     return n;
 }
 
 /* MACs of one type-i row: sum over visited (j,k) of s_k r_j
  * (eq. unequal-row-cost for Q_q: C_i = D_diag + s_i (N - r_i)). */
-int64_t oracle_row_macs(int law, int q, const int64_t *s, const int64_t *r, int i)
+int64_t oracle_row_macs(int law, const unsigned char *edges, int q, const int64_t *s, const int64_t *r, int i)
 {
     int64_t n = 0;
     for (int j = 0; j < q; ++j)
         for (int k = 0; k < q; ++k)
-            if (oracle_in_support(law, i, j, k)) n += s[k] * r[j];
+            if (oracle_in_support(law, edges, q, i, j, k)) n += s[k] * r[j];
     return n;
 }
 
@@ -192,7 +211,7 @@ int64_t oracle_row_macs(int law, int q, const int64_t *s, const int64_t *r, int 
  * number of block products a type-i row visits.  Returns -1 on an
  * out-of-range type.
  */
-int64_t oracle_proj_fwd(int q, const int64_t *s, const int64_t *r, int law,
+int64_t oracle_proj_fwd(int q, const int64_t *s, const int64_t *r, int law, const unsigned char *edges,
                         int64_t M, const int32_t *t,
                         const double *X, const double *W, const double *bias,
                         int act, double *Z_out, double *Y,
@@ -213,10 +232,10 @@ int64_t oracle_proj_fwd(int q, const int64_t *s, const int64_t *r, int law,
         int64_t Mi = 0;
         for (int64_t b = 0; b < M; ++b)
             if (t[b] == i) I[Mi++] = b;                 /* I_i */
-        if (products_per_type) products_per_type[i] = oracle_products_per_type(law, q, i);
+        if (products_per_type) products_per_type[i] = oracle_products_per_type(law, edges, q, i);
         for (int j = 0; j < q; ++j) {
             for (int k = 0; k < q; ++k) {
-                if (!oracle_in_support(law, i, j, k)) continue;
+                if (!oracle_in_support(law, edges, q, i, j, k)) continue;
                 /* Y_j[I_i] += X_k[I_i] W_kj */
                 #pragma omp parallel for schedule(static)
                 for (int64_t m = 0; m < Mi; ++m) {
@@ -259,7 +278,7 @@ int64_t oracle_proj_fwd(int q, const int64_t *s, const int64_t *r, int law,
  * multiplied elementwise by act'(Zprev) (the gradient through the activation
  * that produced this projection's input).  dX is overwritten.
  */
-int oracle_proj_bwd_data(int q, const int64_t *s, const int64_t *r, int law,
+int oracle_proj_bwd_data(int q, const int64_t *s, const int64_t *r, int law, const unsigned char *edges,
                          int64_t M, const int32_t *t,
                          const double *dY, const double *W,
                          const double *Zprev, int act_prev, double *dX)
@@ -278,7 +297,7 @@ int oracle_proj_bwd_data(int q, const int64_t *s, const int64_t *r, int law,
         for (int j = 0; j < q; ++j) {
             const double *yj = dY + b * N + R[j];
             for (int k = 0; k < q; ++k) {
-                if (!oracle_in_support(law, i, j, k)) continue;
+                if (!oracle_in_support(law, edges, q, i, j, k)) continue;
                 double *xk = xb + S[k];
                 for (int64_t e = 0; e < s[k]; ++e) {
                     const double *wrow = W + (S[k] + e) * N + R[j];
@@ -301,7 +320,7 @@ int oracle_proj_bwd_data(int q, const int64_t *s, const int64_t *r, int law,
  * dbias = sum_b ybar_b.  Both are overwritten with the full-batch sum, so a
  * block that no row's support reaches comes out zero.
  */
-int oracle_proj_bwd_weight(int q, const int64_t *s, const int64_t *r, int law,
+int oracle_proj_bwd_weight(int q, const int64_t *s, const int64_t *r, int law, const unsigned char *edges,
                            int64_t M, const int32_t *t,
                            const double *X, const double *dY,
                            double *dW, double *dbias)
@@ -324,7 +343,7 @@ int oracle_proj_bwd_weight(int q, const int64_t *s, const int64_t *r, int law,
             const int i = t[b];
             const double xe = X[b * K + kk];
             for (int j = 0; j < q; ++j) {
-                if (!oracle_in_support(law, i, j, k)) continue;
+                if (!oracle_in_support(law, edges, q, i, j, k)) continue;
                 const double *yj = dY + b * N + R[j];
                 double *dwj = dwrow + R[j];
                 for (int64_t c = 0; c < r[j]; ++c) dwj[c] += xe * yj[c];
@@ -349,7 +368,7 @@ int oracle_proj_bwd_weight(int q, const int64_t *s, const int64_t *r, int law,
  * Written directly from the square rule, independently of the typed
  * projection above.
  */
-void oracle_square_law(int law, int q, int64_t bs, const double *A, const double *B, double *C);
+void oracle_square_law(int law, const unsigned char *edges, int q, int64_t bs, const double *A, const double *B, double *C);
 
 void oracle_square_star(int q, int64_t bs, const double *A, const double *B, double *C)
 {
@@ -377,7 +396,7 @@ void oracle_square_star(int q, int64_t bs, const double *A, const double *B, dou
  * (eqs. vjp-wii, vjp-wij, vjp-wjj).  For checking large shapes, where the
  * full gradient is too slow to form on the CPU.
  */
-int oracle_bwd_weight_entries(int q, const int64_t *s, const int64_t *r, int law,
+int oracle_bwd_weight_entries(int q, const int64_t *s, const int64_t *r, int law, const unsigned char *edges,
                               int64_t M, const int32_t *t,
                               const double *X, const double *dY,
                               int64_t n_entries, const int64_t *kk_idx,
@@ -397,7 +416,7 @@ int oracle_bwd_weight_entries(int q, const int64_t *s, const int64_t *r, int law
         while (n >= R[j + 1]) ++j;
         double acc = 0.0;
         for (int64_t b = 0; b < M; ++b)
-            if (oracle_in_support(law, t[b], j, k)) acc += X[b * K + kk] * dY[b * N + n];
+            if (oracle_in_support(law, edges, q, t[b], j, k)) acc += X[b * K + kk] * dY[b * N + n];
         out[e] = acc;
     }
     return 0;
@@ -422,7 +441,7 @@ int oracle_num_threads(void)
  * For law 0 this is oracle_square_star; the tests check law 2 against the
  * tensor product of two copies of the q = 2 rule.
  */
-void oracle_square_law(int law, int q, int64_t bs, const double *A, const double *B, double *C)
+void oracle_square_law(int law, const unsigned char *edges, int q, int64_t bs, const double *A, const double *B, double *C)
 {
     const int64_t n = q * bs;
     memset(C, 0, sizeof(double) * (size_t)(n * n));
@@ -430,7 +449,7 @@ void oracle_square_law(int law, int q, int64_t bs, const double *A, const double
     for (int i = 0; i < q; ++i)
         for (int j = 0; j < q; ++j)
             for (int k = 0; k < q; ++k) {
-                if (!oracle_in_support(law, i, j, k)) continue;
+                if (!oracle_in_support(law, edges, q, i, j, k)) continue;
                 for (int64_t u = 0; u < bs; ++u)
                     for (int64_t v = 0; v < bs; ++v) {
                         double acc = 0.0;

@@ -734,3 +734,189 @@ def test_gated_decode_stack_is_layers_of_the_gated_ffn():
     got = oracle.decode_stack_gated(up, down, t, X, Ws[0], bs[0], Ws[1], bs[1], Ws[2], bs[2],
                                     mirror_bf16=False)
     np.testing.assert_allclose(got, h, atol=1e-12)
+
+
+# ---- P16: the graph algebra Q_G (Sec. "Graph Products with Exact Cost") -------------
+
+def _random_graph(q, p, seed):
+    """A directed graph on q vertices without self-loops, each edge present
+    with probability p."""
+    g = rng(40, q, seed)
+    E = (g.random((q, q)) < p).astype(np.uint8)
+    np.fill_diagonal(E, 0)
+    return E
+
+
+GRAPHS = [
+    ("path3", np.array([[0, 1, 0], [0, 0, 1], [0, 0, 0]], np.uint8)),
+    ("cycle4", np.array([[0, 1, 0, 0], [0, 0, 1, 0], [0, 0, 0, 1], [1, 0, 0, 0]], np.uint8)),
+    ("star_out4", np.array([[0, 1, 1, 1], [0, 0, 0, 0], [0, 0, 0, 0], [0, 0, 0, 0]], np.uint8)),
+    ("random5", _random_graph(5, 0.45, 1)),
+    ("random6", _random_graph(6, 0.3, 2)),
+]
+
+
+def _graph_table(E):
+    """Nonzero basis products of Q_G from eq. graph-basis-products: vertex
+    slots (i,i) = e_i and edge slots (i,j) = a_ij for the edges i -> j of G,
+    e_i e_i = e_i, e_i a_ij = a_ij, a_ij e_j = a_ij; every other product of
+    basis elements (edge times edge, mismatched indices) vanishes."""
+    q = E.shape[0]
+    slots = [(i, i) for i in range(q)] + [(i, j) for i in range(q) for j in range(q) if E[i, j] and i != j]
+    table = {}
+    for x in slots:
+        for w in slots:
+            if x[0] == x[1] and w[0] == w[1] and x[0] == w[0]:
+                table[(x, w)] = x                      # e_i e_i = e_i
+            elif x[0] == x[1] and w[0] != w[1] and w[0] == x[0]:
+                table[(x, w)] = w                      # e_i a_ij = a_ij
+            elif x[0] != x[1] and w[0] == w[1] and x[1] == w[0]:
+                table[(x, w)] = x                      # a_ij e_j = a_ij
+    return slots, table
+
+
+def _slot_mask(E, bs):
+    q = E.shape[0]
+    m = np.zeros((q * bs, q * bs))
+    for i in range(q):
+        for j in range(q):
+            if i == j or E[i, j]:
+                m[i * bs:(i + 1) * bs, j * bs:(j + 1) * bs] = 1
+    return m
+
+
+def _graph_alg(E, s, r):
+    return Alg(E.shape[0], tuple(s), tuple(r), "graph", tuple(tuple(int(v) for v in row) for row in E))
+
+
+@pytest.mark.parametrize("name,E", GRAPHS)
+def test_graph_bruteforce_structure_constants(name, E):
+    """Square product of Q_G (x) M_b from the basis products, against the
+    oracle's square rule and its typed projection (row block i of A is a
+    type-i token; non-slot blocks of A and W are zero)."""
+    q, bs = E.shape[0], 2
+    slots, table = _graph_table(E)
+    g = rng(41, q)
+    n = q * bs
+    mask = _slot_mask(E, bs)
+    A, B = g.standard_normal((n, n)) * mask, g.standard_normal((n, n)) * mask
+    C = np.zeros((n, n))
+    for (sx, sw), sc in table.items():
+        for u in range(bs):
+            for v in range(bs):
+                a = A[sx[0] * bs + u, sx[1] * bs + v]
+                for z in range(bs):
+                    C[sc[0] * bs + u, sc[1] * bs + z] += a * B[sw[0] * bs + v, sw[1] * bs + z]
+    np.testing.assert_allclose(oracle.square_law("graph", q, bs, A, B, edges=E), C, atol=1e-12)
+    alg = Alg(q, (bs,) * q, (bs,) * q, "graph", tuple(map(tuple, E)))
+    t = np.repeat(np.arange(q), bs).astype(np.int32)
+    Y, _, _, ppt = oracle.proj_fwd(alg, t, A, B)
+    np.testing.assert_allclose(Y, C, atol=1e-12)
+    # the number of basis products is the exact bilinear rank |V| + 2|E| (eq. graph-rank)
+    nE = int(E.sum())
+    assert len(table) == q + 2 * nE
+    assert sum(oracle.products_per_type("graph", q, i, edges=E) for i in range(q)) == q + 2 * nE
+    for i in range(q):
+        assert oracle.products_per_type("graph", q, i, edges=E) == 1 + 2 * int(E[i].sum())
+        assert ppt[i] == 1 + 2 * int(E[i].sum())
+
+
+@pytest.mark.parametrize("name,E", GRAPHS)
+def test_graph_typed_rule_is_masked_dense(name, E):
+    """Independent formulation of the typed rule (eqs. graph-product-vertex,
+    graph-product-edge): Y[I_i] = X[I_i] (W . Mask_i) with Mask_i[kk, n] = 1
+    when group(n) = i and group(kk) = i, or group(n) = j for an edge i -> j
+    and group(kk) in {i, j}; the gradients are the same masked products."""
+    q = E.shape[0]
+    s, r = [2 + (g % 3) for g in range(q)], [3 - (g % 2) for g in range(q)]
+    alg = _graph_alg(E, s, r)
+    gk = np.repeat(np.arange(q), s)
+    gn = np.repeat(np.arange(q), r)
+    g = rng(42, q)
+    M = 23
+    X, W, G = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N)), g.standard_normal((M, alg.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, W)
+    dX = oracle.proj_bwd_data(alg, t, G, W)
+    dW, db = oracle.proj_bwd_weight(alg, t, X, G)
+    Yr, dXr, dWr = np.zeros_like(Y), np.zeros_like(dX), np.zeros_like(dW)
+    for i in range(q):
+        out_ok = (gn == i) | E[i][gn].astype(bool)
+        mask = (out_ok[None, :] & ((gk[:, None] == i) | (gk[:, None] == gn[None, :]))).astype(float)
+        rows = np.nonzero(t == i)[0]
+        Yr[rows] = X[rows] @ (W * mask)
+        dXr[rows] = G[rows] @ (W * mask).T
+        dWr += (X[rows].T @ G[rows]) * mask
+    np.testing.assert_allclose(Y, Yr, atol=1e-12)
+    np.testing.assert_allclose(dX, dXr, atol=1e-12)
+    np.testing.assert_allclose(dW, dWr, atol=1e-12)
+    np.testing.assert_allclose(db, G.sum(0), atol=1e-12)
+
+
+def test_graph_special_cases():
+    """The complete graph is the star law Q_q; the empty graph keeps only the
+    vertex products (a type-i row's output is x_i W_ii in group i, zero in the
+    groups that are not its slots)."""
+    q = 4
+    alg_s = Alg(q, (3, 2, 2, 1), (2, 3, 1, 2), "star")
+    full = np.ones((q, q), np.uint8) - np.eye(q, dtype=np.uint8)
+    g = rng(43)
+    M = 17
+    X, W = g.standard_normal((M, alg_s.K)), g.standard_normal((alg_s.K, alg_s.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    Ys, _, _, _ = oracle.proj_fwd(alg_s, t, X, W)
+    Yg, _, _, _ = oracle.proj_fwd(_graph_alg(full, alg_s.s, alg_s.r), t, X, W)
+    np.testing.assert_array_equal(Yg, Ys)
+    Ye, _, _, _ = oracle.proj_fwd(_graph_alg(np.zeros((q, q), np.uint8), alg_s.s, alg_s.r), t, X, W)
+    S = np.concatenate([[0], np.cumsum(alg_s.s)])
+    R = np.concatenate([[0], np.cumsum(alg_s.r)])
+    ref = np.zeros_like(Ye)
+    for b in range(M):
+        i = t[b]
+        ref[b, R[i]:R[i + 1]] = X[b, S[i]:S[i + 1]] @ W[S[i]:S[i + 1], R[i]:R[i + 1]]
+    np.testing.assert_allclose(Ye, ref, atol=1e-12)
+
+
+@pytest.mark.parametrize("name,E", GRAPHS)
+def test_graph_associativity_unit_composition(name, E):
+    """Q_G is associative and unital (Proposition "Structure"): on slot-
+    supported block arrays (A * B) * C = A * (B * C) and the sum of the
+    vertex identities is the unit; and the typed projection composes,
+    Phi_W2(Phi_W1(X)) = Phi_{W1 * W2}(X), when the inputs' non-slot groups
+    are zero."""
+    q, bs = E.shape[0], 3
+    n = q * bs
+    mask = _slot_mask(E, bs)
+    g = rng(44, q)
+    A, B, C = (g.standard_normal((n, n)) * mask for _ in range(3))
+    sq = lambda P, Q: oracle.square_law("graph", q, bs, P, Q, edges=E)
+    np.testing.assert_allclose(sq(sq(A, B), C), sq(A, sq(B, C)), atol=1e-11)
+    I = np.eye(n)
+    np.testing.assert_allclose(sq(I, B), B, atol=0)
+    np.testing.assert_allclose(sq(A, I), A, atol=0)
+    alg = Alg(q, (bs,) * q, (bs,) * q, "graph", tuple(map(tuple, E)))
+    M = 19
+    t = g.integers(0, q, M).astype(np.int32)
+    X = g.standard_normal((M, n))
+    for b in range(M):  # a type-i token carries only its slots
+        X[b] *= mask[t[b] * bs]
+    W1, W2 = g.standard_normal((n, n)) * mask, g.standard_normal((n, n)) * mask
+    Y1, _, _, _ = oracle.proj_fwd(alg, t, X, W1)
+    Y2, _, _, _ = oracle.proj_fwd(alg, t, Y1, W2)
+    Y12, _, _, _ = oracle.proj_fwd(alg, t, X, sq(W1, W2))
+    np.testing.assert_allclose(Y2, Y12, atol=1e-11)
+
+
+def test_graph_adjoint_identity():
+    E = GRAPHS[3][1]
+    q = E.shape[0]
+    alg = _graph_alg(E, [2, 3, 1, 2, 2], [3, 1, 2, 2, 1])
+    g = rng(45)
+    M = 15
+    X, W, G = g.standard_normal((M, alg.K)), g.standard_normal((alg.K, alg.N)), g.standard_normal((M, alg.N))
+    t = g.integers(0, q, M).astype(np.int32)
+    Y, _, _, _ = oracle.proj_fwd(alg, t, X, W)
+    dX = oracle.proj_bwd_data(alg, t, G, W)
+    dW, _ = oracle.proj_bwd_weight(alg, t, X, G)
+    a, b, c = np.sum(Y * G), np.sum(X * dX), np.sum(W * dW)
+    assert abs(a - b) < 1e-10 * max(1, abs(a)) and abs(a - c) < 1e-10 * max(1, abs(a))
