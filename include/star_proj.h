@@ -88,16 +88,31 @@ typedef enum { STAR_ACT_NONE = 0, STAR_ACT_GELU = 1, STAR_ACT_GELU_TANH = 2 } st
  * group k for output group j when every bit of k equals that bit of i or of
  * j (2^h(i,j) products per output group, 6^L in all).  q must be 1, 2 or 4
  * (STAR_ERR_UNSUPPORTED otherwise); q = 2 is STAR_LAW_STAR, q = 4 the
- * 36-product law of the paper's pretraining pilot. */
-typedef enum { STAR_LAW_STAR = 0, STAR_LAW_DENSE = 1, STAR_LAW_TENSOR2 = 2 } star_law;
+ * 36-product law of the paper's pretraining pilot.  STAR_LAW_GRAPH: the graph
+ * algebra Q_G of a directed graph G without self-loops on the q groups
+ * (Sec. "Graph Products with Exact Cost", eqs. graph-basis-products,
+ * graph-product-vertex, graph-product-edge): a type-i row's slots are its
+ * vertex slot i and the edge slots (i, j) of the edges i -> j, so
+ * B(i,i) = {i}, B(i,j) = {i, j} for an edge, and B(i,j) is empty for a
+ * non-edge j != i: that output group is not a slot of the row and receives
+ * no product (Y = act(bias) there), its input group is never read, and the
+ * weight blocks W_ij of non-edges are not parameters (their gradient is
+ * written as zeros).  A type-i row costs 1 + 2 outdeg(i) block products,
+ * |V| + 2|E| over all types (eq. graph-rank); the complete graph is
+ * STAR_LAW_STAR. */
+typedef enum { STAR_LAW_STAR = 0, STAR_LAW_DENSE = 1, STAR_LAW_TENSOR2 = 2, STAR_LAW_GRAPH = 3 } star_law;
 
 /* An algebra layout.  s and r are host arrays of q widths (input groups,
- * output groups). */
+ * output groups).  edges: for STAR_LAW_GRAPH a host array of q x q bytes,
+ * edges[i * q + j] != 0 for the edge i -> j (the diagonal is ignored), read
+ * during the call only; NULL for the other laws (STAR_ERR_ARG if NULL with
+ * STAR_LAW_GRAPH). */
 typedef struct {
     int32_t q;
     const int64_t *s;
     const int64_t *r;
     star_law law;
+    const uint8_t *edges;
 } star_algebra;
 
 typedef enum {

@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "STAR_OK", 1: "STAR_ERR_ARG", 2: "STAR_ERR_SHAPE", 3: "STAR_E
                 7: "STAR_ERR_HIP"}
 DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 ACTS = {"none": 0, "gelu": 1, "gelu_tanh": 2}
-LAWS = {"star": 0, "dense": 1, "tensor2": 2}
+LAWS = {"star": 0, "dense": 1, "tensor2": 2, "graph": 3}
 OPS = {"fwd": 0, "bwd_data": 1, "bwd_weight": 2, "ffn_fwd": 3, "decode": 4}
 MAX_Q = 64
 
@@ -37,7 +37,8 @@ class StarError(RuntimeError):
 
 class _CAlgebra(ctypes.Structure):
     _fields_ = [("q", ctypes.c_int32), ("s", ctypes.POINTER(ctypes.c_int64)),
-                ("r", ctypes.POINTER(ctypes.c_int64)), ("law", ctypes.c_int)]
+                ("r", ctypes.POINTER(ctypes.c_int64)), ("law", ctypes.c_int),
+                ("edges", ctypes.POINTER(ctypes.c_uint8))]
 
 
 def _load() -> ctypes.CDLL:
@@ -89,23 +90,38 @@ LIB = _load()
 
 
 class Algebra:
-    """q groups of input widths ``s`` and output widths ``r`` under a law."""
+    """q groups of input widths ``s`` and output widths ``r`` under a law;
+    law ``"graph"`` takes ``edges``, a q x q 0/1 matrix (edges[i][j] for the
+    edge i -> j of the graph algebra Q_G; the diagonal is ignored)."""
 
-    def __init__(self, q: int, s: Sequence[int], r: Sequence[int], law: str = "star"):
+    def __init__(self, q: int, s: Sequence[int], r: Sequence[int], law: str = "star", edges=None):
         self.q, self.law = int(q), law
         self.s, self.r = tuple(int(v) for v in s), tuple(int(v) for v in r)
         if len(self.s) != self.q or len(self.r) != self.q:
             raise ValueError("s and r need q entries each")
+        self.edges = None
+        if edges is not None:
+            rows = [[int(bool(v)) for v in row] for row in edges]
+            if len(rows) != self.q or any(len(row) != self.q for row in rows):
+                raise ValueError("edges must be a q x q matrix")
+            self.edges = tuple(tuple(row) for row in rows)
+        if law == "graph" and self.edges is None:
+            raise ValueError('law "graph" needs edges')
         self._s = (ctypes.c_int64 * self.q)(*self.s)
         self._r = (ctypes.c_int64 * self.q)(*self.r)
+        self._e = None
+        if self.edges is not None:
+            self._e = (ctypes.c_uint8 * (self.q * self.q))(*[v for row in self.edges for v in row])
         self._c = _CAlgebra(self.q, ctypes.cast(self._s, ctypes.POINTER(ctypes.c_int64)),
-                            ctypes.cast(self._r, ctypes.POINTER(ctypes.c_int64)), LAWS[law])
+                            ctypes.cast(self._r, ctypes.POINTER(ctypes.c_int64)), LAWS[law],
+                            ctypes.cast(self._e, ctypes.POINTER(ctypes.c_uint8)) if self._e is not None
+                            else None)
 
     @classmethod
-    def equal(cls, q: int, K: int, N: int, law: str = "star") -> "Algebra":
+    def equal(cls, q: int, K: int, N: int, law: str = "star", edges=None) -> "Algebra":
         if K % q or N % q:
             raise ValueError("equal groups need q | K and q | N")
-        return cls(q, [K // q] * q, [N // q] * q, law)
+        return cls(q, [K // q] * q, [N // q] * q, law, edges)
 
     @property
     def K(self) -> int:
@@ -120,7 +136,7 @@ class Algebra:
         return ctypes.byref(self._c)
 
     def with_law(self, law: str) -> "Algebra":
-        return Algebra(self.q, self.s, self.r, law)
+        return Algebra(self.q, self.s, self.r, law, self.edges)
 
     def __repr__(self):
         return f"Algebra(q={self.q}, s={self.s}, r={self.r}, law={self.law!r})"

@@ -34,6 +34,8 @@ struct Alg {
   int law = 0;
   int64_t S[kMaxQGroups + 1];  // input group starts
   int64_t R[kMaxQGroups + 1];  // output group starts
+  uint64_t adj[kMaxQGroups] = {};     // law 3: bit j of adj[i] for the edge i -> j
+  uint64_t adj_in[kMaxQGroups] = {};  // law 3: bit i of adj_in[j] for the edge i -> j
   int64_t K() const { return S[q]; }
   int64_t N() const { return R[q]; }
   int64_t s(int g) const { return S[g + 1] - S[g]; }
@@ -41,15 +43,22 @@ struct Alg {
 };
 
 // k in B(i, j) for the law (host side of the kernels' rule)
-bool host_in_support(int law, int i, int j, int k) {
-  if (law == STAR_LAW_TENSOR2) return ((k ^ i) & (k ^ j)) == 0;
-  return law == STAR_LAW_DENSE || k == i || k == j;
+bool host_in_support(const Alg& a, int i, int j, int k) {
+  if (a.law == STAR_LAW_TENSOR2) return ((k ^ i) & (k ^ j)) == 0;
+  if (a.law == STAR_LAW_GRAPH) {
+    if (j == i) return k == i;
+    return ((a.adj[i] >> j) & 1ull) && (k == i || k == j);
+  }
+  return a.law == STAR_LAW_DENSE || k == i || k == j;
 }
 
 star_status parse_alg(const star_algebra* a, Alg& out) {
   if (!a || !a->s || !a->r) return STAR_ERR_ARG;
   if (a->q < 1 || a->q > kMaxQGroups) return STAR_ERR_ARG;
-  if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE && a->law != STAR_LAW_TENSOR2) return STAR_ERR_ARG;
+  if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE && a->law != STAR_LAW_TENSOR2 &&
+      a->law != STAR_LAW_GRAPH)
+    return STAR_ERR_ARG;
+  if (a->law == STAR_LAW_GRAPH && !a->edges) return STAR_ERR_ARG;
   // the tensor power needs q = 2^L; the kernels take every contraction as
   // at most two contiguous group ranges, which holds for L <= 2
   if (a->law == STAR_LAW_TENSOR2 && a->q != 1 && a->q != 2 && a->q != 4) return STAR_ERR_UNSUPPORTED;
@@ -63,6 +72,14 @@ star_status parse_alg(const star_algebra* a, Alg& out) {
     out.R[g + 1] = out.R[g] + a->r[g];
     if (out.S[g + 1] > kMaxDim || out.R[g + 1] > kMaxDim) return STAR_ERR_SHAPE;
   }
+  for (int g = 0; g < kMaxQGroups; ++g) out.adj[g] = out.adj_in[g] = 0;
+  if (a->law == STAR_LAW_GRAPH)
+    for (int i = 0; i < a->q; ++i)
+      for (int j = 0; j < a->q; ++j)
+        if (i != j && a->edges[i * a->q + j]) {  // the diagonal is ignored
+          out.adj[i] |= 1ull << j;
+          out.adj_in[j] |= 1ull << i;
+        }
   return STAR_OK;
 }
 
@@ -244,6 +261,8 @@ StackPlan stack_plan(const Alg& u, const Alg& d, int64_t M, int n_layers, bool g
   sp.end = cur;
   bool same_groups = u.q == d.q && u.law == d.law;
   for (int g = 0; same_groups && g <= u.q; ++g) same_groups = d.S[g] == u.R[g] && d.R[g] == u.S[g];
+  // one support table for both projections (the graph law: the same graph)
+  for (int g = 0; same_groups && g < u.q; ++g) same_groups = u.adj[g] == d.adj[g];
   sp.ok = M >= 1 && M <= kDecodeMaxRows && n_layers <= kStackMaxLayers && same_groups &&
           decode_stack_smem(static_cast<int>(M), kmax, static_cast<int>(D), sp.ns, gated) > 0 &&
           sp.grid <= cu_count();
@@ -271,6 +290,10 @@ void fill_common(GemmParams& p, const Alg& a, int64_t M, int elem, const int32_t
   for (int g = 0; g <= a.q; ++g) {
     p.S[g] = static_cast<int32_t>(a.S[g]);
     p.R[g] = static_cast<int32_t>(a.R[g]);
+  }
+  for (int g = 0; g < kMaxQGroups; ++g) {
+    p.adj[g] = a.adj[g];
+    p.adj_in[g] = a.adj_in[g];
   }
   p.nsplit = 1;
 }
@@ -336,7 +359,10 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
   const int nw = kFp32NW;
   fill_tiles(p.NTp, a.R, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_proj_gemm(kModeFwd, p, nw, upper, stream));
+  star_status st = hip_status(launch_proj_gemm(kModeFwd, p, nw, upper, stream));
+  // graph law: the output groups that are not slots of a row's type
+  if (st == STAR_OK && a.law == STAR_LAW_GRAPH) st = hip_status(launch_graph_fill(kModeFwd, p, stream));
+  return st;
 }
 
 star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a) {
@@ -396,7 +422,7 @@ star_status star_count_products(const star_algebra* alg, int64_t* per_type) {
   for (int i = 0; i < a.q; ++i) {
     int64_t n = 0;
     for (int j = 0; j < a.q; ++j)
-      for (int k = 0; k < a.q; ++k) n += host_in_support(a.law, i, j, k) ? 1 : 0;
+      for (int k = 0; k < a.q; ++k) n += host_in_support(a, i, j, k) ? 1 : 0;
     per_type[i] = n;
   }
   return STAR_OK;
@@ -412,7 +438,7 @@ star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_typ
     int64_t row = 0;
     for (int j = 0; j < a.q; ++j)
       for (int k = 0; k < a.q; ++k)
-        if (host_in_support(a.law, i, j, k)) row += a.s(k) * a.r(j);
+        if (host_in_support(a, i, j, k)) row += a.s(k) * a.r(j);
     total += rows_per_type[i] * row;
   }
   *macs = total;
@@ -513,7 +539,10 @@ star_status star_proj_bwd_data_planned(const star_algebra* alg, int64_t M, const
   const int nw = kFp32NW;
   fill_tiles(p.NTp, a.S, a.q, 64 * nw);
   const int64_t upper = rows_upper * static_cast<int64_t>(p.NTp[a.q]);
-  return hip_status(launch_proj_gemm(kModeBwdData, p, nw, upper, stream));
+  st = hip_status(launch_proj_gemm(kModeBwdData, p, nw, upper, stream));
+  // graph law: zero gradient for the input groups that are not slots
+  if (st == STAR_OK && a.law == STAR_LAW_GRAPH) st = hip_status(launch_graph_fill(kModeBwdData, p, stream));
+  return st;
 }
 
 star_status star_proj_bwd_data(const star_algebra* alg, int64_t M, const int32_t* row_type,
@@ -555,7 +584,8 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
     return STAR_ERR_ALIGN;
   const BwdWs bw = bwd_weight_layout(a, M);
   const bool pipelined = xt == STAR_BF16;
-  if ((pipelined || bw.nsplit > 1) && M > 0 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
+  const bool need_ws = pipelined || bw.nsplit > 1 || (a.law == STAR_LAW_GRAPH && dbias);
+  if (need_ws && M > 0 && (!ws || ws_bytes < bw.end)) return STAR_ERR_WORKSPACE;
   if (ws && !aligned16(ws)) return STAR_ERR_ALIGN;
   // M = 0 still defines the output: an empty sum
   if (M == 0) {
@@ -596,7 +626,9 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   p.A = X;
   p.B = dY;
   p.dW = dW;
-  p.dbias = dbias;
+  // the graph law's diagonal tiles do not contract over every row, so its
+  // bias gradient is summed apart (below)
+  p.dbias = a.law == STAR_LAW_GRAPH ? nullptr : dbias;
   p.nsplit = bw.nsplit;
   if (bw.nsplit > 1) {
     p.partial = at<float>(ws, bw.partial);
@@ -604,8 +636,14 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   }
   const int64_t upper = static_cast<int64_t>(p.MTp[a.q]) * p.NTp[a.q] * p.nsplit;
   st = hip_status(launch_gemm(kModeBwdWeight, p, kBwdWeightNW, persistent_grid(upper), stream));
-  if (st != STAR_OK || bw.nsplit == 1) return st;
-  return hip_status(launch_split_reduce(p, stream));
+  if (st == STAR_OK && bw.nsplit > 1) st = hip_status(launch_split_reduce(p, stream));
+  if (st != STAR_OK || a.law != STAR_LAW_GRAPH || !dbias) return st;
+  const int32_t chunk = static_cast<int32_t>((M + kColSumChunks - 1) / kColSumChunks);
+  float* cs = at<float>(ws, bw.colsum);
+  st = hip_status(launch_column_sum_f32(static_cast<const float*>(dY), p.N, p.perm, p.offsets, a.q, p.M, chunk,
+                                        kColSumChunks, cs, stream));
+  if (st != STAR_OK) return st;
+  return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
 }
 
 star_status star_proj_bwd_weight(const star_algebra* alg, int64_t M, const int32_t* row_type,
@@ -735,6 +773,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
     fill_tiles(k.NTu, u.R, u.q, kDecodeTileN);
     fill_tiles(k.NTd, d.R, d.q, kDecodeTileN);
     k.types = row_type;
+    for (int g = 0; g < kMaxQGroups; ++g) k.adj[g] = u.adj[g];
     k.X = static_cast<const uint16_t*>(X);
     for (int l = 0; l < n_layers; ++l) {
       k.Wu[l] = static_cast<const uint16_t*>(W_up[l]);
@@ -782,6 +821,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
       p.R[g] = static_cast<int32_t>(a.R[g]);
     }
     fill_tiles(p.NTp, a.R, a.q, kDecodeTileN);
+    for (int g = 0; g < kMaxQGroups; ++g) p.adj[g] = a.adj[g];
     p.types = row_type;
     p.act = act;
     p.residual = residual;

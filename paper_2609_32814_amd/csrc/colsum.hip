@@ -9,14 +9,15 @@ namespace starq {
 namespace {
 
 // part[c][n] = sum over rows [c * chunk, (c + 1) * chunk) of the rows of
-// valid type of the bf16 matrix src [M][N].  When every row has a valid type
+// valid type of the bf16 (or fp32) matrix src [M][N].  When every row has a valid type
 // (offsets[q] == M) the rows are taken in their own order (contiguous
 // reads); otherwise in type-sorted order, row perm[position] for positions
 // below offsets[q].  A block covers 256 columns: thread (g, r) adds 8
 // columns (one 16-byte load per row) over rows r, r + 8, ... of the chunk in
 // order, then the 8 row lanes are added in order through LDS, so the result
 // does not depend on scheduling.
-__global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restrict__ src, int32_t N,
+template <typename T>
+__global__ __launch_bounds__(256) void column_sum_kernel(const T* __restrict__ src, int32_t N,
                                                          const int32_t* __restrict__ perm,
                                                          const int32_t* __restrict__ offsets, int q,
                                                          int32_t M, int32_t chunk, float* __restrict__ part) {
@@ -31,11 +32,18 @@ __global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restr
   if (n0 < N) {
     for (int32_t r = r0 + rl; r < r1; r += 8) {
       const int32_t row = natural ? r : perm[r];
-      const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row) * N + n0);
-      sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
-      sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
-      sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
-      sum[6] += bf16_to_f32(v.w & 0xffffu); sum[7] += bf16_to_f32(v.w >> 16);
+      if constexpr (sizeof(T) == 2) {
+        const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row) * N + n0);
+        sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
+        sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
+        sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
+        sum[6] += bf16_to_f32(v.w & 0xffffu); sum[7] += bf16_to_f32(v.w >> 16);
+      } else {
+        const float4 a = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(row) * N + n0);
+        const float4 b = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(row) * N + n0 + 4);
+        sum[0] += a.x; sum[1] += a.y; sum[2] += a.z; sum[3] += a.w;
+        sum[4] += b.x; sum[5] += b.y; sum[6] += b.z; sum[7] += b.w;
+      }
     }
   }
 #pragma unroll
@@ -54,7 +62,14 @@ __global__ __launch_bounds__(256) void column_sum_kernel(const uint16_t* __restr
 
 hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm, const int32_t* offsets,
                              int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream) {
-  hipLaunchKernelGGL(column_sum_kernel, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
+  hipLaunchKernelGGL(column_sum_kernel<uint16_t>, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
+                     N, perm, offsets, q, M, chunk, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_column_sum_f32(const float* src, int32_t N, const int32_t* perm, const int32_t* offsets,
+                                 int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream) {
+  hipLaunchKernelGGL(column_sum_kernel<float>, dim3((N + 255) / 256, nchunks), dim3(256), 0, stream, src,
                      N, perm, offsets, q, M, chunk, part);
   return hipGetLastError();
 }

@@ -135,9 +135,16 @@ __device__ __forceinline__ void settle_all(const uint64_t* const (&src)[N], uint
 }
 
 // k in B(i, j): law 0 {i, j}; law 1 every group; law 2 (tensor power of
-// the two-group law) every bit of k equal to that bit of i or of j
-__device__ __forceinline__ bool in_support(int law, int i, int j, int k) {
+// the two-group law) every bit of k equal to that bit of i or of j; law 3
+// (graph algebra, bit j of adj[i] for the edge i -> j) {i} for j = i, {i, j}
+// for an edge, nothing otherwise
+__device__ __forceinline__ bool in_support(int law, const uint64_t* adj, int i, int j, int k) {
   if (law == 2) return ((k ^ i) & (k ^ j)) == 0;
+  if (law == 3) {
+    // graph algebra: B(i,i) = {i}, B(i,j) = {i, j} for an edge i -> j, empty otherwise
+    if (j == i) return k == i;
+    return ((adj[i] >> j) & 1ull) && (k == i || k == j);
+  }
   return law == 1 || k == i || k == j;
 }
 __device__ __forceinline__ int group_of(const int32_t* starts, int q, int32_t x) {
@@ -237,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
       const int t = lane < M ? p.types[lane] : -1;
       const bool valid = t >= 0 && t < p.q;
       for (int g = 0; g < p.q; ++g) {
-        const unsigned long long m = __ballot(valid && in_support(p.law, t, it.j, g));
+        const unsigned long long m = __ballot(valid && in_support(p.law, p.adj, t, it.j, g));
         if (lane == 0) rowmask_s[slot][g] = m;
       }
     }

@@ -347,8 +347,7 @@ __global__ __launch_bounds__(THREADS, 1) void star_gemm_kernel(const GemmParams 
   // stage s of tile t into the loader registers
   auto load_stage = [&](const Tile& t, const Rows<UPT>& r, int32_t s) {
     int32_t k0, kend;
-    if (s < t.n0) { k0 = t.seg0_lo + s * BK; kend = t.seg0_hi; }
-    else { k0 = t.seg1_lo + (s - t.n0) * BK; kend = t.seg1_hi; }
+    step_range<MODE, LAW, BK>(p, t, p.offsets, s, k0, kend);
     if constexpr (MODE == kModeFwd) {
       la.load(Ag, p.K, r.a, k0, kend);
       lb.load(Bg, p.N, k0, t.cstart, t.cend, [&](int32_t k) { return k < kend ? k : -1; });
@@ -548,22 +547,26 @@ __global__ void fill_zero_kernel(float* __restrict__ dst, int64_t n) {
     dst[i] = 0.f;
 }
 
-template <typename T, int MODE, int WN>
-hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
+template <typename T, int MODE, int WN, int LAW>
+hipError_t launch_law(const GemmParams& p, int grid, hipStream_t stream) {
   using G = Geo<WN>;
-  auto kern = p.law == 1 ? star_gemm_kernel<T, MODE, 1, WN>
-                         : (p.law == 2 ? star_gemm_kernel<T, MODE, 2, WN> : star_gemm_kernel<T, MODE, 0, WN>);
+  auto kern = star_gemm_kernel<T, MODE, LAW, WN>;
   // allow more than the default dynamic LDS (once per kernel and device)
-  static std::atomic<unsigned long long> lds_set[3] = {{0}, {0}, {0}};
-  hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 0, WN>), lds_set[0],
-                                     G::SMEM);
-  if (attr == hipSuccess)
-    attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 1, WN>), lds_set[1], G::SMEM);
-  if (attr == hipSuccess)
-    attr = ensure_lds_limit(reinterpret_cast<const void*>(star_gemm_kernel<T, MODE, 2, WN>), lds_set[2], G::SMEM);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(kern), lds_set, G::SMEM);
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(THREADS), G::SMEM, stream, p);
   return hipGetLastError();
+}
+
+template <typename T, int MODE, int WN>
+hipError_t launch_typed(const GemmParams& p, int grid, hipStream_t stream) {
+  switch (p.law) {
+    case 1: return launch_law<T, MODE, WN, 1>(p, grid, stream);
+    case 2: return launch_law<T, MODE, WN, 2>(p, grid, stream);
+    case 3: return launch_law<T, MODE, WN, 3>(p, grid, stream);
+    default: return launch_law<T, MODE, WN, 0>(p, grid, stream);
+  }
 }
 
 // fp32 operands only: bf16 operands run in the pipelined kernel.

@@ -309,13 +309,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       }
       rows_from_lds = false;
     }
-    if (ls < lt.n0) {
-      sk0 = lt.seg0_lo + ls * BK;
-      skend = lt.seg0_hi;
-    } else {
-      sk0 = lt.seg1_lo + (ls - lt.n0) * BK;
-      skend = lt.seg1_hi;
-    }
+    step_range<MODE, LAW, BK>(p, lt, offs_s, ls, sk0, skend);
     if constexpr (MODE == kModeBwdWeight) {
       if (!((pok >> (lstg & 1)) & 1u)) {
         // the rows of this stage were not copied ahead (first stage, or the
@@ -360,15 +354,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         // reader was the previous step's copies)
         int32_t nlo = 0, nhi = 0;
         bool next = false;
-        // positions of step st of tile t (segment 0, then segment 1)
-        auto stage_range = [](const Tile& t, int32_t st, int32_t& lo, int32_t& hi) {
-          if (st < t.n0) {
-            lo = t.seg0_lo + st * BK;
-            hi = t.seg0_hi;
-          } else {
-            lo = t.seg1_lo + (st - t.n0) * BK;
-            hi = t.seg1_hi;
-          }
+        // positions of step st of tile t
+        auto stage_range = [&](const Tile& t, int32_t st, int32_t& lo, int32_t& hi) {
+          step_range<MODE, LAW, BK>(p, t, offs_s, st, lo, hi);
         };
         if (ls + 1 < lt.nsteps) {
           stage_range(lt, ls + 1, nlo, nhi);
@@ -734,6 +722,7 @@ hipError_t launch_act(const GemmParams& p, int64_t upper, int cus, hipStream_t s
 
 template <int MODE>
 hipError_t launch_async(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
+  if (p.law == 3) return launch_act<MODE, 3>(p, upper, cus, stream);
   if (p.law == 2) return launch_act<MODE, 2>(p, upper, cus, stream);
   return p.law == 1 ? launch_act<MODE, 1>(p, upper, cus, stream)
                     : launch_act<MODE, 0>(p, upper, cus, stream);
@@ -746,10 +735,14 @@ int gemm_async_tile_n() { return BN; }
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream) {
   if (mode == kModeFwd) return launch_async<kModeFwd>(p, upper_tiles, cus, stream);
-  if (mode == kModeBwdWeight)
-    return p.law == 1 ? launch_one<kModeBwdWeight, 1, kActNone>(p, upper_tiles, cus, stream)
-                      : (p.law == 2 ? launch_one<kModeBwdWeight, 2, kActNone>(p, upper_tiles, cus, stream)
-                                    : launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream));
+  if (mode == kModeBwdWeight) {
+    switch (p.law) {
+      case 1: return launch_one<kModeBwdWeight, 1, kActNone>(p, upper_tiles, cus, stream);
+      case 2: return launch_one<kModeBwdWeight, 2, kActNone>(p, upper_tiles, cus, stream);
+      case 3: return launch_one<kModeBwdWeight, 3, kActNone>(p, upper_tiles, cus, stream);
+      default: return launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream);
+    }
+  }
   return launch_async<kModeBwdData>(p, upper_tiles, cus, stream);
 }
 

@@ -40,7 +40,7 @@ __device__ __forceinline__ uint32_t word_of(const uint4& r, int w) {
   return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
 }
 
-enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3, kSelTensor = 4 };
+enum Sel : int { kSelNone = 0, kSelOnly = 1, kSelExcept = 2, kSelAll = 3, kSelTensor = 4, kSelGraph = 10 };
 
 // Law 2, the tensor power of the two-group law (q = 2^L): input group k is
 // in B(i, j) when every bit of k equals that bit of i or of j.
@@ -76,12 +76,78 @@ __device__ __forceinline__ void mask_ranges(uint32_t m, int& lo0, int& hi0, int&
   hi1 = lo1 + __builtin_ctz(~(rest >> lo1));
 }
 
+// Law 3, the graph algebra Q_G (bit j of p.adj[i] marks the edge i -> j): a
+// type-i row's slots are its vertex slot i and the edge slots of its
+// out-edges, so B(i,i) = {i}, B(i,j) = {i, j} for an edge i -> j and B(i,j)
+// is empty for a non-edge.  Bit x set when x is in the contraction of a tile
+// of class i and C-column group j, as for tensor_mask.
+__device__ __forceinline__ uint64_t graph_mask(const GemmParams& p, int mode, int i, int j) {
+  const uint64_t bi = 1ull << i, bj = 1ull << j;
+  const bool edge = (p.adj[i] >> j) & 1ull;
+  if (mode == kModeFwd) return j == i ? bi : (edge ? (bi | bj) : 0ull);
+  if (mode == kModeBwdData) return j == i ? (bi | p.adj[i]) : (edge ? bj : 0ull);
+  // weight gradient (C rows input group i, columns output group j): the row
+  // types x whose B(x, j) holds i: for i = j, j itself and every x with an
+  // edge x -> j; for i != j, i itself if it has the edge i -> j
+  return i == j ? (bj | p.adj_in[j]) : (edge ? bi : 0ull);
+}
+// law 3: pass 0 holds the tiles that contract over two or more groups, pass 1
+// those over one; tiles over none are in no pass (their outputs are not
+// slots: launch_graph_fill writes them) except in the weight gradient,
+// whose pass 1 holds them (they are written as zeros)
+__device__ __forceinline__ bool graph_in_pass(const GemmParams& p, int sel, int i, int j) {
+  const int mode = (sel - kSelGraph) >> 1, pass = (sel - kSelGraph) & 1;
+  const int n = __popcll(graph_mask(p, mode, i, j));
+  return pass == 0 ? n >= 2 : (n == 1 || (n == 0 && mode == kModeBwdWeight));
+}
+
+// Law 3: the contraction of a tile is the concatenation, in group order, of
+// the ranges [bound(x), bound(x + 1)) of the groups x in `mask` (bound: input
+// group starts, output group starts or type offsets), cut to positions
+// [c0, c1) of that concatenation; a K step never straddles two groups.
+template <int BK, typename BF>
+__device__ __forceinline__ int32_t graph_steps(uint64_t mask, BF bound, int32_t c0, int32_t c1) {
+  int32_t steps = 0, cum = 0;
+  while (mask) {
+    const int x = __builtin_ctzll(mask);
+    mask &= mask - 1;
+    const int32_t lo = bound(x), len = bound(x + 1) - lo;
+    const int32_t a = max(cum, c0), b = min(cum + len, c1);
+    if (b > a) steps += (b - a + BK - 1) / BK;
+    cum += len;
+  }
+  return steps;
+}
+template <int BK, typename BF>
+__device__ __forceinline__ void graph_step_range(uint64_t mask, BF bound, int32_t c0, int32_t c1, int32_t st,
+                                                 int32_t& lo_out, int32_t& hi_out) {
+  int32_t cum = 0;
+  lo_out = hi_out = 0;
+  while (mask) {
+    const int x = __builtin_ctzll(mask);
+    mask &= mask - 1;
+    const int32_t lo = bound(x), len = bound(x + 1) - lo;
+    const int32_t a = max(cum, c0), b = min(cum + len, c1);
+    if (b > a) {
+      const int32_t n = (b - a + BK - 1) / BK;
+      if (st < n) {
+        lo_out = lo + (a - cum) + st * BK;
+        hi_out = lo + (b - cum);
+        return;
+      }
+      st -= n;
+    }
+    cum += len;
+  }
+}
+
 // A pass selects, per class, the C-column groups of its tiles: the star
 // law puts the tiles with two K segments first, the dense law has one pass;
 // law 2 puts the tiles that contract over more than half of the groups
 // first, with the mode folded into the selector.
 __device__ __forceinline__ int sel_for(int mode, int law, int pass) {
   if (law == 1) return pass == 0 ? kSelAll : kSelNone;
+  if (law == 3) return kSelGraph + 2 * mode + pass;
   if (law == 2) return kSelTensor + 2 * mode + pass;
   if (mode == kModeFwd) return pass == 0 ? kSelExcept : kSelOnly;
   return pass == 0 ? kSelOnly : kSelExcept;  // BWD_DATA and BWD_WEIGHT
@@ -98,6 +164,12 @@ __device__ __forceinline__ bool tensor_in_pass(const GemmParams& p, int sel, int
 __device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
   const int nti = p.NTp[i + 1] - p.NTp[i];
   const int nt = p.NTp[p.q];
+  if (sel >= kSelGraph) {
+    int n = 0;
+    for (int j = 0; j < p.q; ++j)
+      if (graph_in_pass(p, sel, i, j)) n += p.NTp[j + 1] - p.NTp[j];
+    return n;
+  }
   if (sel >= kSelTensor) {
     int n = 0;
     for (int j = 0; j < p.q; ++j)
@@ -115,6 +187,15 @@ __device__ __forceinline__ int ncols_sel(const GemmParams& p, int sel, int i) {
 __device__ __forceinline__ int col_tile_global(const GemmParams& p, int sel, int i, int c) {
   if (sel == kSelOnly) return p.NTp[i] + c;
   if (sel == kSelExcept) return c < p.NTp[i] ? c : c + (p.NTp[i + 1] - p.NTp[i]);
+  if (sel >= kSelGraph) {
+    for (int j = 0; j < p.q; ++j) {
+      if (!graph_in_pass(p, sel, i, j)) continue;
+      const int ntj = p.NTp[j + 1] - p.NTp[j];
+      if (c < ntj) return p.NTp[j] + c;
+      c -= ntj;
+    }
+    return p.NTp[p.q];  // not reached: c < ncols_sel
+  }
   if (sel >= kSelTensor) {
     // the c-th column tile over the pass's groups, in group order
     for (int j = 0; j < p.q; ++j) {
@@ -221,7 +302,7 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.mt = ru;
     t.cstart = p.R[cg] + nt * BN;
     t.cend = p.R[cg + 1];
-    if (LAW == 1) {
+    if (LAW == 1 || LAW == 3) {
       t.seg0_lo = 0; t.seg0_hi = p.K;
     } else if (LAW == 2) {
       int a0, a1, b0, b1;
@@ -241,7 +322,7 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
       mask_ranges(tensor_mask(kModeBwdData, p.q, cls, cg), a0, a1, b0, b1);
       t.seg0_lo = p.R[a0]; t.seg0_hi = p.R[a1];
       t.seg1_lo = p.R[b0]; t.seg1_hi = p.R[b1];
-    } else if (LAW == 1 || cg == cls) {
+    } else if (LAW == 1 || LAW == 3 || cg == cls) {
       t.seg0_lo = 0; t.seg0_hi = p.N;
     } else {
       t.seg0_lo = p.R[cg]; t.seg0_hi = p.R[cg + 1];
@@ -263,6 +344,8 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
       b0 = offs[tb0]; b1 = offs[tb1];
     } else if (LAW == 0 && cg != cls) {
       a0 = offs[cls]; a1 = offs[cls + 1];
+    } else if (LAW == 3) {
+      a0 = a1 = 0;  // set below from the graph mask
     } else {
       a0 = 0; a1 = offs[p.q];
     }
@@ -279,14 +362,70 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.pos0 = offs[cls] + t.mt * bm;
     t.nrows = min(bm, offs[cls + 1] - t.pos0);
   }
-  t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
-  t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;
+  if constexpr (LAW == 3) {
+    // the graph law: seg0 holds the contraction's group mask, seg1 the
+    // positions [c0, c1) of its concatenated ranges this tile covers (all
+    // of them, or the split's chunk for the weight gradient)
+    const uint64_t m = graph_mask(p, MODE, cls, cg);
+    int32_t total = 0, c0 = 0, c1 = 0;
+    auto count = [&](auto bound) {
+      for (uint64_t r = m; r; r &= r - 1) {
+        const int x = __builtin_ctzll(r);
+        total += bound(x + 1) - bound(x);
+      }
+      if (MODE == kModeBwdWeight) {
+        const int32_t cs = (total + p.nsplit - 1) / p.nsplit;
+        c0 = min(total, t.split * cs);
+        c1 = min(total, c0 + cs);
+      } else {
+        c1 = total;
+      }
+      t.nsteps = graph_steps<BK>(m, bound, c0, c1);
+    };
+    if constexpr (MODE == kModeFwd) count([&](int x) { return p.S[x]; });
+    else if constexpr (MODE == kModeBwdData) count([&](int x) { return p.R[x]; });
+    else count([&](int x) { return offs[x]; });
+    t.seg0_lo = static_cast<int32_t>(static_cast<uint32_t>(m));
+    t.seg0_hi = static_cast<int32_t>(static_cast<uint32_t>(m >> 32));
+    t.seg1_lo = c0;
+    t.seg1_hi = c1;
+    t.n0 = 0;
+    // the bias gradient sums every row; the graph law's diagonal blocks do
+    // not contract over all of them, so it is summed apart
+    t.do_dbias = 0;
+  } else {
+    t.n0 = (t.seg0_hi - t.seg0_lo + BK - 1) / BK;
+    t.nsteps = t.n0 + (t.seg1_hi - t.seg1_lo + BK - 1) / BK;
+  }
   // every field is uniform over the workgroup: keep it in scalar registers
   int32_t* f = reinterpret_cast<int32_t*>(&t);
 #pragma unroll
   for (int k = 0; k < static_cast<int>(sizeof(Tile) / sizeof(int32_t)); ++k)
     f[k] = __builtin_amdgcn_readfirstlane(f[k]);
   return t;
+}
+
+// K range of step st of tile t: [lo, ...) with the end of its segment in hi
+// (offs: the type offsets, for the weight gradient's positions).
+template <int MODE, int LAW, int BK>
+__device__ __forceinline__ void step_range(const GemmParams& p, const Tile& t, const int32_t* offs, int32_t st,
+                                           int32_t& lo, int32_t& hi) {
+  if constexpr (LAW == 3) {
+    const uint64_t m = static_cast<uint64_t>(static_cast<uint32_t>(t.seg0_lo)) |
+                       (static_cast<uint64_t>(static_cast<uint32_t>(t.seg0_hi)) << 32);
+    if constexpr (MODE == kModeFwd)
+      graph_step_range<BK>(m, [&](int x) { return p.S[x]; }, t.seg1_lo, t.seg1_hi, st, lo, hi);
+    else if constexpr (MODE == kModeBwdData)
+      graph_step_range<BK>(m, [&](int x) { return p.R[x]; }, t.seg1_lo, t.seg1_hi, st, lo, hi);
+    else
+      graph_step_range<BK>(m, [&](int x) { return offs[x]; }, t.seg1_lo, t.seg1_hi, st, lo, hi);
+  } else if (st < t.n0) {
+    lo = t.seg0_lo + st * BK;
+    hi = t.seg0_hi;
+  } else {
+    lo = t.seg1_lo + (st - t.n0) * BK;
+    hi = t.seg1_hi;
+  }
 }
 
 }  // namespace gemm

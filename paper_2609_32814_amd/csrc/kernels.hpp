@@ -20,7 +20,7 @@ enum GemmMode : int { kModeFwd = 0, kModeBwdData = 1, kModeBwdWeight = 2 };
 // column-tile prefix NTp over the column groups of C are host-computed.
 struct GemmParams {
   int32_t q;
-  int32_t law;  // 0 star, 1 dense
+  int32_t law;  // 0 star, 1 dense, 2 tensor power, 3 graph
   int32_t M;
   int32_t K;
   int32_t N;
@@ -47,6 +47,10 @@ struct GemmParams {
   float* partial;     // [nsplit][K][N] when nsplit > 1
   float* dbias_part;  // [nsplit][N] when nsplit > 1
   int32_t nsplit;
+  // law 3 (graph algebra): bit j of adj[i] marks the edge i -> j, bit i of
+  // adj_in[j] the same edge (so adj_in[j] holds the in-neighbours of j)
+  uint64_t adj[kMaxQGroups];
+  uint64_t adj_in[kMaxQGroups];
 };
 
 hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* perm,
@@ -67,6 +71,16 @@ int gemm_async_tile_n();
 // else in type-sorted order (row perm[position], positions below offsets[q]).
 hipError_t launch_column_sum(const uint16_t* src, int32_t N, const int32_t* perm, const int32_t* offsets,
                              int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream);
+// The same for an fp32 src.
+hipError_t launch_column_sum_f32(const float* src, int32_t N, const int32_t* perm, const int32_t* offsets,
+                                 int q, int32_t M, int32_t chunk, int nchunks, float* part, hipStream_t stream);
+// Law 3 (graph algebra): the output blocks of a forward or activation-gradient
+// product that no row's support reaches: for each row of valid type i, the
+// columns of every C-column group j that is not a slot of a type-i row
+// (forward: output groups j != i with no edge i -> j, written act(bias) and,
+// if p.Z, bias; activation gradient: input groups k != i with no edge i -> k,
+// written 0).  Every other element of the output is the GEMM's.
+hipError_t launch_graph_fill(int mode, const GemmParams& p, hipStream_t stream);
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream);
 // Gated FFN elementwise parts (swiglu.hip); n a multiple of 8, elem 1 bf16
@@ -116,6 +130,7 @@ struct DecodePhase {
   float* h_out;           // down: new running state [M][N] (fp32), or null
   void* Y;                // down, last layer: final output, or null
   int32_t ydtype;
+  uint64_t adj[kMaxQGroups];  // law 3: bit j of adj[i] marks the edge i -> j
 };
 
 // The whole decode stack in one persistent launch (see decode_stack.hip).
@@ -149,6 +164,7 @@ struct DecodeStack {
   // the tag being the layer that wrote the word plus one
   uint64_t* tH;     // [M][F / 2] bf16 pairs of H
   uint64_t* tpart;  // [2][ns][M][D] fp32 down partial sums, by layer parity
+  uint64_t adj[kMaxQGroups];  // law 3: bit j of adj[i] marks the edge i -> j
 };
 // Arrival counters: each sits alone on a 256-byte line (kCounterStride ints).
 constexpr int kCounterStride = 64;

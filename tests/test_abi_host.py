@@ -175,3 +175,29 @@ def test_tensor_power_law_counts_and_limits(P):
     assert P.star_count_macs(a, rows) == sum(n * oracle.row_macs(oa, i) for i, n in enumerate(rows))
     with pytest.raises(RuntimeError):
         P.star_count_products(P.Algebra.equal(8, 64, 64, "tensor2"))
+
+
+def test_graph_law_counts_and_arguments(P):
+    """Law "graph": per-type products 1 + 2 outdeg(i) (eq. graph-rank: |V| +
+    2|E| over all types), MACs from the same support, and the ABI refuses the
+    law without an edge matrix."""
+    import numpy as np
+    import oracle
+    E = np.array([[0, 1, 1, 0], [0, 0, 0, 1], [1, 0, 0, 0], [0, 0, 0, 0]], np.uint8)
+    a = P.Algebra(4, [8, 16, 24, 8], [16, 8, 8, 32], "graph", E)
+    per = P.star_count_products(a)
+    assert per == [1 + 2 * int(E[i].sum()) for i in range(4)]
+    assert sum(per) == 4 + 2 * int(E.sum())
+    oa = oracle.Alg(4, a.s, a.r, "graph", tuple(map(tuple, E)))
+    rows = [5, 0, 7, 3]
+    assert P.star_count_macs(a, rows) == sum(n * oracle.row_macs(oa, i) for i, n in enumerate(rows))
+    # the diagonal of the edge matrix is ignored
+    E2 = E.copy()
+    np.fill_diagonal(E2, 1)
+    assert P.star_count_products(P.Algebra(4, a.s, a.r, "graph", E2)) == per
+    # no edge matrix: STAR_ERR_ARG from the ABI itself
+    bare = P.binding._CAlgebra(a._c.q, a._c.s, a._c.r, 3, None)
+    out = (ctypes.c_int64 * 4)()
+    assert P.binding.LIB.star_count_products(ctypes.byref(bare), out) == 1
+    with pytest.raises(ValueError):
+        P.Algebra(2, [8, 8], [8, 8], "graph")
