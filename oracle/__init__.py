@@ -97,6 +97,13 @@ def _load():
         lib.oracle_num_threads.argtypes = []
         lib.oracle_in_support.restype = i32
         lib.oracle_in_support.argtypes = [i32, u8p, i32, i32, i32, i32]
+        lib.oracle_attn_in_group.restype = i32
+        lib.oracle_attn_in_group.argtypes = [i32, i32, i32, i32]
+        lib.oracle_attn_fwd.restype = i32
+        lib.oracle_attn_fwd.argtypes = [i32, i32, i64, i32, i32, i64, i64, i32p, f64p, f64p, f64p, f64p]
+        lib.oracle_attn_decode.restype = i32
+        lib.oracle_attn_decode.argtypes = [i32, i32, i64, i32, i32, i64, i64, i32p, i32p, f64p, f64p, f64p,
+                                           f64p]
         _lib = lib
     return _lib
 
@@ -431,3 +438,49 @@ def decode_stack_gated(up: Alg, down: Alg, t, X, W_gates, b_gates, W_ups, b_ups,
         f, _, _, _ = proj_fwd(down, t, H, Wd, bd, "none")
         h = h + f if residual else f
     return h
+
+
+# ---- algebraic attention ------------------------------------------------------
+
+
+def attn_in_group(law: str, i: int, j: int, a: int) -> bool:
+    """Whether feature group a is in F(i, j) (eqs. feature-set,
+    tensor-square-feature-set)."""
+    return bool(_load().oracle_attn_in_group(LAWS[law], i, j, a))
+
+
+def attn_fwd(q: int, law: str, m: int, n_heads: int, n_kv: int, B: int, S: int, pos_type, Q, K, V):
+    """Causal attention with the algebraic score (Alg. attention-training,
+    forward): Q [B S, n_heads q m], K and V [B S, n_kv q m], token-major;
+    pos_type[p] is the type of position p.  Returns O like Q."""
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    pt = np.ascontiguousarray(pos_type, dtype=np.int32)
+    dh = q * m
+    assert Q.shape == (B * S, n_heads * dh) and K.shape == (B * S, n_kv * dh) and V.shape == K.shape
+    assert pt.shape == (S,)
+    O = np.empty_like(Q)
+    st = _load().oracle_attn_fwd(q, LAWS[law], m, n_heads, n_kv, B, S, _p(pt, ctypes.c_int32), _p(Q, ctypes.c_double),
+                                 _p(K, ctypes.c_double), _p(V, ctypes.c_double), _p(O, ctypes.c_double))
+    if st != 0:
+        raise ValueError("bad attention arguments (type out of range or head counts)")
+    return O
+
+
+def attn_decode(q: int, law: str, m: int, n_heads: int, n_kv: int, pos_type, cache_len, Q, K_cache, V_cache):
+    """One decode step (Alg. attention-decoding): Q [B, n_heads q m]; the
+    caches [B, S_max, n_kv q m] hold cache_len[b] positions of sequence b,
+    whose query is at position cache_len[b] - 1.  Returns O [B, n_heads q m]."""
+    Q, Kc, Vc = _f64(Q), _f64(K_cache), _f64(V_cache)
+    pt = np.ascontiguousarray(pos_type, dtype=np.int32)
+    cl = np.ascontiguousarray(cache_len, dtype=np.int32)
+    B, S_max = Kc.shape[0], Kc.shape[1]
+    dh = q * m
+    assert Q.shape == (B, n_heads * dh) and Kc.shape == (B, S_max, n_kv * dh) and Vc.shape == Kc.shape
+    assert pt.shape == (S_max,) and cl.shape == (B,)
+    O = np.empty_like(Q)
+    st = _load().oracle_attn_decode(q, LAWS[law], m, n_heads, n_kv, B, S_max, _p(pt, ctypes.c_int32),
+                                    _p(cl, ctypes.c_int32), _p(Q, ctypes.c_double), _p(Kc, ctypes.c_double),
+                                    _p(Vc, ctypes.c_double), _p(O, ctypes.c_double))
+    if st != 0:
+        raise ValueError("bad attention arguments")
+    return O

@@ -459,3 +459,135 @@ void oracle_square_law(int law, const unsigned char *edges, int q, int64_t bs, c
             }
     #undef BLK
 }
+
+/* ---- algebraic attention (appendix "Attention Extension and Detailed Cost
+ * Accounting") ------------------------------------------------------------
+ *
+ * One head of width d_h = q m is split into q groups of width m.  A query at
+ * position p (type i = tau(p)) and a key at position u (type j = tau(u))
+ * meet on the feature groups F(i,j) (eq. feature-set): {i} if i = j, else
+ * {i, j} for the star law; every group for the dense law (ordinary
+ * attention); for the tensor power, every beta whose bits each equal the
+ * bit of i or of j (eq. tensor-square-feature-set).  The raw score is the
+ * sum over a in F(i,j) of <Q_p^(a), K_u^(a)> (eq. attention-raw-score), the
+ * score divides it by sqrt(|F(i,j)| m) (eqs. attention-support-size,
+ * attention-score), keys after the query are masked (eq. causal-mask), and
+ * the output is the softmax-weighted sum of the full value vectors
+ * (eq. softmax-pv: dense value aggregation).
+ *
+ * Layouts: token-major rows, head h at columns [h d_h, (h+1) d_h), group a of
+ * a head at [a m, (a+1) m) within it.  Head h reads key/value head
+ * h / (n_heads / n_kv) (grouped-query attention).
+ */
+int oracle_attn_in_group(int law, int i, int j, int a)
+{
+    if (law == ORACLE_LAW_DENSE) return 1;
+    if (law == ORACLE_LAW_TENSOR2) {
+        for (int bit = 0; bit < 30; ++bit) {
+            const int b = (a >> bit) & 1, x = (i >> bit) & 1, y = (j >> bit) & 1;
+            if (b != x && b != y) return 0;
+        }
+        return 1;
+    }
+    return a == i || a == j;
+}
+
+/* score of query row qr (type i) and key row kr (type j) of one head pair */
+static double attn_score(int law, int q, int64_t m, int i, int j, const double *qr, const double *kr)
+{
+    double r = 0.0;
+    int nf = 0;
+    for (int a = 0; a < q; ++a) {
+        if (!oracle_attn_in_group(law, i, j, a)) continue;
+        ++nf;
+        for (int64_t c = 0; c < m; ++c) r += qr[a * m + c] * kr[a * m + c];
+    }
+    return r / sqrt((double)nf * (double)m);
+}
+
+/* Causal attention over B sequences of S positions (Alg. attention-training,
+ * forward): Q [B S, n_heads d_h], K, V [B S, n_kv d_h], O [B S, n_heads d_h];
+ * pos_type[p] is the type of position p.  Returns 0, or -1 for an
+ * out-of-range type or a head count that does not divide. */
+int oracle_attn_fwd(int q, int law, int64_t m, int n_heads, int n_kv, int64_t B, int64_t S,
+                    const int32_t *pos_type, const double *Q, const double *K, const double *V, double *O)
+{
+    if (n_kv <= 0 || n_heads % n_kv) return -1;
+    for (int64_t p = 0; p < S; ++p)
+        if (pos_type[p] < 0 || pos_type[p] >= q) return -1;
+    const int64_t dh = q * m, ldq = n_heads * dh, ldk = n_kv * dh;
+    const int group = n_heads / n_kv;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int h = 0; h < n_heads; ++h) {
+            const int hk = h / group;
+            double *s = (double *)malloc(sizeof(double) * (size_t)S);
+            for (int64_t p = 0; p < S; ++p) {
+                const double *qr = Q + (b * S + p) * ldq + h * dh;
+                double mx = -INFINITY;
+                for (int64_t u = 0; u <= p; ++u) {
+                    s[u] = attn_score(law, q, m, pos_type[p], pos_type[u], qr, K + (b * S + u) * ldk + hk * dh);
+                    if (s[u] > mx) mx = s[u];
+                }
+                double den = 0.0;
+                for (int64_t u = 0; u <= p; ++u) {
+                    s[u] = exp(s[u] - mx);
+                    den += s[u];
+                }
+                double *o = O + (b * S + p) * ldq + h * dh;
+                for (int64_t c = 0; c < dh; ++c) o[c] = 0.0;
+                for (int64_t u = 0; u <= p; ++u) {
+                    const double w = s[u] / den;
+                    const double *vr = V + (b * S + u) * ldk + hk * dh;
+                    for (int64_t c = 0; c < dh; ++c) o[c] += w * vr[c];
+                }
+            }
+            free(s);
+        }
+    return 0;
+}
+
+/* One decode step (Alg. attention-decoding): sequence b has cache_len[b]
+ * cached positions 0..cache_len[b]-1 (the new token's key and value already
+ * appended) and its query is at position cache_len[b] - 1.  Q [B, n_heads
+ * d_h]; K_cache, V_cache [B, S_max, n_kv d_h]; O [B, n_heads d_h]. */
+int oracle_attn_decode(int q, int law, int64_t m, int n_heads, int n_kv, int64_t B, int64_t S_max,
+                       const int32_t *pos_type, const int32_t *cache_len, const double *Q,
+                       const double *Kc, const double *Vc, double *O)
+{
+    if (n_kv <= 0 || n_heads % n_kv) return -1;
+    const int64_t dh = q * m, ldq = n_heads * dh, ldk = n_kv * dh;
+    const int group = n_heads / n_kv;
+    for (int64_t b = 0; b < B; ++b) {
+        if (cache_len[b] < 1 || cache_len[b] > S_max) return -1;
+        for (int64_t u = 0; u < cache_len[b]; ++u)
+            if (pos_type[u] < 0 || pos_type[u] >= q) return -1;
+    }
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int h = 0; h < n_heads; ++h) {
+            const int hk = h / group;
+            const int64_t L = cache_len[b], p = L - 1;
+            double *s = (double *)malloc(sizeof(double) * (size_t)L);
+            const double *qr = Q + b * ldq + h * dh;
+            double mx = -INFINITY;
+            for (int64_t u = 0; u < L; ++u) {
+                s[u] = attn_score(law, q, m, pos_type[p], pos_type[u], qr, Kc + (b * S_max + u) * ldk + hk * dh);
+                if (s[u] > mx) mx = s[u];
+            }
+            double den = 0.0;
+            for (int64_t u = 0; u < L; ++u) {
+                s[u] = exp(s[u] - mx);
+                den += s[u];
+            }
+            double *o = O + b * ldq + h * dh;
+            for (int64_t c = 0; c < dh; ++c) o[c] = 0.0;
+            for (int64_t u = 0; u < L; ++u) {
+                const double w = s[u] / den;
+                const double *vr = Vc + (b * S_max + u) * ldk + hk * dh;
+                for (int64_t c = 0; c < dh; ++c) o[c] += w * vr[c];
+            }
+            free(s);
+        }
+    return 0;
+}

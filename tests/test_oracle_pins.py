@@ -920,3 +920,94 @@ def test_graph_adjoint_identity():
     dW, _ = oracle.proj_bwd_weight(alg, t, X, G)
     a, b, c = np.sum(Y * G), np.sum(X * dX), np.sum(W * dW)
     assert abs(a - b) < 1e-10 * max(1, abs(a)) and abs(a - c) < 1e-10 * max(1, abs(a))
+
+
+# ---- P17: algebraic attention (appendix "Attention Extension") -------------------------
+
+def _dense_causal_attention(Q, K, V, S, scale):
+    """Textbook causal softmax attention of one head for one sequence."""
+    s = (Q @ K.T) * scale
+    s[np.triu_indices(S, 1)] = -np.inf
+    s -= s.max(1, keepdims=True)
+    P = np.exp(s)
+    P /= P.sum(1, keepdims=True)
+    return P @ V
+
+
+def test_attention_dense_law_is_ordinary_attention():
+    """With every group in the support the score is the standard
+    <Q_p, K_u> / sqrt(d_h) and the oracle is ordinary causal attention."""
+    q, m, S = 4, 8, 13
+    g = rng(50)
+    Q, K, V = (g.standard_normal((S, q * m)) for _ in range(3))
+    pt = (np.arange(S) % q).astype(np.int32)
+    O = oracle.attn_fwd(q, "dense", m, 1, 1, 1, S, pt, Q, K, V)
+    np.testing.assert_allclose(O, _dense_causal_attention(Q, K, V, S, 1 / np.sqrt(q * m)), atol=1e-12)
+    # q = 1 under the star law is the same ordinary attention with 1/sqrt(m)
+    O1 = oracle.attn_fwd(1, "star", q * m, 1, 1, 1, S, np.zeros(S, np.int32), Q, K, V)
+    np.testing.assert_allclose(O1, _dense_causal_attention(Q, K, V, S, 1 / np.sqrt(q * m)), atol=1e-12)
+
+
+@pytest.mark.parametrize("law,q", [("star", 2), ("star", 3), ("tensor2", 4)])
+def test_attention_raw_score_is_the_typed_product(law, q):
+    """The raw score of a type-i query and a type-j key is the (query, key)
+    entry of Q *_q K^T (the block identity stated with eq.
+    attention-raw-score): computed here through the (pinned) projection
+    oracle with X = Q and W = K^T, its output groups the keys of each type.
+    The values are one-hot on the positions, so the output row of query p
+    is its softmax row, whose log-ratios give the scores; those must equal
+    the typed product divided by sqrt(|F(i,j)| m)."""
+    m = 6
+    S = q * m  # V_u = e_u needs d_h = q m >= S
+    g = rng(51, q)
+    Q, K = g.standard_normal((S, q * m)), g.standard_normal((S, q * m))
+    V = np.eye(S)
+    pt = np.array([(5 * p + 1) % q for p in range(S)], np.int32)  # a non-cyclic schedule
+    O = oracle.attn_fwd(q, law, m, 1, 1, 1, S, pt, Q, K, V)
+    order = np.argsort(pt, kind="stable")
+    widths = tuple(int((pt == j).sum()) for j in range(q))
+    alg = Alg(q, (m,) * q, widths, law)
+    R, _, _, _ = oracle.proj_fwd(alg, pt, Q, K[order].T)
+    raw = np.empty((S, S))
+    raw[:, order] = R
+    nf = np.array([[sum(oracle.attn_in_group(law, i, j, a) for a in range(q)) for j in range(q)] for i in range(q)])
+    score = raw / np.sqrt(nf[pt][:, pt] * m)
+    for p in range(1, S):
+        lr = np.log(O[p, :p + 1]) - np.log(O[p, 0])
+        np.testing.assert_allclose(lr, score[p, :p + 1] - score[p, 0], atol=1e-9)
+        assert np.all(O[p, p + 1:] == 0)  # causal
+    # star law: |F(i,i)| = 1 and |F(i,j)| = 2 (eq. attention-support-size)
+    if law == "star":
+        assert all(nf[i, i] == 1 for i in range(q))
+        assert all(nf[i, j] == 2 for i in range(q) for j in range(q) if i != j)
+
+
+def test_attention_causality_gqa_and_decode():
+    """A query's output ignores later keys and values (Proposition
+    "Causality"); head h reads key/value head h // (n_heads / n_kv); and one
+    decode step over a cache of L positions is row L - 1 of the forward."""
+    q, m, B, S, nh, nkv = 2, 8, 2, 11, 4, 2
+    dh = q * m
+    g = rng(52)
+    Q = g.standard_normal((B * S, nh * dh))
+    K = g.standard_normal((B * S, nkv * dh))
+    V = g.standard_normal((B * S, nkv * dh))
+    pt = (np.arange(S) % q).astype(np.int32)
+    O = oracle.attn_fwd(q, "star", m, nh, nkv, B, S, pt, Q, K, V)
+    K2, V2 = K.copy(), V.copy()
+    K2[S + 7:2 * S] += 3.0
+    V2[S + 7:2 * S] -= 5.0
+    O2 = oracle.attn_fwd(q, "star", m, nh, nkv, B, S, pt, Q, K2, V2)
+    np.testing.assert_array_equal(O2[:S + 7], O[:S + 7])
+    assert not np.allclose(O2[S + 7:], O[S + 7:])
+    for h in range(nh):
+        hk = h // (nh // nkv)
+        Oh = oracle.attn_fwd(q, "star", m, 1, 1, B, S, pt, Q[:, h * dh:(h + 1) * dh],
+                             K[:, hk * dh:(hk + 1) * dh], V[:, hk * dh:(hk + 1) * dh])
+        np.testing.assert_allclose(O[:, h * dh:(h + 1) * dh], Oh, atol=1e-13)
+    L = np.array([5, 11], np.int32)
+    Kc, Vc = K.reshape(B, S, -1), V.reshape(B, S, -1)
+    Qd = np.stack([Q[b * S + L[b] - 1] for b in range(B)])
+    Od = oracle.attn_decode(q, "star", m, nh, nkv, pt, L, Qd, Kc, Vc)
+    for b in range(B):
+        np.testing.assert_allclose(Od[b], O[b * S + L[b] - 1], atol=1e-13)
