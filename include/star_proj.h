@@ -378,6 +378,85 @@ star_status star_swiglu_bwd(int64_t n, const void *dH, const void *Z_gate, const
 star_status star_add(int64_t n, const void *a, const void *b, star_dtype dt, void *out,
                      hipStream_t stream);
 
+/*
+ * Algebraic attention (appendix "Attention Extension and Detailed Cost
+ * Accounting"; Algs. attention-training and attention-decoding, their score
+ * and aggregation steps).  Each head of width d_h = q m is split into q
+ * feature groups of width m.  For a query at position p of type i and a key
+ * at position u <= p of type j, the score keeps the groups a in F(i, j):
+ *
+ *     s_pu = sum over a in F(i, j) of <Q_p^(a), K_u^(a)> / sqrt(|F(i, j)| m)
+ *
+ * (eqs. feature-set, attention-raw-score, attention-support-size,
+ * attention-score), with F(i, i) = {i}, F(i, j) = {i, j} for STAR_LAW_STAR,
+ * every group for STAR_LAW_DENSE (ordinary attention with the 1/sqrt(d_h)
+ * rule: the same-code control), and the groups whose every bit equals that
+ * bit of i or of j for STAR_LAW_TENSOR2 (eq. tensor-square-feature-set,
+ * q = 1, 2 or 4).  Keys after the query are masked (eq. causal-mask); the
+ * output is the softmax-weighted sum of the full value rows (eq. softmax-pv).
+ * Softmax and accumulation run in fp32; the probabilities enter the value
+ * product rounded to bf16.
+ *
+ * Layouts (row-major, token-major): Q and O hold [batch][seq_len][n_heads]
+ * [head_dim], K and V [batch][seq_len][n_kv_heads][head_dim]; query head h
+ * uses key/value head h / (n_heads / n_kv_heads) (grouped-query attention).
+ * Group a of a head is its features [a m, (a + 1) m).  Q, K and V are BF16,
+ * O is F32 or BF16; every tensor pointer 16-byte aligned.  STAR_LAW_GRAPH is
+ * not defined for attention (STAR_ERR_UNSUPPORTED).
+ */
+typedef struct {
+    int32_t batch;       /* sequences B (0: no-op) */
+    int32_t seq_len;     /* forward: positions S per sequence; decode: cache capacity */
+    int32_t n_heads;     /* query heads */
+    int32_t n_kv_heads;  /* key/value heads, dividing n_heads */
+    int32_t head_dim;    /* d_h: 64 or 128 (STAR_ERR_UNSUPPORTED otherwise) */
+    int32_t q;           /* groups per head; m = head_dim / q a multiple of 8 */
+    star_law law;
+} star_attn_shape;
+
+/* Causal forward over whole sequences (training or prefill).
+ *   plan  device plan of the position types, built by
+ *         star_type_plan(q, seq_len, pos_type, ...) from device
+ *         int32 pos_type[seq_len], the type of each position (the same for
+ *         every sequence).  A position whose type lies outside [0, q) is
+ *         neither a query nor a key and its output rows are not written.
+ *   lse   device float[batch][n_heads][seq_len] or NULL: the natural
+ *         log-sum-exp of each query's scaled scores (the softmax
+ *         normaliser a backward pass needs).
+ * Errors: STAR_ERR_ARG (null pointer, bad law), STAR_ERR_SHAPE (a size
+ * below zero, n_kv_heads not dividing n_heads, a grid too large),
+ * STAR_ERR_UNSUPPORTED (head_dim, q or m outside the supported set),
+ * STAR_ERR_DTYPE, STAR_ERR_ALIGN. */
+star_status star_attn_fwd(const star_attn_shape *shape, const void *plan, const void *Q,
+                          const void *K, const void *V, star_dtype dt, void *O, star_dtype ot,
+                          float *lse, hipStream_t stream);
+
+/* One decode step over a KV cache (Alg. attention-decoding): one new query
+ * row per sequence, attending to the cached keys and values at positions
+ * 0 .. cache_len[b] - 1, the last of which is the query's own position (its
+ * key and value already appended by the caller).  The cache keeps every
+ * feature of every key (eq. kv-cache-shape): a later query of another type
+ * reads other groups of the same key.
+ *   shape->seq_len  the cache capacity S_max
+ *   pos_type   device int32[S_max]: the type of each cache position
+ *   cache_len  device int32[batch]: valid cache entries per sequence; values
+ *              above S_max count as S_max; a sequence with cache_len <= 0,
+ *              or whose query position has a type outside [0, q), gets a zero
+ *              output row.  Cached keys of a type outside [0, q) are skipped.
+ *   Q          device [batch][n_heads][head_dim], BF16
+ *   K_cache, V_cache  device [batch][S_max][n_kv_heads][head_dim], BF16
+ *   O          device [batch][n_heads][head_dim] of dtype ot
+ *   ws         device workspace of star_attn_decode_workspace_bytes(shape)
+ *              bytes: the per-chunk partial results.
+ * The cache is split into chunks of 128 (head_dim 64) or 64 (head_dim 128)
+ * positions, each read once for the up to 8 query heads of one key/value
+ * head that one workgroup serves; a second kernel merges the chunks. */
+size_t star_attn_decode_workspace_bytes(const star_attn_shape *shape);
+star_status star_attn_decode(const star_attn_shape *shape, const int32_t *pos_type,
+                             const int32_t *cache_len, const void *Q, const void *K_cache,
+                             const void *V_cache, star_dtype dt, void *O, star_dtype ot, void *ws,
+                             size_t ws_bytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *star_status_string(star_status s);
 

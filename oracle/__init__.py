@@ -100,7 +100,7 @@ def _load():
         lib.oracle_attn_in_group.restype = i32
         lib.oracle_attn_in_group.argtypes = [i32, i32, i32, i32]
         lib.oracle_attn_fwd.restype = i32
-        lib.oracle_attn_fwd.argtypes = [i32, i32, i64, i32, i32, i64, i64, i32p, f64p, f64p, f64p, f64p]
+        lib.oracle_attn_fwd.argtypes = [i32, i32, i64, i32, i32, i64, i64, i32p, f64p, f64p, f64p, f64p, f64p]
         lib.oracle_attn_decode.restype = i32
         lib.oracle_attn_decode.argtypes = [i32, i32, i64, i32, i32, i64, i64, i32p, i32p, f64p, f64p, f64p,
                                            f64p]
@@ -449,21 +449,26 @@ def attn_in_group(law: str, i: int, j: int, a: int) -> bool:
     return bool(_load().oracle_attn_in_group(LAWS[law], i, j, a))
 
 
-def attn_fwd(q: int, law: str, m: int, n_heads: int, n_kv: int, B: int, S: int, pos_type, Q, K, V):
+def attn_fwd(q: int, law: str, m: int, n_heads: int, n_kv: int, B: int, S: int, pos_type, Q, K, V,
+             want_lse: bool = False):
     """Causal attention with the algebraic score (Alg. attention-training,
     forward): Q [B S, n_heads q m], K and V [B S, n_kv q m], token-major;
-    pos_type[p] is the type of position p.  Returns O like Q."""
+    pos_type[p] is the type of position p.  Returns O like Q, and with
+    ``want_lse`` also the natural log of each query's softmax denominator
+    [B, n_heads, S]."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     pt = np.ascontiguousarray(pos_type, dtype=np.int32)
     dh = q * m
     assert Q.shape == (B * S, n_heads * dh) and K.shape == (B * S, n_kv * dh) and V.shape == K.shape
     assert pt.shape == (S,)
     O = np.empty_like(Q)
+    lse = np.empty((B, n_heads, S), np.float64) if want_lse else None
     st = _load().oracle_attn_fwd(q, LAWS[law], m, n_heads, n_kv, B, S, _p(pt, ctypes.c_int32), _p(Q, ctypes.c_double),
-                                 _p(K, ctypes.c_double), _p(V, ctypes.c_double), _p(O, ctypes.c_double))
+                                 _p(K, ctypes.c_double), _p(V, ctypes.c_double), _p(O, ctypes.c_double),
+                                 _p(lse, ctypes.c_double) if want_lse else None)
     if st != 0:
         raise ValueError("bad attention arguments (type out of range or head counts)")
-    return O
+    return (O, lse) if want_lse else O
 
 
 def attn_decode(q: int, law: str, m: int, n_heads: int, n_kv: int, pos_type, cache_len, Q, K_cache, V_cache):

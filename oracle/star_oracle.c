@@ -507,10 +507,13 @@ static double attn_score(int law, int q, int64_t m, int i, int j, const double *
 
 /* Causal attention over B sequences of S positions (Alg. attention-training,
  * forward): Q [B S, n_heads d_h], K, V [B S, n_kv d_h], O [B S, n_heads d_h];
- * pos_type[p] is the type of position p.  Returns 0, or -1 for an
+ * pos_type[p] is the type of position p.  lse, if not NULL, receives
+ * [B, n_heads, S] the natural log of the softmax denominator of each query,
+ * log sum_{u <= p} exp(s_pu) (eq. softmax-pv).  Returns 0, or -1 for an
  * out-of-range type or a head count that does not divide. */
 int oracle_attn_fwd(int q, int law, int64_t m, int n_heads, int n_kv, int64_t B, int64_t S,
-                    const int32_t *pos_type, const double *Q, const double *K, const double *V, double *O)
+                    const int32_t *pos_type, const double *Q, const double *K, const double *V, double *O,
+                    double *lse)
 {
     if (n_kv <= 0 || n_heads % n_kv) return -1;
     for (int64_t p = 0; p < S; ++p)
@@ -534,6 +537,7 @@ int oracle_attn_fwd(int q, int law, int64_t m, int n_heads, int n_kv, int64_t B,
                     s[u] = exp(s[u] - mx);
                     den += s[u];
                 }
+                if (lse) lse[(b * n_heads + h) * S + p] = mx + log(den);
                 double *o = O + (b * S + p) * ldq + h * dh;
                 for (int64_t c = 0; c < dh; ++c) o[c] = 0.0;
                 for (int64_t u = 0; u <= p; ++u) {

@@ -41,6 +41,12 @@ class _CAlgebra(ctypes.Structure):
                 ("edges", ctypes.POINTER(ctypes.c_uint8))]
 
 
+class _CAttnShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seq_len", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("q", ctypes.c_int32),
+                ("law", ctypes.c_int)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_32814_amd.build`")
@@ -75,13 +81,19 @@ def _load() -> ctypes.CDLL:
     lib.star_swiglu_fwd.argtypes = [i64, P, P, E, P, P]
     lib.star_swiglu_bwd.argtypes = [i64, P, P, P, E, P, P, P]
     lib.star_add.argtypes = [i64, P, P, E, P, P]
+    S = ctypes.POINTER(_CAttnShape)
+    lib.star_attn_fwd.argtypes = [S, P, P, P, P, E, P, E, P, P]
+    lib.star_attn_decode_workspace_bytes.argtypes = [S]
+    lib.star_attn_decode_workspace_bytes.restype = sz
+    lib.star_attn_decode.argtypes = [S, P, P, P, P, P, E, P, E, P, sz, P]
     lib.star_status_string.argtypes = [E]
     lib.star_status_string.restype = ctypes.c_char_p
     for name in ("star_proj_fwd", "star_proj_bwd_data", "star_proj_bwd_weight", "star_ffn_fwd",
                  "star_decode", "star_count_products", "star_count_macs", "star_validate_types",
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
                  "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add",
-                 "star_decode_gated", "star_decode_status", "star_decode_noalloc"):
+                 "star_decode_gated", "star_decode_status", "star_decode_noalloc", "star_attn_fwd",
+                 "star_attn_decode"):
         getattr(lib, name).restype = E
     return lib
 
@@ -629,3 +641,86 @@ def star_swiglu_ffn_bwd(up: Algebra, down: Algebra, row_type: torch.Tensor, X: t
     dX = star_add(dX, star_proj_bwd_data_planned(up, plan, dZu, W_up, out_dtype=torch.float32), out=dX)
     return dict(dX=dX, dZ_gate=dZg, dZ_up=dZu, dW_gate=dW_gate, db_gate=db_gate, dW_up=dW_up,
                 db_up=db_up, dW_down=dW_down, db_down=db_down)
+
+
+# ---- algebraic attention ------------------------------------------------------
+
+class AttnShape:
+    """Shape of an algebraic-attention call: ``batch`` sequences of
+    ``seq_len`` positions (the cache capacity for decode), ``n_heads`` query
+    and ``n_kv_heads`` key/value heads of width ``head_dim`` = q m, under
+    ``law`` ("star", "dense" or "tensor2")."""
+
+    def __init__(self, batch: int, seq_len: int, n_heads: int, n_kv_heads: int, head_dim: int, q: int,
+                 law: str = "star"):
+        self.batch, self.seq_len, self.n_heads = int(batch), int(seq_len), int(n_heads)
+        self.n_kv_heads, self.head_dim, self.q, self.law = int(n_kv_heads), int(head_dim), int(q), law
+        self._c = _CAttnShape(self.batch, self.seq_len, self.n_heads, self.n_kv_heads, self.head_dim,
+                              self.q, LAWS[law])
+
+    @property
+    def ref(self):
+        return ctypes.byref(self._c)
+
+    def with_law(self, law: str) -> "AttnShape":
+        return AttnShape(self.batch, self.seq_len, self.n_heads, self.n_kv_heads, self.head_dim, self.q, law)
+
+    def __repr__(self):
+        return (f"AttnShape(batch={self.batch}, seq_len={self.seq_len}, n_heads={self.n_heads}, "
+                f"n_kv_heads={self.n_kv_heads}, head_dim={self.head_dim}, q={self.q}, law={self.law!r})")
+
+
+def star_attn_fwd(shape: AttnShape, plan: torch.Tensor, Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                  O=None, out_dtype=torch.bfloat16, lse=None, want_lse: bool = False):
+    """Causal algebraic attention over whole sequences.  ``plan`` is the type
+    plan of the position types (``star_type_plan(q, pos_type)``); Q is
+    [B, S, n_heads, d_h], K and V [B, S, n_kv_heads, d_h], bf16.  Returns O
+    (and the log-sum-exp [B, n_heads, S] when ``want_lse`` or ``lse`` is
+    given)."""
+    B, S, H, Hkv, D = shape.batch, shape.seq_len, shape.n_heads, shape.n_kv_heads, shape.head_dim
+    dev = Q.device if isinstance(Q, torch.Tensor) else None
+    _need(Q, "Q", (B, S, H, D), _BF16, dev)
+    _need(K, "K", (B, S, Hkv, D), _BF16, dev)
+    _need(V, "V", (B, S, Hkv, D), _BF16, dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
+    if O is None:
+        O = torch.empty((B, S, H, D), dtype=out_dtype, device=dev)
+    _need(O, "O", (B, S, H, D), _FLOATS, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((B, H, S), dtype=torch.float32, device=dev)
+    _opt(lse, "lse", (B, H, S), _F32, dev)
+    _gpu(dev)
+    _check(LIB.star_attn_fwd(shape.ref, _ptr(plan), _ptr(Q), _ptr(K), _ptr(V), DTYPES[torch.bfloat16], _ptr(O),
+                             _dt(O), _ptr(lse), _stream(dev)), "star_attn_fwd")
+    return (O, lse) if lse is not None else O
+
+
+def star_attn_decode_workspace_bytes(shape: AttnShape) -> int:
+    return int(LIB.star_attn_decode_workspace_bytes(shape.ref))
+
+
+def star_attn_decode(shape: AttnShape, pos_type: torch.Tensor, cache_len: torch.Tensor, Q: torch.Tensor,
+                     K_cache: torch.Tensor, V_cache: torch.Tensor, O=None, out_dtype=torch.bfloat16, ws=None):
+    """One decode step: Q [B, n_heads, d_h] against the caches
+    [B, S_max, n_kv_heads, d_h] (bf16), ``cache_len`` [B] valid entries per
+    sequence (the query sits at position cache_len - 1), ``pos_type``
+    [S_max].  Returns O [B, n_heads, d_h]."""
+    B, S, H, Hkv, D = shape.batch, shape.seq_len, shape.n_heads, shape.n_kv_heads, shape.head_dim
+    dev = Q.device if isinstance(Q, torch.Tensor) else None
+    _need(Q, "Q", (B, H, D), _BF16, dev)
+    _need(K_cache, "K_cache", (B, S, Hkv, D), _BF16, dev)
+    _need(V_cache, "V_cache", (B, S, Hkv, D), _BF16, dev)
+    _need(pos_type, "pos_type", (S,), _I32, dev)
+    _need(cache_len, "cache_len", (B,), _I32, dev)
+    if O is None:
+        O = torch.empty((B, H, D), dtype=out_dtype, device=dev)
+    _need(O, "O", (B, H, D), _FLOATS, dev)
+    need = star_attn_decode_workspace_bytes(shape)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    _need(ws, "ws", tuple(ws.shape), None, dev)
+    _gpu(dev)
+    _check(LIB.star_attn_decode(shape.ref, _ptr(pos_type), _ptr(cache_len), _ptr(Q), _ptr(K_cache),
+                                _ptr(V_cache), DTYPES[torch.bfloat16], _ptr(O), _dt(O), _ptr(ws),
+                                ws.numel() * ws.element_size(), _stream(dev)), "star_attn_decode")
+    return O

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libstarq.so")
-SOURCES = ["plan.hip", "gemm.hip", "gemm_async.hip", "colsum.hip", "swiglu.hip", "decode.hip", "decode_stack.hip", "graph_fill.hip", "scratch.hip", "api.cpp"]
+SOURCES = ["plan.hip", "gemm.hip", "gemm_async.hip", "colsum.hip", "swiglu.hip", "decode.hip", "decode_stack.hip", "graph_fill.hip", "scratch.hip", "attention.hip", "api.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -972,4 +972,115 @@ star_status star_add(int64_t n, const void* a, const void* b, star_dtype dt, voi
   return hip_status(launch_add(n, dt == STAR_BF16 ? 1 : 0, a, b, out, stream));
 }
 
+// ---- algebraic attention --------------------------------------------------
+
+namespace {
+struct AttnShape {
+  int32_t B, S, H, Hkv, D, q, law;
+};
+star_status parse_attn(const star_attn_shape* sh, AttnShape& a) {
+  if (!sh) return STAR_ERR_ARG;
+  if (sh->law != STAR_LAW_STAR && sh->law != STAR_LAW_DENSE && sh->law != STAR_LAW_TENSOR2) {
+    return sh->law == STAR_LAW_GRAPH ? STAR_ERR_UNSUPPORTED : STAR_ERR_ARG;
+  }
+  if (sh->batch < 0 || sh->seq_len < 0 || sh->n_heads < 1 || sh->n_kv_heads < 1) return STAR_ERR_SHAPE;
+  if (sh->n_heads % sh->n_kv_heads) return STAR_ERR_SHAPE;
+  if (sh->head_dim != 64 && sh->head_dim != 128) return STAR_ERR_UNSUPPORTED;
+  if (sh->q < 1 || sh->head_dim % sh->q || (sh->head_dim / sh->q) % 8) return STAR_ERR_UNSUPPORTED;
+  if (sh->law == STAR_LAW_TENSOR2 && sh->q != 1 && sh->q != 2 && sh->q != 4) return STAR_ERR_UNSUPPORTED;
+  if (sh->seq_len > (1 << 30)) return STAR_ERR_SHAPE;
+  a = {sh->batch, sh->seq_len, sh->n_heads, sh->n_kv_heads, sh->head_dim, sh->q, sh->law};
+  return STAR_OK;
+}
+AttnParams attn_params(const AttnShape& a) {
+  AttnParams p{};
+  p.B = a.B;
+  p.S = a.S;
+  p.n_heads = a.H;
+  p.n_kv = a.Hkv;
+  p.head_dim = a.D;
+  p.q = a.q;
+  p.law = a.law;
+  return p;
+}
+struct AttnDecWs {
+  int32_t chunk = 0, nchunks = 0;
+  size_t part_o = 0, part_ml = 0, end = 0;
+};
+AttnDecWs attn_dec_layout(const AttnShape& a) {
+  AttnDecWs w;
+  w.chunk = attn_decode_chunk(a.D);
+  w.nchunks = (std::max(a.S, 1) + w.chunk - 1) / w.chunk;
+  const size_t slots = static_cast<size_t>(a.B) * a.H * w.nchunks;
+  w.part_o = 0;
+  w.part_ml = align_up(sizeof(float) * slots * a.D);
+  w.end = align_up(w.part_ml + sizeof(float) * 2 * slots);
+  return w;
+}
+}  // namespace
+
+star_status star_attn_fwd(const star_attn_shape* shape, const void* plan, const void* Q, const void* K,
+                          const void* V, star_dtype dt, void* O, star_dtype ot, float* lse, hipStream_t stream) {
+  AttnShape a;
+  star_status st = parse_attn(shape, a);
+  if (st != STAR_OK) return st;
+  if (dt != STAR_BF16 || !valid_dtype(ot)) return STAR_ERR_DTYPE;
+  if (a.B == 0 || a.S == 0) return STAR_OK;
+  if (!plan || !Q || !K || !V || !O) return STAR_ERR_ARG;
+  if (!aligned16(plan) || !aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return STAR_ERR_ALIGN;
+  if (lse && !aligned4(lse)) return STAR_ERR_ALIGN;
+  const int64_t items = attn_fwd_items(a.S, a.q);
+  if (static_cast<int64_t>(a.B) * a.H * items > 0x7fffffff) return STAR_ERR_SHAPE;
+  const PlanWs pw = plan_layout(a.S, a.q);
+  AttnParams p = attn_params(a);
+  p.Q = Q;
+  p.K = K;
+  p.V = V;
+  p.O = O;
+  p.odtype = ot == STAR_BF16 ? 1 : 0;
+  p.lse = lse;
+  p.perm = at<int32_t>(const_cast<void*>(plan), pw.perm);
+  p.offsets = at<int32_t>(const_cast<void*>(plan), pw.offsets);
+  p.items_per_bh = static_cast<int32_t>(items);
+  return hip_status(launch_attn_fwd(p, stream));
+}
+
+size_t star_attn_decode_workspace_bytes(const star_attn_shape* shape) {
+  AttnShape a;
+  if (parse_attn(shape, a) != STAR_OK) return 0;
+  return attn_dec_layout(a).end;
+}
+
+star_status star_attn_decode(const star_attn_shape* shape, const int32_t* pos_type, const int32_t* cache_len,
+                             const void* Q, const void* K_cache, const void* V_cache, star_dtype dt, void* O,
+                             star_dtype ot, void* ws, size_t ws_bytes, hipStream_t stream) {
+  AttnShape a;
+  star_status st = parse_attn(shape, a);
+  if (st != STAR_OK) return st;
+  if (dt != STAR_BF16 || !valid_dtype(ot)) return STAR_ERR_DTYPE;
+  if (a.B == 0) return STAR_OK;
+  if (a.S == 0) return STAR_ERR_SHAPE;  // a decode step needs a cache
+  if (!pos_type || !cache_len || !Q || !K_cache || !V_cache || !O) return STAR_ERR_ARG;
+  if (!aligned4(pos_type) || !aligned4(cache_len)) return STAR_ERR_ALIGN;
+  if (!aligned16(Q) || !aligned16(K_cache) || !aligned16(V_cache) || !aligned16(O)) return STAR_ERR_ALIGN;
+  const AttnDecWs w = attn_dec_layout(a);
+  if (!ws || ws_bytes < w.end) return STAR_ERR_WORKSPACE;
+  if (!aligned16(ws)) return STAR_ERR_ALIGN;
+  AttnParams p = attn_params(a);
+  p.head_groups = (a.H / a.Hkv + kAttnDecHeads - 1) / kAttnDecHeads;
+  if (a.B > 65535 || static_cast<int64_t>(a.Hkv) * p.head_groups > 65535) return STAR_ERR_SHAPE;
+  p.Q = Q;
+  p.K = K_cache;
+  p.V = V_cache;
+  p.O = O;
+  p.odtype = ot == STAR_BF16 ? 1 : 0;
+  p.pos_type = pos_type;
+  p.cache_len = cache_len;
+  p.chunk = w.chunk;
+  p.nchunks = w.nchunks;
+  p.part_o = at<float>(ws, w.part_o);
+  p.part_ml = at<float>(ws, w.part_ml);
+  return hip_status(launch_attn_decode(p, stream));
+}
+
 }  // extern "C"

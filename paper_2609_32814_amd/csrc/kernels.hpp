@@ -184,6 +184,40 @@ hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t strea
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
 
+// ---- algebraic attention ------------------------------------------------------
+
+// Feature groups of width m = head_dim / q inside every head; layouts are
+// token-major: Q and O [B][S][n_heads][head_dim], K and V
+// [B][S][n_kv][head_dim] (bf16), query head h reads key/value head
+// h / (n_heads / n_kv).
+struct AttnParams {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* O;
+  int32_t odtype;  // 0 fp32, 1 bf16
+  float* lse;      // forward: natural log-sum-exp per (sequence, head, position), or null
+  int32_t B, S, n_heads, n_kv, head_dim, q, law;
+  // forward: the type plan of the S positions (perm sorted by type, stable)
+  const int32_t* perm;
+  const int32_t* offsets;
+  int32_t items_per_bh;  // grid = B * n_heads * items_per_bh
+  // decode: S is the cache capacity; one query row per sequence
+  const int32_t* pos_type;   // [S]
+  const int32_t* cache_len;  // [B]
+  int32_t chunk, nchunks;    // keys per split and splits over S
+  int32_t head_groups;       // query heads of one key/value head, in slices of kAttnDecHeads
+  float* part_o;             // [B][n_heads][nchunks][head_dim]
+  float* part_ml;            // [B][n_heads][nchunks][2]: running max (base 2), sum
+};
+constexpr int kAttnDecHeads = 8;  // query heads per decode workgroup
+// Forward work items per (sequence, head): 128-row query blocks over all types.
+inline int32_t attn_fwd_items(int32_t S, int32_t q) { return (S + 127 * q) / 128; }
+hipError_t launch_attn_fwd(const AttnParams& p, hipStream_t stream);
+// Keys per decode split for a head width.
+int32_t attn_decode_chunk(int32_t head_dim);
+hipError_t launch_attn_decode(const AttnParams& p, hipStream_t stream);
+
 // The static workspace of star_decode_noalloc (scratch.hip): its size, and
 // its device address on the current device (looked up on the first call per
 // device, then cached).

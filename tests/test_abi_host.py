@@ -201,3 +201,69 @@ def test_graph_law_counts_and_arguments(P):
     assert P.binding.LIB.star_count_products(ctypes.byref(bare), out) == 1
     with pytest.raises(ValueError):
         P.Algebra(2, [8, 8], [8, 8], "graph")
+
+
+def _attn_shape(P, **kw):
+    base = dict(batch=2, seq_len=100, n_heads=4, n_kv_heads=2, head_dim=64, q=4, law=0)
+    base.update(kw)
+    return P.binding._CAttnShape(**base)
+
+
+def _raw_attn_fwd(P, sh, dt=1, ot=0, ptrs=16, lse=None):
+    V = ctypes.c_void_p
+    p = V(ptrs) if ptrs else None
+    return P.binding.LIB.star_attn_fwd(ctypes.byref(sh), p, p, p, p, dt, p, ot, V(lse) if lse else None, None)
+
+
+def _raw_attn_dec(P, sh, ws_bytes=1 << 20, ptr=16, ws=16):
+    V = ctypes.c_void_p
+    p = V(ptr)
+    return P.binding.LIB.star_attn_decode(ctypes.byref(sh), p, p, p, p, p, 1, p, 0, V(ws) if ws else None,
+                                          ws_bytes, None)
+
+
+def test_attention_argument_errors(P):
+    """Attention calls reject bad shapes, laws, dtypes and pointers on the
+    host (fake pointers are never dereferenced)."""
+    err = {v: k for k, v in P.binding.STATUS_NAMES.items()}
+    assert _raw_attn_fwd(P, _attn_shape(P, law=3)) == err["STAR_ERR_UNSUPPORTED"]  # graph law
+    assert _raw_attn_fwd(P, _attn_shape(P, law=7)) == err["STAR_ERR_ARG"]
+    assert _raw_attn_fwd(P, _attn_shape(P, head_dim=96, q=2)) == err["STAR_ERR_UNSUPPORTED"]
+    assert _raw_attn_fwd(P, _attn_shape(P, q=3)) == err["STAR_ERR_UNSUPPORTED"]    # 64 % 3
+    assert _raw_attn_fwd(P, _attn_shape(P, q=16)) == err["STAR_ERR_UNSUPPORTED"]   # m = 4
+    assert _raw_attn_fwd(P, _attn_shape(P, q=8, law=2)) == err["STAR_ERR_UNSUPPORTED"]  # tensor power q = 8
+    assert _raw_attn_fwd(P, _attn_shape(P, n_kv_heads=3)) == err["STAR_ERR_SHAPE"]
+    assert _raw_attn_fwd(P, _attn_shape(P, batch=-1)) == err["STAR_ERR_SHAPE"]
+    assert _raw_attn_fwd(P, _attn_shape(P), dt=0) == err["STAR_ERR_DTYPE"]
+    assert _raw_attn_fwd(P, _attn_shape(P), ot=5) == err["STAR_ERR_DTYPE"]
+    assert _raw_attn_fwd(P, _attn_shape(P), ptrs=None) == err["STAR_ERR_ARG"]
+    assert _raw_attn_fwd(P, _attn_shape(P), ptrs=24) == err["STAR_ERR_ALIGN"]
+    assert _raw_attn_fwd(P, _attn_shape(P), lse=18) == err["STAR_ERR_ALIGN"]
+    assert _raw_attn_fwd(P, _attn_shape(P, batch=0)) == 0                    # no-op
+    assert _raw_attn_fwd(P, _attn_shape(P, seq_len=0), ptrs=None) == 0
+    need = P.star_attn_decode_workspace_bytes(P.AttnShape(2, 100, 4, 2, 64, 4))
+    # two chunks of 128 positions, 4 heads, 2 sequences: 64 features + (max, sum)
+    assert need >= 2 * 4 * 1 * (64 + 2) * 4
+    assert P.star_attn_decode_workspace_bytes(P.AttnShape(2, 100, 4, 2, 64, 4, "graph")) == 0
+    assert _raw_attn_dec(P, _attn_shape(P), ws_bytes=need - 1) == err["STAR_ERR_WORKSPACE"]
+    assert _raw_attn_dec(P, _attn_shape(P), ws=None) == err["STAR_ERR_WORKSPACE"]
+    assert _raw_attn_dec(P, _attn_shape(P), ptr=8) == err["STAR_ERR_ALIGN"]
+    assert _raw_attn_dec(P, _attn_shape(P, seq_len=0)) == err["STAR_ERR_SHAPE"]
+    assert _raw_attn_dec(P, _attn_shape(P, batch=0)) == 0
+
+
+def test_attention_binding_refuses_bad_tensors(P):
+    import torch
+    sh = P.AttnShape(1, 8, 2, 1, 64, 2)
+    Q = torch.zeros((1, 8, 2, 64), dtype=torch.bfloat16)
+    K = torch.zeros((1, 8, 1, 64), dtype=torch.bfloat16)
+    plan = torch.zeros(64, dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        P.star_attn_fwd(sh, plan, Q, K[:, :4], K)               # wrong shape
+    with pytest.raises(TypeError):
+        P.star_attn_fwd(sh, plan, Q.float(), K, K)              # wrong dtype
+    with pytest.raises(ValueError):
+        P.star_attn_fwd(sh, plan, Q, K, K)                      # CPU tensors
+    with pytest.raises(ValueError):
+        P.star_attn_decode(sh, torch.zeros(8, dtype=torch.int32), torch.ones(1, dtype=torch.int32),
+                           torch.zeros((1, 2, 64), dtype=torch.bfloat16), K, K)

@@ -1011,3 +1011,31 @@ def test_attention_causality_gqa_and_decode():
     Od = oracle.attn_decode(q, "star", m, nh, nkv, pt, L, Qd, Kc, Vc)
     for b in range(B):
         np.testing.assert_allclose(Od[b], O[b * S + L[b] - 1], atol=1e-13)
+
+
+def test_attention_log_sum_exp():
+    """The log of each query's softmax denominator: for the dense law it is
+    scipy's logsumexp of the causal row of Q K^T / sqrt(d_h); for the star
+    law, asking for it leaves the output unchanged, and at the first
+    position (a single key of the query's own type) it is that key's score
+    over the one group F(0, 0) = {0}."""
+    from scipy.special import logsumexp
+    q, m, S, nh = 4, 8, 17, 2
+    dh = q * m
+    g = rng(53)
+    Q, K, V = g.standard_normal((S, nh * dh)), g.standard_normal((S, dh)), g.standard_normal((S, dh))
+    pt = np.array([(3 * p + 2) % q for p in range(S)], np.int32)
+    _, lse = oracle.attn_fwd(q, "dense", m, nh, 1, 1, S, pt, Q, K, V, want_lse=True)
+    for h in range(nh):
+        s = Q[:, h * dh:(h + 1) * dh] @ K.T / np.sqrt(dh)
+        for p in range(S):
+            np.testing.assert_allclose(lse[0, h, p], logsumexp(s[p, :p + 1]), rtol=0, atol=1e-12)
+    m2, S2 = 6, 12
+    Qs, Ks = g.standard_normal((S2, 2 * m2)), g.standard_normal((S2, 2 * m2))
+    pt2 = (np.arange(S2) % 2).astype(np.int32)
+    O, lse2 = oracle.attn_fwd(2, "star", m2, 1, 1, 1, S2, pt2, Qs, Ks, np.eye(S2), want_lse=True)
+    np.testing.assert_allclose(O.sum(1), 1.0, atol=1e-13)
+    O_plain = oracle.attn_fwd(2, "star", m2, 1, 1, 1, S2, pt2, Qs, Ks, np.eye(S2))
+    np.testing.assert_array_equal(O, O_plain)
+    # at p = 0 the single key gives lse = s_00 = <Q_0^(0), K_0^(0)> / sqrt(m)
+    np.testing.assert_allclose(lse2[0, 0, 0], Qs[0, :m2] @ Ks[0, :m2] / np.sqrt(m2), atol=1e-13)
