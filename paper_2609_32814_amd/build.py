@@ -37,9 +37,15 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; the ROCm toolchain is required to build libstarq")
 
 
+# Per-source flags.  The attention kernels keep their MFMA accumulators in
+# VGPRs: the softmax works on every score, and accumulators in AGPRs would
+# cost a v_accvgpr_read/write pair per value per step.
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

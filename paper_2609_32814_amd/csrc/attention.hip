@@ -53,7 +53,6 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 constexpr int kFwdThreads = 256;  // 4 wavefronts
 constexpr int kQRows = 32;        // query rows per wave
 constexpr int kBlockRows = 128;   // query rows per workgroup
-constexpr int kKeys = 32;         // keys per block
 
 __device__ __attribute__((aligned(256))) uint32_t g_attn_zero[64];
 
@@ -83,41 +82,71 @@ __device__ __forceinline__ uint32_t attn_fmask(int law, int q, int i, int j) {
   return f;
 }
 
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  return static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to bf16 (nearest even) and packed, low half first:
+// one v_cvt_pk_bf16_f32.
+// max / sum of a value and its partner lane l ^ 32 (v_permlane32_swap; both
+// lanes get the same result)
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ uint32_t pair16(short lo, short hi) {
-  return static_cast<uint16_t>(lo) | (static_cast<uint32_t>(static_cast<uint16_t>(hi)) << 16);
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Value block in LDS: 32 key rows of DH bf16; the 16-byte chunk c of row r
-// sits at chunk c ^ 2 (r & 3), so the 4 rows of a transposing read fall on
-// distinct banks.
-template <int DH>
-__device__ __forceinline__ int vrow_off(int r, int c) {
-  return r * (DH * 2) + ((c ^ (2 * (r & 3))) << 4);
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
+
+// LDS tiles of one 64-key step: a plane per 16-byte feature chunk, each
+// plane the chunk of the 64 key rows in row order (1 KB, exactly one
+// global-to-LDS copy with lane = row), padded to kPlane bytes so that the
+// transposing reads of neighbouring planes fall on different banks.  The key
+// tile holds only the chunks of the selected groups F(i, j), packed in
+// chunk order; the value tile holds every chunk.
+constexpr int kStepKeys = 64;
+constexpr int kPlane = 1024 + 64;
+
+template <int DH>
+constexpr int fwd_tile_bytes() { return (DH / 8) * kPlane; }
+template <int DH>
+constexpr int fwd_smem() { return 2 * 2 * fwd_tile_bytes<DH>(); }  // two stages of (K, V)
 
 template <int DH>
 __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams p) {
   constexpr int NCH = DH / 32;  // 32-feature output chunks
   constexpr int KS = DH / 16;   // 16-feature contraction steps over a head
-  constexpr int CPR = DH / 8;   // 16-byte chunks per row
-  constexpr int RPC = 64 / CPR; // rows per 1 KB copy
-  __shared__ __attribute__((aligned(16))) char vblk[kKeys * DH * 2];
-  __shared__ int32_t kpos_s[kKeys];
+  constexpr int CPR = DH / 8;   // 16-byte chunks (planes) per row
+  constexpr int TILE = fwd_tile_bytes<DH>();
+  extern __shared__ __attribute__((aligned(16))) char tiles[];  // [stage][K, V][planes]
   __shared__ int32_t qpos_s[kBlockRows];
+  __shared__ int32_t kpos_s[2][kStepKeys];
+  __shared__ int32_t off_s[32 + 1];
+  __shared__ int32_t nstep_s[32];
+  // per key type j: F(i, j) as a group mask, the selected chunks as a mask,
+  // their count, the score scale (bits), then the selected chunks in order
+  __shared__ uint32_t tab_s[32][4 + 16];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lr = lane & 31, lh = lane >> 5;
-  const int q = p.q, m = DH / q;
+  const int q = p.q, m = DH / q, cpg = m / 8;
 
-  // ---- work item.  Consecutive workgroups take the same block level of
-  // different (sequence, head) pairs, and the latest (longest) query blocks
-  // of every type come first.
+  // ---- work item.  Workgroup w runs on XCD w % 8 (round-robin dispatch);
+  // each XCD takes a contiguous range of (sequence, head) pairs, so the query
+  // blocks of one pair run side by side and share its keys and values in that
+  // XCD's L2.  Within a pair the latest (longest) query blocks come first.
   const int32_t BH = p.B * p.n_heads;
-  const int32_t bh = blockIdx.x % BH;
-  int32_t r = blockIdx.x / BH;
+  const int64_t n_items = static_cast<int64_t>(BH) * p.items_per_bh;
+  const int64_t per_xcd = (n_items + 7) / 8;
+  const int64_t item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (item >= n_items) return;
+  const int32_t bh = static_cast<int32_t>(item / p.items_per_bh);
+  int32_t r = static_cast<int32_t>(item % p.items_per_bh);
   int i = -1;
   int32_t qb = 0;
   for (int32_t lvl = 0; i < 0; ++lvl) {
@@ -150,24 +179,105 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
     const int32_t pos = q0 + threadIdx.x;
     qpos_s[threadIdx.x] = pos < qend ? p.perm[pos] : -1;
   }
+  if (threadIdx.x <= q) off_s[threadIdx.x] = p.offsets[threadIdx.x];
+  if (threadIdx.x < q) {
+    const int j = threadIdx.x;
+    nstep_s[j] = 0;
+    const uint32_t fm = attn_fmask(p.law, q, i, j);
+    uint32_t csel = 0;
+    int n = 0;
+    for (int a = 0; a < q; ++a)
+      if ((fm >> a) & 1u) {
+        csel |= ((1u << cpg) - 1u) << (a * cpg);
+        for (int c = 0; c < cpg; ++c) tab_s[j][4 + n++] = a * cpg + c;
+      }
+    tab_s[j][0] = fm;
+    tab_s[j][1] = csel;
+    tab_s[j][2] = n;
+    tab_s[j][3] = __float_as_uint(kLog2e * __builtin_amdgcn_rsqf(static_cast<float>(__popc(fm) * m)));
+  }
   __syncthreads();
   // positions increase along the block: the workgroup's last query, and the
   // wave's first and last
   const int32_t nvalid = min(kBlockRows, qend - q0);
   const int32_t wg_last = qpos_s[nvalid - 1];
   const int32_t wv = min(kQRows, nvalid - wave * kQRows);  // valid rows of this wave (may be <= 0)
-  const int32_t wave_first = wv > 0 ? qpos_s[wave * kQRows] : 0x7fffffff;
-  const int32_t wave_last = wv > 0 ? qpos_s[wave * kQRows + wv - 1] : -1;
+  // (read through readfirstlane: the compiler then branches on them as
+  // wave-uniform values)
+  const int32_t wave_first = wv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[wave * kQRows]) : 0x7fffffff;
+  const int32_t wave_last = wv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[wave * kQRows + wv - 1]) : -1;
+  const int32_t my_qpos = qpos_s[wave * kQRows + lr];
+
+  // ---- steps per key type: the 64-key blocks of type j whose first
+  // position precedes the workgroup's last query (one flag per thread over
+  // all blocks of all types)
+  for (int32_t x = threadIdx.x;; x += kFwdThreads) {
+    int j = 0;
+    int32_t base = 0, nb = 0;
+    for (; j < q; ++j) {
+      nb = (off_s[j + 1] - off_s[j] + kStepKeys - 1) / kStepKeys;
+      if (x < base + nb) break;
+      base += nb;
+    }
+    if (j == q) break;
+    if (p.perm[off_s[j] + kStepKeys * (x - base)] <= wg_last) atomicAdd(&nstep_s[j], 1);
+  }
 
   // the wave's query rows as the B operand: lane half lh holds features
   // 16 ks + 8 lh .. + 7 of row lr for every step ks
-  const int32_t my_qpos = qpos_s[wave * kQRows + lr];
   uint4 qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     qf[ks] = make_uint4(0, 0, 0, 0);
     if (my_qpos >= 0) qf[ks] = *reinterpret_cast<const uint4*>(Qg + static_cast<int64_t>(my_qpos) * ldq + 16 * ks + 8 * lh);
   }
+  __syncthreads();
+  // step counts and offsets are the same for every lane: readfirstlane makes
+  // the step loop and its branches scalar
+  auto nsteps = [&](int j) { return __builtin_amdgcn_readfirstlane(nstep_s[j]); };
+  auto tab = [&](int j, int f) { return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(tab_s[j][f])); };
+  auto offs = [&](int j) { return __builtin_amdgcn_readfirstlane(off_s[j]); };
+  int32_t T = 0;
+  for (int j = 0; j < q; ++j) T += nsteps(j);
+
+  // step iterator: (type, block), skipping types without steps
+  struct It {
+    int j;
+    int32_t c;
+  };
+  auto normalize = [&](It& it) {
+    while (it.j < q && it.c >= nsteps(it.j)) {
+      ++it.j;
+      it.c = 0;
+    }
+  };
+  auto advance = [&](It& it) {
+    ++it.c;
+    normalize(it);
+  };
+  // the position of this lane's key row in a step (INT_MAX past the type's end)
+  auto load_kp = [&](const It& it) -> int32_t {
+    if (it.j >= q) return 0x7fffffff;
+    const int32_t k = offs(it.j) + kStepKeys * it.c + lane;
+    return k < offs(it.j + 1) ? p.perm[k] : 0x7fffffff;
+  };
+  // global-to-LDS copies of a step's key planes (selected chunks only) and
+  // value planes; lane = key row
+  const void* zero = g_attn_zero;
+  auto issue = [&](const It& it, int32_t kp, int stage) {
+    char* Kt = tiles + stage * 2 * TILE;
+    char* Vt = Kt + TILE;
+    const int nsel = static_cast<int>(tab(it.j, 2));
+    const bool ok = kp < p.S;
+    const uint16_t* krow = Kg + static_cast<int64_t>(ok ? kp : 0) * ldk;
+    const uint16_t* vrow = Vg + static_cast<int64_t>(ok ? kp : 0) * ldk;
+    for (int k = wave; k < nsel; k += 4) {
+      const int c = static_cast<int>(tab(it.j, 4 + k));
+      dma16(ok ? static_cast<const void*>(krow + 8 * c) : zero, lds_addr(Kt + k * kPlane));
+    }
+    for (int c = wave; c < CPR; c += 4)
+      dma16(ok ? static_cast<const void*>(vrow + 8 * c) : zero, lds_addr(Vt + c * kPlane));
+  };
 
   // online softmax state of the lane's query (shared with lane l ^ 32)
   float run_max = -INFINITY, run_sum = 0.f;
@@ -177,115 +287,157 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
 
-  for (int j = 0; j < q; ++j) {
-    const uint32_t fmask = attn_fmask(p.law, q, i, j);
-    const float scale = kLog2e * __builtin_amdgcn_rsqf(static_cast<float>(__popc(fmask) * m));
-    const int32_t k_lo = p.offsets[j], k_hi = p.offsets[j + 1];
-    for (int32_t k0 = k_lo; k0 < k_hi; k0 += kKeys) {
-      if (threadIdx.x < kKeys) kpos_s[threadIdx.x] = k0 + static_cast<int32_t>(threadIdx.x) < k_hi ? p.perm[k0 + threadIdx.x] : 0x7fffffff;
-      __syncthreads();
-      const int32_t first = kpos_s[0];
-      if (first > wg_last) {  // this block and the rest of type j follow every query
-        __syncthreads();
-        break;
-      }
-      // the value block into LDS (rows past the type's end copy zeros)
-      for (int cb = wave; cb < kKeys / RPC; cb += 4) {
-        const int row = cb * RPC + lane / CPR;
-        const int c = (lane % CPR) ^ (2 * (row & 3));
-        const int32_t kp = kpos_s[row];
-        const void* g = kp < p.S ? static_cast<const void*>(Vg + static_cast<int64_t>(kp) * ldk + 8 * c)
-                                 : static_cast<const void*>(g_attn_zero);
-        dma16(g, lds_addr(vblk + cb * 1024));
-      }
-      const bool active = first <= wave_last;  // some key of the block precedes a query of the wave
-      float s[16];
-      if (active) {
-        const int32_t kp = kpos_s[lr];
-        const uint16_t* kr = Kg + static_cast<int64_t>(kp < p.S ? kp : 0) * ldk;
+  It cur{0, 0};
+  normalize(cur);
+  It nxt = cur;
+  advance(nxt);
+  int32_t kp_cur = load_kp(cur);
+  int32_t kp_nxt = load_kp(nxt);
+  if (T > 0) {
+    wait_vm_all();
+    if (wave == 0) kpos_s[0][lane] = kp_cur;
+    issue(cur, kp_cur, 0);
+  }
+  for (int32_t s = 0; s < T; ++s) {
+    wait_vm_all();    // this step's copies and the next step's positions
+    __syncthreads();  // the tiles of step s are visible; step s - 1 is done everywhere
+    It nn = nxt;
+    advance(nn);
+    if (s + 1 < T) {
+      if (wave == 0) kpos_s[(s + 1) & 1][lane] = kp_nxt;
+      issue(nxt, kp_nxt, (s + 1) & 1);
+      kp_nxt = load_kp(nn);
+    }
+
+    const char* Kt = tiles + (s & 1) * 2 * TILE;
+    const char* Vt = Kt + TILE;
+    const int32_t* kps = kpos_s[s & 1];
+    // chunk c of the head is plane popc(csel below c) of the key tile
+    const uint32_t csel = tab(cur.j, 1);
+    const float scale = __uint_as_float(tab(cur.j, 3));
+    // first keys of the two halves and last key of each half (uniform)
+    const int32_t kf0 = __builtin_amdgcn_readfirstlane(kps[0]), kf1 = __builtin_amdgcn_readfirstlane(kps[32]);
+    const int32_t kl0 = __builtin_amdgcn_readfirstlane(kps[31]), kl1 = __builtin_amdgcn_readfirstlane(kps[63]);
+    if (kf0 <= wave_last) {  // some key of the step precedes a query of the wave
+      float sv[2][16];
+      float bmax = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        if ((t ? kf1 : kf0) > wave_last) {  // the second half follows every query of the wave
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sv[t][e] = -INFINITY;
+          continue;
+        }
         f32x16_t sa;
 #pragma unroll
         for (int e = 0; e < 16; ++e) sa[e] = 0.f;
+        const char* Krow = Kt + (32 * t + lr) * 16;
+        if (cpg >= 2) {
+          // m >= 16: the 16 features of a step lie in one group, selected or
+          // not as a whole; the lane half lh reads the step's second plane
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const int a0 = (16 * ks) / m, a1 = (16 * ks + 15) / m;
-          if (!(((fmask >> a0) | (fmask >> a1)) & 1u)) continue;
-          const int al = (16 * ks + 8 * lh) / m;
-          uint4 kf = make_uint4(0, 0, 0, 0);
-          if ((fmask >> al) & 1u) kf = *reinterpret_cast<const uint4*>(kr + 16 * ks + 8 * lh);
-          sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
-                                                        __builtin_bit_cast(bf16x8_t, qf[ks]), sa, 0, 0, 0);
+          for (int ks = 0; ks < KS; ++ks) {
+            if (!((csel >> (2 * ks)) & 1u)) continue;
+            const int pl = __popc(csel & ((1u << (2 * ks)) - 1u)) + lh;
+            const uint4 kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
+            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                          __builtin_bit_cast(bf16x8_t, qf[ks]), sa, 0, 0, 0);
+          }
+        } else {
+          // m = 8: the two halves of a step are two groups; a lane whose
+          // group is not selected reads plane 0 and contributes zeros
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            if (!((csel >> (2 * ks)) & 3u)) continue;
+            const int c = 2 * ks + lh;
+            const bool on = (csel >> c) & 1u;
+            const int pl = on ? __popc(csel & ((1u << c) - 1u)) : 0;
+            uint4 kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
+            if (!on) kf = make_uint4(0, 0, 0, 0);
+            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                          __builtin_bit_cast(bf16x8_t, qf[ks]), sa, 0, 0, 0);
+          }
         }
-        // lane holds query lr against keys 8 (e / 4) + 4 lh + e % 4
-        const bool full = kpos_s[kKeys - 1] <= wave_first;  // no key of the block follows a query of the wave
-        float bmax = -INFINITY;
+        // lane holds query lr against keys 32 t + 8 (e / 4) + 4 lh + e % 4;
+        // the causal mask is needed only where a key of this half follows a
+        // query of the wave
+        if ((t ? kl1 : kl0) > wave_first) {
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const int4 kq = *reinterpret_cast<const int4*>(kps + 32 * t + 8 * a + 4 * lh);
+            if (kq.x > my_qpos) sa[4 * a + 0] = -INFINITY;
+            if (kq.y > my_qpos) sa[4 * a + 1] = -INFINITY;
+            if (kq.z > my_qpos) sa[4 * a + 2] = -INFINITY;
+            if (kq.w > my_qpos) sa[4 * a + 3] = -INFINITY;
+          }
+        }
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int kk = 8 * (e / 4) + 4 * lh + (e % 4);
-          float v = sa[e] * scale;
-          if (!full && kpos_s[kk] > my_qpos) v = -INFINITY;
-          s[e] = v;
-          bmax = fmaxf(bmax, v);
+          sv[t][e] = sa[e];
+          bmax = fmaxf(bmax, sa[e]);
         }
-        bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-        const float new_max = fmaxf(run_max, bmax);
-        // a row whose keys so far are all masked keeps max -inf and zero
-        // probabilities
-        const bool none = new_max == -INFINITY;
-        const float corr = none ? 1.f : __builtin_amdgcn_exp2f(run_max - new_max);
-        float bsum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float pe = none ? 0.f : __builtin_amdgcn_exp2f(s[e] - new_max);
-          s[e] = pe;
-          bsum += pe;
-        }
-        bsum += __shfl_xor(bsum, 32);
-        run_sum = run_sum * corr + bsum;
-        run_max = new_max;
+      }
+      // the step's largest scaled score (base 2) of the lane's query
+      bmax = max_xor32(bmax) * scale;
+      // Lazy rescaling: the running maximum moves (and the accumulators are
+      // rescaled) only when a score exceeds it by more than 8, so every
+      // probability stays below 2^8; the normalisation by the sum at the end
+      // is unchanged.  A row whose keys so far are all masked keeps -inf.
+      const bool need = bmax > run_max + 8.f;
+      if (__ballot(need) != 0) {
+        const float corr = need ? __builtin_amdgcn_exp2f(run_max - bmax) : 1.f;
+        if (need) run_max = bmax;
+        run_sum *= corr;
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
 #pragma unroll
           for (int e = 0; e < 16; ++e) acc[c][e] *= corr;
       }
-      wait_vm_all();
-      __syncthreads();  // the value block has landed
-      if (active) {
-        // O^T += V^T P^T in two 16-key steps: step kk takes the lane's
-        // probabilities e = 8 kk .. 8 kk + 7, the keys 16 kk + 4 lh + 0..3
-        // and 16 kk + 8 + 4 lh + 0..3
-        const int g = lane >> 4, pp = lane & 15;
-        const int rr = pp >> 2, qq = pp & 3;
+      const float base = run_max == -INFINITY ? 0.f : run_max;
+      float bsum = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          uint4 pf;
-          pf.x = pack_bf16(s[8 * kk + 0], s[8 * kk + 1]);
-          pf.y = pack_bf16(s[8 * kk + 2], s[8 * kk + 3]);
-          pf.z = pack_bf16(s[8 * kk + 4], s[8 * kk + 5]);
-          pf.w = pack_bf16(s[8 * kk + 6], s[8 * kk + 7]);
-          const int row0 = 16 * kk + 4 * (g >> 1) + rr;
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-          for (int c = 0; c < NCH; ++c) {
-            // in 16-lane group g, lanes 4 rr + qq address features
-            // f .. f + 3 of key rows row0 and row0 + 8; lane pp receives
-            // feature 32 c + 16 (g & 1) + pp of those 4 + 4 rows
-            const int f = 32 * c + 16 * (g & 1) + 4 * qq;
-            const char* a0 = vblk + vrow_off<DH>(row0, f >> 3) + ((f >> 2) & 1) * 8;
-            const char* a1 = vblk + vrow_off<DH>(row0 + 8, f >> 3) + ((f >> 2) & 1) * 8;
-            const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0));
-            const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a1));
-            uint4 vf;
-            vf.x = pair16(w0[0], w0[1]);
-            vf.y = pair16(w0[2], w0[3]);
-            vf.z = pair16(w1[0], w1[1]);
-            vf.w = pair16(w1[2], w1[3]);
-            acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
-                                                             __builtin_bit_cast(bf16x8_t, pf), acc[c], 0, 0, 0);
-          }
+        for (int e = 0; e < 16; ++e) {
+          const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[t][e], scale, -base));
+          sv[t][e] = pe;
+          bsum += pe;
+        }
+      run_sum += sum_xor32(bsum);
+
+      // O^T += V^T P^T in 16-key steps: step kk takes the probabilities of
+      // half kk / 2, e = 8 (kk % 2) .. + 7, i.e. the keys 16 kk + 4 lh + 0..3
+      // and 16 kk + 8 + 4 lh + 0..3
+      const bool second = kf1 <= wave_last;
+      const int g = lane >> 4, pp = lane & 15;
+      const int rr = pp >> 2, qq = pp & 3;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        if (kk >= 2 && !second) break;
+        const float* sp = &sv[kk >> 1][8 * (kk & 1)];
+        uint4 pf;
+        pf.x = pack_bf16(sp[0], sp[1]);
+        pf.y = pack_bf16(sp[2], sp[3]);
+        pf.z = pack_bf16(sp[4], sp[5]);
+        pf.w = pack_bf16(sp[6], sp[7]);
+        const int row0 = 16 * kk + 4 * (g >> 1) + rr;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          // in 16-lane group g, lanes 4 rr + qq address features f .. f + 3
+          // of key rows row0 and row0 + 8; lane pp receives feature
+          // 32 c + 16 (g & 1) + pp of those 4 + 4 rows
+          const int f = 32 * c + 16 * (g & 1) + 4 * qq;
+          const char* a0 = Vt + (f >> 3) * kPlane + row0 * 16 + ((f >> 2) & 1) * 8;
+          const uint2 w0 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0)));
+          const uint2 w1 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0 + 8 * 16)));
+          const uint4 vf = make_uint4(w0.x, w0.y, w1.x, w1.y);
+          acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
+                                                           __builtin_bit_cast(bf16x8_t, pf), acc[c], 0, 0, 0);
         }
       }
-      __syncthreads();  // every wave is done with the value block and the key positions
     }
+    cur = nxt;
+    nxt = nn;
   }
 
   // ---- O = acc / sum: lane holds query lr, features 32 c + 8 a + 4 lh + 0..3
@@ -515,6 +667,15 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(const AttnParams 
 }
 
 template <int DH>
+hipError_t launch_fwd_dh(const AttnParams& p, unsigned grid, hipStream_t stream) {
+  static std::atomic<unsigned long long> set{0};
+  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(attn_fwd_kernel<DH>), set, fwd_smem<DH>());
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_fwd_kernel<DH>, dim3(grid), dim3(kFwdThreads), fwd_smem<DH>(), stream, p);
+  return hipGetLastError();
+}
+
+template <int DH>
 hipError_t launch_decode_dh(const AttnParams& p, hipStream_t stream) {
   constexpr int T = DH / 8;
   const int gmax = std::min(kAttnDecHeads, p.n_heads / p.n_kv);
@@ -533,14 +694,14 @@ hipError_t launch_decode_dh(const AttnParams& p, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_attn_fwd(const AttnParams& p, hipStream_t stream) {
-  const int64_t grid = static_cast<int64_t>(p.B) * p.n_heads * p.items_per_bh;
-  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t items = static_cast<int64_t>(p.B) * p.n_heads * p.items_per_bh;
+  const int64_t grid = 8 * ((items + 7) / 8);
+  if (items <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   switch (p.head_dim) {
-    case 64: hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(static_cast<unsigned>(grid)), dim3(kFwdThreads), 0, stream, p); break;
-    case 128: hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(static_cast<unsigned>(grid)), dim3(kFwdThreads), 0, stream, p); break;
+    case 64: return launch_fwd_dh<64>(p, static_cast<unsigned>(grid), stream);
+    case 128: return launch_fwd_dh<128>(p, static_cast<unsigned>(grid), stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 int32_t attn_decode_chunk(int32_t head_dim) {
