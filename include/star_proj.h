@@ -424,7 +424,8 @@ typedef struct {
  *         log-sum-exp of each query's scaled scores (the softmax
  *         normaliser a backward pass needs).
  * Errors: STAR_ERR_ARG (null pointer, bad law), STAR_ERR_SHAPE (a size
- * below zero, n_kv_heads not dividing n_heads, a grid too large),
+ * below zero, n_kv_heads not dividing n_heads, seq_len above 262144, a grid
+ * too large),
  * STAR_ERR_UNSUPPORTED (head_dim, q or m outside the supported set),
  * STAR_ERR_DTYPE, STAR_ERR_ALIGN. */
 star_status star_attn_fwd(const star_attn_shape *shape, const void *plan, const void *Q,

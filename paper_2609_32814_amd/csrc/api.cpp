@@ -1009,7 +1009,7 @@ struct AttnDecWs {
 };
 AttnDecWs attn_dec_layout(const AttnShape& a) {
   AttnDecWs w;
-  w.chunk = attn_decode_chunk(a.D);
+  w.chunk = attn_decode_chunk(a.D, a.B, a.Hkv, (a.H / a.Hkv + kAttnDecHeads - 1) / kAttnDecHeads, std::max(a.S, 1));
   w.nchunks = (std::max(a.S, 1) + w.chunk - 1) / w.chunk;
   const size_t slots = static_cast<size_t>(a.B) * a.H * w.nchunks;
   w.part_o = 0;
@@ -1029,6 +1029,7 @@ star_status star_attn_fwd(const star_attn_shape* shape, const void* plan, const 
   if (!plan || !Q || !K || !V || !O) return STAR_ERR_ARG;
   if (!aligned16(plan) || !aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return STAR_ERR_ALIGN;
   if (lse && !aligned4(lse)) return STAR_ERR_ALIGN;
+  if (a.S > kAttnFwdMaxSeq) return STAR_ERR_SHAPE;
   const int64_t items = attn_fwd_items(a.S, a.q);
   if (static_cast<int64_t>(a.B) * a.H * items > 0x7fffffff) return STAR_ERR_SHAPE;
   const PlanWs pw = plan_layout(a.S, a.q);
@@ -1068,7 +1069,7 @@ star_status star_attn_decode(const star_attn_shape* shape, const int32_t* pos_ty
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
   AttnParams p = attn_params(a);
   p.head_groups = (a.H / a.Hkv + kAttnDecHeads - 1) / kAttnDecHeads;
-  if (a.B > 65535 || static_cast<int64_t>(a.Hkv) * p.head_groups > 65535) return STAR_ERR_SHAPE;
+  if (a.B > 65535 || w.nchunks > 65535) return STAR_ERR_SHAPE;
   p.Q = Q;
   p.K = K_cache;
   p.V = V_cache;

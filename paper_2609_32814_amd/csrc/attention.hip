@@ -50,8 +50,7 @@ namespace {
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define STARQ_LDS __attribute__((address_space(3)))
 
-constexpr int kFwdThreads = 256;  // 4 wavefronts
-constexpr int kQRows = 32;        // query rows per wave
+constexpr int kQRows = 32;        // query rows per MFMA tile
 constexpr int kBlockRows = 128;   // query rows per workgroup
 
 __device__ __attribute__((aligned(256))) uint32_t g_attn_zero[64];
@@ -109,6 +108,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 // tile holds only the chunks of the selected groups F(i, j), packed in
 // chunk order; the value tile holds every chunk.
 constexpr int kStepKeys = 64;
+// 64-key blocks over all types the forward can index (positions up to
+// kAttnFwdMaxSeq plus a partial block per type), rounded up to the 256 block
+// flags one pass of a 256-thread workgroup writes
+constexpr int kFwdMaxBlocks = (kAttnFwdMaxSeq / kStepKeys + 32 + 255) / 256 * 256;
 constexpr int kPlane = 1024 + 64;
 
 template <int DH>
@@ -116,8 +119,18 @@ constexpr int fwd_tile_bytes() { return (DH / 8) * kPlane; }
 template <int DH>
 constexpr int fwd_smem() { return 2 * 2 * fwd_tile_bytes<DH>(); }  // two stages of (K, V)
 
+// Query tiles of 32 rows per wave (one: four waves per 128-row block).
 template <int DH>
-__global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams p) {
+constexpr int fwd_qtiles() { return 1; }
+template <int DH>
+constexpr int fwd_threads() { return 64 * (kBlockRows / (kQRows * fwd_qtiles<DH>())); }
+
+// M8: groups of 8 features (two groups per 16-feature contraction step).
+template <int DH, bool M8>
+__global__ __launch_bounds__(fwd_threads<DH>()) void attn_fwd_kernel(const AttnParams p) {
+  constexpr int QT = fwd_qtiles<DH>();    // 32-row query tiles per wave
+  constexpr int NW = fwd_threads<DH>() / 64;
+  constexpr int NT = NW * 64;
   constexpr int NCH = DH / 32;  // 32-feature output chunks
   constexpr int KS = DH / 16;   // 16-feature contraction steps over a head
   constexpr int CPR = DH / 8;   // 16-byte chunks (planes) per row
@@ -127,6 +140,7 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
   __shared__ int32_t kpos_s[2][kStepKeys];
   __shared__ int32_t off_s[32 + 1];
   __shared__ int32_t nstep_s[32];
+  __shared__ uint64_t bits_s[kFwdMaxBlocks / 64];
   // per key type j: F(i, j) as a group mask, the selected chunks as a mask,
   // their count, the score scale (bits), then the selected chunks in order
   __shared__ uint32_t tab_s[32][4 + 16];
@@ -175,61 +189,100 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
   const uint16_t* Kg = static_cast<const uint16_t*>(p.K) + static_cast<int64_t>(b) * p.S * ldk + hk * DH;
   const uint16_t* Vg = static_cast<const uint16_t*>(p.V) + static_cast<int64_t>(b) * p.S * ldk + hk * DH;
 
-  if (threadIdx.x < kBlockRows) {
-    const int32_t pos = q0 + threadIdx.x;
-    qpos_s[threadIdx.x] = pos < qend ? p.perm[pos] : -1;
+  // ---- prologue: one round of global loads (the block's query positions,
+  // its last query, the first position of every 64-key block of every type,
+  // and the key rows of the first two blocks of type 0, the likely first
+  // steps), then the step counts.
+  const int32_t nvalid = min(kBlockRows, qend - q0);
+  const int32_t wg_last = p.perm[q0 + nvalid - 1];
+  for (int x = threadIdx.x; x < kBlockRows; x += NT) {
+    const int32_t pos = q0 + x;
+    qpos_s[x] = pos < qend ? p.perm[pos] : -1;
   }
   if (threadIdx.x <= q) off_s[threadIdx.x] = p.offsets[threadIdx.x];
+  // Groups are taken in the rotated order a' = (a - i) mod q, so that the
+  // query's own group i, which every F(i, j) holds, comes first: the first
+  // contraction step of every key tile is then always selected.
   if (threadIdx.x < q) {
     const int j = threadIdx.x;
-    nstep_s[j] = 0;
     const uint32_t fm = attn_fmask(p.law, q, i, j);
-    uint32_t csel = 0;
+    uint32_t csel = 0;  // selected chunks, rotated order
     int n = 0;
-    for (int a = 0; a < q; ++a)
+    for (int ar = 0; ar < q; ++ar) {
+      const int a = (ar + i) % q;
       if ((fm >> a) & 1u) {
-        csel |= ((1u << cpg) - 1u) << (a * cpg);
+        csel |= ((1u << cpg) - 1u) << (ar * cpg);
         for (int c = 0; c < cpg; ++c) tab_s[j][4 + n++] = a * cpg + c;
       }
+    }
     tab_s[j][0] = fm;
     tab_s[j][1] = csel;
     tab_s[j][2] = n;
     tab_s[j][3] = __float_as_uint(kLog2e * __builtin_amdgcn_rsqf(static_cast<float>(__popc(fm) * m)));
   }
-  __syncthreads();
-  // positions increase along the block: the workgroup's last query, and the
-  // wave's first and last
-  const int32_t nvalid = min(kBlockRows, qend - q0);
-  const int32_t wg_last = qpos_s[nvalid - 1];
-  const int32_t wv = min(kQRows, nvalid - wave * kQRows);  // valid rows of this wave (may be <= 0)
-  // (read through readfirstlane: the compiler then branches on them as
-  // wave-uniform values)
-  const int32_t wave_first = wv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[wave * kQRows]) : 0x7fffffff;
-  const int32_t wave_last = wv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[wave * kQRows + wv - 1]) : -1;
-  const int32_t my_qpos = qpos_s[wave * kQRows + lr];
-
-  // ---- steps per key type: the 64-key blocks of type j whose first
-  // position precedes the workgroup's last query (one flag per thread over
-  // all blocks of all types)
-  for (int32_t x = threadIdx.x;; x += kFwdThreads) {
-    int j = 0;
-    int32_t base = 0, nb = 0;
-    for (; j < q; ++j) {
-      nb = (off_s[j + 1] - off_s[j] + kStepKeys - 1) / kStepKeys;
-      if (x < base + nb) break;
+  const int32_t off0 = p.offsets[0], off1 = p.offsets[1];
+  int32_t kp_cur = off0 + lane < off1 ? p.perm[off0 + lane] : 0x7fffffff;
+  int32_t kp_nxt = off0 + kStepKeys + lane < off1 ? p.perm[off0 + kStepKeys + lane] : 0x7fffffff;
+  // one bit per 64-key block, all types in order: does the block start at
+  // or before the workgroup's last query?
+  int32_t NB = 0;
+  for (int j = 0; j < q; ++j) NB += (p.offsets[j + 1] - p.offsets[j] + kStepKeys - 1) / kStepKeys;
+  for (int32_t x0 = 0; x0 < NB; x0 += NT) {
+    const int32_t x = x0 + threadIdx.x;
+    int32_t first = 0x7fffffff;
+    int32_t base = 0;
+    for (int j = 0; j < q; ++j) {
+      const int32_t oj = p.offsets[j], nb = (p.offsets[j + 1] - oj + kStepKeys - 1) / kStepKeys;
+      if (x >= base && x < base + nb) first = p.perm[oj + kStepKeys * (x - base)];
       base += nb;
     }
-    if (j == q) break;
-    if (p.perm[off_s[j] + kStepKeys * (x - base)] <= wg_last) atomicAdd(&nstep_s[j], 1);
+    const uint64_t bal = __ballot(first <= wg_last);
+    if (lane == 0) bits_s[(x0 >> 6) + wave] = bal;
   }
+  __syncthreads();
+  // steps of type j: the set bits among its blocks
+  if (threadIdx.x < q) {
+    const int j = threadIdx.x;
+    int32_t base = 0;
+    for (int t = 0; t < j; ++t) base += (off_s[t + 1] - off_s[t] + kStepKeys - 1) / kStepKeys;
+    const int32_t nb = (off_s[j + 1] - off_s[j] + kStepKeys - 1) / kStepKeys;
+    int32_t n = 0;
+    for (int32_t x = base; x < base + nb;) {
+      const int32_t w = x >> 6, lo = x & 63, hi = min(64, lo + (base + nb - x));
+      uint64_t word = bits_s[w] >> lo;
+      if (hi - lo < 64) word &= (1ull << (hi - lo)) - 1ull;
+      n += __popcll(word);
+      x += hi - lo;
+    }
+    nstep_s[j] = n;
+  }
+  // positions increase along the block: the first and last query of each of
+  // the wave's tiles (read through readfirstlane: the compiler then branches
+  // on them as wave-uniform values)
+  int32_t tfirst[QT], tlast[QT], my_qpos[QT];
+#pragma unroll
+  for (int u = 0; u < QT; ++u) {
+    const int row0 = (wave * QT + u) * kQRows;
+    const int32_t tv = min(kQRows, nvalid - row0);  // valid rows of this tile (may be <= 0)
+    tfirst[u] = tv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[row0]) : 0x7fffffff;
+    tlast[u] = tv > 0 ? __builtin_amdgcn_readfirstlane(qpos_s[row0 + tv - 1]) : -1;
+    my_qpos[u] = qpos_s[row0 + lr];
+  }
+  const int32_t wave_last = tlast[QT - 1] >= 0 ? tlast[QT - 1] : tlast[0];
 
-  // the wave's query rows as the B operand: lane half lh holds features
-  // 16 ks + 8 lh .. + 7 of row lr for every step ks
-  uint4 qf[KS];
+  // the wave's query rows as B operands: for rotated step ks lane half lh
+  // holds the 8 features at rotated position 16 ks + 8 lh of row lr of each
+  // tile, i.e. offset o of rotated group a' (physical group (a' + i) mod q)
+  uint4 qf[QT][KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    qf[ks] = make_uint4(0, 0, 0, 0);
-    if (my_qpos >= 0) qf[ks] = *reinterpret_cast<const uint4*>(Qg + static_cast<int64_t>(my_qpos) * ldq + 16 * ks + 8 * lh);
+    const int fr = 16 * ks + 8 * lh;
+    const int fphys = ((fr / m + i) % q) * m + fr % m;
+#pragma unroll
+    for (int u = 0; u < QT; ++u) {
+      qf[u][ks] = make_uint4(0, 0, 0, 0);
+      if (my_qpos[u] >= 0) qf[u][ks] = *reinterpret_cast<const uint4*>(Qg + static_cast<int64_t>(my_qpos[u]) * ldq + fphys);
+    }
   }
   __syncthreads();
   // step counts and offsets are the same for every lane: readfirstlane makes
@@ -271,28 +324,35 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
     const bool ok = kp < p.S;
     const uint16_t* krow = Kg + static_cast<int64_t>(ok ? kp : 0) * ldk;
     const uint16_t* vrow = Vg + static_cast<int64_t>(ok ? kp : 0) * ldk;
-    for (int k = wave; k < nsel; k += 4) {
+    for (int k = wave; k < nsel; k += NW) {
       const int c = static_cast<int>(tab(it.j, 4 + k));
       dma16(ok ? static_cast<const void*>(krow + 8 * c) : zero, lds_addr(Kt + k * kPlane));
     }
-    for (int c = wave; c < CPR; c += 4)
+    for (int c = wave; c < CPR; c += NW)
       dma16(ok ? static_cast<const void*>(vrow + 8 * c) : zero, lds_addr(Vt + c * kPlane));
   };
 
-  // online softmax state of the lane's query (shared with lane l ^ 32)
-  float run_max = -INFINITY, run_sum = 0.f;
-  f32x16_t acc[NCH];
+  // online softmax state of the lane's query in each tile (shared with lane
+  // l ^ 32)
+  float run_max[QT], run_sum[QT];
+  f32x16_t acc[QT][NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c)
+  for (int u = 0; u < QT; ++u) {
+    run_max[u] = -INFINITY;
+    run_sum[u] = 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[u][c][e] = 0.f;
+  }
 
   It cur{0, 0};
   normalize(cur);
   It nxt = cur;
   advance(nxt);
-  int32_t kp_cur = load_kp(cur);
-  int32_t kp_nxt = load_kp(nxt);
+  // the speculative rows were those of type 0, blocks 0 and 1
+  if (cur.j != 0 || cur.c != 0) kp_cur = load_kp(cur);
+  if (nxt.j != 0 || nxt.c != 1) kp_nxt = load_kp(nxt);
   if (T > 0) {
     wait_vm_all();
     if (wave == 0) kpos_s[0][lane] = kp_cur;
@@ -315,111 +375,120 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
     // chunk c of the head is plane popc(csel below c) of the key tile
     const uint32_t csel = tab(cur.j, 1);
     const float scale = __uint_as_float(tab(cur.j, 3));
-    // first keys of the two halves and last key of each half (uniform)
+    // first and last keys of the two halves (uniform)
     const int32_t kf0 = __builtin_amdgcn_readfirstlane(kps[0]), kf1 = __builtin_amdgcn_readfirstlane(kps[32]);
     const int32_t kl0 = __builtin_amdgcn_readfirstlane(kps[31]), kl1 = __builtin_amdgcn_readfirstlane(kps[63]);
     if (kf0 <= wave_last) {  // some key of the step precedes a query of the wave
-      float sv[2][16];
-      float bmax = -INFINITY;
+      // Every query tile and both key halves are computed; keys after a
+      // query are removed by the causal mask (a half past the type's end has
+      // positions INT_MAX).
+      f32x16_t sc[QT][2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        if ((t ? kf1 : kf0) > wave_last) {  // the second half follows every query of the wave
-#pragma unroll
-          for (int e = 0; e < 16; ++e) sv[t][e] = -INFINITY;
-          continue;
-        }
-        f32x16_t sa;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sa[e] = 0.f;
         const char* Krow = Kt + (32 * t + lr) * 16;
-        if (cpg >= 2) {
-          // m >= 16: the 16 features of a step lie in one group, selected or
-          // not as a whole; the lane half lh reads the step's second plane
+        // rotated step ks uses key planes popc(csel below 2 ks) + lh; step 0
+        // (the query's own group) is always selected and starts the sum
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            if (!((csel >> (2 * ks)) & 1u)) continue;
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks > 0 && !((csel >> (2 * ks)) & 3u)) continue;
+          uint4 kf;
+          if constexpr (!M8) {
+            // m >= 16: a step's 16 features lie in one group
             const int pl = __popc(csel & ((1u << (2 * ks)) - 1u)) + lh;
-            const uint4 kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
-            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
-                                                          __builtin_bit_cast(bf16x8_t, qf[ks]), sa, 0, 0, 0);
-          }
-        } else {
-          // m = 8: the two halves of a step are two groups; a lane whose
-          // group is not selected reads plane 0 and contributes zeros
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            if (!((csel >> (2 * ks)) & 3u)) continue;
+            kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
+          } else {
+            // m = 8: the halves of a step are two groups; a lane whose group
+            // is not selected reads plane 0 and contributes zeros
             const int c = 2 * ks + lh;
             const bool on = (csel >> c) & 1u;
             const int pl = on ? __popc(csel & ((1u << c) - 1u)) : 0;
-            uint4 kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
+            kf = *reinterpret_cast<const uint4*>(Krow + pl * kPlane);
             if (!on) kf = make_uint4(0, 0, 0, 0);
-            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
-                                                          __builtin_bit_cast(bf16x8_t, qf[ks]), sa, 0, 0, 0);
           }
-        }
-        // lane holds query lr against keys 32 t + 8 (e / 4) + 4 lh + e % 4;
-        // the causal mask is needed only where a key of this half follows a
-        // query of the wave
-        if ((t ? kl1 : kl0) > wave_first) {
 #pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            const int4 kq = *reinterpret_cast<const int4*>(kps + 32 * t + 8 * a + 4 * lh);
-            if (kq.x > my_qpos) sa[4 * a + 0] = -INFINITY;
-            if (kq.y > my_qpos) sa[4 * a + 1] = -INFINITY;
-            if (kq.z > my_qpos) sa[4 * a + 2] = -INFINITY;
-            if (kq.w > my_qpos) sa[4 * a + 3] = -INFINITY;
+          for (int u = 0; u < QT; ++u) {
+            if (ks == 0)
+              sc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                                 __builtin_bit_cast(bf16x8_t, qf[u][0]), f32x16_t{}, 0, 0, 0);
+            else
+              sc[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                                 __builtin_bit_cast(bf16x8_t, qf[u][ks]), sc[u][t], 0, 0, 0);
           }
-        }
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          sv[t][e] = sa[e];
-          bmax = fmaxf(bmax, sa[e]);
         }
       }
-      // the step's largest scaled score (base 2) of the lane's query
-      bmax = max_xor32(bmax) * scale;
+      // lane holds query lr of tile u against keys 32 t + 8 (e / 4) + 4 lh + e % 4
+      bool need_any = false;
+      float bmax[QT];
+#pragma unroll
+      for (int u = 0; u < QT; ++u) {
+        bmax[u] = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          // the causal mask is needed only where a key of this half follows
+          // the tile's first query
+          if ((t ? kl1 : kl0) > tfirst[u]) {
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+              const int4 kq = *reinterpret_cast<const int4*>(kps + 32 * t + 8 * a + 4 * lh);
+              if (kq.x > my_qpos[u]) sc[u][t][4 * a + 0] = -INFINITY;
+              if (kq.y > my_qpos[u]) sc[u][t][4 * a + 1] = -INFINITY;
+              if (kq.z > my_qpos[u]) sc[u][t][4 * a + 2] = -INFINITY;
+              if (kq.w > my_qpos[u]) sc[u][t][4 * a + 3] = -INFINITY;
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 16; ++e) bmax[u] = fmaxf(bmax[u], sc[u][t][e]);
+        }
+        // the step's largest scaled score (base 2) of the lane's query
+        bmax[u] = max_xor32(bmax[u]) * scale;
+        need_any |= bmax[u] > run_max[u] + 8.f;
+      }
       // Lazy rescaling: the running maximum moves (and the accumulators are
       // rescaled) only when a score exceeds it by more than 8, so every
       // probability stays below 2^8; the normalisation by the sum at the end
       // is unchanged.  A row whose keys so far are all masked keeps -inf.
-      const bool need = bmax > run_max + 8.f;
-      if (__ballot(need) != 0) {
-        const float corr = need ? __builtin_amdgcn_exp2f(run_max - bmax) : 1.f;
-        if (need) run_max = bmax;
-        run_sum *= corr;
+      if (__ballot(need_any) != 0) {
 #pragma unroll
-        for (int c = 0; c < NCH; ++c)
+        for (int u = 0; u < QT; ++u) {
+          const bool need = bmax[u] > run_max[u] + 8.f;
+          const float corr = need ? __builtin_amdgcn_exp2f(run_max[u] - bmax[u]) : 1.f;
+          if (need) run_max[u] = bmax[u];
+          run_sum[u] *= corr;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) acc[c][e] *= corr;
-      }
-      const float base = run_max == -INFINITY ? 0.f : run_max;
-      float bsum = 0.f;
+          for (int c = 0; c < NCH; ++c)
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[t][e], scale, -base));
-          sv[t][e] = pe;
-          bsum += pe;
+            for (int e = 0; e < 16; ++e) acc[u][c][e] *= corr;
         }
-      run_sum += sum_xor32(bsum);
+      }
+      // probabilities, packed to bf16 as the B operands of the value product:
+      // pf[u][kk] holds the keys 16 kk + 4 lh + 0..3 and 16 kk + 8 + 4 lh + 0..3
+      uint4 pf[QT][4];
+#pragma unroll
+      for (int u = 0; u < QT; ++u) {
+        const float base = run_max[u] == -INFINITY ? 0.f : run_max[u];
+        float bsum = 0.f;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          float pe[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[u][t][e], scale, -base));
+            bsum += pe[e];
+          }
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2)
+            pf[u][2 * t + k2] = make_uint4(pack_bf16(pe[8 * k2 + 0], pe[8 * k2 + 1]), pack_bf16(pe[8 * k2 + 2], pe[8 * k2 + 3]),
+                                           pack_bf16(pe[8 * k2 + 4], pe[8 * k2 + 5]), pack_bf16(pe[8 * k2 + 6], pe[8 * k2 + 7]));
+        }
+        run_sum[u] += sum_xor32(bsum);
+      }
 
-      // O^T += V^T P^T in 16-key steps: step kk takes the probabilities of
-      // half kk / 2, e = 8 (kk % 2) .. + 7, i.e. the keys 16 kk + 4 lh + 0..3
-      // and 16 kk + 8 + 4 lh + 0..3
-      const bool second = kf1 <= wave_last;
+      // O^T += V^T P^T in 16-key steps; each value fragment serves every
+      // query tile
       const int g = lane >> 4, pp = lane & 15;
       const int rr = pp >> 2, qq = pp & 3;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        if (kk >= 2 && !second) break;
-        const float* sp = &sv[kk >> 1][8 * (kk & 1)];
-        uint4 pf;
-        pf.x = pack_bf16(sp[0], sp[1]);
-        pf.y = pack_bf16(sp[2], sp[3]);
-        pf.z = pack_bf16(sp[4], sp[5]);
-        pf.w = pack_bf16(sp[6], sp[7]);
         const int row0 = 16 * kk + 4 * (g >> 1) + rr;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
@@ -431,8 +500,10 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
           const uint2 w0 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0)));
           const uint2 w1 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0 + 8 * 16)));
           const uint4 vf = make_uint4(w0.x, w0.y, w1.x, w1.y);
-          acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
-                                                           __builtin_bit_cast(bf16x8_t, pf), acc[c], 0, 0, 0);
+#pragma unroll
+          for (int u = 0; u < QT; ++u)
+              acc[u][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vf),
+                                                                  __builtin_bit_cast(bf16x8_t, pf[u][kk]), acc[u][c], 0, 0, 0);
         }
       }
     }
@@ -440,17 +511,20 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
     nxt = nn;
   }
 
-  // ---- O = acc / sum: lane holds query lr, features 32 c + 8 a + 4 lh + 0..3
-  if (my_qpos >= 0) {
-    const float inv = run_sum > 0.f ? 1.f / run_sum : 0.f;
-    const int64_t o = (static_cast<int64_t>(b) * p.S + my_qpos) * ldq + h * DH;
+  // ---- O = acc / sum: lane holds query lr of each tile, features
+  // 32 c + 8 a + 4 lh + 0..3
+#pragma unroll
+  for (int u = 0; u < QT; ++u) {
+    if (my_qpos[u] < 0) continue;
+    const float inv = run_sum[u] > 0.f ? 1.f / run_sum[u] : 0.f;
+    const int64_t o = (static_cast<int64_t>(b) * p.S + my_qpos[u]) * ldq + h * DH;
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const int f = 32 * c + 8 * a + 4 * lh;
-        const float v0 = acc[c][4 * a] * inv, v1 = acc[c][4 * a + 1] * inv;
-        const float v2 = acc[c][4 * a + 2] * inv, v3 = acc[c][4 * a + 3] * inv;
+        const float v0 = acc[u][c][4 * a] * inv, v1 = acc[u][c][4 * a + 1] * inv;
+        const float v2 = acc[u][c][4 * a + 2] * inv, v3 = acc[u][c][4 * a + 3] * inv;
         if (p.odtype == 0) {
           *reinterpret_cast<float4*>(static_cast<float*>(p.O) + o + f) = make_float4(v0, v1, v2, v3);
         } else {
@@ -458,8 +532,8 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
         }
       }
     if (p.lse && lh == 0) {
-      const float l = run_sum > 0.f ? (run_max + __log2f(run_sum)) * 0.6931471805599453f : -INFINITY;
-      p.lse[(static_cast<int64_t>(b) * p.n_heads + h) * p.S + my_qpos] = l;
+      const float l = run_sum[u] > 0.f ? (run_max[u] + __log2f(run_sum[u])) * 0.6931471805599453f : -INFINITY;
+      p.lse[(static_cast<int64_t>(b) * p.n_heads + h) * p.S + my_qpos[u]] = l;
     }
   }
 }
@@ -467,42 +541,41 @@ __global__ __launch_bounds__(kFwdThreads) void attn_fwd_kernel(const AttnParams 
 // ---- decode ---------------------------------------------------------------------
 
 constexpr int kDecThreads = 256;
-constexpr int kDecKeysPerTeam = 4;
+constexpr int kDecBatch = 4;  // keys per team per batch (loads issued together)
+constexpr int kDecMaxChunk = 8 * kDecBatch * kDecThreads / 8;  // the longest chunk (head width 64)
 
-template <int DH>
-constexpr int dec_chunk() { return kDecKeysPerTeam * (kDecThreads / (DH / 8)); }
-template <int DH>
-constexpr int dec_smem_max() { return static_cast<int>(sizeof(float)) * (kDecThreads / (DH / 8)) * kAttnDecHeads * DH; }
-
-// One chunk of the cache of one sequence against up to kAttnDecHeads query
-// heads that share one key/value head.
-template <int DH>
+// One chunk of the cache of one sequence against up to G query heads that
+// share one key/value head.  Teams of T = DH / 8 lanes take the keys
+// u0 + team + NT k in order, a batch of 4 at a time, and keep an online
+// softmax per head in registers (running base-2 maximum, sum, and the lane's
+// 8 output features); the teams are merged at the end through LDS.
+template <int DH, int G>
 __global__ __launch_bounds__(kDecThreads) void attn_decode_part_kernel(const AttnParams p) {
   constexpr int T = DH / 8;            // lanes per key
   constexpr int NT = kDecThreads / T;  // teams
-  constexpr int CH = dec_chunk<DH>();  // keys per chunk
-  constexpr int G = kAttnDecHeads;
-  extern __shared__ __attribute__((aligned(16))) float dsm[];  // [NT][gh][DH] team partial outputs
-  __shared__ float sc[G][CH];          // scores, then probabilities
+  extern __shared__ __attribute__((aligned(16))) float dsm[];  // [NT][gh][DH + 2] team states
   __shared__ uint32_t fm_s[32];        // F(i, j) as a bit mask, per key type j
-  __shared__ float ml_s[G][2];
+  __shared__ int32_t types_s[kDecMaxChunk];  // types of the chunk's positions
 
-  const int chunk = blockIdx.x;
-  const int hk = blockIdx.y / p.head_groups, hg = blockIdx.y % p.head_groups;
+  // the head index varies fastest over the grid: workgroups dispatched
+  // together read the same cache rows (all heads of a position are adjacent)
+  const int chunk = blockIdx.y;
+  const int hk = blockIdx.x / p.head_groups, hg = blockIdx.x % p.head_groups;
   const int b = blockIdx.z;
   const int g_all = p.n_heads / p.n_kv;
-  const int h0 = hk * g_all + hg * G;
-  const int gh = min(G, g_all - hg * G);
+  const int h0 = hk * g_all + hg * kAttnDecHeads;
+  const int gh = min(G, g_all - hg * kAttnDecHeads);
   const int q = p.q, m = DH / q;
   const int32_t L = min(p.cache_len[b], p.S);
-  const int32_t u0 = chunk * CH;
+  const int32_t u0 = chunk * p.chunk;
   if (L <= 0 || u0 >= L) return;
   const int i = p.pos_type[L - 1];
   if (static_cast<unsigned>(i) >= static_cast<unsigned>(q)) return;  // the merge writes zeros
-  const int32_t u1 = min(L, u0 + CH);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t u1 = min(L, u0 + p.chunk);
+  const int tid = threadIdx.x;
   const int team = tid / T, t = tid % T;
   if (tid < q) fm_s[tid] = attn_fmask(p.law, q, i, tid);
+  for (int32_t r = tid; r < u1 - u0; r += kDecThreads) types_s[r] = p.pos_type[u0 + r];
 
   const int64_t ldq = static_cast<int64_t>(p.n_heads) * DH, ldk = static_cast<int64_t>(p.n_kv) * DH;
   const uint16_t* Kc = static_cast<const uint16_t*>(p.K) + static_cast<int64_t>(b) * p.S * ldk + hk * DH + 8 * t;
@@ -523,118 +596,133 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_part_kernel(const Att
   __syncthreads();
   const int al = (8 * t) / m;  // the lane's feature group
 
-  // ---- scores of the team's keys u0 + team + NT k
-  int32_t jt[kDecKeysPerTeam];
-  uint4 kv[kDecKeysPerTeam];
+  float mrun[G], lrun[G], o[G][8];
 #pragma unroll
-  for (int k = 0; k < kDecKeysPerTeam; ++k) {
-    const int32_t u = u0 + team + NT * k;
-    jt[k] = u < u1 ? p.pos_type[u] : -1;
-    const bool key_ok = static_cast<unsigned>(jt[k]) < static_cast<unsigned>(q);
-    kv[k] = make_uint4(0, 0, 0, 0);
-    if (key_ok && ((fm_s[key_ok ? jt[k] : 0] >> al) & 1u)) kv[k] = *reinterpret_cast<const uint4*>(Kc + static_cast<int64_t>(u) * ldk);
-  }
-#pragma unroll
-  for (int k = 0; k < kDecKeysPerTeam; ++k) {
-    const uint32_t w[4] = {kv[k].x, kv[k].y, kv[k].z, kv[k].w};
-    float kf[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      kf[2 * e] = bf16_to_f32(w[e] & 0xffffu);
-      kf[2 * e + 1] = bf16_to_f32(w[e] >> 16);
-    }
-    float d[G];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-      float a = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a += qf[hh][e] * kf[e];
-      d[hh] = a;
-    }
-#pragma unroll
-    for (int o = T / 2; o > 0; o >>= 1)
-#pragma unroll
-      for (int hh = 0; hh < G; ++hh) d[hh] += __shfl_xor(d[hh], o, T);
-    const int32_t u = u0 + team + NT * k;
-    if (t == 0 && u < u1) {
-      const bool key_ok = static_cast<unsigned>(jt[k]) < static_cast<unsigned>(q);
-      const float scale = key_ok ? kLog2e * __builtin_amdgcn_rsqf(static_cast<float>(__popc(fm_s[jt[k]]) * m)) : 0.f;
-#pragma unroll
-      for (int hh = 0; hh < G; ++hh) sc[hh][u - u0] = key_ok ? d[hh] * scale : -INFINITY;
-    }
-  }
-  __syncthreads();
-
-  // ---- the chunk's softmax, one wave per head
-  const int32_t n = u1 - u0;
-  for (int hh = wave; hh < gh; hh += kDecThreads / 64) {
-    float mx = -INFINITY;
-    for (int32_t u = lane; u < n; u += 64) mx = fmaxf(mx, sc[hh][u]);
-    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-    float sum = 0.f;
-    for (int32_t u = lane; u < n; u += 64) {
-      const float e = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[hh][u] - mx);
-      sc[hh][u] = e;
-      sum += e;
-    }
-    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
-    if (lane == 0) {
-      ml_s[hh][0] = mx;
-      ml_s[hh][1] = sum;
-    }
-  }
-  __syncthreads();
-
-  // ---- the team's weighted value rows, then the teams summed in order
-  uint4 vv[kDecKeysPerTeam];
-#pragma unroll
-  for (int k = 0; k < kDecKeysPerTeam; ++k) {
-    const int32_t u = u0 + team + NT * k;
-    vv[k] = make_uint4(0, 0, 0, 0);
-    if (u < u1) vv[k] = *reinterpret_cast<const uint4*>(Vc + static_cast<int64_t>(u) * ldk);
-  }
-  float o[G][8];
-#pragma unroll
-  for (int hh = 0; hh < G; ++hh)
+  for (int hh = 0; hh < G; ++hh) {
+    mrun[hh] = -INFINITY;
+    lrun[hh] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[hh][e] = 0.f;
+  }
+  // key u of batch kb of this team: ub(kb) + NT k with ub(kb) = u0 + team +
+  // kBatch NT kb; its type (or -1 past the chunk) from LDS
+  const int32_t n = u1 - u0;
+  const int nb = (n - team + kDecBatch * NT - 1) / (kDecBatch * NT);  // batches of this team
+  struct Batch {
+    uint4 kv[kDecBatch], vv[kDecBatch];
+    int32_t jt[kDecBatch];
+  };
+  auto load = [&](int kb, Batch& bt) {
 #pragma unroll
-  for (int k = 0; k < kDecKeysPerTeam; ++k) {
-    const int32_t u = u0 + team + NT * k;
-    if (u >= u1) continue;
-    const uint32_t w[4] = {vv[k].x, vv[k].y, vv[k].z, vv[k].w};
-    float vf[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      vf[2 * e] = bf16_to_f32(w[e] & 0xffffu);
-      vf[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+    for (int k = 0; k < kDecBatch; ++k) {
+      const int32_t r = team + NT * (kDecBatch * kb + k);  // position within the chunk
+      const int32_t j = r < n ? types_s[r] : -1;
+      bt.jt[k] = j;
+      const bool key_ok = static_cast<unsigned>(j) < static_cast<unsigned>(q);
+      const int64_t u = u0 + r;
+      bt.kv[k] = make_uint4(0, 0, 0, 0);
+      bt.vv[k] = make_uint4(0, 0, 0, 0);
+      if (key_ok && ((fm_s[key_ok ? j : 0] >> al) & 1u)) bt.kv[k] = *reinterpret_cast<const uint4*>(Kc + u * ldk);
+      if (key_ok) bt.vv[k] = *reinterpret_cast<const uint4*>(Vc + u * ldk);
     }
+  };
+  auto compute = [&](const Batch& bt) {
+    // scores (base 2), -inf for keys past the chunk or of an out-of-range type
+    float sc[kDecBatch][G];
+#pragma unroll
+    for (int k = 0; k < kDecBatch; ++k) {
+      const uint32_t w[4] = {bt.kv[k].x, bt.kv[k].y, bt.kv[k].z, bt.kv[k].w};
+      float kf[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        kf[2 * e] = bf16_to_f32(w[e] & 0xffffu);
+        kf[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+      }
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a += qf[hh][e] * kf[e];
+        sc[k][hh] = a;
+      }
+#pragma unroll
+      for (int o2 = T / 2; o2 > 0; o2 >>= 1)
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) sc[k][hh] += __shfl_xor(sc[k][hh], o2, T);
+      const bool key_ok = static_cast<unsigned>(bt.jt[k]) < static_cast<unsigned>(q);
+      const float scale = key_ok ? kLog2e * __builtin_amdgcn_rsqf(static_cast<float>(__popc(fm_s[key_ok ? bt.jt[k] : 0]) * m)) : 0.f;
+#pragma unroll
+      for (int hh = 0; hh < G; ++hh) sc[k][hh] = key_ok ? sc[k][hh] * scale : -INFINITY;
+    }
+    // online softmax update per head
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
-      const float pw = hh < gh ? sc[hh][u - u0] : 0.f;
+      float bm = sc[0][hh];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[hh][e] += pw * vf[e];
+      for (int k = 1; k < kDecBatch; ++k) bm = fmaxf(bm, sc[k][hh]);
+      const float nm = fmaxf(mrun[hh], bm);
+      if (nm == -INFINITY) continue;  // nothing valid yet (team-uniform)
+      const float corr = __builtin_amdgcn_exp2f(mrun[hh] - nm);
+      mrun[hh] = nm;
+      lrun[hh] *= corr;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[hh][e] *= corr;
+#pragma unroll
+      for (int k = 0; k < kDecBatch; ++k) {
+        const float pk = __builtin_amdgcn_exp2f(sc[k][hh] - nm);
+        lrun[hh] += pk;
+        const uint32_t w[4] = {bt.vv[k].x, bt.vv[k].y, bt.vv[k].z, bt.vv[k].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[hh][2 * e] += pk * bf16_to_f32(w[e] & 0xffffu);
+          o[hh][2 * e + 1] += pk * bf16_to_f32(w[e] >> 16);
+        }
+      }
     }
+  };
+  // two batches in flight: the next batch's rows are requested before the
+  // current one is used
+  Batch b0, b1;
+  if (nb > 0) load(0, b0);
+  for (int kb = 0; kb < nb; kb += 2) {
+    if (kb + 1 < nb) load(kb + 1, b1);
+    compute(b0);
+    if (kb + 1 >= nb) break;
+    if (kb + 2 < nb) load(kb + 2, b0);
+    compute(b1);
   }
+  // ---- merge the teams: state of team tm, head hh at dsm[(tm gh + hh)(DH + 2)]
 #pragma unroll
   for (int hh = 0; hh < G; ++hh) {
     if (hh >= gh) break;
-    float* dst = dsm + (static_cast<int64_t>(team) * gh + hh) * DH + 8 * t;
-    *reinterpret_cast<float4*>(dst) = make_float4(o[hh][0], o[hh][1], o[hh][2], o[hh][3]);
-    *reinterpret_cast<float4*>(dst + 4) = make_float4(o[hh][4], o[hh][5], o[hh][6], o[hh][7]);
+    float* dst = dsm + (static_cast<int64_t>(team) * gh + hh) * (DH + 2);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dst[8 * t + e] = o[hh][e];
+    if (t == 0) {
+      dst[DH] = mrun[hh];
+      dst[DH + 1] = lrun[hh];
+    }
   }
   __syncthreads();
   const int64_t slot0 = (static_cast<int64_t>(b) * p.n_heads + h0) * p.nchunks + chunk;
   for (int x = tid; x < gh * DH; x += kDecThreads) {
     const int hh = x / DH, f = x % DH;
-    float a = 0.f;
-    for (int tm = 0; tm < NT; ++tm) a += dsm[(tm * gh + hh) * DH + f];
-    p.part_o[(slot0 + static_cast<int64_t>(hh) * p.nchunks) * DH + f] = a;
-  }
-  if (tid < gh) {
-    const int64_t s = slot0 + static_cast<int64_t>(tid) * p.nchunks;
-    p.part_ml[2 * s] = ml_s[tid][0];
-    p.part_ml[2 * s + 1] = ml_s[tid][1];
+    float M = -INFINITY;
+    for (int tm = 0; tm < NT; ++tm) M = fmaxf(M, dsm[(tm * gh + hh) * (DH + 2) + DH]);
+    float a = 0.f, l = 0.f;
+    if (M != -INFINITY)
+      for (int tm = 0; tm < NT; ++tm) {
+        const float* st = dsm + (tm * gh + hh) * (DH + 2);
+        const float w = __builtin_amdgcn_exp2f(st[DH] - M);
+        a += w * st[f];
+        l += w * st[DH + 1];
+      }
+    const int64_t sl = slot0 + static_cast<int64_t>(hh) * p.nchunks;
+    p.part_o[sl * DH + f] = a;
+    if (f == 0) {
+      p.part_ml[2 * sl] = M;
+      p.part_ml[2 * sl + 1] = l;
+    }
   }
 }
 
@@ -642,14 +730,13 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_part_kernel(const Att
 // sum_c 2^(m_c - M) l_c with M the largest chunk maximum.
 template <int DH>
 __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(const AttnParams p) {
-  constexpr int CH = dec_chunk<DH>();
   const int b = blockIdx.x / p.n_heads, h = blockIdx.x % p.n_heads;
   const int f = threadIdx.x;
   const int32_t L = min(p.cache_len[b], p.S);
   float v = 0.f;
   const bool ok = L > 0 && static_cast<unsigned>(p.pos_type[L - 1]) < static_cast<unsigned>(p.q);
   if (ok) {
-    const int32_t nch = (L + CH - 1) / CH;
+    const int32_t nch = (L + p.chunk - 1) / p.chunk;
     const int64_t s0 = (static_cast<int64_t>(b) * p.n_heads + h) * p.nchunks;
     float mx = -INFINITY;
     for (int32_t c = 0; c < nch; ++c) mx = fmaxf(mx, p.part_ml[2 * (s0 + c)]);
@@ -666,29 +753,39 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(const AttnParams 
   store_out(p.O, p.odtype, static_cast<int64_t>(b) * p.n_heads * DH + h * DH + f, v);
 }
 
-template <int DH>
+template <int DH, bool M8>
 hipError_t launch_fwd_dh(const AttnParams& p, unsigned grid, hipStream_t stream) {
   static std::atomic<unsigned long long> set{0};
-  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(attn_fwd_kernel<DH>), set, fwd_smem<DH>());
+  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(attn_fwd_kernel<DH, M8>), set, fwd_smem<DH>());
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_fwd_kernel<DH>, dim3(grid), dim3(kFwdThreads), fwd_smem<DH>(), stream, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<DH, M8>), dim3(grid), dim3(fwd_threads<DH>()), fwd_smem<DH>(), stream, p);
   return hipGetLastError();
 }
 
-template <int DH>
-hipError_t launch_decode_dh(const AttnParams& p, hipStream_t stream) {
+template <int DH, int G>
+hipError_t launch_decode_g(const AttnParams& p, hipStream_t stream) {
   constexpr int T = DH / 8;
-  const int gmax = std::min(kAttnDecHeads, p.n_heads / p.n_kv);
-  const size_t smem = sizeof(float) * static_cast<size_t>(kDecThreads / T) * gmax * DH;
+  const size_t smem = sizeof(float) * static_cast<size_t>(kDecThreads / T) * G * (DH + 2);
   static std::atomic<unsigned long long> set{0};
-  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(attn_decode_part_kernel<DH>), set, dec_smem_max<DH>());
+  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(attn_decode_part_kernel<DH, G>), set, static_cast<int>(smem));
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_decode_part_kernel<DH>, dim3(p.nchunks, p.n_kv * p.head_groups, p.B), dim3(kDecThreads), smem,
-                     stream, p);
+  hipLaunchKernelGGL((attn_decode_part_kernel<DH, G>), dim3(p.n_kv * p.head_groups, p.nchunks, p.B), dim3(kDecThreads),
+                     smem, stream, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(attn_decode_merge_kernel<DH>, dim3(p.B * p.n_heads), dim3(DH), 0, stream, p);
   return hipGetLastError();
+}
+
+// query heads per workgroup: the group size rounded up to a power of two,
+// at most kAttnDecHeads
+template <int DH>
+hipError_t launch_decode_dh(const AttnParams& p, hipStream_t stream) {
+  const int g = std::min(kAttnDecHeads, p.n_heads / p.n_kv);
+  if (g <= 1) return launch_decode_g<DH, 1>(p, stream);
+  if (g <= 2) return launch_decode_g<DH, 2>(p, stream);
+  if (g <= 4) return launch_decode_g<DH, 4>(p, stream);
+  return launch_decode_g<DH, 8>(p, stream);
 }
 
 }  // namespace
@@ -698,14 +795,24 @@ hipError_t launch_attn_fwd(const AttnParams& p, hipStream_t stream) {
   const int64_t grid = 8 * ((items + 7) / 8);
   if (items <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   switch (p.head_dim) {
-    case 64: return launch_fwd_dh<64>(p, static_cast<unsigned>(grid), stream);
-    case 128: return launch_fwd_dh<128>(p, static_cast<unsigned>(grid), stream);
+    case 64:
+      return p.head_dim / p.q == 8 ? launch_fwd_dh<64, true>(p, static_cast<unsigned>(grid), stream)
+                                   : launch_fwd_dh<64, false>(p, static_cast<unsigned>(grid), stream);
+    case 128:
+      return p.head_dim / p.q == 8 ? launch_fwd_dh<128, true>(p, static_cast<unsigned>(grid), stream)
+                                   : launch_fwd_dh<128, false>(p, static_cast<unsigned>(grid), stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-int32_t attn_decode_chunk(int32_t head_dim) {
-  return head_dim == 64 ? dec_chunk<64>() : head_dim == 128 ? dec_chunk<128>() : 0;
+int32_t attn_decode_chunk(int32_t head_dim, int32_t batch, int32_t n_kv, int32_t head_groups, int32_t S) {
+  // one batch of keys per team is the least; longer chunks (fewer, longer
+  // workgroups, less merging) while the grid keeps about 2048 workgroups
+  const int32_t base = kDecBatch * (kDecThreads / (head_dim / 8));
+  int32_t chunk = base;
+  const int64_t rows = static_cast<int64_t>(batch) * n_kv * head_groups;
+  while (chunk < 8 * base && rows * ((S + 2 * chunk - 1) / (2 * chunk)) >= 2048) chunk *= 2;
+  return chunk;
 }
 
 hipError_t launch_attn_decode(const AttnParams& p, hipStream_t stream) {

@@ -211,11 +211,13 @@ struct AttnParams {
   float* part_ml;            // [B][n_heads][nchunks][2]: running max (base 2), sum
 };
 constexpr int kAttnDecHeads = 8;  // query heads per decode workgroup
+constexpr int32_t kAttnFwdMaxSeq = 1 << 18;  // positions per sequence in the forward
 // Forward work items per (sequence, head): 128-row query blocks over all types.
 inline int32_t attn_fwd_items(int32_t S, int32_t q) { return (S + 127 * q) / 128; }
 hipError_t launch_attn_fwd(const AttnParams& p, hipStream_t stream);
-// Keys per decode split for a head width.
-int32_t attn_decode_chunk(int32_t head_dim);
+// Keys per decode split for a shape (a multiple of the 4 keys per team of
+// one batch; the same for every call with that shape).
+int32_t attn_decode_chunk(int32_t head_dim, int32_t batch, int32_t n_kv, int32_t head_groups, int32_t S);
 hipError_t launch_attn_decode(const AttnParams& p, hipStream_t stream);
 
 // The static workspace of star_decode_noalloc (scratch.hip): its size, and
