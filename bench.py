@@ -15,12 +15,14 @@ through the same kernels), warm and cache-flushed kernel times, the decode
 stack (12 layers, M in {1, 8, 32, 64}) in HBM GB/s and FFN tokens/s, the
 roofline of the dominant kernel measured with HIP events, and the CPU oracle
 timed on this host, plus the FFN training step (M = 16384, forward and
-backward) and the fixed-block q sweep (q = 2..16) unless ``--no-extra``.
+backward), the fixed-block q sweep (q = 2..16), the tensor-square and pilot
+FFNs, and algebraic attention (causal forward and one decode step) unless
+``--no-extra``.
 
 Every figure follows the paper's timing protocol: twelve trials per
 configuration alternating the star law and its dense control, warm trials of
 back-to-back runs lasting at least 2 ms, cache-flushed trials of one run
-after touching 512 MiB, medians reported.
+after reading 512 MiB of another buffer, medians reported.
 """
 
 from __future__ import annotations
@@ -88,8 +90,9 @@ class Protocol:
     held-out trials alternate the order of the methods compared (the star
     law and its same-code dense control); a warm trial replays one method
     back to back until the faster method's replays take at least 2 ms, a
-    cache-flushed trial touches 512 MiB outside the timed interval and times
-    a single run; the figures reported are medians over the trials.  Every
+    cache-flushed trial reads 512 MiB of another buffer outside the timed
+    interval and times a single run; the figures reported are medians over
+    the trials.  Every
     time comes from HIP events on the stream the library launches on."""
 
     def __init__(self, torch, flush, trials):
@@ -212,10 +215,16 @@ def main():
     import paper_2609_32814_amd as P
     import synth
 
-    flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    # Cache flush: stream 512 MiB (twice the Infinity Cache) of another
+    # buffer through the caches by *reading* it.  Writing it instead (a fill)
+    # leaves the caches full of dirty lines whose write-backs then compete
+    # with the timed kernel's reads: a plain 201 MB streaming read measured
+    # 2.84 TB/s after a 512 MiB fill and 5.9-6.1 TB/s after this read pass.
+    flush_buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    flush_sink = torch.empty((), dtype=torch.float32, device=dev)
 
     def flush():
-        flush_buf.fill_(1.0)
+        torch.sum(flush_buf, dim=0, out=flush_sink)
 
     T = Protocol(torch, flush, args.trials)
 
@@ -346,6 +355,7 @@ def main():
         result["qsweep"] = bench_qsweep(P, synth, torch, np, dev, T, flush, args)
         result["tensor2"] = bench_tensor2(P, synth, torch, np, dev, T, args)
         result["pilot_ffn"] = bench_pilot_ffn(P, synth, torch, np, dev, T, args)
+        result["attention"] = bench_attention(P, synth, torch, np, dev, T, flush, args)
 
     # ---- CPU oracle baseline -------------------------------------------------
     if not args.no_cpu:
@@ -440,7 +450,7 @@ def bench_decode(P, synth, torch, np, dev, T, flush, args):
             f"({s['GBps_flushed']} GB/s flushed), dense {res['dense']['step_us_warm']} us warm; "
             f"status clear {status_clear}")
     out["protocol"] = f"medians of {T.trials} trials alternating star and dense; warm = back-to-back steps, " \
-                      "flushed = one step after touching 512 MiB"
+                      "flushed = one step after reading 512 MiB of another buffer"
     return out
 
 
@@ -624,6 +634,106 @@ def bench_pilot_ffn(P, synth, torch, np, dev, T, args):
         dec[f"M{Md}"] = one
     res["decode"] = dec
     log("pilot_ffn:", json.dumps(res))
+    return res
+
+
+def attn_pair_macs(pt, q, law, m, dh, oracle_in_group):
+    """Multiply-accumulates of one causal head over one sequence: every
+    allowed pair (u <= p) costs |F(i, j)| m for the score plus d_h for the
+    value aggregation (eqs. attention-raw-score, softmax-pv)."""
+    import numpy as np
+    S = len(pt)
+    onehot = np.zeros((S, q), np.int64)
+    onehot[np.arange(S), pt] = 1
+    upto = np.cumsum(onehot, axis=0)  # keys of type j at positions <= p
+    pairs = np.zeros((q, q), np.int64)
+    np.add.at(pairs, pt, upto)        # pairs[i][j]: queries of type i with keys of type j
+    nf = np.array([[sum(oracle_in_group(law, i, j, a) for a in range(q)) for j in range(q)] for i in range(q)])
+    score = int((pairs * nf).sum()) * m
+    return score + int(pairs.sum()) * dh, int(pairs.sum()), int(np.trace(pairs))
+
+
+def bench_attention(P, synth, torch, np, dev, T, flush, args):
+    """Algebraic attention (appendix "Attention Extension"): the causal
+    forward at 16 sequences x 1536 positions (the pilot's context), 12 heads
+    of 64 (the 110M-class width 768), q = 4 (star law Q_4, and the tensor
+    square with the interval schedule) and q = 2, each beside the same-code
+    dense control; and one decode step over a 2048-position cache for
+    M in {1, 8, 32, 64} sequences at random positions."""
+    F_IN = lambda law, i, j, a: (law == "dense") or (law == "tensor2" and ((a ^ i) & (a ^ j)) == 0) or \
+        (law == "star" and a in (i, j))
+    B, S, H, D = 16, 1536, 12, 64
+    Q = torch.randn(B, S, H, D, device=dev).to(torch.bfloat16)
+    K = torch.randn(B, S, H, D, device=dev).to(torch.bfloat16)
+    V = torch.randn(B, S, H, D, device=dev).to(torch.bfloat16)
+    O = torch.empty(B, S, H, D, device=dev, dtype=torch.bfloat16)
+    fwd = {"workload": "causal algebraic attention forward, 16 x 1536 positions, 12 heads of 64, bf16 in, "
+                       "fp32 softmax, bf16 out; flops: 2 x (|F| m score + d_h value) per allowed pair"}
+    for q, law, kind in ((4, "star", "cyclic"), (4, "tensor2", "interval"), (2, "star", "cyclic")):
+        pt = (np.arange(S) % q if kind == "cyclic" else (np.arange(S) % 768) // (768 // q)).astype(np.int32)
+        plan = P.star_type_plan(q, torch.from_numpy(pt).to(dev))
+        shapes = {lw: P.AttnShape(B, S, H, H, D, q, lw) for lw in (law, "dense")}
+        r = T.compare({lw: (lambda sh=sh: P.star_attn_fwd(sh, plan, Q, K, V, O=O)) for lw, sh in shapes.items()})
+        one = {"q": q, "schedule": kind}
+        for lw in (law, "dense"):
+            macs, pairs, same = attn_pair_macs(pt, q, lw, D // q, D, F_IN)
+            fl = 2.0 * macs * B * H
+            us = r[lw]["warm_ms"] * 1e3
+            one[lw] = {"kernel_us": round(us, 1), "kernel_us_flushed": round(r[lw]["flushed_ms"] * 1e3, 1),
+                       "tflops": round(fl / (us * 1e-6) / 1e12, 1), "gflop": round(fl / 1e9, 2),
+                       "mfma_peak_frac": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        macs_s, _, _ = attn_pair_macs(pt, q, law, D // q, D, F_IN)
+        macs_d, pairs, _ = attn_pair_macs(pt, q, "dense", D // q, D, F_IN)
+        rho = (macs_s - pairs * D) / (pairs * D)  # score fraction (eq. attention-exact-ratio for Q_q)
+        one["rho_score"] = round(rho, 4)
+        one["speedup"] = round(one["dense"]["kernel_us"] / one[law]["kernel_us"], 3)
+        one["ceiling_2_over_1_plus_rho"] = round(2 / (1 + rho), 3)
+        fwd[f"{law}_q{q}"] = one
+    # torch's own causal attention on the same dense problem, for reference
+    qt, kt, vt = (x.transpose(1, 2).contiguous() for x in (Q, K, V))
+    r = T.compare({"sdpa": lambda: torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)},
+                  flushed=False)
+    fwd["torch_sdpa_dense_us"] = round(r["sdpa"]["warm_ms"] * 1e3, 1)
+    del Q, K, V, O, qt, kt, vt
+    torch.cuda.empty_cache()
+
+    # ---- one decode step over the cache
+    Smax, q = 2048, 4
+    pt_all = (np.arange(Smax) % q).astype(np.int32)
+    ptd = torch.from_numpy(pt_all).to(dev)
+    dec = {"workload": "one decode step, cache of 2048 positions x 12 heads of 64 (bf16), q = 4, "
+                       "positions rng.integers(0, 2048, M); bytes: the selected key groups + full value rows"}
+    for Md in (1, 8, 32, 64):
+        pos = synth.decode_positions(9, Md)
+        Ld = torch.from_numpy((pos + 1).astype(np.int32)).to(dev)
+        Kc = torch.randn(Md, Smax, H, D, device=dev).to(torch.bfloat16)
+        Vc = torch.randn(Md, Smax, H, D, device=dev).to(torch.bfloat16)
+        Qd = torch.randn(Md, H, D, device=dev).to(torch.bfloat16)
+        Od = torch.empty(Md, H, D, device=dev, dtype=torch.bfloat16)
+        shapes = {lw: P.AttnShape(Md, Smax, H, H, D, q, lw) for lw in ("star", "dense")}
+        ws = torch.empty(P.star_attn_decode_workspace_bytes(shapes["star"]), dtype=torch.uint8, device=dev)
+        r = T.compare({lw: (lambda sh=sh: P.star_attn_decode(sh, ptd, Ld, Qd, Kc, Vc, O=Od, ws=ws))
+                       for lw, sh in shapes.items()})
+        one = {}
+        for lw in ("star", "dense"):
+            nbytes = 0
+            for b in range(Md):
+                L = int(pos[b]) + 1
+                i = pt_all[L - 1]
+                js = pt_all[:L]
+                nf = np.array([sum(F_IN(lw, i, j, a) for a in range(q)) for j in range(q)])[js]
+                nbytes += (int(nf.sum()) * (D // q) + L * D) * 2 * H
+            us = r[lw]["warm_ms"] * 1e3
+            usf = r[lw]["flushed_ms"] * 1e3
+            one[lw] = {"step_us_warm": round(us, 1), "step_us_flushed": round(usf, 1),
+                       "gbs_flushed": round(nbytes / (usf * 1e-6) / 1e9, 1), "mbytes": round(nbytes / 1e6, 1),
+                       "hbm_frac_flushed": round(nbytes / (usf * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        one["speedup_warm"] = round(one["dense"]["step_us_warm"] / one["star"]["step_us_warm"], 3)
+        dec[f"M{Md}"] = one
+        del Kc, Vc
+        torch.cuda.empty_cache()
+    res = {"forward": fwd, "decode": dec}
+    log("attention:", json.dumps(res))
     return res
 
 
