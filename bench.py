@@ -81,6 +81,8 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 256 MiB device copy (for HBM counter calibration)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--attention-only", action="store_true",
+                    help="only the algebraic-attention section (for profiling its kernels)")
     return ap.parse_args()
 
 
@@ -227,6 +229,9 @@ def main():
         torch.sum(flush_buf, dim=0, out=flush_sink)
 
     T = Protocol(torch, flush, args.trials)
+    if args.attention_only:
+        print(json.dumps({"attention": bench_attention(P, synth, torch, np, dev, T, flush, args)}), flush=True)
+        return
 
     # ---- primary workload ----------------------------------------------------
     M, K, N, q, SEQ = 8192, 768, 3072, 2, 1024
