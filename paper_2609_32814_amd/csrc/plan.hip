@@ -1,7 +1,8 @@
 // Type plan: the per-type row index sets I_i of Alg. 1 as one stable
 // permutation of the rows grouped by type, plus per-type offsets.
 //
-// One workgroup of 1024 threads (16 wavefronts).  All threads first copy the
+// Up to 64 Ki rows: many workgroups (type_plan_wide_kernel below).  Longer
+// type vectors: one workgroup of 1024 threads (16 wavefronts).  All threads first copy the
 // type vector into LDS as bytes with independent coalesced loads (one round
 // trip to memory instead of one per window), for up to 64 Ki rows; longer
 // vectors are read from memory in the passes below.  The rows are cut into
@@ -131,6 +132,79 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
   }
 }
 
+// Many-workgroup plan for M <= kPlanLdsRows: workgroup g places rows
+// [1024 g, 1024 g + 1024).  Every workgroup reads the whole type vector
+// (at most 256 KB, from L2) and counts, per type, all rows and the rows
+// before its own range; the type offsets and its own bases follow without
+// any cross-workgroup synchronisation.  Its rows then go out in order: the
+// rank of a row is the number of rows of its type in earlier wavefronts of
+// the workgroup plus those in earlier lanes of its own (ballots), so the
+// permutation is stable.  Workgroup 0 writes the offsets.
+constexpr int kPlanRowsPerBlock = kPlanThreads;
+
+__global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int32_t* __restrict__ types,
+                                                                      int32_t M, int q, int nbits,
+                                                                      int32_t* __restrict__ perm,
+                                                                      int32_t* __restrict__ offsets) {
+  __shared__ int32_t total[kMaxQ + 1], before[kMaxQ + 1];
+  __shared__ int32_t wcount[kPlanWaves][kMaxQ + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t r0 = blockIdx.x * kPlanRowsPerBlock;
+  for (int i = threadIdx.x; i <= q; i += kPlanThreads) total[i] = before[i] = 0;
+  for (int i = threadIdx.x; i < kPlanWaves * (kMaxQ + 1); i += kPlanThreads) (&wcount[0][0])[i] = 0;
+  __syncthreads();
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  auto cls = [&](int t) { return (t >= 0 && t < q) ? t : q; };
+  // per-type counts over all rows and over the rows before r0, a 64-row
+  // window per wavefront at a time, 8 windows' loads in flight
+  constexpr int kBatch = 8;
+  for (int32_t base = 0; base < M; base += kPlanThreads * kBatch) {
+    int v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int32_t row = base + u * kPlanThreads + threadIdx.x;
+      v[u] = row < M ? types[row] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int32_t wrow = base + u * kPlanThreads + wave * 64;  // the window's first row (wave-uniform)
+      if (wrow >= M) break;
+      const int32_t row = wrow + lane;
+      const bool in = row < M;
+      const int t = cls(v[u]);
+      const uint64_t active = __ballot(in);
+      const uint64_t m = match_type(t, t < q, nbits) & active;
+      if (in && (m & lt_mask) == 0) {
+        atomicAdd(&total[t], __popcll(m));
+        if (wrow < r0) atomicAdd(&before[t], __popcll(m));  // windows never straddle r0
+      }
+    }
+  }
+  // this workgroup's rows: per-wavefront counts per type
+  const int32_t row = r0 + threadIdx.x;
+  const bool in = row < M;
+  const int t = in ? cls(types[row]) : 0;
+  const uint64_t active = __ballot(in);
+  const uint64_t m = match_type(t, t < q, nbits) & active;
+  if (in && (m & lt_mask) == 0) wcount[wave][t] = __popcll(m);
+  __syncthreads();
+  if (in) {
+    // offset of type t, the rows of type t before this workgroup and before
+    // this wavefront in it, and the lanes below this one
+    int32_t pos = 0;
+    for (int u = 0; u < t; ++u) pos += total[u];
+    pos += before[t];
+    for (int w = 0; w < wave; ++w) pos += wcount[w][t];
+    pos += __popcll(m & lt_mask);
+    perm[pos] = row;
+  }
+  if (blockIdx.x == 0 && threadIdx.x <= q) {
+    int32_t o = 0;
+    for (int u = 0; u < static_cast<int>(threadIdx.x); ++u) o += total[u];
+    offsets[threadIdx.x] = o;
+  }
+}
+
 __global__ void count_bad_types_kernel(const int32_t* __restrict__ types, int64_t M, int q,
                                        unsigned long long* __restrict__ n_bad) {
   unsigned long long local = 0;
@@ -149,8 +223,14 @@ hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* per
                             int32_t* offsets, hipStream_t stream) {
   int nbits = 0;
   while ((1 << nbits) < q + 1) ++nbits;
-  hipLaunchKernelGGL(type_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, types,
-                     static_cast<int32_t>(M), q, nbits, perm, offsets);
+  if (M > 0 && M <= kPlanLdsRows) {
+    const unsigned blocks = static_cast<unsigned>((M + kPlanRowsPerBlock - 1) / kPlanRowsPerBlock);
+    hipLaunchKernelGGL(type_plan_wide_kernel, dim3(blocks), dim3(kPlanThreads), 0, stream, types,
+                       static_cast<int32_t>(M), q, nbits, perm, offsets);
+  } else {
+    hipLaunchKernelGGL(type_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, types,
+                       static_cast<int32_t>(M), q, nbits, perm, offsets);
+  }
   return hipGetLastError();
 }
 
