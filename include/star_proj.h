@@ -333,6 +333,21 @@ star_status star_proj_bwd_weight_planned(const star_algebra *alg, int64_t M, con
                                          star_dtype dyt, float *dW, float *dbias, void *ws,
                                          size_t ws_bytes, hipStream_t stream);
 
+/* Tile size of the forward product for bf16 operands (Sec. "Kernel Scaling
+ * on Transformer Shapes": the algebraic kernel's tile is calibrated per
+ * shape).  STAR_TILES_AUTO, the default, takes tiles of 64 rows x 128
+ * columns when the 256 x 256 tiles would be at most three quarters full
+ * (rows taken as spread evenly over the types) or fewer than 128;
+ * STAR_TILES_WIDE and STAR_TILES_SMALL force one size.  Input groups
+ * narrower than 64 always take the small tiles, fp32 operands always their
+ * own kernel.  Applies to star_proj_fwd, star_proj_fwd_planned and the
+ * projections of star_ffn_fwd.  Process-wide (every device and stream),
+ * read when a call launches.  Returns the previous choice, or -1 (nothing
+ * changed) for a value outside the enum.  Both sizes give the same results
+ * to rounding: the K order within a group is the same, the tiles differ. */
+typedef enum { STAR_TILES_AUTO = 0, STAR_TILES_WIDE = 1, STAR_TILES_SMALL = 2 } star_tiles;
+int star_set_fwd_tiles(int tiles);
+
 /* Workspace bytes an entry point needs (alg2 is the down algebra for
  * STAR_OP_FFN_FWD and STAR_OP_DECODE, else ignored).  Returns 0 for invalid
  * arguments. */

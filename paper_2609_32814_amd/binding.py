@@ -70,6 +70,8 @@ def _load() -> ctypes.CDLL:
     lib.star_workspace_bytes.argtypes = [i32, A, A, i64]
     lib.star_workspace_bytes.restype = sz
     lib.star_count_products.argtypes = [A, ctypes.POINTER(i64)]
+    lib.star_set_fwd_tiles.argtypes = [ctypes.c_int]
+    lib.star_set_fwd_tiles.restype = ctypes.c_int
     lib.star_count_macs.argtypes = [A, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.star_validate_types.argtypes = [i64, P, i32, ctypes.POINTER(i64), P, sz, P]
     lib.star_plan_bytes.argtypes = [i32, i64]
@@ -234,6 +236,19 @@ def star_status_string(status: int) -> str:
 
 def star_workspace_bytes(op: str, alg: Algebra, alg2: Algebra | None, M: int) -> int:
     return int(LIB.star_workspace_bytes(OPS[op], alg.ref, alg2.ref if alg2 else None, int(M)))
+
+
+TILES = {"auto": 0, "wide": 1, "small": 2}
+
+
+def star_set_fwd_tiles(tiles: str) -> str:
+    """Forward tile size for bf16 operands: "auto" (by the wide tiles' fill),
+    "wide" (256 x 256) or "small" (64 x 128); process-wide.  Returns the
+    previous setting."""
+    if tiles not in TILES:
+        raise ValueError(f"tiles must be one of {sorted(TILES)}, not {tiles!r}")
+    prev = int(LIB.star_set_fwd_tiles(TILES[tiles]))
+    return {v: k for k, v in TILES.items()}[prev]
 
 
 def star_count_products(alg: Algebra) -> list[int]:

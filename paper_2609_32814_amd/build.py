@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libstarq.so")
-SOURCES = ["plan.hip", "gemm.hip", "gemm_async.hip", "colsum.hip", "swiglu.hip", "decode.hip", "decode_stack.hip", "graph_fill.hip", "scratch.hip", "attention.hip", "api.cpp"]
+SOURCES = ["plan.hip", "gemm.hip", "gemm_async.hip", "gemm_narrow.hip", "colsum.hip", "swiglu.hip", "decode.hip", "decode_stack.hip", "graph_fill.hip", "scratch.hip", "attention.hip", "api.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -39,8 +39,11 @@ def hipcc() -> str:
 
 # Per-source flags.  The attention kernels keep their MFMA accumulators in
 # VGPRs: the softmax works on every score, and accumulators in AGPRs would
-# cost a v_accvgpr_read/write pair per value per step.
-EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# cost a v_accvgpr_read/write pair per value per step.  The small-tile GEMM
+# does the same: its tiles are a few K steps long, so the epilogue's reads
+# of the accumulators are a large share of its instructions.
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "gemm_narrow.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:

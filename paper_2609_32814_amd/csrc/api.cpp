@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -323,8 +324,44 @@ star_status hip_status(hipError_t e) { return e == hipSuccess ? STAR_OK : STAR_E
 // column tiles are wider, so the tile counts are redone for it); fp32
 // operands the register-staged one.  `upper` bounds the number of tiles of
 // the register-staged kernel.
+// The forward takes the small-tile kernel (64 rows x 128 columns) when the
+// wide kernel's 256 x 256 tiles would be at most three quarters full (rows
+// taken as spread evenly over the types; a group's last column tile counts
+// its empty columns) or too few to fill the chip, and when an input group is
+// narrower than 64 (a 64-wide K step would span groups).  The bar was set
+// by timing both kernels on the projection shapes of the paper's kernel
+// study (M = 512, 2048, 8192; q = 4 to 64).
+std::atomic<int> g_fwd_tiles{STAR_TILES_AUTO};
+
+bool use_narrow_fwd(const GemmParams& p) {
+  if (p.elem != 1) return false;
+  for (int g = 0; g < p.q; ++g)
+    if (p.S[g + 1] - p.S[g] < 64) return true;
+  const int forced = g_fwd_tiles.load(std::memory_order_relaxed);
+  if (forced != STAR_TILES_AUTO) return forced == STAR_TILES_SMALL;
+  if (static_cast<int64_t>(p.M) < p.q) return true;
+  const double m = static_cast<double>(p.M) / p.q;  // rows per type
+  const double row_tiles = std::ceil(m / 256.0);
+  double cols = 0.0, col_tiles = 0.0;
+  for (int g = 0; g < p.q; ++g) {
+    const int w = p.R[g + 1] - p.R[g];
+    cols += w;
+    col_tiles += (w + 255) / 256;
+  }
+  if (col_tiles == 0.0) return true;
+  const double fill = (m / (256.0 * row_tiles)) * (cols / (256.0 * col_tiles));
+  return fill <= 0.75 || p.q * row_tiles * col_tiles < 128.0;
+}
+
 hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
                             hipStream_t stream) {
+  if (mode == kModeFwd && use_narrow_fwd(p)) {
+    GemmParams pn = p;
+    const int tn = gemm_narrow_cols();
+    pn.NTp[0] = 0;
+    for (int g = 0; g < p.q; ++g) pn.NTp[g + 1] = pn.NTp[g] + (p.R[g + 1] - p.R[g] + tn - 1) / tn;
+    return launch_gemm_narrow(pn, gemm_narrow_row_blocks_upper(p.M, p.q), pn.NTp[p.q], cu_count(), stream);
+  }
   if (p.elem == 1) {
     GemmParams pa = p;
     const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
@@ -412,6 +449,11 @@ size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_alge
     default:
       return 0;
   }
+}
+
+int star_set_fwd_tiles(int tiles) {
+  if (tiles != STAR_TILES_AUTO && tiles != STAR_TILES_WIDE && tiles != STAR_TILES_SMALL) return -1;
+  return g_fwd_tiles.exchange(tiles);
 }
 
 star_status star_count_products(const star_algebra* alg, int64_t* per_type) {

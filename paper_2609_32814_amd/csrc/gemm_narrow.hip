@@ -1,0 +1,499 @@
+// Forward product for many small groups (§"Kernels"; §"Kernel Scaling on
+// Transformer Shapes"): when each row type has few rows (M / q well below a
+// 256-row tile) or the groups are narrow, the 256 x 256 tiles of the
+// persistent GEMM are mostly empty.  Here a tile is 64 rows of one type
+// (rows taken in type order through the plan) x 128 columns of one output
+// group, the contraction is the concatenation of the input groups in the
+// law's B(i, j) (a K step of 64 never straddles two groups; a group's last
+// step is zero-padded), and a workgroup of 4 wavefronts (2 x 2, each 32 rows
+// x 64 columns: two v_mfma_f32_32x32x16_bf16 blocks) computes it with both
+// operands staged in LDS by direct global-to-LDS copies.  Workgroups are
+// persistent: each walks its tiles as one stream of K steps whose copies run
+// two steps ahead across tile boundaries (each tile has few steps), with the
+// rows of the next tiles fetched while earlier tiles compute.
+// Bias, activation, an optional pre-activation store and the bf16/fp32
+// output follow in the epilogue.
+//
+// Work order: workgroup w runs on XCD w mod 8; each XCD takes a contiguous
+// range of the tile list in (row block, column tile) order, so the tiles of
+// one block of rows of one type run side by side on one XCD (its rows and
+// the diagonal weight blocks stay in that XCD's L2) and each off-diagonal
+// weight block is read once.
+//
+// The paper's second schedule (the diagonal maps over all rows, then the
+// type-dependent maps) serves the same regime; here both products of a
+// tile are accumulated in registers before one output store.
+#include <algorithm>
+
+#include "gemm_common.hpp"
+
+namespace starq {
+
+namespace {
+
+using namespace gemm;
+
+constexpr int kNThreads = 256;
+constexpr int kNRows = 64;                 // rows per tile
+constexpr int kNCols = 128;                // columns per tile
+constexpr int kNK = 64;                    // K per step
+constexpr int kA = kNRows * kNK * 2;       // 8 KB
+constexpr int kB = kNK * kNCols * 2;       // 16 KB
+constexpr int kStage = kA + kB;
+constexpr int kNStages = 3;                // copies run two K steps ahead
+constexpr int kNSmem = kNStages * kStage;  // 72 KB: two workgroups per CU
+constexpr int kSlots = 5;                  // tiles described in LDS (the consumer's and 4 ahead)
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+#define STARQ_LDS __attribute__((address_space(3)))
+
+// source of the copies that must land as zeros
+__device__ __attribute__((aligned(256))) uint32_t g_narrow_zero[256];
+// Where the epilogue's lanes without an output element store: every lane
+// stores each of its output blocks, so the number of stores in flight is
+// known.  A lane's sink covers one row of its blocks (at most 240 bytes);
+// kSinkSets sets of 64 lanes spread the writes over workgroups.
+constexpr int kSinkSets = 16;
+constexpr int kSinkLane = 256;
+__device__ __attribute__((aligned(256))) char g_narrow_sink[kSinkSets * 64 * kSinkLane];
+
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" : : "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));  // vmcnt(N)
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_vm_all() { wait_vm<0>(); }
+// vmcnt(6 + n) for an even n <= 40 known only at run time (else vmcnt(0))
+template <int N>
+__device__ __forceinline__ void wait_vm_after(int n) {
+  if constexpr (N > 40) {
+    wait_vm_all();
+  } else {
+    if (n == N) wait_vm<6 + N>();
+    else wait_vm_after<N + 2>(n);
+  }
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p)));
+}
+__device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
+// input groups in B(i, j) of the forward product, as a bit mask
+__device__ __forceinline__ uint64_t fwd_mask(const GemmParams& p, int i, int j) {
+  if (p.law == 1) return p.q >= 64 ? ~0ull : ((1ull << p.q) - 1ull);
+  if (p.law == 2) return tensor_mask(kModeFwd, p.q, i, j);
+  if (p.law == 3) return graph_mask(p, kModeFwd, i, j);
+  return (1ull << i) | (1ull << j);
+}
+
+// LDS layouts.  A: 64 rows x 64 K (128 bytes a row), 16-byte chunk c of row r
+// at chunk c ^ (r & 7).  B: 64 K rows x 128 columns (256 bytes a row), chunk c
+// of K row k at chunk c ^ 2 (k & 3).  Both keep the MFMA operand reads free of
+// bank conflicts (a row-contiguous read of 8 rows, a transposing read of 4).
+__device__ __forceinline__ int a_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+__device__ __forceinline__ int b_off(int k, int c) { return k * 256 + ((c ^ (2 * (k & 3))) << 4); }
+
+// A tile of the list: rows [pos0, pend) of the plan, columns [cstart, cend),
+// the input groups of its contraction and its K steps (0: nothing to do).
+struct NTile {
+  int32_t pos0, pend, cstart, cend, nsteps;
+  uint64_t mask;
+};
+
+// The fp32 epilogue of one tile for one lane: row 32 wr + lr of the tile (`row`
+// in the output, `rok` whether it exists), columns 64 wc + 32 cb + 8 a +
+// 4 lh + 0..3 for cb < 2, a < 4.  Every lane stores all 8 blocks (and 8 of Z
+// when asked for): blocks without an element go to the lane's sink.
+__device__ __forceinline__ void narrow_epilogue(const GemmParams& p, const f32x16_t (&acc)[2], bool rok, int32_t row,
+                                                int32_t cstart, int32_t cend, int cl0, const float* bias_tile,
+                                                char* sink) {
+  constexpr int esz = 4;
+  const int64_t off = (static_cast<int64_t>(row) * p.N + cstart + cl0) * esz;
+  char* yb = rok ? static_cast<char*>(p.Y) + off : sink;
+  char* zb = p.Z ? (rok ? static_cast<char*>(p.Z) + off : sink) : nullptr;
+  const bool full = cend - cstart == kNCols;
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int cl = cl0 + 32 * cb + 8 * a;
+      const int bo = (32 * cb + 8 * a) * esz;
+      const bool cok = full || cstart + cl < cend;
+      float v[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) v[x] = acc[cb][4 * a + x];
+      if (p.bias) {
+        const float4 bv = *reinterpret_cast<const float4*>(bias_tile + cl);
+        v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+      }
+      auto put = [&](char* base) {
+        *reinterpret_cast<float4*>((cok ? base : sink) + bo) = make_float4(v[0], v[1], v[2], v[3]);
+      };
+      if (zb) put(zb);
+      if (p.act != kActNone) {
+#pragma unroll
+        for (int x = 0; x < 4; ++x) v[x] = act_apply(p.act, v[x]);
+      }
+      put(yb);
+    }
+}
+
+__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams p, int32_t n_ct, int32_t wg_per_xcd) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];  // kNStages stages of (A, B)
+  __shared__ int32_t rows_s[kSlots][kNRows];                    // plan positions of the tile's rows
+  __shared__ __attribute__((aligned(16))) float bias_s[kSlots][256];  // the tile's bias (first kNCols)
+  __shared__ __attribute__((aligned(16))) int32_t desc_s[kSlots][8];  // the tile: see schedule()
+
+  const int lane = threadIdx.x & 63;
+  const int wave = uni(threadIdx.x >> 6);
+  const int wr = wave >> 1, wc = wave & 1;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int q = p.q;
+
+  // the plan's offsets, lane t holding type t's, and the running count of
+  // 64-row blocks over the types
+  int32_t o0 = 0, o1 = 0, nb = 0;
+  if (lane < q) {
+    o0 = p.offsets[lane];
+    o1 = p.offsets[lane + 1];
+    nb = (o1 - o0 + kNRows - 1) / kNRows;
+  }
+  int32_t incl = nb;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t u = __shfl_up(incl, d);
+    if (lane >= d) incl += u;
+  }
+  // per-group figures, lane x holding group x's: column tile prefix and
+  // column range of output group x, contraction range and K steps of input
+  // group x
+  int32_t ntp0 = 0, ntp1 = 0x7fffffff, r0 = 0, r1 = 0, s0 = 0, s1 = 0, ns = 0;
+  if (lane < q) {
+    ntp0 = p.NTp[lane];
+    r0 = p.R[lane];
+    r1 = p.R[lane + 1];
+    s0 = p.S[lane];
+    s1 = p.S[lane + 1];
+    ns = (s1 - s0 + kNK - 1) / kNK;
+    if (lane + 1 < q) ntp1 = p.NTp[lane + 1];
+  }
+  int ns_bits = 0;  // bits of the largest step count
+  while (__ballot((ns >> ns_bits) != 0)) ++ns_bits;
+
+  // The tile list, in order: type by type, the column tiles in order, and
+  // for each the type's 64-row blocks in order (the blocks that share a
+  // weight tile are neighbours in the list, so they run together).  Item
+  // `item` is type i's, the first whose running block count times the
+  // column tiles passes it; the steps are those of the input groups in the
+  // mask, counted bit plane by bit plane of the per-group step counts.
+  const int32_t n_blocks = __builtin_amdgcn_readlane(incl, q - 1);
+  auto decode = [&](int32_t item) -> NTile {
+    NTile t;
+    const int i = __builtin_ctzll(__ballot(lane < q && incl * n_ct > item));
+    const int32_t nbi = __builtin_amdgcn_readlane(nb, i);
+    const int32_t local = item - (__builtin_amdgcn_readlane(incl, i) - nbi) * n_ct;
+    const int32_t ct = local / nbi;
+    const int32_t blk = local - ct * nbi;
+    t.pos0 = __builtin_amdgcn_readlane(o0, i) + blk * kNRows;
+    t.pend = min(__builtin_amdgcn_readlane(o1, i), t.pos0 + kNRows);
+    const int j = __popcll(__ballot(ct >= ntp1));
+    t.cstart = __builtin_amdgcn_readlane(r0, j) + (ct - __builtin_amdgcn_readlane(ntp0, j)) * kNCols;
+    t.cend = min(__builtin_amdgcn_readlane(r1, j), t.cstart + kNCols);
+    t.mask = fwd_mask(p, i, j);  // empty for a graph-law non-slot (the fill kernel writes it)
+    t.nsteps = 0;
+    for (int b = 0; b < ns_bits; ++b) t.nsteps += __popcll(__ballot((ns >> b) & 1) & t.mask) << b;
+    return t;
+  };
+
+  // This workgroup's tiles: XCD x (workgroup w runs on XCD w mod 8) owns a
+  // contiguous eighth of the list and its workgroups take every
+  // wg_per_xcd-th item of it, so neighbouring tiles run side by side on one
+  // XCD and share its L2.
+  const int32_t n_items = n_blocks * n_ct;
+  const int32_t per_xcd = (n_items + 7) / 8;
+  const int32_t last = min(n_items, ((blockIdx.x & 7) + 1) * per_xcd);
+  int32_t s_item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+
+  const uint16_t* X = static_cast<const uint16_t*>(p.A);
+  const uint16_t* W = static_cast<const uint16_t*>(p.B);
+  const void* zero = g_narrow_zero;
+  const uint32_t smem_base = lds_addr(smem);
+
+  // ---- scheduler (wave 0): the n-th tile of this workgroup is described in
+  // slot n mod kSlots, kSlots - 1 tiles ahead of the consumer: its row count,
+  // columns, steps and group mask, with the plan positions of its rows and
+  // its bias copied straight into LDS (lanes past the rows or columns, and
+  // every lane without a bias, copy zeros: always 2 copies).  A tile of no
+  // steps ends the list.  The producer reaches a tile at least two
+  // iterations after it was described, so the copies issued for it are
+  // older than the element copies waited for by then.
+  int32_t s_n = 0;
+  auto schedule = [&]() {
+    if (wave != 0) return;
+    NTile t;
+    t.nsteps = 0;
+    for (; s_item < last; s_item += wg_per_xcd) {
+      t = decode(s_item);
+      if (t.nsteps > 0) break;
+    }
+    const int slot = s_n % kSlots;
+    if (s_item < last) {
+      s_item += wg_per_xcd;
+    } else {
+      t.nsteps = 0;
+      t.pos0 = t.pend = t.cstart = t.cend = 0;
+      t.mask = 0;
+    }
+    dma4(lane < t.pend - t.pos0 ? static_cast<const void*>(p.perm + t.pos0 + lane) : zero, lds_addr(rows_s[slot]));
+    dma16(p.bias && t.cstart + 4 * lane < t.cend ? static_cast<const void*>(p.bias + t.cstart + 4 * lane) : zero,
+          lds_addr(bias_s[slot]));
+    if (lane == 0) {
+      *reinterpret_cast<int4*>(desc_s[slot]) = make_int4(t.pend - t.pos0, t.cstart, t.cend, t.nsteps);
+      *reinterpret_cast<int4*>(desc_s[slot] + 4) =
+          make_int4(static_cast<int32_t>(t.mask), static_cast<int32_t>(t.mask >> 32), 0, 0);
+    }
+    ++s_n;
+  };
+
+  // ---- producer: the stream of (tile, K step) elements, copied
+  // kNStages - 1 elements ahead of the consumer; every element is 6 copies
+  // per wave (2 of A, 4 of B).  A tile's descriptor is read when its first
+  // element is copied (a barrier after the scheduler wrote it); the copy
+  // sources of its A rows and B columns are set up then, and each step
+  // offsets them by its K.  Rows past the tile's read row 0 and columns past
+  // it read the group's last columns: their products are never stored.
+  int32_t p_n = 0, p_s = 0, p_nsteps = 0, p_k = 0, p_kend = 0;
+  uint64_t p_mask = 0;
+  bool p_fresh = true, p_done = false;
+  const uint16_t* abase[2];
+  const uint16_t* bbase[4];
+  auto produce = [&](int stage) -> bool {
+    if (p_fresh) {
+      p_fresh = false;
+      const int4 d0 = *reinterpret_cast<const int4*>(desc_s[p_n % kSlots]);
+      const int4 d1 = *reinterpret_cast<const int4*>(desc_s[p_n % kSlots] + 4);
+      p_nsteps = uni(d0.w);
+      if (p_nsteps == 0) {
+        p_done = true;
+      } else {
+        const int32_t cstart = uni(d0.y);
+        p_mask = static_cast<uint64_t>(static_cast<uint32_t>(uni(d1.x))) |
+                 (static_cast<uint64_t>(static_cast<uint32_t>(uni(d1.y))) << 32);
+        const int x = __builtin_ctzll(p_mask);
+        p_k = __builtin_amdgcn_readlane(s0, x);
+        p_kend = __builtin_amdgcn_readlane(s1, x);
+        p_s = 0;
+        const int32_t* rows = rows_s[p_n % kSlots];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int r = 8 * (wave + 4 * u) + (lane >> 3), c = (lane & 7) ^ (r & 7);
+          abase[u] = X + static_cast<int64_t>(rows[r]) * p.K + 8 * c;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kr = 4 * (wave + 4 * u) + (lane >> 4), c = (lane & 15) ^ (2 * (kr & 3));
+          const int32_t col = min(cstart + 8 * c, p.N - 8);
+          bbase[u] = W + static_cast<int64_t>(kr) * p.N + col;
+        }
+      }
+    }
+    if (p_done) return false;
+    const uint32_t As = smem_base + stage * kStage, Bs = As + kA;
+    const int64_t kofs = static_cast<int64_t>(p_k) * p.N;
+    if (p_kend - p_k >= kNK) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) dma16(abase[u] + p_k, As + (wave + 4 * u) * 1024);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) dma16(bbase[u] + kofs, Bs + (wave + 4 * u) * 1024);
+    } else {  // the group's last step runs past its end: zeros there
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int r = 8 * (wave + 4 * u) + (lane >> 3), c = (lane & 7) ^ (r & 7);
+        dma16(p_k + 8 * c < p_kend ? static_cast<const void*>(abase[u] + p_k) : zero, As + (wave + 4 * u) * 1024);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int kr = 4 * (wave + 4 * u) + (lane >> 4);
+        dma16(p_k + kr < p_kend ? static_cast<const void*>(bbase[u] + kofs) : zero, Bs + (wave + 4 * u) * 1024);
+      }
+    }
+    // advance: next K step of this group, next group, or the next tile
+    p_k += kNK;
+    if (p_k >= p_kend) {
+      p_mask &= p_mask - 1;
+      if (p_mask) {
+        const int x = __builtin_ctzll(p_mask);
+        p_k = __builtin_amdgcn_readlane(s0, x);
+        p_kend = __builtin_amdgcn_readlane(s1, x);
+      }
+    }
+    if (++p_s == p_nsteps) {
+      ++p_n;
+      p_fresh = true;
+    }
+    return true;
+  };
+
+  // ---- prologue: the first kSlots - 1 tiles described, then the first
+  // kNStages - 1 elements copied
+  for (int n = 0; n < kSlots - 1; ++n) schedule();
+  wait_vm_all();
+  __syncthreads();
+  bool ahead = false;  // whether the element after the consumer's was copied
+  for (int e = 0; e < kNStages - 1; ++e) ahead = produce(e);
+
+  // ---- consumer
+  auto read_tile = [&](int n, int32_t& nrows, int32_t& cstart, int32_t& cend, int32_t& nsteps) {
+    const int4 d0 = *reinterpret_cast<const int4*>(desc_s[n % kSlots]);
+    nrows = uni(d0.x);
+    cstart = uni(d0.y);
+    cend = uni(d0.z);
+    nsteps = uni(d0.w);
+  };
+  int32_t c_n = 0, c_s = 0, c_nrows, c_cstart, c_cend, c_nsteps;
+  read_tile(0, c_nrows, c_cstart, c_cend, c_nsteps);
+  f32x16_t acc[2];
+  const int g = lane >> 4, pp = lane & 15;
+  const int rr = pp >> 2, qq = pp & 3;
+  char* sink = g_narrow_sink + ((blockIdx.x % kSinkSets) * 64 + lane) * kSinkLane;
+  // stores of the output blocks at the ends of the last two iterations and
+  // the scheduler's copies of the last one (issued after the copies of this
+  // iteration's element); per tile each lane stores 4 chunks of 16 bytes of
+  // a bf16 output, 8 blocks of an fp32 one, and as many again of Z
+  const int n_st = (p.ydtype == 0 ? 8 : 4) * (p.Z ? 2 : 1);
+  int st1 = 0, st2 = 0, sd1 = 0;
+  for (int32_t e = 0; c_nsteps > 0; ++e) {
+    // Memory operations complete in order for the counter: element e's
+    // copies have landed once no more are outstanding than were issued after
+    // them: the 6 copies of element e + 1, the stores of the last two
+    // iterations and the scheduler's copies of the last one.
+    const int after = st1 + st2 + sd1;
+    if (!ahead) wait_vm_all();
+    else wait_vm_after<0>(after);
+    st2 = st1;
+    st1 = 0;
+    sd1 = 0;
+    __syncthreads();  // element e and the scheduler's last writes are visible;
+                      // element e - 1 and the tile before this one are done with
+    const bool first = c_s == 0;
+    if (first) {
+      schedule();  // tile c_n + 4, into the slot of tile c_n - 1
+      if (wave == 0) sd1 = 2;
+    }
+    ahead = produce((e + kNStages - 1) % kNStages);
+    const char* As = smem + (e % kNStages) * kStage;
+    const char* Bs = As + kA;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      // B operand of the C^T block: 8 consecutive K of row 32 wr + lr
+      const uint4 xf = *reinterpret_cast<const uint4*>(As + a_off(32 * wr + lr, 2 * ks + lh));
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        // A operand: 8 consecutive K of column 64 wc + 32 cb + lr, by two
+        // transposing reads of 4 K rows each
+        const int col = 64 * wc + 32 * cb + 16 * (g & 1) + 4 * qq;  // this lane's 4 addressed columns
+        const int k1 = 16 * ks + 8 * (g >> 1) + rr;
+        const char* a0 = Bs + b_off(k1, col >> 3) + ((col >> 2) & 1) * 8;
+        const char* a1 = Bs + b_off(k1 + 4, col >> 3) + ((col >> 2) & 1) * 8;
+        const uint2 w0 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0)));
+        const uint2 w1 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a1)));
+        const bf16x8_t wf = __builtin_bit_cast(bf16x8_t, make_uint4(w0.x, w0.y, w1.x, w1.y));
+        if (ks == 0 && first)
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, __builtin_bit_cast(bf16x8_t, xf), f32x16_t{}, 0, 0, 0);
+        else
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, __builtin_bit_cast(bf16x8_t, xf), acc[cb], 0, 0, 0);
+      }
+    }
+    if (++c_s < c_nsteps) continue;
+    // ---- epilogue of the tile
+    {
+      const int r = 32 * wr + lr;
+      const bool rok = r < c_nrows;
+      const int32_t row = rows_s[c_n % kSlots][r];
+      const float* bt = bias_s[c_n % kSlots];
+      if (p.ydtype == 0) {
+        narrow_epilogue(p, acc, rok, row, c_cstart, c_cend, 64 * wc + 4 * lh, bt, sink);
+      } else {
+        // bf16 through LDS, in the stage this iteration consumed (free until
+        // the next iteration's copies): the 64 x 128 values go in with row r
+        // at r * 256 bytes and 16-byte chunk c at c ^ (r & 15), then each
+        // thread stores 16-byte chunks of whole rows (16 lanes a row)
+        char* T = smem + (e % kNStages) * kStage;
+        const int32_t* rows = rows_s[c_n % kSlots];
+        auto pass = [&](void* out, bool activate) {
+          __syncthreads();  // every wave is done reading the stage (or the last pass)
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+              const int cl = 64 * wc + 32 * cb + 8 * a + 4 * lh;
+              float v[4];
+#pragma unroll
+              for (int x = 0; x < 4; ++x) v[x] = acc[cb][4 * a + x];
+              if (p.bias) {
+                const float4 bv = *reinterpret_cast<const float4*>(bt + cl);
+                v[0] += bv.x; v[1] += bv.y; v[2] += bv.z; v[3] += bv.w;
+              }
+              if (activate) {
+#pragma unroll
+                for (int x = 0; x < 4; ++x) v[x] = act_apply(p.act, v[x]);
+              }
+              *reinterpret_cast<uint2*>(T + r * 256 + (((cl >> 3) ^ (r & 15)) << 4) + ((cl >> 2) & 1) * 8) =
+                  make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
+            }
+          __syncthreads();
+#pragma unroll
+          for (int it = 0; it < 4; ++it) {
+            const int id = threadIdx.x + kNThreads * it, tr = id >> 4, c = id & 15;
+            const uint4 val = *reinterpret_cast<const uint4*>(T + tr * 256 + ((c ^ (tr & 15)) << 4));
+            const bool ok = tr < c_nrows && c_cstart + 8 * c < c_cend;
+            const int64_t off = (static_cast<int64_t>(rows[tr]) * p.N + c_cstart + 8 * c) * 2;
+            *reinterpret_cast<uint4*>(ok ? static_cast<char*>(out) + off : sink + 16 * it) = val;
+          }
+        };
+        if (p.Z) pass(p.Z, false);
+        pass(p.Y, p.act != kActNone);
+      }
+      st1 = n_st;
+    }
+    ++c_n;
+    c_s = 0;
+    read_tile(c_n, c_nrows, c_cstart, c_cend, c_nsteps);  // written at the start of tile c_n - 4
+  }
+}
+
+}  // namespace
+
+int32_t gemm_narrow_row_blocks_upper(int64_t M, int q) { return static_cast<int32_t>(M / kNRows + q); }
+int gemm_narrow_cols() { return kNCols; }
+
+hipError_t launch_gemm_narrow(const GemmParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream) {
+  // n_rb bounds the row blocks from above (the kernel counts them from the
+  // plan's offsets)
+  const int64_t items = static_cast<int64_t>(n_rb) * n_ct;
+  if (items <= 0 || items > 0x7fffff00 || p.N < 8) return hipErrorInvalidValue;
+  // persistent: two workgroups per CU (72 KB of LDS each), the same number
+  // on every XCD, no more than there are items per XCD
+  const int64_t per_xcd = (items + 7) / 8;
+  const int wg_per_xcd = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(per_xcd, 2 * std::max(cus, 8) / 8)));
+  static std::atomic<unsigned long long> set{0};
+  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(gemm_narrow_kernel), set, kNSmem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(gemm_narrow_kernel, dim3(8 * wg_per_xcd), dim3(kNThreads), kNSmem, stream, p, n_ct, wg_per_xcd);
+  return hipGetLastError();
+}
+
+}  // namespace starq

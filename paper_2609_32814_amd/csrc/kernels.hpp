@@ -83,6 +83,12 @@ hipError_t launch_column_sum_f32(const float* src, int32_t N, const int32_t* per
 hipError_t launch_graph_fill(int mode, const GemmParams& p, hipStream_t stream);
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream);
+// Small-tile forward (gemm_narrow.hip): tiles of 64 rows of one type x
+// gemm_narrow_cols() columns of one output group; p.NTp counts column tiles
+// of that width; n_rb bounds the row blocks over all types.
+int gemm_narrow_cols();
+int32_t gemm_narrow_row_blocks_upper(int64_t M, int q);
+hipError_t launch_gemm_narrow(const GemmParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream);
 // Gated FFN elementwise parts (swiglu.hip); n a multiple of 8, elem 1 bf16
 // or 0 fp32, 16-byte aligned buffers.
 hipError_t launch_swiglu_fwd(int64_t n, int elem, const void* zg, const void* zu, void* h, hipStream_t stream);

@@ -38,6 +38,18 @@ def test_binding_names_match_abi(P):
         assert hasattr(P, n), n
 
 
+def test_set_fwd_tiles(P):
+    assert P.star_set_fwd_tiles("wide") == "auto"
+    assert P.star_set_fwd_tiles("small") == "wide"
+    assert P.star_set_fwd_tiles("auto") == "small"
+    with pytest.raises(ValueError):
+        P.star_set_fwd_tiles("huge")
+    lib = ctypes.CDLL(P.LIB_PATH)
+    lib.star_set_fwd_tiles.restype = ctypes.c_int
+    assert lib.star_set_fwd_tiles(3) == -1 and lib.star_set_fwd_tiles(-1) == -1
+    assert P.star_set_fwd_tiles("auto") == "auto"
+
+
 def test_count_products(P):
     for q in (1, 2, 3, 8, 16, 64):
         a = P.Algebra.equal(q, 8 * q, 8 * q)

@@ -170,10 +170,11 @@ def _types(kind, M, q, seed):
     return t
 
 
+@pytest.mark.parametrize("tiles", ["wide", "small"])
 @pytest.mark.parametrize("law", ["star", "dense"])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 @pytest.mark.parametrize("q,s,r,M,types", PIPE_SHAPES)
-def test_fwd_pipelined_shapes(P, law, out, q, s, r, M, types):
+def test_fwd_pipelined_shapes(P, tiles, law, out, q, s, r, M, types):
     import torch
     ga, oa = algs(P, q, s, r, law)
     seed = 400 + q + M
@@ -182,8 +183,12 @@ def test_fwd_pipelined_shapes(P, law, out, q, s, r, M, types):
     bias = synth.gaussian(seed, 2, (oa.N,), 0.02, "f32")
     t = _types(types, M, q, seed)
     odt = torch.float32 if out == "f32" else torch.bfloat16
-    Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
-                           Z_out=True, out_dtype=odt)
+    P.star_set_fwd_tiles(tiles)
+    try:
+        Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(bias.exact), "gelu",
+                               Z_out=True, out_dtype=odt)
+    finally:
+        P.star_set_fwd_tiles("auto")
     refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, bias.exact, "gelu", want_z=True)
     assert rel_fro(to_host(Z), refZ) <= TOL_BF16
     assert rel_fro(to_host(Y), refY) <= TOL_BF16
