@@ -14,11 +14,10 @@
 // Bias, activation, an optional pre-activation store and the bf16/fp32
 // output follow in the epilogue.
 //
-// Work order: workgroup w runs on XCD w mod 8; each XCD takes a contiguous
-// range of the tile list in (row block, column tile) order, so the tiles of
-// one block of rows of one type run side by side on one XCD (its rows and
-// the diagonal weight blocks stay in that XCD's L2) and each off-diagonal
-// weight block is read once.
+// Work order: workgroup w runs on XCD w mod 8; each XCD owns an eighth of
+// the row blocks (or of the column tiles, when there are fewer than 8 row
+// blocks) and sweeps the column tiles band by band of its row blocks, so a
+// weight tile is fetched once per band and the band's rows stay in L2.
 //
 // The paper's second schedule (the diagonal maps over all rows, then the
 // type-dependent maps) serves the same regime; here both products of a
@@ -151,7 +150,8 @@ __device__ __forceinline__ void narrow_epilogue(const GemmParams& p, const f32x1
     }
 }
 
-__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams p, int32_t n_ct, int32_t wg_per_xcd) {
+__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams p, int32_t n_ct, int32_t wg_per_xcd,
+                                                                 int32_t band) {
   extern __shared__ __attribute__((aligned(16))) char smem[];  // kNStages stages of (A, B)
   __shared__ int32_t rows_s[kSlots][kNRows];                    // plan positions of the tile's rows
   __shared__ __attribute__((aligned(16))) float bias_s[kSlots][256];  // the tile's bias (first kNCols)
@@ -193,20 +193,40 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
   int ns_bits = 0;  // bits of the largest step count
   while (__ballot((ns >> ns_bits) != 0)) ++ns_bits;
 
-  // The tile list, in order: type by type, the column tiles in order, and
-  // for each the type's 64-row blocks in order (the blocks that share a
-  // weight tile are neighbours in the list, so they run together).  Item
-  // `item` is type i's, the first whose running block count times the
-  // column tiles passes it; the steps are those of the input groups in the
-  // mask, counted bit plane by bit plane of the per-group step counts.
+  // The tiles: (row block rb, column tile ct), the row blocks numbered type
+  // by type (block rb is type i's, the first whose running block count
+  // passes rb).  XCD x (workgroup w runs on XCD w mod 8) owns a region: an
+  // eighth of the row blocks with every column tile, or, with fewer than 8
+  // row blocks, every row block with an eighth of the column tiles.  Within
+  // it the row blocks go in bands of `band` (rows whose X fits in a part of
+  // the XCD's L2) and each band runs column tile by column tile, its row
+  // blocks side by side: a weight tile is fetched once per band (the
+  // diagonal blocks, which every type reads, once per band instead of once
+  // per type) and the band's rows stay in L2.  The region's workgroups take
+  // every wg_per_xcd-th item.  A tile's steps are those of the input groups
+  // in its mask, counted bit plane by bit plane of the per-group step counts.
   const int32_t n_blocks = __builtin_amdgcn_readlane(incl, q - 1);
+  const int xcd = blockIdx.x & 7;
+  int32_t rb0 = 0, rb1 = n_blocks, ct0 = 0, ct1 = n_ct;
+  if (n_blocks >= 8) {
+    rb0 = xcd * n_blocks / 8;
+    rb1 = (xcd + 1) * n_blocks / 8;
+  } else {
+    ct0 = xcd * n_ct / 8;
+    ct1 = (xcd + 1) * n_ct / 8;
+  }
+  const int32_t nrb = rb1 - rb0, nct = ct1 - ct0;
+  const int32_t band_items = band * nct;
   auto decode = [&](int32_t item) -> NTile {
     NTile t;
-    const int i = __builtin_ctzll(__ballot(lane < q && incl * n_ct > item));
-    const int32_t nbi = __builtin_amdgcn_readlane(nb, i);
-    const int32_t local = item - (__builtin_amdgcn_readlane(incl, i) - nbi) * n_ct;
-    const int32_t ct = local / nbi;
-    const int32_t blk = local - ct * nbi;
+    const int32_t bi = item / band_items;
+    const int32_t within = item - bi * band_items;
+    const int32_t bsz = min(band, nrb - bi * band);
+    const int32_t cl = within / bsz;
+    const int32_t rb = rb0 + bi * band + (within - cl * bsz);
+    const int32_t ct = ct0 + cl;
+    const int i = __builtin_ctzll(__ballot(lane < q && incl > rb));
+    const int32_t blk = rb - (__builtin_amdgcn_readlane(incl, i) - __builtin_amdgcn_readlane(nb, i));
     t.pos0 = __builtin_amdgcn_readlane(o0, i) + blk * kNRows;
     t.pend = min(__builtin_amdgcn_readlane(o1, i), t.pos0 + kNRows);
     const int j = __popcll(__ballot(ct >= ntp1));
@@ -217,15 +237,8 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
     for (int b = 0; b < ns_bits; ++b) t.nsteps += __popcll(__ballot((ns >> b) & 1) & t.mask) << b;
     return t;
   };
-
-  // This workgroup's tiles: XCD x (workgroup w runs on XCD w mod 8) owns a
-  // contiguous eighth of the list and its workgroups take every
-  // wg_per_xcd-th item of it, so neighbouring tiles run side by side on one
-  // XCD and share its L2.
-  const int32_t n_items = n_blocks * n_ct;
-  const int32_t per_xcd = (n_items + 7) / 8;
-  const int32_t last = min(n_items, ((blockIdx.x & 7) + 1) * per_xcd);
-  int32_t s_item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  const int32_t last = nrb * nct;
+  int32_t s_item = blockIdx.x >> 3;
 
   const uint16_t* X = static_cast<const uint16_t*>(p.A);
   const uint16_t* W = static_cast<const uint16_t*>(p.B);
@@ -492,7 +505,10 @@ hipError_t launch_gemm_narrow(const GemmParams& p, int32_t n_rb, int32_t n_ct, i
   static std::atomic<unsigned long long> set{0};
   hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(gemm_narrow_kernel), set, kNSmem);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(gemm_narrow_kernel, dim3(8 * wg_per_xcd), dim3(kNThreads), kNSmem, stream, p, n_ct, wg_per_xcd);
+  // bands of row blocks whose X rows take at most 2 MB (half an XCD's L2)
+  const int32_t band = static_cast<int32_t>(std::max<int64_t>(1, (int64_t{2} << 20) / (int64_t{kNRows} * p.K * 2)));
+  hipLaunchKernelGGL(gemm_narrow_kernel, dim3(8 * wg_per_xcd), dim3(kNThreads), kNSmem, stream, p, n_ct, wg_per_xcd,
+                     band);
   return hipGetLastError();
 }
 
