@@ -792,9 +792,10 @@ def bench_qsweep(P, synth, torch, np, dev, T, flush, args):
 
 # The paper's pure expansion projections (§"Kernel Scaling on Transformer
 # Shapes", Tab. kernel-products): D -> F at M rows, the q grid {4, 8, 16, 32,
-# 64} (the paper's grid for Qwen3-32B is {32, 64, 128, 256}; q is at most 64
-# here).  Its figures (BF16 on an H200 NVL: q*, dense us, algebraic us, warm /
-# flushed speedups) are context from other hardware, not targets.
+# 64} (the paper's) widened to 128 and 256 for every shape (the paper's grid
+# for Qwen3-32B is {32, 64, 128, 256}).  Its figures (BF16 on an H200 NVL:
+# q*, dense us, algebraic us, warm / flushed speedups) are context from other
+# hardware, not targets.
 KERNEL_PRODUCT_SHAPES = [
     ("Qwen3-1.7B", 2048, 2048, 6144, {"q": 32, "dense_us": 75.7, "q_us": 24.9, "speedup": [3.04, 2.84]}),
     ("Qwen3-4B", 2048, 2560, 9728, {"q": 32, "dense_us": 160.6, "q_us": 51.1, "speedup": [3.14, 2.94]}),
@@ -806,6 +807,21 @@ KERNEL_PRODUCT_SHAPES = [
     ("Qwen3-32B M32768", 32768, 5120, 25600,
      {"q": 256, "dense_us": 13458.6, "q_us": 1169.4, "speedup": [11.51, 11.70]}),
 ]
+
+
+def group_widths(total, q):
+    """q group widths summing to total, multiples of 8: equal when total / q
+    is a multiple of 8, else alternating total / q - 4 and total / q + 4 when
+    total / q is 4 more than a multiple of 8 (the paper's equal blocks
+    before tile padding, e.g. 20 -> 16, 24); None otherwise."""
+    if total % q:
+        return None
+    w = total // q
+    if w % 8 == 0:
+        return [w] * q
+    if w % 8 == 4 and w > 4 and q % 2 == 0:
+        return [w - 4, w + 4] * (q // 2)
+    return None
 
 
 def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
@@ -828,12 +844,14 @@ def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
         dense = lambda: torch.matmul(X, W, out=Y)
         grid = {}
         best = None
-        for q in ((min(paper["q"], 64),) if args.products_fixed else (4, 8, 16, 32, 64)):
-            if D % (8 * q) or F % (8 * q):
+        for q in ((paper["q"],) if args.products_fixed else (4, 8, 16, 32, 64, 128, 256)):
+            sw, rw = group_widths(D, q), group_widths(F, q)
+            if sw is None or rw is None:
                 continue
-            alg = P.Algebra.equal(q, D, F)
+            alg = P.Algebra(q, sw, rw)
             plan = P.star_type_plan(q, torch.from_numpy(synth.cyclic_types(M, q)).to(dev))
-            for tiles in (("auto",) if args.products_fixed else ("wide", "small")):
+            sizes = ("auto",) if args.products_fixed else (("wide", "small") if q <= 64 else ("small",))
+            for tiles in sizes:
                 P.star_set_fwd_tiles(tiles)
                 fn = lambda a=alg, pl=plan: P.star_proj_fwd_planned(a, pl, X, W, Y=Y)
                 ms = statistics.median(T._run(fn, 20, False) for _ in range(3))
@@ -853,7 +871,7 @@ def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
         macs = P.star_count_macs(alg, rows)
         byts = 2 * (M * D + D * F + M * F)
         out[name] = {
-            "M": M, "D": D, "F": F, "q_star": q, "tiles": tiles, "block": [M // q, D // q, F // q],
+            "M": M, "D": D, "F": F, "q_star": q, "tiles": tiles, "block": [M // q, D / q, F / q],
             "dense_us": round(d_ms * 1e3, 1), "q_us": round(s_ms * 1e3, 1),
             "dense_us_flushed": round(d_f * 1e3, 1), "q_us_flushed": round(s_f * 1e3, 1),
             "speedup": [round(d_ms / s_ms, 2), round(d_f / s_f, 2)],

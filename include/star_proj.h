@@ -29,7 +29,13 @@
  *    errors are found on the host before anything is launched: the call then
  *    returns a non-zero status and writes nothing.  A failed launch returns
  *    STAR_ERR_HIP.  Nothing is printed and no exception crosses the ABI.
- *  - Group widths must be positive multiples of 8 and q at most STAR_MAX_Q.
+ *  - Group widths must be positive multiples of 8 and q at most STAR_MAX_Q,
+ *    except where an entry point says otherwise: the forward product of the
+ *    star and dense laws with bf16 operands (star_proj_fwd,
+ *    star_proj_fwd_planned), the type plan and the counting helpers take q
+ *    up to STAR_MAX_Q_FWD (the paper's kernel study sweeps q to 256).  A q
+ *    in (STAR_MAX_Q, STAR_MAX_Q_FWD] elsewhere is STAR_ERR_UNSUPPORTED; a q
+ *    above STAR_MAX_Q_FWD is STAR_ERR_ARG.
  *    Operand, output, bias and workspace pointers must be 16-byte aligned.
  *  - Row types must lie in [0, q).  This is not checked by the compute calls
  *    (star_validate_types checks it).  In the projection and FFN calls a row
@@ -57,6 +63,7 @@ extern "C" {
 #endif
 
 #define STAR_MAX_Q 64
+#define STAR_MAX_Q_FWD 256
 
 typedef enum {
     STAR_OK = 0,
@@ -138,6 +145,9 @@ typedef enum {
  *   Y         device [M, N] of dtype yt: act(Z)
  *   ws        device workspace of at least
  *             star_workspace_bytes(STAR_OP_FWD, alg, NULL, M) bytes
+ * q up to STAR_MAX_Q_FWD for the star and dense laws with bf16 operands
+ * (the 64 x 128 tiles of star_set_fwd_tiles; STAR_ERR_UNSUPPORTED for other
+ * laws or fp32 operands at q > STAR_MAX_Q).
  */
 star_status star_proj_fwd(const star_algebra *alg, int64_t M, const int32_t *row_type,
                           const void *X, star_dtype xt, const void *W, star_dtype wt,
@@ -308,6 +318,7 @@ star_status star_decode_gated(const star_algebra *up, const star_algebra *down, 
  *         by int32 offsets[q+1].  Rows with a type outside [0, q) are placed
  *         after offsets[q] and left out of every product.
  */
+ /* q up to STAR_MAX_Q_FWD. */
 size_t star_plan_bytes(int32_t q, int64_t M);
 star_status star_type_plan(int32_t q, int64_t M, const int32_t *row_type, void *plan,
                            size_t plan_bytes, hipStream_t stream);

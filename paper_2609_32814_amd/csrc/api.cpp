@@ -33,8 +33,8 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 struct Alg {
   int q = 0;
   int law = 0;
-  int64_t S[kMaxQGroups + 1];  // input group starts
-  int64_t R[kMaxQGroups + 1];  // output group starts
+  int64_t S[kMaxQFwd + 1];  // input group starts
+  int64_t R[kMaxQFwd + 1];  // output group starts
   uint64_t adj[kMaxQGroups] = {};     // law 3: bit j of adj[i] for the edge i -> j
   uint64_t adj_in[kMaxQGroups] = {};  // law 3: bit i of adj_in[j] for the edge i -> j
   int64_t K() const { return S[q]; }
@@ -53,12 +53,16 @@ bool host_in_support(const Alg& a, int i, int j, int k) {
   return a.law == STAR_LAW_DENSE || k == i || k == j;
 }
 
-star_status parse_alg(const star_algebra* a, Alg& out) {
+// `large`: the caller takes q up to STAR_MAX_Q_FWD (the forward product of
+// the star and dense laws); elsewhere q is at most STAR_MAX_Q.
+star_status parse_alg(const star_algebra* a, Alg& out, bool large = false) {
   if (!a || !a->s || !a->r) return STAR_ERR_ARG;
-  if (a->q < 1 || a->q > kMaxQGroups) return STAR_ERR_ARG;
+  if (a->q < 1 || a->q > kMaxQFwd) return STAR_ERR_ARG;
   if (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE && a->law != STAR_LAW_TENSOR2 &&
       a->law != STAR_LAW_GRAPH)
     return STAR_ERR_ARG;
+  if (a->q > kMaxQGroups && (!large || (a->law != STAR_LAW_STAR && a->law != STAR_LAW_DENSE)))
+    return STAR_ERR_UNSUPPORTED;
   if (a->law == STAR_LAW_GRAPH && !a->edges) return STAR_ERR_ARG;
   // the tensor power needs q = 2^L; the kernels take every contraction as
   // at most two contiguous group ranges, which holds for L <= 2
@@ -353,14 +357,39 @@ bool use_narrow_fwd(const GemmParams& p) {
   return fill <= 0.75 || p.q * row_tiles * col_tiles < 128.0;
 }
 
+// The small-tile forward: column tiles per output group, then the launch.
+hipError_t launch_narrow(NarrowParams& pn, hipStream_t stream) {
+  const int tn = gemm_narrow_cols();
+  pn.NTp[0] = 0;
+  for (int g = 0; g < pn.q; ++g) pn.NTp[g + 1] = pn.NTp[g] + (pn.R[g + 1] - pn.R[g] + tn - 1) / tn;
+  return launch_gemm_narrow(pn, gemm_narrow_row_blocks_upper(pn.M, pn.q), pn.NTp[pn.q], cu_count(), stream);
+}
+
 hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper,
                             hipStream_t stream) {
   if (mode == kModeFwd && use_narrow_fwd(p)) {
-    GemmParams pn = p;
-    const int tn = gemm_narrow_cols();
-    pn.NTp[0] = 0;
-    for (int g = 0; g < p.q; ++g) pn.NTp[g + 1] = pn.NTp[g] + (p.R[g + 1] - p.R[g] + tn - 1) / tn;
-    return launch_gemm_narrow(pn, gemm_narrow_row_blocks_upper(p.M, p.q), pn.NTp[p.q], cu_count(), stream);
+    NarrowParams pn;
+    std::memset(&pn, 0, sizeof(pn));
+    pn.q = p.q;
+    pn.law = p.law;
+    pn.M = p.M;
+    pn.K = p.K;
+    pn.N = p.N;
+    pn.act = p.act;
+    pn.ydtype = p.ydtype;
+    pn.perm = p.perm;
+    pn.offsets = p.offsets;
+    pn.A = p.A;
+    pn.B = p.B;
+    pn.bias = p.bias;
+    pn.Z = p.Z;
+    pn.Y = p.Y;
+    for (int g = 0; g <= p.q; ++g) {
+      pn.S[g] = p.S[g];
+      pn.R[g] = p.R[g];
+    }
+    for (int g = 0; g < kMaxQGroups; ++g) pn.adj[g] = p.adj[g];
+    return launch_narrow(pn, stream);
   }
   if (p.elem == 1) {
     GemmParams pa = p;
@@ -383,6 +412,29 @@ star_status run_plan(const int32_t* row_type, int64_t M, int q, void* ws, const 
 star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t* offsets,
                     const void* X, const void* W, int elem, const float* bias, star_act act,
                     void* Z, void* Y, star_dtype yt, hipStream_t stream) {
+  if (a.q > kMaxQGroups) {  // more groups than the other kernels take: the small tiles
+    NarrowParams pn;
+    std::memset(&pn, 0, sizeof(pn));
+    pn.q = a.q;
+    pn.law = a.law;
+    pn.M = static_cast<int32_t>(M);
+    pn.K = static_cast<int32_t>(a.K());
+    pn.N = static_cast<int32_t>(a.N());
+    pn.act = act;
+    pn.ydtype = yt;
+    pn.perm = perm;
+    pn.offsets = offsets;
+    pn.A = X;
+    pn.B = W;
+    pn.bias = bias;
+    pn.Z = Z;
+    pn.Y = Y;
+    for (int g = 0; g <= a.q; ++g) {
+      pn.S[g] = static_cast<int32_t>(a.S[g]);
+      pn.R[g] = static_cast<int32_t>(a.R[g]);
+    }
+    return hip_status(launch_narrow(pn, stream));
+  }
   GemmParams p;
   fill_common(p, a, M, elem, perm, offsets);
   p.A = X;
@@ -402,8 +454,9 @@ star_status run_fwd(const Alg& a, int64_t M, const int32_t* perm, const int32_t*
   return st;
 }
 
-star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a) {
-  star_status st = parse_alg(alg, a);
+star_status check_common(const star_algebra* alg, int64_t M, const int32_t* row_type, Alg& a,
+                         bool large = false) {
+  star_status st = parse_alg(alg, a, large);
   if (st != STAR_OK) return st;
   if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
   if (M > 0 && !row_type) return STAR_ERR_ARG;
@@ -432,7 +485,7 @@ const char* star_status_string(star_status s) {
 size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_algebra* alg2,
                             int64_t M) {
   Alg a;
-  if (parse_alg(alg, a) != STAR_OK || M < 0) return 0;
+  if (parse_alg(alg, a, op == STAR_OP_FWD) != STAR_OK || M < 0) return 0;
   switch (op) {
     case STAR_OP_FWD:
     case STAR_OP_BWD_DATA:
@@ -458,7 +511,7 @@ int star_set_fwd_tiles(int tiles) {
 
 star_status star_count_products(const star_algebra* alg, int64_t* per_type) {
   Alg a;
-  star_status st = parse_alg(alg, a);
+  star_status st = parse_alg(alg, a, true);
   if (st != STAR_OK) return st;
   if (!per_type) return STAR_ERR_ARG;
   for (int i = 0; i < a.q; ++i) {
@@ -472,7 +525,7 @@ star_status star_count_products(const star_algebra* alg, int64_t* per_type) {
 
 star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_type, int64_t* macs) {
   Alg a;
-  star_status st = parse_alg(alg, a);
+  star_status st = parse_alg(alg, a, true);
   if (st != STAR_OK) return st;
   if (!rows_per_type || !macs) return STAR_ERR_ARG;
   int64_t total = 0;
@@ -488,13 +541,13 @@ star_status star_count_macs(const star_algebra* alg, const int64_t* rows_per_typ
 }
 
 size_t star_plan_bytes(int32_t q, int64_t M) {
-  if (q < 1 || q > kMaxQGroups || M < 0 || M > kMaxDim) return 0;
+  if (q < 1 || q > kMaxQFwd || M < 0 || M > kMaxDim) return 0;
   return plan_layout(M, q).end;
 }
 
 star_status star_type_plan(int32_t q, int64_t M, const int32_t* row_type, void* plan,
                            size_t plan_bytes, hipStream_t stream) {
-  if (q < 1 || q > kMaxQGroups) return STAR_ERR_ARG;
+  if (q < 1 || q > kMaxQFwd) return STAR_ERR_ARG;
   if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
   if (M == 0) return STAR_OK;
   if (!row_type || !plan) return STAR_ERR_ARG;
@@ -512,10 +565,11 @@ star_status star_proj_fwd_planned(const star_algebra* alg, int64_t M, const void
                                   const float* bias, star_act act, void* Z_out, void* Y,
                                   star_dtype yt, hipStream_t stream) {
   Alg a;
-  star_status st = parse_alg(alg, a);
+  star_status st = parse_alg(alg, a, true);
   if (st != STAR_OK) return st;
   if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
   if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(yt) || xt != wt) return STAR_ERR_DTYPE;
+  if (a.q > kMaxQGroups && xt != STAR_BF16) return STAR_ERR_UNSUPPORTED;
   if (!valid_act(act)) return STAR_ERR_ARG;
   if (M == 0) return STAR_OK;
   if (!plan || !X || !W || !Y) return STAR_ERR_ARG;
@@ -533,9 +587,10 @@ star_status star_proj_fwd(const star_algebra* alg, int64_t M, const int32_t* row
                           const float* bias, star_act act, void* Z_out, void* Y, star_dtype yt,
                           void* ws, size_t ws_bytes, hipStream_t stream) {
   Alg a;
-  star_status st = check_common(alg, M, row_type, a);
+  star_status st = check_common(alg, M, row_type, a, true);
   if (st != STAR_OK) return st;
   if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(yt) || xt != wt) return STAR_ERR_DTYPE;
+  if (a.q > kMaxQGroups && xt != STAR_BF16) return STAR_ERR_UNSUPPORTED;
   if (!valid_act(act)) return STAR_ERR_ARG;
   if (M == 0) return STAR_OK;
   if (!X || !W || !Y) return STAR_ERR_ARG;

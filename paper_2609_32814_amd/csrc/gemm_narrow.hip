@@ -4,8 +4,9 @@
 // persistent GEMM are mostly empty.  Here a tile is 64 rows of one type
 // (rows taken in type order through the plan) x 128 columns of one output
 // group, the contraction is the concatenation of the input groups in the
-// law's B(i, j) (a K step of 64 never straddles two groups; a group's last
-// step is zero-padded), and a workgroup of 4 wavefronts (2 x 2, each 32 rows
+// law's B(i, j) (at most two contiguous K ranges for every law; it runs in
+// 64-deep K steps that may span both ranges, and the last one is zero-filled
+// past its end), and a workgroup of 4 wavefronts (2 x 2, each 32 rows
 // x 64 columns: two v_mfma_f32_32x32x16_bf16 blocks) computes it with both
 // operands staged in LDS by direct global-to-LDS copies.  Workgroups are
 // persistent: each walks its tiles as one stream of K steps whose copies run
@@ -90,12 +91,35 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
-// input groups in B(i, j) of the forward product, as a bit mask
-__device__ __forceinline__ uint64_t fwd_mask(const GemmParams& p, int i, int j) {
-  if (p.law == 1) return p.q >= 64 ? ~0ull : ((1ull << p.q) - 1ull);
-  if (p.law == 2) return tensor_mask(kModeFwd, p.q, i, j);
-  if (p.law == 3) return graph_mask(p, kModeFwd, i, j);
-  return (1ull << i) | (1ull << j);
+// The contraction of the forward tile (row type i, output group j) as at
+// most two contiguous K ranges [a0, a0 + l0) and [a1, a1 + l1): B(i, j) is
+// {i, j} for the star law (the graph law: {i} on the diagonal, {i, j} on an
+// edge, nothing otherwise), every group for the dense law, and for the
+// tensor square at most two runs of consecutive groups.
+__device__ __forceinline__ void fwd_ranges(const NarrowParams& p, int i, int j, int32_t& a0, int32_t& l0,
+                                           int32_t& a1, int32_t& l1) {
+  a0 = l0 = a1 = l1 = 0;
+  if (p.law == 1) {
+    l0 = p.K;
+    return;
+  }
+  if (p.law == 2) {
+    int lo0, hi0, lo1, hi1;
+    mask_ranges(tensor_mask(kModeFwd, p.q, i, j), lo0, hi0, lo1, hi1);
+    a0 = p.S[lo0];
+    l0 = p.S[hi0] - a0;
+    a1 = p.S[lo1];
+    l1 = p.S[hi1] - a1;
+    return;
+  }
+  if (p.law == 3 && i != j && !((p.adj[i] >> j) & 1ull)) return;  // not a slot of the row
+  const int lo = min(i, j), hi = max(i, j);
+  a0 = p.S[lo];
+  l0 = p.S[lo + 1] - a0;
+  if (hi != lo) {
+    a1 = p.S[hi];
+    l1 = p.S[hi + 1] - a1;
+  }
 }
 
 // LDS layouts.  A: 64 rows x 64 K (128 bytes a row), 16-byte chunk c of row r
@@ -106,17 +130,17 @@ __device__ __forceinline__ int a_off(int r, int c) { return r * 128 + ((c ^ (r &
 __device__ __forceinline__ int b_off(int k, int c) { return k * 256 + ((c ^ (2 * (k & 3))) << 4); }
 
 // A tile of the list: rows [pos0, pend) of the plan, columns [cstart, cend),
-// the input groups of its contraction and its K steps (0: nothing to do).
+// the K ranges of its contraction and its K steps (0: nothing to do).
 struct NTile {
   int32_t pos0, pend, cstart, cend, nsteps;
-  uint64_t mask;
+  int32_t a0, l0, a1, l1;
 };
 
 // The fp32 epilogue of one tile for one lane: row 32 wr + lr of the tile (`row`
 // in the output, `rok` whether it exists), columns 64 wc + 32 cb + 8 a +
 // 4 lh + 0..3 for cb < 2, a < 4.  Every lane stores all 8 blocks (and 8 of Z
 // when asked for): blocks without an element go to the lane's sink.
-__device__ __forceinline__ void narrow_epilogue(const GemmParams& p, const f32x16_t (&acc)[2], bool rok, int32_t row,
+__device__ __forceinline__ void narrow_epilogue(const NarrowParams& p, const f32x16_t (&acc)[2], bool rok, int32_t row,
                                                 int32_t cstart, int32_t cend, int cl0, const float* bias_tile,
                                                 char* sink) {
   constexpr int esz = 4;
@@ -150,7 +174,7 @@ __device__ __forceinline__ void narrow_epilogue(const GemmParams& p, const f32x1
     }
 }
 
-__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams p, int32_t n_ct, int32_t wg_per_xcd,
+__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowParams p, int32_t n_ct, int32_t wg_per_xcd,
                                                                  int32_t band) {
   extern __shared__ __attribute__((aligned(16))) char smem[];  // kNStages stages of (A, B)
   __shared__ int32_t rows_s[kSlots][kNRows];                    // plan positions of the tile's rows
@@ -163,35 +187,39 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
   const int lr = lane & 31, lh = lane >> 5;
   const int q = p.q;
 
-  // the plan's offsets, lane t holding type t's, and the running count of
-  // 64-row blocks over the types
-  int32_t o0 = 0, o1 = 0, nb = 0;
-  if (lane < q) {
-    o0 = p.offsets[lane];
-    o1 = p.offsets[lane + 1];
-    nb = (o1 - o0 + kNRows - 1) / kNRows;
-  }
-  int32_t incl = nb;
+  // Per-type and per-group tables in chunks of 64 (chunk c, lane l: type or
+  // group 64 c + l): the running count of 64-row blocks over the types and
+  // the column-tile prefix of the output groups (past the last group: no
+  // tile reaches it).
+  constexpr int kCh = kMaxQFwd / 64;
+  int32_t incl[kCh], ntp1[kCh];
+  int32_t n_blocks = 0;
 #pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int32_t u = __shfl_up(incl, d);
-    if (lane >= d) incl += u;
+  for (int c = 0; c < kCh; ++c) {
+    const int t = 64 * c + lane;
+    int32_t v = 0;
+    ntp1[c] = 0x7fffffff;
+    if (t < q) {
+      v = (p.offsets[t + 1] - p.offsets[t] + kNRows - 1) / kNRows;
+      if (t + 1 < q) ntp1[c] = p.NTp[t + 1];
+    }
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int32_t u = __shfl_up(v, d);
+      if (lane >= d) v += u;
+    }
+    incl[c] = n_blocks + v;
+    n_blocks += __builtin_amdgcn_readlane(v, 63);
   }
-  // per-group figures, lane x holding group x's: column tile prefix and
-  // column range of output group x, contraction range and K steps of input
-  // group x
-  int32_t ntp0 = 0, ntp1 = 0x7fffffff, r0 = 0, r1 = 0, s0 = 0, s1 = 0, ns = 0;
-  if (lane < q) {
-    ntp0 = p.NTp[lane];
-    r0 = p.R[lane];
-    r1 = p.R[lane + 1];
-    s0 = p.S[lane];
-    s1 = p.S[lane + 1];
-    ns = (s1 - s0 + kNK - 1) / kNK;
-    if (lane + 1 < q) ntp1 = p.NTp[lane + 1];
-  }
-  int ns_bits = 0;  // bits of the largest step count
-  while (__ballot((ns >> ns_bits) != 0)) ++ns_bits;
+  // the value lane (x mod 64) holds in chunk x / 64 of a table
+  auto pick = [&](const int32_t (&tab)[kCh], int x) -> int32_t {
+    const int c = x >> 6;
+    int32_t v = tab[0];
+#pragma unroll
+    for (int k = 1; k < kCh; ++k)
+      if (c == k) v = tab[k];
+    return __builtin_amdgcn_readlane(v, x & 63);
+  };
 
   // The tiles: (row block rb, column tile ct), the row blocks numbered type
   // by type (block rb is type i's, the first whose running block count
@@ -203,9 +231,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
   // blocks side by side: a weight tile is fetched once per band (the
   // diagonal blocks, which every type reads, once per band instead of once
   // per type) and the band's rows stay in L2.  The region's workgroups take
-  // every wg_per_xcd-th item.  A tile's steps are those of the input groups
-  // in its mask, counted bit plane by bit plane of the per-group step counts.
-  const int32_t n_blocks = __builtin_amdgcn_readlane(incl, q - 1);
+  // every wg_per_xcd-th item.
   const int xcd = blockIdx.x & 7;
   int32_t rb0 = 0, rb1 = n_blocks, ct0 = 0, ct1 = n_ct;
   if (n_blocks >= 8) {
@@ -225,16 +251,23 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
     const int32_t cl = within / bsz;
     const int32_t rb = rb0 + bi * band + (within - cl * bsz);
     const int32_t ct = ct0 + cl;
-    const int i = __builtin_ctzll(__ballot(lane < q && incl > rb));
-    const int32_t blk = rb - (__builtin_amdgcn_readlane(incl, i) - __builtin_amdgcn_readlane(nb, i));
-    t.pos0 = __builtin_amdgcn_readlane(o0, i) + blk * kNRows;
-    t.pend = min(__builtin_amdgcn_readlane(o1, i), t.pos0 + kNRows);
-    const int j = __popcll(__ballot(ct >= ntp1));
-    t.cstart = __builtin_amdgcn_readlane(r0, j) + (ct - __builtin_amdgcn_readlane(ntp0, j)) * kNCols;
-    t.cend = min(__builtin_amdgcn_readlane(r1, j), t.cstart + kNCols);
-    t.mask = fwd_mask(p, i, j);  // empty for a graph-law non-slot (the fill kernel writes it)
-    t.nsteps = 0;
-    for (int b = 0; b < ns_bits; ++b) t.nsteps += __popcll(__ballot((ns >> b) & 1) & t.mask) << b;
+    int i = 0;  // the type: the first whose running block count passes rb
+#pragma unroll
+    for (int c = kCh - 1; c >= 0; --c) {
+      const uint64_t m = __ballot(64 * c + lane < q && incl[c] > rb);
+      if (m) i = 64 * c + __builtin_ctzll(m);
+    }
+    const int32_t o_i = p.offsets[i], o_i1 = p.offsets[i + 1];
+    const int32_t blk = rb - (pick(incl, i) - (o_i1 - o_i + kNRows - 1) / kNRows);
+    t.pos0 = o_i + blk * kNRows;
+    t.pend = min(o_i1, t.pos0 + kNRows);
+    int j = 0;  // the output group: column tiles at or past the next groups' prefixes
+#pragma unroll
+    for (int c = 0; c < kCh; ++c) j += __popcll(__ballot(ct >= ntp1[c]));
+    t.cstart = p.R[j] + (ct - p.NTp[j]) * kNCols;
+    t.cend = min(p.R[j + 1], t.cstart + kNCols);
+    fwd_ranges(p, i, j, t.a0, t.l0, t.a1, t.l1);
+    t.nsteps = (t.l0 + t.l1 + kNK - 1) / kNK;
     return t;
   };
   const int32_t last = nrb * nct;
@@ -268,15 +301,14 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
     } else {
       t.nsteps = 0;
       t.pos0 = t.pend = t.cstart = t.cend = 0;
-      t.mask = 0;
+      t.a0 = t.l0 = t.a1 = t.l1 = 0;
     }
     dma4(lane < t.pend - t.pos0 ? static_cast<const void*>(p.perm + t.pos0 + lane) : zero, lds_addr(rows_s[slot]));
     dma16(p.bias && t.cstart + 4 * lane < t.cend ? static_cast<const void*>(p.bias + t.cstart + 4 * lane) : zero,
           lds_addr(bias_s[slot]));
     if (lane == 0) {
       *reinterpret_cast<int4*>(desc_s[slot]) = make_int4(t.pend - t.pos0, t.cstart, t.cend, t.nsteps);
-      *reinterpret_cast<int4*>(desc_s[slot] + 4) =
-          make_int4(static_cast<int32_t>(t.mask), static_cast<int32_t>(t.mask >> 32), 0, 0);
+      *reinterpret_cast<int4*>(desc_s[slot] + 4) = make_int4(t.a0, t.l0, t.a1, t.l1);
     }
     ++s_n;
   };
@@ -285,11 +317,14 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
   // kNStages - 1 elements ahead of the consumer; every element is 6 copies
   // per wave (2 of A, 4 of B).  A tile's descriptor is read when its first
   // element is copied (a barrier after the scheduler wrote it); the copy
-  // sources of its A rows and B columns are set up then, and each step
-  // offsets them by its K.  Rows past the tile's read row 0 and columns past
-  // it read the group's last columns: their products are never stored.
-  int32_t p_n = 0, p_s = 0, p_nsteps = 0, p_k = 0, p_kend = 0;
-  uint64_t p_mask = 0;
+  // sources of its A rows and B columns are set up then.  Step s covers
+  // positions [64 s, 64 s + 64) of the concatenated K ranges: a lane's
+  // position below l0 reads K = a0 + position, below l0 + l1 K = a1 +
+  // position - l0, past that zeros (8-wide A chunks never span the two
+  // ranges: the widths are multiples of 8).  Rows past the tile's read row 0
+  // and columns past it read the group's last columns: their products are
+  // never stored.
+  int32_t p_n = 0, p_s = 0, p_nsteps = 0, p_a0 = 0, p_l0 = 0, p_a1 = 0, p_len = 0;
   bool p_fresh = true, p_done = false;
   const uint16_t* abase[2];
   const uint16_t* bbase[4];
@@ -303,11 +338,10 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
         p_done = true;
       } else {
         const int32_t cstart = uni(d0.y);
-        p_mask = static_cast<uint64_t>(static_cast<uint32_t>(uni(d1.x))) |
-                 (static_cast<uint64_t>(static_cast<uint32_t>(uni(d1.y))) << 32);
-        const int x = __builtin_ctzll(p_mask);
-        p_k = __builtin_amdgcn_readlane(s0, x);
-        p_kend = __builtin_amdgcn_readlane(s1, x);
+        p_a0 = uni(d1.x);
+        p_l0 = uni(d1.y);
+        p_a1 = uni(d1.z);
+        p_len = p_l0 + uni(d1.w);
         p_s = 0;
         const int32_t* rows = rows_s[p_n % kSlots];
 #pragma unroll
@@ -325,32 +359,28 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
     }
     if (p_done) return false;
     const uint32_t As = smem_base + stage * kStage, Bs = As + kA;
-    const int64_t kofs = static_cast<int64_t>(p_k) * p.N;
-    if (p_kend - p_k >= kNK) {
+    const int32_t pos = kNK * p_s;
+    const int32_t k0 = p_a0 + pos, k1 = p_a1 - p_l0 + pos;  // K of position pos + x: k0 + x or k1 + x
+    if (pos + kNK <= p_l0 || (pos >= p_l0 && pos + kNK <= p_len)) {  // the step lies in one range
+      const int32_t k = pos + kNK <= p_l0 ? k0 : k1;
+      const int64_t kofs = static_cast<int64_t>(k) * p.N;
 #pragma unroll
-      for (int u = 0; u < 2; ++u) dma16(abase[u] + p_k, As + (wave + 4 * u) * 1024);
+      for (int u = 0; u < 2; ++u) dma16(abase[u] + k, As + (wave + 4 * u) * 1024);
 #pragma unroll
       for (int u = 0; u < 4; ++u) dma16(bbase[u] + kofs, Bs + (wave + 4 * u) * 1024);
-    } else {  // the group's last step runs past its end: zeros there
+    } else {  // the step spans both ranges or runs past the end
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int r = 8 * (wave + 4 * u) + (lane >> 3), c = (lane & 7) ^ (r & 7);
-        dma16(p_k + 8 * c < p_kend ? static_cast<const void*>(abase[u] + p_k) : zero, As + (wave + 4 * u) * 1024);
+        const int r = 8 * (wave + 4 * u) + (lane >> 3), x = 8 * ((lane & 7) ^ (r & 7));
+        const int32_t k = pos + x < p_l0 ? k0 : k1;
+        dma16(pos + x < p_len ? static_cast<const void*>(abase[u] + k) : zero, As + (wave + 4 * u) * 1024);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int kr = 4 * (wave + 4 * u) + (lane >> 4);
-        dma16(p_k + kr < p_kend ? static_cast<const void*>(bbase[u] + kofs) : zero, Bs + (wave + 4 * u) * 1024);
-      }
-    }
-    // advance: next K step of this group, next group, or the next tile
-    p_k += kNK;
-    if (p_k >= p_kend) {
-      p_mask &= p_mask - 1;
-      if (p_mask) {
-        const int x = __builtin_ctzll(p_mask);
-        p_k = __builtin_amdgcn_readlane(s0, x);
-        p_kend = __builtin_amdgcn_readlane(s1, x);
+        const int x = 4 * (wave + 4 * u) + (lane >> 4);
+        const int32_t k = pos + x < p_l0 ? k0 : k1;
+        dma16(pos + x < p_len ? static_cast<const void*>(bbase[u] + static_cast<int64_t>(k) * p.N) : zero,
+              Bs + (wave + 4 * u) * 1024);
       }
     }
     if (++p_s == p_nsteps) {
@@ -493,7 +523,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const GemmParams
 int32_t gemm_narrow_row_blocks_upper(int64_t M, int q) { return static_cast<int32_t>(M / kNRows + q); }
 int gemm_narrow_cols() { return kNCols; }
 
-hipError_t launch_gemm_narrow(const GemmParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream) {
+hipError_t launch_gemm_narrow(const NarrowParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream) {
   // n_rb bounds the row blocks from above (the kernel counts them from the
   // plan's offsets)
   const int64_t items = static_cast<int64_t>(n_rb) * n_ct;

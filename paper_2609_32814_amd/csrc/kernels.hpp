@@ -88,7 +88,30 @@ hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles,
 // of that width; n_rb bounds the row blocks over all types.
 int gemm_narrow_cols();
 int32_t gemm_narrow_row_blocks_upper(int64_t M, int q);
-hipError_t launch_gemm_narrow(const GemmParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream);
+// Its parameters: the forward product for q up to kMaxQFwd groups (the
+// star and dense laws; the other laws for q <= kMaxQGroups).
+constexpr int kMaxQFwd = 256;
+struct NarrowParams {
+  int32_t q;
+  int32_t law;
+  int32_t M;
+  int32_t K;
+  int32_t N;
+  int32_t act;
+  int32_t ydtype;
+  const int32_t* perm;
+  const int32_t* offsets;
+  const void* A;  // X [M, K] bf16
+  const void* B;  // W [K, N] bf16
+  const float* bias;
+  void* Z;
+  void* Y;
+  int32_t S[kMaxQFwd + 1];    // input group starts
+  int32_t R[kMaxQFwd + 1];    // output group starts
+  int32_t NTp[kMaxQFwd + 1];  // column tiles per output group, prefix
+  uint64_t adj[kMaxQGroups];  // law 3 (q <= kMaxQGroups): bit j of adj[i] marks the edge i -> j
+};
+hipError_t launch_gemm_narrow(const NarrowParams& p, int32_t n_rb, int32_t n_ct, int cus, hipStream_t stream);
 // Gated FFN elementwise parts (swiglu.hip); n a multiple of 8, elem 1 bf16
 // or 0 fp32, 16-byte aligned buffers.
 hipError_t launch_swiglu_fwd(int64_t n, int elem, const void* zg, const void* zu, void* h, hipStream_t stream);

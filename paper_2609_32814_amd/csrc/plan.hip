@@ -3,7 +3,7 @@
 //
 // Up to 64 Ki rows: many workgroups (type_plan_wide_kernel below).  Longer
 // type vectors: one workgroup of 1024 threads (16 wavefronts).  All threads first copy the
-// type vector into LDS as bytes with independent coalesced loads (one round
+// type vector into LDS as 16-bit values with independent coalesced loads (one round
 // trip to memory instead of one per window), for up to 64 Ki rows; longer
 // vectors are read from memory in the passes below.  The rows are cut into
 // 16 contiguous chunks, one per wavefront; a wavefront walks its chunk in
@@ -23,6 +23,7 @@ namespace starq {
 namespace {
 
 constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxQ = kMaxQFwd;  // types the plan takes (the forward product's limit)
 constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kPlanLdsRows = 65536;
 
@@ -42,11 +43,11 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
                                                                  int32_t* __restrict__ perm,
                                                                  int32_t* __restrict__ offsets) {
   // counts[w][t], t = q is the out-of-range bucket
-  __shared__ int32_t counts[kPlanWaves][kMaxQ + 1];
-  __shared__ uint8_t tl[kPlanLdsRows];  // type (or q if out of range) per row
+  __shared__ int32_t counts[kPlanWaves][kPlanMaxQ + 1];
+  __shared__ uint16_t tl[kPlanLdsRows];  // type (or q if out of range) per row
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kPlanWaves * (kMaxQ + 1); i += kPlanThreads)
+  for (int i = threadIdx.x; i < kPlanWaves * (kPlanMaxQ + 1); i += kPlanThreads)
     (&counts[0][0])[i] = 0;
   const bool in_lds = M <= kPlanLdsRows;
   if (in_lds) {
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int32_t row = base + u * kPlanThreads + threadIdx.x;
-        if (row < M) tl[row] = static_cast<uint8_t>((v[u] >= 0 && v[u] < q) ? v[u] : q);
+        if (row < M) tl[row] = static_cast<uint16_t>((v[u] >= 0 && v[u] < q) ? v[u] : q);
       }
     }
   }
@@ -146,12 +147,12 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
                                                                       int32_t M, int q, int nbits,
                                                                       int32_t* __restrict__ perm,
                                                                       int32_t* __restrict__ offsets) {
-  __shared__ int32_t total[kMaxQ + 1], before[kMaxQ + 1];
-  __shared__ int32_t wcount[kPlanWaves][kMaxQ + 1];
+  __shared__ int32_t total[kPlanMaxQ + 1], before[kPlanMaxQ + 1];
+  __shared__ int32_t wcount[kPlanWaves][kPlanMaxQ + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int32_t r0 = blockIdx.x * kPlanRowsPerBlock;
   for (int i = threadIdx.x; i <= q; i += kPlanThreads) total[i] = before[i] = 0;
-  for (int i = threadIdx.x; i < kPlanWaves * (kMaxQ + 1); i += kPlanThreads) (&wcount[0][0])[i] = 0;
+  for (int i = threadIdx.x; i < kPlanWaves * (kPlanMaxQ + 1); i += kPlanThreads) (&wcount[0][0])[i] = 0;
   __syncthreads();
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   auto cls = [&](int t) { return (t >= 0 && t < q) ? t : q; };

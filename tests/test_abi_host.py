@@ -105,9 +105,36 @@ def test_argument_errors_before_launch(P):
     assert _raw_fwd(P, good.ref, 4, ws=0) == 5                         # no workspace
     assert _raw_fwd(P, good.ref, -1) == 2                              # negative M
     assert _raw_fwd(P, good.ref, 0, X=0, W=0, Y=0, ws=0, rt=0) == 0    # M = 0: no-op
-    big = B.Algebra(65, [8] * 65, [8] * 65)
-    assert _raw_fwd(P, big.ref, 4) == 1                                # q above STAR_MAX_Q
+    big = B.Algebra(257, [8] * 257, [8] * 257)
+    assert _raw_fwd(P, big.ref, 4) == 1                                # q above STAR_MAX_Q_FWD
     assert P.star_status_string(5).startswith("workspace")
+
+
+def test_large_q_limits(P):
+    """q in (64, 256]: the forward product of the star and dense laws with
+    bf16 operands, the plan and the counting helpers take it; everything
+    else refuses it on the host (fake pointers, nothing launched)."""
+    import numpy as np
+    import paper_2609_32814_amd.binding as B
+    err = {v: k for k, v in P.binding.STATUS_NAMES.items()}
+    a128 = B.Algebra.equal(128, 16 * 128, 40 * 128)
+    assert P.star_count_products(a128) == [255] * 128
+    assert P.star_count_products(B.Algebra.equal(256, 8 * 256, 8 * 256)) == [511] * 256
+    assert P.star_count_macs(a128, [1] * 128) == 128 * 40 * 16 * (1 + 2 * 127)
+    assert P.star_workspace_bytes("fwd", a128, None, 1000) >= 4 * 1000 + 4 * 129
+    assert P.star_workspace_bytes("bwd_data", a128, None, 1000) == 0
+    assert P.star_workspace_bytes("bwd_weight", a128, None, 1000) == 0
+    assert P.star_plan_bytes(256, 10) > 0 and P.star_plan_bytes(257, 10) == 0
+    assert _raw_fwd(P, a128.ref, 4, xt=0, wt=0, yt=0) == err["STAR_ERR_UNSUPPORTED"]  # fp32 operands
+    E = np.zeros((65, 65), np.uint8)
+    E[0, 1] = 1
+    g65 = B.Algebra(65, [8] * 65, [8] * 65, "graph", E)
+    assert _raw_fwd(P, g65.ref, 4) == err["STAR_ERR_UNSUPPORTED"]                      # graph law
+    V = ctypes.c_void_p
+    st = P.binding.LIB.star_proj_bwd_data(a128.ref, 4, V(16), V(16), 1, V(16), 1, None, 0, V(16), 1,
+                                          V(16), 1 << 20, None)
+    assert st == err["STAR_ERR_UNSUPPORTED"]
+    assert P.binding.LIB.star_type_plan(257, 4, V(16), V(16), 1 << 20, None) == err["STAR_ERR_ARG"]
 
 
 def test_decode_rejects_too_many_rows(P):

@@ -1,6 +1,6 @@
 """GPU parity of the forward product with many small groups (Sec. "Kernel
 Scaling on Transformer Shapes"): the tiles of 64 rows x 128 columns that
-carry q up to 64 at the widths of the paper's projection study, against the
+carry q up to 256 at the widths of the paper's projection study, against the
 fp64 oracle on the same seeded inputs.
 
 Each case runs the same inputs through both tile sizes (forced with
@@ -10,8 +10,9 @@ tiles (groups 64 wide; under the graph law a diagonal-only tile contracts a
 single group and the tiles of non-edges are skipped), K tails (input widths
 not multiples of 64), column tails (output widths not multiples of 128),
 empty and one-row types, every law, bias, GELU and the pre-activation, fp32
-and bf16 outputs, and the paper's projection shapes at full size on sampled
-rows (the product is row-local).
+and bf16 outputs, q = 128 and 256 (K steps spanning several 8- to 40-wide
+groups), and the paper's projection shapes at full size on sampled rows (the
+product is row-local).
 """
 
 import numpy as np
@@ -145,6 +146,47 @@ def test_small_tiles_graph_law(P):
         assert rel_fro(to_host(Y), refY) <= TOL_BF16, tiles
 
 
+# q above 64 (the star and dense laws): groups 8 to 40 wide, so a 64-deep K
+# step spans both ranges of a tile's contraction or several groups
+LARGE_Q = [
+    ("star", 128, [16] * 128, [40] * 128, 3000, "random"),
+    ("star", 256, _s([8, 16, 24, 40], 256), _s([8, 24, 136, 96], 256), 2000, "gaps"),
+    ("dense", 128, [16] * 128, [8] * 128, 400, "random"),
+]
+
+
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+@pytest.mark.parametrize("law,q,s,r,M,types", LARGE_Q)
+def test_large_q_bias_gelu(P, out, law, q, s, r, M, types):
+    import torch
+    ga, oa = P.Algebra(q, s, r, law), oracle.Alg(q, tuple(s), tuple(r), law)
+    seed = 2600 + q + M
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, "bf16")
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), 0.05, "bf16")
+    b = synth.gaussian(seed, 2, (oa.N,), 0.05, "f32")
+    t = _types(types, M, q, seed)
+    odt = torch.float32 if out == "f32" else torch.bfloat16
+    refY, refZ, _, _ = oracle.proj_fwd(oa, t, X.exact, W.exact, b.exact, "gelu", want_z=True)
+    Y, Z = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), f32_dev(b.exact), "gelu", Z_out=True,
+                           out_dtype=odt)
+    gY, gZ = to_host(Y), to_host(Z)
+    assert rel_fro(gZ, refZ) <= TOL_BF16
+    assert rel_fro(gY, refY) <= TOL_BF16
+    live = np.linalg.norm(refZ, axis=1) > 0
+    diff = np.linalg.norm(gZ - refZ, axis=1)[live] / np.linalg.norm(refZ, axis=1)[live]
+    assert diff.max() <= 4 * TOL_BF16
+
+
+def test_large_q_refused_where_not_built(P):
+    """fp32 operands at q > 64 are refused before anything runs."""
+    import torch
+    ga = P.Algebra.equal(128, 16 * 128, 16 * 128)
+    X = torch.zeros((4, 16 * 128), device="cuda")
+    W = torch.zeros((16 * 128, 16 * 128), device="cuda")
+    with pytest.raises(Exception, match="UNSUPPORTED|unsupported"):
+        P.star_proj_fwd(ga, types_dev(np.zeros(4, np.int32)), X, W)
+
+
 def _sample_rows(M, n, seed):
     rng = np.random.default_rng([seed, 11])
     return np.unique(np.concatenate([[0, 1, M - 2, M - 1], rng.choice(M, n, replace=False)]))
@@ -160,7 +202,7 @@ SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("name,D,F,q", SHAPES)
+@pytest.mark.parametrize("name,D,F,q", SHAPES + [("Qwen3-1.7B", 2048, 6144, 128), ("Qwen3-8B", 4096, 12288, 256)])
 def test_projection_shapes_full_size_sampled(P, name, D, F, q):
     import torch
     M = 2048
