@@ -24,6 +24,7 @@
 // type-dependent maps) serves the same regime; here both products of a
 // tile are accumulated in registers before one output store.
 #include <algorithm>
+#include <type_traits>
 
 #include "gemm_common.hpp"
 
@@ -96,7 +97,9 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 // {i, j} for the star law (the graph law: {i} on the diagonal, {i, j} on an
 // edge, nothing otherwise), every group for the dense law, and for the
 // tensor square at most two runs of consecutive groups.
-__device__ __forceinline__ void fwd_ranges(const NarrowParams& p, int i, int j, int32_t& a0, int32_t& l0,
+// `S(x)`: the start of input group x (x <= q).
+template <typename SF>
+__device__ __forceinline__ void fwd_ranges(const NarrowParams& p, SF S, int i, int j, int32_t& a0, int32_t& l0,
                                            int32_t& a1, int32_t& l1) {
   a0 = l0 = a1 = l1 = 0;
   if (p.law == 1) {
@@ -106,19 +109,19 @@ __device__ __forceinline__ void fwd_ranges(const NarrowParams& p, int i, int j, 
   if (p.law == 2) {
     int lo0, hi0, lo1, hi1;
     mask_ranges(tensor_mask(kModeFwd, p.q, i, j), lo0, hi0, lo1, hi1);
-    a0 = p.S[lo0];
-    l0 = p.S[hi0] - a0;
-    a1 = p.S[lo1];
-    l1 = p.S[hi1] - a1;
+    a0 = S(lo0);
+    l0 = S(hi0) - a0;
+    a1 = S(lo1);
+    l1 = S(hi1) - a1;
     return;
   }
   if (p.law == 3 && i != j && !((p.adj[i] >> j) & 1ull)) return;  // not a slot of the row
   const int lo = min(i, j), hi = max(i, j);
-  a0 = p.S[lo];
-  l0 = p.S[lo + 1] - a0;
+  a0 = S(lo);
+  l0 = S(lo + 1) - a0;
   if (hi != lo) {
-    a1 = p.S[hi];
-    l1 = p.S[hi + 1] - a1;
+    a1 = S(hi);
+    l1 = S(hi + 1) - a1;
   }
 }
 
@@ -128,6 +131,45 @@ __device__ __forceinline__ void fwd_ranges(const NarrowParams& p, int i, int j, 
 // bank conflicts (a row-contiguous read of 8 rows, a transposing read of 4).
 __device__ __forceinline__ int a_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 __device__ __forceinline__ int b_off(int k, int c) { return k * 256 + ((c ^ (2 * (k & 3))) << 4); }
+
+// A per-lane table of kMaxQFwd entries in four chunks of 64 (chunk c, lane
+// l: entry 64 c + l), held in named registers: chunks are reached by
+// compile-time index (get) or through scalars (entry), never by address, so
+// the table never moves to scratch memory.
+struct Ch4 {
+  int32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+  template <int C>
+  __device__ __forceinline__ int32_t& get() {
+    if constexpr (C == 0) return v0;
+    else if constexpr (C == 1) return v1;
+    else if constexpr (C == 2) return v2;
+    else return v3;
+  }
+  // entry 64 c + l (uniform) of a table of NCH chunks: every chunk's lane l
+  // read into a scalar, then the scalar selected (a select of the vectors
+  // could be turned into an indexed access of a stack copy)
+  template <int NCH>
+  __device__ __forceinline__ int32_t entry(int c, int l) const {
+    if constexpr (NCH == 1) {
+      return __builtin_amdgcn_readlane(v0, l);
+    } else {
+      const int32_t e0 = __builtin_amdgcn_readlane(v0, l), e1 = __builtin_amdgcn_readlane(v1, l);
+      const int32_t e2 = __builtin_amdgcn_readlane(v2, l), e3 = __builtin_amdgcn_readlane(v3, l);
+      return c == 0 ? e0 : (c == 1 ? e1 : (c == 2 ? e2 : e3));
+    }
+  }
+};
+static_assert(kMaxQFwd == 4 * 64, "four chunks of 64");
+// f(chunk) for the first NCH chunks (1: q <= 64, 4: q <= 256)
+template <int NCH, typename F>
+__device__ __forceinline__ void each_chunk(F&& f) {
+  f(std::integral_constant<int, 0>{});
+  if constexpr (NCH > 1) {
+    f(std::integral_constant<int, 1>{});
+    f(std::integral_constant<int, 2>{});
+    f(std::integral_constant<int, 3>{});
+  }
+}
 
 // A tile of the list: rows [pos0, pend) of the plan, columns [cstart, cend),
 // the K ranges of its contraction and its K steps (0: nothing to do).
@@ -174,6 +216,7 @@ __device__ __forceinline__ void narrow_epilogue(const NarrowParams& p, const f32
     }
 }
 
+template <int NCH>
 __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowParams p, int32_t n_ct, int32_t wg_per_xcd,
                                                                  int32_t band) {
   extern __shared__ __attribute__((aligned(16))) char smem[];  // kNStages stages of (A, B)
@@ -187,38 +230,40 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
   const int lr = lane & 31, lh = lane >> 5;
   const int q = p.q;
 
-  // Per-type and per-group tables in chunks of 64 (chunk c, lane l: type or
-  // group 64 c + l): the running count of 64-row blocks over the types and
-  // the column-tile prefix of the output groups (past the last group: no
-  // tile reaches it).
-  constexpr int kCh = kMaxQFwd / 64;
-  int32_t incl[kCh], ntp1[kCh];
+  // Per-type and per-group tables in registers, in chunks of 64 (chunk c,
+  // lane l: type or group 64 c + l), so that describing a tile reads no
+  // memory: the plan offsets and the running count of 64-row blocks of the
+  // types; the input group starts, output group starts and column-tile
+  // prefix of the groups, and that prefix one group on (past the last
+  // group: no tile reaches it).  Entry q of the starts is K, N or M.
+  Ch4 off, incl, s0, r0, ntp0, ntp1;
   int32_t n_blocks = 0;
-#pragma unroll
-  for (int c = 0; c < kCh; ++c) {
+  const int32_t off_end = p.offsets[q];
+  each_chunk<NCH>([&](auto C) {
+    constexpr int c = decltype(C)::value;
     const int t = 64 * c + lane;
     int32_t v = 0;
-    ntp1[c] = 0x7fffffff;
+    ntp1.get<c>() = 0x7fffffff;
     if (t < q) {
+      off.get<c>() = p.offsets[t];
       v = (p.offsets[t + 1] - p.offsets[t] + kNRows - 1) / kNRows;
-      if (t + 1 < q) ntp1[c] = p.NTp[t + 1];
+      s0.get<c>() = p.S[t];
+      r0.get<c>() = p.R[t];
+      ntp0.get<c>() = p.NTp[t];
+      if (t + 1 < q) ntp1.get<c>() = p.NTp[t + 1];
     }
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const int32_t u = __shfl_up(v, d);
       if (lane >= d) v += u;
     }
-    incl[c] = n_blocks + v;
+    incl.get<c>() = n_blocks + v;
     n_blocks += __builtin_amdgcn_readlane(v, 63);
-  }
-  // the value lane (x mod 64) holds in chunk x / 64 of a table
-  auto pick = [&](const int32_t (&tab)[kCh], int x) -> int32_t {
-    const int c = x >> 6;
-    int32_t v = tab[0];
-#pragma unroll
-    for (int k = 1; k < kCh; ++k)
-      if (c == k) v = tab[k];
-    return __builtin_amdgcn_readlane(v, x & 63);
+  });
+  // entry x of a table (x < q), else `end`
+  auto pick = [&](const Ch4& tab, int x, int32_t end) -> int32_t {
+    if (x >= q) return end;
+    return tab.template entry<NCH>(x >> 6, x & 63);
   };
 
   // The tiles: (row block rb, column tile ct), the row blocks numbered type
@@ -251,22 +296,21 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
     const int32_t cl = within / bsz;
     const int32_t rb = rb0 + bi * band + (within - cl * bsz);
     const int32_t ct = ct0 + cl;
-    int i = 0;  // the type: the first whose running block count passes rb
-#pragma unroll
-    for (int c = kCh - 1; c >= 0; --c) {
-      const uint64_t m = __ballot(64 * c + lane < q && incl[c] > rb);
-      if (m) i = 64 * c + __builtin_ctzll(m);
-    }
-    const int32_t o_i = p.offsets[i], o_i1 = p.offsets[i + 1];
-    const int32_t blk = rb - (pick(incl, i) - (o_i1 - o_i + kNRows - 1) / kNRows);
+    int i = -1;  // the type: the first whose running block count passes rb
+    each_chunk<NCH>([&](auto C) {
+      constexpr int c = decltype(C)::value;
+      const uint64_t m = __ballot(64 * c + lane < q && incl.get<c>() > rb);
+      if (i < 0 && m) i = 64 * c + __builtin_ctzll(m);
+    });
+    const int32_t o_i = pick(off, i, off_end), o_i1 = pick(off, i + 1, off_end);
+    const int32_t blk = rb - (pick(incl, i, 0) - (o_i1 - o_i + kNRows - 1) / kNRows);
     t.pos0 = o_i + blk * kNRows;
     t.pend = min(o_i1, t.pos0 + kNRows);
     int j = 0;  // the output group: column tiles at or past the next groups' prefixes
-#pragma unroll
-    for (int c = 0; c < kCh; ++c) j += __popcll(__ballot(ct >= ntp1[c]));
-    t.cstart = p.R[j] + (ct - p.NTp[j]) * kNCols;
-    t.cend = min(p.R[j + 1], t.cstart + kNCols);
-    fwd_ranges(p, i, j, t.a0, t.l0, t.a1, t.l1);
+    each_chunk<NCH>([&](auto C) { j += __popcll(__ballot(ct >= ntp1.get<decltype(C)::value>())); });
+    t.cstart = pick(r0, j, p.N) + (ct - pick(ntp0, j, n_ct)) * kNCols;
+    t.cend = min(pick(r0, j + 1, p.N), t.cstart + kNCols);
+    fwd_ranges(p, [&](int x) { return pick(s0, x, p.K); }, i, j, t.a0, t.l0, t.a1, t.l1);
     t.nsteps = (t.l0 + t.l1 + kNK - 1) / kNK;
     return t;
   };
@@ -532,13 +576,13 @@ hipError_t launch_gemm_narrow(const NarrowParams& p, int32_t n_rb, int32_t n_ct,
   // on every XCD, no more than there are items per XCD
   const int64_t per_xcd = (items + 7) / 8;
   const int wg_per_xcd = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(per_xcd, 2 * std::max(cus, 8) / 8)));
-  static std::atomic<unsigned long long> set{0};
-  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(gemm_narrow_kernel), set, kNSmem);
+  static std::atomic<unsigned long long> set1{0}, set4{0};
+  auto kern = p.q <= 64 ? gemm_narrow_kernel<1> : gemm_narrow_kernel<4>;
+  hipError_t e = ensure_lds_limit(reinterpret_cast<const void*>(kern), p.q <= 64 ? set1 : set4, kNSmem);
   if (e != hipSuccess) return e;
   // bands of row blocks whose X rows take at most 2 MB (half an XCD's L2)
   const int32_t band = static_cast<int32_t>(std::max<int64_t>(1, (int64_t{2} << 20) / (int64_t{kNRows} * p.K * 2)));
-  hipLaunchKernelGGL(gemm_narrow_kernel, dim3(8 * wg_per_xcd), dim3(kNThreads), kNSmem, stream, p, n_ct, wg_per_xcd,
-                     band);
+  hipLaunchKernelGGL(kern, dim3(8 * wg_per_xcd), dim3(kNThreads), kNSmem, stream, p, n_ct, wg_per_xcd, band);
   return hipGetLastError();
 }
 
