@@ -16,7 +16,7 @@ _EXPORTS = (
     "star_workspace_bytes", "star_swiglu_fwd", "star_swiglu_bwd", "star_add", "star_swiglu_ffn_fwd",
     "star_swiglu_ffn_bwd", "star_decode_gated", "star_decode_status", "star_decode_noalloc",
     "AttnShape", "star_attn_fwd", "star_attn_decode", "star_attn_decode_workspace_bytes",
-    "star_set_fwd_tiles",
+    "star_set_fwd_tiles", "star_swiglu_merged_fwd", "star_swiglu_up_fwd_planned", "pack_gate_up",
 )
 
 __all__ = list(_EXPORTS)

@@ -83,6 +83,8 @@ def _load() -> ctypes.CDLL:
     lib.star_swiglu_fwd.argtypes = [i64, P, P, E, P, P]
     lib.star_swiglu_bwd.argtypes = [i64, P, P, P, E, P, P, P]
     lib.star_add.argtypes = [i64, P, P, E, P, P]
+    lib.star_swiglu_merged_fwd.argtypes = [i64, i64, P, E, P, P]
+    lib.star_swiglu_up_fwd_planned.argtypes = [A, i64, P, P, E, P, E, P, P, P, E, P]
     S = ctypes.POINTER(_CAttnShape)
     lib.star_attn_fwd.argtypes = [S, P, P, P, P, E, P, E, P, P]
     lib.star_attn_decode_workspace_bytes.argtypes = [S]
@@ -95,7 +97,7 @@ def _load() -> ctypes.CDLL:
                  "star_type_plan", "star_proj_fwd_planned", "star_proj_bwd_data_planned",
                  "star_proj_bwd_weight_planned", "star_swiglu_fwd", "star_swiglu_bwd", "star_add",
                  "star_decode_gated", "star_decode_status", "star_decode_noalloc", "star_attn_fwd",
-                 "star_attn_decode"):
+                 "star_attn_decode", "star_swiglu_merged_fwd", "star_swiglu_up_fwd_planned"):
         getattr(lib, name).restype = E
     return lib
 
@@ -151,6 +153,11 @@ class Algebra:
 
     def with_law(self, law: str) -> "Algebra":
         return Algebra(self.q, self.s, self.r, law, self.edges)
+
+    def merged_gate_up(self) -> "Algebra":
+        """The algebra of the merged gate/up product of this up layout:
+        output widths doubled (gate and up of each group side by side)."""
+        return Algebra(self.q, self.s, [2 * x for x in self.r], self.law, self.edges)
 
     def __repr__(self):
         return f"Algebra(q={self.q}, s={self.s}, r={self.r}, law={self.law!r})"
@@ -596,6 +603,63 @@ def star_swiglu_fwd(Z_gate: torch.Tensor, Z_up: torch.Tensor, H=None) -> torch.T
     _check(LIB.star_swiglu_fwd(Z_gate.numel(), _ptr(Z_gate), _ptr(Z_up), _dt(Z_gate), _ptr(H),
                                _stream(Z_gate.device)), "star_swiglu_fwd")
     return H
+
+
+def pack_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
+    """The merged gate/up layout of star_swiglu_up_fwd_planned: the last
+    dimension (F, a multiple of 32) of ``gate`` and ``up`` interleaved in
+    32-wide chunks (gate chunk c, then up chunk c).  A one-time layout
+    conversion of the weights W [D, F] or biases [F] (torch ops; not part of
+    the product)."""
+    if gate.shape != up.shape or gate.shape[-1] % 32:
+        raise ValueError("gate and up need the same shape, the last dimension a multiple of 32")
+    lead, F = tuple(gate.shape[:-1]), gate.shape[-1]
+    g = gate.reshape(*lead, F // 32, 1, 32)
+    u = up.reshape(*lead, F // 32, 1, 32)
+    return torch.cat((g, u), dim=-2).reshape(*lead, 2 * F).contiguous()
+
+
+def star_swiglu_merged_fwd(Z_gu: torch.Tensor, H=None) -> torch.Tensor:
+    """H [M, F] = silu(gate) . up from a merged gate/up output Z_gu [M, 2F]
+    (gate and up interleaved in 32-feature chunks; elementwise, on the GPU)."""
+    if Z_gu.dim() != 2 or Z_gu.shape[1] % 64:
+        raise ValueError("Z_gu must be [M, 2F] with F a multiple of 32")
+    M, F = Z_gu.shape[0], Z_gu.shape[1] // 2
+    _need(Z_gu, "Z_gu", (M, 2 * F), _FLOATS)
+    if H is None:
+        H = torch.empty((M, F), dtype=Z_gu.dtype, device=Z_gu.device)
+    _need(H, "H", (M, F), (Z_gu.dtype,), Z_gu.device)
+    _gpu(Z_gu.device)
+    _check(LIB.star_swiglu_merged_fwd(M, F, _ptr(Z_gu), _dt(Z_gu), _ptr(H), _stream(Z_gu.device)),
+           "star_swiglu_merged_fwd")
+    return H
+
+
+def star_swiglu_up_fwd_planned(alg_gu: Algebra, plan: torch.Tensor, X: torch.Tensor, W_gu: torch.Tensor,
+                               b_gu: torch.Tensor | None = None, Z_out=None, H=None, out_dtype=None):
+    """H = silu(Z_gate) . Z_up of the merged gate/up product X *_q W_gu
+    (+ b_gu), SwiGLU applied in the product's epilogue.  ``alg_gu`` is the
+    merged algebra (Algebra.merged_gate_up), W_gu and b_gu from pack_gate_up.
+    ``Z_out=True`` also returns the merged pre-activation [M, 2F].  Returns H,
+    or (H, Z)."""
+    M, dev = _rows(X, "X", alg_gu.K)
+    _need(W_gu, "W_gu", (alg_gu.K, alg_gu.N), (X.dtype,), dev)
+    _opt(b_gu, "b_gu", (alg_gu.N,), _F32, dev)
+    _need(plan, "plan", tuple(plan.shape), None, dev)
+    F = alg_gu.N // 2
+    if H is None:
+        H = torch.empty((M, F), dtype=out_dtype or X.dtype, device=dev)
+    _need(H, "H", (M, F), _FLOATS, dev)
+    want_z = Z_out is not None and Z_out is not False
+    if Z_out is True:
+        Z_out = torch.empty((M, alg_gu.N), dtype=H.dtype, device=dev)
+    if want_z:
+        _need(Z_out, "Z_out", (M, alg_gu.N), (H.dtype,), dev)
+    _gpu(dev)
+    _check(LIB.star_swiglu_up_fwd_planned(alg_gu.ref, M, _ptr(plan), _ptr(X), _dt(X), _ptr(W_gu), _dt(W_gu),
+                                          _ptr(b_gu), _ptr(Z_out) if want_z else None, _ptr(H), _dt(H),
+                                          _stream(dev)), "star_swiglu_up_fwd_planned")
+    return (H, Z_out) if want_z else H
 
 
 def star_swiglu_bwd(dH: torch.Tensor, Z_gate: torch.Tensor, Z_up: torch.Tensor):

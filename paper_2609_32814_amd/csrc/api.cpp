@@ -1056,6 +1056,60 @@ star_status star_swiglu_fwd(int64_t n, const void* Z_gate, const void* Z_up, sta
   return hip_status(launch_swiglu_fwd(n, dt == STAR_BF16 ? 1 : 0, Z_gate, Z_up, H, stream));
 }
 
+star_status star_swiglu_merged_fwd(int64_t M, int64_t F, const void* Z_gu, star_dtype dt, void* H,
+                                   hipStream_t stream) {
+  if (!valid_dtype(dt)) return STAR_ERR_DTYPE;
+  if (M < 0 || F < 0 || M > kMaxDim || F > kMaxDim) return STAR_ERR_SHAPE;
+  if (F % 32) return STAR_ERR_ALIGN;
+  if (M == 0 || F == 0) return STAR_OK;
+  if (!Z_gu || !H) return STAR_ERR_ARG;
+  if (!aligned16(Z_gu) || !aligned16(H)) return STAR_ERR_ALIGN;
+  return hip_status(launch_swiglu_merged(M, F, dt == STAR_BF16 ? 1 : 0, Z_gu, H, stream));
+}
+
+star_status star_swiglu_up_fwd_planned(const star_algebra* alg_gu, int64_t M, const void* plan, const void* X,
+                                       star_dtype xt, const void* W_gu, star_dtype wt, const float* b_gu,
+                                       void* Z_out, void* H, star_dtype ht, hipStream_t stream) {
+  Alg a;
+  star_status st = parse_alg(alg_gu, a, true);
+  if (st != STAR_OK) return st;
+  if (a.law == STAR_LAW_GRAPH) return STAR_ERR_UNSUPPORTED;
+  for (int g = 0; g < a.q; ++g)
+    if (a.r(g) % 64) return STAR_ERR_UNSUPPORTED;
+  if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
+  if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(ht) || xt != wt) return STAR_ERR_DTYPE;
+  if (xt != STAR_BF16) return STAR_ERR_UNSUPPORTED;
+  if (M == 0) return STAR_OK;
+  if (!plan || !X || !W_gu || !H) return STAR_ERR_ARG;
+  if (!aligned16(plan) || !aligned16(X) || !aligned16(W_gu) || !aligned16(H) || (Z_out && !aligned16(Z_out)) ||
+      (b_gu && !aligned16(b_gu)))
+    return STAR_ERR_ALIGN;
+  const PlanWs pw = plan_layout(M, a.q);
+  void* pl = const_cast<void*>(plan);
+  NarrowParams pn;
+  std::memset(&pn, 0, sizeof(pn));
+  pn.q = a.q;
+  pn.law = a.law;
+  pn.M = static_cast<int32_t>(M);
+  pn.K = static_cast<int32_t>(a.K());
+  pn.N = static_cast<int32_t>(a.N());
+  pn.act = STAR_ACT_NONE;
+  pn.ydtype = ht;
+  pn.swiglu = 1;
+  pn.perm = at<int32_t>(pl, pw.perm);
+  pn.offsets = at<int32_t>(pl, pw.offsets);
+  pn.A = X;
+  pn.B = W_gu;
+  pn.bias = b_gu;
+  pn.Z = Z_out;
+  pn.Y = H;
+  for (int g = 0; g <= a.q; ++g) {
+    pn.S[g] = static_cast<int32_t>(a.S[g]);
+    pn.R[g] = static_cast<int32_t>(a.R[g]);
+  }
+  return hip_status(launch_narrow(pn, stream));
+}
+
 star_status star_swiglu_bwd(int64_t n, const void* dH, const void* Z_gate, const void* Z_up, star_dtype dt,
                             void* dZ_gate, void* dZ_up, hipStream_t stream) {
   star_status st = check_elementwise(n, dt, {dH, Z_gate, Z_up, dZ_gate, dZ_up});

@@ -89,6 +89,12 @@ __device__ __forceinline__ float gelu_erf(float z) {
 
 // Tanh form 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))): error at most
 // 1e-6 + 2^-22 |value|.
+// The logistic function for SiLU (z sigma(z)): the hardware exp2 and
+// reciprocal, about 1 ulp each.  Every SwiGLU kernel uses this one.
+__device__ __forceinline__ float sigmoid_fast(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-z * 1.4426950408889634f));
+}
+
 __device__ __forceinline__ float act_apply(int act, float z) {
   if (act == kActGelu) return gelu_erf(z);
   if (act == kActGeluTanh) {

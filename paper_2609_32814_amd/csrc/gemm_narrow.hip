@@ -182,13 +182,14 @@ struct NTile {
 // in the output, `rok` whether it exists), columns 64 wc + 32 cb + 8 a +
 // 4 lh + 0..3 for cb < 2, a < 4.  Every lane stores all 8 blocks (and 8 of Z
 // when asked for): blocks without an element go to the lane's sink.
+// Y_out (with activation `act`) and Z_out (pre-activation) may be null.
 __device__ __forceinline__ void narrow_epilogue(const NarrowParams& p, const f32x16_t (&acc)[2], bool rok, int32_t row,
                                                 int32_t cstart, int32_t cend, int cl0, const float* bias_tile,
-                                                char* sink) {
+                                                char* sink, void* Y_out, void* Z_out, int act) {
   constexpr int esz = 4;
   const int64_t off = (static_cast<int64_t>(row) * p.N + cstart + cl0) * esz;
-  char* yb = rok ? static_cast<char*>(p.Y) + off : sink;
-  char* zb = p.Z ? (rok ? static_cast<char*>(p.Z) + off : sink) : nullptr;
+  char* yb = Y_out ? (rok ? static_cast<char*>(Y_out) + off : sink) : nullptr;
+  char* zb = Z_out ? (rok ? static_cast<char*>(Z_out) + off : sink) : nullptr;
   const bool full = cend - cstart == kNCols;
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb)
@@ -208,11 +209,11 @@ __device__ __forceinline__ void narrow_epilogue(const NarrowParams& p, const f32
         *reinterpret_cast<float4*>((cok ? base : sink) + bo) = make_float4(v[0], v[1], v[2], v[3]);
       };
       if (zb) put(zb);
-      if (p.act != kActNone) {
+      if (act != kActNone) {
 #pragma unroll
-        for (int x = 0; x < 4; ++x) v[x] = act_apply(p.act, v[x]);
+        for (int x = 0; x < 4; ++x) v[x] = act_apply(act, v[x]);
       }
-      put(yb);
+      if (yb) put(yb);
     }
 }
 
@@ -460,7 +461,9 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
   // the scheduler's copies of the last one (issued after the copies of this
   // iteration's element); per tile each lane stores 4 chunks of 16 bytes of
   // a bf16 output, 8 blocks of an fp32 one, and as many again of Z
-  const int n_st = (p.ydtype == 0 ? 8 : 4) * (p.Z ? 2 : 1);
+  // (SwiGLU: half as many of H, plus those of Z when asked for)
+  const int n_st = p.swiglu ? (p.ydtype == 0 ? 4 + (p.Z ? 8 : 0) : 2 + (p.Z ? 4 : 0))
+                            : (p.ydtype == 0 ? 8 : 4) * (p.Z ? 2 : 1);
   int st1 = 0, st2 = 0, sd1 = 0;
   for (int32_t e = 0; c_nsteps > 0; ++e) {
     // Memory operations complete in order for the counter: element e's
@@ -512,7 +515,8 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
       const int32_t row = rows_s[c_n % kSlots][r];
       const float* bt = bias_s[c_n % kSlots];
       if (p.ydtype == 0) {
-        narrow_epilogue(p, acc, rok, row, c_cstart, c_cend, 64 * wc + 4 * lh, bt, sink);
+        if (!p.swiglu) narrow_epilogue(p, acc, rok, row, c_cstart, c_cend, 64 * wc + 4 * lh, bt, sink, p.Y, p.Z, p.act);
+        else if (p.Z) narrow_epilogue(p, acc, rok, row, c_cstart, c_cend, 64 * wc + 4 * lh, bt, sink, nullptr, p.Z, 0);
       } else {
         // bf16 through LDS, in the stage this iteration consumed (free until
         // the next iteration's copies): the 64 x 128 values go in with row r
@@ -552,7 +556,55 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
           }
         };
         if (p.Z) pass(p.Z, false);
-        pass(p.Y, p.act != kActNone);
+        if (!p.swiglu) pass(p.Y, p.act != kActNone);
+      }
+      if (p.swiglu) {
+        // H = silu(gate) . up: the wave's columns 64 wc + [0, 32) are gate
+        // values (cb = 0) and 64 wc + [32, 64) the up values of the same
+        // features (cb = 1); H feature 32 wc + 8 a + 4 lh + x of the tile,
+        // column c_cstart / 2 + that of H [M, N / 2]
+        float h[4][4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            const int cl = 64 * wc + 8 * a + 4 * lh + x;
+            float g = acc[0][4 * a + x], u = acc[1][4 * a + x];
+            if (p.bias) {
+              g += bt[cl];
+              u += bt[cl + 32];
+            }
+            h[a][x] = g * sigmoid_fast(g) * u;
+          }
+        const int32_t hn = p.N / 2, hw = (c_cend - c_cstart) / 2;  // H row width, the tile's H columns
+        if (p.ydtype == 0) {  // fp32: from the registers
+          const int64_t off = (static_cast<int64_t>(row) * hn + c_cstart / 2 + 32 * wc + 4 * lh) * 4;
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const bool ok = rok && 32 * wc + 8 * a + 4 * lh < hw;
+            *reinterpret_cast<float4*>((ok ? static_cast<char*>(p.Y) + off : sink) + 32 * a) =
+                make_float4(h[a][0], h[a][1], h[a][2], h[a][3]);
+          }
+        } else {  // bf16: 64 rows x 64 features through LDS, 16-byte chunks of whole rows
+          char* T = smem + (e % kNStages) * kStage;
+          const int32_t* rows = rows_s[c_n % kSlots];
+          __syncthreads();  // every wave is done reading the stage (or the Z pass)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const int fl = 32 * wc + 8 * a + 4 * lh;
+            *reinterpret_cast<uint2*>(T + r * 128 + (((fl >> 3) ^ (r & 7)) << 4) + ((fl >> 2) & 1) * 8) =
+                make_uint2(pack_bf16(h[a][0], h[a][1]), pack_bf16(h[a][2], h[a][3]));
+          }
+          __syncthreads();
+#pragma unroll
+          for (int it = 0; it < 2; ++it) {
+            const int id = threadIdx.x + kNThreads * it, tr = id >> 3, c = id & 7;
+            const uint4 val = *reinterpret_cast<const uint4*>(T + tr * 128 + ((c ^ (tr & 7)) << 4));
+            const bool ok = tr < c_nrows && 8 * c < hw;
+            const int64_t off = (static_cast<int64_t>(rows[tr]) * hn + c_cstart / 2 + 8 * c) * 2;
+            *reinterpret_cast<uint4*>(ok ? static_cast<char*>(p.Y) + off : sink + 16 * it) = val;
+          }
+        }
       }
       st1 = n_st;
     }

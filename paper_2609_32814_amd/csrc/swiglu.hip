@@ -1,7 +1,8 @@
 // Elementwise parts of a gated (SwiGLU) FFN, whose three projections run
 // through the row-typed GEMM: H = silu(Z_g) . Z_u forward, and backward
 // dZ_g = dH . Z_u . silu'(Z_g), dZ_u = dH . silu(Z_g); plus the sum of the
-// two activation gradients dX = dX_g + dX_u.  SiLU is z sigma(z) with the
+// two activation gradients dX = dX_g + dX_u; and the forward from a merged
+// gate/up projection's output (gate and up interleaved in 32-feature chunks).  SiLU is z sigma(z) with the
 // logistic sigma from the hardware exp2 and reciprocal (about 1 ulp each),
 // and sigma'(z) = sigma (1 - sigma).  Every kernel streams 16 bytes per
 // thread per operand: HBM-bound, a grid-stride loop over n / 8 (bf16) or
@@ -12,12 +13,6 @@
 namespace starq {
 
 namespace {
-
-constexpr float kLog2eF = 1.4426950408889634f;
-
-__device__ __forceinline__ float sigmoid_fast(float z) {
-  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-z * kLog2eF));
-}
 
 template <typename T> struct Vec;
 template <> struct Vec<uint16_t> {
@@ -59,6 +54,28 @@ __global__ __launch_bounds__(256) void swiglu_fwd_kernel(int64_t nv, const void*
     float g[N], u[N], o[N];
     Vec<T>::load(zg, v, g);
     Vec<T>::load(zu, v, u);
+#pragma unroll
+    for (int i = 0; i < N; ++i) o[i] = g[i] * sigmoid_fast(g[i]) * u[i];
+    Vec<T>::store(h, v, o);
+  }
+}
+
+// Gate and up interleaved in 32-feature chunks (the merged projection's
+// layout): feature f's gate at column 64 (f / 32) + f % 32 of a 2F-wide row,
+// its up value 32 columns on.  Vector v covers features 8 v .. 8 v + 7 of the
+// flattened [M, F] output (F a multiple of 32, so a vector never leaves its
+// chunk).
+template <typename T>
+__global__ __launch_bounds__(256) void swiglu_merged_kernel(int64_t nv, int64_t F, const void* __restrict__ zgu,
+                                                            void* __restrict__ h) {
+  constexpr int N = Vec<T>::N;
+  for (int64_t v = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; v < nv;
+       v += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t e = v * N, row = e / F, f = e - row * F;
+    const int64_t g_el = row * 2 * F + 64 * (f / 32) + f % 32;  // element index of the gate values
+    float g[N], u[N], o[N];
+    Vec<T>::load(zgu, g_el / N, g);
+    Vec<T>::load(zgu, (g_el + 32) / N, u);
 #pragma unroll
     for (int i = 0; i < N; ++i) o[i] = g[i] * sigmoid_fast(g[i]) * u[i];
     Vec<T>::store(h, v, o);
@@ -117,6 +134,18 @@ hipError_t launch_swiglu_fwd(int64_t n, int elem, const void* zg, const void* zu
   } else {
     const int64_t nv = n / 4;
     hipLaunchKernelGGL(swiglu_fwd_kernel<float>, dim3(blocks_for(nv)), dim3(256), 0, stream, nv, zg, zu, h);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_merged(int64_t M, int64_t F, int elem, const void* zgu, void* h, hipStream_t stream) {
+  const int64_t n = M * F;
+  if (elem == 1) {
+    const int64_t nv = n / 8;
+    hipLaunchKernelGGL(swiglu_merged_kernel<uint16_t>, dim3(blocks_for(nv)), dim3(256), 0, stream, nv, F, zgu, h);
+  } else {
+    const int64_t nv = n / 4;
+    hipLaunchKernelGGL(swiglu_merged_kernel<float>, dim3(blocks_for(nv)), dim3(256), 0, stream, nv, F, zgu, h);
   }
   return hipGetLastError();
 }
