@@ -408,14 +408,14 @@ star_status star_add(int64_t n, const void *a, const void *b, star_dtype dt, voi
  * Merged gate/up (§"Kernel Benchmark Details": the SwiGLU comparison merges
  * the gate and up projections on both sides; Tab. kernel-ffn).  The two
  * D x F maps share the row types and the input, so they run as one D x 2F
- * product whose output columns hold gate and up interleaved in 32-feature
- * chunks: feature f's gate at column 64 (f / 32) + f % 32, its up value 32
- * columns on.  With the output groups of the up layout r_j (multiples of
- * 32), the merged algebra has output widths 2 r_j and the same law; its
- * weight bank W_gu [D, 2F] and bias b_gu [2F] are W_gate, W_up (and
- * b_gate, b_up) interleaved the same way.
+ * product whose output columns hold gate and up interleaved in 8-feature
+ * chunks: feature f's gate at column 16 (f / 8) + f % 8, its up value 8
+ * columns on.  With the output groups of the up layout r_j (multiples of 8),
+ * the merged algebra has output widths 2 r_j and the same law; its weight
+ * bank W_gu [D, 2F] and bias b_gu [2F] are W_gate, W_up (and b_gate, b_up)
+ * interleaved the same way.
  *   star_swiglu_merged_fwd: H [M, F] = silu(gate) . up from the merged
- *       product's output Z_gu [M, 2F] (dtype dt; F a multiple of 32; every
+ *       product's output Z_gu [M, 2F] (dtype dt; F a multiple of 8; every
  *       buffer device memory, 16-byte aligned).
  *   star_swiglu_up_fwd_planned: the merged product with SwiGLU applied in
  *       its epilogue: H [M, F] (dtype ht) = silu(Z_gate) . Z_up, Z from the
@@ -423,7 +423,7 @@ star_status star_add(int64_t n, const void *a, const void *b, star_dtype dt, voi
  *       (the merged pre-activation [M, 2F], dtype ht) is given.  bf16 X and
  *       W_gu; plan from star_type_plan; q up to STAR_MAX_Q_FWD; the star,
  *       dense and tensor laws (STAR_ERR_UNSUPPORTED for the graph law or an
- *       output width not a multiple of 64).
+ *       output width not a multiple of 16).
  */
 star_status star_swiglu_merged_fwd(int64_t M, int64_t F, const void *Z_gu, star_dtype dt, void *H,
                                    hipStream_t stream);

@@ -607,23 +607,23 @@ def star_swiglu_fwd(Z_gate: torch.Tensor, Z_up: torch.Tensor, H=None) -> torch.T
 
 def pack_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
     """The merged gate/up layout of star_swiglu_up_fwd_planned: the last
-    dimension (F, a multiple of 32) of ``gate`` and ``up`` interleaved in
-    32-wide chunks (gate chunk c, then up chunk c).  A one-time layout
+    dimension (F, a multiple of 8) of ``gate`` and ``up`` interleaved in
+    8-wide chunks (gate chunk c, then up chunk c).  A one-time layout
     conversion of the weights W [D, F] or biases [F] (torch ops; not part of
     the product)."""
-    if gate.shape != up.shape or gate.shape[-1] % 32:
-        raise ValueError("gate and up need the same shape, the last dimension a multiple of 32")
+    if gate.shape != up.shape or gate.shape[-1] % 8:
+        raise ValueError("gate and up need the same shape, the last dimension a multiple of 8")
     lead, F = tuple(gate.shape[:-1]), gate.shape[-1]
-    g = gate.reshape(*lead, F // 32, 1, 32)
-    u = up.reshape(*lead, F // 32, 1, 32)
+    g = gate.reshape(*lead, F // 8, 1, 8)
+    u = up.reshape(*lead, F // 8, 1, 8)
     return torch.cat((g, u), dim=-2).reshape(*lead, 2 * F).contiguous()
 
 
 def star_swiglu_merged_fwd(Z_gu: torch.Tensor, H=None) -> torch.Tensor:
     """H [M, F] = silu(gate) . up from a merged gate/up output Z_gu [M, 2F]
-    (gate and up interleaved in 32-feature chunks; elementwise, on the GPU)."""
-    if Z_gu.dim() != 2 or Z_gu.shape[1] % 64:
-        raise ValueError("Z_gu must be [M, 2F] with F a multiple of 32")
+    (gate and up interleaved in 8-feature chunks; elementwise, on the GPU)."""
+    if Z_gu.dim() != 2 or Z_gu.shape[1] % 16:
+        raise ValueError("Z_gu must be [M, 2F] with F a multiple of 8")
     M, F = Z_gu.shape[0], Z_gu.shape[1] // 2
     _need(Z_gu, "Z_gu", (M, 2 * F), _FLOATS)
     if H is None:

@@ -1060,7 +1060,7 @@ star_status star_swiglu_merged_fwd(int64_t M, int64_t F, const void* Z_gu, star_
                                    hipStream_t stream) {
   if (!valid_dtype(dt)) return STAR_ERR_DTYPE;
   if (M < 0 || F < 0 || M > kMaxDim || F > kMaxDim) return STAR_ERR_SHAPE;
-  if (F % 32) return STAR_ERR_ALIGN;
+  if (F % 8) return STAR_ERR_ALIGN;
   if (M == 0 || F == 0) return STAR_OK;
   if (!Z_gu || !H) return STAR_ERR_ARG;
   if (!aligned16(Z_gu) || !aligned16(H)) return STAR_ERR_ALIGN;
@@ -1075,7 +1075,7 @@ star_status star_swiglu_up_fwd_planned(const star_algebra* alg_gu, int64_t M, co
   if (st != STAR_OK) return st;
   if (a.law == STAR_LAW_GRAPH) return STAR_ERR_UNSUPPORTED;
   for (int g = 0; g < a.q; ++g)
-    if (a.r(g) % 64) return STAR_ERR_UNSUPPORTED;
+    if (a.r(g) % 16) return STAR_ERR_UNSUPPORTED;
   if (M < 0 || M > kMaxDim) return STAR_ERR_SHAPE;
   if (!valid_dtype(xt) || !valid_dtype(wt) || !valid_dtype(ht) || xt != wt) return STAR_ERR_DTYPE;
   if (xt != STAR_BF16) return STAR_ERR_UNSUPPORTED;

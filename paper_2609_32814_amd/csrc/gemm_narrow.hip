@@ -559,41 +559,44 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const NarrowPara
         if (!p.swiglu) pass(p.Y, p.act != kActNone);
       }
       if (p.swiglu) {
-        // H = silu(gate) . up: the wave's columns 64 wc + [0, 32) are gate
-        // values (cb = 0) and 64 wc + [32, 64) the up values of the same
-        // features (cb = 1); H feature 32 wc + 8 a + 4 lh + x of the tile,
-        // column c_cstart / 2 + that of H [M, N / 2]
-        float h[4][4];
+        // H = silu(gate) . up: columns alternate 8 gate, 8 up, so the
+        // lane's block a = 2 pp holds gate values and a = 2 pp + 1 the up
+        // values of the same features: H feature
+        // 32 wc + 16 cb + 8 pp + 4 lh + x of the tile, column c_cstart / 2 +
+        // that of H [M, N / 2]
+        float h[4][4];  // [2 cb + pp][x]
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+        for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-          for (int x = 0; x < 4; ++x) {
-            const int cl = 64 * wc + 8 * a + 4 * lh + x;
-            float g = acc[0][4 * a + x], u = acc[1][4 * a + x];
-            if (p.bias) {
-              g += bt[cl];
-              u += bt[cl + 32];
+          for (int pp2 = 0; pp2 < 2; ++pp2)
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+              const int cl = 64 * wc + 32 * cb + 16 * pp2 + 4 * lh + x;
+              float g = acc[cb][8 * pp2 + x], u = acc[cb][8 * pp2 + 4 + x];
+              if (p.bias) {
+                g += bt[cl];
+                u += bt[cl + 8];
+              }
+              h[2 * cb + pp2][x] = g * sigmoid_fast(g) * u;
             }
-            h[a][x] = g * sigmoid_fast(g) * u;
-          }
         const int32_t hn = p.N / 2, hw = (c_cend - c_cstart) / 2;  // H row width, the tile's H columns
         if (p.ydtype == 0) {  // fp32: from the registers
           const int64_t off = (static_cast<int64_t>(row) * hn + c_cstart / 2 + 32 * wc + 4 * lh) * 4;
 #pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            const bool ok = rok && 32 * wc + 8 * a + 4 * lh < hw;
-            *reinterpret_cast<float4*>((ok ? static_cast<char*>(p.Y) + off : sink) + 32 * a) =
-                make_float4(h[a][0], h[a][1], h[a][2], h[a][3]);
+          for (int b = 0; b < 4; ++b) {  // feature 32 wc + 8 b + 4 lh + 0..3
+            const bool ok = rok && 32 * wc + 8 * b + 4 * lh < hw;
+            *reinterpret_cast<float4*>((ok ? static_cast<char*>(p.Y) + off : sink) + 32 * b) =
+                make_float4(h[b][0], h[b][1], h[b][2], h[b][3]);
           }
         } else {  // bf16: 64 rows x 64 features through LDS, 16-byte chunks of whole rows
           char* T = smem + (e % kNStages) * kStage;
           const int32_t* rows = rows_s[c_n % kSlots];
           __syncthreads();  // every wave is done reading the stage (or the Z pass)
 #pragma unroll
-          for (int a = 0; a < 4; ++a) {
-            const int fl = 32 * wc + 8 * a + 4 * lh;
+          for (int b = 0; b < 4; ++b) {
+            const int fl = 32 * wc + 8 * b + 4 * lh;
             *reinterpret_cast<uint2*>(T + r * 128 + (((fl >> 3) ^ (r & 7)) << 4) + ((fl >> 2) & 1) * 8) =
-                make_uint2(pack_bf16(h[a][0], h[a][1]), pack_bf16(h[a][2], h[a][3]));
+                make_uint2(pack_bf16(h[b][0], h[b][1]), pack_bf16(h[b][2], h[b][3]));
           }
           __syncthreads();
 #pragma unroll

@@ -100,7 +100,7 @@ struct NarrowParams {
   int32_t act;
   int32_t ydtype;
   int32_t swiglu;  // 1: Y is H [M, N / 2] = silu(gate) . up, the N columns gate and up
-                   // interleaved in 32-column chunks (Z, if given, the N columns)
+                   // interleaved in 8-column chunks (Z, if given, the N columns)
   const int32_t* perm;
   const int32_t* offsets;
   const void* A;  // X [M, K] bf16
@@ -117,7 +117,7 @@ hipError_t launch_gemm_narrow(const NarrowParams& p, int32_t n_rb, int32_t n_ct,
 // Gated FFN elementwise parts (swiglu.hip); n a multiple of 8, elem 1 bf16
 // or 0 fp32, 16-byte aligned buffers.
 hipError_t launch_swiglu_fwd(int64_t n, int elem, const void* zg, const void* zu, void* h, hipStream_t stream);
-// H [M, F] from Z [M, 2F] with gate and up interleaved in 32-feature chunks
+// H [M, F] from Z [M, 2F] with gate and up interleaved in 8-feature chunks
 hipError_t launch_swiglu_merged(int64_t M, int64_t F, int elem, const void* zgu, void* h, hipStream_t stream);
 hipError_t launch_swiglu_bwd(int64_t n, int elem, const void* dh, const void* zg, const void* zu, void* dzg,
                              void* dzu, hipStream_t stream);

@@ -2,7 +2,7 @@
 // through the row-typed GEMM: H = silu(Z_g) . Z_u forward, and backward
 // dZ_g = dH . Z_u . silu'(Z_g), dZ_u = dH . silu(Z_g); plus the sum of the
 // two activation gradients dX = dX_g + dX_u; and the forward from a merged
-// gate/up projection's output (gate and up interleaved in 32-feature chunks).  SiLU is z sigma(z) with the
+// gate/up projection's output (gate and up interleaved in 8-feature chunks).  SiLU is z sigma(z) with the
 // logistic sigma from the hardware exp2 and reciprocal (about 1 ulp each),
 // and sigma'(z) = sigma (1 - sigma).  Every kernel streams 16 bytes per
 // thread per operand: HBM-bound, a grid-stride loop over n / 8 (bf16) or
@@ -60,11 +60,11 @@ __global__ __launch_bounds__(256) void swiglu_fwd_kernel(int64_t nv, const void*
   }
 }
 
-// Gate and up interleaved in 32-feature chunks (the merged projection's
-// layout): feature f's gate at column 64 (f / 32) + f % 32 of a 2F-wide row,
-// its up value 32 columns on.  Vector v covers features 8 v .. 8 v + 7 of the
-// flattened [M, F] output (F a multiple of 32, so a vector never leaves its
-// chunk).
+// Gate and up interleaved in 8-feature chunks (the merged projection's
+// layout): feature f's gate at column 16 (f / 8) + f % 8 of a 2F-wide row,
+// its up value 8 columns on.  Vector v covers features N v .. N v + N - 1 of
+// the flattened [M, F] output (N = 8 bf16 or 4 fp32; F a multiple of 8, so a
+// vector never leaves its chunk).
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_merged_kernel(int64_t nv, int64_t F, const void* __restrict__ zgu,
                                                             void* __restrict__ h) {
@@ -72,10 +72,10 @@ __global__ __launch_bounds__(256) void swiglu_merged_kernel(int64_t nv, int64_t 
   for (int64_t v = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; v < nv;
        v += static_cast<int64_t>(gridDim.x) * blockDim.x) {
     const int64_t e = v * N, row = e / F, f = e - row * F;
-    const int64_t g_el = row * 2 * F + 64 * (f / 32) + f % 32;  // element index of the gate values
+    const int64_t g_el = row * 2 * F + 16 * (f / 8) + f % 8;  // element index of the gate values
     float g[N], u[N], o[N];
     Vec<T>::load(zgu, g_el / N, g);
-    Vec<T>::load(zgu, (g_el + 32) / N, u);
+    Vec<T>::load(zgu, (g_el + 8) / N, u);
 #pragma unroll
     for (int i = 0; i < N; ++i) o[i] = g[i] * sigmoid_fast(g[i]) * u[i];
     Vec<T>::store(h, v, o);

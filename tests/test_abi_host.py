@@ -51,18 +51,18 @@ def test_set_fwd_tiles(P):
 
 
 def test_pack_gate_up_layout(P):
-    """Gate and up interleaved in 32-wide chunks of the last axis (CPU)."""
+    """Gate and up interleaved in 8-wide chunks of the last axis (CPU)."""
     import torch
     g = torch.arange(3 * 96, dtype=torch.float32).reshape(3, 96)
     u = -g - 1
     m = P.pack_gate_up(g, u)
     assert m.shape == (3, 192)
-    for c in range(3):
-        assert torch.equal(m[:, 64 * c:64 * c + 32], g[:, 32 * c:32 * c + 32])
-        assert torch.equal(m[:, 64 * c + 32:64 * c + 64], u[:, 32 * c:32 * c + 32])
+    for c in range(12):
+        assert torch.equal(m[:, 16 * c:16 * c + 8], g[:, 8 * c:8 * c + 8])
+        assert torch.equal(m[:, 16 * c + 8:16 * c + 16], u[:, 8 * c:8 * c + 8])
     assert torch.equal(P.pack_gate_up(g[0], u[0]), m[0])
     with pytest.raises(ValueError):
-        P.pack_gate_up(g[:, :40], u[:, :40])
+        P.pack_gate_up(g[:, :44], u[:, :44])
 
 
 def test_swiglu_merged_argument_errors(P):
@@ -77,11 +77,11 @@ def test_swiglu_merged_argument_errors(P):
         return L.star_swiglu_up_fwd_planned(alg.ref, 4, V(16), V(16), xt, V(16), xt, None, None, V(16), ht, None)
 
     good = B.Algebra.equal(2, 64, 128).merged_gate_up()
-    assert fused(B.Algebra(2, [64, 64], [96, 64])) == err["STAR_ERR_UNSUPPORTED"]  # merged width not 64k
+    assert fused(B.Algebra(2, [64, 64], [88, 64])) == err["STAR_ERR_UNSUPPORTED"]  # merged width not 16k
     assert fused(good, xt=0) == err["STAR_ERR_UNSUPPORTED"]                        # fp32 operands
     E = np.array([[0, 1], [0, 0]], np.uint8)
     assert fused(B.Algebra(2, [64, 64], [128, 128], "graph", E)) == err["STAR_ERR_UNSUPPORTED"]
-    assert L.star_swiglu_merged_fwd(4, 40, V(16), 1, V(16), None) == err["STAR_ERR_ALIGN"]  # F not 32k
+    assert L.star_swiglu_merged_fwd(4, 44, V(16), 1, V(16), None) == err["STAR_ERR_ALIGN"]  # F not 8k
     assert L.star_swiglu_merged_fwd(4, 64, V(16), 7, V(16), None) == err["STAR_ERR_DTYPE"]
     assert L.star_swiglu_merged_fwd(4, 64, None, 1, V(16), None) == err["STAR_ERR_ARG"]
     assert L.star_swiglu_merged_fwd(0, 64, None, 1, None, None) == 0                       # M = 0: no-op
