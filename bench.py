@@ -83,6 +83,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--products-only", action="store_true",
                     help="only the kernel-products section (the paper's projection shapes)")
+    ap.add_argument("--ffn-only", action="store_true",
+                    help="only the complete SwiGLU FFN section (the paper's merged gate/up comparison)")
     ap.add_argument("--products-shape", default=None,
                     help="kernel products: only the named shape (e.g. Qwen3-8B)")
     ap.add_argument("--products-fixed", action="store_true",
@@ -113,9 +115,12 @@ class Protocol:
 
     def _run(self, fn, reps, flushed):
         torch = self.torch
-        if flushed:
-            self.flush()
         torch.cuda.synchronize()
+        if flushed:
+            # the flush runs before the first event in stream order, and the
+            # host queues the timed work while it runs, so the timed
+            # interval holds the work alone (not its launch latency)
+            self.flush()
         e0, e1 = self.ev(), self.ev()
         e0.record()
         for _ in range(reps):
@@ -237,6 +242,9 @@ def main():
     T = Protocol(torch, flush, args.trials)
     if args.attention_only:
         print(json.dumps({"attention": bench_attention(P, synth, torch, np, dev, T, flush, args)}), flush=True)
+        return
+    if args.ffn_only:
+        print(json.dumps({"kernel_ffn": bench_kernel_ffn(P, synth, torch, np, dev, T, flush, args)}), flush=True)
         return
     if args.products_only:
         print(json.dumps({"kernel_products": bench_kernel_products(P, synth, torch, np, dev, T, flush, args)}),
@@ -373,6 +381,8 @@ def main():
         result["attention"] = bench_attention(P, synth, torch, np, dev, T, flush, args)
         log("kernel products (calibrated q and tile against hipBLASLt):")
         result["kernel_products"] = bench_kernel_products(P, synth, torch, np, dev, T, flush, args)
+        log("kernel FFN (merged gate/up SwiGLU, q = 32, against hipBLASLt):")
+        result["kernel_ffn"] = bench_kernel_ffn(P, synth, torch, np, dev, T, flush, args)
 
     # ---- CPU oracle baseline -------------------------------------------------
     if not args.no_cpu:
@@ -806,7 +816,17 @@ KERNEL_PRODUCT_SHAPES = [
     ("Qwen3-32B M8192", 8192, 5120, 25600, {"q": 128, "dense_us": 3337.4, "q_us": 400.7, "speedup": [8.33, 8.60]}),
     ("Qwen3-32B M32768", 32768, 5120, 25600,
      {"q": 256, "dense_us": 13458.6, "q_us": 1169.4, "speedup": [11.51, 11.70]}),
+    # one row (Tab. kernel-products-fixed: q fixed at 32)
+    ("Qwen3-1.7B M1", 1, 2048, 6144, {"q": 32, "fixed": True, "dense_us": 9.5, "q_us": 3.8, "speedup": [2.51, 1.89]}),
+    ("Qwen3-4B M1", 1, 2560, 9728, {"q": 32, "fixed": True, "dense_us": 14.0, "q_us": 4.1, "speedup": [3.43, 2.72]}),
+    ("Qwen3-8B M1", 1, 4096, 12288, {"q": 32, "fixed": True, "dense_us": 30.7, "q_us": 4.4, "speedup": [7.07, 4.14]}),
+    ("Qwen3-30B-A3B expert M1", 1, 2048, 768,
+     {"q": 32, "fixed": True, "dense_us": 6.5, "q_us": 3.3, "speedup": [2.00, 1.36]}),
+    ("DeepSeek-V3 expert M1", 1, 7168, 2048, {"q": 32, "fixed": True, "dense_us": 10.9, "q_us": 3.8, "speedup": [2.87, 2.20]}),
 ]
+
+
+kGraphCalls = 10
 
 
 def group_widths(total, q):
@@ -844,13 +864,14 @@ def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
         dense = lambda: torch.matmul(X, W, out=Y)
         grid = {}
         best = None
-        for q in ((paper["q"],) if args.products_fixed else (4, 8, 16, 32, 64, 128, 256)):
+        fixed = args.products_fixed or paper.get("fixed", False)
+        for q in ((paper["q"],) if fixed else (4, 8, 16, 32, 64, 128, 256)):
             sw, rw = group_widths(D, q), group_widths(F, q)
             if sw is None or rw is None:
                 continue
             alg = P.Algebra(q, sw, rw)
             plan = P.star_type_plan(q, torch.from_numpy(synth.cyclic_types(M, q)).to(dev))
-            sizes = ("auto",) if args.products_fixed else (("wide", "small") if q <= 64 else ("small",))
+            sizes = ("auto",) if fixed else (("wide", "small") if q <= 64 else ("small",))
             for tiles in sizes:
                 P.star_set_fwd_tiles(tiles)
                 fn = lambda a=alg, pl=plan: P.star_proj_fwd_planned(a, pl, X, W, Y=Y)
@@ -860,18 +881,39 @@ def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
                     best = (ms, q, tiles, alg, plan)
         P.star_set_fwd_tiles("auto")
         _, q, tiles, alg, plan = best
+        # The protocol on HIP graph replays (the paper replays CUDA graphs):
+        # warm trials replay a graph of kGraphCalls back-to-back products
+        # (per-product time = replay / kGraphCalls, so the launch cost of
+        # one replay is spread), flushed trials a graph of one product.
+        star = lambda: P.star_proj_fwd_planned(alg, plan, X, W, Y=Y)
         P.star_set_fwd_tiles(tiles)
         try:
-            r = T.compare({"dense": dense, "star": lambda: P.star_proj_fwd_planned(alg, plan, X, W, Y=Y)})
+            graphs = {}
+            for method, fn in (("dense", dense), ("star", star)):
+                many = lambda fn=fn: [fn() for _ in range(kGraphCalls)]
+                graphs[method] = (graphed(torch, many), graphed(torch, fn))
+            warm = T.compare({n: g[0][0] for n, g in graphs.items()}, flushed=False)
+            cold = T.compare({n: g[1][0] for n, g in graphs.items()}, warm=False)
         finally:
             P.star_set_fwd_tiles("auto")
-        d_ms, s_ms = r["dense"]["warm_ms"], r["star"]["warm_ms"]
-        d_f, s_f = r["dense"]["flushed_ms"], r["star"]["flushed_ms"]
-        rows = [M // q] * q
+        del graphs
+        d_ms, s_ms = warm["dense"]["warm_ms"] / kGraphCalls, warm["star"]["warm_ms"] / kGraphCalls
+        d_f, s_f = cold["dense"]["flushed_ms"], cold["star"]["flushed_ms"]
+        rows = np.bincount(synth.cyclic_types(M, q), minlength=q)
         macs = P.star_count_macs(alg, rows)
-        byts = 2 * (M * D + D * F + M * F)
+        # algorithmic bytes: X, Y and the weight blocks some present type
+        # reads (all of them once every type is present; at M = 1 the
+        # row's own input group against every output group plus the diagonal)
+        present = sorted(set(int(v) for v in synth.cyclic_types(M, q)))
+        if len(present) == q:
+            wbytes = 2 * D * F
+        else:
+            sw, rw = group_widths(D, q), group_widths(F, q)
+            blocks = {(k, j) for i in present for j in range(q) for k in {i, j}}
+            wbytes = 2 * sum(sw[k] * rw[j] for k, j in blocks)
+        byts = 2 * (M * D + M * F) + wbytes
         out[name] = {
-            "M": M, "D": D, "F": F, "q_star": q, "tiles": tiles, "block": [M // q, D / q, F / q],
+            "M": M, "D": D, "F": F, "q_star": q, "tiles": tiles, "block": [M / q, D / q, F / q],
             "dense_us": round(d_ms * 1e3, 1), "q_us": round(s_ms * 1e3, 1),
             "dense_us_flushed": round(d_f * 1e3, 1), "q_us_flushed": round(s_f * 1e3, 1),
             "speedup": [round(d_ms / s_ms, 2), round(d_f / s_f, 2)],
@@ -885,6 +927,89 @@ def bench_kernel_products(P, synth, torch, np, dev, T, flush, args):
             f"(flushed {s_f*1e3:.1f} vs {d_f*1e3:.1f}); speedup {d_ms/s_ms:.2f} / {d_f/s_f:.2f}")
         del X, W, Y
         torch.cuda.empty_cache()
+    return out
+
+
+# The paper's complete SwiGLU forward at q = 32 (§"Kernel Benchmark
+# Details", Tab. kernel-ffn): D -> 2F merged gate/up, SwiGLU, F -> D, at
+# M = 1 and 2048; its figures (H200 NVL: dense us, algebraic us, warm /
+# flushed speedups) are context from other hardware.
+KERNEL_FFN_SHAPES = [
+    ("Qwen3-1.7B", 2048, 6144, {1: [30.2, 8.7, 3.45, 2.46], 2048: [273.7, 107.4, 2.55, 2.45]}),
+    ("Qwen3-4B", 2560, 9728, {1: [49.1, 10.4, 4.74, 3.21], 2048: [539.3, 193.8, 2.78, 2.68]}),
+    ("Qwen3-8B", 4096, 12288, {1: [83.6, 12.6, 6.64, 4.12], 2048: [1031.9, 247.3, 4.17, 3.92]}),
+    ("Qwen3-30B-A3B expert", 2048, 768, {1: [11.5, 6.7, 1.71, 1.42], 2048: [40.3, 23.2, 1.74, 1.54]}),
+    ("DeepSeek-V3 expert", 7168, 2048, {1: [33.4, 8.5, 3.94, 2.75], 2048: [304.2, 81.3, 3.74, 3.40]}),
+]
+
+
+def bench_kernel_ffn(P, synth, torch, np, dev, T, flush, args):
+    """Per shape and M: the dense FFN (merged gate/up and down products
+    through torch.matmul, i.e. hipBLASLt, with star_swiglu_merged_fwd
+    between them), the algebraic FFN with the same merged layout and the
+    same activation kernel (the paper's comparison), and the algebraic FFN
+    with SwiGLU fused into the merged product's epilogue.  The type plan is
+    built once per batch outside the timed work (every layer shares it).
+    Warm trials replay a graph of kGraphCalls FFNs, flushed trials a graph of
+    one."""
+    q = 32
+    out = {}
+    for name, D, F, paper in KERNEL_FFN_SHAPES:
+        for M in (1, 2048):
+            g = torch.Generator(device=dev)
+            g.manual_seed(8_000_000 + M + D + F)
+            rnd = lambda shape, std: (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+            X = rnd((M, D), 1.0)
+            W_gu = rnd((D, 2 * F), D ** -0.5)  # gate and up interleaved in 8-feature chunks
+            W_dn = rnd((F, D), F ** -0.5)
+            Z = torch.empty((M, 2 * F), dtype=torch.bfloat16, device=dev)
+            H = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+            Y = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
+            up = P.Algebra.equal(q, D, F)
+            gu, dn = up.merged_gate_up(), P.Algebra.equal(q, F, D)
+            plan = P.star_type_plan(q, torch.from_numpy(synth.cyclic_types(M, q)).to(dev))
+
+            def dense():
+                torch.matmul(X, W_gu, out=Z)
+                P.star_swiglu_merged_fwd(Z, H=H)
+                torch.matmul(H, W_dn, out=Y)
+
+            def algebra():
+                P.star_proj_fwd_planned(gu, plan, X, W_gu, Y=Z)
+                P.star_swiglu_merged_fwd(Z, H=H)
+                P.star_proj_fwd_planned(dn, plan, H, W_dn, Y=Y)
+
+            def fused():
+                P.star_swiglu_up_fwd_planned(gu, plan, X, W_gu, H=H)
+                P.star_proj_fwd_planned(dn, plan, H, W_dn, Y=Y)
+
+            fns = {"dense": dense, "algebra": algebra, "algebra_fused": fused}
+            graphs = {}
+            for method, fn in fns.items():
+                many = lambda fn=fn: [fn() for _ in range(kGraphCalls)]
+                graphs[method] = (graphed(torch, many), graphed(torch, fn))
+            warm = T.compare({m: gr[0][0] for m, gr in graphs.items()}, flushed=False)
+            cold = T.compare({m: gr[1][0] for m, gr in graphs.items()}, warm=False)
+            del graphs
+            us = {m: warm[m]["warm_ms"] / kGraphCalls * 1e3 for m in fns}
+            fus = {m: cold[m]["flushed_ms"] * 1e3 for m in fns}
+            pd = paper[M]
+            out[f"{name} M{M}"] = {
+                "M": M, "D": D, "F": F, "q": q,
+                "dense_us": round(us["dense"], 1), "algebra_us": round(us["algebra"], 1),
+                "algebra_fused_us": round(us["algebra_fused"], 1),
+                "dense_us_flushed": round(fus["dense"], 1), "algebra_us_flushed": round(fus["algebra"], 1),
+                "algebra_fused_us_flushed": round(fus["algebra_fused"], 1),
+                "speedup": [round(us["dense"] / us["algebra"], 2), round(fus["dense"] / fus["algebra"], 2)],
+                "speedup_fused": [round(us["dense"] / us["algebra_fused"], 2),
+                                  round(fus["dense"] / fus["algebra_fused"], 2)],
+                "paper_h200_context": {"dense_us": pd[0], "algebra_us": pd[1], "speedup": pd[2:]},
+            }
+            log(f"  {name} M={M}: dense {us['dense']:.1f} us, algebra {us['algebra']:.1f} us "
+                f"(fused {us['algebra_fused']:.1f}); flushed {fus['dense']:.1f} / {fus['algebra']:.1f} / "
+                f"{fus['algebra_fused']:.1f}")
+            del X, W_gu, W_dn, Z, H, Y
+            torch.cuda.empty_cache()
     return out
 
 
