@@ -219,8 +219,11 @@ star_status star_ffn_fwd(const star_algebra *up, const star_algebra *down, int64
  * (without `residual` the FFN output replaces h).  The hidden activation is
  * stored in bfloat16.  This is a skinny, weight-bandwidth-bound product: every
  * weight block that some row's support reaches is read once per step, and a
- * block no row's support reaches is not read.  D and F must be at most 4096
- * (STAR_ERR_UNSUPPORTED otherwise); M at most 64.  A row whose type lies
+ * block no row's support reaches is not read.  D and F must be at most 32768
+ * (STAR_ERR_UNSUPPORTED otherwise); M at most 64.  Shapes whose column tiles
+ * fit one workgroup per CU (D, F up to a few thousand) run as one persistent
+ * launch for the whole stack; wider ones, and a stack the persistent launch
+ * cannot hold, run one launch per projection.  A row whose type lies
  * outside [0, q) reaches no weight block: each layer adds act(b_up) *_q
  * nothing + b_down = b_down, so its Y row is X + the sum of the b_down[l]
  * (without `residual`: b_down of the last layer, or zeros without biases).
@@ -261,8 +264,8 @@ star_status star_decode(const star_algebra *up, const star_algebra *down, int32_
  *           is kept in the static buffer and not reported
  * A shape whose star_decode workspace (star_workspace_bytes(STAR_OP_DECODE,
  * up, down, M)) exceeds STAR_DECODE_SCRATCH_BYTES returns STAR_ERR_WORKSPACE
- * before anything is launched; every shape the decode kernels take (D, F <=
- * 4096, M <= 64) fits.  Every call on one device shares that device's
+ * before anything is launched; every shape with D, F <= 4096 and M <= 64
+ * fits (wider ones may not).  Every call on one device shares that device's
  * buffer, and each call clears the parts that must start at zero: calls that
  * overlap in time on one device (other streams, other threads) race and
  * give unspecified results; calls ordered on one stream do not.

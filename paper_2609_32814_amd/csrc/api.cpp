@@ -497,7 +497,9 @@ size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_alge
       Alg d;
       if (parse_alg(alg2, d) != STAR_OK) return 0;
       const int64_t m = std::min<int64_t>(M, kDecodeMaxRows);
-      return std::max(decode_layout(a, m).end, stack_plan(a, d, std::max<int64_t>(m, 1), 1).end);
+      // the single-launch stack's layout only where the stack can run
+      const StackPlan sp = stack_plan(a, d, std::max<int64_t>(m, 1), 1);
+      return sp.ok ? std::max(decode_layout(a, m).end, sp.end) : decode_layout(a, m).end;
     }
     default:
       return 0;
@@ -835,7 +837,7 @@ star_status decode_impl(const star_algebra* up, const star_algebra* down, int32_
   }
   const DecodeWs dw = decode_layout(u, M);
   const StackPlan sp = stack_plan(u, d, M, n_layers, gated);
-  if (!ws || ws_bytes < std::max(dw.end, sp.end)) return STAR_ERR_WORKSPACE;
+  if (!ws || ws_bytes < (sp.ok ? std::max(dw.end, sp.end) : dw.end)) return STAR_ERR_WORKSPACE;
   if (!aligned16(ws)) return STAR_ERR_ALIGN;
   // the gated FFN runs only in the persistent stack
   if (gated && !sp.ok) return STAR_ERR_UNSUPPORTED;

@@ -15,7 +15,8 @@
 // every fourth needed slice straight from global memory into LDS with one
 // 16-byte-per-lane direct load (32 rows x 32 bytes = 1 KB per slice), all
 // issued before any is consumed, so the whole weight tile is in flight at
-// once.  The wavefront then reads each slice back with the LDS transpose
+// once (in passes of up to 128 slices when K is wider than 4096: a wave
+// reuses only its own slots, so the passes need no barrier).  The wavefront then reads each slice back with the LDS transpose
 // read (two reads give every lane 8 consecutive K values of one column),
 // loads the rows' 8-element input pieces (zero where the support skips
 // them), and multiplies with v_mfma_f32_16x16x32_bf16.  The four
@@ -36,6 +37,7 @@ constexpr int kThreads = 256;
 constexpr int TN = kDecodeTileN;      // 16 output columns
 constexpr int SLICE = kDecodeSliceK;  // 32 K rows
 constexpr int kRedBytes = 4 * 4 * 64 * 16;  // 4 waves x 4 row blocks x 64 lanes x float4
+constexpr int kPassSlices = 128;            // slices held in LDS at once (128 KB)
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define STARQ_LDS __attribute__((address_space(3)))
@@ -64,8 +66,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ unsigned long long rowmask_s[kMaxQGroups];
   __shared__ int16_t slices_s[kDecodeMaxK / SLICE];
-  __shared__ int32_t nslices_s;
-  __shared__ int32_t wave_cnt_s[2];
+  __shared__ int32_t wave_cnt_s[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -94,44 +95,31 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
     }
   }
   __syncthreads();
-  // needed slices, in K order: one slice per thread, compacted with ballots
-  {
-    const int nsl = (p.K + SLICE - 1) / SLICE;  // <= 128, the first two waves
+  // needed slices, in K order: one slice per thread a round (256 slices a
+  // round), compacted with ballots
+  const int nsl = (p.K + SLICE - 1) / SLICE;  // <= kDecodeMaxK / SLICE
+  int32_t found = 0;                          // needed slices before this round
+  for (int base = 0; base < nsl; base += kThreads) {
+    const int sl = base + tid;
     bool need = false;
-    if (tid < nsl) {
+    if (sl < nsl) {
       for (int piece = 0; piece < SLICE / 8; ++piece) {
-        const int32_t k = tid * SLICE + piece * 8;
+        const int32_t k = sl * SLICE + piece * 8;
         if (k < p.K && rowmask_s[group_of(p.S, p.q, k)]) need = true;
       }
     }
     const unsigned long long bal = __ballot(need);
-    if (wave < 2 && lane == 0) wave_cnt_s[wave] = __popcll(bal);
+    if (lane == 0) wave_cnt_s[wave] = __popcll(bal);
     __syncthreads();
     if (need) {
-      const int before = (wave == 1 ? wave_cnt_s[0] : 0) +
-                         __popcll(bal & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
-      slices_s[before] = static_cast<int16_t>(tid);
+      int before = found + __popcll(bal & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+      for (int w = 0; w < wave; ++w) before += wave_cnt_s[w];
+      slices_s[before] = static_cast<int16_t>(sl);
     }
-    if (tid == 0) nslices_s = wave_cnt_s[0] + wave_cnt_s[1];
+    found += wave_cnt_s[0] + wave_cnt_s[1] + wave_cnt_s[2] + wave_cnt_s[3];
+    __syncthreads();  // every thread has read the counts before the next round writes them
   }
-  __syncthreads();
-  const int nslices = nslices_s;
-
-  // stream this wave's slices into LDS: lane l carries row l/2, 16 bytes
-  // (8 columns) at half l%2.  Rows past K repeat row K-1 and columns past
-  // the group repeat its first column (finite values; their products are
-  // either multiplied by zero inputs or never stored).
-  for (int i = wave; i < nslices; i += 4) {
-    int32_t row = slices_s[i] * SLICE + (lane >> 1);
-    row = row < p.K ? row : p.K - 1;
-    int32_t col = n0 + 8 * (lane & 1);
-    col = col < nend ? col : n0;
-    const uint16_t* g = p.W + static_cast<int64_t>(row) * p.N + col;
-    __builtin_amdgcn_global_load_lds(g, (STARQ_LDS void*)(lds + i * 1024), 16, 0, 0);
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __builtin_amdgcn_wave_barrier();
-  __asm__ volatile("" ::: "memory");
+  const int nslices = found;
 
   // compute: lane group G = lane/16 holds K rows 8G..8G+7 of a slice for
   // column n0 + lane%16 (transpose reads), and the input pieces of rows
@@ -142,8 +130,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   f32x4_t acc[4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // input pieces of slice `i` (zero where the row's support skips it),
-  // prefetched two slices ahead
+  // input pieces of slice `i` (zero where the row's support skips it)
   auto load_x = [&](int i, uint4 (&xv)[4]) {
     const int32_t kk = slices_s[i] * SLICE + 8 * G;
     const unsigned long long gm = kk < p.K ? rowmask_s[group_of(p.S, p.q, kk)] : 0ull;
@@ -155,37 +142,61 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
       xv[mb] = ok ? xa : make_uint4(0, 0, 0, 0);
     }
   };
-  uint4 x0[4], x1[4], x2[4];
-  if (wave < nslices) load_x(wave, x0);
-  if (wave + 4 < nslices) load_x(wave + 4, x1);
-  for (int i = wave; i < nslices; i += 4) {
-    if (i + 8 < nslices) load_x(i + 8, x2);
-    const char* base = lds + i * 1024 + (8 * G + (pl >> 2)) * 32 + (pl & 3) * 8;
-    const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base));
-    const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base + 128));
-    uint4 wf;
-    wf.x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
-    wf.y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
-    wf.z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
-    wf.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
+  for (int p0 = 0; p0 < nslices; p0 += kPassSlices) {
+    const int p1 = min(nslices, p0 + kPassSlices);
+    // stream this wave's slices of the pass into LDS (slot i - p0): lane l
+    // carries row l/2, 16 bytes (8 columns) at half l%2.  Rows past K repeat
+    // row K-1 and columns past the group repeat its first column (finite
+    // values; their products are either multiplied by zero inputs or never
+    // stored).
+    for (int i = p0 + wave; i < p1; i += 4) {
+      int32_t row = slices_s[i] * SLICE + (lane >> 1);
+      row = row < p.K ? row : p.K - 1;
+      int32_t col = n0 + 8 * (lane & 1);
+      col = col < nend ? col : n0;
+      const uint16_t* g = p.W + static_cast<int64_t>(row) * p.N + col;
+      __builtin_amdgcn_global_load_lds(g, (STARQ_LDS void*)(lds + (i - p0) * 1024), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+    __asm__ volatile("" ::: "memory");
+    // the input pieces, prefetched two slices ahead
+    uint4 x0[4], x1[4], x2[4];
+    if (p0 + wave < p1) load_x(p0 + wave, x0);
+    if (p0 + wave + 4 < p1) load_x(p0 + wave + 4, x1);
+    for (int i = p0 + wave; i < p1; i += 4) {
+      if (i + 8 < p1) load_x(i + 8, x2);
+      const char* base = lds + (i - p0) * 1024 + (8 * G + (pl >> 2)) * 32 + (pl & 3) * 8;
+      const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base));
+      const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(base + 128));
+      uint4 wf;
+      wf.x = static_cast<uint16_t>(w0[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[1])) << 16);
+      wf.y = static_cast<uint16_t>(w0[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w0[3])) << 16);
+      wf.z = static_cast<uint16_t>(w1[0]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[1])) << 16);
+      wf.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      if (mb < mblocks) {
-        // D[n][m] += W^T x^T: lane ends with 4 consecutive columns of row m
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf),
-                                                          __builtin_bit_cast(bf16x8_t, x0[mb]),
-                                                          acc[mb], 0, 0, 0);
+      for (int mb = 0; mb < 4; ++mb) {
+        if (mb < mblocks) {
+          // D[n][m] += W^T x^T: lane ends with 4 consecutive columns of row m
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf),
+                                                            __builtin_bit_cast(bf16x8_t, x0[mb]),
+                                                            acc[mb], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        x0[mb] = x1[mb];
+        x1[mb] = x2[mb];
       }
     }
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      x0[mb] = x1[mb];
-      x1[mb] = x2[mb];
-    }
+    // the wave's slots are free for the next pass once its reads are done
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+    __asm__ volatile("" ::: "memory");
   }
 
   // add the four waves' partial sums in a fixed order
-  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + (kDecodeMaxK / SLICE) * 1024);
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + kPassSlices * 1024);
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) red[(wave * 4 + mb) * 64 + lane] = acc[mb];
   __syncthreads();
@@ -243,7 +254,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
 
 }  // namespace
 
-size_t decode_phase_smem() { return (kDecodeMaxK / SLICE) * 1024 + kRedBytes; }
+size_t decode_phase_smem() { return kPassSlices * 1024 + kRedBytes; }
 
 hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream) {
   static std::atomic<unsigned long long> lds_set{0};

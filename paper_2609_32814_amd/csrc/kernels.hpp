@@ -137,7 +137,7 @@ constexpr int kTileM = 256;
 constexpr int kDecodeMaxRows = 64;  // rows per step (one new token per sequence)
 constexpr int kDecodeTileN = 16;    // output columns per workgroup
 constexpr int kDecodeSliceK = 32;   // K rows per streamed slice
-constexpr int kDecodeMaxK = 4096;   // input width of either projection
+constexpr int kDecodeMaxK = 32768;  // input width of either projection (one-launch-per-projection path)
 
 // One projection of one decode step: out = epilogue(A *_q W + bias) over M
 // rows, a workgroup per 16 output columns.

@@ -116,6 +116,9 @@ def test_workspace_sizes(P):
     dec = P.star_workspace_bytes("decode", a, d, 64)
     assert dec >= 64 * 768 * 4 + 64 * 768 * 2 + 64 * 3072 * 2
     assert P.star_workspace_bytes("fwd", P.Algebra(2, [7, 9], [8, 8]), None, 10) == 0
+    # projections wider than 4096 decode one launch per projection
+    wu, wd = P.Algebra.equal(4, 1024, 8192), P.Algebra.equal(4, 8192, 1024)
+    assert P.star_workspace_bytes("decode", wu, wd, 16) >= 16 * 1024 * 4 + 16 * 8192 * 2
 
 
 def _raw_fwd(P, alg_c, M, xt=1, wt=1, yt=1, X=16, W=16, Y=16, ws=16, ws_bytes=1 << 20,

@@ -543,6 +543,31 @@ def test_decode_wide_model(P, M):
     assert rel_fro(to_host(Y), ref) <= TOL_BF16
 
 
+@pytest.mark.parametrize("M", [1, 16])
+@pytest.mark.parametrize("D,F", [(1024, 8192), (6144, 2048)])
+def test_decode_wider_than_4096(P, M, D, F):
+    """A projection input wider than 4096 (the down map's F, or the up map's
+    D): the per-projection kernel streams its weight slices through LDS in
+    passes of 128 slices."""
+    import torch
+    q, L = 4, 2
+    up_g, up_o = algs(P, q, [D // q] * q, [F // q] * q)
+    dn_g, dn_o = algs(P, q, [F // q] * q, [D // q] * q)
+    seed = 850 + M + D
+    Wu = [synth.gaussian(seed, 10 + l, (D, F), 0.02, "bf16") for l in range(L)]
+    Wd = [synth.gaussian(seed, 40 + l, (F, D), 0.02, "bf16") for l in range(L)]
+    bu = [synth.gaussian(seed, 70 + l, (F,), 0.02, "f32") for l in range(L)]
+    bd = [synth.gaussian(seed, 90 + l, (D,), 0.02, "f32") for l in range(L)]
+    X = synth.gaussian(seed, 1, (M, D), 1.0, "bf16")
+    t = (synth.decode_positions(seed, M) % q).astype(np.int32)
+    Y = P.star_decode(up_g, dn_g, types_dev(t), to_dev(X), [to_dev(w) for w in Wu], [f32_dev(b.exact) for b in bu],
+                      [to_dev(w) for w in Wd], [f32_dev(b.exact) for b in bd], "gelu", True,
+                      out_dtype=torch.float32)
+    ref = oracle.decode_stack(up_o, dn_o, t, X.exact, [w.exact for w in Wu], [b.exact for b in bu],
+                              [w.exact for w in Wd], [b.exact for b in bd])
+    assert rel_fro(to_host(Y), ref) <= TOL_BF16
+
+
 # ---- full-size workloads (sampled) ---------------------------------------------------
 
 def _sample_rows(M, n, seed):
