@@ -26,8 +26,12 @@
 // the current one (it seeds the accumulators) and, for the weight gradient,
 // the rows of the next stage (a plain load whose value is used would make
 // the compiler wait for every copy in flight, which it does not see).  Lanes whose
-// element lies outside an operand (rows past a type's count, K or columns
-// past a group's end) copy from a page of zeros.
+// K element lies past the step's range copy from a page of zeros; in the
+// forward product and the activation gradient, rows and columns past a
+// tile's end read some other row or column of the operand instead (their
+// products are never stored), so that a copy's source is one add away from
+// a per-tile offset, and each 16-wide slice's copies sit between its MFMAs
+// (a burst of copies ahead of them held the MFMAs back).
 //
 // LDS layouts, per stage:
 //  * K-contiguous rows (X and dY rows, and W read as W^T): 128 bytes
@@ -43,6 +47,7 @@
 //    of those 4 rows, so two reads give a lane 8 consecutive K values of one
 //    column, which is the MFMA operand layout.
 #include <algorithm>
+#include <type_traits>
 
 #include "gemm_common.hpp"
 
@@ -151,7 +156,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   const void* zero = g_zero_page;
   const int q = p.q;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int lr = lane & 31, lh = lane >> 5;
 
@@ -272,6 +277,41 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     const int row = 8 * (wave + kWaves * j) + (lane >> 3);
     rl[j] = row < lt.nrows ? p.perm[lt.pos0 + row] : -1;
   }
+  // Copies of the forward product and the activation gradient: per tile,
+  // the lane's A source of copy j (its row's base plus its 16-byte chunk; a
+  // row past the tile's end reads row 0, whose products land in accumulator
+  // rows that are never stored) and its B source relative to the step's B
+  // base (forward: columns past the matrix end are clamped to its last 8;
+  // activation gradient: rows of W past the tile's columns read its first
+  // one; neither product is stored).  A step then adds one uniform offset
+  // and tests one uniform length, so a copy is an add and a select.
+  constexpr bool kFast = MODE != kModeBwdWeight;
+  const int fa_chunk = (lane & 7) ^ ((4 * (wave & 1) + (lane >> 4)) & 7);  // K-contiguous chunk of every copy j
+  const int fb_kr = 2 * wave + (lane >> 5);                                // forward B: K row of copy 0
+  const int fb_chunk = (lane & 31) ^ (4 * (fb_kr & 3));                    // forward B: column chunk
+  // (offsets in 16-byte units: K and N are multiples of 8, and the operands
+  // are far below 64 GB)
+  uint32_t aoff[DMA_A];
+  uint32_t boff[MODE == kModeFwd ? 1 : DMA_B];
+  auto tile_ptrs = [&]() {
+    if constexpr (kFast) {
+      const uint32_t lda8 = static_cast<uint32_t>((MODE == kModeFwd ? p.K : p.N) >> 3);
+#pragma unroll
+      for (int j = 0; j < DMA_A; ++j) aoff[j] = static_cast<uint32_t>(max(rl[j], 0)) * lda8 + fa_chunk;
+      if constexpr (MODE == kModeFwd) {
+        boff[0] = static_cast<uint32_t>(fb_kr) * static_cast<uint32_t>(p.N >> 3) +
+                  static_cast<uint32_t>(min(fb_chunk, (p.N - 8 - lt.cstart) >> 3));
+      } else {
+#pragma unroll
+        for (int j = 0; j < DMA_B; ++j) {
+          const int row = 8 * (wave + kWaves * j) + (lane >> 3);
+          const int32_t kk = lt.cstart + (lt.cstart + row < lt.cend ? row : 0);
+          boff[j] = static_cast<uint32_t>(kk) * static_cast<uint32_t>(p.N >> 3) + fa_chunk;
+        }
+      }
+    }
+  };
+  tile_ptrs();
   bool has_ln = advance(lit, ln);
   // the load side passes over tiles without K steps (weight-gradient splits
   // with empty row ranges); the compute side writes their zeros
@@ -294,13 +334,23 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   // j = 0, the row-index and bias copies), stage_end moves the load side on.
   char* sA = smem;
   char* sB = smem + A_BYTES;
-  int32_t sk0 = 0, skend = 0;
+  int32_t sk0 = 0, skend = 0, klen = 0;
+  // LDS addresses of the load slot's A and B tiles (uniform: kept in scalar
+  // registers, the copies' M0)
+  const uint32_t lds0 = lds_addr(smem);
+  uint32_t la = lds0, lb = lds0 + A_BYTES;
+  const char* astep = reinterpret_cast<const char*>(Ag);  // forward: X at column sk0
+  const char* bstep = reinterpret_cast<const char*>(Bg);  // forward: W at row sk0, column cstart of the load tile
   auto stage_begin = [&](int slot) {
-    if (!lvalid) return;
     sA = smem + slot * STAGE_BYTES;
     sB = sA + A_BYTES;
+    la = lds0 + slot * STAGE_BYTES;
+    lb = la + A_BYTES;
+    // past the last stage the copies repeat the previous step's sources
+    // into the free slot
+    if (!lvalid) return;
     if (rows_from_lds) {
-      // ln's indices were copied with lt's stages, all of which have landed
+      // ln's indices were copied with lt's first stage, which has landed
       // (every step waits for all copies in flight)
 #pragma unroll
       for (int j = 0; j < DMA_A; ++j) {
@@ -308,8 +358,28 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         rl[j] = row < lt.nrows ? rows_s[lseq & (kRowBufs - 1)][row] : -1;
       }
       rows_from_lds = false;
+      tile_ptrs();
     }
     step_range<MODE, LAW, BK>(p, lt, offs_s, ls, sk0, skend);
+    klen = skend - sk0;
+    if constexpr (kFast) {
+      astep = reinterpret_cast<const char*>(Ag + sk0);
+      bstep = MODE == kModeFwd ? reinterpret_cast<const char*>(Bg + static_cast<int64_t>(sk0) * p.N + lt.cstart)
+                               : reinterpret_cast<const char*>(Bg + sk0);
+      if (ls == 0) {
+        if (wave < 4) {
+          // row indices of the next tile
+          const int r = 64 * wave + lane;
+          const void* g = (has_ln && r < ln.nrows) ? static_cast<const void*>(p.perm + ln.pos0 + r) : zero;
+          dma4(g, lds_addr(&rows_s[(lseq + 1) & (kRowBufs - 1)][64 * wave]));
+        } else if (MODE == kModeFwd) {
+          // bias of this tile's columns, 64 per wave
+          const int32_t col = lt.cstart + 64 * (wave - 4) + lane;
+          const void* g = (p.bias && col < lt.cend) ? static_cast<const void*>(p.bias + col) : zero;
+          dma4(g, lds_addr(&bias_s[lseq & (kRowBufs - 1)][64 * (wave - 4)]));
+        }
+      }
+    }
     if constexpr (MODE == kModeBwdWeight) {
       if (!((pok >> (lstg & 1)) & 1u)) {
         // the rows of this stage were not copied ahead (first stage, or the
@@ -331,7 +401,32 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       }
     }
   };
+  // forward and activation gradient: A copy j and B copy j of this wave
+  // (uniform step offset and length, a select for the K tail)
+  auto copy_a = [&](int j) {
+    const bool ok = 8 * fa_chunk < klen;
+    const void* g = ok ? static_cast<const void*>(astep + static_cast<uint64_t>(aoff[j]) * 16) : zero;
+    dma16(g, la + (wave + kWaves * j) * 1024);
+  };
+  auto copy_b = [&](int j) {
+    const void* g;
+    if constexpr (MODE == kModeFwd) {
+      const bool ok = fb_kr + 2 * kWaves * j < klen;
+      g = ok ? static_cast<const void*>(bstep + static_cast<int64_t>(2 * kWaves * j) * p.N * 2 +
+                                        static_cast<uint64_t>(boff[0]) * 16)
+             : zero;
+    } else {
+      const bool ok = 8 * fa_chunk < klen;
+      g = ok ? static_cast<const void*>(bstep + static_cast<uint64_t>(boff[j]) * 16) : zero;
+    }
+    dma16(g, lb + (wave + kWaves * j) * 1024);
+  };
   auto stage_copy = [&](int j) {
+    if constexpr (kFast) {
+      copy_a(j);
+      copy_b(j);
+      return;
+    }
     if (!lvalid) return;
     const int ii = wave + kWaves * j;
     if constexpr (MODE == kModeBwdWeight) {
@@ -374,48 +469,6 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         }
       }
       return;
-    }
-    {
-      // A: gathered K-contiguous rows, 8 rows per copy
-      const int64_t lda = (MODE == kModeFwd) ? p.K : p.N;
-      const int row = 8 * ii + (lane >> 3);
-      const int c = (lane & 7) ^ kswz(row);
-      const int32_t k = sk0 + 8 * c;
-      const bool ok = rl[j] >= 0 && k < skend;
-      const void* g = ok ? static_cast<const void*>(Ag + static_cast<int64_t>(rl[j]) * lda + k) : zero;
-      dma16(g, lds_addr(sA + ii * 1024));
-    }
-    if constexpr (MODE == kModeFwd) {
-      // B = W[k][n], N-contiguous: 2 K rows of 256 columns per copy
-      const int kr = 2 * ii + (lane >> 5);
-      const int c = (lane & 31) ^ (4 * (kr & 3));
-      const int32_t k = sk0 + kr;
-      const int32_t col = lt.cstart + 8 * c;
-      const bool ok = k < skend && col < lt.cend;
-      const void* g = ok ? static_cast<const void*>(Bg + static_cast<int64_t>(k) * p.N + col) : zero;
-      dma16(g, lds_addr(sB + ii * 1024));
-    } else {
-      // B = rows kk of W read as W^T, K-contiguous (along n): 8 rows per copy
-      const int row = 8 * ii + (lane >> 3);
-      const int c = (lane & 7) ^ kswz(row);
-      const int32_t kk = lt.cstart + row;
-      const int32_t n = sk0 + 8 * c;
-      const bool ok = kk < lt.cend && n < skend;
-      const void* g = ok ? static_cast<const void*>(Bg + static_cast<int64_t>(kk) * p.N + n) : zero;
-      dma16(g, lds_addr(sB + ii * 1024));
-    }
-    if (j == 0) {
-      if (wave < 4) {
-        // row indices of the next tile (the same copy at every step of lt)
-        const int r = 64 * wave + lane;
-        const void* g = (has_ln && r < ln.nrows) ? static_cast<const void*>(p.perm + ln.pos0 + r) : zero;
-        dma4(g, lds_addr(&rows_s[(lseq + 1) & (kRowBufs - 1)][64 * wave]));
-      } else if (MODE == kModeFwd) {
-        // bias of this tile's columns, 64 per wave
-        const int32_t col = lt.cstart + 64 * (wave - 4) + lane;
-        const void* g = (p.bias && col < lt.cend) ? static_cast<const void*>(p.bias + col) : zero;
-        dma4(g, lds_addr(&bias_s[lseq & (kRowBufs - 1)][64 * (wave - 4)]));
-      }
     }
   };
   auto stage_end = [&]() {
@@ -545,15 +598,43 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       const bool wact = MODE == kModeBwdWeight || wave_rows_live(wm, ct.nrows);
       uint4 fa[2][4], fb[2][2];
       read_frags(As, Bs, 0, fa[0], fb[0]);
+      if constexpr (kFast) {
+        // The next stage's A and B copies of each 16-wide slice go between
+        // its MFMAs (after the second and the fourth): issued in a burst
+        // ahead of them, they held the MFMAs back.  The step is one block
+        // either way (a wave whose rows are all past a half-height tile's
+        // end runs the copies only).
+        auto slices = [&](auto on) {
 #pragma unroll
-      for (int rs = 0; rs < 4; ++rs) {
-        if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
-        stage_copy(rs);  // the next stage's copies ride along with the MFMAs
-        if (wact) {
+          for (int rs = 0; rs < 4; ++rs) {
+            if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi)
+            for (int mi = 0; mi < 4; ++mi) {
+              if constexpr (decltype(on)::value) {
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
+                for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
+              }
+              if (mi == 0 || mi == 1) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (mi == 0) copy_a(rs); else copy_b(rs);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            }
+          }
+        };
+        if (wact) slices(std::true_type{});
+        else slices(std::false_type{});
+      } else {
+#pragma unroll
+        for (int rs = 0; rs < 4; ++rs) {
+          if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
+          stage_copy(rs);  // the next stage's copies ride along with the MFMAs
+          if (wact) {
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+              for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
+          }
         }
       }
     }
