@@ -351,7 +351,9 @@ star_status star_proj_bwd_weight_planned(const star_algebra *alg, int64_t M, con
  * on Transformer Shapes": the algebraic kernel's tile is calibrated per
  * shape).  STAR_TILES_AUTO, the default, takes tiles of 64 rows x 128
  * columns when the 256 x 256 tiles would be at most three quarters full
- * (rows taken as spread evenly over the types) or fewer than 128;
+ * (rows taken as spread evenly over the types) and a tile contracts over
+ * fewer than 1024 input features on average (K for the dense law, two
+ * groups' worth otherwise), or when they would be fewer than 128;
  * STAR_TILES_WIDE and STAR_TILES_SMALL force one size.  Input groups
  * narrower than 64 always take the small tiles, fp32 operands always their
  * own kernel.  Applies to star_proj_fwd, star_proj_fwd_planned and the

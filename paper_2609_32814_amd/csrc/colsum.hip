@@ -15,7 +15,9 @@ namespace {
 // below offsets[q].  A block covers 256 columns: thread (g, r) adds 8
 // columns (one 16-byte load per row) over rows r, r + 8, ... of the chunk in
 // order, then the 8 row lanes are added in order through LDS, so the result
-// does not depend on scheduling.
+// does not depend on scheduling.  The rows are loaded 8 at a time before
+// they are added (one load in flight per thread left the kernel waiting on
+// memory latency).
 template <typename T>
 __global__ __launch_bounds__(256) void column_sum_kernel(const T* __restrict__ src, int32_t N,
                                                          const int32_t* __restrict__ perm,
@@ -30,19 +32,43 @@ __global__ __launch_bounds__(256) void column_sum_kernel(const T* __restrict__ s
   const int32_t r0 = c * chunk, r1 = min(rows, r0 + chunk);
   float sum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (n0 < N) {
-    for (int32_t r = r0 + rl; r < r1; r += 8) {
-      const int32_t row = natural ? r : perm[r];
+    constexpr int U = 8;  // rows in flight per thread
+    for (int32_t rb = r0 + rl; rb < r1; rb += 8 * U) {
+      int32_t row[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int32_t r = rb + 8 * u;
+        row[u] = r < r1 ? (natural ? r : perm[r]) : -1;
+      }
       if constexpr (sizeof(T) == 2) {
-        const uint4 v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row) * N + n0);
-        sum[0] += bf16_to_f32(v.x & 0xffffu); sum[1] += bf16_to_f32(v.x >> 16);
-        sum[2] += bf16_to_f32(v.y & 0xffffu); sum[3] += bf16_to_f32(v.y >> 16);
-        sum[4] += bf16_to_f32(v.z & 0xffffu); sum[5] += bf16_to_f32(v.z >> 16);
-        sum[6] += bf16_to_f32(v.w & 0xffffu); sum[7] += bf16_to_f32(v.w >> 16);
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          v[u] = row[u] >= 0 ? *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(row[u]) * N + n0)
+                             : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (row[u] < 0) continue;
+          sum[0] += bf16_to_f32(v[u].x & 0xffffu); sum[1] += bf16_to_f32(v[u].x >> 16);
+          sum[2] += bf16_to_f32(v[u].y & 0xffffu); sum[3] += bf16_to_f32(v[u].y >> 16);
+          sum[4] += bf16_to_f32(v[u].z & 0xffffu); sum[5] += bf16_to_f32(v[u].z >> 16);
+          sum[6] += bf16_to_f32(v[u].w & 0xffffu); sum[7] += bf16_to_f32(v[u].w >> 16);
+        }
       } else {
-        const float4 a = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(row) * N + n0);
-        const float4 b = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(row) * N + n0 + 4);
-        sum[0] += a.x; sum[1] += a.y; sum[2] += a.z; sum[3] += a.w;
-        sum[4] += b.x; sum[5] += b.y; sum[6] += b.z; sum[7] += b.w;
+        float4 a[U], b[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const bool ok = row[u] >= 0;
+          const float* pr = src + static_cast<int64_t>(ok ? row[u] : 0) * N + n0;
+          a[u] = ok ? *reinterpret_cast<const float4*>(pr) : make_float4(0.f, 0.f, 0.f, 0.f);
+          b[u] = ok ? *reinterpret_cast<const float4*>(pr + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (row[u] < 0) continue;
+          sum[0] += a[u].x; sum[1] += a[u].y; sum[2] += a[u].z; sum[3] += a[u].w;
+          sum[4] += b[u].x; sum[5] += b[u].y; sum[6] += b[u].z; sum[7] += b[u].w;
+        }
       }
     }
   }

@@ -520,15 +520,28 @@ __global__ __launch_bounds__(THREADS, 1) void star_gemm_kernel(const GemmParams 
   }
 }
 
+// out = sum over s of part[s], in split order (so the result does not depend
+// on timing).  The partials of up to 8 splits are loaded together before
+// any is added: one dependent load after another left each thread waiting
+// out nsplit memory round trips.
 __global__ void split_reduce_kernel(const float* __restrict__ part, int nsplit, int64_t n,
                                     float* __restrict__ out) {
   const int64_t n4 = n >> 2;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4;
        i += (int64_t)gridDim.x * blockDim.x) {
-    float4 acc = reinterpret_cast<const float4*>(part)[i];
-    for (int s = 1; s < nsplit; ++s) {
-      const float4 v = reinterpret_cast<const float4*>(part + static_cast<int64_t>(s) * n)[i];
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < nsplit; s0 += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        v[k] = s0 + k < nsplit ? reinterpret_cast<const float4*>(part + static_cast<int64_t>(s0 + k) * n)[i]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (s0 + k < nsplit) {
+          acc.x += v[k].x; acc.y += v[k].y; acc.z += v[k].z; acc.w += v[k].w;
+        }
+      }
     }
     reinterpret_cast<float4*>(out)[i] = acc;
   }

@@ -293,7 +293,15 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   // are far below 64 GB)
   uint32_t aoff[DMA_A];
   uint32_t boff[MODE == kModeFwd ? 1 : DMA_B];
+  // weight gradient: the lane's columns of X and of dY (its 16-byte chunk of
+  // the tile's rows and columns of dW; chunks past the tile's end read
+  // others, clamped into the matrix, whose products are not stored)
+  int32_t wa_col = 0, wb_col = 0;
   auto tile_ptrs = [&]() {
+    if constexpr (MODE == kModeBwdWeight) {
+      wa_col = min(lt.rstart + 8 * fb_chunk, p.K - 8);
+      wb_col = min(lt.cstart + 8 * fb_chunk, p.N - 8);
+    }
     if constexpr (kFast) {
       const uint32_t lda8 = static_cast<uint32_t>((MODE == kModeFwd ? p.K : p.N) >> 3);
 #pragma unroll
@@ -330,10 +338,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
 
   // A stage is copied in three parts so that the copies can be spread over
   // the MFMAs of the step being computed: stage_begin picks the stage's K
-  // range, stage_copy(j) issues A copy j and B copy j of this wave (and, for
-  // j = 0, the row-index and bias copies), stage_end moves the load side on.
-  char* sA = smem;
-  char* sB = smem + A_BYTES;
+  // range and issues the small copies (row indices of the next tile and
+  // bias at a tile's first stage; the weight gradient's perm entries of the
+  // next stage), copy_a(j) / copy_b(j) issue A copy j and B copy j of this
+  // wave, stage_end moves the load side on.
   int32_t sk0 = 0, skend = 0, klen = 0;
   // LDS addresses of the load slot's A and B tiles (uniform: kept in scalar
   // registers, the copies' M0)
@@ -342,8 +350,6 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   const char* astep = reinterpret_cast<const char*>(Ag);  // forward: X at column sk0
   const char* bstep = reinterpret_cast<const char*>(Bg);  // forward: W at row sk0, column cstart of the load tile
   auto stage_begin = [&](int slot) {
-    sA = smem + slot * STAGE_BYTES;
-    sB = sA + A_BYTES;
     la = lds0 + slot * STAGE_BYTES;
     lb = la + A_BYTES;
     // past the last stage the copies repeat the previous step's sources
@@ -352,10 +358,12 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     if (rows_from_lds) {
       // ln's indices were copied with lt's first stage, which has landed
       // (every step waits for all copies in flight)
+      if constexpr (kFast) {
 #pragma unroll
-      for (int j = 0; j < DMA_A; ++j) {
-        const int row = 8 * (wave + kWaves * j) + (lane >> 3);
-        rl[j] = row < lt.nrows ? rows_s[lseq & (kRowBufs - 1)][row] : -1;
+        for (int j = 0; j < DMA_A; ++j) {
+          const int row = 8 * (wave + kWaves * j) + (lane >> 3);
+          rl[j] = row < lt.nrows ? rows_s[lseq & (kRowBufs - 1)][row] : -1;
+        }
       }
       rows_from_lds = false;
       tile_ptrs();
@@ -399,18 +407,46 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         const int kr = 2 * (wave + kWaves * j) + (lane >> 5);
         rl[j] = sk0 + kr < skend ? prow_s[lstg & 1][kr] : -1;
       }
+      // rows of the next stage, into the other perm slot (free: its last
+      // reader was the previous step's start)
+      int32_t nlo = 0, nhi = 0;
+      bool next = false;
+      if (ls + 1 < lt.nsteps) {
+        step_range<MODE, LAW, BK>(p, lt, offs_s, ls + 1, nlo, nhi);
+        next = true;
+      } else if (has_ln && ln.nsteps > 0) {
+        step_range<MODE, LAW, BK>(p, ln, offs_s, 0, nlo, nhi);
+        next = true;
+      }
+      const uint32_t bit = 1u << ((lstg + 1) & 1);
+      pok = next ? (pok | bit) : (pok & ~bit);
+      if (next && wave == 0) {
+        const int32_t npos = nlo + lane;
+        dma4(npos < nhi ? static_cast<const void*>(p.perm + npos) : zero, lds_addr(&prow_s[(lstg + 1) & 1][0]));
+      }
     }
   };
-  // forward and activation gradient: A copy j and B copy j of this wave
-  // (uniform step offset and length, a select for the K tail)
+  // A copy j and B copy j of this wave.  Forward and activation gradient:
+  // a uniform step offset and length, a select for the K tail.  Weight
+  // gradient: A = X rows over the tile's K columns, B = dY rows over its N
+  // columns, 2 positions of the type-sorted order per copy (rows read at the
+  // step's start from the perm entries copied ahead), the zero page past
+  // the step's range.
   auto copy_a = [&](int j) {
-    const bool ok = 8 * fa_chunk < klen;
-    const void* g = ok ? static_cast<const void*>(astep + static_cast<uint64_t>(aoff[j]) * 16) : zero;
+    const void* g;
+    if constexpr (MODE == kModeBwdWeight) {
+      g = rl[j] >= 0 ? static_cast<const void*>(Ag + static_cast<int64_t>(rl[j]) * p.K + wa_col) : zero;
+    } else {
+      const bool ok = 8 * fa_chunk < klen;
+      g = ok ? static_cast<const void*>(astep + static_cast<uint64_t>(aoff[j]) * 16) : zero;
+    }
     dma16(g, la + (wave + kWaves * j) * 1024);
   };
   auto copy_b = [&](int j) {
     const void* g;
-    if constexpr (MODE == kModeFwd) {
+    if constexpr (MODE == kModeBwdWeight) {
+      g = rl[j] >= 0 ? static_cast<const void*>(Bg + static_cast<int64_t>(rl[j]) * p.N + wb_col) : zero;
+    } else if constexpr (MODE == kModeFwd) {
       const bool ok = fb_kr + 2 * kWaves * j < klen;
       g = ok ? static_cast<const void*>(bstep + static_cast<int64_t>(2 * kWaves * j) * p.N * 2 +
                                         static_cast<uint64_t>(boff[0]) * 16)
@@ -422,54 +458,8 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     dma16(g, lb + (wave + kWaves * j) * 1024);
   };
   auto stage_copy = [&](int j) {
-    if constexpr (kFast) {
-      copy_a(j);
-      copy_b(j);
-      return;
-    }
-    if (!lvalid) return;
-    const int ii = wave + kWaves * j;
-    if constexpr (MODE == kModeBwdWeight) {
-      // A = X rows over the tile's K columns, B = dY rows over its N
-      // columns, at the tile's positions in the type-sorted order (rows from
-      // perm, copied ahead into prow_s); 2 positions of 256 columns per
-      // copy, both N-contiguous like W in the forward product
-      const int kr = 2 * ii + (lane >> 5);
-      const int c = (lane & 31) ^ (4 * (kr & 3));
-      const int32_t ka = lt.rstart + 8 * c;
-      const int32_t nb = lt.cstart + 8 * c;
-      const bool pin = rl[j] >= 0;
-      const int64_t row = rl[j];
-      const void* ga = (pin && ka < lt.rend) ? static_cast<const void*>(Ag + row * p.K + ka) : zero;
-      const void* gb = (pin && nb < lt.cend) ? static_cast<const void*>(Bg + row * p.N + nb) : zero;
-      dma16(ga, lds_addr(sA + ii * 1024));
-      dma16(gb, lds_addr(sB + ii * 1024));
-      if (j == 0) {
-        // rows of the next stage, into the other perm slot (free: its last
-        // reader was the previous step's copies)
-        int32_t nlo = 0, nhi = 0;
-        bool next = false;
-        // positions of step st of tile t
-        auto stage_range = [&](const Tile& t, int32_t st, int32_t& lo, int32_t& hi) {
-          step_range<MODE, LAW, BK>(p, t, offs_s, st, lo, hi);
-        };
-        if (ls + 1 < lt.nsteps) {
-          stage_range(lt, ls + 1, nlo, nhi);
-          next = true;
-        } else if (has_ln && ln.nsteps > 0) {
-          stage_range(ln, 0, nlo, nhi);
-          next = true;
-        }
-        const uint32_t bit = 1u << ((lstg + 1) & 1);
-        pok = next ? (pok | bit) : (pok & ~bit);
-        if (next && wave == 0) {
-          const int32_t npos = nlo + lane;
-          dma4(npos < nhi ? static_cast<const void*>(p.perm + npos) : zero,
-               lds_addr(&prow_s[(lstg + 1) & 1][0]));
-        }
-      }
-      return;
-    }
+    copy_a(j);
+    copy_b(j);
   };
   auto stage_end = [&]() {
     if (!lvalid) return;
@@ -598,7 +588,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       const bool wact = MODE == kModeBwdWeight || wave_rows_live(wm, ct.nrows);
       uint4 fa[2][4], fb[2][2];
       read_frags(As, Bs, 0, fa[0], fb[0]);
-      if constexpr (kFast) {
+      {
         // The next stage's A and B copies of each 16-wide slice go between
         // its MFMAs (after the second and the fourth): issued in a burst
         // ahead of them, they held the MFMAs back.  The step is one block
@@ -624,18 +614,6 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         };
         if (wact) slices(std::true_type{});
         else slices(std::false_type{});
-      } else {
-#pragma unroll
-        for (int rs = 0; rs < 4; ++rs) {
-          if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
-          stage_copy(rs);  // the next stage's copies ride along with the MFMAs
-          if (wact) {
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-              for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
-          }
-        }
       }
     }
     stage_end();
