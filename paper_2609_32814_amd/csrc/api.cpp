@@ -11,6 +11,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <initializer_list>
+#include <vector>
 
 #include "../../include/star_proj.h"
 #include "kernels.hpp"
@@ -141,20 +142,97 @@ int bwd_weight_nsplit(const Alg& a, int64_t M) {
   return static_cast<int>(std::max<int64_t>(ns, 1));
 }
 
-// Weight gradient with bf16 operands (pipelined kernel, 256 x 256 tiles):
-// the same rule on its own tile count.
-int bwd_weight_nsplit_async(const Alg& a, int64_t M) {
-  const int tn = gemm_async_tile_n();
-  int64_t mt = 0, nt = 0;
-  for (int g = 0; g < a.q; ++g) {
-    mt += tiles_of(a.s(g), kTileM);
-    nt += tiles_of(a.r(g), tn);
-  }
-  const int64_t base = mt * nt;
+// Weight gradient with bf16 operands (pipelined kernel, 256-row tiles of
+// tn columns): the same rule on its own tile count.
+int64_t nsplit_rule(int64_t base, int64_t M) {
   int64_t ns = (256 + base - 1) / base;
   ns = std::min<int64_t>(ns, 8);
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, M / 1024));
-  return static_cast<int>(std::max<int64_t>(ns, 1));
+  return std::max<int64_t>(ns, 1);
+}
+
+// Column tiles of width tn over the output groups (r) or the input groups.
+int64_t col_tiles(const Alg& a, bool over_r, int tn) {
+  int64_t n = 0;
+  for (int g = 0; g < a.q; ++g) n += tiles_of(over_r ? a.r(g) : a.s(g), tn);
+  return n;
+}
+
+// Column-tile width of the pipelined bf16 kernel: 256, or 192 (star and
+// dense laws) where the launch's estimated makespan is shorter, a 192-wide
+// K step counted as 0.9 of a 256-wide one (its copies and per-step costs do
+// not shrink with its MFMAs).  The estimate deals the two passes' tiles (K
+// steps each, in the kernel's order, rows taken as spread evenly over the
+// types, as the host does not read the per-type counts) the way the kernel
+// does on 256 CUs: an eighth of each pass per XCD, in snake order over the
+// XCD's 32 workgroups, each tile also paying its epilogue.  Checked against
+// measured pairs: 8192 x 768 -> 3072 at q = 2 (192: 512 tiles, one long and
+// one short per CU), the 384-wide groups of 16384 x 3072 -> 768 (192: no
+// padding), and the weight gradient 768 x 3072 over 16384 rows (256: at 192
+// the split count drops to 4 and the diagonal tiles run long).
+double deal_makespan(const std::vector<int32_t>* passes, double epi) {
+  constexpr int kGrid = 256, kSlots = kGrid / 8;
+  double worst = 0.0;
+  for (int x = 0; x < 8; ++x) {
+    double load[kSlots] = {};
+    int64_t v = 0;
+    for (int ps = 0; ps < 2; ++ps) {
+      const int64_t n = static_cast<int64_t>(passes[ps].size()), chunk = (n + 7) / 8;
+      for (int64_t t = x * chunk; t < std::min(n, (x + 1) * chunk); ++t, ++v) {
+        const int64_t r = v / kSlots, pos = v % kSlots;
+        load[(r & 1) ? kSlots - 1 - pos : pos] += passes[ps][t] + epi;
+      }
+    }
+    for (double l : load) worst = std::max(worst, l);
+  }
+  return worst;
+}
+int steps_of(int64_t w) { return static_cast<int>((w + 63) / 64); }
+// mode: the kernel's (forward, activation gradient, weight gradient)
+double async_makespan(const Alg& a, int mode, int64_t M, int tn, bool act) {
+  std::vector<int32_t> passes[2];
+  const int q = a.q;
+  const int64_t per = (M + q - 1) / q;  // rows of a type
+  if (mode == kModeBwdWeight) {
+    int64_t mt = 0;
+    for (int g = 0; g < q; ++g) mt += tiles_of(a.s(g), kTileM);
+    const int64_t ns = nsplit_rule(mt * col_tiles(a, true, tn), M);
+    for (int i = 0; i < q; ++i)
+      for (int j = 0; j < q; ++j) {
+        const bool diag = i == j || a.law == STAR_LAW_DENSE;
+        const int st = steps_of(((diag ? M : per) + ns - 1) / ns);
+        passes[i == j ? 0 : 1].insert(passes[i == j ? 0 : 1].end(), tiles_of(a.s(i), kTileM) * tiles_of(a.r(j), tn) * ns,
+                                      st);
+      }
+    return deal_makespan(passes, 1.0 * tn / 256);
+  }
+  const int rt = tiles_of(per, kTileM);
+  const bool fwd = mode == kModeFwd;
+  for (int i = 0; i < q; ++i)
+    for (int u = 0; u < rt; ++u)
+      for (int j = 0; j < q; ++j) {
+        const int ct = tiles_of(fwd ? a.r(j) : a.s(j), tn);
+        int st;
+        if (a.law == STAR_LAW_DENSE) st = steps_of(fwd ? a.K() : a.N());
+        else if (fwd) st = steps_of(a.s(j)) + (j != i ? steps_of(a.s(i)) : 0);
+        else st = j == i ? steps_of(a.N()) : steps_of(a.r(j));
+        // pass 0: forward, the two-segment tiles; activation gradient, the
+        // tiles over every output group
+        const int ps = a.law == STAR_LAW_DENSE ? 0 : (fwd ? (j != i ? 0 : 1) : (j == i ? 0 : 1));
+        passes[ps].insert(passes[ps].end(), ct, st);
+      }
+  const double epi = (act ? (fwd ? 3.0 : 2.0) : 1.0) * tn / 256;
+  return deal_makespan(passes, epi);
+}
+int async_tile_n(const Alg& a, int mode, int64_t M, bool act) {
+  if (a.law != STAR_LAW_STAR && a.law != STAR_LAW_DENSE) return 256;
+  return 0.9 * async_makespan(a, mode, M, 192, act) < async_makespan(a, mode, M, 256, act) ? 192 : 256;
+}
+int async_tile_n_weight(const Alg& a, int64_t M) { return async_tile_n(a, kModeBwdWeight, M, false); }
+int bwd_weight_nsplit_async(const Alg& a, int64_t M) {
+  int64_t mt = 0;
+  for (int g = 0; g < a.q; ++g) mt += tiles_of(a.s(g), kTileM);
+  return static_cast<int>(nsplit_rule(mt * col_tiles(a, true, async_tile_n_weight(a, M)), M));
 }
 
 constexpr int kColSumChunks = 64;  // row chunks of the bias-gradient column sums
@@ -303,6 +381,18 @@ void fill_common(GemmParams& p, const Alg& a, int64_t M, int elem, const int32_t
   p.nsplit = 1;
 }
 
+// the law and group widths of a parameter block, for host-side tile choices
+Alg alg_of(const GemmParams& p) {
+  Alg a;
+  a.q = p.q;
+  a.law = p.law;
+  for (int g = 0; g <= p.q; ++g) {
+    a.S[g] = p.S[g];
+    a.R[g] = p.R[g];
+  }
+  return a;
+}
+
 // column-tile prefix over groups of widths given by starts G
 void fill_tiles(int32_t* pfx, const int64_t* G, int q, int tile) {
   pfx[0] = 0;
@@ -400,7 +490,8 @@ hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper
   if (p.elem == 1) {
     GemmParams pa = p;
     const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
-    const int tn = gemm_async_tile_n();
+    const int tn = async_tile_n(alg_of(p), mode, p.M, p.act != STAR_ACT_NONE);
+    pa.tile_n = tn;
     pa.NTp[0] = 0;
     for (int g = 0; g < p.q; ++g) pa.NTp[g + 1] = pa.NTp[g] + (G[g + 1] - G[g] + tn - 1) / tn;
     const int64_t rows_upper = static_cast<int64_t>(p.M) / kTileM + p.q;
@@ -706,7 +797,8 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   if (pipelined) {
     // every tile contracts over a range of type-sorted positions; the
     // kernel reads the rows of X and dY at those positions through perm
-    fill_tiles(p.NTp, a.R, a.q, gemm_async_tile_n());
+    p.tile_n = async_tile_n_weight(a, M);
+    fill_tiles(p.NTp, a.R, a.q, p.tile_n);
     fill_tiles(p.MTp, a.S, a.q, kTileM);
     p.A = X;
     p.B = dY;
@@ -1133,6 +1225,8 @@ star_status star_add(int64_t n, const void* a, const void* b, star_dtype dt, voi
 
 // ---- algebraic attention --------------------------------------------------
 
+// (helpers: C++ linkage inside the C-linkage block)
+extern "C++" {
 namespace {
 struct AttnShape {
   int32_t B, S, H, Hkv, D, q, law;
@@ -1177,6 +1271,7 @@ AttnDecWs attn_dec_layout(const AttnShape& a) {
   return w;
 }
 }  // namespace
+}  // extern "C++"
 
 star_status star_attn_fwd(const star_attn_shape* shape, const void* plan, const void* Q, const void* K,
                           const void* V, star_dtype dt, void* O, star_dtype ot, float* lse, hipStream_t stream) {

@@ -59,7 +59,7 @@ using namespace gemm;
 
 constexpr int kThreads = 512;                   // 8 wavefronts
 constexpr int kWaves = kThreads / 64;
-constexpr int BN = 256;
+constexpr int BN = 256;                         // LDS column capacity of a B tile
 constexpr int BK = 64;
 constexpr int A_BYTES = BM * BK * 2;            // 256 rows x 64 bf16: 32 KB
 constexpr int B_BYTES = BN * BK * 2;            // 256 columns x 64 bf16: 32 KB
@@ -109,11 +109,24 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// whether rows wm * 128 .. wm * 128 + 127 of a tile with `nrows` rows hold
-// any row (uniform over the wave)
-__device__ __forceinline__ bool wave_rows_live(int wm, int32_t nrows) {
-  return __builtin_amdgcn_readfirstlane(wm * (BM / 2) < nrows ? 1 : 0) != 0;
+// whether the wave's rows, from tile row row0 on, hold any of a tile's
+// `nrows` rows (uniform over the wave)
+__device__ __forceinline__ bool wave_rows_live(int row0, int32_t nrows) {
+  return __builtin_amdgcn_readfirstlane(row0 < nrows ? 1 : 0) != 0;
 }
+
+// Tile shapes: 256 rows x TN columns, 8 wavefronts.  TN = 256: waves 2 x 4
+// of 128 x 64; TN = 192: waves 4 x 2 of 64 x 96 (groups 384 or 1536 wide
+// take whole tiles).  The LDS tiles keep 256 columns of room either way.
+template <int TN> struct Lay {
+  static_assert(TN == 256 || TN == 192, "tile width 256 or 192");
+  static constexpr int WNW = TN == 256 ? 4 : 2;  // waves along N
+  static constexpr int WMW = kWaves / WNW;        // waves along M
+  static constexpr int TMW = BM / WMW;            // rows of a wave
+  static constexpr int TNW = TN / WNW;            // columns of a wave
+  static constexpr int MI = TMW / 32;             // 32-row MFMA blocks
+  static constexpr int NI = TNW / 32;             // 32-column MFMA blocks
+};
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
@@ -136,8 +149,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
-template <int MODE, int LAW, int ACT>
+template <int MODE, int LAW, int ACT, int TN>
 __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const GemmParams p) {
+  using L = Lay<TN>;
+  constexpr int MI = L::MI, NI = L::NI, TMW = L::TMW, TNW = L::TNW;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   // row tiles per class: [0] BM rows, [1] BM / 2 rows (weight gradient:
   // row tiles x splits, both)
@@ -157,7 +172,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   const int q = p.q;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / L::WNW, wn = wave % L::WNW;
   const int lr = lane & 31, lh = lane >> 5;
 
   for (int i = threadIdx.x; i <= q; i += kThreads) offs_s[i] = p.offsets[i];
@@ -235,7 +250,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     int cls = 0;
     while (logical >= pf[cls + 1]) ++cls;
     const bool hh = ps == 1 && half1;
-    t = make_tile<MODE, LAW, BN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pf[cls],
+    t = make_tile<MODE, LAW, TN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pf[cls],
                                      units_s[hh ? 1 : 0][cls], offs_s, hh ? BM / 2 : BM);
     return true;
   };
@@ -243,9 +258,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   // weight gradient: a split whose row range is empty contributes zeros
   auto zero_tile = [&](const Tile& t) {
     float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(t.split) * p.K * p.N : p.dW;
-    for (int idx = threadIdx.x; idx < BM * BN / 4; idx += kThreads) {
-      const int32_t r = t.rstart + idx / (BN / 4);
-      const int32_t c = t.cstart + (idx % (BN / 4)) * 4;
+    for (int idx = threadIdx.x; idx < BM * TN / 4; idx += kThreads) {
+      const int32_t r = t.rstart + idx / (TN / 4);
+      const int32_t c = t.cstart + (idx % (TN / 4)) * 4;
       if (r < t.rend && c < t.cend)
         *reinterpret_cast<float4*>(out + static_cast<int64_t>(r) * p.N + c) = make_float4(0.f, 0.f, 0.f, 0.f);
     }
@@ -300,7 +315,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   auto tile_ptrs = [&]() {
     if constexpr (MODE == kModeBwdWeight) {
       wa_col = min(lt.rstart + 8 * fb_chunk, p.K - 8);
-      wb_col = min(lt.cstart + 8 * fb_chunk, p.N - 8);
+      wb_col = min(lt.cstart + 8 * (fb_chunk < TN / 8 ? fb_chunk : 0), p.N - 8);
     }
     if constexpr (kFast) {
       const uint32_t lda8 = static_cast<uint32_t>((MODE == kModeFwd ? p.K : p.N) >> 3);
@@ -308,7 +323,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       for (int j = 0; j < DMA_A; ++j) aoff[j] = static_cast<uint32_t>(max(rl[j], 0)) * lda8 + fa_chunk;
       if constexpr (MODE == kModeFwd) {
         boff[0] = static_cast<uint32_t>(fb_kr) * static_cast<uint32_t>(p.N >> 3) +
-                  static_cast<uint32_t>(min(fb_chunk, (p.N - 8 - lt.cstart) >> 3));
+                  static_cast<uint32_t>(min(fb_chunk < TN / 8 ? fb_chunk : 0, (p.N - 8 - lt.cstart) >> 3));
       } else {
 #pragma unroll
         for (int j = 0; j < DMA_B; ++j) {
@@ -452,6 +467,8 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
                                         static_cast<uint64_t>(boff[0]) * 16)
              : zero;
     } else {
+      // (rows of W past the tile width are not copied)
+      if (j >= TN / 64) return;
       const bool ok = 8 * fa_chunk < klen;
       g = ok ? static_cast<const void*>(bstep + static_cast<uint64_t>(boff[j]) * 16) : zero;
     }
@@ -477,7 +494,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       }
     }
   };
-  static_assert(DMA_A == 4 && DMA_B == 4, "one A and one B copy per K slice of a step");
+  static_assert(DMA_A == 4 && DMA_B == 4, "one A and one B copy per K slice of a step (fewer B copies at TN 192)");
 
   // fragments of one 16-wide K slice
   // 8 consecutive K values of one column from an N-contiguous tile, by two
@@ -493,29 +510,29 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     f.w = static_cast<uint16_t>(w1[2]) | (static_cast<uint32_t>(static_cast<uint16_t>(w1[3])) << 16);
     return f;
   };
-  auto read_frags = [&](const char* As, const char* Bs, int rs, uint4 (&fa)[4], uint4 (&fb)[2]) {
+  auto read_frags = [&](const char* As, const char* Bs, int rs, uint4 (&fa)[MI], uint4 (&fb)[NI]) {
     if constexpr (MODE == kModeBwdWeight) {
       const int gq = lane >> 4, pp = lane & 15;
       const int k = 16 * rs + 8 * (gq >> 1) + (pp >> 2);
       const int cq = 16 * (gq & 1) + 4 * (pp & 3);
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) fa[mi] = tr_frag(As, k, wm * 128 + mi * 32 + cq);
+      for (int mi = 0; mi < MI; ++mi) fa[mi] = tr_frag(As, k, wm * TMW + mi * 32 + cq);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) fb[ni] = tr_frag(Bs, k, wn * 64 + ni * 32 + cq);
+      for (int ni = 0; ni < NI; ++ni) fb[ni] = tr_frag(Bs, k, wn * TNW + ni * 32 + cq);
       return;
     }
     const int kp = 2 * rs + lh;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-      const int row = wm * 128 + mi * 32 + lr;
+    for (int mi = 0; mi < MI; ++mi) {
+      const int row = wm * TMW + mi * 32 + lr;
       fa[mi] = *reinterpret_cast<const uint4*>(As + krow_off(row, kp));
     }
     if constexpr (MODE == kModeFwd) {
       const int gq = lane >> 4, pp = lane & 15;
       const int k = 16 * rs + 8 * (gq >> 1) + (pp >> 2);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int col = wn * 64 + ni * 32 + 16 * (gq & 1) + 4 * (pp & 3);
+      for (int ni = 0; ni < NI; ++ni) {
+        const int col = wn * TNW + ni * 32 + 16 * (gq & 1) + 4 * (pp & 3);
         const char* a0 = Bs + kcol_off(k, col >> 3) + ((col >> 2) & 1) * 8;
         const v4i16_t w0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0));
         const v4i16_t w1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((STARQ_LDS v4i16_t*)(a0 + 4 * 512));
@@ -526,18 +543,18 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       }
     } else {
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int row = wn * 64 + ni * 32 + lr;
+      for (int ni = 0; ni < NI; ++ni) {
+        const int row = wn * TNW + ni * 32 + lr;
         fb[ni] = *reinterpret_cast<const uint4*>(Bs + krow_off(row, kp));
       }
     }
   };
 
-  f32x16_t acc[4][2];
+  f32x16_t acc[MI][NI];
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0.f;
 
@@ -554,7 +571,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   stage_end();
 
   // first columns of the lane's groups of 4 consecutive outputs
-  auto lcol = [&](int ni, int a) { return wn * 64 + ni * 32 + 8 * a + 4 * lh; };
+  auto lcol = [&](int ni, int a) { return wn * TNW + ni * 32 + 8 * a + 4 * lh; };
 
   int32_t cseq = 0, cs = 0;
   int slot = 0;
@@ -566,13 +583,13 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       // a tile starts: the accumulators start from the bias (forward; its
       // copy came with this step's operands) or from zero
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
+      for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
           float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
           if constexpr (MODE == kModeFwd) bv = *reinterpret_cast<const float4*>(&bias_s[cseq & (kRowBufs - 1)][lcol(ni, a)]);
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi) {
+          for (int mi = 0; mi < MI; ++mi) {
             acc[mi][ni][4 * a + 0] = bv.x;
             acc[mi][ni][4 * a + 1] = bv.y;
             acc[mi][ni][4 * a + 2] = bv.z;
@@ -583,10 +600,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     {
       const char* As = smem + slot * STAGE_BYTES;
       const char* Bs = As + A_BYTES;
-      // a wave whose 128 rows are all past the tile's rows (half-height
-      // tiles) skips the MFMAs
-      const bool wact = MODE == kModeBwdWeight || wave_rows_live(wm, ct.nrows);
-      uint4 fa[2][4], fb[2][2];
+      // a wave whose rows are all past the tile's rows (half-height tiles)
+      // skips the MFMAs
+      const bool wact = MODE == kModeBwdWeight || wave_rows_live(wm * TMW, ct.nrows);
+      uint4 fa[2][MI], fb[2][NI];
       read_frags(As, Bs, 0, fa[0], fb[0]);
       {
         // The next stage's A and B copies of each 16-wide slice go between
@@ -599,14 +616,12 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
           for (int rs = 0; rs < 4; ++rs) {
             if (rs + 1 < 4) read_frags(As, Bs, rs + 1, fa[(rs + 1) & 1], fb[(rs + 1) & 1]);
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi) {
-              if constexpr (decltype(on)::value) {
-#pragma unroll
-                for (int ni = 0; ni < 2; ++ni) mma(acc[mi][ni], fb[rs & 1][ni], fa[rs & 1][mi], uint16_t());
-              }
-              if (mi == 0 || mi == 1) {
+            for (int x = 0; x < MI * NI; ++x) {
+              if constexpr (decltype(on)::value)
+                mma(acc[x / NI][x % NI], fb[rs & 1][x % NI], fa[rs & 1][x / NI], uint16_t());
+              if (x == 1 || x == 3) {
                 __builtin_amdgcn_sched_barrier(0);
-                if (mi == 0) copy_a(rs); else copy_b(rs);
+                if (x == 1) copy_a(rs); else copy_b(rs);
                 __builtin_amdgcn_sched_barrier(0);
               }
             }
@@ -625,50 +640,50 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
       // dW rows k (C rows) x 4 consecutive columns n per lane group
       float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(ct.split) * p.K * p.N : p.dW;
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int32_t k = ct.rstart + wm * 128 + mi * 32 + lr;
-        float* yr = out + static_cast<int64_t>(k) * p.N + ct.cstart + wn * 64 + 4 * lh;
+      for (int mi = 0; mi < MI; ++mi) {
+        const int32_t k = ct.rstart + wm * TMW + mi * 32 + lr;
+        float* yr = out + static_cast<int64_t>(k) * p.N + ct.cstart + wn * TNW + 4 * lh;
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
           for (int a = 0; a < 4; ++a)
-            if (k < ct.rend && ct.cstart + wn * 64 + ni * 32 + 8 * a + 4 * lh < ct.cend)
+            if (k < ct.rend && ct.cstart + wn * TNW + ni * 32 + 8 * a + 4 * lh < ct.cend)
               *reinterpret_cast<float4*>(yr + ni * 32 + 8 * a) =
                   make_float4(acc[mi][ni][4 * a], acc[mi][ni][4 * a + 1], acc[mi][ni][4 * a + 2],
                               acc[mi][ni][4 * a + 3]);
       }
-    } else if (wave_rows_live(wm, ct.nrows))
-    // The arithmetic runs over all 128 accumulators of the lane without
+    } else if (wave_rows_live(wm * TMW, ct.nrows))
+    // The arithmetic runs over all the lane's accumulators without
     // control flow (so independent values interleave); only the memory
     // accesses are predicated on the row and column being inside the tile.
     {
       const int buf = cseq & (kRowBufs - 1);
       const int64_t ldc = (MODE == kModeFwd) ? p.N : p.K;
-      bool rv[4], cv[2][4];
-      int64_t rbase[4];
+      bool rv[MI], cv[NI][4];
+      int64_t rbase[MI];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int row = wm * 128 + mi * 32 + lr;
+      for (int mi = 0; mi < MI; ++mi) {
+        const int row = wm * TMW + mi * 32 + lr;
         rv[mi] = row < ct.nrows;
         rbase[mi] = static_cast<int64_t>(rv[mi] ? rows_s[buf][row] : 0) * ldc + ct.cstart;
       }
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
+      for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
         for (int a = 0; a < 4; ++a) cv[ni][a] = ct.cstart + lcol(ni, a) < ct.cend;
       // the bf16 stores write 8-column groups at ni * 32 + 16 pr of the
       // lane's columns (column ends are multiples of 8)
-      const int clim8 = ct.cend - ct.cstart - wn * 64 - 8 * lh;
+      const int clim8 = ct.cend - ct.cstart - wn * TNW - 8 * lh;
 
-      // the lane's 4 x 2 x 4 groups of 4 consecutive outputs: one row
+      // the lane's MI x NI x 4 groups of 4 consecutive outputs: one row
       // pointer per 32-row block, constant offsets for the rest
       auto store_tile = [&](void* out) {
         if (p.ydtype == 0) {
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi) {
-            float* yr = static_cast<float*>(out) + rbase[mi] + wn * 64 + 4 * lh;
+          for (int mi = 0; mi < MI; ++mi) {
+            float* yr = static_cast<float*>(out) + rbase[mi] + wn * TNW + 4 * lh;
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
+            for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
               for (int a = 0; a < 4; ++a)
                 if (rv[mi] && cv[ni][a])
@@ -684,10 +699,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
           // (half the store instructions of 8-byte pieces; measured 9 % off
           // the forward kernel at 8192 x 768 x 3072).
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi) {
-            uint16_t* yr = static_cast<uint16_t*>(out) + rbase[mi] + wn * 64;
+          for (int mi = 0; mi < MI; ++mi) {
+            uint16_t* yr = static_cast<uint16_t*>(out) + rbase[mi] + wn * TNW;
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
+            for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
               for (int pr = 0; pr < 2; ++pr) {
                 const int a0 = 2 * pr, a1 = 2 * pr + 1;
@@ -708,9 +723,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         if (p.Z) store_tile(p.Z);
         if constexpr (ACT != kActNone) {
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi)
+          for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
+            for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
               for (int e = 0; e < 16; ++e) acc[mi][ni][e] = act_apply(ACT, acc[mi][ni][e]);
         }
@@ -719,10 +734,10 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
         // 4 values at a time (the fence keeps the compiler from hoisting
         // every Z_prev load and derivative, which would not fit in registers)
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-          const uint16_t* zr = static_cast<const uint16_t*>(p.Zprev) + rbase[mi] + wn * 64 + 4 * lh;
+        for (int mi = 0; mi < MI; ++mi) {
+          const uint16_t* zr = static_cast<const uint16_t*>(p.Zprev) + rbase[mi] + wn * TNW + 4 * lh;
 #pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
+          for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
             for (int a = 0; a < 4; ++a) {
               uint2 zw = make_uint2(0, 0);
@@ -756,9 +771,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   wait_vm_all();
 }
 
-template <int MODE, int LAW, int ACT>
+template <int MODE, int LAW, int ACT, int TN>
 hipError_t launch_one(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
-  auto kern = star_gemm_async_kernel<MODE, LAW, ACT>;
+  auto kern = star_gemm_async_kernel<MODE, LAW, ACT, TN>;
   static std::atomic<unsigned long long> lds_set{0};
   const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(kern), lds_set, SMEM);
   if (attr != hipSuccess) return attr;
@@ -770,12 +785,26 @@ hipError_t launch_one(const GemmParams& p, int64_t upper, int cus, hipStream_t s
   return hipGetLastError();
 }
 
+// the 192-wide tiles are built for the star and dense laws only
+template <int MODE, int LAW, int ACT>
+hipError_t launch_tn(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
+  if constexpr (LAW <= 1) {
+    if (p.tile_n == 192) return launch_one<MODE, LAW, ACT, 192>(p, upper, cus, stream);
+  }
+  if (p.tile_n != 256) return hipErrorInvalidValue;
+  return launch_one<MODE, LAW, ACT, 256>(p, upper, cus, stream);
+}
+
 template <int MODE, int LAW>
 hipError_t launch_act(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
-  switch (p.act) {
-    case kActGelu: return launch_one<MODE, LAW, kActGelu>(p, upper, cus, stream);
-    case kActGeluTanh: return launch_one<MODE, LAW, kActGeluTanh>(p, upper, cus, stream);
-    default: return launch_one<MODE, LAW, kActNone>(p, upper, cus, stream);
+  if constexpr (MODE == kModeBwdWeight) {
+    return launch_tn<MODE, LAW, kActNone>(p, upper, cus, stream);
+  } else {
+    switch (p.act) {
+      case kActGelu: return launch_tn<MODE, LAW, kActGelu>(p, upper, cus, stream);
+      case kActGeluTanh: return launch_tn<MODE, LAW, kActGeluTanh>(p, upper, cus, stream);
+      default: return launch_tn<MODE, LAW, kActNone>(p, upper, cus, stream);
+    }
   }
 }
 
@@ -789,21 +818,11 @@ hipError_t launch_async(const GemmParams& p, int64_t upper, int cus, hipStream_t
 
 }  // namespace
 
-int gemm_async_tile_n() { return BN; }
-
 hipError_t launch_gemm_async(int mode, const GemmParams& p, int64_t upper_tiles, int cus,
                              hipStream_t stream) {
   if (mode == kModeFwd) return launch_async<kModeFwd>(p, upper_tiles, cus, stream);
-  if (mode == kModeBwdWeight) {
-    switch (p.law) {
-      case 1: return launch_one<kModeBwdWeight, 1, kActNone>(p, upper_tiles, cus, stream);
-      case 2: return launch_one<kModeBwdWeight, 2, kActNone>(p, upper_tiles, cus, stream);
-      case 3: return launch_one<kModeBwdWeight, 3, kActNone>(p, upper_tiles, cus, stream);
-      default: return launch_one<kModeBwdWeight, 0, kActNone>(p, upper_tiles, cus, stream);
-    }
-  }
+  if (mode == kModeBwdWeight) return launch_async<kModeBwdWeight>(p, upper_tiles, cus, stream);
   return launch_async<kModeBwdData>(p, upper_tiles, cus, stream);
 }
-
 
 }  // namespace starq

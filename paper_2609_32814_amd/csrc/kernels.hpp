@@ -47,6 +47,9 @@ struct GemmParams {
   float* partial;     // [nsplit][K][N] when nsplit > 1
   float* dbias_part;  // [nsplit][N] when nsplit > 1
   int32_t nsplit;
+  // bf16 pipelined kernel: columns of a C tile (256, or 192 for the star and
+  // dense laws); p.NTp counts column tiles of that width
+  int32_t tile_n;
   // law 3 (graph algebra): bit j of adj[i] marks the edge i -> j, bit i of
   // adj_in[j] the same edge (so adj_in[j] holds the in-neighbours of j)
   uint64_t adj[kMaxQGroups];
@@ -61,11 +64,11 @@ hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
 // Persistent grouped GEMM for fp32 operands: tiles of kTileM rows x 128
 // columns (nw must be 2), `grid` workgroups of 256 threads.
 hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream);
-// bf16 forward / activation-gradient GEMM fed by direct global-to-LDS
-// copies: tiles of kTileM x gemm_async_tile_n() (p.NTp must count column
-// tiles of that width); `upper_tiles` bounds the tile count and `cus` is the
-// device's CU count (the kernel picks its persistent grid from both).
-int gemm_async_tile_n();
+// bf16 forward / activation-gradient / weight-gradient GEMM fed by direct
+// global-to-LDS copies: tiles of kTileM x p.tile_n (256, or 192 for laws 0
+// and 1; p.NTp must count column tiles of that width); `upper_tiles` bounds
+// the tile count and `cus` is the device's CU count (the kernel picks its
+// persistent grid from both).
 // part[c][n] = sum over rows [c chunk, (c + 1) chunk) of the rows of valid
 // type of the bf16 matrix src [M][N]: in row order when every row is valid,
 // else in type-sorted order (row perm[position], positions below offsets[q]).
