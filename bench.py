@@ -45,7 +45,7 @@ FLUSH_BYTES = 512 << 20    # twice the 256 MB Infinity Cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "star_gemm_fwd_cfg2_traffic.json")
 GEMM_SRCS = [os.path.join(ROOT, "paper_2609_32814_amd", "csrc", f)
              for f in ("gemm_async.hip", "gemm_common.hpp")]
-GEMM_KERNEL = "star_gemm_async_kernel<fwd, star, gelu>"
+GEMM_KERNEL = "star_gemm_async_kernel<fwd, star, gelu, {tn}>"  # tn: the calibrated tile width
 
 
 def gemm_src_hash():
@@ -162,18 +162,20 @@ class Protocol:
             o["reps"] = reps
         return out
 
-    def kernel_mean(self, pre, fn, n):
-        """Mean duration of fn() from an event pair around each call, with
-        pre() (the type plan) outside the pairs."""
+    def graph_mean(self, replay, per_replay, reps):
+        """Mean duration of one launch from an event pair around `reps`
+        replays of a HIP graph holding `per_replay` launches back to back
+        (no host launch gaps inside the timed interval, so the mean is the
+        kernels' own time, as a kernel trace measures it)."""
         torch = self.torch
-        ks = [(self.ev(), self.ev()) for _ in range(n)]
-        for s0, s1 in ks:
-            pre()
-            s0.record()
-            fn()
-            s1.record()
         torch.cuda.synchronize()
-        return statistics.mean(s0.elapsed_time(s1) for s0, s1 in ks)
+        e0, e1 = self.ev(), self.ev()
+        e0.record()
+        for _ in range(reps):
+            replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * per_replay)
 
 
 def graphed(torch, fn):
@@ -271,37 +273,66 @@ def main():
     def run_plan():
         P.star_type_plan(q, td, plan)
 
-    def step_of(a):
+    # Tile calibration per law (the paper calibrates the tile on each shape):
+    # a short warm trial of the 256 x 256 and 256 x 192 tiles, the faster
+    # taken for every timing below (set before each launch, so the two laws
+    # can alternate with their own tiles).
+    tiles = {"star": "auto", "dense": "auto"}
+
+    def step_of(a, law):
         def step():
+            P.star_set_fwd_tiles(tiles[law])
             run_plan()
             P.star_proj_fwd_planned(a, plan, Xd, Wd, bd, "gelu", Y=Y)
         return step
 
-    def gemm_of(a):
-        return lambda: P.star_proj_fwd_planned(a, plan, Xd, Wd, bd, "gelu", Y=Y)
+    def gemm_of(a, law):
+        def gemm():
+            P.star_set_fwd_tiles(tiles[law])
+            P.star_proj_fwd_planned(a, plan, Xd, Wd, bd, "gelu", Y=Y)
+        return gemm
+
+    run_plan()
+    calib = {}
+    for law, a in (("star", alg), ("dense", dalg)):
+        res = {}
+        for t_ in ("wide", "wide192"):
+            tiles[law] = t_
+            g = gemm_of(a, law)
+            for _ in range(3):
+                g()
+            res[t_] = round(statistics.median(T._run(g, 10, False) for _ in range(5)) * 1e3, 2)
+        tiles[law] = min(res, key=res.get)
+        calib[law] = res
+    log(f"primary tile calibration (warm us per launch): {calib} -> {tiles}")
 
     log("primary: star_2 FFN up-projection M=8192 768->3072 bf16 + bias + GELU")
     for _ in range(args.warmup):
-        step_of(alg)()
-        step_of(dalg)()
+        step_of(alg, "star")()
+        step_of(dalg, "dense")()
     # the step (type plan + GEMM) as eager launches and as a HIP graph replay,
     # star and dense in alternating trials
-    g_star, keep1 = graphed(torch, step_of(alg))
-    g_dense, keep2 = graphed(torch, step_of(dalg))
-    steps = T.compare({"star_eager": step_of(alg), "dense_eager": step_of(dalg),
+    g_star, keep1 = graphed(torch, step_of(alg, "star"))
+    g_dense, keep2 = graphed(torch, step_of(dalg, "dense"))
+    steps = T.compare({"star_eager": step_of(alg, "star"), "dense_eager": step_of(dalg, "dense"),
                        "star_graph": g_star, "dense_graph": g_dense})
     del keep1, keep2
-    # the GEMM alone (the plan already built): warm mean per launch from an
-    # event pair around each launch, and cache-flushed single launches
+    # the GEMM alone (the plan already built): warm mean per launch over
+    # graph replays of 10 launches, and cache-flushed single launches
     run_plan()
+    kern_graphs = {}
+    for name, a in (("star", alg), ("dense", dalg)):
+        g_fn = gemm_of(a, name)
+        kern_graphs[name] = graphed(torch, lambda g_fn=g_fn: [g_fn() for _ in range(10)])
     kern_trials = {"star": [], "dense": []}
     for k in range(args.trials):
         for name in (("star", "dense") if k % 2 == 0 else ("dense", "star")):
-            a = alg if name == "star" else dalg
-            kern_trials[name].append(T.kernel_mean(lambda: None, gemm_of(a), max(10, args.steps // 2)))
+            kern_trials[name].append(T.graph_mean(kern_graphs[name][0], 10, max(2, args.steps // 10)))
+    del kern_graphs
     kern = statistics.median(kern_trials["star"])
     d_kern = statistics.median(kern_trials["dense"])
-    flushed = T.compare({"star": gemm_of(alg), "dense": gemm_of(dalg)}, warm=False)
+    flushed = T.compare({"star": gemm_of(alg, "star"), "dense": gemm_of(dalg, "dense")}, warm=False)
+    P.star_set_fwd_tiles("auto")
     star_flushed, dense_flushed = flushed["star"]["flushed_ms"], flushed["dense"]["flushed_ms"]
     eager_ms, graph_ms = steps["star_eager"]["warm_ms"], steps["star_graph"]["warm_ms"]
     ms = min(eager_ms, graph_ms)
@@ -313,16 +344,18 @@ def main():
         f"  -> {value:.1f} TFLOP/s step, {achieved:.1f} TFLOP/s kernel")
     log(f"  dense step {d_step_ms*1e3:.1f} us  kernel {d_kern*1e3:.1f} us  flushed {dense_flushed*1e3:.1f} us")
 
+    tn = 192 if tiles["star"] == "wide192" else 256
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
-        if tr.get("gemm_src_sha256") == gemm_src_hash():
+        # counters of this code and this tile width only
+        if tr.get("gemm_src_sha256") == gemm_src_hash() and tr.get("tile_n") == tn:
             traffic = tr.get("hbm_bytes_per_launch")
 
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic, "kernel": GEMM_KERNEL,
+                "traffic": traffic, "kernel": GEMM_KERNEL.format(tn=tn),
                 "kernel_mean_us": round(kern * 1e3, 2)}
     dense_ctrl = {
         "kernel_mean_us": round(d_kern * 1e3, 2),
@@ -350,7 +383,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": "star_2 FFN up-projection + bias + GELU, M=8192 (8x1024 tokens), "
                                "768->3072 in blocks 384x1536, bf16 in / fp32 acc / bf16 out, "
-                               "row type = position mod 2",
+                               "row type = position in the sequence mod 2",
                    "M": M, "K": K, "N": N, "q": q, "retained_gflop": round(flops_star / 1e9, 3),
                    "parallelism": "single GPU",
                    "step": "type plan + fused GEMM; medians of 12 trials alternating star and dense, "
@@ -359,8 +392,8 @@ def main():
                    "step_us_eager": round(eager_ms * 1e3, 2),
                    "step_us_graph": round(graph_ms * 1e3, 2),
                    "trials": args.trials, "reps_per_warm_trial": steps["star_eager"]["reps"],
-                   "tile": "256 x 256 x 64, 8 waves of 128 x 64, one persistent workgroup per CU "
-                           "(the one configuration that fits; see the design notes)"},
+                   "tile": f"256 x {tn} x 64, 8 waves, one persistent workgroup per CU",
+                   "tile_calibration_us": calib, "tiles": dict(tiles)},
         "roofline": roofline,
         "dense_control": dense_ctrl,
         "mfma_peak_frac_step": round(value / PEAK_BF16_TFLOPS, 4),

@@ -353,15 +353,24 @@ star_status star_proj_bwd_weight_planned(const star_algebra *alg, int64_t M, con
  * columns when the 256 x 256 tiles would be at most three quarters full
  * (rows taken as spread evenly over the types) and a tile contracts over
  * fewer than 1024 input features on average (K for the dense law, two
- * groups' worth otherwise), or when they would be fewer than 128;
- * STAR_TILES_WIDE and STAR_TILES_SMALL force one size.  Input groups
+ * groups' worth otherwise), or when they would be fewer than 128; else
+ * tiles of 256 rows x 256 columns, or x 192 columns (star and dense laws)
+ * where those pad fewer output columns (groups 384 wide) and an estimate of
+ * the persistent kernel's tile deal favours them.  STAR_TILES_WIDE (256 x
+ * 256), STAR_TILES_WIDE192 (256 x 192 for the star and dense laws, 256 x
+ * 256 for the others) and STAR_TILES_SMALL force one size.  Input groups
  * narrower than 64 always take the small tiles, fp32 operands always their
  * own kernel.  Applies to star_proj_fwd, star_proj_fwd_planned and the
  * projections of star_ffn_fwd.  Process-wide (every device and stream),
  * read when a call launches.  Returns the previous choice, or -1 (nothing
  * changed) for a value outside the enum.  Both sizes give the same results
  * to rounding: the K order within a group is the same, the tiles differ. */
-typedef enum { STAR_TILES_AUTO = 0, STAR_TILES_WIDE = 1, STAR_TILES_SMALL = 2 } star_tiles;
+typedef enum {
+  STAR_TILES_AUTO = 0,
+  STAR_TILES_WIDE = 1,
+  STAR_TILES_SMALL = 2,
+  STAR_TILES_WIDE192 = 3
+} star_tiles;
 int star_set_fwd_tiles(int tiles);
 
 /* Workspace bytes an entry point needs (alg2 is the down algebra for

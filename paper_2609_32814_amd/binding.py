@@ -245,13 +245,14 @@ def star_workspace_bytes(op: str, alg: Algebra, alg2: Algebra | None, M: int) ->
     return int(LIB.star_workspace_bytes(OPS[op], alg.ref, alg2.ref if alg2 else None, int(M)))
 
 
-TILES = {"auto": 0, "wide": 1, "small": 2}
+TILES = {"auto": 0, "wide": 1, "small": 2, "wide192": 3}
 
 
 def star_set_fwd_tiles(tiles: str) -> str:
-    """Forward tile size for bf16 operands: "auto" (by the wide tiles' fill),
-    "wide" (256 x 256) or "small" (64 x 128); process-wide.  Returns the
-    previous setting."""
+    """Forward tile size for bf16 operands: "auto" (by the tiles' fill and
+    padding), "wide" (256 x 256), "wide192" (256 x 192 for the star and dense
+    laws) or "small" (64 x 128); process-wide.  Returns the previous
+    setting."""
     if tiles not in TILES:
         raise ValueError(f"tiles must be one of {sorted(TILES)}, not {tiles!r}")
     prev = int(LIB.star_set_fwd_tiles(TILES[tiles]))

@@ -224,8 +224,18 @@ double async_makespan(const Alg& a, int mode, int64_t M, int tn, bool act) {
   const double epi = (act ? (fwd ? 3.0 : 2.0) : 1.0) * tn / 256;
   return deal_makespan(passes, epi);
 }
+// The default takes 192 only where it pads fewer C columns as well: without
+// padding to remove, the 192-wide tiles' extra re-reads of the row tiles
+// (a third more column tiles per row tile) made them slower on row types in
+// short runs (192 rows: 78 against 63 us for the dense 8192 x 768 -> 3072),
+// even where the deal favours them (1024-row runs: 57 against 63 us).
+int padded_cols(const Alg& a, bool over_r, int tn) {
+  return static_cast<int>(col_tiles(a, over_r, tn) * tn);
+}
 int async_tile_n(const Alg& a, int mode, int64_t M, bool act) {
   if (a.law != STAR_LAW_STAR && a.law != STAR_LAW_DENSE) return 256;
+  const bool over_r = mode != kModeBwdData;
+  if (padded_cols(a, over_r, 192) >= padded_cols(a, over_r, 256)) return 256;
   return 0.9 * async_makespan(a, mode, M, 192, act) < async_makespan(a, mode, M, 256, act) ? 192 : 256;
 }
 int async_tile_n_weight(const Alg& a, int64_t M) { return async_tile_n(a, kModeBwdWeight, M, false); }
@@ -490,7 +500,12 @@ hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper
   if (p.elem == 1) {
     GemmParams pa = p;
     const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
-    const int tn = async_tile_n(alg_of(p), mode, p.M, p.act != STAR_ACT_NONE);
+    int tn = async_tile_n(alg_of(p), mode, p.M, p.act != STAR_ACT_NONE);
+    if (mode == kModeFwd) {
+      const int forced = g_fwd_tiles.load(std::memory_order_relaxed);
+      if (forced == STAR_TILES_WIDE) tn = 256;
+      if (forced == STAR_TILES_WIDE192) tn = p.law == STAR_LAW_STAR || p.law == STAR_LAW_DENSE ? 192 : 256;
+    }
     pa.tile_n = tn;
     pa.NTp[0] = 0;
     for (int g = 0; g < p.q; ++g) pa.NTp[g + 1] = pa.NTp[g] + (G[g + 1] - G[g] + tn - 1) / tn;
@@ -604,7 +619,9 @@ size_t star_workspace_bytes(int32_t op, const star_algebra* alg, const star_alge
 }
 
 int star_set_fwd_tiles(int tiles) {
-  if (tiles != STAR_TILES_AUTO && tiles != STAR_TILES_WIDE && tiles != STAR_TILES_SMALL) return -1;
+  if (tiles != STAR_TILES_AUTO && tiles != STAR_TILES_WIDE && tiles != STAR_TILES_SMALL &&
+      tiles != STAR_TILES_WIDE192)
+    return -1;
   return g_fwd_tiles.exchange(tiles);
 }
 

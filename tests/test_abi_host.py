@@ -41,12 +41,13 @@ def test_binding_names_match_abi(P):
 def test_set_fwd_tiles(P):
     assert P.star_set_fwd_tiles("wide") == "auto"
     assert P.star_set_fwd_tiles("small") == "wide"
-    assert P.star_set_fwd_tiles("auto") == "small"
+    assert P.star_set_fwd_tiles("wide192") == "small"
+    assert P.star_set_fwd_tiles("auto") == "wide192"
     with pytest.raises(ValueError):
         P.star_set_fwd_tiles("huge")
     lib = ctypes.CDLL(P.LIB_PATH)
     lib.star_set_fwd_tiles.restype = ctypes.c_int
-    assert lib.star_set_fwd_tiles(3) == -1 and lib.star_set_fwd_tiles(-1) == -1
+    assert lib.star_set_fwd_tiles(4) == -1 and lib.star_set_fwd_tiles(-1) == -1
     assert P.star_set_fwd_tiles("auto") == "auto"
 
 

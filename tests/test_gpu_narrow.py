@@ -3,8 +3,9 @@ Scaling on Transformer Shapes"): the tiles of 64 rows x 128 columns that
 carry q up to 256 at the widths of the paper's projection study, against the
 fp64 oracle on the same seeded inputs.
 
-Each case runs the same inputs through both tile sizes (forced with
-star_set_fwd_tiles) and through the automatic choice, and covers: several
+Each case runs the same inputs through every tile size (forced with
+star_set_fwd_tiles: 64 x 128, 256 x 256 and 256 x 192) and through the
+automatic choice, and covers: several
 tiles per workgroup (the copy stream runs across tile boundaries), one-step
 tiles (groups 64 wide; under the graph law a diagonal-only tile contracts a
 single group and the tiles of non-edges are skipped), K tails (input widths
@@ -49,7 +50,7 @@ def _types(kind, M, q, seed):
 
 def _run_all_tiles(P, ga, t, X, W, b, act, want_z, odt):
     out = {}
-    for tiles in ("small", "wide", "auto"):
+    for tiles in ("small", "wide", "wide192", "auto"):
         P.star_set_fwd_tiles(tiles)
         try:
             res = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W), None if b is None else f32_dev(b.exact),

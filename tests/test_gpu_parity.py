@@ -156,6 +156,8 @@ PIPE_SHAPES = [
     # long contractions (17 and 9 K steps) and a one-type class of 1 row
     (2, [1040, 520], [264, 136], 771, "one_row"),
     (1, [776], [392], 1100, "cyclic"),
+    # groups 384 wide (whole 256 x 192 tiles) next to ones with a tail of 8
+    (2, [384, 392], [384, 200], 2100, "random"),
 ]
 
 
@@ -170,7 +172,7 @@ def _types(kind, M, q, seed):
     return t
 
 
-@pytest.mark.parametrize("tiles", ["wide", "small"])
+@pytest.mark.parametrize("tiles", ["wide", "wide192", "small"])
 @pytest.mark.parametrize("law", ["star", "dense"])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 @pytest.mark.parametrize("q,s,r,M,types", PIPE_SHAPES)
@@ -311,6 +313,7 @@ def test_half_height_last_round(P, law, mode):
     (3, [40, 64, 24], [48, 16, 136], 4100),  # several splits, ragged
     (4, [32] * 4, [64] * 4, 2049),
     (2, [128, 128], [128, 128], 0),     # empty batch: zero gradients
+    (2, [384, 392], [384, 384], 3000),  # output groups 384 wide
 ])
 def test_bwd_weight_parity(P, law, dtype, q, s, r, M):
     ga, oa = algs(P, q, s, r, law)
