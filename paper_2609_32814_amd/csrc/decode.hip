@@ -26,6 +26,8 @@
 // Column tiles are mapped to workgroups so that the four tiles sharing a
 // 128-byte line of a weight row run on the same XCD (workgroups are
 // dispatched round-robin over the 8 XCDs) and share one L2 fetch.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -37,7 +39,7 @@ constexpr int kThreads = 256;
 constexpr int TN = kDecodeTileN;      // 16 output columns
 constexpr int SLICE = kDecodeSliceK;  // 32 K rows
 constexpr int kRedBytes = 4 * 4 * 64 * 16;  // 4 waves x 4 row blocks x 64 lanes x float4
-constexpr int kPassSlices = 128;            // slices held in LDS at once (128 KB)
+constexpr int kPassSlices = 128;            // most slices held in LDS at once (128 KB)
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 #define STARQ_LDS __attribute__((address_space(3)))
@@ -56,15 +58,23 @@ __device__ __forceinline__ bool in_support(int law, const uint64_t* adj, int i, 
   return law == 1 || k == i || k == j;
 }
 
+// the input group of index x: the last g with starts[g] <= x, by binary
+// search over the starts (held in LDS: searched from the kernel's argument
+// block, every step was a dependent scalar load)
 __device__ __forceinline__ int group_of(const int32_t* starts, int q, int32_t x) {
-  int g = 0;
-  while (g + 1 < q && x >= starts[g + 1]) ++g;
-  return g;
+  int lo = 0, hi = q - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (x >= starts[mid]) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhase p) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ unsigned long long rowmask_s[kMaxQGroups];
+  __shared__ int32_t S_s[kMaxQGroups + 1];
   __shared__ int16_t slices_s[kDecodeMaxK / SLICE];
   __shared__ int32_t wave_cnt_s[4];
 
@@ -83,6 +93,9 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   const int32_t n0 = p.R[j] + (ct - p.NTp[j]) * TN;
   const int32_t nend = p.R[j + 1];
 
+  // the input group starts, searched from LDS below
+  for (int i = tid; i <= p.q; i += kThreads) S_s[i] = p.S[i];
+  __syncthreads();
   // which rows need block (g, j), per input group g: wave 0 holds one row
   // per lane and takes one ballot per group
   if (wave == 0) {
@@ -105,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
     if (sl < nsl) {
       for (int piece = 0; piece < SLICE / 8; ++piece) {
         const int32_t k = sl * SLICE + piece * 8;
-        if (k < p.K && rowmask_s[group_of(p.S, p.q, k)]) need = true;
+        if (k < p.K && rowmask_s[group_of(S_s, p.q, k)]) need = true;
       }
     }
     const unsigned long long bal = __ballot(need);
@@ -133,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   // input pieces of slice `i` (zero where the row's support skips it)
   auto load_x = [&](int i, uint4 (&xv)[4]) {
     const int32_t kk = slices_s[i] * SLICE + 8 * G;
-    const unsigned long long gm = kk < p.K ? rowmask_s[group_of(p.S, p.q, kk)] : 0ull;
+    const unsigned long long gm = kk < p.K ? rowmask_s[group_of(S_s, p.q, kk)] : 0ull;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       const int m = 16 * mb + pl;
@@ -142,8 +155,9 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
       xv[mb] = ok ? xa : make_uint4(0, 0, 0, 0);
     }
   };
-  for (int p0 = 0; p0 < nslices; p0 += kPassSlices) {
-    const int p1 = min(nslices, p0 + kPassSlices);
+  const int pass = p.slots;  // slices held in LDS at once (the launch's LDS room)
+  for (int p0 = 0; p0 < nslices; p0 += pass) {
+    const int p1 = min(nslices, p0 + pass);
     // stream this wave's slices of the pass into LDS (slot i - p0): lane l
     // carries row l/2, 16 bytes (8 columns) at half l%2.  Rows past K repeat
     // row K-1 and columns past the group repeat its first column (finite
@@ -196,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
   }
 
   // add the four waves' partial sums in a fixed order
-  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + kPassSlices * 1024);
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(lds + p.slots * 1024);
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) red[(wave * 4 + mb) * 64 + lane] = acc[mb];
   __syncthreads();
@@ -254,16 +268,31 @@ __global__ __launch_bounds__(kThreads) void decode_phase_kernel(const DecodePhas
 
 }  // namespace
 
-size_t decode_phase_smem() { return kPassSlices * 1024 + kRedBytes; }
+// LDS slots for the slices a workgroup can need: the support of output
+// group j over the rows' types reaches at most min(q, M + 1) groups under
+// the star and graph laws (B(t, j) within {t, j}), every group under the
+// others; a group of s inputs spans at most ceil(s / 32) + 1 slices.  Fewer
+// slots let more workgroups share a CU (a single row at q = 32 needs about
+// 10 of the 128).
+int decode_phase_slots(const DecodePhase& p) {
+  const int reach = (p.law == 0 || p.law == 3) ? std::min(p.q, p.M + 1) : p.q;
+  int widest = 0;
+  for (int g = 0; g < p.q; ++g) widest = std::max(widest, (p.S[g + 1] - p.S[g] + SLICE - 1) / SLICE + 1);
+  const int nsl = (p.K + SLICE - 1) / SLICE;
+  return std::max(1, std::min({kPassSlices, nsl, reach * widest}));
+}
 
-hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream) {
+size_t decode_phase_smem(int slots) { return static_cast<size_t>(slots) * 1024 + kRedBytes; }
+
+hipError_t launch_decode_phase(DecodePhase p, hipStream_t stream) {
   static std::atomic<unsigned long long> lds_set{0};
   const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(decode_phase_kernel), lds_set,
-                                           static_cast<int>(decode_phase_smem()));
+                                           static_cast<int>(decode_phase_smem(kPassSlices)));
   if (attr != hipSuccess) return attr;
+  p.slots = decode_phase_slots(p);
   const int nt = p.NTp[p.q];
   const int grid = (nt + 31) / 32 * 32;
-  hipLaunchKernelGGL(decode_phase_kernel, dim3(grid), dim3(kThreads), decode_phase_smem(), stream, p);
+  hipLaunchKernelGGL(decode_phase_kernel, dim3(grid), dim3(kThreads), decode_phase_smem(p.slots), stream, p);
   return hipGetLastError();
 }
 

@@ -147,10 +147,17 @@ __device__ __forceinline__ bool in_support(int law, const uint64_t* adj, int i, 
   }
   return law == 1 || k == i || k == j;
 }
+// the input group of index x: the last g with starts[g] <= x, by binary
+// search over the starts (held in LDS: searched from the kernel's argument
+// block, every step was a dependent scalar load)
 __device__ __forceinline__ int group_of(const int32_t* starts, int q, int32_t x) {
-  int g = 0;
-  while (g + 1 < q && x >= starts[g + 1]) ++g;
-  return g;
+  int lo = 0, hi = q - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (x >= starts[mid]) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 // One projection item: 16 output columns [n0, nend) of output group j, K
@@ -522,9 +529,16 @@ __global__ __launch_bounds__(kThreads) void decode_stack_kernel(const DecodeStac
   const int my_dn = 4 * (lane >> 4);
 
   // prologue: slice plans and copy offsets, then the weights of layer 0
+  // (the group starts searched from LDS)
+  __shared__ int32_t SD_s[kMaxQGroups + 1], SF_s[kMaxQGroups + 1];
+  for (int i = tid; i <= p.q; i += kThreads) {
+    SD_s[i] = p.SD[i];
+    SF_s[i] = p.SF[i];
+  }
+  __syncthreads();
   int32_t off_u[NOFF], off_d[NOFF];
-  if (iu.valid) plan(0, iu, p.SD);
-  if (idn.valid) plan(1, idn, p.SF);
+  if (iu.valid) plan(0, iu, SD_s);
+  if (idn.valid) plan(1, idn, SF_s);
   if (iu.valid) copy_offsets(0, iu, p.F, off_u);
   if (idn.valid) copy_offsets(1, idn, p.D, off_d);
   if (iu.valid) copy(0, p.Wu[0], off_u);

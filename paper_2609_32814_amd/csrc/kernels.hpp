@@ -167,6 +167,7 @@ struct DecodePhase {
   void* Y;                // down, last layer: final output, or null
   int32_t ydtype;
   uint64_t adj[kMaxQGroups];  // law 3: bit j of adj[i] marks the edge i -> j
+  int32_t slots;              // LDS slice slots (set by launch_decode_phase)
 };
 
 // The whole decode stack in one persistent launch (see decode_stack.hip).
@@ -218,7 +219,7 @@ bool decode_stack_resident(int M, int kmax, int D, int ns, bool gated, int nt_up
 // device not held by other work); p.cnt must be zero.
 hipError_t launch_decode_stack(const DecodeStack& p, int grid, hipStream_t stream);
 
-hipError_t launch_decode_phase(const DecodePhase& p, hipStream_t stream);
+hipError_t launch_decode_phase(DecodePhase p, hipStream_t stream);
 
 // ---- algebraic attention ------------------------------------------------------
 
