@@ -188,23 +188,24 @@ double deal_makespan(const std::vector<int32_t>* passes, double epi) {
   return worst;
 }
 int steps_of(int64_t w) { return static_cast<int>((w + 63) / 64); }
-// mode: the kernel's (forward, activation gradient, weight gradient)
-double async_makespan(const Alg& a, int mode, int64_t M, int tn, bool act) {
+// mode: the kernel's (forward, activation gradient, weight gradient); tm
+// the tile height (the weight gradient's, over the input groups)
+double async_makespan(const Alg& a, int mode, int64_t M, int tm, int tn, bool act) {
   std::vector<int32_t> passes[2];
   const int q = a.q;
   const int64_t per = (M + q - 1) / q;  // rows of a type
   if (mode == kModeBwdWeight) {
     int64_t mt = 0;
-    for (int g = 0; g < q; ++g) mt += tiles_of(a.s(g), kTileM);
+    for (int g = 0; g < q; ++g) mt += tiles_of(a.s(g), tm);
     const int64_t ns = nsplit_rule(mt * col_tiles(a, true, tn), M);
     for (int i = 0; i < q; ++i)
       for (int j = 0; j < q; ++j) {
         const bool diag = i == j || a.law == STAR_LAW_DENSE;
         const int st = steps_of(((diag ? M : per) + ns - 1) / ns);
-        passes[i == j ? 0 : 1].insert(passes[i == j ? 0 : 1].end(), tiles_of(a.s(i), kTileM) * tiles_of(a.r(j), tn) * ns,
+        passes[i == j ? 0 : 1].insert(passes[i == j ? 0 : 1].end(), tiles_of(a.s(i), tm) * tiles_of(a.r(j), tn) * ns,
                                       st);
       }
-    return deal_makespan(passes, 1.0 * tn / 256);
+    return deal_makespan(passes, 1.0 * tm * tn / (256 * 256));
   }
   const int rt = tiles_of(per, kTileM);
   const bool fwd = mode == kModeFwd;
@@ -236,13 +237,39 @@ int async_tile_n(const Alg& a, int mode, int64_t M, bool act) {
   if (a.law != STAR_LAW_STAR && a.law != STAR_LAW_DENSE) return 256;
   const bool over_r = mode != kModeBwdData;
   if (padded_cols(a, over_r, 192) >= padded_cols(a, over_r, 256)) return 256;
-  return 0.9 * async_makespan(a, mode, M, 192, act) < async_makespan(a, mode, M, 256, act) ? 192 : 256;
+  return 0.9 * async_makespan(a, mode, M, 256, 192, act) < async_makespan(a, mode, M, 256, 256, act) ? 192 : 256;
 }
-int async_tile_n_weight(const Alg& a, int64_t M) { return async_tile_n(a, kModeBwdWeight, M, false); }
+// Weight gradient: 256 x 256, 256 x 192 (columns over 384-wide output
+// groups) or 192 x 256 (rows over 384-wide input groups), the one that pads
+// the fewest dW cells, if the deal estimate agrees (a smaller tile counted
+// as 0.9 of a 256 x 256 one per step).
+struct TileShape {
+  int tm, tn;
+};
+TileShape async_tiles_weight(const Alg& a, int64_t M) {
+  if (a.law != STAR_LAW_STAR && a.law != STAR_LAW_DENSE) return {256, 256};
+  auto padded = [&](int tm, int tn) {
+    int64_t rows = 0;
+    for (int g = 0; g < a.q; ++g) rows += static_cast<int64_t>(tiles_of(a.s(g), tm)) * tm;
+    return rows * padded_cols(a, true, tn);
+  };
+  const double base = async_makespan(a, kModeBwdWeight, M, 256, 256, false);
+  TileShape best{256, 256};
+  int64_t best_pad = padded(256, 256);
+  for (const TileShape c : {TileShape{256, 192}, TileShape{192, 256}}) {
+    const int64_t pad = padded(c.tm, c.tn);
+    if (pad < best_pad && 0.9 * async_makespan(a, kModeBwdWeight, M, c.tm, c.tn, false) < base) {
+      best = c;
+      best_pad = pad;
+    }
+  }
+  return best;
+}
 int bwd_weight_nsplit_async(const Alg& a, int64_t M) {
+  const TileShape ts = async_tiles_weight(a, M);
   int64_t mt = 0;
-  for (int g = 0; g < a.q; ++g) mt += tiles_of(a.s(g), kTileM);
-  return static_cast<int>(nsplit_rule(mt * col_tiles(a, true, async_tile_n_weight(a, M)), M));
+  for (int g = 0; g < a.q; ++g) mt += tiles_of(a.s(g), ts.tm);
+  return static_cast<int>(nsplit_rule(mt * col_tiles(a, true, ts.tn), M));
 }
 
 constexpr int kColSumChunks = 64;  // row chunks of the bias-gradient column sums
@@ -501,6 +528,7 @@ hipError_t launch_proj_gemm(int mode, const GemmParams& p, int nw, int64_t upper
     GemmParams pa = p;
     const int32_t* G = (mode == kModeFwd) ? p.R : p.S;  // output column groups
     int tn = async_tile_n(alg_of(p), mode, p.M, p.act != STAR_ACT_NONE);
+    pa.tile_m = kTileM;
     if (mode == kModeFwd) {
       const int forced = g_fwd_tiles.load(std::memory_order_relaxed);
       if (forced == STAR_TILES_WIDE) tn = 256;
@@ -814,9 +842,11 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   if (pipelined) {
     // every tile contracts over a range of type-sorted positions; the
     // kernel reads the rows of X and dY at those positions through perm
-    p.tile_n = async_tile_n_weight(a, M);
+    const TileShape ts = async_tiles_weight(a, M);
+    p.tile_m = ts.tm;
+    p.tile_n = ts.tn;
     fill_tiles(p.NTp, a.R, a.q, p.tile_n);
-    fill_tiles(p.MTp, a.S, a.q, kTileM);
+    fill_tiles(p.MTp, a.S, a.q, p.tile_m);
     p.A = X;
     p.B = dY;
     p.dW = dW;

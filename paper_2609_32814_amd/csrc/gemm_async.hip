@@ -115,14 +115,16 @@ __device__ __forceinline__ bool wave_rows_live(int row0, int32_t nrows) {
   return __builtin_amdgcn_readfirstlane(row0 < nrows ? 1 : 0) != 0;
 }
 
-// Tile shapes: 256 rows x TN columns, 8 wavefronts.  TN = 256: waves 2 x 4
-// of 128 x 64; TN = 192: waves 4 x 2 of 64 x 96 (groups 384 or 1536 wide
-// take whole tiles).  The LDS tiles keep 256 columns of room either way.
-template <int TN> struct Lay {
-  static_assert(TN == 256 || TN == 192, "tile width 256 or 192");
+// Tile shapes: TM rows x TN columns, 8 wavefronts.  256 x 256: waves 2 x 4
+// of 128 x 64; 256 x 192: waves 4 x 2 of 64 x 96 (groups 384 or 1536 wide
+// take whole tiles); 192 x 256 (weight gradient only, rows over 384-wide
+// input groups): waves 2 x 4 of 96 x 64.  The LDS tiles keep 256 rows and
+// 256 columns of room either way.
+template <int TM, int TN> struct Lay {
+  static_assert((TM == 256 && (TN == 256 || TN == 192)) || (TM == 192 && TN == 256), "tile shape");
   static constexpr int WNW = TN == 256 ? 4 : 2;  // waves along N
   static constexpr int WMW = kWaves / WNW;        // waves along M
-  static constexpr int TMW = BM / WMW;            // rows of a wave
+  static constexpr int TMW = TM / WMW;            // rows of a wave
   static constexpr int TNW = TN / WNW;            // columns of a wave
   static constexpr int MI = TMW / 32;             // 32-row MFMA blocks
   static constexpr int NI = TNW / 32;             // 32-column MFMA blocks
@@ -149,9 +151,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
-template <int MODE, int LAW, int ACT, int TN>
+template <int MODE, int LAW, int ACT, int TM, int TN>
 __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const GemmParams p) {
-  using L = Lay<TN>;
+  static_assert(MODE == kModeBwdWeight || TM == BM, "tiles of fewer rows: weight gradient only");
+  using L = Lay<TM, TN>;
   constexpr int MI = L::MI, NI = L::NI, TMW = L::TMW, TNW = L::TNW;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   // row tiles per class: [0] BM rows, [1] BM / 2 rows (weight gradient:
@@ -251,14 +254,14 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
     while (logical >= pf[cls + 1]) ++cls;
     const bool hh = ps == 1 && half1;
     t = make_tile<MODE, LAW, TN, BK>(p, sel_for(MODE, LAW, ps), cls, logical - pf[cls],
-                                     units_s[hh ? 1 : 0][cls], offs_s, hh ? BM / 2 : BM);
+                                     units_s[hh ? 1 : 0][cls], offs_s, hh ? BM / 2 : TM);
     return true;
   };
 
   // weight gradient: a split whose row range is empty contributes zeros
   auto zero_tile = [&](const Tile& t) {
     float* out = p.nsplit > 1 ? p.partial + static_cast<int64_t>(t.split) * p.K * p.N : p.dW;
-    for (int idx = threadIdx.x; idx < BM * TN / 4; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < TM * TN / 4; idx += kThreads) {
       const int32_t r = t.rstart + idx / (TN / 4);
       const int32_t c = t.cstart + (idx % (TN / 4)) * 4;
       if (r < t.rend && c < t.cend)
@@ -314,7 +317,7 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   int32_t wa_col = 0, wb_col = 0;
   auto tile_ptrs = [&]() {
     if constexpr (MODE == kModeBwdWeight) {
-      wa_col = min(lt.rstart + 8 * fb_chunk, p.K - 8);
+      wa_col = min(lt.rstart + 8 * (fb_chunk < TM / 8 ? fb_chunk : 0), p.K - 8);
       wb_col = min(lt.cstart + 8 * (fb_chunk < TN / 8 ? fb_chunk : 0), p.N - 8);
     }
     if constexpr (kFast) {
@@ -771,9 +774,9 @@ __global__ __launch_bounds__(kThreads, 1) void star_gemm_async_kernel(const Gemm
   wait_vm_all();
 }
 
-template <int MODE, int LAW, int ACT, int TN>
+template <int MODE, int LAW, int ACT, int TM, int TN>
 hipError_t launch_one(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
-  auto kern = star_gemm_async_kernel<MODE, LAW, ACT, TN>;
+  auto kern = star_gemm_async_kernel<MODE, LAW, ACT, TM, TN>;
   static std::atomic<unsigned long long> lds_set{0};
   const hipError_t attr = ensure_lds_limit(reinterpret_cast<const void*>(kern), lds_set, SMEM);
   if (attr != hipSuccess) return attr;
@@ -785,14 +788,18 @@ hipError_t launch_one(const GemmParams& p, int64_t upper, int cus, hipStream_t s
   return hipGetLastError();
 }
 
-// the 192-wide tiles are built for the star and dense laws only
+// the 192-wide and 192-high tiles are built for the star and dense laws
+// only, the 192-high ones for the weight gradient
 template <int MODE, int LAW, int ACT>
 hipError_t launch_tn(const GemmParams& p, int64_t upper, int cus, hipStream_t stream) {
   if constexpr (LAW <= 1) {
-    if (p.tile_n == 192) return launch_one<MODE, LAW, ACT, 192>(p, upper, cus, stream);
+    if (p.tile_m == 256 && p.tile_n == 192) return launch_one<MODE, LAW, ACT, 256, 192>(p, upper, cus, stream);
+    if constexpr (MODE == kModeBwdWeight) {
+      if (p.tile_m == 192 && p.tile_n == 256) return launch_one<MODE, LAW, ACT, 192, 256>(p, upper, cus, stream);
+    }
   }
-  if (p.tile_n != 256) return hipErrorInvalidValue;
-  return launch_one<MODE, LAW, ACT, 256>(p, upper, cus, stream);
+  if (p.tile_m != 256 || p.tile_n != 256) return hipErrorInvalidValue;
+  return launch_one<MODE, LAW, ACT, 256, 256>(p, upper, cus, stream);
 }
 
 template <int MODE, int LAW>

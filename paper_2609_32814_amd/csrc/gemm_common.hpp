@@ -332,7 +332,7 @@ __device__ __forceinline__ Tile make_tile(const GemmParams& p, int sel, int cls,
     t.split = ru % p.nsplit;
     t.cstart = p.R[cg] + nt * BN;
     t.cend = p.R[cg + 1];
-    t.rstart = p.S[cls] + t.mt * BM;
+    t.rstart = p.S[cls] + t.mt * bm;
     t.rend = p.S[cls + 1];
     // the type-sorted positions this tile contracts over: one or two
     // ranges, cut into nsplit chunks of their concatenation

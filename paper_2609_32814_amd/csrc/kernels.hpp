@@ -47,9 +47,10 @@ struct GemmParams {
   float* partial;     // [nsplit][K][N] when nsplit > 1
   float* dbias_part;  // [nsplit][N] when nsplit > 1
   int32_t nsplit;
-  // bf16 pipelined kernel: columns of a C tile (256, or 192 for the star and
-  // dense laws); p.NTp counts column tiles of that width
-  int32_t tile_n;
+  // bf16 pipelined kernel: rows and columns of a C tile (256 x 256, 256 x
+  // 192 for the star and dense laws, 192 x 256 for their weight gradient);
+  // p.NTp counts column tiles of that width, p.MTp row tiles of that height
+  int32_t tile_m, tile_n;
   // law 3 (graph algebra): bit j of adj[i] marks the edge i -> j, bit i of
   // adj_in[j] the same edge (so adj_in[j] holds the in-neighbours of j)
   uint64_t adj[kMaxQGroups];
@@ -65,8 +66,8 @@ hipError_t launch_count_bad_types(const int32_t* types, int64_t M, int q,
 // columns (nw must be 2), `grid` workgroups of 256 threads.
 hipError_t launch_gemm(int mode, const GemmParams& p, int nw, int grid, hipStream_t stream);
 // bf16 forward / activation-gradient / weight-gradient GEMM fed by direct
-// global-to-LDS copies: tiles of kTileM x p.tile_n (256, or 192 for laws 0
-// and 1; p.NTp must count column tiles of that width); `upper_tiles` bounds
+// global-to-LDS copies: tiles of p.tile_m x p.tile_n (see GemmParams; p.NTp
+// and p.MTp must count tiles of that shape); `upper_tiles` bounds
 // the tile count and `cus` is the device's CU count (the kernel picks its
 // persistent grid from both).
 // part[c][n] = sum over rows [c chunk, (c + 1) chunk) of the rows of valid

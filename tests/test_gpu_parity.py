@@ -314,6 +314,7 @@ def test_half_height_last_round(P, law, mode):
     (4, [32] * 4, [64] * 4, 2049),
     (2, [128, 128], [128, 128], 0),     # empty batch: zero gradients
     (2, [384, 392], [384, 384], 3000),  # output groups 384 wide
+    (2, [384, 384], [512, 256], 2500),  # input groups 384 wide (192-row tiles)
 ])
 def test_bwd_weight_parity(P, law, dtype, q, s, r, M):
     ga, oa = algs(P, q, s, r, law)
