@@ -143,12 +143,19 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_kernel(const int32_t* 
 // permutation is stable.  Workgroup 0 writes the offsets.
 constexpr int kPlanRowsPerBlock = kPlanThreads;
 
+//
+// NT > 0 (q + 1 = NT classes, few types): the counting pass takes one ballot
+// per class and window and keeps the counts in wave-uniform registers (no
+// LDS atomics); the wavefronts' counts are summed after the pass.  NT = 0:
+// any q, a match-any per window and LDS atomics from the leading lanes.
+template <int NT>
 __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int32_t* __restrict__ types,
                                                                       int32_t M, int q, int nbits,
                                                                       int32_t* __restrict__ perm,
                                                                       int32_t* __restrict__ offsets) {
   __shared__ int32_t total[kPlanMaxQ + 1], before[kPlanMaxQ + 1];
   __shared__ int32_t wcount[kPlanWaves][kPlanMaxQ + 1];
+  __shared__ int32_t wtot[kPlanWaves][NT > 0 ? NT : 1], wbef[kPlanWaves][NT > 0 ? NT : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int32_t r0 = blockIdx.x * kPlanRowsPerBlock;
   for (int i = threadIdx.x; i <= q; i += kPlanThreads) total[i] = before[i] = 0;
@@ -158,6 +165,7 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
   auto cls = [&](int t) { return (t >= 0 && t < q) ? t : q; };
   // per-type counts over all rows and over the rows before r0, a 64-row
   // window per wavefront at a time, 8 windows' loads in flight
+  int32_t cnt[NT > 0 ? NT : 1] = {}, bef[NT > 0 ? NT : 1] = {};
   constexpr int kBatch = 8;
   for (int32_t base = 0; base < M; base += kPlanThreads * kBatch) {
     int v[kBatch];
@@ -168,16 +176,40 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const int32_t wrow = base + u * kPlanThreads + wave * 64;  // the window's first row (wave-uniform)
+      const int32_t wbase = base + u * kPlanThreads;  // workgroup-uniform
+      if (wbase >= M) break;
+      if constexpr (NT > 0) {
+        // the windows before r0 are those with wbase < r0 (both multiples of
+        // the workgroup's row count): keep the counts reached at r0
+        if (wbase == r0) {
+#pragma unroll
+          for (int k = 0; k < NT; ++k) bef[k] = cnt[k];
+        }
+      }
+      const int32_t wrow = wbase + wave * 64;  // the window's first row (wave-uniform)
       if (wrow >= M) break;
       const int32_t row = wrow + lane;
       const bool in = row < M;
       const int t = cls(v[u]);
-      const uint64_t active = __ballot(in);
-      const uint64_t m = match_type(t, t < q, nbits) & active;
-      if (in && (m & lt_mask) == 0) {
-        atomicAdd(&total[t], __popcll(m));
-        if (wrow < r0) atomicAdd(&before[t], __popcll(m));  // windows never straddle r0
+      if constexpr (NT > 0) {
+#pragma unroll
+        for (int k = 0; k < NT; ++k) cnt[k] += __popcll(__ballot(in && t == k));
+      } else {
+        const uint64_t active = __ballot(in);
+        const uint64_t m = match_type(t, t < q, nbits) & active;
+        if (in && (m & lt_mask) == 0) {
+          atomicAdd(&total[t], __popcll(m));
+          if (wrow < r0) atomicAdd(&before[t], __popcll(m));  // windows never straddle r0
+        }
+      }
+    }
+  }
+  if constexpr (NT > 0) {
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < NT; ++k) {
+        wtot[wave][k] = cnt[k];
+        wbef[wave][k] = bef[k];
       }
     }
   }
@@ -189,6 +221,18 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
   const uint64_t m = match_type(t, t < q, nbits) & active;
   if (in && (m & lt_mask) == 0) wcount[wave][t] = __popcll(m);
   __syncthreads();
+  if constexpr (NT > 0) {
+    if (threadIdx.x < NT) {
+      int32_t a = 0, b = 0;
+      for (int w = 0; w < kPlanWaves; ++w) {
+        a += wtot[w][threadIdx.x];
+        b += wbef[w][threadIdx.x];
+      }
+      total[threadIdx.x] = a;
+      before[threadIdx.x] = b;
+    }
+    __syncthreads();
+  }
   if (in) {
     // offset of type t, the rows of type t before this workgroup and before
     // this wavefront in it, and the lanes below this one
@@ -226,8 +270,23 @@ hipError_t launch_type_plan(const int32_t* types, int64_t M, int q, int32_t* per
   while ((1 << nbits) < q + 1) ++nbits;
   if (M > 0 && M <= kPlanLdsRows) {
     const unsigned blocks = static_cast<unsigned>((M + kPlanRowsPerBlock - 1) / kPlanRowsPerBlock);
-    hipLaunchKernelGGL(type_plan_wide_kernel, dim3(blocks), dim3(kPlanThreads), 0, stream, types,
-                       static_cast<int32_t>(M), q, nbits, perm, offsets);
+    const int32_t m32 = static_cast<int32_t>(M);
+    switch (q + 1) {
+#define STARQ_PLAN_NT(nt)                                                                        \
+  case nt:                                                                                       \
+    hipLaunchKernelGGL(type_plan_wide_kernel<nt>, dim3(blocks), dim3(kPlanThreads), 0, stream, \
+                       types, m32, q, nbits, perm, offsets);                                     \
+    break;
+      STARQ_PLAN_NT(2)
+      STARQ_PLAN_NT(3)
+      STARQ_PLAN_NT(4)
+      STARQ_PLAN_NT(5)
+      STARQ_PLAN_NT(9)
+#undef STARQ_PLAN_NT
+      default:
+        hipLaunchKernelGGL(type_plan_wide_kernel<0>, dim3(blocks), dim3(kPlanThreads), 0, stream,
+                           types, m32, q, nbits, perm, offsets);
+    }
   } else {
     hipLaunchKernelGGL(type_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, types,
                        static_cast<int32_t>(M), q, nbits, perm, offsets);

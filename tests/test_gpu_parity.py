@@ -683,7 +683,8 @@ def test_planned_entry_points_match(P):
 @pytest.mark.parametrize("q,M,bad", [(2, 8192, False), (1, 300, False), (3, 1000, True),
                                      (64, 5000, True), (7, 70001, True), (16, 64, False),
                                      (4, 16384, True), (2, 65536, True), (5, 65537, False),
-                                     (3, 1025, True), (2, 1, False), (64, 65535, True)])
+                                     (3, 1025, True), (2, 1, False), (64, 65535, True),
+                                     (8, 9000, True), (4, 3073, False), (1, 4096, True)])
 def test_type_plan_is_stable_partition(P, q, M, bad):
     """The plan is the stable partition of the rows by type (a stable sort of
     the type keys, out-of-range types as a last key) and the per-type
