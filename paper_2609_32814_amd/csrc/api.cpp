@@ -863,7 +863,7 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
     st = hip_status(launch_column_sum(static_cast<const uint16_t*>(dY), p.N, p.perm, p.offsets, a.q, p.M,
                                       chunk, kColSumChunks, cs, stream));
     if (st != STAR_OK) return st;
-    return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
+    return hip_status(launch_sum_chunks(cs, kColSumChunks, p.N, dbias, stream));
   }
   fill_tiles(p.NTp, a.R, a.q, 64 * kBwdWeightNW);
   fill_tiles(p.MTp, a.S, a.q, kTileM);
@@ -887,7 +887,7 @@ star_status star_proj_bwd_weight_planned(const star_algebra* alg, int64_t M, con
   st = hip_status(launch_column_sum_f32(static_cast<const float*>(dY), p.N, p.perm, p.offsets, a.q, p.M, chunk,
                                         kColSumChunks, cs, stream));
   if (st != STAR_OK) return st;
-  return hip_status(launch_sum_partials(cs, kColSumChunks, p.N, dbias, stream));
+  return hip_status(launch_sum_chunks(cs, kColSumChunks, p.N, dbias, stream));
 }
 
 star_status star_proj_bwd_weight(const star_algebra* alg, int64_t M, const int32_t* row_type,

@@ -618,9 +618,7 @@ hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream) {
                      p.nsplit, nKN, p.dW);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.dbias == nullptr) return e;
-  hipLaunchKernelGGL(split_reduce_kernel, dim3(8), dim3(256), 0, stream, p.dbias_part, p.nsplit,
-                     static_cast<int64_t>(p.N), p.dbias);
-  return hipGetLastError();
+  return launch_sum_chunks(p.dbias_part, p.nsplit, p.N, p.dbias, stream);
 }
 
 }  // namespace starq

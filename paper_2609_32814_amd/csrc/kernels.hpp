@@ -130,6 +130,10 @@ hipError_t launch_split_reduce(const GemmParams& p, hipStream_t stream);
 // out[i] = sum over c < n_parts of part[c * n + i], in c order.
 hipError_t launch_sum_partials(const float* part, int n_parts, int64_t n, float* out,
                                hipStream_t stream);
+// The same for few outputs (a bias gradient's n columns) over many parts:
+// the parts of one output are spread over eight threads, added in a fixed
+// order.
+hipError_t launch_sum_chunks(const float* part, int nparts, int32_t n, float* out, hipStream_t stream);
 // Zero-fills n floats with a kernel (safe to record in a HIP graph).
 hipError_t launch_fill_zero(float* dst, int64_t n, hipStream_t stream);
 
