@@ -39,22 +39,6 @@ enum Act : int { kActNone = 0, kActGelu = 1, kActGeluTanh = 2 };
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-// erf from Abramowitz & Stegun 7.1.26: erf(x) = 1 - (a1 t + ... + a5 t^5)
-// exp(-x^2), t = 1 / (1 + p x), x >= 0; |error| <= 1.5e-7.  The reciprocal
-// and exponential are the hardware approximations (about 1 ulp).
-__device__ __forceinline__ float erf_as7126(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
-  float poly = 1.061405429f;
-  poly = poly * t - 1.453152027f;
-  poly = poly * t + 1.421413741f;
-  poly = poly * t - 0.284496736f;
-  poly = poly * t + 0.254829592f;
-  poly *= t;
-  const float y = 1.0f - poly * __builtin_amdgcn_exp2f(-(ax * ax) * kLog2e);
-  return copysignf(y, x);
-}
-
 // tanh(u) = 1 - 2 / (1 + exp(2u)); the absolute error stays near 1e-7 over
 // the whole range (saturating to +-1), which is what the tanh-form GELU needs.
 __device__ __forceinline__ float tanh_fast(float u) {
@@ -104,13 +88,25 @@ __device__ __forceinline__ float act_apply(int act, float z) {
   return z;
 }
 
-// d act / dz.  Erf form Phi(z) + z phi(z) (Phi through A&S 7.1.26): error
-// at most 1e-6.  Tanh form: error at most 5e-6 (the 1 - t^2 factor loses
-// digits where tanh saturates).
+// d act / dz.  Erf form Phi(z) + z phi(z), Phi through A&S 7.1.26 at
+// x = |z| / sqrt 2; its factor exp(-x^2) = exp(-z^2 / 2) is also
+// sqrt(2 pi) phi(z), so one exponential serves both terms.  Error at most
+// 1e-6.  Tanh form: error at most 5e-6 (the 1 - t^2 factor loses digits
+// where tanh saturates).
 __device__ __forceinline__ float act_deriv(int act, float z) {
-  if (act == kActGelu)
-    return 0.5f * (1.0f + erf_as7126(z * 0.70710678118654752f)) +
-           z * 0.39894228040143268f * __builtin_amdgcn_exp2f(-0.5f * z * z * kLog2e);
+  if (act == kActGelu) {
+    const float x = fabsf(z) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * x);
+    float poly = 1.061405429f;
+    poly = poly * t - 1.453152027f;
+    poly = poly * t + 1.421413741f;
+    poly = poly * t - 0.284496736f;
+    poly = poly * t + 0.254829592f;
+    poly *= t;
+    const float e = __builtin_amdgcn_exp2f(-(x * x) * kLog2e);
+    const float tail = 0.5f * poly * e;  // 1 - Phi(|z|)
+    return fmaf(z * 0.39894228040143268f, e, z >= 0.0f ? 1.0f - tail : tail);
+  }
   if (act == kActGeluTanh) {
     const float u = 0.79788456080286536f * (z + 0.044715f * z * z * z);
     const float t = tanh_fast(u);
