@@ -214,7 +214,7 @@ def main():
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the star projection "
               "is row-local and shards over token rows with one dW all-reduce per step, "
-              "which this build does not implement.", file=sys.stderr)
+              "which is not implemented here.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
