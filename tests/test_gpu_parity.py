@@ -334,6 +334,28 @@ def test_bwd_weight_parity(P, law, dtype, q, s, r, M):
     assert np.array_equal(to_host(dW2), to_host(dW)) and np.array_equal(to_host(db2), to_host(db))
 
 
+@pytest.mark.parametrize("r", [[384, 392], [1024, 1032]])
+def test_bwd_weight_out_of_range_types_left_out(P, r):
+    """Rows whose type is outside [0, q) are left out of the weight and bias
+    gradients: the result equals the oracle's over the valid rows alone.  The
+    bias column sums then walk the rows in type-sorted order through perm
+    (the 16-row-lane blocks for 776 columns, the 8-row-lane ones for 2056)."""
+    ga, oa = algs(P, 2, [384, 384], r)
+    M = 3000
+    X = synth.gaussian(331, 0, (M, oa.K), 1.0, "bf16")
+    dY = synth.gaussian(331, 1, (M, oa.N), 1.0, "bf16")
+    rng = np.random.default_rng([331, 3])
+    t = rng.integers(0, 2, M).astype(np.int32)
+    bad = rng.choice(M, size=M // 17, replace=False)
+    t_bad = t.copy()
+    t_bad[bad] = rng.choice(np.array([-1, 2, 7, 1 << 20], dtype=np.int32), size=bad.size)
+    dW, db = P.star_proj_bwd_weight(ga, types_dev(t_bad), to_dev(X), to_dev(dY))
+    good = np.setdiff1d(np.arange(M), bad)
+    rW, rb = oracle.proj_bwd_weight(oa, t[good], X.exact[good], dY.exact[good])
+    assert rel_fro(to_host(dW), rW) <= TOL_BF16
+    assert rel_fro(to_host(db), rb) <= TOL_BF16
+
+
 def test_bwd_weight_absent_type_gives_zero_blocks(P):
     ga, oa = algs(P, 3, [32, 48, 40], [56, 24, 64])
     M = 600
