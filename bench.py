@@ -274,9 +274,10 @@ def main():
         P.star_type_plan(q, td, plan)
 
     # Tile calibration per law (the paper calibrates the tile on each shape):
-    # a short warm trial of the 256 x 256 and 256 x 192 tiles, the faster
-    # taken for every timing below (set before each launch, so the two laws
-    # can alternate with their own tiles).
+    # a short warm trial of each tile shape the kernels offer here (256 x 256,
+    # 256 x 192, and the 64 x 128 small tiles), the fastest taken for every
+    # timing below (set before each launch, so the two laws can alternate
+    # with their own tiles).
     tiles = {"star": "auto", "dense": "auto"}
 
     def step_of(a, law):
@@ -296,7 +297,7 @@ def main():
     calib = {}
     for law, a in (("star", alg), ("dense", dalg)):
         res = {}
-        for t_ in ("wide", "wide192"):
+        for t_ in ("wide", "wide192", "small"):
             tiles[law] = t_
             g = gemm_of(a, law)
             for _ in range(3):
@@ -344,7 +345,7 @@ def main():
         f"  -> {value:.1f} TFLOP/s step, {achieved:.1f} TFLOP/s kernel")
     log(f"  dense step {d_step_ms*1e3:.1f} us  kernel {d_kern*1e3:.1f} us  flushed {dense_flushed*1e3:.1f} us")
 
-    tn = 192 if tiles["star"] == "wide192" else 256
+    tn = {"wide192": 192, "small": 0}.get(tiles["star"], 256)  # 0: the small-tile kernel
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
@@ -355,7 +356,8 @@ def main():
 
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic, "kernel": GEMM_KERNEL.format(tn=tn),
+                "traffic": traffic,
+                "kernel": GEMM_KERNEL.format(tn=tn) if tn else "gemm_narrow_kernel<1> (64 x 128 tiles)",
                 "kernel_mean_us": round(kern * 1e3, 2)}
     dense_ctrl = {
         "kernel_mean_us": round(d_kern * 1e3, 2),
@@ -392,7 +394,8 @@ def main():
                    "step_us_eager": round(eager_ms * 1e3, 2),
                    "step_us_graph": round(graph_ms * 1e3, 2),
                    "trials": args.trials, "reps_per_warm_trial": steps["star_eager"]["reps"],
-                   "tile": f"256 x {tn} x 64, 8 waves, one persistent workgroup per CU",
+                   "tile": (f"256 x {tn} x 64, 8 waves, one persistent workgroup per CU" if tn
+                            else "64 x 128 small tiles"),
                    "tile_calibration_us": calib, "tiles": dict(tiles)},
         "roofline": roofline,
         "dense_control": dense_ctrl,
