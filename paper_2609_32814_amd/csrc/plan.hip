@@ -165,7 +165,10 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
   auto cls = [&](int t) { return (t >= 0 && t < q) ? t : q; };
   // per-type counts over all rows and over the rows before r0, a 64-row
   // window per wavefront at a time, 8 windows' loads in flight
+  // (NT > 0: the valid classes by ballots on the raw type, the out-of-range
+  // class as the rest of the rows counted)
   int32_t cnt[NT > 0 ? NT : 1] = {}, bef[NT > 0 ? NT : 1] = {};
+  int32_t all = 0, all_bef = 0;
   constexpr int kBatch = 8;
   for (int32_t base = 0; base < M; base += kPlanThreads * kBatch) {
     int v[kBatch];
@@ -183,18 +186,20 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
         // the workgroup's row count): keep the counts reached at r0
         if (wbase == r0) {
 #pragma unroll
-          for (int k = 0; k < NT; ++k) bef[k] = cnt[k];
+          for (int k = 0; k < NT - 1; ++k) bef[k] = cnt[k];
+          all_bef = all;
         }
       }
       const int32_t wrow = wbase + wave * 64;  // the window's first row (wave-uniform)
       if (wrow >= M) break;
       const int32_t row = wrow + lane;
       const bool in = row < M;
-      const int t = cls(v[u]);
       if constexpr (NT > 0) {
+        all += __popcll(__ballot(in));
 #pragma unroll
-        for (int k = 0; k < NT; ++k) cnt[k] += __popcll(__ballot(in && t == k));
+        for (int k = 0; k < NT - 1; ++k) cnt[k] += __popcll(__ballot(in && v[u] == k));
       } else {
+        const int t = cls(v[u]);
         const uint64_t active = __ballot(in);
         const uint64_t m = match_type(t, t < q, nbits) & active;
         if (in && (m & lt_mask) == 0) {
@@ -206,11 +211,16 @@ __global__ __launch_bounds__(kPlanThreads) void type_plan_wide_kernel(const int3
   }
   if constexpr (NT > 0) {
     if (lane == 0) {
+      int32_t valid = 0, valid_bef = 0;
 #pragma unroll
-      for (int k = 0; k < NT; ++k) {
+      for (int k = 0; k < NT - 1; ++k) {
         wtot[wave][k] = cnt[k];
         wbef[wave][k] = bef[k];
+        valid += cnt[k];
+        valid_bef += bef[k];
       }
+      wtot[wave][NT - 1] = all - valid;
+      wbef[wave][NT - 1] = all_bef - valid_bef;
     }
   }
   // this workgroup's rows: per-wavefront counts per type
