@@ -218,3 +218,31 @@ def test_projection_shapes_full_size_sampled(P, name, D, F, q):
     assert rel_fro(to_host(Y[rows]), ref) <= TOL_BF16
     del Y
     torch.cuda.empty_cache()
+
+
+# The kernel study's largest runs (Tab. kernel-products): Qwen3-32B's
+# expansion 5120 -> 25600 at M = 8192, q = 128 (groups 40 / 200 wide) and at
+# M = 32768, q = 256, where the equal widths 20 / 100 are not multiples of 8
+# and alternate 16 / 24 and 96 / 104 (same totals, same block products).
+@pytest.mark.parametrize("M,q,s,r", [
+    (8192, 128, [40] * 128, [200] * 128),
+    (32768, 256, [16, 24] * 128, [96, 104] * 128),
+])
+def test_qwen3_32b_large_q_full_size_sampled(P, M, q, s, r):
+    import torch
+    ga, oa = P.Algebra(q, s, r), oracle.Alg(q, tuple(s), tuple(r))
+    seed = 2700 + q
+    X = synth.gaussian(seed, 0, (M, oa.K), 1.0, "bf16")
+    W = synth.gaussian(seed, 1, (oa.K, oa.N), (1.0 / oa.K) ** 0.5, "bf16")
+    t = synth.cyclic_types(M, q)
+    Y = P.star_proj_fwd(ga, types_dev(t), to_dev(X), to_dev(W))
+    rows = _sample_rows(M, 160, seed)
+    ref, _, _, _ = oracle.proj_fwd(oa, t[rows], X.exact[rows], W.exact)
+    got = to_host(Y[rows])
+    del Y
+    torch.cuda.empty_cache()
+    assert rel_fro(got, ref) <= TOL_BF16
+    # every sampled row on its own (each row type reaches 2q - 1 of the q^2 blocks)
+    live = np.linalg.norm(ref, axis=1) > 0
+    diff = np.linalg.norm(got - ref, axis=1)[live] / np.linalg.norm(ref, axis=1)[live]
+    assert diff.max() <= 4 * TOL_BF16
