@@ -127,3 +127,36 @@ def test_gated_ffn_merged_matches_oracle(P, q):
     H = P.star_swiglu_up_fwd_planned(ga_up.merged_gate_up(), plan, to_dev(X), P.pack_gate_up(to_dev(Wg), to_dev(Wu)))
     Y = P.star_proj_fwd_planned(ga_dn, plan, H, to_dev(Wd))
     assert rel_fro(to_host(Y), Yref) <= TOL_BF16
+
+
+def _sample_rows(M, n, seed):
+    rng = np.random.default_rng([seed, 11])
+    return np.unique(np.concatenate([[0, 1, M - 2, M - 1], rng.choice(M, n, replace=False)]))
+
+
+# The SwiGLU comparison's shapes at full size (Tab. kernel-ffn, q = 32,
+# M = 2048): the fused merged gate/up and the down product over all rows,
+# checked against the oracle on sampled rows (every step is row-local).
+@pytest.mark.parametrize("name,D,F", [("Qwen3-8B", 4096, 12288), ("DeepSeek-V3 expert", 7168, 2048)])
+def test_gated_ffn_merged_kernel_study_sampled(P, name, D, F):
+    import torch
+    q, M = 32, 2048
+    up, down = oracle.Alg.equal(q, D, F), oracle.Alg.equal(q, F, D)
+    ga_up, ga_dn = P.Algebra.equal(q, D, F), P.Algebra.equal(q, F, D)
+    seed = 3300 + D
+    X = synth.gaussian(seed, 0, (M, D), 1.0, "bf16")
+    Wg = synth.gaussian(seed, 1, (D, F), (1.0 / D) ** 0.5, "bf16")
+    Wu = synth.gaussian(seed, 2, (D, F), (1.0 / D) ** 0.5, "bf16")
+    Wd = synth.gaussian(seed, 3, (F, D), (1.0 / F) ** 0.5, "bf16")
+    t = synth.cyclic_types(M, q)
+    plan = P.star_type_plan(q, types_dev(t))
+    H = P.star_swiglu_up_fwd_planned(ga_up.merged_gate_up(), plan, to_dev(X), P.pack_gate_up(to_dev(Wg), to_dev(Wu)))
+    Y = P.star_proj_fwd_planned(ga_dn, plan, H, to_dev(Wd))
+    rows = _sample_rows(M, 160, seed)
+    got = to_host(Y[rows])
+    del H, Y
+    torch.cuda.empty_cache()
+    Zg, _, _, _ = oracle.proj_fwd(up, t[rows], X.exact[rows], Wg.exact)
+    Zu, _, _, _ = oracle.proj_fwd(up, t[rows], X.exact[rows], Wu.exact)
+    Yref, _, _, _ = oracle.proj_fwd(down, t[rows], oracle.round_bf16(oracle.act("silu", Zg) * Zu), Wd.exact)
+    assert rel_fro(got, Yref) <= TOL_BF16
